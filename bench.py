@@ -1,0 +1,336 @@
+"""DMS decode-attention benchmark on one MI355X.
+
+One step = one DMS decode step of every layer for the whole batch: append of
+the new token (delayed release, slot recycling, page pops), the split-K
+decode over the retained slots and the log-sum-exp combine, all through the
+libdms C ABI.  The cache state is built beforehand through the library's own
+chunk commits from seeded synthetic inputs.
+
+Prints one JSON line.  `value` is the whole step's algorithmic retained-KV
+bytes (every retained key and value row read once) divided by the step time,
+in GB/s; `roofline` reports the same bytes against the decode kernel's own
+duration, timed with HIP events around each launch.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+# Synthetic stand-ins for the paper's reasoning-model shapes (Qwen-R1 family).
+WORKLOADS = {
+    "qwen-r1-32b-8x": dict(layers=64, batch=128, kv_heads=8, group=5, head_dim=128,
+                           context=32768, window=256, p_evict=7 / 8, seed=3,
+                           desc="Qwen-R1-32B-shaped DMS decode, 8 prompts x 16 chains, "
+                                "context 32768, w=256, flags Bernoulli(7/8)"),
+    "qwen-r1-1.5b-8x": dict(layers=28, batch=32, kv_heads=2, group=6, head_dim=128,
+                            context=8192, window=256, p_evict=7 / 8, seed=1,
+                            desc="Qwen-R1-1.5B-shaped DMS decode, context 8192, w=256, "
+                                 "flags Bernoulli(7/8)"),
+    "qwen-r1-7b-4x": dict(layers=28, batch=64, kv_heads=4, group=7, head_dim=128,
+                          context=(4096, 32768), window=256, p_evict=3 / 4, seed=2,
+                          desc="Qwen-R1-7B-shaped DMS decode, contexts uniform in "
+                               "[4096, 32768], w=256, flags Bernoulli(3/4)"),
+}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def contexts(wl, rng_seed):
+    import numpy as np
+    c = wl["context"]
+    if isinstance(c, tuple):
+        rng = np.random.default_rng(rng_seed)
+        return rng.integers(c[0], c[1] + 1, size=wl["batch"]).astype(np.int64)
+    return np.full(wl["batch"], c, dtype=np.int64)
+
+
+def build(wl, steps_total, chunk_tokens, dev):
+    """Allocate the cache and fill every layer's state with its context."""
+    import numpy as np
+    import torch
+
+    import dms_synth as sy
+    from paper_2506_05345_amd import dms
+
+    B, H, g, D, w, p = (wl["batch"], wl["kv_heads"], wl["group"], wl["head_dim"],
+                        wl["window"], wl["p_evict"])
+    nl, seed = wl["layers"], wl["seed"]
+    P = 64
+    ctx = contexts(wl, seed)
+    ctx_t = torch.as_tensor(ctx, device=dev)
+    seqs = torch.arange(B, device=dev, dtype=torch.int64)
+    heads = torch.arange(H, device=dev, dtype=torch.int64)
+    # exact retained counts at decode start (flags are a pure function of the
+    # coordinates), used only to size the page pool
+    max_pages_head, pages_layer = 0, 0
+    L0 = []
+    for layer in range(nl):
+        Lh = torch.zeros((B, H), dtype=torch.int64, device=dev)
+        for p0 in range(0, int(ctx.max()), 8192):
+            pos = torch.arange(p0, min(p0 + 8192, int(ctx.max())), device=dev)
+            f = sy.flags_torch(seed, p, layer, seqs[:, None, None], heads[None, None, :],
+                               pos[None, :, None], dev)
+            keep = (pos[None, :, None] < (ctx_t[:, None, None] - w)) & (f == 0)
+            Lh += keep.sum(dim=1)
+        Lh += torch.clamp(ctx_t, max=w)[:, None]
+        L0.append(Lh)
+        need = torch.div(Lh + steps_total + P - 1, P, rounding_mode="floor")
+        max_pages_head = max(max_pages_head, int(need.max()))
+        pages_layer = max(pages_layer, int(need.sum()))
+    cfg = dms.make_config(nl, B, H, g, D, w, P, pages_layer + 8, max_pages_head + 1,
+                          chunk_tokens * B)
+    mb, pb, wb, _ = dms.dms_layout(cfg)
+    log(f"pool {pb * nl / 2**30:.1f} GiB ({pages_layer + 8} pages/layer), meta "
+        f"{mb / 2**30:.2f} GiB, workspace {wb / 2**20:.1f} MiB")
+    cache = dms.DmsCache(cfg, device=dev)
+    gen = torch.Generator(device=dev)
+    sid = torch.arange(B, dtype=torch.int32, device=dev)
+    t0 = time.perf_counter()
+    for layer in range(nl):
+        gen.manual_seed(seed * 1000 + layer)
+        done = np.zeros(B, np.int64)
+        while (done < ctx).any():
+            lens = np.minimum(chunk_tokens, ctx - done)
+            cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+            T = int(cu[-1])
+            k = torch.randn((T, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+            v = torch.randn((T, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+            # flags of every sequence's next positions, varlen layout [T, H]
+            seq_of = torch.repeat_interleave(seqs, torch.as_tensor(lens, device=dev))
+            start = torch.as_tensor(cu[:-1], device=dev, dtype=torch.int64)
+            pos = (torch.arange(T, device=dev) - torch.repeat_interleave(start, torch.as_tensor(lens, device=dev))
+                   + torch.as_tensor(done, device=dev)[seq_of])
+            f = sy.flags_torch(seed, p, layer, seq_of[:, None], heads[None, :], pos[:, None], dev)
+            dms.dms_append_chunk(cache.ctx, layer, B, sid, torch.as_tensor(cu, device=dev), T,
+                                 int(lens.max()), k, v, f)
+            done += lens
+        if layer % 8 == 7 or layer == nl - 1:
+            torch.cuda.synchronize()
+            log(f"built layers 0..{layer} ({time.perf_counter() - t0:.1f}s)")
+    st = dms.dms_status(cache.ctx)
+    if st != 0:
+        raise RuntimeError(f"state build failed: {dms.dms_strerror(st)}")
+    # the device's retained lengths must equal the closed form
+    out = torch.empty((B, H), dtype=torch.int32, device=dev)
+    for layer in range(nl):
+        dms.dms_retained_lengths(cache.ctx, layer, B, sid, out)
+        if not torch.equal(out.to(torch.int64), L0[layer]):
+            raise RuntimeError(f"layer {layer}: retained lengths differ from the closed form")
+    return cache, ctx, L0
+
+
+def step_inputs(wl, ctx, steps_total, dev):
+    """Per (step, layer) decode inputs and the retained length of every head
+    at every step (closed form from the flags)."""
+    import torch
+
+    import dms_synth as sy
+    B, H, g, D, w, p = (wl["batch"], wl["kv_heads"], wl["group"], wl["head_dim"],
+                        wl["window"], wl["p_evict"])
+    nl, seed = wl["layers"], wl["seed"]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seed * 7919 + 17)
+    q = torch.randn((steps_total, nl, B, H * g, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    k = torch.randn((steps_total, nl, B, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    v = torch.randn((steps_total, nl, B, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    ctx_t = torch.as_tensor(ctx, device=dev)
+    seqs = torch.arange(B, device=dev, dtype=torch.int64)
+    heads = torch.arange(H, device=dev, dtype=torch.int64)
+    steps = torch.arange(steps_total, device=dev, dtype=torch.int64)
+    flags = torch.empty((steps_total, nl, B, H), dtype=torch.uint8, device=dev)
+    fresh = torch.empty((steps_total, nl, B, H), dtype=torch.int64, device=dev)
+    for layer in range(nl):
+        pos = ctx_t[None, :, None] + steps[:, None, None]          # [S, B, 1]
+        flags[:, layer] = sy.flags_torch(seed, p, layer, seqs[None, :, None], heads[None, None, :],
+                                         pos, dev)
+        # token t takes a fresh slot unless t >= w and token t - w was flagged
+        prev = sy.flags_torch(seed, p, layer, seqs[None, :, None], heads[None, None, :],
+                              pos - w, dev)
+        fresh[:, layer] = ((pos < w) | (prev == 0)).to(torch.int64)
+    return q, k, v, flags, fresh
+
+
+def cpu_baseline(wl, ctx, budget_s=12.0):
+    """Time the CPU oracle's dense masked attention on sampled heads."""
+    import numpy as np
+
+    import dms_synth as sy
+    from oracle import dense_dms_attention_head
+
+    B, H, g, D, w, p = (wl["batch"], wl["kv_heads"], wl["group"], wl["head_dim"],
+                        wl["window"], wl["p_evict"])
+    nl, seed = wl["layers"], wl["seed"]
+    rng = np.random.default_rng(12345)
+    triples = [(int(rng.integers(nl)), int(rng.integers(B)), int(rng.integers(H))) for _ in range(6)]
+    f32 = sy.bf16_bits_to_f32_np
+    head_steps, bytes_equiv, elapsed = 0, 0, 0.0
+    samples = []
+    for (layer, s, h) in triples:
+        T = int(ctx[s]) + 8
+        pos = np.arange(T)
+        kh = f32(sy.head_sequence_np(seed, sy.STREAM_K, layer, s, h, pos, D))
+        vh = f32(sy.head_sequence_np(seed, sy.STREAM_V, layer, s, h, pos, D))
+        fh = sy.flags_np(seed, p, layer, s, h, pos)
+        qd = np.arange(D)[None, None, :]
+        qh = f32(sy.token_vectors_np(seed, sy.STREAM_Q, layer, s, (h * g + np.arange(g))[None, :, None],
+                                     pos[-8:][:, None, None], qd))
+        samples.append((kh, vh, fh, qh, T))
+    t_start = time.perf_counter()
+    while elapsed < budget_s:
+        for (kh, vh, fh, qh, T) in samples:
+            for i in range(4):
+                t = T - 8 + i
+                t0 = time.perf_counter()
+                dense_dms_attention_head(qh[i:i + 1], kh[:t + 1], vh[:t + 1], fh[:t + 1], w, [t])
+                elapsed += time.perf_counter() - t0
+                head_steps += 1
+                visible = min(w, t + 1) + int(np.sum(fh[: max(0, t - w + 1)] == 0))
+                bytes_equiv += visible * 2 * D * 2
+        if time.perf_counter() - t_start > 4 * budget_s:
+            break
+    threads = os.cpu_count()
+    try:
+        from threadpoolctl import threadpool_info
+        info = threadpool_info()
+        if info:
+            threads = max(int(x.get("num_threads", 1)) for x in info)
+    except Exception:
+        pass
+    return {
+        "value": bytes_equiv / elapsed / 1e9,
+        "unit": "GB/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{head_steps} head-steps (one KV head, its {g} query heads, one decode "
+                  f"position, dense float64 masked attention over the full history) on "
+                  f"{len(samples)} sampled (layer, sequence, KV head) triples; value = their "
+                  f"retained-KV bytes / CPU time",
+        "head_steps_per_s": head_steps / elapsed,
+        "seconds": elapsed,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="qwen-r1-32b-8x", choices=sorted(WORKLOADS))
+    ap.add_argument("--chunk", type=int, default=4096)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; the DMS decode path "
+                                   "has no multi-GPU mode (--gpus must be 1)"}))
+        sys.exit(2)
+
+    import torch
+    from paper_2506_05345_amd import dms
+
+    wl = WORKLOADS[args.workload]
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    S = args.steps + args.warmup
+    cache, ctx, L0 = build(wl, S, args.chunk, dev)
+    q, k, v, flags, fresh = step_inputs(wl, ctx, S, dev)
+    B, H, g, D, nl = wl["batch"], wl["kv_heads"], wl["group"], wl["head_dim"], wl["layers"]
+    sid = torch.arange(B, dtype=torch.int32, device=dev)
+    out = torch.empty((nl, B, H * g, D), dtype=torch.float32, device=dev)
+    # retained length of every head when step s attends (after its append)
+    Lstep = torch.stack(L0)[None] + torch.cumsum(fresh, dim=0)        # [S, nl, B, H]
+    kv_bytes = Lstep.sum(dim=(1, 2, 3)).to(torch.float64) * 2 * D * 2  # per step, all layers
+
+    def run_step(s):
+        for layer in range(nl):
+            dms.dms_decode_step(cache.ctx, layer, B, sid, q[s, layer], k[s, layer], v[s, layer],
+                                flags[s, layer], out[layer])
+
+    for s in range(args.warmup):
+        run_step(s)
+    torch.cuda.synchronize()
+    log("warmup done")
+    dms.dms_profile_start(cache.ctx, args.steps * nl)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record()
+    for s in range(args.warmup, S):
+        run_step(s)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms, launches = dms.dms_profile_stop(cache.ctx)
+    step_ms = ev0.elapsed_time(ev1) / args.steps
+    st = dms.dms_status(cache.ctx)
+    if st != 0:
+        raise RuntimeError(f"decode failed: {dms.dms_strerror(st)}")
+    # the device bookkeeping must have followed the closed form through every step
+    lens = torch.empty((B, H), dtype=torch.int32, device=dev)
+    for layer in range(nl):
+        dms.dms_retained_lengths(cache.ctx, layer, B, sid, lens)
+        if not torch.equal(lens.to(torch.int64), Lstep[-1, layer]):
+            raise RuntimeError(f"layer {layer}: retained lengths diverged from the closed form")
+    timed_bytes = float(kv_bytes[args.warmup:].sum())
+    per_step_bytes = timed_bytes / args.steps
+    value = per_step_bytes / (step_ms * 1e-3) / 1e9
+    per_launch_bytes = timed_bytes / (args.steps * nl)
+    kern_avg_ms = kern_ms / max(launches, 1)
+    achieved = per_launch_bytes / (kern_avg_ms * 1e-3) / 1e9
+    mean_L = float(Lstep[args.warmup:].double().mean())
+    res = {
+        "metric": "DMS decode attn: achieved KV HBM GB/s (% of peak) + decode tok/s at 8x",
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": wl["desc"],
+            "layers": nl, "batch": B, "kv_heads": H, "query_heads": H * g,
+            "head_dim": D, "window": wl["window"], "p_evict": wl["p_evict"],
+            "context": wl["context"] if not isinstance(wl["context"], tuple) else list(wl["context"]),
+            "mean_retained_tokens": round(mean_L, 1),
+            "effective_compression": round(float((ctx.mean() + args.warmup + args.steps / 2) / mean_L), 2),
+            "parallelism": "single GPU",
+        },
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 1),
+        "decode_tok_per_s": round(B / (step_ms * 1e-3), 1),
+        "wall_ms_per_step": round(1e3 * wall / args.steps, 4),
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "kernel": "decode_kernel<128>",
+            "kernel_avg_us": round(1e3 * kern_avg_ms, 2),
+            "bytes_per_launch": int(per_launch_bytes),
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle")
+        res["cpu_baseline"] = cpu_baseline(wl, ctx)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,243 @@
+/*
+ * dms.h -- C ABI of libdms: Dynamic Memory Sparsification (DMS) inference on
+ * one AMD Instinct MI355X (gfx950).
+ *
+ * Method (arxiv 2506.05345, "Inference-Time Hyper-Scaling with KV Cache
+ * Compression"):
+ *   - every new key/value pair (k_t, v_t) of every KV head carries a binary
+ *     eviction decision alpha_t (Sec. 3.1 "Eviction Decisions", Eq. 1;
+ *     binarised by rounding at inference, Sec. 3.2);
+ *   - a pair flagged at step t stays visible until step t + w and is then
+ *     removed (Sec. 3.1 "Delayed Eviction via Sliding Window"): key j is
+ *     visible to query t iff j <= t and (j > t - w or alpha_j = 0), the binary
+ *     case of the mask M_alpha of Fig. 1b;
+ *   - the removed pair's cache slot is overwritten by an incoming pair, and
+ *     the cache is paged with pages owned by one attention head (Sec. 3.2,
+ *     inference paragraph on performance);
+ *   - prefill applies the same mask, passed as a vector of decisions rather
+ *     than a T x T matrix (Sec. 3.1 "Performance Considerations", Sec. 3.2).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *   Hkv = num_kv_heads, g = group_size, Hq = Hkv * g, d = head_dim,
+ *   P = page_size, w = window.  Query head q attends with KV head q / g.
+ *   Keys and queries are passed after any positional encoding; the library
+ *   never applies positions (keys "carry positional information", Sec. 3.2),
+ *   so the order of retained slots is irrelevant to attention.
+ *
+ *   bf16 tensors are IEEE bfloat16 bit patterns (uint16), row-major, densely
+ *   packed.  Decode inputs: q [n, Hq, d], k / v [n, Hkv, d], flags [n, Hkv]
+ *   (uint8, 0 = keep, nonzero = evict after w steps), seq_ids [n] int32.
+ *   Chunk inputs are "varlen": sequence i owns tokens cu_seqlens[i] ..
+ *   cu_seqlens[i+1]-1 of q [T, Hq, d], k / v [T, Hkv, d], flags [T, Hkv].
+ *   Outputs are float32 [n, Hq, d] (decode) or [T, Hq, d] (prefill).
+ *
+ *   Pointers named *_dev are device pointers; *_host are host pointers.
+ *   `stream` is a hipStream_t (NULL = the null stream).  Every call only
+ *   enqueues work on `stream` and returns; device buffers passed in must
+ *   stay valid until that work completes.  One context may be used from one
+ *   stream at a time (the workspace is shared by all layers).
+ *
+ * Ownership
+ * ---------
+ *   The caller allocates and frees every device buffer: the state buffer
+ *   (`meta`), one KV pool per layer, and the workspace, sized by
+ *   dms_layout().  libdms never allocates or frees device memory; a context
+ *   (dms_ctx) is a small host object holding the configuration and the
+ *   caller's pointers.
+ *
+ * Errors
+ * ------
+ *   Every call returns DMS_OK (0) or a negative code.  Argument errors are
+ *   detected on the host before any HIP call and change nothing.  Errors
+ *   that only the device can see (page pool exhausted, a head over
+ *   max_pages_per_head, out-of-range or duplicate sequence ids) are
+ *   recorded in a sticky status word inside `meta`: the offending call
+ *   changes no state, and every later state-changing or attention call on
+ *   the context does nothing (outputs are left untouched) until
+ *   dms_clear_status().  dms_status() reads the word.
+ */
+#ifndef DMS_H_
+#define DMS_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  DMS_OK = 0,
+  DMS_ERR_INVALID = -1,       /* bad configuration or argument (host check) */
+  DMS_ERR_UNSUPPORTED = -2,   /* valid but not implemented (e.g. head_dim 96) */
+  DMS_ERR_HIP = -3,           /* a HIP runtime call or launch failed */
+  DMS_ERR_OUT_OF_PAGES = -4,  /* device: free-page stack exhausted */
+  DMS_ERR_CAPACITY = -5,      /* device: a head needs more than max_pages_per_head */
+  DMS_ERR_BAD_SEQ = -6        /* device: sequence id out of range or repeated */
+};
+
+typedef struct dms_config {
+  int32_t num_layers;         /* >= 1; layers are independent caches */
+  int32_t max_seqs;           /* sequence ids are 0 .. max_seqs-1 (<= 65536) */
+  int32_t num_kv_heads;       /* Hkv >= 1 */
+  int32_t group_size;         /* g = Hq / Hkv, 1 .. 16 */
+  int32_t head_dim;           /* d: 64 or 128 */
+  int32_t window;             /* w >= 1: eviction delay = sliding window */
+  int32_t page_size;          /* P tokens per page: 32, 64, 128 or 256 */
+  int32_t num_pages;          /* pages in each layer's pool */
+  int32_t max_pages_per_head; /* page-table length of one (seq, head) */
+  int32_t max_chunk_tokens;   /* largest total token count of one chunk call */
+  float softmax_scale;        /* <= 0 selects 1 / sqrt(head_dim) */
+} dms_config;
+
+typedef struct dms_ctx dms_ctx;
+
+/*
+ * Byte offsets of the per-layer state inside `meta` (for dms_export_state
+ * readers).  Layer l's region starts at layer0 + l * layer_stride.  Arrays:
+ *   pos        int32 [max_seqs]                    tokens appended per sequence
+ *   len        int32 [max_seqs][Hkv]               retained slots L per head
+ *   ring       int32 [max_seqs][Hkv][w]            slot of position p at p % w,
+ *                                                  bit 31 = that token's flag
+ *   page_table int32 [max_seqs][Hkv][max_pages_per_head]  page of slots
+ *                                                  i*P .. i*P+P-1 (-1 = none)
+ *   slot_meta  int32 [max_seqs][Hkv][max_pages_per_head*P] position held by
+ *                                                  a live slot, bit 31 = flag
+ *   stack      int32 [num_pages]                   free-page stack, entries
+ *                                                  0 .. top-1 are free pages
+ *   top        int32                               stack height
+ * The sticky status word is the int32 at offset `status`.
+ * Only entries that the method defines are meaningful: ring entries of
+ * positions >= pos - w, page-table entries below ceil(L / P), slot_meta
+ * entries below L, stack entries below top.
+ */
+typedef struct dms_state_offsets {
+  size_t status, layer0, layer_stride;
+  size_t pos, len, ring, page_table, slot_meta, stack, top;
+} dms_state_offsets;
+
+/*
+ * Page layout in a layer's pool (`page_bytes` each, page i at i*page_bytes):
+ *   K   bf16 [P][d]   token-major rows (slot % P selects the row)
+ *   V^T bf16 [d][P]   value rows transposed: element (e, s) is V[s][e]
+ * A slot s of a head lives in page page_table[s / P] at row s % P.
+ */
+
+/* Sizes of the caller-owned buffers for `cfg`.  Host only; validates cfg.
+ * meta_bytes: state of all layers + status; pool_bytes: ONE layer's pool;
+ * workspace_bytes: scratch shared by all calls of a context. */
+int dms_layout(const dms_config* cfg, size_t* meta_bytes, size_t* pool_bytes,
+               size_t* workspace_bytes, size_t* page_bytes);
+
+/* Offsets of the state arrays in `meta`.  Host only. */
+int dms_state_layout(const dms_config* cfg, dms_state_offsets* out);
+
+/* Create a context over caller-owned device buffers.  Host only: no HIP call,
+ * the state is NOT initialised (call dms_init_state).  pools_dev_host is a
+ * host array of num_layers device pointers (copied). */
+int dms_create(const dms_config* cfg, void* meta_dev, void* const* pools_dev_host,
+               void* workspace_dev, dms_ctx** out);
+
+/* Free the host context (never touches device memory). */
+int dms_destroy(dms_ctx* ctx);
+
+/* Initialise every layer's state: no sequences, all pages free
+ * (stack[i] = num_pages-1-i, so pages are popped 0, 1, 2, ...), status 0. */
+int dms_init_state(dms_ctx* ctx, void* stream);
+
+/* Release the listed sequences in every layer (layer = -1) or one layer:
+ * their pages are pushed back on the free stack (sequences in call order,
+ * heads ascending, each head's pages in page-table order), and pos, L and the
+ * ring are cleared.  seq_ids_dev: int32 [n]. */
+int dms_seq_reset(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, void* stream);
+
+/* Append one token per listed sequence to one layer (Sec. 3.2 cache
+ * management).  For each (sequence, KV head), with t = pos:
+ *   if t >= w and the token at t - w was flagged, the new token takes that
+ *   token's slot (the flagged token leaves the cache now, w steps after its
+ *   decision); otherwise it takes the next fresh slot L (L += 1), popping a
+ *   page when that slot starts a page.  Pops follow call order, then head.
+ * Then the ring remembers (slot, flag) for position t and pos += 1.
+ * k_dev, v_dev: bf16 [n, Hkv, d]; flags_dev: uint8 [n, Hkv]. */
+int dms_append(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+               const void* k_dev, const void* v_dev, const uint8_t* flags_dev,
+               void* stream);
+
+/* Decode attention of one layer over the current cache: every query head
+ * attends to all live slots of its KV head, which are exactly the keys
+ * visible to the latest position (decode reads only retained tokens; the
+ * cost is the KV bytes read, Sec. 1 and Appendix I).  Split over the
+ * retained tokens of all heads, merged by log-sum-exp.
+ * q_dev: bf16 [n, Hq, d]; out_dev: float32 [n, Hq, d]. */
+int dms_decode(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+               const void* q_dev, float* out_dev, void* stream);
+
+/* One decode step of one layer: dms_append of (k, v, flags) followed by
+ * dms_decode of q, so the new token attends to itself and to every token
+ * still retained (release of t - w, then append of t, then attention). */
+int dms_decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+                    const void* q_dev, const void* k_dev, const void* v_dev,
+                    const uint8_t* flags_dev, float* out_dev, void* stream);
+
+/* Append a chunk of tokens per sequence with no attention: the result equals
+ * appending them one by one in position order, except that page pops of the
+ * whole call go in the order (sequence in call order, head, position).
+ * cu_seqlens_dev: int32 [n+1] device array, cu[0] = 0, non-decreasing,
+ * cu[n] = total_tokens <= max_chunk_tokens, no sequence longer than
+ * max_seqlen (host values used to size the launch; a device array that
+ * disagrees with them sets DMS_ERR_INVALID in the sticky status).
+ * k_dev, v_dev: bf16 [total_tokens, Hkv, d]; flags_dev: uint8 [total_tokens, Hkv]. */
+int dms_append_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+                     const int32_t* cu_seqlens_dev, int total_tokens, int max_seqlen,
+                     const void* k_dev, const void* v_dev, const uint8_t* flags_dev,
+                     void* stream);
+
+/* Masked chunked prefill of one layer (Sec. 3.2: DMS sparsity also skips
+ * prefill work; the mask travels as the decision vector, Sec. 3.1).  Query
+ * at position t of a chunk attends to the cached retained tokens and to the
+ * chunk's own keys j <= t with j > t - w or flag_j = 0 -- cached tokens
+ * flagged within the last w positions expire inside the chunk by the same
+ * rule.  Then the chunk is committed as by dms_append_chunk.
+ * Arguments as for dms_append_chunk, plus q_dev: bf16 [total_tokens, Hq, d]
+ * and out_dev: float32 [total_tokens, Hq, d]. */
+int dms_prefill_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+                      const int32_t* cu_seqlens_dev, int total_tokens, int max_seqlen,
+                      const void* q_dev, const void* k_dev, const void* v_dev,
+                      const uint8_t* flags_dev, float* out_dev, void* stream);
+
+/* Retained lengths L of the listed sequences of one layer (the paper's
+ * per-step "KV-cache token reads", Sec. 5.1): out_dev int32 [n, Hkv]. */
+int dms_retained_lengths(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+                         int32_t* out_dev, void* stream);
+
+/* Copy one layer's state region (dms_state_offsets) plus nothing else into
+ * host memory: bytes must be >= layer_stride.  Synchronises `stream`. */
+int dms_export_state(dms_ctx* ctx, int layer, void* dst_host, size_t bytes, void* stream);
+
+/* Synchronise `stream` and return the sticky device status (DMS_OK or a
+ * negative DMS_ERR_* code), or DMS_ERR_HIP if the copy fails. */
+int dms_status(dms_ctx* ctx, void* stream);
+
+/* Reset the sticky status to DMS_OK (enqueued on `stream`). */
+int dms_clear_status(dms_ctx* ctx, void* stream);
+
+/* Kernel timing instrumentation (not part of the method).  While a session
+ * is active the library records a pair of HIP events around each split-K
+ * decode kernel it launches, for at most max_launches launches; later
+ * launches are not recorded.  Events are created here and destroyed by
+ * dms_profile_stop (no device memory is allocated). */
+int dms_profile_start(dms_ctx* ctx, int max_launches);
+
+/* Wait for the recorded events and end the session: *total_ms = summed
+ * duration of the recorded decode kernels, *launches = how many. */
+int dms_profile_stop(dms_ctx* ctx, float* total_ms, int* launches);
+
+/* Static description of an error code. */
+const char* dms_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DMS_H_ */

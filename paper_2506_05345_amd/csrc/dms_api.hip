@@ -1,0 +1,393 @@
+// C-ABI entry points of libdms: configuration checks, buffer layout, the host
+// context and the per-call argument validation that runs before any HIP call.
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+#include "dms_common.h"
+
+namespace dms {
+
+int validate_config(const dms_config& c) {
+  if (c.num_layers < 1 || c.max_seqs < 1 || c.max_seqs > kMaxSeqs) return DMS_ERR_INVALID;
+  if (c.num_kv_heads < 1 || c.group_size < 1 || c.window < 1) return DMS_ERR_INVALID;
+  if (c.group_size > kMaxGroup) return DMS_ERR_UNSUPPORTED;
+  if (c.head_dim < 1) return DMS_ERR_INVALID;
+  if (c.head_dim != 64 && c.head_dim != 128) return DMS_ERR_UNSUPPORTED;
+  if (c.page_size != 32 && c.page_size != 64 && c.page_size != 128 && c.page_size != 256)
+    return DMS_ERR_INVALID;
+  if (c.num_pages < 1 || c.max_pages_per_head < 1 || c.max_chunk_tokens < 0) return DMS_ERR_INVALID;
+  if (!(c.softmax_scale <= 0.0f || isfinite(c.softmax_scale))) return DMS_ERR_INVALID;
+  if (isnan(c.softmax_scale)) return DMS_ERR_INVALID;
+  // slot and page indices are int32 on the device
+  if (static_cast<int64_t>(c.max_pages_per_head) * c.page_size >= (int64_t(1) << 31)) return DMS_ERR_INVALID;
+  if (static_cast<int64_t>(c.max_seqs) * c.num_kv_heads > (int64_t(1) << 22)) return DMS_ERR_INVALID;
+  if (static_cast<int64_t>(c.max_chunk_tokens) * c.num_kv_heads >= (int64_t(1) << 31)) return DMS_ERR_INVALID;
+  return DMS_OK;
+}
+
+Layout make_layout(const dms_config& c) {
+  Layout lo{};
+  const size_t S = c.max_seqs, H = c.num_kv_heads, w = c.window;
+  const size_t maxp = c.max_pages_per_head, P = c.page_size, D = c.head_dim;
+  lo.max_slots = static_cast<int>(maxp * P);
+  lo.max_heads = static_cast<int>(S * H);
+  lo.max_partials = kMaxWaves + lo.max_heads;
+  // meta
+  lo.status = 0;
+  lo.layer0 = kAlign;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, kAlign); return o; };
+  lo.pos = take(S * 4);
+  lo.len = take(S * H * 4);
+  lo.ring = take(S * H * w * 4);
+  lo.page_table = take(S * H * maxp * 4);
+  lo.slot_meta = take(S * H * maxp * P * 4);
+  lo.stack = take(static_cast<size_t>(c.num_pages) * 4);
+  lo.top = take(4);
+  lo.layer_stride = off;
+  lo.meta_bytes = lo.layer0 + lo.layer_stride * c.num_layers;
+  // pool
+  lo.page_bytes = 2 * P * D * 2;
+  lo.pool_bytes = lo.page_bytes * static_cast<size_t>(c.num_pages);
+  // workspace
+  off = 0;
+  const size_t NH = lo.max_heads, NP = lo.max_partials;
+  lo.ws_head_desc = take(NH * sizeof(HeadDesc));
+  lo.ws_cum_tiles = take((NH + 1) * 4);
+  lo.ws_part_ml = take(NP * kMaxGroup * 8);
+  lo.ws_part_acc = take(NP * c.group_size * D * 4);
+  lo.ws_ck_need = take(NH * 4);
+  lo.ws_ck_fresh = take(NH * 4);
+  lo.ws_ck_base = take(NH * 4);
+  lo.ws_ck_pos0 = take(S * 4);
+  lo.ws_ck_err = take(16);
+  lo.ws_ck_slot = take(static_cast<size_t>(c.max_chunk_tokens) * H * 4);
+  lo.ws_pf_cum = take((NH + 1) * 4);
+  lo.ws_pf_meta = take(static_cast<size_t>(c.max_chunk_tokens) * H * 4);
+  lo.workspace_bytes = off;
+  return lo;
+}
+
+struct Ctx {
+  dms_config cfg;
+  Layout lo;
+  void* meta;
+  std::vector<void*> pools;
+  void* ws;
+  int decode_waves;  // resident decode waves, found on first decode
+  // decode-kernel timing session
+  std::vector<hipEvent_t> ev;
+  int ev_used = 0;
+  bool profiling = false;
+};
+
+}  // namespace dms
+
+using dms::Ctx;
+
+struct dms_ctx {
+  Ctx c;
+};
+
+namespace {
+
+inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+inline int hip_rc(hipError_t e) { return e == hipSuccess ? DMS_OK : DMS_ERR_HIP; }
+
+// Event pair for the next decode launch of a timing session (or nulls).
+void next_events(Ctx& c, hipEvent_t* a, hipEvent_t* b) {
+  *a = nullptr;
+  *b = nullptr;
+  if (!c.profiling || c.ev_used + 2 > static_cast<int>(c.ev.size())) return;
+  *a = c.ev[c.ev_used];
+  *b = c.ev[c.ev_used + 1];
+  c.ev_used += 2;
+}
+
+int check_call(const dms_ctx* ctx, int layer, int n, const void* seq_ids) {
+  if (!ctx) return DMS_ERR_INVALID;
+  if (layer < 0 || layer >= ctx->c.cfg.num_layers) return DMS_ERR_INVALID;
+  if (n < 1 || n > ctx->c.cfg.max_seqs) return DMS_ERR_INVALID;
+  if (!seq_ids) return DMS_ERR_INVALID;
+  return DMS_OK;
+}
+
+int check_chunk(const dms_ctx* ctx, const int32_t* cu, int total, int max_len) {
+  if (!cu) return DMS_ERR_INVALID;
+  if (total < 0 || total > ctx->c.cfg.max_chunk_tokens) return DMS_ERR_INVALID;
+  if (max_len < 0 || max_len > total) return DMS_ERR_INVALID;
+  if (total > 0 && max_len == 0) return DMS_ERR_INVALID;
+  return DMS_OK;
+}
+
+int ensure_waves(dms_ctx* ctx) {
+  if (ctx->c.decode_waves > 0) return DMS_OK;
+  int w = dms::decode_resident_waves(ctx->c.cfg);
+  if (w <= 0) return DMS_ERR_HIP;
+  ctx->c.decode_waves = w < dms::kMaxWaves ? w : dms::kMaxWaves;
+  return DMS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dms_layout(const dms_config* cfg, size_t* meta_bytes, size_t* pool_bytes,
+               size_t* workspace_bytes, size_t* page_bytes) {
+  if (!cfg) return DMS_ERR_INVALID;
+  int rc = dms::validate_config(*cfg);
+  if (rc) return rc;
+  dms::Layout lo = dms::make_layout(*cfg);
+  if (meta_bytes) *meta_bytes = lo.meta_bytes;
+  if (pool_bytes) *pool_bytes = lo.pool_bytes;
+  if (workspace_bytes) *workspace_bytes = lo.workspace_bytes;
+  if (page_bytes) *page_bytes = lo.page_bytes;
+  return DMS_OK;
+}
+
+int dms_state_layout(const dms_config* cfg, dms_state_offsets* out) {
+  if (!cfg || !out) return DMS_ERR_INVALID;
+  int rc = dms::validate_config(*cfg);
+  if (rc) return rc;
+  dms::Layout lo = dms::make_layout(*cfg);
+  out->status = lo.status;
+  out->layer0 = lo.layer0;
+  out->layer_stride = lo.layer_stride;
+  out->pos = lo.pos;
+  out->len = lo.len;
+  out->ring = lo.ring;
+  out->page_table = lo.page_table;
+  out->slot_meta = lo.slot_meta;
+  out->stack = lo.stack;
+  out->top = lo.top;
+  return DMS_OK;
+}
+
+int dms_create(const dms_config* cfg, void* meta_dev, void* const* pools_dev_host,
+               void* workspace_dev, dms_ctx** out) {
+  if (!cfg || !meta_dev || !pools_dev_host || !workspace_dev || !out) return DMS_ERR_INVALID;
+  int rc = dms::validate_config(*cfg);
+  if (rc) return rc;
+  for (int l = 0; l < cfg->num_layers; ++l)
+    if (!pools_dev_host[l]) return DMS_ERR_INVALID;
+  dms_ctx* ctx = new (std::nothrow) dms_ctx;
+  if (!ctx) return DMS_ERR_INVALID;
+  ctx->c.cfg = *cfg;
+  if (!(ctx->c.cfg.softmax_scale > 0.0f))
+    ctx->c.cfg.softmax_scale = 1.0f / sqrtf(static_cast<float>(cfg->head_dim));
+  ctx->c.lo = dms::make_layout(*cfg);
+  ctx->c.meta = meta_dev;
+  ctx->c.pools.assign(pools_dev_host, pools_dev_host + cfg->num_layers);
+  ctx->c.ws = workspace_dev;
+  ctx->c.decode_waves = 0;
+  *out = ctx;
+  return DMS_OK;
+}
+
+int dms_destroy(dms_ctx* ctx) {
+  if (!ctx) return DMS_ERR_INVALID;
+  for (auto& e : ctx->c.ev) hipEventDestroy(e);
+  delete ctx;
+  return DMS_OK;
+}
+
+int dms_init_state(dms_ctx* ctx, void* stream) {
+  if (!ctx) return DMS_ERR_INVALID;
+  return hip_rc(dms::launch_init_state(ctx->c.cfg, ctx->c.lo, ctx->c.meta, ctx->c.ws,
+                                       as_stream(stream)));
+}
+
+int dms_seq_reset(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, void* stream) {
+  if (!ctx) return DMS_ERR_INVALID;
+  if (layer < -1 || layer >= ctx->c.cfg.num_layers) return DMS_ERR_INVALID;
+  if (n < 1 || n > ctx->c.cfg.max_seqs || !seq_ids_dev) return DMS_ERR_INVALID;
+  return hip_rc(dms::launch_seq_reset(ctx->c.cfg, ctx->c.lo, ctx->c.meta, layer, n, seq_ids_dev,
+                                      as_stream(stream)));
+}
+
+int dms_append(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const void* k_dev,
+               const void* v_dev, const uint8_t* flags_dev, void* stream) {
+  int rc = check_call(ctx, layer, n, seq_ids_dev);
+  if (rc) return rc;
+  if (!k_dev || !v_dev || !flags_dev) return DMS_ERR_INVALID;
+  const Ctx& c = ctx->c;
+  hipStream_t st = as_stream(stream);
+  hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, flags_dev,
+                                  true, st);
+  if (e == hipSuccess)
+    e = dms::launch_scatter(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, k_dev, v_dev, st);
+  return hip_rc(e);
+}
+
+int dms_decode(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const void* q_dev,
+               float* out_dev, void* stream) {
+  int rc = check_call(ctx, layer, n, seq_ids_dev);
+  if (rc) return rc;
+  if (!q_dev || !out_dev) return DMS_ERR_INVALID;
+  if ((rc = ensure_waves(ctx))) return rc;
+  const Ctx& c = ctx->c;
+  hipStream_t st = as_stream(stream);
+  hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, nullptr,
+                                  false, st);
+  hipEvent_t e0, e1;
+  next_events(ctx->c, &e0, &e1);
+  if (e == hipSuccess)
+    e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, out_dev,
+                           c.decode_waves, st, e0, e1);
+  return hip_rc(e);
+}
+
+int dms_decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const void* q_dev,
+                    const void* k_dev, const void* v_dev, const uint8_t* flags_dev,
+                    float* out_dev, void* stream) {
+  int rc = check_call(ctx, layer, n, seq_ids_dev);
+  if (rc) return rc;
+  if (!q_dev || !k_dev || !v_dev || !flags_dev || !out_dev) return DMS_ERR_INVALID;
+  if ((rc = ensure_waves(ctx))) return rc;
+  const Ctx& c = ctx->c;
+  hipStream_t st = as_stream(stream);
+  hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, flags_dev,
+                                  true, st);
+  if (e == hipSuccess)
+    e = dms::launch_scatter(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, k_dev, v_dev, st);
+  hipEvent_t e0, e1;
+  next_events(ctx->c, &e0, &e1);
+  if (e == hipSuccess)
+    e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, out_dev,
+                           c.decode_waves, st, e0, e1);
+  return hip_rc(e);
+}
+
+int dms_append_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+                     const int32_t* cu_seqlens_dev, int total_tokens, int max_seqlen,
+                     const void* k_dev, const void* v_dev, const uint8_t* flags_dev,
+                     void* stream) {
+  int rc = check_call(ctx, layer, n, seq_ids_dev);
+  if (rc) return rc;
+  if ((rc = check_chunk(ctx, cu_seqlens_dev, total_tokens, max_seqlen))) return rc;
+  if (total_tokens == 0) return DMS_OK;
+  if (!k_dev || !v_dev || !flags_dev) return DMS_ERR_INVALID;
+  const Ctx& c = ctx->c;
+  return hip_rc(dms::launch_chunk_commit(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n,
+                                         seq_ids_dev, cu_seqlens_dev, total_tokens, max_seqlen,
+                                         k_dev, v_dev, flags_dev, as_stream(stream)));
+}
+
+int dms_prefill_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+                      const int32_t* cu_seqlens_dev, int total_tokens, int max_seqlen,
+                      const void* q_dev, const void* k_dev, const void* v_dev,
+                      const uint8_t* flags_dev, float* out_dev, void* stream) {
+  int rc = check_call(ctx, layer, n, seq_ids_dev);
+  if (rc) return rc;
+  if ((rc = check_chunk(ctx, cu_seqlens_dev, total_tokens, max_seqlen))) return rc;
+  if (total_tokens == 0) return DMS_OK;
+  if (!q_dev || !k_dev || !v_dev || !flags_dev || !out_dev) return DMS_ERR_INVALID;
+  const Ctx& c = ctx->c;
+  hipStream_t st = as_stream(stream);
+  hipError_t e = dms::launch_prefill_attention(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer,
+                                               n, seq_ids_dev, cu_seqlens_dev, total_tokens,
+                                               max_seqlen, q_dev, k_dev, v_dev, flags_dev,
+                                               out_dev, st);
+  if (e == hipSuccess)
+    e = dms::launch_chunk_commit(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, seq_ids_dev,
+                                 cu_seqlens_dev, total_tokens, max_seqlen, k_dev, v_dev,
+                                 flags_dev, st);
+  return hip_rc(e);
+}
+
+int dms_retained_lengths(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+                         int32_t* out_dev, void* stream) {
+  int rc = check_call(ctx, layer, n, seq_ids_dev);
+  if (rc) return rc;
+  if (!out_dev) return DMS_ERR_INVALID;
+  return hip_rc(dms::launch_retained(ctx->c.cfg, ctx->c.lo, ctx->c.meta, layer, n, seq_ids_dev,
+                                     out_dev, as_stream(stream)));
+}
+
+int dms_export_state(dms_ctx* ctx, int layer, void* dst_host, size_t bytes, void* stream) {
+  if (!ctx || !dst_host) return DMS_ERR_INVALID;
+  if (layer < 0 || layer >= ctx->c.cfg.num_layers) return DMS_ERR_INVALID;
+  if (bytes < ctx->c.lo.layer_stride) return DMS_ERR_INVALID;
+  hipStream_t st = as_stream(stream);
+  const char* src = static_cast<const char*>(ctx->c.meta) + ctx->c.lo.layer0 +
+                    static_cast<size_t>(layer) * ctx->c.lo.layer_stride;
+  hipError_t e = hipStreamSynchronize(st);
+  if (e == hipSuccess) e = hipMemcpy(dst_host, src, ctx->c.lo.layer_stride, hipMemcpyDeviceToHost);
+  return hip_rc(e);
+}
+
+int dms_status(dms_ctx* ctx, void* stream) {
+  if (!ctx) return DMS_ERR_INVALID;
+  int32_t v = 0;
+  hipError_t e = hipStreamSynchronize(as_stream(stream));
+  if (e == hipSuccess)
+    e = hipMemcpy(&v, static_cast<char*>(ctx->c.meta) + ctx->c.lo.status, sizeof(v),
+                  hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return DMS_ERR_HIP;
+  return v;
+}
+
+int dms_clear_status(dms_ctx* ctx, void* stream) {
+  if (!ctx) return DMS_ERR_INVALID;
+  int32_t* status = reinterpret_cast<int32_t*>(static_cast<char*>(ctx->c.meta) + ctx->c.lo.status);
+  return hip_rc(dms::launch_set_status(status, 0, as_stream(stream)));
+}
+
+int dms_profile_start(dms_ctx* ctx, int max_launches) {
+  if (!ctx || max_launches < 1 || ctx->c.profiling) return DMS_ERR_INVALID;
+  Ctx& c = ctx->c;
+  c.ev.assign(2 * static_cast<size_t>(max_launches), nullptr);
+  for (auto& e : c.ev) {
+    if (hipEventCreate(&e) != hipSuccess) {
+      for (auto& x : c.ev)
+        if (x) hipEventDestroy(x);
+      c.ev.clear();
+      return DMS_ERR_HIP;
+    }
+  }
+  c.ev_used = 0;
+  c.profiling = true;
+  return DMS_OK;
+}
+
+int dms_profile_stop(dms_ctx* ctx, float* total_ms, int* launches) {
+  if (!ctx || !ctx->c.profiling) return DMS_ERR_INVALID;
+  Ctx& c = ctx->c;
+  float sum = 0.0f;
+  int rc = DMS_OK;
+  for (int i = 0; i + 1 < c.ev_used; i += 2) {
+    float ms = 0.0f;
+    if (hipEventSynchronize(c.ev[i + 1]) != hipSuccess ||
+        hipEventElapsedTime(&ms, c.ev[i], c.ev[i + 1]) != hipSuccess) {
+      rc = DMS_ERR_HIP;
+      break;
+    }
+    sum += ms;
+  }
+  if (total_ms) *total_ms = sum;
+  if (launches) *launches = c.ev_used / 2;
+  for (auto& e : c.ev) hipEventDestroy(e);
+  c.ev.clear();
+  c.ev_used = 0;
+  c.profiling = false;
+  return rc;
+}
+
+const char* dms_strerror(int code) {
+  switch (code) {
+    case DMS_OK: return "ok";
+    case DMS_ERR_INVALID: return "invalid configuration or argument";
+    case DMS_ERR_UNSUPPORTED: return "unsupported configuration";
+    case DMS_ERR_HIP: return "HIP runtime error";
+    case DMS_ERR_OUT_OF_PAGES: return "KV page pool exhausted";
+    case DMS_ERR_CAPACITY: return "a head exceeds max_pages_per_head";
+    case DMS_ERR_BAD_SEQ: return "sequence id out of range or repeated in one call";
+    default: return "unknown error code";
+  }
+}
+
+}  // extern "C"

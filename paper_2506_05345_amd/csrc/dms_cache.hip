@@ -1,0 +1,636 @@
+// DMS KV-cache management on the device (paper Sec. 3.2, inference): per-head
+// paged slots, delayed eviction through the w-entry ring, in-place slot
+// recycling, the free-page stack, chunk commits and sequence release.
+//
+// Every state change of one call is planned before it is applied, so a call
+// that would exhaust the page pool (or overflow a head's page table) changes
+// nothing and only records the error in the sticky status word.
+#include "dms_common.h"
+
+namespace dms {
+namespace {
+
+constexpr int kPlanThreads = 1024;
+
+__device__ inline int load_status(const int32_t* status) {
+  return __atomic_load_n(status, __ATOMIC_RELAXED);
+}
+
+// ---------------------------------------------------------------------------
+// State initialisation and status
+// ---------------------------------------------------------------------------
+
+struct InitArgs {
+  char* meta;
+  int32_t* ck_err;
+  size_t layer0, layer_stride, pos, len, ring, page_table, stack, top;
+  int64_t n_pos, n_len, n_ring, n_pt;
+  int num_pages;
+};
+
+__global__ void init_state_kernel(InitArgs a) {
+  char* b = a.meta + a.layer0 + static_cast<size_t>(blockIdx.y) * a.layer_stride;
+  int32_t* pos = reinterpret_cast<int32_t*>(b + a.pos);
+  int32_t* len = reinterpret_cast<int32_t*>(b + a.len);
+  int32_t* ring = reinterpret_cast<int32_t*>(b + a.ring);
+  int32_t* pt = reinterpret_cast<int32_t*>(b + a.page_table);
+  int32_t* stack = reinterpret_cast<int32_t*>(b + a.stack);
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  const int64_t t0 = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  for (int64_t i = t0; i < a.n_pos; i += stride) pos[i] = 0;
+  for (int64_t i = t0; i < a.n_len; i += stride) len[i] = 0;
+  for (int64_t i = t0; i < a.n_ring; i += stride) ring[i] = 0;
+  for (int64_t i = t0; i < a.n_pt; i += stride) pt[i] = -1;
+  for (int64_t i = t0; i < a.num_pages; i += stride) stack[i] = a.num_pages - 1 - static_cast<int32_t>(i);
+  if (t0 == 0) {
+    *reinterpret_cast<int32_t*>(b + a.top) = a.num_pages;
+    if (blockIdx.y == 0) {
+      *reinterpret_cast<int32_t*>(a.meta) = 0;  // status
+      a.ck_err[0] = 0;
+      a.ck_err[1] = 0;
+    }
+  }
+}
+
+__global__ void set_status_kernel(int32_t* status, int value) {
+  if (threadIdx.x == 0) atomicExch(reinterpret_cast<int*>(status), value);
+}
+
+// ---------------------------------------------------------------------------
+// Sequence-id validation shared by the single-block planners
+// ---------------------------------------------------------------------------
+
+// Returns true (in every thread) when some id is out of range or repeated.
+__device__ bool bad_seq_ids(const int32_t* seq_ids, int n, int max_seqs, uint32_t* seen) {
+  for (int i = threadIdx.x; i < (max_seqs + 31) / 32; i += blockDim.x) seen[i] = 0;
+  __syncthreads();
+  int bad = 0;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    int s = seq_ids[i];
+    if (s < 0 || s >= max_seqs) {
+      bad = 1;
+    } else {
+      uint32_t bit = 1u << (s & 31);
+      uint32_t old = atomicOr(&seen[s >> 5], bit);
+      if (old & bit) bad = 1;
+    }
+  }
+  return __syncthreads_or(bad) != 0;
+}
+
+// ---------------------------------------------------------------------------
+// Sequence release
+// ---------------------------------------------------------------------------
+
+struct ResetArgs {
+  char* meta;
+  size_t layer0, layer_stride;
+  size_t pos, len, ring, page_table, stack, top;
+  int32_t* status;
+  const int32_t* seq_ids;
+  int n, H, w, P, maxp, max_seqs, first_layer;
+};
+
+__global__ __launch_bounds__(kPlanThreads) void seq_reset_kernel(ResetArgs a) {
+  __shared__ uint32_t seen[kMaxSeqs / 32];
+  __shared__ int lds[17];
+  __shared__ int s_abort;
+  if (threadIdx.x == 0) s_abort = load_status(a.status) != 0;
+  __syncthreads();
+  if (s_abort) return;
+  if (bad_seq_ids(a.seq_ids, a.n, a.max_seqs, seen)) {
+    if (threadIdx.x == 0) set_status(a.status, DMS_ERR_BAD_SEQ);
+    return;
+  }
+  char* b = a.meta + a.layer0 + static_cast<size_t>(a.first_layer + blockIdx.x) * a.layer_stride;
+  int32_t* pos = reinterpret_cast<int32_t*>(b + a.pos);
+  int32_t* len = reinterpret_cast<int32_t*>(b + a.len);
+  int32_t* ring = reinterpret_cast<int32_t*>(b + a.ring);
+  int32_t* pt = reinterpret_cast<int32_t*>(b + a.page_table);
+  int32_t* stack = reinterpret_cast<int32_t*>(b + a.stack);
+  int32_t* top = reinterpret_cast<int32_t*>(b + a.top);
+  const int NH = a.n * a.H;
+  const int top0 = *top;
+  int run = 0;
+  for (int base = 0; base < NH; base += blockDim.x) {
+    const int hh = base + threadIdx.x;
+    int np = 0, sh = 0;
+    if (hh < NH) {
+      sh = a.seq_ids[hh / a.H] * a.H + hh % a.H;
+      np = (len[sh] + a.P - 1) / a.P;
+    }
+    int tot;
+    int off = block_exclusive_scan(np, lds, &tot);
+    if (hh < NH) {
+      for (int k = 0; k < np; ++k) {
+        stack[top0 + run + off + k] = pt[static_cast<size_t>(sh) * a.maxp + k];
+        pt[static_cast<size_t>(sh) * a.maxp + k] = -1;
+      }
+      len[sh] = 0;
+      for (int e = 0; e < a.w; ++e) ring[static_cast<size_t>(sh) * a.w + e] = 0;
+    }
+    run += tot;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < a.n; i += blockDim.x) pos[a.seq_ids[i]] = 0;
+  if (threadIdx.x == 0) *top = top0 + run;
+}
+
+// ---------------------------------------------------------------------------
+// Decode append planning (rule R1 for one token per sequence) + per-head
+// descriptors and tile prefix sums for the decode kernel
+// ---------------------------------------------------------------------------
+
+struct PlanArgs {
+  LayerState st;
+  int32_t* status;
+  const int32_t* seq_ids;
+  const uint8_t* flags;  // [n, H] or null when not appending
+  HeadDesc* desc;        // [n*H]
+  int32_t* cum_tiles;    // [n*H + 1]
+  int n, H, w, P, maxp, max_slots, max_seqs, append;
+};
+
+struct HeadStep {
+  int sh, t, slot, reuse;
+};
+
+__device__ inline HeadStep r1_step(const PlanArgs& a, int hh) {
+  HeadStep r;
+  const int s = a.seq_ids[hh / a.H];
+  r.sh = s * a.H + hh % a.H;
+  r.t = a.st.pos[s];
+  const int32_t e = a.st.ring[static_cast<size_t>(r.sh) * a.w + r.t % a.w];
+  // the token that entered w steps ago leaves now if it was flagged; the
+  // incoming token takes its slot
+  r.reuse = (r.t >= a.w) && (static_cast<uint32_t>(e) & kFlagBit);
+  r.slot = r.reuse ? static_cast<int>(static_cast<uint32_t>(e) & ~kFlagBit) : a.st.len[r.sh];
+  return r;
+}
+
+__global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
+  __shared__ uint32_t seen[kMaxSeqs / 32];
+  __shared__ int lds[17];
+  __shared__ int s_abort;
+  if (threadIdx.x == 0) s_abort = load_status(a.status) != 0;
+  __syncthreads();
+  if (s_abort) return;
+  if (bad_seq_ids(a.seq_ids, a.n, a.max_seqs, seen)) {
+    if (threadIdx.x == 0) set_status(a.status, DMS_ERR_BAD_SEQ);
+    return;
+  }
+  const int NH = a.n * a.H;
+  const int top0 = *a.st.top;
+  int total_need = 0;
+  if (a.append) {
+    int cap = 0;
+    for (int base = 0; base < NH; base += blockDim.x) {
+      const int hh = base + threadIdx.x;
+      int need = 0;
+      if (hh < NH) {
+        HeadStep r = r1_step(a, hh);
+        if (!r.reuse) {
+          if (r.slot >= a.max_slots) cap = 1;
+          need = (r.slot % a.P) == 0;
+        }
+      }
+      int tot;
+      block_exclusive_scan(need, lds, &tot);
+      total_need += tot;
+    }
+    cap = __syncthreads_or(cap);
+    if (cap || total_need > top0) {
+      if (threadIdx.x == 0) set_status(a.status, cap ? DMS_ERR_CAPACITY : DMS_ERR_OUT_OF_PAGES);
+      return;
+    }
+  }
+  int run_pop = 0, run_tiles = 0;
+  for (int base = 0; base < NH; base += blockDim.x) {
+    const int hh = base + threadIdx.x;
+    int need = 0, tiles = 0, Lnew = 0, slot = -1, sh = 0, t = 0, fresh = 0;
+    if (hh < NH) {
+      if (a.append) {
+        HeadStep r = r1_step(a, hh);
+        sh = r.sh;
+        t = r.t;
+        slot = r.slot;
+        fresh = !r.reuse;
+        need = fresh && (slot % a.P) == 0;
+        Lnew = a.st.len[sh] + fresh;
+      } else {
+        sh = a.seq_ids[hh / a.H] * a.H + hh % a.H;
+        Lnew = a.st.len[sh];
+      }
+      tiles = (Lnew + kTile - 1) / kTile;
+    }
+    int totp, tott;
+    const int pop = run_pop + block_exclusive_scan(need, lds, &totp);
+    const int ct = run_tiles + block_exclusive_scan(tiles, lds, &tott);
+    if (hh < NH) {
+      if (a.append) {
+        const uint32_t f = a.flags[hh] ? kFlagBit : 0u;
+        if (need) a.st.page_table[static_cast<size_t>(sh) * a.maxp + slot / a.P] = a.st.stack[top0 - 1 - pop];
+        if (fresh) a.st.len[sh] = Lnew;
+        a.st.ring[static_cast<size_t>(sh) * a.w + t % a.w] = static_cast<int32_t>(static_cast<uint32_t>(slot) | f);
+        a.st.slot_meta[static_cast<size_t>(sh) * a.max_slots + slot] = static_cast<int32_t>(static_cast<uint32_t>(t) | f);
+      }
+      a.desc[hh] = make_int4(Lnew, sh, slot, 0);
+      a.cum_tiles[hh + 1] = ct + tiles;
+    }
+    run_pop += totp;
+    run_tiles += tott;
+  }
+  if (threadIdx.x == 0) a.cum_tiles[0] = 0;
+  __syncthreads();  // every read of pos above happens before these writes
+  if (a.append) {
+    for (int i = threadIdx.x; i < a.n; i += blockDim.x) a.st.pos[a.seq_ids[i]] += 1;
+    if (threadIdx.x == 0) *a.st.top = top0 - total_need;
+  }
+}
+
+// Copy each appended token's K row and V column into its slot.
+struct ScatterArgs {
+  const int32_t* status;
+  const HeadDesc* desc;
+  const int32_t* page_table;
+  char* pool;
+  const uint16_t* k;
+  const uint16_t* v;
+  size_t page_bytes;
+  int D, P, maxp;
+};
+
+__global__ __launch_bounds__(64) void scatter_kernel(ScatterArgs a) {
+  if (load_status(a.status) != 0) return;
+  const int hh = blockIdx.x;
+  const HeadDesc d = a.desc[hh];
+  const int slot = d.z;
+  const int page = a.page_table[static_cast<size_t>(d.y) * a.maxp + slot / a.P];
+  const int row = slot % a.P;
+  char* pg = a.pool + static_cast<size_t>(page) * a.page_bytes;
+  const int lane = threadIdx.x;
+  if (lane < a.D / 8)
+    reinterpret_cast<uint4*>(pg + static_cast<size_t>(row) * a.D * 2)[lane] =
+        reinterpret_cast<const uint4*>(a.k + static_cast<size_t>(hh) * a.D)[lane];
+  uint16_t* vt = reinterpret_cast<uint16_t*>(pg + static_cast<size_t>(a.P) * a.D * 2);
+  for (int e = lane; e < a.D; e += 64) vt[e * a.P + row] = a.v[static_cast<size_t>(hh) * a.D + e];
+}
+
+struct RetainedArgs {
+  const int32_t* len;
+  const int32_t* seq_ids;
+  int32_t* out;
+  int n, H;
+};
+
+__global__ void retained_kernel(RetainedArgs a) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < a.n * a.H) a.out[i] = a.len[a.seq_ids[i / a.H] * a.H + i % a.H];
+}
+
+// ---------------------------------------------------------------------------
+// Chunk commit: rule R1 applied to C tokens of each (sequence, head) at once.
+//
+// For chunk token c at position t = pos0 + c: it reuses the slot of position
+// t - w iff t >= w and that token was flagged ("reuse"); otherwise it is
+// fresh and takes slot L0 + (number of fresh chunk tokens before c).  A
+// reusing token's slot is found by walking back in steps of w until a fresh
+// chunk token or a position from before the chunk (read from the ring).
+// Only tokens whose slot is not taken over later inside the chunk write K/V.
+// ---------------------------------------------------------------------------
+
+struct ChunkArgs {
+  LayerState st;
+  int32_t* status;
+  const int32_t* seq_ids;
+  const int32_t* cu;
+  const uint8_t* flags;   // [T, H]
+  const uint16_t* k;      // [T, H, D]
+  const uint16_t* v;
+  char* pool;
+  size_t page_bytes;
+  int32_t* need;          // [n*H] pages to pop per head
+  int32_t* fresh;         // [n*H] fresh tokens per head
+  int32_t* base;          // [n*H] first pop index per head
+  int32_t* pos0;          // [n] position of each sequence before the chunk
+  int32_t* err;           // call-local error word, err[1] = stack height before the call
+  int32_t* slots;         // [T, H] slot of every chunk token
+  int n, H, w, P, D, maxp, max_slots, max_seqs, total, max_len;
+};
+
+__device__ inline int chunk_flag(const ChunkArgs& a, int tok0, int c, int h) {
+  return a.flags[static_cast<size_t>(tok0 + c) * a.H + h] != 0;
+}
+
+// Does chunk token c (position pos0 + c) reuse the slot of position pos0 + c - w?
+__device__ inline bool chunk_reuse(const ChunkArgs& a, int sh, int h, int tok0, int pos0, int c) {
+  const int t = pos0 + c;
+  if (t < a.w) return false;
+  const int j = c - a.w;
+  if (j >= 0) return chunk_flag(a, tok0, j, h);
+  const int32_t e = a.st.ring[static_cast<size_t>(sh) * a.w + (t - a.w) % a.w];
+  return (static_cast<uint32_t>(e) & kFlagBit) != 0;
+}
+
+// Pass 1 (one block per head): count fresh tokens and the pages they need.
+__global__ __launch_bounds__(256) void chunk_count_kernel(ChunkArgs a) {
+  __shared__ int lds[17];
+  if (load_status(a.status) != 0) return;
+  const int hh = blockIdx.x;
+  const int i = hh / a.H, h = hh % a.H;
+  const int s = a.seq_ids[i];
+  const int tok0 = a.cu[i], C = a.cu[i + 1] - a.cu[i];
+  bool bad = (s < 0 || s >= a.max_seqs || C < 0 || C > a.max_len || a.cu[0] != 0 ||
+              a.cu[a.n] != a.total || tok0 < 0 || tok0 + C > a.total);
+  if (bad) {
+    if (threadIdx.x == 0) atomicCAS(reinterpret_cast<int*>(a.err), 0, DMS_ERR_INVALID);
+    return;
+  }
+  const int sh = s * a.H + h;
+  const int pos0 = a.st.pos[s];
+  int cnt = 0;
+  for (int c0 = 0; c0 < C; c0 += blockDim.x) {
+    const int c = c0 + threadIdx.x;
+    int f = (c < C) && !chunk_reuse(a, sh, h, tok0, pos0, c);
+    int tot;
+    block_exclusive_scan(f, lds, &tot);
+    cnt += tot;
+  }
+  if (threadIdx.x == 0) {
+    const int L0 = a.st.len[sh];
+    const int L1 = L0 + cnt;
+    if (L1 > a.max_slots) atomicCAS(reinterpret_cast<int*>(a.err), 0, DMS_ERR_CAPACITY);
+    a.fresh[hh] = cnt;
+    a.need[hh] = (L1 + a.P - 1) / a.P - (L0 + a.P - 1) / a.P;
+    if (h == 0) a.pos0[i] = pos0;
+  }
+}
+
+// Pass 2 (one block): validate ids, order the pops, reserve the pages.
+__global__ __launch_bounds__(kPlanThreads) void chunk_pages_kernel(ChunkArgs a) {
+  __shared__ uint32_t seen[kMaxSeqs / 32];
+  __shared__ int lds[17];
+  __shared__ int s_abort;
+  if (threadIdx.x == 0) s_abort = load_status(a.status) != 0;
+  __syncthreads();
+  if (s_abort) return;
+  // pass 1 of this call ran iff this pass runs: consume and clear its error word
+  const int err = *a.err;
+  __syncthreads();
+  if (threadIdx.x == 0) a.err[0] = 0;
+  if (bad_seq_ids(a.seq_ids, a.n, a.max_seqs, seen)) {
+    if (threadIdx.x == 0) set_status(a.status, DMS_ERR_BAD_SEQ);
+    return;
+  }
+  const int NH = a.n * a.H;
+  const int top0 = *a.st.top;
+  int run = 0;
+  for (int base = 0; base < NH; base += blockDim.x) {
+    const int hh = base + threadIdx.x;
+    const int nd = hh < NH ? a.need[hh] : 0;
+    int tot;
+    const int off = block_exclusive_scan(nd, lds, &tot);
+    if (hh < NH) a.base[hh] = run + off;
+    run += tot;
+  }
+  if (threadIdx.x == 0) {
+    if (err != 0) {
+      set_status(a.status, err);
+    } else if (run > top0) {
+      set_status(a.status, DMS_ERR_OUT_OF_PAGES);
+    } else {
+      *a.st.top = top0 - run;
+      a.err[1] = top0;
+    }
+  }
+  __syncthreads();
+  // positions advance here: pass 1 has read them, pass 3 uses pos0
+  if (err == 0 && run <= top0)
+    for (int i = threadIdx.x; i < a.n; i += blockDim.x)
+      a.st.pos[a.seq_ids[i]] = a.pos0[i] + (a.cu[i + 1] - a.cu[i]);
+}
+
+// Pass 3 (one block per head): slots, page table, ring, slot metadata, K/V.
+__global__ __launch_bounds__(256) void chunk_commit_kernel(ChunkArgs a) {
+  __shared__ int lds[17];
+  if (load_status(a.status) != 0) return;
+  const int top_before = a.err[1];
+  const int hh = blockIdx.x;
+  const int i = hh / a.H, h = hh % a.H;
+  const int s = a.seq_ids[i];
+  const int sh = s * a.H + h;
+  const int tok0 = a.cu[i], C = a.cu[i + 1] - a.cu[i];
+  const int pos0 = a.pos0[i];
+  const int L0 = a.st.len[sh];
+  const size_t pt_base = static_cast<size_t>(sh) * a.maxp;
+  // new pages, popped in page-index order from this head's reserved range
+  const int first_new_page = (L0 + a.P - 1) / a.P;
+  for (int k = threadIdx.x; k < a.need[hh]; k += blockDim.x)
+    a.st.page_table[pt_base + first_new_page + k] = a.st.stack[top_before - 1 - (a.base[hh] + k)];
+  // fresh slot numbers
+  int run = 0;
+  for (int c0 = 0; c0 < C; c0 += blockDim.x) {
+    const int c = c0 + threadIdx.x;
+    const int f = (c < C) && !chunk_reuse(a, sh, h, tok0, pos0, c);
+    int tot;
+    const int off = block_exclusive_scan(f, lds, &tot);
+    if (f) a.slots[static_cast<size_t>(tok0 + c) * a.H + h] = L0 + run + off;
+    run += tot;
+  }
+  __syncthreads();
+  // reused slots: follow the stride-w chain back to a fresh token or the ring
+  for (int c = threadIdx.x; c < C; c += blockDim.x) {
+    if (!chunk_reuse(a, sh, h, tok0, pos0, c)) continue;
+    int x = c;
+    while (x >= 0 && chunk_reuse(a, sh, h, tok0, pos0, x)) x -= a.w;
+    int slot;
+    if (x >= 0) {
+      slot = a.slots[static_cast<size_t>(tok0 + x) * a.H + h];
+    } else {
+      const int32_t e = a.st.ring[static_cast<size_t>(sh) * a.w + (pos0 + x) % a.w];
+      slot = static_cast<int>(static_cast<uint32_t>(e) & ~kFlagBit);
+    }
+    a.slots[static_cast<size_t>(tok0 + c) * a.H + h] = slot;
+  }
+  __syncthreads();  // ring reads above complete before the ring is rewritten
+  const int ring_from = C > a.w ? C - a.w : 0;
+  char* pool = a.pool;
+  for (int c = threadIdx.x; c < C; c += blockDim.x) {
+    const int fl = chunk_flag(a, tok0, c, h);
+    const uint32_t fb = fl ? kFlagBit : 0u;
+    const int slot = a.slots[static_cast<size_t>(tok0 + c) * a.H + h];
+    if (c >= ring_from)
+      a.st.ring[static_cast<size_t>(sh) * a.w + (pos0 + c) % a.w] =
+          static_cast<int32_t>(static_cast<uint32_t>(slot) | fb);
+    const bool survives = (c + a.w >= C) || !fl;
+    if (survives)
+      a.st.slot_meta[static_cast<size_t>(sh) * a.max_slots + slot] =
+          static_cast<int32_t>(static_cast<uint32_t>(pos0 + c) | fb);
+  }
+  if (threadIdx.x == 0) a.st.len[sh] = L0 + a.fresh[hh];
+  __syncthreads();  // page-table entries written above are visible to the copies below
+  // K rows and V columns of surviving tokens: D/8 lanes per token for K
+  const int kq = a.D / 8;
+  for (int idx = threadIdx.x; idx < C * kq; idx += blockDim.x) {
+    const int c = idx / kq, part = idx % kq;
+    if (!((c + a.w >= C) || !chunk_flag(a, tok0, c, h))) continue;
+    const int slot = a.slots[static_cast<size_t>(tok0 + c) * a.H + h];
+    const int page = a.st.page_table[pt_base + slot / a.P];
+    char* pg = pool + static_cast<size_t>(page) * a.page_bytes;
+    const size_t src = (static_cast<size_t>(tok0 + c) * a.H + h) * a.D;
+    reinterpret_cast<uint4*>(pg + static_cast<size_t>(slot % a.P) * a.D * 2)[part] =
+        reinterpret_cast<const uint4*>(a.k + src)[part];
+    uint16_t* vt = reinterpret_cast<uint16_t*>(pg + static_cast<size_t>(a.P) * a.D * 2);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) vt[(part * 8 + e) * a.P + slot % a.P] = a.v[src + part * 8 + e];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_init_state(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                             hipStream_t st) {
+  InitArgs a;
+  a.meta = static_cast<char*>(meta);
+  a.ck_err = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_ck_err);
+  a.layer0 = lo.layer0;
+  a.layer_stride = lo.layer_stride;
+  a.pos = lo.pos;
+  a.len = lo.len;
+  a.ring = lo.ring;
+  a.page_table = lo.page_table;
+  a.stack = lo.stack;
+  a.top = lo.top;
+  a.n_pos = c.max_seqs;
+  a.n_len = static_cast<int64_t>(c.max_seqs) * c.num_kv_heads;
+  a.n_ring = a.n_len * c.window;
+  a.n_pt = a.n_len * c.max_pages_per_head;
+  a.num_pages = c.num_pages;
+  dim3 grid(256, c.num_layers);
+  hipLaunchKernelGGL(init_state_kernel, grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_set_status(int32_t* status, int value, hipStream_t st) {
+  hipLaunchKernelGGL(set_status_kernel, dim3(1), dim3(64), 0, st, status, value);
+  return hipGetLastError();
+}
+
+hipError_t launch_seq_reset(const dms_config& c, const Layout& lo, void* meta, int layer, int n,
+                            const int32_t* seq_ids, hipStream_t st) {
+  ResetArgs a;
+  a.meta = static_cast<char*>(meta);
+  a.layer0 = lo.layer0;
+  a.layer_stride = lo.layer_stride;
+  a.pos = lo.pos;
+  a.len = lo.len;
+  a.ring = lo.ring;
+  a.page_table = lo.page_table;
+  a.stack = lo.stack;
+  a.top = lo.top;
+  a.status = reinterpret_cast<int32_t*>(static_cast<char*>(meta) + lo.status);
+  a.seq_ids = seq_ids;
+  a.n = n;
+  a.H = c.num_kv_heads;
+  a.w = c.window;
+  a.P = c.page_size;
+  a.maxp = c.max_pages_per_head;
+  a.max_seqs = c.max_seqs;
+  a.first_layer = layer < 0 ? 0 : layer;
+  const int nl = layer < 0 ? c.num_layers : 1;
+  hipLaunchKernelGGL(seq_reset_kernel, dim3(nl), dim3(kPlanThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* ws, int layer,
+                       int n, const int32_t* seq_ids, const uint8_t* flags, bool append,
+                       hipStream_t st) {
+  PlanArgs a;
+  a.st = layer_state(lo, meta, layer);
+  a.status = reinterpret_cast<int32_t*>(static_cast<char*>(meta) + lo.status);
+  a.seq_ids = seq_ids;
+  a.flags = flags;
+  a.desc = reinterpret_cast<HeadDesc*>(static_cast<char*>(ws) + lo.ws_head_desc);
+  a.cum_tiles = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_cum_tiles);
+  a.n = n;
+  a.H = c.num_kv_heads;
+  a.w = c.window;
+  a.P = c.page_size;
+  a.maxp = c.max_pages_per_head;
+  a.max_slots = lo.max_slots;
+  a.max_seqs = c.max_seqs;
+  a.append = append ? 1 : 0;
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
+                          int layer, int n, const void* k, const void* v, hipStream_t st) {
+  ScatterArgs a;
+  LayerState s = layer_state(lo, meta, layer);
+  a.status = reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status);
+  a.desc = reinterpret_cast<const HeadDesc*>(static_cast<char*>(ws) + lo.ws_head_desc);
+  a.page_table = s.page_table;
+  a.pool = static_cast<char*>(pool);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.page_bytes = lo.page_bytes;
+  a.D = c.head_dim;
+  a.P = c.page_size;
+  a.maxp = c.max_pages_per_head;
+  hipLaunchKernelGGL(scatter_kernel, dim3(n * c.num_kv_heads), dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_retained(const dms_config& c, const Layout& lo, void* meta, int layer, int n,
+                           const int32_t* seq_ids, int32_t* out, hipStream_t st) {
+  RetainedArgs a;
+  a.len = layer_state(lo, meta, layer).len;
+  a.seq_ids = seq_ids;
+  a.out = out;
+  a.n = n;
+  a.H = c.num_kv_heads;
+  const int total = n * c.num_kv_heads;
+  hipLaunchKernelGGL(retained_kernel, dim3((total + 255) / 256), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_chunk_commit(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                               void* pool, int layer, int n, const int32_t* seq_ids,
+                               const int32_t* cu, int total_tokens, int max_len, const void* k,
+                               const void* v, const uint8_t* flags, hipStream_t st) {
+  ChunkArgs a;
+  char* w = static_cast<char*>(ws);
+  a.st = layer_state(lo, meta, layer);
+  a.status = reinterpret_cast<int32_t*>(static_cast<char*>(meta) + lo.status);
+  a.seq_ids = seq_ids;
+  a.cu = cu;
+  a.flags = flags;
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.pool = static_cast<char*>(pool);
+  a.page_bytes = lo.page_bytes;
+  a.need = reinterpret_cast<int32_t*>(w + lo.ws_ck_need);
+  a.fresh = reinterpret_cast<int32_t*>(w + lo.ws_ck_fresh);
+  a.base = reinterpret_cast<int32_t*>(w + lo.ws_ck_base);
+  a.pos0 = reinterpret_cast<int32_t*>(w + lo.ws_ck_pos0);
+  a.err = reinterpret_cast<int32_t*>(w + lo.ws_ck_err);
+  a.slots = reinterpret_cast<int32_t*>(w + lo.ws_ck_slot);
+  a.n = n;
+  a.H = c.num_kv_heads;
+  a.w = c.window;
+  a.P = c.page_size;
+  a.D = c.head_dim;
+  a.maxp = c.max_pages_per_head;
+  a.max_slots = lo.max_slots;
+  a.max_seqs = c.max_seqs;
+  a.total = total_tokens;
+  a.max_len = max_len;
+  const int NH = n * c.num_kv_heads;
+  hipLaunchKernelGGL(chunk_count_kernel, dim3(NH), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(chunk_pages_kernel, dim3(1), dim3(kPlanThreads), 0, st, a);
+  hipLaunchKernelGGL(chunk_commit_kernel, dim3(NH), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace dms

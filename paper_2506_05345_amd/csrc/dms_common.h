@@ -1,0 +1,149 @@
+// Internal definitions shared by the libdms translation units: buffer layout,
+// per-layer state views and small device helpers.  gfx950 (CDNA4) only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/dms.h"
+
+namespace dms {
+
+constexpr int kTile = 32;            // tokens per decode tile (k of one PV MFMA)
+constexpr int kMaxWaves = 8192;      // upper bound on decode waves (workspace sizing)
+constexpr int kMaxGroup = 16;        // query heads per KV head (MFMA column count)
+constexpr int kMaxSeqs = 65536;      // sequence-id bitmap of the planning kernel
+constexpr uint32_t kFlagBit = 0x80000000u;
+constexpr int kAlign = 256;
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Offsets of everything inside the caller's three buffers.
+struct Layout {
+  // meta
+  size_t status, layer0, layer_stride;
+  size_t pos, len, ring, page_table, slot_meta, stack, top;
+  size_t meta_bytes;
+  // pool of one layer
+  size_t page_bytes, pool_bytes;
+  // workspace
+  size_t ws_head_desc, ws_cum_tiles, ws_part_ml, ws_part_acc;
+  size_t ws_ck_need, ws_ck_fresh, ws_ck_base, ws_ck_pos0, ws_ck_err, ws_ck_slot;
+  size_t ws_pf_cum, ws_pf_meta;
+  size_t workspace_bytes;
+  int max_heads, max_partials, max_slots;
+};
+
+// Host-side validation; returns DMS_OK or an error code.
+int validate_config(const dms_config& c);
+Layout make_layout(const dms_config& c);
+
+// Device view of one layer's state.
+struct LayerState {
+  int32_t* pos;         // [S]
+  int32_t* len;         // [S][Hkv]
+  int32_t* ring;        // [S][Hkv][w]
+  int32_t* page_table;  // [S][Hkv][max_pages]
+  int32_t* slot_meta;   // [S][Hkv][max_slots]
+  int32_t* stack;       // [num_pages]
+  int32_t* top;         // [1]
+};
+
+inline LayerState layer_state(const Layout& lo, void* meta, int layer) {
+  char* b = static_cast<char*>(meta) + lo.layer0 + static_cast<size_t>(layer) * lo.layer_stride;
+  LayerState s;
+  s.pos = reinterpret_cast<int32_t*>(b + lo.pos);
+  s.len = reinterpret_cast<int32_t*>(b + lo.len);
+  s.ring = reinterpret_cast<int32_t*>(b + lo.ring);
+  s.page_table = reinterpret_cast<int32_t*>(b + lo.page_table);
+  s.slot_meta = reinterpret_cast<int32_t*>(b + lo.slot_meta);
+  s.stack = reinterpret_cast<int32_t*>(b + lo.stack);
+  s.top = reinterpret_cast<int32_t*>(b + lo.top);
+  return s;
+}
+
+// Per-head descriptor written by the planning kernels, one per (seq in call,
+// KV head) in call order: x = retained length L, y = state head index
+// (seq * Hkv + head), z = slot written by this call's token (decode), w = 0.
+typedef int4 HeadDesc;
+
+// ---------------------------------------------------------------------------
+// Device helpers
+// ---------------------------------------------------------------------------
+
+// Inclusive prefix sum across one wave64.
+__device__ inline int wave_inclusive_scan(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    int u = __shfl_up(v, off, 64);
+    if (lane >= off) v += u;
+  }
+  return v;
+}
+
+// Exclusive prefix sum across the block (blockDim.x multiple of 64, <= 1024).
+// `lds` holds 17 ints.  Returns the exclusive prefix; *total gets the block sum.
+__device__ inline int block_exclusive_scan(int v, int* lds, int* total) {
+  const int lane = threadIdx.x & 63;
+  const int wid = threadIdx.x >> 6;
+  const int nw = blockDim.x >> 6;
+  int inc = wave_inclusive_scan(v);
+  if (lane == 63) lds[wid] = inc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int run = 0;
+    for (int i = 0; i < nw; ++i) {
+      int t = lds[i];
+      lds[i] = run;
+      run += t;
+    }
+    lds[16] = run;
+  }
+  __syncthreads();
+  int excl = lds[wid] + inc - v;
+  *total = lds[16];
+  __syncthreads();
+  return excl;
+}
+
+// Record the first device-side error (vector atomic; never a scalar store).
+__device__ inline void set_status(int32_t* status, int code) {
+  atomicCAS(reinterpret_cast<int*>(status), 0, code);
+}
+
+// ---------------------------------------------------------------------------
+// Launchers implemented in the kernel translation units
+// ---------------------------------------------------------------------------
+
+struct Ctx;  // host context (dms_api.hip)
+
+hipError_t launch_init_state(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                             hipStream_t st);
+hipError_t launch_set_status(int32_t* status, int value, hipStream_t st);
+hipError_t launch_seq_reset(const dms_config& c, const Layout& lo, void* meta, int layer,
+                            int n, const int32_t* seq_ids, hipStream_t st);
+hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* ws, int layer,
+                       int n, const int32_t* seq_ids, const uint8_t* flags, bool append,
+                       hipStream_t st);
+hipError_t launch_scatter(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                          void* pool, int layer, int n, const void* k, const void* v,
+                          hipStream_t st);
+hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                         void* pool, int layer, int n, const void* q, float* out,
+                         int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop);
+int decode_resident_waves(const dms_config& c);
+hipError_t launch_retained(const dms_config& c, const Layout& lo, void* meta, int layer, int n,
+                           const int32_t* seq_ids, int32_t* out, hipStream_t st);
+hipError_t launch_chunk_commit(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                               void* pool, int layer, int n, const int32_t* seq_ids,
+                               const int32_t* cu, int total_tokens, int max_len, const void* k,
+                               const void* v, const uint8_t* flags, hipStream_t st);
+hipError_t launch_prefill_attention(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                                    void* pool, int layer, int n, const int32_t* seq_ids,
+                                    const int32_t* cu, int total_tokens, int max_len,
+                                    const void* q, const void* k, const void* v,
+                                    const uint8_t* flags, float* out, hipStream_t st);
+
+}  // namespace dms

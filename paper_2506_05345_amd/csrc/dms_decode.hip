@@ -1,0 +1,371 @@
+// GQA split-K flash-decode over the retained DMS slots, gfx950.
+//
+// After the append of step t, the live slots of a head are exactly the keys
+// visible to query t (paper Sec. 3.1-3.2: a flagged key leaves the cache when
+// it leaves the window), so decode attention needs no mask: every query head
+// of a group attends to slots 0 .. L-1 of its KV head.  The cost is the KV
+// bytes read (Sec. 1; Appendix I), so the kernel is built around streaming
+// those bytes once:
+//
+//  * Work split: the retained tokens of all (sequence, KV head) pairs of the
+//    call are cut into 32-token tiles, and the flat tile list is divided into
+//    equal contiguous ranges, one per resident wave ("stream-K"): ragged
+//    per-head lengths (Sec. 3.1: heads compress at different rates) do not
+//    unbalance the chip.  A wave that covers a whole head writes the final
+//    output; otherwise it writes a partial (running max, sum, accumulator)
+//    merged by the combine kernel with log-sum-exp weights.
+//  * Per tile, each lane issues 16-byte loads straight into MFMA operand
+//    registers: K rows [P][d] of the page as the A operand of S^T = K Q^T and
+//    the transposed value block V^T [d][P] of the page as the A operand of
+//    O^T = V^T P^T.  No LDS round trip is needed.  The group's g query heads
+//    fill g of the 16 MFMA columns.
+//  * The 16x16 accumulator layout puts rows 4*(lane/16) .. +3 of column
+//    lane%16 in each lane.  Tile rows of the first / second score MFMA are
+//    assigned tokens 8*(r/4) + r%4 and 8*(r/4) + 4 + r%4, so after both MFMAs
+//    lane group G holds the scores of tokens 8G .. 8G+7 -- exactly the k
+//    slice the PV MFMA's B operand wants in that lane.  Scores never leave
+//    registers.
+//  * Online softmax in the exp2 domain: per-lane max over its 8 scores, then
+//    two cross-row shuffles; the running sum stays per lane until the end.
+#include "dms_common.h"
+
+namespace dms {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+
+constexpr int kWavesPerBlock = 4;
+
+__device__ inline int load_status(const int32_t* status) {
+  return __atomic_load_n(status, __ATOMIC_RELAXED);
+}
+
+__device__ inline f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+__device__ inline u32x4 ldg16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+struct DecodeArgs {
+  const int32_t* status;
+  const HeadDesc* desc;      // [NH]
+  const int32_t* cum_tiles;  // [NH + 1]
+  const int32_t* page_table; // layer page table base
+  const char* pool;          // layer pool base
+  const uint16_t* q;         // [NH * g, D]
+  float2* part_ml;           // [partials][16]  (max in log2 units, sum)
+  float* part_acc;           // [partials][g][D]
+  float* out;                // [NH * g, D]
+  size_t page_bytes;
+  int NH, g, maxp, P, log2P, W;
+  float scale_log2;          // softmax scale * log2(e)
+};
+
+template <int D>
+struct Frag {
+  u32x4 ka[D / 32];  // K rows of score MFMA 0 (tokens 8*(r/4) + r%4)
+  u32x4 kb[D / 32];  // K rows of score MFMA 1 (tokens 8*(r/4) + 4 + r%4)
+  u32x4 vt[D / 16];  // V^T rows d = 16b + r, tokens 8G .. 8G+7
+};
+
+// Load one full 32-token tile that starts at slot tok0 of the head.
+template <int D>
+__device__ inline void load_tile(Frag<D>& f, const DecodeArgs& a, const int32_t* pt, int tok0,
+                                 int r, int G) {
+  const int page = pt[tok0 >> a.log2P];
+  const int row0 = tok0 & (a.P - 1);
+  const char* pg = a.pool + static_cast<size_t>(page) * a.page_bytes;
+  const int ra = row0 + 8 * (r >> 2) + (r & 3);
+  const char* k0 = pg + (static_cast<size_t>(ra) * D + 8 * G) * 2;
+  const char* k1 = k0 + 4 * D * 2;
+#pragma unroll
+  for (int s = 0; s < D / 32; ++s) {
+    f.ka[s] = ldg16(k0 + s * 64);
+    f.kb[s] = ldg16(k1 + s * 64);
+  }
+  const char* v0 = pg + static_cast<size_t>(a.P) * D * 2 + (static_cast<size_t>(r) * a.P + row0 + 8 * G) * 2;
+#pragma unroll
+  for (int b = 0; b < D / 16; ++b) f.vt[b] = ldg16(v0 + static_cast<size_t>(b) * 16 * a.P * 2);
+}
+
+// Load the last, partial tile of a head: rows at or past L are not read, and
+// value elements of those tokens are zero.
+template <int D>
+__device__ inline void load_tail(Frag<D>& f, const DecodeArgs& a, const int32_t* pt, int tok0,
+                                 int L, int r, int G) {
+  const int page = pt[tok0 >> a.log2P];
+  const int row0 = tok0 & (a.P - 1);
+  const char* pg = a.pool + static_cast<size_t>(page) * a.page_bytes;
+  const int ta = 8 * (r >> 2) + (r & 3);
+  const int valid = L - tok0;  // 1 .. 31
+  const char* k0 = pg + (static_cast<size_t>(row0 + ta) * D + 8 * G) * 2;
+  const char* k1 = k0 + 4 * D * 2;
+  const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int s = 0; s < D / 32; ++s) {
+    f.ka[s] = ta < valid ? ldg16(k0 + s * 64) : z;
+    f.kb[s] = ta + 4 < valid ? ldg16(k1 + s * 64) : z;
+  }
+  const int nv = valid - 8 * G;  // tokens of this lane's 8 that exist
+  const char* v0 = pg + static_cast<size_t>(a.P) * D * 2 + (static_cast<size_t>(r) * a.P + row0 + 8 * G) * 2;
+#pragma unroll
+  for (int b = 0; b < D / 16; ++b) {
+    u32x4 x = nv > 0 ? ldg16(v0 + static_cast<size_t>(b) * 16 * a.P * 2) : z;
+    // zero the 16-bit elements of tokens >= L (element j holds token 8G + j)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (j >= nv) {
+        const unsigned int keep = (j & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+        x[j >> 1] &= keep;
+      }
+    }
+    f.vt[b] = x;
+  }
+}
+
+template <int D>
+struct Acc {
+  f32x4 o[D / 16];
+  float m, l;
+};
+
+// Scores, online softmax update and PV accumulation for one tile.
+// `valid` = number of live tokens in the tile (32 except in a head's tail).
+template <int D>
+__device__ inline void compute_tile(Acc<D>& acc, const Frag<D>& f, const u32x4* qf, float scale,
+                                    int valid, int G) {
+  f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < D / 32; ++s) {
+    s0 = mfma_bf16(f.ka[s], qf[s], s0);
+    s1 = mfma_bf16(f.kb[s], qf[s], s1);
+  }
+  float sc[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    sc[i] = s0[i] * scale;
+    sc[4 + i] = s1[i] * scale;
+  }
+  if (valid < kTile) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (8 * G + j >= valid) sc[j] = -INFINITY;
+  }
+  float mx = sc[0];
+#pragma unroll
+  for (int j = 1; j < 8; ++j) mx = fmaxf(mx, sc[j]);
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const float m_new = fmaxf(acc.m, mx);
+  const float alpha = __builtin_amdgcn_exp2f(acc.m - m_new);
+  bf16x8 p;
+  float psum = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const __bf16 pb = static_cast<__bf16>(__builtin_amdgcn_exp2f(sc[j] - m_new));
+    p[j] = pb;
+    psum += static_cast<float>(pb);
+  }
+  acc.l = acc.l * alpha + psum;
+  acc.m = m_new;
+  const u32x4 pu = __builtin_bit_cast(u32x4, p);
+#pragma unroll
+  for (int b = 0; b < D / 16; ++b) {
+    acc.o[b] *= alpha;
+    acc.o[b] = mfma_bf16(f.vt[b], pu, acc.o[b]);
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
+  if (load_status(a.status) != 0) return;
+  const int lane = threadIdx.x & 63;
+  const int wave = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+  const int r = lane & 15, G = lane >> 4;
+  const int total = a.cum_tiles[a.NH];
+  const int chunk = (total + a.W - 1) / a.W;
+  int tb = wave * chunk;
+  const int te = min(tb + chunk, total);
+  if (tb >= te) return;
+  // head containing tile tb: last hh with cum_tiles[hh] <= tb
+  int lo = 0, hi = a.NH;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (a.cum_tiles[mid] <= tb) lo = mid; else hi = mid;
+  }
+  int hh = lo;
+  while (tb < te) {
+    while (a.cum_tiles[hh + 1] <= tb) ++hh;
+    const int c0 = a.cum_tiles[hh], c1 = a.cum_tiles[hh + 1];
+    const int seg_end = min(te, c1);
+    const HeadDesc d = a.desc[hh];
+    const int L = d.x;
+    const int32_t* pt = a.page_table + static_cast<size_t>(d.y) * a.maxp;
+    // query fragments (B operand): column r = query head of the group
+    u32x4 qf[D / 32];
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    const char* qrow = reinterpret_cast<const char*>(a.q + (static_cast<size_t>(hh) * a.g + r) * D);
+#pragma unroll
+    for (int s = 0; s < D / 32; ++s) qf[s] = r < a.g ? ldg16(qrow + (32 * s + 8 * G) * 2) : z;
+    Acc<D> acc;
+#pragma unroll
+    for (int b = 0; b < D / 16; ++b) acc.o[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    acc.m = -INFINITY;
+    acc.l = 0.f;
+    // full tiles, software-pipelined one tile ahead; the head's partial tail last
+    const int t_lo = tb - c0;
+    const int t_hi = seg_end - c0;
+    const int full_hi = (seg_end == c1 && (L & (kTile - 1))) ? t_hi - 1 : t_hi;
+    if (t_lo < full_hi) {
+      Frag<D> fa, fb;
+      load_tile<D>(fa, a, pt, t_lo * kTile, r, G);
+      int t = t_lo;
+      while (true) {
+        if (t + 1 < full_hi) load_tile<D>(fb, a, pt, (t + 1) * kTile, r, G);
+        compute_tile<D>(acc, fa, qf, a.scale_log2, kTile, G);
+        if (++t >= full_hi) break;
+        if (t + 1 < full_hi) load_tile<D>(fa, a, pt, (t + 1) * kTile, r, G);
+        compute_tile<D>(acc, fb, qf, a.scale_log2, kTile, G);
+        if (++t >= full_hi) break;
+      }
+    }
+    if (full_hi < t_hi) {
+      Frag<D> ft;
+      const int tok0 = full_hi * kTile;
+      load_tail<D>(ft, a, pt, tok0, L, r, G);
+      compute_tile<D>(acc, ft, qf, a.scale_log2, L - tok0, G);
+    }
+    float l = acc.l;
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    if (tb == c0 && seg_end == c1) {
+      if (r < a.g) {
+        const float inv = 1.0f / l;
+        float* o = a.out + (static_cast<size_t>(hh) * a.g + r) * D + 4 * G;
+#pragma unroll
+        for (int b = 0; b < D / 16; ++b) *reinterpret_cast<f32x4*>(o + 16 * b) = acc.o[b] * inv;
+      }
+    } else {
+      const size_t pid = static_cast<size_t>(wave) + hh;
+      if (r < a.g) {
+        if (G == 0) a.part_ml[pid * kMaxGroup + r] = make_float2(acc.m, l);
+        float* o = a.part_acc + (pid * a.g + r) * D + 4 * G;
+#pragma unroll
+        for (int b = 0; b < D / 16; ++b) *reinterpret_cast<f32x4*>(o + 16 * b) = acc.o[b];
+      }
+    }
+    tb = seg_end;
+    ++hh;
+  }
+}
+
+// Merge the partials of heads that spanned several waves; zero the output
+// of heads with no retained token.
+struct CombineArgs {
+  const int32_t* status;
+  const int32_t* cum_tiles;
+  const float2* part_ml;
+  const float* part_acc;
+  float* out;
+  int NH, g, D, W;
+};
+
+__global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
+  if (load_status(a.status) != 0) return;
+  const int hh = blockIdx.x;
+  const int c0 = a.cum_tiles[hh], c1 = a.cum_tiles[hh + 1];
+  const int total = a.cum_tiles[a.NH];
+  const int gd = a.g * a.D;
+  float* out = a.out + static_cast<size_t>(hh) * gd;
+  if (c0 == c1) {
+    for (int e = threadIdx.x; e < gd; e += blockDim.x) out[e] = 0.f;
+    return;
+  }
+  const int chunk = (total + a.W - 1) / a.W;
+  const int w0 = c0 / chunk, w1 = (c1 - 1) / chunk;
+  if (w0 == w1) return;
+  for (int e = threadIdx.x; e < gd; e += blockDim.x) {
+    const int r = e / a.D, dd = e % a.D;
+    float M = -INFINITY;
+    for (int w = w0; w <= w1; ++w) M = fmaxf(M, a.part_ml[(static_cast<size_t>(w) + hh) * kMaxGroup + r].x);
+    float num = 0.f, den = 0.f;
+    for (int w = w0; w <= w1; ++w) {
+      const size_t pid = static_cast<size_t>(w) + hh;
+      const float2 ml = a.part_ml[pid * kMaxGroup + r];
+      const float sc = __builtin_amdgcn_exp2f(ml.x - M);
+      num += sc * a.part_acc[(pid * a.g + r) * a.D + dd];
+      den += sc * ml.y;
+    }
+    out[e] = num / den;
+  }
+}
+
+template <int D>
+hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
+                           int layer, int n, const void* q, float* out, int waves, hipStream_t st,
+                           hipEvent_t ev_start, hipEvent_t ev_stop) {
+  char* w = static_cast<char*>(ws);
+  DecodeArgs a;
+  a.status = reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status);
+  a.desc = reinterpret_cast<const HeadDesc*>(w + lo.ws_head_desc);
+  a.cum_tiles = reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles);
+  a.page_table = layer_state(lo, meta, layer).page_table;
+  a.pool = static_cast<const char*>(pool);
+  a.q = static_cast<const uint16_t*>(q);
+  a.part_ml = reinterpret_cast<float2*>(w + lo.ws_part_ml);
+  a.part_acc = reinterpret_cast<float*>(w + lo.ws_part_acc);
+  a.out = out;
+  a.page_bytes = lo.page_bytes;
+  a.NH = n * c.num_kv_heads;
+  a.g = c.group_size;
+  a.maxp = c.max_pages_per_head;
+  a.P = c.page_size;
+  a.log2P = __builtin_ctz(static_cast<unsigned>(c.page_size));
+  a.W = waves;
+  a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
+  if (ev_start) hipEventRecord(ev_start, st);
+  hipLaunchKernelGGL(decode_kernel<D>, dim3(waves / kWavesPerBlock), dim3(256), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (ev_stop) hipEventRecord(ev_stop, st);
+  if (e != hipSuccess) return e;
+  CombineArgs b;
+  b.status = a.status;
+  b.cum_tiles = a.cum_tiles;
+  b.part_ml = a.part_ml;
+  b.part_acc = a.part_acc;
+  b.out = out;
+  b.NH = a.NH;
+  b.g = a.g;
+  b.D = D;
+  b.W = waves;
+  hipLaunchKernelGGL(combine_kernel, dim3(a.NH), dim3(256), 0, st, b);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
+                         int layer, int n, const void* q, float* out, int waves, hipStream_t st,
+                         hipEvent_t ev_start, hipEvent_t ev_stop) {
+  if (c.head_dim == 128)
+    return launch_decode_d<128>(c, lo, meta, ws, pool, layer, n, q, out, waves, st, ev_start, ev_stop);
+  return launch_decode_d<64>(c, lo, meta, ws, pool, layer, n, q, out, waves, st, ev_start, ev_stop);
+}
+
+int decode_resident_waves(const dms_config& c) {
+  int dev = 0, cus = 0, blocks = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return -1;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
+  hipError_t e = c.head_dim == 128
+      ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_kernel<128>, 256, 0)
+      : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_kernel<64>, 256, 0);
+  if (e != hipSuccess || blocks < 1) return -1;
+  int waves = cus * blocks * kWavesPerBlock;
+  if (waves > kMaxWaves) waves = kMaxWaves / kWavesPerBlock * kWavesPerBlock;
+  return waves;
+}
+
+}  // namespace dms

@@ -1,0 +1,313 @@
+"""Python binding of libdms (include/dms.h).
+
+The functions named ``dms_*`` mirror the C entry points one to one and only
+marshal arguments: device pointers may be given as integers or as tensors
+(their ``data_ptr()``), streams as integers, ``torch.cuda.Stream`` objects or
+None (the current stream).  :class:`DmsCache` is plumbing on top: it lets
+PyTorch allocate the caller-owned buffers the library works in.
+
+There is no fallback: if ``libdms.so`` is missing the first call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdms.so")
+
+DMS_OK = 0
+DMS_ERR_INVALID = -1
+DMS_ERR_UNSUPPORTED = -2
+DMS_ERR_HIP = -3
+DMS_ERR_OUT_OF_PAGES = -4
+DMS_ERR_CAPACITY = -5
+DMS_ERR_BAD_SEQ = -6
+
+
+class DmsConfig(ctypes.Structure):
+    _fields_ = [
+        ("num_layers", ctypes.c_int32),
+        ("max_seqs", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("group_size", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("window", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
+        ("num_pages", ctypes.c_int32),
+        ("max_pages_per_head", ctypes.c_int32),
+        ("max_chunk_tokens", ctypes.c_int32),
+        ("softmax_scale", ctypes.c_float),
+    ]
+
+
+class DmsStateOffsets(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_size_t) for n in
+                ("status", "layer0", "layer_stride", "pos", "len", "ring", "page_table",
+                 "slot_meta", "stack", "top")]
+
+
+class DmsError(RuntimeError):
+    def __init__(self, code: int, where: str = ""):
+        self.code = code
+        super().__init__(f"{where}: {dms_strerror(code)} ({code})")
+
+
+_lib = None
+_VP = ctypes.c_void_p
+_I = ctypes.c_int
+_SZ = ctypes.c_size_t
+
+_SIGS = {
+    "dms_layout": (_I, [ctypes.POINTER(DmsConfig), ctypes.POINTER(_SZ), ctypes.POINTER(_SZ),
+                        ctypes.POINTER(_SZ), ctypes.POINTER(_SZ)]),
+    "dms_state_layout": (_I, [ctypes.POINTER(DmsConfig), ctypes.POINTER(DmsStateOffsets)]),
+    "dms_create": (_I, [ctypes.POINTER(DmsConfig), _VP, ctypes.POINTER(_VP), _VP,
+                        ctypes.POINTER(_VP)]),
+    "dms_destroy": (_I, [_VP]),
+    "dms_init_state": (_I, [_VP, _VP]),
+    "dms_seq_reset": (_I, [_VP, _I, _I, _VP, _VP]),
+    "dms_append": (_I, [_VP, _I, _I, _VP, _VP, _VP, _VP, _VP]),
+    "dms_decode": (_I, [_VP, _I, _I, _VP, _VP, _VP, _VP]),
+    "dms_decode_step": (_I, [_VP, _I, _I, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
+    "dms_append_chunk": (_I, [_VP, _I, _I, _VP, _VP, _I, _I, _VP, _VP, _VP, _VP]),
+    "dms_prefill_chunk": (_I, [_VP, _I, _I, _VP, _VP, _I, _I, _VP, _VP, _VP, _VP, _VP, _VP]),
+    "dms_retained_lengths": (_I, [_VP, _I, _I, _VP, _VP, _VP]),
+    "dms_export_state": (_I, [_VP, _I, _VP, _SZ, _VP]),
+    "dms_status": (_I, [_VP, _VP]),
+    "dms_clear_status": (_I, [_VP, _VP]),
+    "dms_profile_start": (_I, [_VP, _I]),
+    "dms_profile_stop": (_I, [_VP, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(_I)]),
+    "dms_strerror": (ctypes.c_char_p, [_I]),
+}
+
+
+def lib():
+    """Load libdms.so (built in-tree); raises if it is missing."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+        h = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(h, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = h
+    return _lib
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    raise TypeError(f"cannot pass {type(x)} as a pointer")
+
+
+def _stream(s):
+    if s is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def _check(rc, where):
+    if rc != DMS_OK:
+        raise DmsError(rc, where)
+
+
+def make_config(num_layers, max_seqs, num_kv_heads, group_size, head_dim, window,
+                page_size, num_pages, max_pages_per_head, max_chunk_tokens=0,
+                softmax_scale=0.0) -> DmsConfig:
+    return DmsConfig(num_layers, max_seqs, num_kv_heads, group_size, head_dim, window,
+                     page_size, num_pages, max_pages_per_head, max_chunk_tokens,
+                     softmax_scale)
+
+
+# ---------------------------------------------------------------------------
+# Entry points (same names as the C ABI)
+# ---------------------------------------------------------------------------
+
+def dms_layout(cfg: DmsConfig):
+    a, b, c, d = _SZ(), _SZ(), _SZ(), _SZ()
+    _check(lib().dms_layout(ctypes.byref(cfg), ctypes.byref(a), ctypes.byref(b),
+                            ctypes.byref(c), ctypes.byref(d)), "dms_layout")
+    return a.value, b.value, c.value, d.value
+
+
+def dms_state_layout(cfg: DmsConfig) -> DmsStateOffsets:
+    o = DmsStateOffsets()
+    _check(lib().dms_state_layout(ctypes.byref(cfg), ctypes.byref(o)), "dms_state_layout")
+    return o
+
+
+def dms_create(cfg: DmsConfig, meta, pools, workspace):
+    arr = (_VP * cfg.num_layers)(*[_ptr(p) for p in pools])
+    out = _VP()
+    _check(lib().dms_create(ctypes.byref(cfg), _ptr(meta), arr, _ptr(workspace),
+                            ctypes.byref(out)), "dms_create")
+    return out.value
+
+
+def dms_destroy(ctx):
+    _check(lib().dms_destroy(ctx), "dms_destroy")
+
+
+def dms_init_state(ctx, stream=None):
+    _check(lib().dms_init_state(ctx, _stream(stream)), "dms_init_state")
+
+
+def dms_seq_reset(ctx, layer, n, seq_ids, stream=None):
+    _check(lib().dms_seq_reset(ctx, layer, n, _ptr(seq_ids), _stream(stream)), "dms_seq_reset")
+
+
+def dms_append(ctx, layer, n, seq_ids, k, v, flags, stream=None):
+    _check(lib().dms_append(ctx, layer, n, _ptr(seq_ids), _ptr(k), _ptr(v), _ptr(flags),
+                            _stream(stream)), "dms_append")
+
+
+def dms_decode(ctx, layer, n, seq_ids, q, out, stream=None):
+    _check(lib().dms_decode(ctx, layer, n, _ptr(seq_ids), _ptr(q), _ptr(out), _stream(stream)),
+           "dms_decode")
+
+
+def dms_decode_step(ctx, layer, n, seq_ids, q, k, v, flags, out, stream=None):
+    _check(lib().dms_decode_step(ctx, layer, n, _ptr(seq_ids), _ptr(q), _ptr(k), _ptr(v),
+                                 _ptr(flags), _ptr(out), _stream(stream)), "dms_decode_step")
+
+
+def dms_append_chunk(ctx, layer, n, seq_ids, cu_seqlens, total_tokens, max_seqlen, k, v, flags,
+                     stream=None):
+    _check(lib().dms_append_chunk(ctx, layer, n, _ptr(seq_ids), _ptr(cu_seqlens), total_tokens,
+                                  max_seqlen, _ptr(k), _ptr(v), _ptr(flags), _stream(stream)),
+           "dms_append_chunk")
+
+
+def dms_prefill_chunk(ctx, layer, n, seq_ids, cu_seqlens, total_tokens, max_seqlen, q, k, v,
+                      flags, out, stream=None):
+    _check(lib().dms_prefill_chunk(ctx, layer, n, _ptr(seq_ids), _ptr(cu_seqlens), total_tokens,
+                                   max_seqlen, _ptr(q), _ptr(k), _ptr(v), _ptr(flags), _ptr(out),
+                                   _stream(stream)), "dms_prefill_chunk")
+
+
+def dms_retained_lengths(ctx, layer, n, seq_ids, out, stream=None):
+    _check(lib().dms_retained_lengths(ctx, layer, n, _ptr(seq_ids), _ptr(out), _stream(stream)),
+           "dms_retained_lengths")
+
+
+def dms_export_state(ctx, layer, nbytes, stream=None) -> np.ndarray:
+    buf = np.empty(nbytes, dtype=np.uint8)
+    _check(lib().dms_export_state(ctx, layer, buf.ctypes.data, nbytes, _stream(stream)),
+           "dms_export_state")
+    return buf
+
+
+def dms_status(ctx, stream=None) -> int:
+    return lib().dms_status(ctx, _stream(stream))
+
+
+def dms_clear_status(ctx, stream=None):
+    _check(lib().dms_clear_status(ctx, _stream(stream)), "dms_clear_status")
+
+
+def dms_profile_start(ctx, max_launches):
+    _check(lib().dms_profile_start(ctx, max_launches), "dms_profile_start")
+
+
+def dms_profile_stop(ctx):
+    """Returns (total decode-kernel milliseconds, launches recorded)."""
+    ms, n = ctypes.c_float(), _I()
+    _check(lib().dms_profile_stop(ctx, ctypes.byref(ms), ctypes.byref(n)), "dms_profile_stop")
+    return ms.value, n.value
+
+
+def dms_strerror(code: int) -> str:
+    return lib().dms_strerror(code).decode()
+
+
+# ---------------------------------------------------------------------------
+# PyTorch-owned buffers
+# ---------------------------------------------------------------------------
+
+@dataclass
+class LayerStateView:
+    """One layer's exported state as NumPy arrays (see dms_state_offsets)."""
+    pos: np.ndarray
+    L: np.ndarray
+    ring_slot: np.ndarray
+    ring_flag: np.ndarray
+    page_table: np.ndarray
+    slot_pos: np.ndarray
+    slot_flag: np.ndarray
+    stack: np.ndarray
+    top: int
+
+
+class DmsCache:
+    """Device buffers for one context, allocated by PyTorch on ``device``."""
+
+    def __init__(self, cfg: DmsConfig, device="cuda", pool_pages=None):
+        import torch
+        self.cfg = cfg
+        self.meta_bytes, self.pool_bytes, self.ws_bytes, self.page_bytes = dms_layout(cfg)
+        self.offsets = dms_state_layout(cfg)
+        self.meta = torch.empty(self.meta_bytes, dtype=torch.uint8, device=device)
+        self.pools = [torch.empty(self.pool_bytes, dtype=torch.uint8, device=device)
+                      for _ in range(cfg.num_layers)]
+        self.workspace = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=device)
+        self.ctx = dms_create(cfg, self.meta, self.pools, self.workspace)
+        dms_init_state(self.ctx)
+
+    def close(self):
+        if self.ctx:
+            dms_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def export(self, layer) -> LayerStateView:
+        c, o = self.cfg, self.offsets
+        raw = dms_export_state(self.ctx, layer, o.layer_stride)
+        S, H, w = c.max_seqs, c.num_kv_heads, c.window
+        maxp, P = c.max_pages_per_head, c.page_size
+
+        def arr(off, count):
+            return raw[off: off + 4 * count].view(np.int32)
+
+        ring = arr(o.ring, S * H * w).reshape(S, H, w).view(np.uint32)
+        meta = arr(o.slot_meta, S * H * maxp * P).reshape(S, H, maxp * P).view(np.uint32)
+        top = int(arr(o.top, 1)[0])
+        return LayerStateView(
+            pos=arr(o.pos, S).copy(),
+            L=arr(o.len, S * H).reshape(S, H).copy(),
+            ring_slot=(ring & 0x7FFFFFFF).astype(np.int64),
+            ring_flag=(ring >> 31).astype(np.uint8),
+            page_table=arr(o.page_table, S * H * maxp).reshape(S, H, maxp).astype(np.int64),
+            slot_pos=(meta & 0x7FFFFFFF).astype(np.int64),
+            slot_flag=(meta >> 31).astype(np.uint8),
+            stack=arr(o.stack, c.num_pages)[:top].astype(np.int64),
+            top=top,
+        )
+
+    def pool_page_kv(self, layer, page):
+        """(K [P, d], V [P, d]) bf16 bit patterns (uint16) of one page, on the host."""
+        import torch
+        c = self.cfg
+        P, D = c.page_size, c.head_dim
+        raw = self.pools[layer][page * self.page_bytes:(page + 1) * self.page_bytes]
+        u16 = raw.view(torch.int16).cpu().numpy().view(np.uint16)
+        k = u16[: P * D].reshape(P, D)
+        vt = u16[P * D:].reshape(D, P)
+        return k, vt.T.copy()

@@ -1,0 +1,112 @@
+"""C ABI checks that need no GPU: the library loads, exports every function
+declared in include/dms.h, and rejects bad configurations and arguments on
+the host before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2506_05345_amd import dms
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "dms.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dms_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    lib = ctypes.CDLL(dms.LIB_PATH)
+    names = _declared()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(lib, n), n
+    # and the binding wraps each of them under the same name
+    for n in names:
+        assert hasattr(dms, n), n
+
+
+def _cfg(**kw):
+    base = dict(num_layers=2, max_seqs=4, num_kv_heads=2, group_size=2, head_dim=64, window=16,
+                page_size=64, num_pages=32, max_pages_per_head=16, max_chunk_tokens=256)
+    base.update(kw)
+    return dms.make_config(**base)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(window=0), dms.DMS_ERR_INVALID),
+    (dict(window=-3), dms.DMS_ERR_INVALID),
+    (dict(head_dim=96), dms.DMS_ERR_UNSUPPORTED),
+    (dict(head_dim=0), dms.DMS_ERR_INVALID),
+    (dict(group_size=17), dms.DMS_ERR_UNSUPPORTED),
+    (dict(group_size=0), dms.DMS_ERR_INVALID),
+    (dict(page_size=48), dms.DMS_ERR_INVALID),
+    (dict(page_size=16), dms.DMS_ERR_INVALID),
+    (dict(num_layers=0), dms.DMS_ERR_INVALID),
+    (dict(max_seqs=70000), dms.DMS_ERR_INVALID),
+    (dict(num_pages=0), dms.DMS_ERR_INVALID),
+    (dict(max_chunk_tokens=-1), dms.DMS_ERR_INVALID),
+    (dict(softmax_scale=float("nan")), dms.DMS_ERR_INVALID),
+    (dict(softmax_scale=float("inf")), dms.DMS_ERR_INVALID),
+])
+def test_bad_configuration(kw, code):
+    rc = dms.lib().dms_layout(ctypes.byref(_cfg(**kw)), None, None, None, None)
+    assert rc == code
+
+
+def test_layout_sizes():
+    m, p, w, pg = dms.dms_layout(_cfg())
+    assert pg == 2 * 64 * 64 * 2 and p == 32 * pg
+    o = dms.dms_state_layout(_cfg())
+    assert m == o.layer0 + 2 * o.layer_stride
+    # arrays are disjoint and ordered inside a layer's region
+    offs = [o.pos, o.len, o.ring, o.page_table, o.slot_meta, o.stack, o.top]
+    assert offs == sorted(offs) and o.top < o.layer_stride
+
+
+def test_host_side_argument_errors_change_nothing():
+    # fake device pointers: every call below must fail validation before any
+    # HIP call, so nothing is dereferenced
+    cfg = _cfg()
+    L = dms.lib()
+    assert L.dms_create(ctypes.byref(cfg), None, (ctypes.c_void_p * 2)(1, 2), 3,
+                        ctypes.byref(ctypes.c_void_p())) == dms.DMS_ERR_INVALID
+    assert L.dms_create(ctypes.byref(cfg), 1, (ctypes.c_void_p * 2)(1, None), 3,
+                        ctypes.byref(ctypes.c_void_p())) == dms.DMS_ERR_INVALID
+    ctx = dms.dms_create(cfg, 0x1000, [0x2000, 0x3000], 0x4000)
+    try:
+        P = 0x100
+        assert L.dms_append(ctx, 2, 1, P, P, P, P, None) == dms.DMS_ERR_INVALID      # layer
+        assert L.dms_append(ctx, -1, 1, P, P, P, P, None) == dms.DMS_ERR_INVALID
+        assert L.dms_append(ctx, 0, 0, P, P, P, P, None) == dms.DMS_ERR_INVALID      # n
+        assert L.dms_append(ctx, 0, 5, P, P, P, P, None) == dms.DMS_ERR_INVALID      # n > max_seqs
+        assert L.dms_append(ctx, 0, 1, None, P, P, P, None) == dms.DMS_ERR_INVALID   # seq ids
+        assert L.dms_append(ctx, 0, 1, P, None, P, P, None) == dms.DMS_ERR_INVALID
+        assert L.dms_decode(ctx, 0, 1, P, P, None, None) == dms.DMS_ERR_INVALID      # out
+        assert L.dms_decode_step(ctx, 0, 1, P, P, P, P, None, P, None) == dms.DMS_ERR_INVALID
+        # chunk sizes: total over max_chunk_tokens, max_seqlen > total, missing cu
+        assert L.dms_append_chunk(ctx, 0, 1, P, P, 257, 257, P, P, P, None) == dms.DMS_ERR_INVALID
+        assert L.dms_append_chunk(ctx, 0, 1, P, P, 10, 11, P, P, P, None) == dms.DMS_ERR_INVALID
+        assert L.dms_append_chunk(ctx, 0, 1, P, None, 10, 10, P, P, P, None) == dms.DMS_ERR_INVALID
+        assert L.dms_append_chunk(ctx, 0, 1, P, P, -1, 0, P, P, P, None) == dms.DMS_ERR_INVALID
+        assert L.dms_append_chunk(ctx, 0, 1, P, P, 0, 0, P, P, P, None) == dms.DMS_OK  # empty: no-op
+        assert L.dms_prefill_chunk(ctx, 0, 1, P, P, 10, 10, None, P, P, P, P, None) == dms.DMS_ERR_INVALID
+        assert L.dms_seq_reset(ctx, 2, 1, P, None) == dms.DMS_ERR_INVALID
+        assert L.dms_seq_reset(ctx, -2, 1, P, None) == dms.DMS_ERR_INVALID
+        assert L.dms_retained_lengths(ctx, 0, 1, P, None, None) == dms.DMS_ERR_INVALID
+        assert L.dms_export_state(ctx, 0, P, 4, None) == dms.DMS_ERR_INVALID          # too small
+        assert L.dms_profile_start(ctx, 0) == dms.DMS_ERR_INVALID
+        assert L.dms_profile_stop(ctx, None, None) == dms.DMS_ERR_INVALID            # no session
+        assert L.dms_status(None, None) == dms.DMS_ERR_INVALID
+    finally:
+        dms.dms_destroy(ctx)
+    assert L.dms_destroy(None) == dms.DMS_ERR_INVALID
+
+
+def test_error_strings():
+    for code in (0, -1, -2, -3, -4, -5, -6):
+        assert dms.dms_strerror(code) and dms.dms_strerror(code) != "unknown error code"
+    assert dms.dms_strerror(-99) == "unknown error code"
