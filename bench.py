@@ -230,6 +230,8 @@ def main():
     ap.add_argument("--workload", default="qwen-r1-32b-8x", choices=sorted(WORKLOADS))
     ap.add_argument("--chunk", type=int, default=4096)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run a 1 GiB device copy first (reference kernel for HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; the DMS decode path "
@@ -242,6 +244,13 @@ def main():
     wl = WORKLOADS[args.workload]
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        # plain copy of known size: reads 1 GiB, writes 1 GiB
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     S = args.steps + args.warmup
     cache, ctx, L0 = build(wl, S, args.chunk, dev)
     q, k, v, flags, fresh = step_inputs(wl, ctx, S, dev)

@@ -118,10 +118,13 @@ typedef struct dms_state_offsets {
 } dms_state_offsets;
 
 /*
- * Page layout in a layer's pool (`page_bytes` each, page i at i*page_bytes):
- *   K   bf16 [P][d]   token-major rows (slot % P selects the row)
- *   V^T bf16 [d][P]   value rows transposed: element (e, s) is V[s][e]
- * A slot s of a head lives in page page_table[s / P] at row s % P.
+ * Page layout in a layer's pool (`page_bytes` = 4 * P * d bytes, page i at
+ * i * page_bytes).  A slot s of a head lives in page page_table[s / P], tile
+ * (s % P) / 32, row j = s % 32.  A page is P/32 tiles of 128 * d bytes each:
+ *   keys   bf16 [d/32][32 rows][32 dims]: element (j, e) at byte
+ *          (e / 32) * 2048 + j * 64 + (e % 32) * 2 of the tile
+ *   values bf16 [d][32 rows] (transposed): element (j, e) at byte
+ *          64 * d + e * 64 + j * 2 of the tile
  */
 
 /* Sizes of the caller-owned buffers for `cfg`.  Host only; validates cfg.

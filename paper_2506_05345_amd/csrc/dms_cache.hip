@@ -267,13 +267,14 @@ __global__ __launch_bounds__(64) void scatter_kernel(ScatterArgs a) {
   const int slot = d.z;
   const int page = a.page_table[static_cast<size_t>(d.y) * a.maxp + slot / a.P];
   const int row = slot % a.P;
-  char* pg = a.pool + static_cast<size_t>(page) * a.page_bytes;
+  char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * tile_bytes(a.D);
+  const int j = row & 31;
   const int lane = threadIdx.x;
   if (lane < a.D / 8)
-    reinterpret_cast<uint4*>(pg + static_cast<size_t>(row) * a.D * 2)[lane] =
+    *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * lane)) =
         reinterpret_cast<const uint4*>(a.k + static_cast<size_t>(hh) * a.D)[lane];
-  uint16_t* vt = reinterpret_cast<uint16_t*>(pg + static_cast<size_t>(a.P) * a.D * 2);
-  for (int e = lane; e < a.D; e += 64) vt[e * a.P + row] = a.v[static_cast<size_t>(hh) * a.D + e];
+  for (int e = lane; e < a.D; e += 64)
+    *reinterpret_cast<uint16_t*>(tile + v_elem_off(j, e, a.D)) = a.v[static_cast<size_t>(hh) * a.D + e];
 }
 
 struct RetainedArgs {
@@ -454,7 +455,6 @@ __global__ __launch_bounds__(256) void chunk_commit_kernel(ChunkArgs a) {
   }
   __syncthreads();  // ring reads above complete before the ring is rewritten
   const int ring_from = C > a.w ? C - a.w : 0;
-  char* pool = a.pool;
   for (int c = threadIdx.x; c < C; c += blockDim.x) {
     const int fl = chunk_flag(a, tok0, c, h);
     const uint32_t fb = fl ? kFlagBit : 0u;
@@ -476,13 +476,15 @@ __global__ __launch_bounds__(256) void chunk_commit_kernel(ChunkArgs a) {
     if (!((c + a.w >= C) || !chunk_flag(a, tok0, c, h))) continue;
     const int slot = a.slots[static_cast<size_t>(tok0 + c) * a.H + h];
     const int page = a.st.page_table[pt_base + slot / a.P];
-    char* pg = pool + static_cast<size_t>(page) * a.page_bytes;
+    const int row = slot % a.P;
+    char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * tile_bytes(a.D);
+    const int j = row & 31;
     const size_t src = (static_cast<size_t>(tok0 + c) * a.H + h) * a.D;
-    reinterpret_cast<uint4*>(pg + static_cast<size_t>(slot % a.P) * a.D * 2)[part] =
+    *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * part)) =
         reinterpret_cast<const uint4*>(a.k + src)[part];
-    uint16_t* vt = reinterpret_cast<uint16_t*>(pg + static_cast<size_t>(a.P) * a.D * 2);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) vt[(part * 8 + e) * a.P + slot % a.P] = a.v[src + part * 8 + e];
+    for (int e = 0; e < 8; ++e)
+      *reinterpret_cast<uint16_t*>(tile + v_elem_off(j, part * 8 + e, a.D)) = a.v[src + part * 8 + e];
   }
 }
 

@@ -63,6 +63,20 @@ inline LayerState layer_state(const Layout& lo, void* meta, int layer) {
   return s;
 }
 
+// Pool page layout.  A page holds P/32 tiles of 32 consecutive slots; each
+// tile is 128*D bytes, keys first, then values:
+//   K part [D/32][32 slots][32 dims] bf16  -- element (j, e) at (e/32)*2048 + j*64 + (e%32)*2
+//   V part [D][32 slots] bf16 (transposed) -- element (j, e) at 64*D + e*64 + j*2
+// so the 32 tokens a decode tile reads are one contiguous 16 KB block (D = 128)
+// and every 16-byte lane load of the decode kernel covers whole cache lines.
+__host__ __device__ inline size_t tile_bytes(int D) { return static_cast<size_t>(D) * 128; }
+__host__ __device__ inline size_t k_elem_off(int j, int e) {
+  return static_cast<size_t>(e >> 5) * 2048 + j * 64 + (e & 31) * 2;
+}
+__host__ __device__ inline size_t v_elem_off(int j, int e, int D) {
+  return static_cast<size_t>(D) * 64 + e * 64 + j * 2;
+}
+
 // Per-head descriptor written by the planning kernels, one per (seq in call,
 // KV head) in call order: x = retained length L, y = state head index
 // (seq * Hkv + head), z = slot written by this call's token (decode), w = 0.

@@ -14,11 +14,13 @@
 //    unbalance the chip.  A wave that covers a whole head writes the final
 //    output; otherwise it writes a partial (running max, sum, accumulator)
 //    merged by the combine kernel with log-sum-exp weights.
-//  * Per tile, each lane issues 16-byte loads straight into MFMA operand
-//    registers: K rows [P][d] of the page as the A operand of S^T = K Q^T and
-//    the transposed value block V^T [d][P] of the page as the A operand of
-//    O^T = V^T P^T.  No LDS round trip is needed.  The group's g query heads
-//    fill g of the 16 MFMA columns.
+//  * Pages are stored tile-major: the 32 tokens of a tile are one contiguous
+//    block (keys as D/32 sub-blocks of 32 x 32 dims, then values transposed,
+//    D rows of 32 tokens).  Per tile each lane issues 16-byte loads straight
+//    into MFMA operand registers -- keys as the A operand of S^T = K Q^T,
+//    transposed values as the A operand of O^T = V^T P^T -- and every load
+//    instruction covers whole 128-byte lines.  No LDS round trip is needed.
+//    The group's g query heads fill g of the 16 MFMA columns.
 //  * The 16x16 accumulator layout puts rows 4*(lane/16) .. +3 of column
 //    lane%16 in each lane.  Tile rows of the first / second score MFMA are
 //    assigned tokens 8*(r/4) + r%4 and 8*(r/4) + 4 + r%4, so after both MFMAs
@@ -49,20 +51,16 @@ __device__ inline f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
 
 __device__ inline u32x4 ldg16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
 
-struct DecodeArgs {
-  const int32_t* status;
-  const HeadDesc* desc;      // [NH]
-  const int32_t* cum_tiles;  // [NH + 1]
-  const int32_t* page_table; // layer page table base
-  const char* pool;          // layer pool base
-  const uint16_t* q;         // [NH * g, D]
-  float2* part_ml;           // [partials][16]  (max in log2 units, sum)
-  float* part_acc;           // [partials][g][D]
-  float* out;                // [NH * g, D]
+struct DecodeParams {
   size_t page_bytes;
   int NH, g, maxp, P, log2P, W;
-  float scale_log2;          // softmax scale * log2(e)
+  float scale_log2;  // softmax scale * log2(e)
 };
+
+// Scores are exponentiated against a per-lane reference max that is only
+// raised when a tile's max exceeds it by more than this (log2 units), so the
+// accumulator is rescaled rarely; probabilities stay below 2^kRescale.
+constexpr float kRescale = 8.0f;
 
 template <int D>
 struct Frag {
@@ -71,53 +69,43 @@ struct Frag {
   u32x4 vt[D / 16];  // V^T rows d = 16b + r, tokens 8G .. 8G+7
 };
 
-// Load one full 32-token tile that starts at slot tok0 of the head.
+// Per-lane byte offsets inside a 32-token tile (constant for the whole
+// kernel); see the page layout in dms_common.h.
+struct LaneOff {
+  uint32_t k;  // K row 8*(r/4) + r%4 of sub-block 0, elements 8G .. 8G+7
+  uint32_t v;  // V^T row r, tokens 8G .. 8G+7
+};
+
+// Load one full 32-token tile starting at `tile` (wave-uniform address).
 template <int D>
-__device__ inline void load_tile(Frag<D>& f, const DecodeArgs& a, const int32_t* pt, int tok0,
-                                 int r, int G) {
-  const int page = pt[tok0 >> a.log2P];
-  const int row0 = tok0 & (a.P - 1);
-  const char* pg = a.pool + static_cast<size_t>(page) * a.page_bytes;
-  const int ra = row0 + 8 * (r >> 2) + (r & 3);
-  const char* k0 = pg + (static_cast<size_t>(ra) * D + 8 * G) * 2;
-  const char* k1 = k0 + 4 * D * 2;
+__device__ inline void load_tile(Frag<D>& f, const char* tile, LaneOff lo) {
 #pragma unroll
   for (int s = 0; s < D / 32; ++s) {
-    f.ka[s] = ldg16(k0 + s * 64);
-    f.kb[s] = ldg16(k1 + s * 64);
+    f.ka[s] = ldg16(tile + lo.k + s * 2048);
+    f.kb[s] = ldg16(tile + lo.k + 256 + s * 2048);
   }
-  const char* v0 = pg + static_cast<size_t>(a.P) * D * 2 + (static_cast<size_t>(r) * a.P + row0 + 8 * G) * 2;
 #pragma unroll
-  for (int b = 0; b < D / 16; ++b) f.vt[b] = ldg16(v0 + static_cast<size_t>(b) * 16 * a.P * 2);
+  for (int b = 0; b < D / 16; ++b) f.vt[b] = ldg16(tile + lo.v + b * 1024);
 }
 
-// Load the last, partial tile of a head: rows at or past L are not read, and
-// value elements of those tokens are zero.
+// Last, partial tile of a head: rows at or past L are not read and the value
+// elements of those tokens are zero.
 template <int D>
-__device__ inline void load_tail(Frag<D>& f, const DecodeArgs& a, const int32_t* pt, int tok0,
-                                 int L, int r, int G) {
-  const int page = pt[tok0 >> a.log2P];
-  const int row0 = tok0 & (a.P - 1);
-  const char* pg = a.pool + static_cast<size_t>(page) * a.page_bytes;
+__device__ inline void load_tail(Frag<D>& f, const char* tile, LaneOff lo, int valid, int r, int G) {
   const int ta = 8 * (r >> 2) + (r & 3);
-  const int valid = L - tok0;  // 1 .. 31
-  const char* k0 = pg + (static_cast<size_t>(row0 + ta) * D + 8 * G) * 2;
-  const char* k1 = k0 + 4 * D * 2;
   const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
   for (int s = 0; s < D / 32; ++s) {
-    f.ka[s] = ta < valid ? ldg16(k0 + s * 64) : z;
-    f.kb[s] = ta + 4 < valid ? ldg16(k1 + s * 64) : z;
+    f.ka[s] = ta < valid ? ldg16(tile + lo.k + s * 2048) : z;
+    f.kb[s] = ta + 4 < valid ? ldg16(tile + lo.k + 256 + s * 2048) : z;
   }
   const int nv = valid - 8 * G;  // tokens of this lane's 8 that exist
-  const char* v0 = pg + static_cast<size_t>(a.P) * D * 2 + (static_cast<size_t>(r) * a.P + row0 + 8 * G) * 2;
 #pragma unroll
   for (int b = 0; b < D / 16; ++b) {
-    u32x4 x = nv > 0 ? ldg16(v0 + static_cast<size_t>(b) * 16 * a.P * 2) : z;
-    // zero the 16-bit elements of tokens >= L (element j holds token 8G + j)
+    u32x4 x = nv > 0 ? ldg16(tile + lo.v + b * 1024) : z;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      if (j >= nv) {
+      if (j >= nv) {  // element j holds token 8G + j
         const unsigned int keep = (j & 1) ? 0x0000FFFFu : 0xFFFF0000u;
         x[j >> 1] &= keep;
       }
@@ -129,11 +117,10 @@ __device__ inline void load_tail(Frag<D>& f, const DecodeArgs& a, const int32_t*
 template <int D>
 struct Acc {
   f32x4 o[D / 16];
-  float m, l;
+  float m, l;  // reference max (log2 units) and this lane's partial sum
 };
 
-// Scores, online softmax update and PV accumulation for one tile.
-// `valid` = number of live tokens in the tile (32 except in a head's tail).
+// Scores, online softmax and PV accumulation for one tile; `valid` live tokens.
 template <int D>
 __device__ inline void compute_tile(Acc<D>& acc, const Frag<D>& f, const u32x4* qf, float scale,
                                     int valid, int G) {
@@ -154,60 +141,72 @@ __device__ inline void compute_tile(Acc<D>& acc, const Frag<D>& f, const u32x4* 
     for (int j = 0; j < 8; ++j)
       if (8 * G + j >= valid) sc[j] = -INFINITY;
   }
-  float mx = sc[0];
-#pragma unroll
-  for (int j = 1; j < 8; ++j) mx = fmaxf(mx, sc[j]);
+  float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
+                   fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
   mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-  const float m_new = fmaxf(acc.m, mx);
-  const float alpha = __builtin_amdgcn_exp2f(acc.m - m_new);
+  const bool raise = mx > acc.m + kRescale;
+  if (__builtin_amdgcn_ballot_w64(raise)) {
+    const float m_new = raise ? mx : acc.m;
+    const float alpha = __builtin_amdgcn_exp2f(acc.m - m_new);
+    acc.l *= alpha;
+#pragma unroll
+    for (int b = 0; b < D / 16; ++b) acc.o[b] *= alpha;
+    acc.m = m_new;
+  }
   bf16x8 p;
   float psum = 0.f;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    const __bf16 pb = static_cast<__bf16>(__builtin_amdgcn_exp2f(sc[j] - m_new));
+    const __bf16 pb = static_cast<__bf16>(__builtin_amdgcn_exp2f(sc[j] - acc.m));
     p[j] = pb;
     psum += static_cast<float>(pb);
   }
-  acc.l = acc.l * alpha + psum;
-  acc.m = m_new;
+  acc.l += psum;
   const u32x4 pu = __builtin_bit_cast(u32x4, p);
 #pragma unroll
-  for (int b = 0; b < D / 16; ++b) {
-    acc.o[b] *= alpha;
-    acc.o[b] = mfma_bf16(f.vt[b], pu, acc.o[b]);
-  }
+  for (int b = 0; b < D / 16; ++b) acc.o[b] = mfma_bf16(f.vt[b], pu, acc.o[b]);
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
-  if (load_status(a.status) != 0) return;
+__global__ __launch_bounds__(256, 2) void decode_kernel(
+    const int32_t* __restrict__ status, const HeadDesc* __restrict__ desc,
+    const int32_t* __restrict__ cum_tiles, const int32_t* __restrict__ page_table,
+    const char* __restrict__ pool, const uint16_t* __restrict__ q, float2* __restrict__ part_ml,
+    float* __restrict__ part_acc, float* __restrict__ out, DecodeParams a) {
+  if (load_status(status) != 0) return;
   const int lane = threadIdx.x & 63;
-  const int wave = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+  // wave index is uniform across the wave; say so, so that everything derived
+  // from it (head, tile, page) lives in scalar registers
+  const int wave = blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, G = lane >> 4;
-  const int total = a.cum_tiles[a.NH];
+  const int total = cum_tiles[a.NH];
   const int chunk = (total + a.W - 1) / a.W;
   int tb = wave * chunk;
   const int te = min(tb + chunk, total);
   if (tb >= te) return;
+  LaneOff lo;
+  lo.k = static_cast<uint32_t>((8 * (r >> 2) + (r & 3)) * 64 + 16 * G);
+  lo.v = static_cast<uint32_t>(D * 64 + r * 64 + 16 * G);
   // head containing tile tb: last hh with cum_tiles[hh] <= tb
-  int lo = 0, hi = a.NH;
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (a.cum_tiles[mid] <= tb) lo = mid; else hi = mid;
+  int lo_h = 0, hi_h = a.NH;
+  while (hi_h - lo_h > 1) {
+    const int mid = (lo_h + hi_h) >> 1;
+    if (cum_tiles[mid] <= tb) lo_h = mid; else hi_h = mid;
   }
-  int hh = lo;
+  int hh = lo_h;
+  const int tiles_per_page_log2 = a.log2P - 5;
   while (tb < te) {
-    while (a.cum_tiles[hh + 1] <= tb) ++hh;
-    const int c0 = a.cum_tiles[hh], c1 = a.cum_tiles[hh + 1];
+    while (cum_tiles[hh + 1] <= tb) ++hh;
+    const int c0 = cum_tiles[hh], c1 = cum_tiles[hh + 1];
     const int seg_end = min(te, c1);
-    const HeadDesc d = a.desc[hh];
+    const HeadDesc d = desc[hh];
     const int L = d.x;
-    const int32_t* pt = a.page_table + static_cast<size_t>(d.y) * a.maxp;
-    // query fragments (B operand): column r = query head of the group
+    const int32_t* pt = page_table + static_cast<size_t>(d.y) * a.maxp;
+    // query fragments (B operand): column r = query head r of the group
     u32x4 qf[D / 32];
     const u32x4 z = {0u, 0u, 0u, 0u};
-    const char* qrow = reinterpret_cast<const char*>(a.q + (static_cast<size_t>(hh) * a.g + r) * D);
+    const char* qrow = reinterpret_cast<const char*>(q + (static_cast<size_t>(hh) * a.g + r) * D);
 #pragma unroll
     for (int s = 0; s < D / 32; ++s) qf[s] = r < a.g ? ldg16(qrow + (32 * s + 8 * G) * 2) : z;
     Acc<D> acc;
@@ -215,28 +214,40 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     for (int b = 0; b < D / 16; ++b) acc.o[b] = f32x4{0.f, 0.f, 0.f, 0.f};
     acc.m = -INFINITY;
     acc.l = 0.f;
-    // full tiles, software-pipelined one tile ahead; the head's partial tail last
     const int t_lo = tb - c0;
     const int t_hi = seg_end - c0;
     const int full_hi = (seg_end == c1 && (L & (kTile - 1))) ? t_hi - 1 : t_hi;
+    // tile t of the head: page from a scalar load (the whole wave works on
+    // one head), then the tile's 16 KB block inside the page
+    auto tile_of = [&](int t) -> const char* {
+      return pool + static_cast<size_t>(pt[t >> tiles_per_page_log2]) * a.page_bytes +
+             static_cast<size_t>(t & ((1 << tiles_per_page_log2) - 1)) * (D * 128);
+    };
     if (t_lo < full_hi) {
+      // Two register sets; the next tile's loads are always in flight while
+      // the current one is computed (the prefetch is unconditional inside the
+      // loop so the compiler's wait counts only cover the older tile).
       Frag<D> fa, fb;
-      load_tile<D>(fa, a, pt, t_lo * kTile, r, G);
       int t = t_lo;
-      while (true) {
-        if (t + 1 < full_hi) load_tile<D>(fb, a, pt, (t + 1) * kTile, r, G);
+      load_tile<D>(fa, tile_of(t), lo);
+      for (; t + 2 < full_hi; t += 2) {
+        load_tile<D>(fb, tile_of(t + 1), lo);
         compute_tile<D>(acc, fa, qf, a.scale_log2, kTile, G);
-        if (++t >= full_hi) break;
-        if (t + 1 < full_hi) load_tile<D>(fa, a, pt, (t + 1) * kTile, r, G);
+        load_tile<D>(fa, tile_of(t + 2), lo);
         compute_tile<D>(acc, fb, qf, a.scale_log2, kTile, G);
-        if (++t >= full_hi) break;
+      }
+      if (t + 1 < full_hi) {
+        load_tile<D>(fb, tile_of(t + 1), lo);
+        compute_tile<D>(acc, fa, qf, a.scale_log2, kTile, G);
+        compute_tile<D>(acc, fb, qf, a.scale_log2, kTile, G);
+      } else {
+        compute_tile<D>(acc, fa, qf, a.scale_log2, kTile, G);
       }
     }
     if (full_hi < t_hi) {
       Frag<D> ft;
-      const int tok0 = full_hi * kTile;
-      load_tail<D>(ft, a, pt, tok0, L, r, G);
-      compute_tile<D>(acc, ft, qf, a.scale_log2, L - tok0, G);
+      load_tail<D>(ft, tile_of(full_hi), lo, L - full_hi * kTile, r, G);
+      compute_tile<D>(acc, ft, qf, a.scale_log2, L - full_hi * kTile, G);
     }
     float l = acc.l;
     l += __shfl_xor(l, 16, 64);
@@ -244,15 +255,15 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     if (tb == c0 && seg_end == c1) {
       if (r < a.g) {
         const float inv = 1.0f / l;
-        float* o = a.out + (static_cast<size_t>(hh) * a.g + r) * D + 4 * G;
+        float* o = out + (static_cast<size_t>(hh) * a.g + r) * D + 4 * G;
 #pragma unroll
         for (int b = 0; b < D / 16; ++b) *reinterpret_cast<f32x4*>(o + 16 * b) = acc.o[b] * inv;
       }
     } else {
       const size_t pid = static_cast<size_t>(wave) + hh;
       if (r < a.g) {
-        if (G == 0) a.part_ml[pid * kMaxGroup + r] = make_float2(acc.m, l);
-        float* o = a.part_acc + (pid * a.g + r) * D + 4 * G;
+        if (G == 0) part_ml[pid * kMaxGroup + r] = make_float2(acc.m, l);
+        float* o = part_acc + (pid * a.g + r) * D + 4 * G;
 #pragma unroll
         for (int b = 0; b < D / 16; ++b) *reinterpret_cast<f32x4*>(o + 16 * b) = acc.o[b];
       }
@@ -308,16 +319,11 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
                            int layer, int n, const void* q, float* out, int waves, hipStream_t st,
                            hipEvent_t ev_start, hipEvent_t ev_stop) {
   char* w = static_cast<char*>(ws);
-  DecodeArgs a;
-  a.status = reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status);
-  a.desc = reinterpret_cast<const HeadDesc*>(w + lo.ws_head_desc);
-  a.cum_tiles = reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles);
-  a.page_table = layer_state(lo, meta, layer).page_table;
-  a.pool = static_cast<const char*>(pool);
-  a.q = static_cast<const uint16_t*>(q);
-  a.part_ml = reinterpret_cast<float2*>(w + lo.ws_part_ml);
-  a.part_acc = reinterpret_cast<float*>(w + lo.ws_part_acc);
-  a.out = out;
+  const int32_t* status = reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status);
+  const int32_t* cum = reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles);
+  float2* part_ml = reinterpret_cast<float2*>(w + lo.ws_part_ml);
+  float* part_acc = reinterpret_cast<float*>(w + lo.ws_part_acc);
+  DecodeParams a;
   a.page_bytes = lo.page_bytes;
   a.NH = n * c.num_kv_heads;
   a.g = c.group_size;
@@ -326,16 +332,19 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
   a.log2P = __builtin_ctz(static_cast<unsigned>(c.page_size));
   a.W = waves;
   a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
-  if (ev_start) hipEventRecord(ev_start, st);
-  hipLaunchKernelGGL(decode_kernel<D>, dim3(waves / kWavesPerBlock), dim3(256), 0, st, a);
+  if (ev_start) (void)hipEventRecord(ev_start, st);
+  hipLaunchKernelGGL(decode_kernel<D>, dim3(waves / kWavesPerBlock), dim3(256), 0, st, status,
+                     reinterpret_cast<const HeadDesc*>(w + lo.ws_head_desc), cum,
+                     layer_state(lo, meta, layer).page_table, static_cast<const char*>(pool),
+                     static_cast<const uint16_t*>(q), part_ml, part_acc, out, a);
   hipError_t e = hipGetLastError();
-  if (ev_stop) hipEventRecord(ev_stop, st);
+  if (ev_stop) (void)hipEventRecord(ev_stop, st);
   if (e != hipSuccess) return e;
   CombineArgs b;
-  b.status = a.status;
-  b.cum_tiles = a.cum_tiles;
-  b.part_ml = a.part_ml;
-  b.part_acc = a.part_acc;
+  b.status = status;
+  b.cum_tiles = cum;
+  b.part_ml = part_ml;
+  b.part_acc = part_acc;
   b.out = out;
   b.NH = a.NH;
   b.g = a.g;

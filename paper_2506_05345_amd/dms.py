@@ -304,10 +304,14 @@ class DmsCache:
     def pool_page_kv(self, layer, page):
         """(K [P, d], V [P, d]) bf16 bit patterns (uint16) of one page, on the host."""
         import torch
-        c = self.cfg
-        P, D = c.page_size, c.head_dim
         raw = self.pools[layer][page * self.page_bytes:(page + 1) * self.page_bytes]
-        u16 = raw.view(torch.int16).cpu().numpy().view(np.uint16)
-        k = u16[: P * D].reshape(P, D)
-        vt = u16[P * D:].reshape(D, P)
-        return k, vt.T.copy()
+        return unpack_page(raw.view(torch.int16).cpu().numpy().view(np.uint16),
+                           self.cfg.page_size, self.cfg.head_dim)
+
+
+def unpack_page(u16, P, D):
+    """Decode one page (uint16 words, tile-major layout of dms.h) into K, V [P, D]."""
+    tiles = np.asarray(u16).reshape(P // 32, 2, D * 32)
+    k = tiles[:, 0].reshape(P // 32, D // 32, 32, 32).transpose(0, 2, 1, 3).reshape(P, D)
+    v = tiles[:, 1].reshape(P // 32, D, 32).transpose(0, 2, 1).reshape(P, D)
+    return k, v

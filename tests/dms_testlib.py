@@ -71,19 +71,21 @@ def compare_state(view, orc: PagedKVOracle, seqs, check_pages=True):
 def compare_pool(cache, layer, view, seqs, inputs_by_seq):
     """Every live slot holds the K / V bits of the position that owns it."""
     import torch
+    from paper_2506_05345_amd.dms import unpack_page
     c = cache.cfg
     P, Dm = c.page_size, c.head_dim
     raw = cache.pools[layer].view(torch.int16).cpu().numpy().view(np.uint16)
-    pages = raw.reshape(c.num_pages, 2, P * Dm)
+    words = raw.reshape(c.num_pages, -1)
+    decoded = {}
     for s in seqs:
         inp = inputs_by_seq[s]
         for h in range(c.num_kv_heads):
             L = int(view.L[s, h])
-            slots = np.arange(L)
-            pg = view.page_table[s, h, slots // P]
-            rows = slots % P
-            kk = pages[pg, 0].reshape(-1, P, Dm)[np.arange(L), rows]
-            vt = pages[pg, 1].reshape(-1, Dm, P)[np.arange(L), :, rows]
-            owner = view.slot_pos[s, h, :L]
-            assert np.array_equal(kk, inp.k[owner, h]), (s, h)
-            assert np.array_equal(vt, inp.v[owner, h]), (s, h)
+            for slot in range(L):
+                pg = int(view.page_table[s, h, slot // P])
+                if pg not in decoded:
+                    decoded[pg] = unpack_page(words[pg], P, Dm)
+                kk, vv = decoded[pg]
+                owner = view.slot_pos[s, h, slot]
+                assert np.array_equal(kk[slot % P], inp.k[owner, h]), (s, h, slot)
+                assert np.array_equal(vv[slot % P], inp.v[owner, h]), (s, h, slot)

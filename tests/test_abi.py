@@ -110,3 +110,22 @@ def test_error_strings():
     for code in (0, -1, -2, -3, -4, -5, -6):
         assert dms.dms_strerror(code) and dms.dms_strerror(code) != "unknown error code"
     assert dms.dms_strerror(-99) == "unknown error code"
+
+
+def test_unpack_page_matches_documented_offsets():
+    # element (j, e) of tile t: key at (e/32)*2048 + j*64 + (e%32)*2 bytes,
+    # value at 64*D + e*64 + j*2 bytes (include/dms.h)
+    import numpy as np
+    P, D = 64, 128
+    words = np.zeros(P * D * 2, np.uint16)
+    for s in (0, 5, 31, 32, 63):
+        t, j = divmod(s, 32)
+        for e in (0, 7, 31, 32, 100, 127):
+            base = t * 128 * D
+            words[(base + (e // 32) * 2048 + j * 64 + (e % 32) * 2) // 2] = 1000 + s * 200 + e
+            words[(base + 64 * D + e * 64 + j * 2) // 2] = 3 * (1000 + s * 200 + e)
+    k, v = dms.unpack_page(words, P, D)
+    for s in (0, 5, 31, 32, 63):
+        for e in (0, 7, 31, 32, 100, 127):
+            assert k[s, e] == 1000 + s * 200 + e
+            assert v[s, e] == 3 * (1000 + s * 200 + e)
