@@ -247,3 +247,22 @@ def chunk_vectors_torch(seed, stream, layer, seqs, heads, pos0, ntok, head_dim, 
         pp = torch.arange(pos0 + t0, pos0 + t1, device=device, dtype=torch.int64)[:, None, None, None]
         out[t0:t1] = token_vectors_torch(seed, stream, layer, ss, hh, pp, dd, device)
     return out
+
+
+def seq_chunk_vectors_torch(seed, stream, layer, seqs, heads, pos0, ntok, head_dim, device,
+                            max_elems=1 << 26):
+    """[len(seqs), ntok, heads, head_dim] bf16: positions pos0 .. pos0+ntok-1 of
+    every listed sequence, sequence-major (the varlen layout of equal-length
+    chunks), generated in slabs of at most ``max_elems`` elements."""
+    torch = _t()
+    seqs_t = torch.as_tensor(seqs, dtype=torch.int64, device=device)
+    out = torch.empty((len(seqs), ntok, heads, head_dim), dtype=torch.bfloat16, device=device)
+    per_seq_tok = heads * head_dim
+    step = max(1, max_elems // (per_seq_tok * ntok))
+    hh = torch.arange(heads, device=device, dtype=torch.int64)[None, None, :, None]
+    dd = torch.arange(head_dim, device=device, dtype=torch.int64)[None, None, None, :]
+    pp = torch.arange(pos0, pos0 + ntok, device=device, dtype=torch.int64)[None, :, None, None]
+    for i0 in range(0, len(seqs), step):
+        ss = seqs_t[i0:i0 + step][:, None, None, None]
+        out[i0:i0 + step] = token_vectors_torch(seed, stream, layer, ss, hh, pp, dd, device)
+    return out

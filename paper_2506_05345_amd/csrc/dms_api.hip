@@ -236,8 +236,8 @@ int dms_decode(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const
   hipEvent_t e0, e1;
   next_events(ctx->c, &e0, &e1);
   if (e == hipSuccess)
-    e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, out_dev,
-                           c.decode_waves, st, e0, e1);
+    e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, nullptr,
+                           nullptr, out_dev, c.decode_waves, st, e0, e1);
   return hip_rc(e);
 }
 
@@ -250,15 +250,15 @@ int dms_decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, 
   if ((rc = ensure_waves(ctx))) return rc;
   const Ctx& c = ctx->c;
   hipStream_t st = as_stream(stream);
+  // planner (slot choice, page pops, state) -> decode, which also writes the
+  // new K / V into their slots -> combine
   hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, flags_dev,
                                   true, st);
-  if (e == hipSuccess)
-    e = dms::launch_scatter(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, k_dev, v_dev, st);
   hipEvent_t e0, e1;
   next_events(ctx->c, &e0, &e1);
   if (e == hipSuccess)
-    e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, out_dev,
-                           c.decode_waves, st, e0, e1);
+    e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, k_dev,
+                           v_dev, out_dev, c.decode_waves, st, e0, e1);
   return hip_rc(e);
 }
 

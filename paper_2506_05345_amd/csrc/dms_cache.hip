@@ -168,6 +168,57 @@ __device__ inline HeadStep r1_step(const PlanArgs& a, int hh) {
   return r;
 }
 
+// Every head of the call has its own thread: state is read once into
+// registers, both prefix sums (page pops, decode tiles) share one scan.
+__device__ void plan_one_pass(const PlanArgs& a, int NH, int top0) {
+  __shared__ int lds2[34];
+  const int hh = threadIdx.x;
+  const bool act = hh < NH;
+  int sh = 0, t = 0, slot = -1, fresh = 0, need = 0, Lnew = 0, cap = 0;
+  if (act) {
+    const int s = a.seq_ids[hh / a.H];
+    sh = s * a.H + hh % a.H;
+    const int L = a.st.len[sh];
+    if (a.append) {
+      t = a.st.pos[s];
+      const int32_t e = a.st.ring[static_cast<size_t>(sh) * a.w + t % a.w];
+      const bool reuse = (t >= a.w) && (static_cast<uint32_t>(e) & kFlagBit);
+      slot = reuse ? static_cast<int>(static_cast<uint32_t>(e) & ~kFlagBit) : L;
+      fresh = !reuse;
+      cap = fresh && slot >= a.max_slots;
+      need = fresh && (slot % a.P) == 0;
+    }
+    Lnew = L + fresh;
+  }
+  const int tiles = (Lnew + kTile - 1) / kTile;
+  int2 tot;
+  const int2 ex = block_exclusive_scan2(make_int2(need, tiles), lds2, &tot);
+  if (a.append) {
+    cap = __syncthreads_or(cap);
+    if (cap || tot.x > top0) {
+      if (threadIdx.x == 0) set_status(a.status, cap ? DMS_ERR_CAPACITY : DMS_ERR_OUT_OF_PAGES);
+      return;
+    }
+  }
+  if (act) {
+    if (a.append) {
+      const uint32_t f = a.flags[hh] ? kFlagBit : 0u;
+      if (need) a.st.page_table[static_cast<size_t>(sh) * a.maxp + slot / a.P] = a.st.stack[top0 - 1 - ex.x];
+      if (fresh) a.st.len[sh] = Lnew;
+      a.st.ring[static_cast<size_t>(sh) * a.w + t % a.w] = static_cast<int32_t>(static_cast<uint32_t>(slot) | f);
+      a.st.slot_meta[static_cast<size_t>(sh) * a.max_slots + slot] = static_cast<int32_t>(static_cast<uint32_t>(t) | f);
+      // every head of the sequence read pos before the scan's barriers
+      if (hh % a.H == 0) a.st.pos[a.seq_ids[hh / a.H]] = t + 1;
+    }
+    a.desc[hh] = make_int4(Lnew, sh, slot, 0);
+    a.cum_tiles[hh + 1] = ex.y + tiles;
+  }
+  if (threadIdx.x == 0) {
+    a.cum_tiles[0] = 0;
+    if (a.append) *a.st.top = top0 - tot.x;
+  }
+}
+
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   __shared__ uint32_t seen[kMaxSeqs / 32];
   __shared__ int lds[17];
@@ -181,6 +232,10 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   }
   const int NH = a.n * a.H;
   const int top0 = *a.st.top;
+  if (NH <= static_cast<int>(blockDim.x)) {
+    plan_one_pass(a, NH, top0);
+    return;
+  }
   int total_need = 0;
   if (a.append) {
     int cap = 0;

@@ -122,6 +122,38 @@ __device__ inline int block_exclusive_scan(int v, int* lds, int* total) {
   return excl;
 }
 
+// Two exclusive prefix sums across the block in one pass (same contract as
+// block_exclusive_scan; `lds` holds 34 ints).
+__device__ inline int2 block_exclusive_scan2(int2 v, int* lds, int2* total) {
+  const int lane = threadIdx.x & 63;
+  const int wid = threadIdx.x >> 6;
+  const int nw = blockDim.x >> 6;
+  const int ix = wave_inclusive_scan(v.x);
+  const int iy = wave_inclusive_scan(v.y);
+  if (lane == 63) {
+    lds[wid] = ix;
+    lds[17 + wid] = iy;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int rx = 0, ry = 0;
+    for (int i = 0; i < nw; ++i) {
+      const int tx = lds[i], ty = lds[17 + i];
+      lds[i] = rx;
+      lds[17 + i] = ry;
+      rx += tx;
+      ry += ty;
+    }
+    lds[16] = rx;
+    lds[33] = ry;
+  }
+  __syncthreads();
+  const int2 ex = make_int2(lds[wid] + ix - v.x, lds[17 + wid] + iy - v.y);
+  *total = make_int2(lds[16], lds[33]);
+  __syncthreads();
+  return ex;
+}
+
 // Record the first device-side error (vector atomic; never a scalar store).
 __device__ inline void set_status(int32_t* status, int code) {
   atomicCAS(reinterpret_cast<int*>(status), 0, code);
@@ -144,9 +176,12 @@ hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* 
 hipError_t launch_scatter(const dms_config& c, const Layout& lo, void* meta, void* ws,
                           void* pool, int layer, int n, const void* k, const void* v,
                           hipStream_t st);
+// k / v: the tokens appended by this call's planning kernel (written into the
+// pool by the decode kernel itself), or null when nothing was appended.
 hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void* ws,
-                         void* pool, int layer, int n, const void* q, float* out,
-                         int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop);
+                         void* pool, int layer, int n, const void* q, const void* k,
+                         const void* v, float* out, int waves, hipStream_t st,
+                         hipEvent_t ev_start, hipEvent_t ev_stop);
 int decode_resident_waves(const dms_config& c);
 hipError_t launch_retained(const dms_config& c, const Layout& lo, void* meta, int layer, int n,
                            const int32_t* seq_ids, int32_t* out, hipStream_t st);

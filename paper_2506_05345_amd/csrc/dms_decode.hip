@@ -172,8 +172,9 @@ template <int D>
 __global__ __launch_bounds__(256, 2) void decode_kernel(
     const int32_t* __restrict__ status, const HeadDesc* __restrict__ desc,
     const int32_t* __restrict__ cum_tiles, const int32_t* __restrict__ page_table,
-    const char* __restrict__ pool, const uint16_t* __restrict__ q, float2* __restrict__ part_ml,
-    float* __restrict__ part_acc, float* __restrict__ out, DecodeParams a) {
+    char* __restrict__ pool, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_in,
+    const uint16_t* __restrict__ v_in, float2* __restrict__ part_ml, float* __restrict__ part_acc,
+    float* __restrict__ out, DecodeParams a) {
   if (load_status(status) != 0) return;
   const int lane = threadIdx.x & 63;
   // wave index is uniform across the wave; say so, so that everything derived
@@ -219,10 +220,23 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(
     const int full_hi = (seg_end == c1 && (L & (kTile - 1))) ? t_hi - 1 : t_hi;
     // tile t of the head: page from a scalar load (the whole wave works on
     // one head), then the tile's 16 KB block inside the page
-    auto tile_of = [&](int t) -> const char* {
+    auto tile_of = [&](int t) -> char* {
       return pool + static_cast<size_t>(pt[t >> tiles_per_page_log2]) * a.page_bytes +
              static_cast<size_t>(t & ((1 << tiles_per_page_log2) - 1)) * (D * 128);
     };
+    // The token appended by this call (slot d.z) is written into its tile by
+    // the one wave whose segment covers that tile, before the segment's
+    // loads: same-wave stores and loads to one address stay in order.
+    if (k_in != nullptr && d.z >= t_lo * kTile && d.z < t_hi * kTile) {
+      char* tile = const_cast<char*>(tile_of(d.z >> 5));
+      const int j = d.z & 31;
+      if (lane < D / 8)
+        *reinterpret_cast<u32x4*>(tile + k_elem_off(j, 8 * lane)) =
+            reinterpret_cast<const u32x4*>(k_in + static_cast<size_t>(hh) * D)[lane];
+#pragma unroll
+      for (int e = lane; e < D; e += 64)
+        *reinterpret_cast<uint16_t*>(tile + v_elem_off(j, e, D)) = v_in[static_cast<size_t>(hh) * D + e];
+    }
     if (t_lo < full_hi) {
       // Two register sets; the next tile's loads are always in flight while
       // the current one is computed (the prefetch is unconditional inside the
@@ -316,8 +330,8 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
 
 template <int D>
 hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
-                           int layer, int n, const void* q, float* out, int waves, hipStream_t st,
-                           hipEvent_t ev_start, hipEvent_t ev_stop) {
+                           int layer, int n, const void* q, const void* k, const void* v, float* out,
+                           int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
   char* w = static_cast<char*>(ws);
   const int32_t* status = reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status);
   const int32_t* cum = reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles);
@@ -335,8 +349,9 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
   if (ev_start) (void)hipEventRecord(ev_start, st);
   hipLaunchKernelGGL(decode_kernel<D>, dim3(waves / kWavesPerBlock), dim3(256), 0, st, status,
                      reinterpret_cast<const HeadDesc*>(w + lo.ws_head_desc), cum,
-                     layer_state(lo, meta, layer).page_table, static_cast<const char*>(pool),
-                     static_cast<const uint16_t*>(q), part_ml, part_acc, out, a);
+                     layer_state(lo, meta, layer).page_table, static_cast<char*>(pool),
+                     static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                     static_cast<const uint16_t*>(v), part_ml, part_acc, out, a);
   hipError_t e = hipGetLastError();
   if (ev_stop) (void)hipEventRecord(ev_stop, st);
   if (e != hipSuccess) return e;
@@ -357,11 +372,13 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
 }  // namespace
 
 hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
-                         int layer, int n, const void* q, float* out, int waves, hipStream_t st,
-                         hipEvent_t ev_start, hipEvent_t ev_stop) {
+                         int layer, int n, const void* q, const void* k, const void* v, float* out,
+                         int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (c.head_dim == 128)
-    return launch_decode_d<128>(c, lo, meta, ws, pool, layer, n, q, out, waves, st, ev_start, ev_stop);
-  return launch_decode_d<64>(c, lo, meta, ws, pool, layer, n, q, out, waves, st, ev_start, ev_stop);
+    return launch_decode_d<128>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st, ev_start,
+                                ev_stop);
+  return launch_decode_d<64>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st, ev_start,
+                             ev_stop);
 }
 
 int decode_resident_waves(const dms_config& c) {
