@@ -59,6 +59,9 @@ Layout make_layout(const dms_config& c) {
   lo.ws_cum_tiles = take((NH + 1) * 4);
   lo.ws_part_ml = take(NP * kMaxGroup * 8);
   lo.ws_part_acc = take(NP * c.group_size * D * 4);
+  lo.ws_wave_bounds = take((kMaxWaves + 1) * 4);
+  lo.ws_wave_head = take(kMaxWaves * 4);
+  lo.ws_head_cnt = take(NH * 4);
   lo.ws_ck_need = take(NH * 4);
   lo.ws_ck_fresh = take(NH * 4);
   lo.ws_ck_base = take(NH * 4);
@@ -217,7 +220,7 @@ int dms_append(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const
   const Ctx& c = ctx->c;
   hipStream_t st = as_stream(stream);
   hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, flags_dev,
-                                  true, st);
+                                  true, 0, nullptr, st);
   if (e == hipSuccess)
     e = dms::launch_scatter(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, k_dev, v_dev, st);
   return hip_rc(e);
@@ -232,7 +235,7 @@ int dms_decode(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const
   const Ctx& c = ctx->c;
   hipStream_t st = as_stream(stream);
   hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, nullptr,
-                                  false, st);
+                                  false, c.decode_waves, out_dev, st);
   hipEvent_t e0, e1;
   next_events(ctx->c, &e0, &e1);
   if (e == hipSuccess)
@@ -250,10 +253,10 @@ int dms_decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, 
   if ((rc = ensure_waves(ctx))) return rc;
   const Ctx& c = ctx->c;
   hipStream_t st = as_stream(stream);
-  // planner (slot choice, page pops, state) -> decode, which also writes the
-  // new K / V into their slots -> combine
+  // planner (slot choice, page pops, state, wave ranges) -> decode, which
+  // also writes the new K / V into their slots and merges split heads
   hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, flags_dev,
-                                  true, st);
+                                  true, c.decode_waves, out_dev, st);
   hipEvent_t e0, e1;
   next_events(ctx->c, &e0, &e1);
   if (e == hipSuccess)

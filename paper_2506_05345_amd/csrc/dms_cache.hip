@@ -23,6 +23,8 @@ __device__ inline int load_status(const int32_t* status) {
 struct InitArgs {
   char* meta;
   int32_t* ck_err;
+  int32_t* head_cnt;
+  int64_t n_heads;
   size_t layer0, layer_stride, pos, len, ring, page_table, stack, top;
   int64_t n_pos, n_len, n_ring, n_pt;
   int num_pages;
@@ -42,6 +44,8 @@ __global__ void init_state_kernel(InitArgs a) {
   for (int64_t i = t0; i < a.n_ring; i += stride) ring[i] = 0;
   for (int64_t i = t0; i < a.n_pt; i += stride) pt[i] = -1;
   for (int64_t i = t0; i < a.num_pages; i += stride) stack[i] = a.num_pages - 1 - static_cast<int32_t>(i);
+  if (blockIdx.y == 0)
+    for (int64_t i = t0; i < a.n_heads; i += stride) a.head_cnt[i] = 0;
   if (t0 == 0) {
     *reinterpret_cast<int32_t*>(b + a.top) = a.num_pages;
     if (blockIdx.y == 0) {
@@ -148,8 +152,33 @@ struct PlanArgs {
   const uint8_t* flags;  // [n, H] or null when not appending
   HeadDesc* desc;        // [n*H]
   int32_t* cum_tiles;    // [n*H + 1]
-  int n, H, w, P, maxp, max_slots, max_seqs, append;
+  int32_t* wave_bounds;  // [W + 1] first tile of every decode wave
+  int32_t* wave_head;    // [W] head holding that tile
+  float* out;            // nullable: zeroed for heads with no retained token
+  int n, H, w, P, maxp, max_slots, max_seqs, append, W, gD;
 };
+
+// Largest index i in [0, NH] with cum[i] <= b (cum non-decreasing).
+__device__ inline int upper_index(const int32_t* cum, int NH, int b) {
+  int lo = 0, hi = NH;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (cum[mid] <= b) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Tile range of every decode wave: equal contiguous shares of the flat tile
+// list (heads that straddle a boundary are merged by the decode kernel).
+__device__ void wave_ranges(const int32_t* cum, int NH, int W, int32_t* bounds,
+                            int32_t* first_head) {
+  const int total = cum[NH];
+  for (int w = threadIdx.x; w <= W; w += blockDim.x) {
+    const int b = static_cast<int>(static_cast<int64_t>(w) * total / W);
+    bounds[w] = b;
+    if (w < W) first_head[w] = min(upper_index(cum, NH, b), NH - 1);
+  }
+}
 
 struct HeadStep {
   int sh, t, slot, reuse;
@@ -172,6 +201,7 @@ __device__ inline HeadStep r1_step(const PlanArgs& a, int hh) {
 // registers, both prefix sums (page pops, decode tiles) share one scan.
 __device__ void plan_one_pass(const PlanArgs& a, int NH, int top0) {
   __shared__ int lds2[34];
+  __shared__ int32_t cum_lds[kPlanThreads + 1];
   const int hh = threadIdx.x;
   const bool act = hh < NH;
   int sh = 0, t = 0, slot = -1, fresh = 0, need = 0, Lnew = 0, cap = 0;
@@ -212,10 +242,18 @@ __device__ void plan_one_pass(const PlanArgs& a, int NH, int top0) {
     }
     a.desc[hh] = make_int4(Lnew, sh, slot, 0);
     a.cum_tiles[hh + 1] = ex.y + tiles;
+    cum_lds[hh + 1] = ex.y + tiles;
+    if (a.out != nullptr && Lnew == 0)
+      for (int e = 0; e < a.gD; ++e) a.out[static_cast<size_t>(hh) * a.gD + e] = 0.f;
   }
   if (threadIdx.x == 0) {
     a.cum_tiles[0] = 0;
+    cum_lds[0] = 0;
     if (a.append) *a.st.top = top0 - tot.x;
+  }
+  if (a.W > 0) {
+    __syncthreads();
+    wave_ranges(cum_lds, NH, a.W, a.wave_bounds, a.wave_head);
   }
 }
 
@@ -291,6 +329,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
       }
       a.desc[hh] = make_int4(Lnew, sh, slot, 0);
       a.cum_tiles[hh + 1] = ct + tiles;
+      if (a.out != nullptr && Lnew == 0)
+        for (int e = 0; e < a.gD; ++e) a.out[static_cast<size_t>(hh) * a.gD + e] = 0.f;
     }
     run_pop += totp;
     run_tiles += tott;
@@ -301,6 +341,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
     for (int i = threadIdx.x; i < a.n; i += blockDim.x) a.st.pos[a.seq_ids[i]] += 1;
     if (threadIdx.x == 0) *a.st.top = top0 - total_need;
   }
+  if (a.W > 0) wave_ranges(a.cum_tiles, NH, a.W, a.wave_bounds, a.wave_head);
 }
 
 // Copy each appended token's K row and V column into its slot.
@@ -550,6 +591,8 @@ hipError_t launch_init_state(const dms_config& c, const Layout& lo, void* meta, 
   InitArgs a;
   a.meta = static_cast<char*>(meta);
   a.ck_err = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_ck_err);
+  a.head_cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_head_cnt);
+  a.n_heads = lo.max_heads;
   a.layer0 = lo.layer0;
   a.layer_stride = lo.layer_stride;
   a.pos = lo.pos;
@@ -601,8 +644,13 @@ hipError_t launch_seq_reset(const dms_config& c, const Layout& lo, void* meta, i
 
 hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* ws, int layer,
                        int n, const int32_t* seq_ids, const uint8_t* flags, bool append,
-                       hipStream_t st) {
+                       int waves, float* out, hipStream_t st) {
   PlanArgs a;
+  a.wave_bounds = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_wave_bounds);
+  a.wave_head = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_wave_head);
+  a.out = out;
+  a.W = waves;
+  a.gD = c.group_size * c.head_dim;
   a.st = layer_state(lo, meta, layer);
   a.status = reinterpret_cast<int32_t*>(static_cast<char*>(meta) + lo.status);
   a.seq_ids = seq_ids;

@@ -29,6 +29,7 @@ struct Layout {
   size_t page_bytes, pool_bytes;
   // workspace
   size_t ws_head_desc, ws_cum_tiles, ws_part_ml, ws_part_acc;
+  size_t ws_wave_bounds, ws_wave_head, ws_head_cnt;
   size_t ws_ck_need, ws_ck_fresh, ws_ck_base, ws_ck_pos0, ws_ck_err, ws_ck_slot;
   size_t ws_pf_cum, ws_pf_meta;
   size_t workspace_bytes;
@@ -170,9 +171,13 @@ hipError_t launch_init_state(const dms_config& c, const Layout& lo, void* meta, 
 hipError_t launch_set_status(int32_t* status, int value, hipStream_t st);
 hipError_t launch_seq_reset(const dms_config& c, const Layout& lo, void* meta, int layer,
                             int n, const int32_t* seq_ids, hipStream_t st);
+// Planning kernel of a decode call: rule R1 for the appended tokens (when
+// `append`), per-head descriptors, tile prefix sums and, for `waves` > 0, the
+// tile range and first head of every decode wave.  `out` (nullable) gets zeros
+// for heads with no retained token.
 hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* ws, int layer,
                        int n, const int32_t* seq_ids, const uint8_t* flags, bool append,
-                       hipStream_t st);
+                       int waves, float* out, hipStream_t st);
 hipError_t launch_scatter(const dms_config& c, const Layout& lo, void* meta, void* ws,
                           void* pool, int layer, int n, const void* k, const void* v,
                           hipStream_t st);

@@ -9,11 +9,12 @@
 //
 //  * Work split: the retained tokens of all (sequence, KV head) pairs of the
 //    call are cut into 32-token tiles, and the flat tile list is divided into
-//    equal contiguous ranges, one per resident wave ("stream-K"): ragged
-//    per-head lengths (Sec. 3.1: heads compress at different rates) do not
-//    unbalance the chip.  A wave that covers a whole head writes the final
-//    output; otherwise it writes a partial (running max, sum, accumulator)
-//    merged by the combine kernel with log-sum-exp weights.
+//    equal contiguous ranges, one per wave, one wave per SIMD ("stream-K"):
+//    ragged per-head lengths (Sec. 3.1: heads compress at different rates) do
+//    not unbalance the chip.  A wave covering a whole head writes the final
+//    output; a head split over several waves gets partials (running max, sum,
+//    accumulator) and the wave that completes the head's tile count merges
+//    them with log-sum-exp weights (device-coherent accesses, no L2 flush).
 //  * Pages are stored tile-major: the 32 tokens of a tile are one contiguous
 //    block (keys as D/32 sub-blocks of 32 x 32 dims, then values transposed,
 //    D rows of 32 tokens).  Per tile each lane issues 16-byte loads straight
@@ -50,6 +51,17 @@ __device__ inline f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
 }
 
 __device__ inline u32x4 ldg16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+// Device-coherent (sc1) float store / load: agent-scope relaxed atomics, which
+// on gfx950 write through / read around the per-XCD L2.
+__device__ inline void store_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline float load_coherent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// s_waitcnt vmcnt(0): all of this wave's vector memory operations complete.
+constexpr int kWaitVmcnt0 = 0x0F70;
 
 struct DecodeParams {
   size_t page_bytes;
@@ -169,9 +181,11 @@ __device__ inline void compute_tile(Acc<D>& acc, const Frag<D>& f, const u32x4* 
 }
 
 template <int D>
-__global__ __launch_bounds__(256, 2) void decode_kernel(
+__global__ __launch_bounds__(256, 1) void decode_kernel(
     const int32_t* __restrict__ status, const HeadDesc* __restrict__ desc,
-    const int32_t* __restrict__ cum_tiles, const int32_t* __restrict__ page_table,
+    const int32_t* __restrict__ cum_tiles, const int32_t* __restrict__ wave_bounds,
+    const int32_t* __restrict__ wave_head, int32_t* __restrict__ head_cnt,
+    const int32_t* __restrict__ page_table,
     char* __restrict__ pool, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_in,
     const uint16_t* __restrict__ v_in, float2* __restrict__ part_ml, float* __restrict__ part_acc,
     float* __restrict__ out, DecodeParams a) {
@@ -181,21 +195,13 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(
   // from it (head, tile, page) lives in scalar registers
   const int wave = blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, G = lane >> 4;
-  const int total = cum_tiles[a.NH];
-  const int chunk = (total + a.W - 1) / a.W;
-  int tb = wave * chunk;
-  const int te = min(tb + chunk, total);
+  int tb = wave_bounds[wave];
+  const int te = wave_bounds[wave + 1];
   if (tb >= te) return;
   LaneOff lo;
   lo.k = static_cast<uint32_t>((8 * (r >> 2) + (r & 3)) * 64 + 16 * G);
   lo.v = static_cast<uint32_t>(D * 64 + r * 64 + 16 * G);
-  // head containing tile tb: last hh with cum_tiles[hh] <= tb
-  int lo_h = 0, hi_h = a.NH;
-  while (hi_h - lo_h > 1) {
-    const int mid = (lo_h + hi_h) >> 1;
-    if (cum_tiles[mid] <= tb) lo_h = mid; else hi_h = mid;
-  }
-  int hh = lo_h;
+  int hh = wave_head[wave];
   const int tiles_per_page_log2 = a.log2P - 5;
   while (tb < te) {
     while (cum_tiles[hh + 1] <= tb) ++hh;
@@ -274,57 +280,67 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(
         for (int b = 0; b < D / 16; ++b) *reinterpret_cast<f32x4*>(o + 16 * b) = acc.o[b] * inv;
       }
     } else {
+      // Split head: publish this wave's partial; the wave that completes the
+      // head's tile count merges all partials by log-sum-exp and writes the
+      // output.  Partials of head hh come from consecutive waves w, stored at
+      // index w + hh.
+      // Partials are written and read with agent-coherent (sc1) accesses, so
+      // no L2 write-back / invalidate is needed: the stores are complete at
+      // the coherence point once vmcnt drains, before the counter is bumped.
       const size_t pid = static_cast<size_t>(wave) + hh;
       if (r < a.g) {
-        if (G == 0) part_ml[pid * kMaxGroup + r] = make_float2(acc.m, l);
+        float* ml = reinterpret_cast<float*>(part_ml + pid * kMaxGroup + r);
+        if (G == 0) {
+          store_coherent(ml, acc.m);
+          store_coherent(ml + 1, l);
+        }
         float* o = part_acc + (pid * a.g + r) * D + 4 * G;
 #pragma unroll
-        for (int b = 0; b < D / 16; ++b) *reinterpret_cast<f32x4*>(o + 16 * b) = acc.o[b];
+        for (int b = 0; b < D / 16; ++b)
+#pragma unroll
+          for (int i2 = 0; i2 < 4; ++i2) store_coherent(o + 16 * b + i2, acc.o[b][i2]);
+      }
+      __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+      int prev = 0;
+      if (lane == 0) prev = atomicAdd(&head_cnt[hh], seg_end - tb);
+      prev = __shfl(prev, 0, 64);
+      if (prev + (seg_end - tb) == c1 - c0) {
+        int wf = wave, wl = wave;
+        while (wave_bounds[wf] > c0) --wf;
+        while (wave_bounds[wl + 1] < c1) ++wl;
+        if (r < a.g) {
+          // waves with an empty range (more waves than tiles) wrote nothing
+          float M = -INFINITY;
+          for (int w2 = wf; w2 <= wl; ++w2)
+            if (wave_bounds[w2] < wave_bounds[w2 + 1])
+              M = fmaxf(M, load_coherent(reinterpret_cast<const float*>(
+                                  part_ml + (static_cast<size_t>(w2) + hh) * kMaxGroup + r)));
+          float den = 0.f;
+          f32x4 num[D / 16];
+#pragma unroll
+          for (int b = 0; b < D / 16; ++b) num[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+          for (int w2 = wf; w2 <= wl; ++w2) {
+            if (wave_bounds[w2] == wave_bounds[w2 + 1]) continue;
+            const size_t p2 = static_cast<size_t>(w2) + hh;
+            const float* ml = reinterpret_cast<const float*>(part_ml + p2 * kMaxGroup + r);
+            const float sc = __builtin_amdgcn_exp2f(load_coherent(ml) - M);
+            den += sc * load_coherent(ml + 1);
+            const float* src = part_acc + (p2 * a.g + r) * D + 4 * G;
+#pragma unroll
+            for (int b = 0; b < D / 16; ++b)
+#pragma unroll
+              for (int i2 = 0; i2 < 4; ++i2) num[b][i2] += sc * load_coherent(src + 16 * b + i2);
+          }
+          const float inv = 1.0f / den;
+          float* o = out + (static_cast<size_t>(hh) * a.g + r) * D + 4 * G;
+#pragma unroll
+          for (int b = 0; b < D / 16; ++b) *reinterpret_cast<f32x4*>(o + 16 * b) = num[b] * inv;
+        }
+        if (lane == 0) __hip_atomic_store(&head_cnt[hh], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
     tb = seg_end;
     ++hh;
-  }
-}
-
-// Merge the partials of heads that spanned several waves; zero the output
-// of heads with no retained token.
-struct CombineArgs {
-  const int32_t* status;
-  const int32_t* cum_tiles;
-  const float2* part_ml;
-  const float* part_acc;
-  float* out;
-  int NH, g, D, W;
-};
-
-__global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
-  if (load_status(a.status) != 0) return;
-  const int hh = blockIdx.x;
-  const int c0 = a.cum_tiles[hh], c1 = a.cum_tiles[hh + 1];
-  const int total = a.cum_tiles[a.NH];
-  const int gd = a.g * a.D;
-  float* out = a.out + static_cast<size_t>(hh) * gd;
-  if (c0 == c1) {
-    for (int e = threadIdx.x; e < gd; e += blockDim.x) out[e] = 0.f;
-    return;
-  }
-  const int chunk = (total + a.W - 1) / a.W;
-  const int w0 = c0 / chunk, w1 = (c1 - 1) / chunk;
-  if (w0 == w1) return;
-  for (int e = threadIdx.x; e < gd; e += blockDim.x) {
-    const int r = e / a.D, dd = e % a.D;
-    float M = -INFINITY;
-    for (int w = w0; w <= w1; ++w) M = fmaxf(M, a.part_ml[(static_cast<size_t>(w) + hh) * kMaxGroup + r].x);
-    float num = 0.f, den = 0.f;
-    for (int w = w0; w <= w1; ++w) {
-      const size_t pid = static_cast<size_t>(w) + hh;
-      const float2 ml = a.part_ml[pid * kMaxGroup + r];
-      const float sc = __builtin_amdgcn_exp2f(ml.x - M);
-      num += sc * a.part_acc[(pid * a.g + r) * a.D + dd];
-      den += sc * ml.y;
-    }
-    out[e] = num / den;
   }
 }
 
@@ -349,24 +365,15 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
   if (ev_start) (void)hipEventRecord(ev_start, st);
   hipLaunchKernelGGL(decode_kernel<D>, dim3(waves / kWavesPerBlock), dim3(256), 0, st, status,
                      reinterpret_cast<const HeadDesc*>(w + lo.ws_head_desc), cum,
+                     reinterpret_cast<const int32_t*>(w + lo.ws_wave_bounds),
+                     reinterpret_cast<const int32_t*>(w + lo.ws_wave_head),
+                     reinterpret_cast<int32_t*>(w + lo.ws_head_cnt),
                      layer_state(lo, meta, layer).page_table, static_cast<char*>(pool),
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                      static_cast<const uint16_t*>(v), part_ml, part_acc, out, a);
   hipError_t e = hipGetLastError();
   if (ev_stop) (void)hipEventRecord(ev_stop, st);
-  if (e != hipSuccess) return e;
-  CombineArgs b;
-  b.status = status;
-  b.cum_tiles = cum;
-  b.part_ml = part_ml;
-  b.part_acc = part_acc;
-  b.out = out;
-  b.NH = a.NH;
-  b.g = a.g;
-  b.D = D;
-  b.W = waves;
-  hipLaunchKernelGGL(combine_kernel, dim3(a.NH), dim3(256), 0, st, b);
-  return hipGetLastError();
+  return e;
 }
 
 }  // namespace
@@ -381,6 +388,10 @@ hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void
                              ev_stop);
 }
 
+// One decode wave per SIMD (a block of 4 waves per CU).  Measured on MI355X
+// at the Qwen-R1-32B-shaped workload this beats two per SIMD (fewer split
+// heads to merge, same bandwidth); the launch must fit entirely, so the
+// occupancy of the kernel is checked.
 int decode_resident_waves(const dms_config& c) {
   int dev = 0, cus = 0, blocks = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -1;
@@ -389,7 +400,7 @@ int decode_resident_waves(const dms_config& c) {
       ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_kernel<128>, 256, 0)
       : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_kernel<64>, 256, 0);
   if (e != hipSuccess || blocks < 1) return -1;
-  int waves = cus * blocks * kWavesPerBlock;
+  int waves = cus * kWavesPerBlock;
   if (waves > kMaxWaves) waves = kMaxWaves / kWavesPerBlock * kWavesPerBlock;
   return waves;
 }
