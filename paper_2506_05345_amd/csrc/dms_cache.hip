@@ -197,21 +197,51 @@ __device__ inline HeadStep r1_step(const PlanArgs& a, int hh) {
   return r;
 }
 
-// Every head of the call has its own thread: state is read once into
-// registers, both prefix sums (page pops, decode tiles) share one scan.
-__device__ void plan_one_pass(const PlanArgs& a, int NH, int top0) {
+// Decode planning when every head of the call has its own thread (n*H <=
+// 1024, the usual case).  The dependent global loads are kept to three rounds:
+// (status, stack height, sequence ids) -> (pos, L, top of the free stack into
+// LDS) -> the ring entry; both prefix sums (page pops, decode tiles) share one
+// scan, and each wave's first head is computed arithmetically from the tile
+// prefix sums.
+__global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(PlanArgs a) {
+  __shared__ uint32_t seen[kMaxSeqs / 32];
   __shared__ int lds2[34];
-  __shared__ int32_t cum_lds[kPlanThreads + 1];
-  const int hh = threadIdx.x;
-  const bool act = hh < NH;
-  int sh = 0, t = 0, slot = -1, fresh = 0, need = 0, Lnew = 0, cap = 0;
+  __shared__ int32_t stack_lds[kPlanThreads];
+  __shared__ int s_bad;
+  const int tid = threadIdx.x;
+  const int NH = a.n * a.H;
+  const int status = load_status(a.status);
+  const int top0 = *a.st.top;
+  const bool act = tid < NH;
+  const int s = act ? a.seq_ids[tid / a.H] : 0;
+  for (int i = tid; i < (a.max_seqs + 31) / 32; i += blockDim.x) seen[i] = 0;
+  if (tid == 0) s_bad = 0;
+  __syncthreads();
+  if (status != 0) return;
+  // one thread per sequence checks its id: in range and not repeated
+  if (act && tid % a.H == 0) {
+    if (s < 0 || s >= a.max_seqs) {
+      s_bad = 1;
+    } else {
+      const uint32_t bit = 1u << (s & 31);
+      if (atomicOr(&seen[s >> 5], bit) & bit) s_bad = 1;
+    }
+  }
+  __syncthreads();
+  if (s_bad) {
+    if (tid == 0) set_status(a.status, DMS_ERR_BAD_SEQ);
+    return;
+  }
+  const int sh = s * a.H + tid % a.H;
+  int t = 0, slot = -1, fresh = 0, need = 0, Lnew = 0, cap = 0;
+  if (a.append && tid < min(NH, top0)) stack_lds[tid] = a.st.stack[top0 - 1 - tid];
   if (act) {
-    const int s = a.seq_ids[hh / a.H];
-    sh = s * a.H + hh % a.H;
     const int L = a.st.len[sh];
     if (a.append) {
       t = a.st.pos[s];
       const int32_t e = a.st.ring[static_cast<size_t>(sh) * a.w + t % a.w];
+      // the token that entered w steps ago leaves now if it was flagged; the
+      // incoming token takes its slot
       const bool reuse = (t >= a.w) && (static_cast<uint32_t>(e) & kFlagBit);
       slot = reuse ? static_cast<int>(static_cast<uint32_t>(e) & ~kFlagBit) : L;
       fresh = !reuse;
@@ -222,38 +252,44 @@ __device__ void plan_one_pass(const PlanArgs& a, int NH, int top0) {
   }
   const int tiles = (Lnew + kTile - 1) / kTile;
   int2 tot;
-  const int2 ex = block_exclusive_scan2(make_int2(need, tiles), lds2, &tot);
+  const int2 ex = block_exclusive_scan2(make_int2(need, tiles), lds2, &tot);  // barriers
   if (a.append) {
     cap = __syncthreads_or(cap);
     if (cap || tot.x > top0) {
-      if (threadIdx.x == 0) set_status(a.status, cap ? DMS_ERR_CAPACITY : DMS_ERR_OUT_OF_PAGES);
+      if (tid == 0) set_status(a.status, cap ? DMS_ERR_CAPACITY : DMS_ERR_OUT_OF_PAGES);
       return;
     }
   }
+  const int c0 = ex.y, c1 = ex.y + tiles;
   if (act) {
     if (a.append) {
-      const uint32_t f = a.flags[hh] ? kFlagBit : 0u;
-      if (need) a.st.page_table[static_cast<size_t>(sh) * a.maxp + slot / a.P] = a.st.stack[top0 - 1 - ex.x];
+      const uint32_t f = a.flags[tid] ? kFlagBit : 0u;
+      if (need) a.st.page_table[static_cast<size_t>(sh) * a.maxp + slot / a.P] = stack_lds[ex.x];
       if (fresh) a.st.len[sh] = Lnew;
       a.st.ring[static_cast<size_t>(sh) * a.w + t % a.w] = static_cast<int32_t>(static_cast<uint32_t>(slot) | f);
       a.st.slot_meta[static_cast<size_t>(sh) * a.max_slots + slot] = static_cast<int32_t>(static_cast<uint32_t>(t) | f);
       // every head of the sequence read pos before the scan's barriers
-      if (hh % a.H == 0) a.st.pos[a.seq_ids[hh / a.H]] = t + 1;
+      if (tid % a.H == 0) a.st.pos[s] = t + 1;
     }
-    a.desc[hh] = make_int4(Lnew, sh, slot, 0);
-    a.cum_tiles[hh + 1] = ex.y + tiles;
-    cum_lds[hh + 1] = ex.y + tiles;
+    a.desc[tid] = make_int4(Lnew, sh, slot, 0);
+    a.cum_tiles[tid + 1] = c1;
     if (a.out != nullptr && Lnew == 0)
-      for (int e = 0; e < a.gD; ++e) a.out[static_cast<size_t>(hh) * a.gD + e] = 0.f;
+      for (int e = 0; e < a.gD; ++e) a.out[static_cast<size_t>(tid) * a.gD + e] = 0.f;
   }
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     a.cum_tiles[0] = 0;
-    cum_lds[0] = 0;
     if (a.append) *a.st.top = top0 - tot.x;
   }
   if (a.W > 0) {
-    __syncthreads();
-    wave_ranges(cum_lds, NH, a.W, a.wave_bounds, a.wave_head);
+    // wave w starts at tile floor(w * total / W); the head holding tile b
+    // owns every wave w with ceil(c0 * W / total) <= w < ceil(c1 * W / total)
+    const int64_t total = tot.y, W = a.W;
+    for (int w = tid; w <= a.W; w += blockDim.x) a.wave_bounds[w] = static_cast<int>(w * total / W);
+    if (act && c1 > c0) {
+      const int w0 = static_cast<int>((c0 * W + total - 1) / total);
+      const int w1 = min(a.W, static_cast<int>((c1 * W + total - 1) / total));
+      for (int w = w0; w < w1; ++w) a.wave_head[w] = tid;
+    }
   }
 }
 
@@ -270,10 +306,6 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   }
   const int NH = a.n * a.H;
   const int top0 = *a.st.top;
-  if (NH <= static_cast<int>(blockDim.x)) {
-    plan_one_pass(a, NH, top0);
-    return;
-  }
   int total_need = 0;
   if (a.append) {
     int cap = 0;
@@ -665,7 +697,10 @@ hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* 
   a.max_slots = lo.max_slots;
   a.max_seqs = c.max_seqs;
   a.append = append ? 1 : 0;
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, st, a);
+  if (n * c.num_kv_heads <= kPlanThreads)
+    hipLaunchKernelGGL(plan_small_kernel, dim3(1), dim3(kPlanThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, st, a);
   return hipGetLastError();
 }
 
