@@ -222,12 +222,183 @@ def cpu_baseline(wl, ctx, budget_s=12.0):
     }
 
 
+STRESS = dict(layers=64, batch=32, kv_heads=8, group=5, head_dim=128, prefill_seqs=4,
+              chunk=4096, ctx_lo=1024, ctx_hi=131072)
+
+
+def run_stress(args):
+    """Heterogeneous 32B-shaped step: a 4096-token DMS-masked prefill chunk for
+    4 sequences and a decode step for the other 28, on every layer; per-(layer,
+    sequence, head) eviction rates ~ Beta(7,1), contexts log-uniform in
+    [1K, 128K].  Prefill inputs (q/k/v values) are shared by the layers of a
+    step; flags are per layer."""
+    import numpy as np
+    import torch
+
+    import dms_synth as sy
+    from paper_2506_05345_amd import dms
+
+    cfgw = STRESS
+    nl, B, H, g, D, C = (cfgw["layers"], cfgw["batch"], cfgw["kv_heads"], cfgw["group"],
+                         cfgw["head_dim"], cfgw["chunk"])
+    w = args.window
+    seed = 4 if w == 64 else 5
+    dev = "cuda:0"
+    P = 64
+    rng = np.random.default_rng(seed)
+    ctx = np.exp(rng.uniform(np.log(cfgw["ctx_lo"]), np.log(cfgw["ctx_hi"]), size=B)).astype(np.int64)
+    npf = cfgw["prefill_seqs"]
+    pf = np.arange(B - npf, B)
+    dc = np.arange(B - npf)
+    S = args.warmup + args.steps
+    final = ctx.copy()
+    final[pf] += S * C
+    final[dc] += S
+    thr = torch.as_tensor(np.stack([sy.beta71_rates_np(seed, l, np.arange(B)[:, None],
+                                                       np.arange(H)[None, :]) for l in range(nl)]),
+                          device=dev)                                        # [nl, B, H]
+    seqs_t = torch.arange(B, device=dev)
+    heads_t = torch.arange(H, device=dev)
+
+    def flags(layer, seq_t, pos_t):
+        """flags of (seq_t[i], head h, pos_t[i]) -> [len, H] uint8"""
+        return sy.flags_rate_torch(seed, thr[layer][seq_t[:, None], heads_t[None, :]], layer,
+                                   seq_t[:, None], heads_t[None, :], pos_t[:, None], dev)
+
+    # exact retained length of every head after every appended position is
+    # L(t) = min(w, t+1) + #{kept j <= t - w}; size the pool for the end state
+    max_pages, pages = 0, 0
+    for layer in range(nl):
+        need = torch.zeros((B, H), dtype=torch.int64, device=dev)
+        for s in range(B):
+            T = int(final[s])
+            kept = 0
+            for p0 in range(0, max(0, T - w), 65536):
+                pos = torch.arange(p0, min(p0 + 65536, T - w), device=dev)
+                kept = kept + (flags(layer, torch.full_like(pos, s), pos) == 0).sum(dim=0)
+            need[s] = (min(w, T) + kept + P - 1) // P
+        max_pages = max(max_pages, int(need.max()))
+        pages = max(pages, int(need.sum()))
+    cfg = dms.make_config(nl, B, H, g, D, w, P, pages + 64, max_pages + 2, C * B)
+    cache = dms.DmsCache(cfg, device=dev)
+    sid = torch.arange(B, dtype=torch.int32, device=dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seed)
+    t0 = time.perf_counter()
+    for layer in range(nl):
+        done = np.zeros(B, np.int64)
+        while (done < ctx).any():
+            lens = np.minimum(C, ctx - done)
+            cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+            T = int(cu[-1])
+            k = torch.randn((T, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+            v = torch.randn((T, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+            seq_of = torch.as_tensor(np.repeat(np.arange(B), lens), device=dev)
+            pos = torch.as_tensor(np.concatenate([np.arange(done[i], done[i] + lens[i]) for i in range(B)]),
+                                  device=dev)
+            dms.dms_append_chunk(cache.ctx, layer, B, sid, torch.as_tensor(cu, device=dev), T,
+                                 int(lens.max()), k, v, flags(layer, seq_of, pos))
+            done += lens
+    torch.cuda.synchronize()
+    log(f"stress state built ({time.perf_counter() - t0:.1f}s)")
+    if dms.dms_status(cache.ctx) != 0:
+        raise RuntimeError("state build failed")
+    # step inputs: values shared by layers, flags per layer and step
+    pf_sid = torch.as_tensor(pf.astype(np.int32), device=dev)
+    dc_sid = torch.as_tensor(dc.astype(np.int32), device=dev)
+    cu_pf = torch.arange(npf + 1, dtype=torch.int32, device=dev) * C
+    qp = torch.randn((npf * C, H * g, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    kp = torch.randn((npf * C, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    vp = torch.randn((npf * C, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    qd = torch.randn((len(dc), H * g, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    kd = torch.randn((len(dc), H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    vd = torch.randn((len(dc), H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    out_p = torch.empty((npf * C, H * g, D), device=dev)
+    out_d = torch.empty((len(dc), H * g, D), device=dev)
+    fp, fd = {}, {}
+    flops, dbytes = np.zeros(S), np.zeros(S)
+    lens = torch.empty((B, H), dtype=torch.int32, device=dev)
+    for layer in range(nl):
+        dms.dms_retained_lengths(cache.ctx, layer, B, sid, lens)
+        L = lens.to(torch.int64)
+        for st in range(S):
+            # prefill positions of this step and their retained counts
+            ppos = torch.cat([torch.arange(int(ctx[s]) + st * C, int(ctx[s]) + (st + 1) * C, device=dev)
+                              for s in pf])
+            pseq = torch.as_tensor(np.repeat(pf, C), device=dev)
+            fp[layer, st] = flags(layer, pseq, ppos)
+            prev = flags(layer, pseq, ppos - w)
+            fresh = ((ppos[:, None] < w) | (prev == 0)).to(torch.int64).view(npf, C, H)
+            Lq = L[torch.as_tensor(pf, device=dev)][:, None, :] + torch.cumsum(fresh, dim=1)
+            flops[st] += float(Lq.sum()) * g * 4 * D
+            L[torch.as_tensor(pf, device=dev)] = Lq[:, -1]
+            dpos = torch.as_tensor(ctx[dc] + st, device=dev)
+            dseq = torch.as_tensor(dc, device=dev)
+            fd[layer, st] = flags(layer, dseq, dpos)
+            prev = flags(layer, dseq, dpos - w)
+            freshd = ((dpos[:, None] < w) | (prev == 0)).to(torch.int64)
+            L[torch.as_tensor(dc, device=dev)] += freshd
+            dbytes[st] += float(L[torch.as_tensor(dc, device=dev)].sum()) * 2 * D * 2
+
+    def step(st):
+        for layer in range(nl):
+            dms.dms_prefill_chunk(cache.ctx, layer, npf, pf_sid, cu_pf, npf * C, C, qp, kp, vp,
+                                  fp[layer, st], out_p)
+            dms.dms_decode_step(cache.ctx, layer, len(dc), dc_sid, qd, kd, vd, fd[layer, st], out_d)
+
+    for st in range(args.warmup):
+        step(st)
+    torch.cuda.synchronize()
+    dms.dms_profile_start(cache.ctx, 2 * nl * args.steps)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for st in range(args.warmup, S):
+        step(st)
+    e1.record()
+    torch.cuda.synchronize()
+    prof = dms.dms_profile_stop(cache.ctx)
+    if dms.dms_status(cache.ctx) != 0:
+        raise RuntimeError("stress step failed")
+    step_ms = e0.elapsed_time(e1) / args.steps
+    dms_ms, dn = prof[dms.DMS_PROFILE_DECODE]
+    pms, pn = prof[dms.DMS_PROFILE_PREFILL]
+    fl = flops[args.warmup:].sum()
+    db = dbytes[args.warmup:].sum()
+    res = {
+        "metric": "DMS heterogeneous mixed step: prefill TFLOP/s and decode KV GB/s",
+        "value": round(fl / (pms * 1e-3) / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "32B-shaped heterogeneous stress: 64 layers, 32 sequences x 8 KV "
+                               "heads (group 5), per-head eviction rate ~ Beta(7,1), contexts "
+                               "log-uniform in [1K, 128K]; per step a 4096-token masked prefill "
+                               "for 4 sequences and a decode step for 28",
+                   "window": w, "mean_context": float(ctx.mean())},
+        "prefill": {"kernel_avg_us": round(1e3 * pms / pn, 1),
+                    "algorithmic_tflop_per_launch": round(fl / pn / 1e12, 4),
+                    "achieved_tflops": round(fl / (pms * 1e-3) / 1e12, 2),
+                    "peak_tflops": 2500.0,
+                    "frac": round(fl / (pms * 1e-3) / 1e12 / 2500.0, 4)},
+        "decode": {"kernel_avg_us": round(1e3 * dms_ms / dn, 1),
+                   "kv_gb_per_launch": round(db / dn / 1e9, 4),
+                   "achieved_gbs": round(db / (dms_ms * 1e-3) / 1e9, 1),
+                   "frac_of_hbm_peak": round(db / (dms_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+        "decode_tok_per_s": round(len(dc) / (step_ms * 1e-3), 1),
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="qwen-r1-32b-8x", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="qwen-r1-32b-8x",
+                    choices=sorted(WORKLOADS) + ["qwen-r1-32b-stress"])
+    ap.add_argument("--window", type=int, default=256, choices=[64, 256],
+                    help="window of the heterogeneous stress workload")
     ap.add_argument("--chunk", type=int, default=4096)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -243,6 +414,10 @@ def main():
     import torch
     from paper_2506_05345_amd import dms
 
+    if args.workload == "qwen-r1-32b-stress":
+        torch.cuda.set_device(0)
+        run_stress(args)
+        return
     wl = WORKLOADS[args.workload]
     dev = "cuda:0"
     torch.cuda.set_device(0)
@@ -301,7 +476,7 @@ def main():
     for s in range(k_lo, k_hi):
         run_step(s)
     torch.cuda.synchronize()
-    kern_ms, launches = dms.dms_profile_stop(cache.ctx)
+    kern_ms, launches = dms.dms_profile_stop(cache.ctx)[dms.DMS_PROFILE_DECODE]
     if launches != args.steps * nl:
         raise RuntimeError(f"timing events recorded {launches} of {args.steps * nl} decode launches")
     step_ms = ev0.elapsed_time(ev1) / args.steps

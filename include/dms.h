@@ -227,14 +227,19 @@ int dms_clear_status(dms_ctx* ctx, void* stream);
 
 /* Kernel timing instrumentation (not part of the method).  While a session
  * is active the library records a pair of HIP events around each split-K
- * decode kernel it launches, for at most max_launches launches; later
- * launches are not recorded.  Events are created here and destroyed by
- * dms_profile_stop (no device memory is allocated). */
+ * decode kernel and each masked-prefill attention kernel it launches, for at
+ * most max_launches launches in total; later launches are not recorded.
+ * Events are created here and destroyed by dms_profile_stop (no device
+ * memory is allocated). */
 int dms_profile_start(dms_ctx* ctx, int max_launches);
 
-/* Wait for the recorded events and end the session: *total_ms = summed
- * duration of the recorded decode kernels, *launches = how many. */
-int dms_profile_stop(dms_ctx* ctx, float* total_ms, int* launches);
+enum { DMS_PROFILE_DECODE = 0, DMS_PROFILE_PREFILL = 1 };
+
+/* Wait for the recorded events and end the session.  ms_out[k] = summed
+ * duration and launches_out[k] = number of recorded launches of kernel kind
+ * k (DMS_PROFILE_DECODE, DMS_PROFILE_PREFILL); both arrays have 2 entries
+ * and may be NULL. */
+int dms_profile_stop(dms_ctx* ctx, float* ms_out, int* launches_out);
 
 /* Static description of an error code. */
 const char* dms_strerror(int code);

@@ -81,8 +81,9 @@ struct Ctx {
   std::vector<void*> pools;
   void* ws;
   int decode_waves;  // resident decode waves, found on first decode
-  // decode-kernel timing session
+  // kernel timing session: event pairs and the kind of kernel each timed
   std::vector<hipEvent_t> ev;
+  std::vector<int> ev_kind;
   int ev_used = 0;
   bool profiling = false;
 };
@@ -101,13 +102,14 @@ inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
 inline int hip_rc(hipError_t e) { return e == hipSuccess ? DMS_OK : DMS_ERR_HIP; }
 
-// Event pair for the next decode launch of a timing session (or nulls).
-void next_events(Ctx& c, hipEvent_t* a, hipEvent_t* b) {
+// Event pair for the next timed launch of a session (or nulls).
+void next_events(Ctx& c, int kind, hipEvent_t* a, hipEvent_t* b) {
   *a = nullptr;
   *b = nullptr;
   if (!c.profiling || c.ev_used + 2 > static_cast<int>(c.ev.size())) return;
   *a = c.ev[c.ev_used];
   *b = c.ev[c.ev_used + 1];
+  c.ev_kind[c.ev_used / 2] = kind;
   c.ev_used += 2;
 }
 
@@ -193,7 +195,7 @@ int dms_create(const dms_config* cfg, void* meta_dev, void* const* pools_dev_hos
 
 int dms_destroy(dms_ctx* ctx) {
   if (!ctx) return DMS_ERR_INVALID;
-  for (auto& e : ctx->c.ev) hipEventDestroy(e);
+  for (auto& e : ctx->c.ev) (void)hipEventDestroy(e);
   delete ctx;
   return DMS_OK;
 }
@@ -237,7 +239,7 @@ int dms_decode(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const
   hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, nullptr,
                                   false, c.decode_waves, out_dev, st);
   hipEvent_t e0, e1;
-  next_events(ctx->c, &e0, &e1);
+  next_events(ctx->c, DMS_PROFILE_DECODE, &e0, &e1);
   if (e == hipSuccess)
     e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, nullptr,
                            nullptr, out_dev, c.decode_waves, st, e0, e1);
@@ -258,7 +260,7 @@ int dms_decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, 
   hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, flags_dev,
                                   true, c.decode_waves, out_dev, st);
   hipEvent_t e0, e1;
-  next_events(ctx->c, &e0, &e1);
+  next_events(ctx->c, DMS_PROFILE_DECODE, &e0, &e1);
   if (e == hipSuccess)
     e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, k_dev,
                            v_dev, out_dev, c.decode_waves, st, e0, e1);
@@ -291,10 +293,12 @@ int dms_prefill_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev
   if (!q_dev || !k_dev || !v_dev || !flags_dev || !out_dev) return DMS_ERR_INVALID;
   const Ctx& c = ctx->c;
   hipStream_t st = as_stream(stream);
+  hipEvent_t e0, e1;
+  next_events(ctx->c, DMS_PROFILE_PREFILL, &e0, &e1);
   hipError_t e = dms::launch_prefill_attention(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer,
                                                n, seq_ids_dev, cu_seqlens_dev, total_tokens,
                                                max_seqlen, q_dev, k_dev, v_dev, flags_dev,
-                                               out_dev, st);
+                                               out_dev, st, e0, e1);
   if (e == hipSuccess)
     e = dms::launch_chunk_commit(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, seq_ids_dev,
                                  cu_seqlens_dev, total_tokens, max_seqlen, k_dev, v_dev,
@@ -344,10 +348,11 @@ int dms_profile_start(dms_ctx* ctx, int max_launches) {
   if (!ctx || max_launches < 1 || ctx->c.profiling) return DMS_ERR_INVALID;
   Ctx& c = ctx->c;
   c.ev.assign(2 * static_cast<size_t>(max_launches), nullptr);
+  c.ev_kind.assign(static_cast<size_t>(max_launches), 0);
   for (auto& e : c.ev) {
     if (hipEventCreate(&e) != hipSuccess) {
       for (auto& x : c.ev)
-        if (x) hipEventDestroy(x);
+        if (x) (void)hipEventDestroy(x);
       c.ev.clear();
       return DMS_ERR_HIP;
     }
@@ -357,10 +362,11 @@ int dms_profile_start(dms_ctx* ctx, int max_launches) {
   return DMS_OK;
 }
 
-int dms_profile_stop(dms_ctx* ctx, float* total_ms, int* launches) {
+int dms_profile_stop(dms_ctx* ctx, float* ms_out, int* launches_out) {
   if (!ctx || !ctx->c.profiling) return DMS_ERR_INVALID;
   Ctx& c = ctx->c;
-  float sum = 0.0f;
+  float sum[2] = {0.0f, 0.0f};
+  int cnt[2] = {0, 0};
   int rc = DMS_OK;
   for (int i = 0; i + 1 < c.ev_used; i += 2) {
     float ms = 0.0f;
@@ -369,12 +375,17 @@ int dms_profile_stop(dms_ctx* ctx, float* total_ms, int* launches) {
       rc = DMS_ERR_HIP;
       break;
     }
-    sum += ms;
+    const int k = c.ev_kind[i / 2];
+    sum[k] += ms;
+    cnt[k] += 1;
   }
-  if (total_ms) *total_ms = sum;
-  if (launches) *launches = c.ev_used / 2;
-  for (auto& e : c.ev) hipEventDestroy(e);
+  for (int k = 0; k < 2; ++k) {
+    if (ms_out) ms_out[k] = sum[k];
+    if (launches_out) launches_out[k] = cnt[k];
+  }
+  for (auto& e : c.ev) (void)hipEventDestroy(e);
   c.ev.clear();
+  c.ev_kind.clear();
   c.ev_used = 0;
   c.profiling = false;
   return rc;

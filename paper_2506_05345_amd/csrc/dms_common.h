@@ -198,6 +198,7 @@ hipError_t launch_prefill_attention(const dms_config& c, const Layout& lo, void*
                                     void* pool, int layer, int n, const int32_t* seq_ids,
                                     const int32_t* cu, int total_tokens, int max_len,
                                     const void* q, const void* k, const void* v,
-                                    const uint8_t* flags, float* out, hipStream_t st);
+                                    const uint8_t* flags, float* out, hipStream_t st,
+                                    hipEvent_t ev_start, hipEvent_t ev_stop);
 
 }  // namespace dms

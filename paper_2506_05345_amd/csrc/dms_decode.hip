@@ -62,9 +62,14 @@ __device__ inline float load_coherent(const float* p) {
 }
 // s_waitcnt vmcnt(0): all of this wave's vector memory operations complete.
 constexpr int kWaitVmcnt0 = 0x0F70;
+// Raw buffer resource word 3 (32-bit data format, no swizzle) and the sc1
+// cache-policy bit of buffer loads / stores (agent-coherent access).
+constexpr int kBufferDword3 = 0x00020000;
+constexpr int kCachePolicySc1 = 0x10;
 
 struct DecodeParams {
   size_t page_bytes;
+  int part_acc_bytes;   // size of the split-K accumulator area (< 2 GiB)
   int NH, g, maxp, P, log2P, W;
   float scale_log2;  // softmax scale * log2(e)
 };
@@ -180,6 +185,175 @@ __device__ inline void compute_tile(Acc<D>& acc, const Frag<D>& f, const u32x4* 
   for (int b = 0; b < D / 16; ++b) acc.o[b] = mfma_bf16(f.vt[b], pu, acc.o[b]);
 }
 
+__device__ inline float wave_max(float v) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+constexpr int kMergeBatch = 64;   // partials handled per merge round (one per lane)
+
+// Log-sum-exp merge of the partials a head got from waves wf .. wl (index
+// w + hh; waves with an empty range wrote none).  All reads are
+// agent-coherent and issued in parallel: each lane fetches one partial's
+// (max, sum) for every row, row maxima and sums are wave reductions, the
+// weights go through LDS, and the head's g x D outputs are spread over the
+// 64 lanes as 16-byte pieces whose loads for a batch of partials are in
+// flight together.
+template <int D>
+__device__ void merge_head(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsrc,
+                           const int32_t* wave_bounds, float* out, int wf, int wl, int hh, int g,
+                           int lane, float (*wts)[kMaxGroup]) {
+  constexpr int kMaxPieces = kMaxGroup * D / 4 / 64;   // 16-byte pieces per lane
+  const int pieces = g * D / 4;
+  // pass 1: row maxima
+  float M[kMaxGroup];
+#pragma unroll
+  for (int r = 0; r < kMaxGroup; ++r) M[r] = -INFINITY;
+  for (int b0 = wf; b0 <= wl; b0 += kMergeBatch) {
+    const int w2 = b0 + lane;
+    if (w2 <= wl && wave_bounds[w2] < wave_bounds[w2 + 1]) {
+      const float* ml = reinterpret_cast<const float*>(part_ml + (static_cast<size_t>(w2) + hh) * kMaxGroup);
+#pragma unroll
+      for (int r = 0; r < kMaxGroup; ++r)
+        if (r < g) M[r] = fmaxf(M[r], load_coherent(ml + 2 * r));
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < kMaxGroup; ++r)
+    if (r < g) M[r] = wave_max(M[r]);
+  // pass 2: weights, sums and weighted accumulators, one batch of partials at a time
+  float den[kMaxGroup];
+#pragma unroll
+  for (int r = 0; r < kMaxGroup; ++r) den[r] = 0.f;
+  f32x4 num[kMaxPieces];
+#pragma unroll
+  for (int j = 0; j < kMaxPieces; ++j) num[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int b0 = wf; b0 <= wl; b0 += kMergeBatch) {
+    const int w2 = b0 + lane;
+    const bool live = w2 <= wl && wave_bounds[w2] < wave_bounds[w2 + 1];
+    const float* ml = reinterpret_cast<const float*>(part_ml + (static_cast<size_t>(w2) + hh) * kMaxGroup);
+#pragma unroll
+    for (int r = 0; r < kMaxGroup; ++r) {
+      if (r < g) {
+        const float sc = live ? __builtin_amdgcn_exp2f(load_coherent(ml + 2 * r) - M[r]) : 0.f;
+        wts[lane][r] = sc;
+        if (live) den[r] += sc * load_coherent(ml + 2 * r + 1);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const int nb = min(kMergeBatch, wl - b0 + 1);
+    for (int i0 = 0; i0 < nb; i0 += 8) {
+#pragma unroll
+      for (int j = 0; j < kMaxPieces; ++j) {
+        const int f = lane + 64 * j;
+        if (f < pieces) {
+          const int row = 4 * f / D;
+          u32x4 x[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            const size_t p2 = static_cast<size_t>(b0 + i0 + u) + hh;
+            x[u] = (i0 + u < nb) ? __builtin_amdgcn_raw_buffer_load_b128(
+                                       acc_rsrc, static_cast<uint32_t>((p2 * g * D + 4 * f) * 4), 0,
+                                       kCachePolicySc1)
+                                 : u32x4{0u, 0u, 0u, 0u};
+          }
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            if (i0 + u < nb) num[j] += wts[i0 + u][row] * __builtin_bit_cast(f32x4, x[u]);
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();   // weights of this batch read before the next overwrites them
+  }
+#pragma unroll
+  for (int r = 0; r < kMaxGroup; ++r)
+    if (r < g) den[r] = wave_sum(den[r]);
+  float* o = out + static_cast<size_t>(hh) * g * D;
+#pragma unroll
+  for (int j = 0; j < kMaxPieces; ++j) {
+    const int f = lane + 64 * j;
+    if (f < pieces) {
+      const int row = 4 * f / D;
+      float d = den[0];
+#pragma unroll
+      for (int r = 1; r < kMaxGroup; ++r) if (r == row) d = den[r];
+      *reinterpret_cast<f32x4*>(o + 4 * f) = num[j] * (1.0f / d);
+    }
+  }
+}
+
+// Merge of at most 4 partials (the usual case): every load -- each lane's
+// partial (max, sum) and all 16-byte accumulator pieces of all partials --
+// is issued in one round; weights are passed between lanes by shuffles.
+template <int D>
+__device__ void merge_head_small(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsrc,
+                                 const int32_t* wave_bounds, float* out, int wf, int np, int hh,
+                                 int g, int lane) {
+  constexpr int kMaxPieces = kMaxGroup * D / 4 / 64;
+  constexpr int kMaxParts = 4;
+  const int pieces = g * D / 4;
+  const bool live = lane < np && wave_bounds[wf + lane] < wave_bounds[wf + lane + 1];
+  const float* ml = reinterpret_cast<const float*>(
+      part_ml + (static_cast<size_t>(wf + (lane < np ? lane : 0)) + hh) * kMaxGroup);
+  float m[kMaxGroup], l[kMaxGroup];
+#pragma unroll
+  for (int r = 0; r < kMaxGroup; ++r) {
+    m[r] = (live && r < g) ? load_coherent(ml + 2 * r) : -INFINITY;
+    l[r] = (live && r < g) ? load_coherent(ml + 2 * r + 1) : 0.f;
+  }
+  u32x4 x[kMaxPieces][kMaxParts];
+#pragma unroll
+  for (int j = 0; j < kMaxPieces; ++j) {
+    const int f = lane + 64 * j;
+#pragma unroll
+    for (int u = 0; u < kMaxParts; ++u) {
+      const size_t p2 = static_cast<size_t>(wf + u) + hh;
+      x[j][u] = (f < pieces && u < np)
+                    ? __builtin_amdgcn_raw_buffer_load_b128(
+                          acc_rsrc, static_cast<uint32_t>((p2 * g * D + 4 * f) * 4), 0, kCachePolicySc1)
+                    : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  float wgt[kMaxGroup], den[kMaxGroup];
+#pragma unroll
+  for (int r = 0; r < kMaxGroup; ++r) {
+    if (r < g) {
+      const float M = wave_max(m[r]);
+      wgt[r] = live ? __builtin_amdgcn_exp2f(m[r] - M) : 0.f;
+      den[r] = wave_sum(wgt[r] * l[r]);
+    }
+  }
+  float* o = out + static_cast<size_t>(hh) * g * D;
+#pragma unroll
+  for (int j = 0; j < kMaxPieces; ++j) {
+    const int f = lane + 64 * j;
+    const int row = min(4 * f / D, kMaxGroup - 1);
+    f32x4 num = {0.f, 0.f, 0.f, 0.f};
+    float d = 1.f;
+#pragma unroll
+    for (int r = 0; r < kMaxGroup; ++r) {
+      if (r < g) {
+        // every lane takes part in the shuffles; only rows it owns are kept
+#pragma unroll
+        for (int u = 0; u < kMaxParts; ++u) {
+          const float wu = __shfl(wgt[r], u, 64);
+          if (r == row && u < np) num += wu * __builtin_bit_cast(f32x4, x[j][u]);
+        }
+        if (r == row) d = den[r];
+      }
+    }
+    if (f < pieces) *reinterpret_cast<f32x4*>(o + 4 * f) = num * (1.0f / d);
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(256, 1) void decode_kernel(
     const int32_t* __restrict__ status, const HeadDesc* __restrict__ desc,
@@ -189,6 +363,7 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
     char* __restrict__ pool, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_in,
     const uint16_t* __restrict__ v_in, float2* __restrict__ part_ml, float* __restrict__ part_acc,
     float* __restrict__ out, DecodeParams a) {
+  __shared__ float merge_wts[kWavesPerBlock][kMergeBatch][kMaxGroup];
   if (load_status(status) != 0) return;
   const int lane = threadIdx.x & 63;
   // wave index is uniform across the wave; say so, so that everything derived
@@ -288,17 +463,19 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
       // no L2 write-back / invalidate is needed: the stores are complete at
       // the coherence point once vmcnt drains, before the counter is bumped.
       const size_t pid = static_cast<size_t>(wave) + hh;
+      const __amdgpu_buffer_rsrc_t acc_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+          part_acc, static_cast<short>(0), a.part_acc_bytes, kBufferDword3);
       if (r < a.g) {
         float* ml = reinterpret_cast<float*>(part_ml + pid * kMaxGroup + r);
         if (G == 0) {
           store_coherent(ml, acc.m);
           store_coherent(ml + 1, l);
         }
-        float* o = part_acc + (pid * a.g + r) * D + 4 * G;
+        const uint32_t o = static_cast<uint32_t>(((pid * a.g + r) * D + 4 * G) * 4);
 #pragma unroll
         for (int b = 0; b < D / 16; ++b)
-#pragma unroll
-          for (int i2 = 0; i2 < 4; ++i2) store_coherent(o + 16 * b + i2, acc.o[b][i2]);
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc.o[b]), acc_rsrc,
+                                                 o + 64 * b, 0, kCachePolicySc1);
       }
       __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
       int prev = 0;
@@ -308,34 +485,11 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
         int wf = wave, wl = wave;
         while (wave_bounds[wf] > c0) --wf;
         while (wave_bounds[wl + 1] < c1) ++wl;
-        if (r < a.g) {
-          // waves with an empty range (more waves than tiles) wrote nothing
-          float M = -INFINITY;
-          for (int w2 = wf; w2 <= wl; ++w2)
-            if (wave_bounds[w2] < wave_bounds[w2 + 1])
-              M = fmaxf(M, load_coherent(reinterpret_cast<const float*>(
-                                  part_ml + (static_cast<size_t>(w2) + hh) * kMaxGroup + r)));
-          float den = 0.f;
-          f32x4 num[D / 16];
-#pragma unroll
-          for (int b = 0; b < D / 16; ++b) num[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-          for (int w2 = wf; w2 <= wl; ++w2) {
-            if (wave_bounds[w2] == wave_bounds[w2 + 1]) continue;
-            const size_t p2 = static_cast<size_t>(w2) + hh;
-            const float* ml = reinterpret_cast<const float*>(part_ml + p2 * kMaxGroup + r);
-            const float sc = __builtin_amdgcn_exp2f(load_coherent(ml) - M);
-            den += sc * load_coherent(ml + 1);
-            const float* src = part_acc + (p2 * a.g + r) * D + 4 * G;
-#pragma unroll
-            for (int b = 0; b < D / 16; ++b)
-#pragma unroll
-              for (int i2 = 0; i2 < 4; ++i2) num[b][i2] += sc * load_coherent(src + 16 * b + i2);
-          }
-          const float inv = 1.0f / den;
-          float* o = out + (static_cast<size_t>(hh) * a.g + r) * D + 4 * G;
-#pragma unroll
-          for (int b = 0; b < D / 16; ++b) *reinterpret_cast<f32x4*>(o + 16 * b) = num[b] * inv;
-        }
+        if (wl - wf < 4)
+          merge_head_small<D>(part_ml, acc_rsrc, wave_bounds, out, wf, wl - wf + 1, hh, a.g, lane);
+        else
+          merge_head<D>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, a.g, lane,
+                        merge_wts[threadIdx.x >> 6]);
         if (lane == 0) __hip_atomic_store(&head_cnt[hh], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
@@ -355,6 +509,7 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
   float* part_acc = reinterpret_cast<float*>(w + lo.ws_part_acc);
   DecodeParams a;
   a.page_bytes = lo.page_bytes;
+  a.part_acc_bytes = static_cast<int>(static_cast<size_t>(lo.max_partials) * c.group_size * D * 4);
   a.NH = n * c.num_kv_heads;
   a.g = c.group_size;
   a.maxp = c.max_pages_per_head;

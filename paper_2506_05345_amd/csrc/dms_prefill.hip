@@ -358,7 +358,8 @@ template <int D>
 hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
                             int layer, int n, const int32_t* seq_ids, const int32_t* cu,
                             int total_tokens, int max_len, const void* q, const void* k,
-                            const void* v, const uint8_t* flags, float* out, hipStream_t st) {
+                            const void* v, const uint8_t* flags, float* out, hipStream_t st,
+                            hipEvent_t ev_start, hipEvent_t ev_stop) {
   char* w = static_cast<char*>(ws);
   LayerState ls = layer_state(lo, meta, layer);
   PrefillArgs a;
@@ -397,8 +398,11 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 grid((max_len + a.PB - 1) / a.PB, NH);
+  if (ev_start) (void)hipEventRecord(ev_start, st);
   hipLaunchKernelGGL((prefill_kernel<D, kNQ>), grid, dim3(kThreads), 0, st, a);
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (ev_stop) (void)hipEventRecord(ev_stop, st);
+  return e;
 }
 
 }  // namespace
@@ -407,12 +411,13 @@ hipError_t launch_prefill_attention(const dms_config& c, const Layout& lo, void*
                                     void* pool, int layer, int n, const int32_t* seq_ids,
                                     const int32_t* cu, int total_tokens, int max_len,
                                     const void* q, const void* k, const void* v,
-                                    const uint8_t* flags, float* out, hipStream_t st) {
+                                    const uint8_t* flags, float* out, hipStream_t st,
+                                    hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (c.head_dim == 128)
     return launch_prefill_d<128>(c, lo, meta, ws, pool, layer, n, seq_ids, cu, total_tokens,
-                                 max_len, q, k, v, flags, out, st);
+                                 max_len, q, k, v, flags, out, st, ev_start, ev_stop);
   return launch_prefill_d<64>(c, lo, meta, ws, pool, layer, n, seq_ids, cu, total_tokens, max_len,
-                              q, k, v, flags, out, st);
+                              q, k, v, flags, out, st, ev_start, ev_stop);
 }
 
 }  // namespace dms

@@ -222,11 +222,16 @@ def dms_profile_start(ctx, max_launches):
     _check(lib().dms_profile_start(ctx, max_launches), "dms_profile_start")
 
 
+DMS_PROFILE_DECODE = 0
+DMS_PROFILE_PREFILL = 1
+
+
 def dms_profile_stop(ctx):
-    """Returns (total decode-kernel milliseconds, launches recorded)."""
-    ms, n = ctypes.c_float(), _I()
-    _check(lib().dms_profile_stop(ctx, ctypes.byref(ms), ctypes.byref(n)), "dms_profile_stop")
-    return ms.value, n.value
+    """Returns {kind: (total milliseconds, launches recorded)} for the decode
+    and prefill-attention kernels."""
+    ms, n = (ctypes.c_float * 2)(), (_I * 2)()
+    _check(lib().dms_profile_stop(ctx, ms, n), "dms_profile_stop")
+    return {DMS_PROFILE_DECODE: (ms[0], n[0]), DMS_PROFILE_PREFILL: (ms[1], n[1])}
 
 
 def dms_strerror(code: int) -> str:
