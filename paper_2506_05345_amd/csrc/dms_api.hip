@@ -70,6 +70,10 @@ Layout make_layout(const dms_config& c) {
   lo.ws_ck_slot = take(static_cast<size_t>(c.max_chunk_tokens) * H * 4);
   lo.ws_pf_cum = take((NH + 1) * 4);
   lo.ws_pf_meta = take(static_cast<size_t>(c.max_chunk_tokens) * H * 4);
+  // prefill: chunk keys / values and the compacted kept ones, in the pool's
+  // tile layout; sequence i of a call starts at tile cu[i] / 32 + i
+  lo.pf_tiles_per_head = static_cast<int>((static_cast<size_t>(c.max_chunk_tokens) + 31) / 32 + S + 1);
+  lo.ws_pf_tiles = take(2 * H * static_cast<size_t>(lo.pf_tiles_per_head) * D * 128);
   lo.workspace_bytes = off;
   return lo;
 }

@@ -4,23 +4,29 @@
 // (j > t - w or key j is kept) -- the binary mask of Fig. 1b (Sec. 3.1), passed
 // as the per-token decision vector and never materialised (Sec. 3.1
 // "Performance Considerations"); the sparsity it creates is used to skip work
-// (Sec. 3.2).  Keys come from three places:
+// (Sec. 3.2).  For a block of queries [t0, t1) keys come from three places:
 //   1. the cache: the L0 live slots of the head before the chunk; all of them
 //      are visible except flagged tokens of the last w positions, which expire
 //      inside the chunk by the same rule (slot_meta holds owner position and
 //      flag);
-//   2. kept chunk keys older than the query block's window band -- visible to
-//      every query of the block -- gathered from a compacted list built by
-//      prefill_list_kernel (flagged keys there are skipped entirely);
-//   3. the band [max(p0, t0 - w + 1), t1) of chunk keys, masked per element.
+//   2. kept chunk keys before the band -- visible to every query of the
+//      block; flagged ones there are hidden from all of them and skipped;
+//   3. the band: the chunk tiles from the one holding max(p0, t0 - w + 1) to
+//      t1, masked per element.
 //
-// A workgroup (4 waves) owns one (sequence, KV head, block of query
-// positions).  Its columns are (position, query head) pairs packed 16 to an
-// MFMA column block (16 / g positions x g heads); each wave holds NQ column
-// blocks.  Key tiles of 32 are staged into LDS in the pool's tile layout
-// (keys [d/32][32][32], values transposed [d][32]), double buffered, and read
-// by every wave with 16-byte LDS loads straight into MFMA operand registers;
-// scores, masking and the online softmax follow the decode kernel.
+// Pass 0 lists the kept chunk tokens; pass 1 copies the chunk's keys and
+// values, in chunk order and in kept order, into workspace tiles in the
+// pool's tile layout (keys [d/32][32][32], values transposed [d][32]), so the
+// attention pass stages every source the same way.
+//
+// Attention pass: a workgroup (4 waves) owns one (sequence, KV head, block of
+// query positions).  Its columns are (position, query head) pairs packed 16
+// to an MFMA column block (16 / g positions x g heads); each wave holds NQ
+// column blocks.  Key tiles of 32 are staged into LDS (16-byte chunks
+// swizzled against bank conflicts), double buffered, and read by every wave
+// with 16-byte LDS loads straight into MFMA operand registers.  A tile is
+// masked per element only when some query of the block does not see one of
+// its keys; the online softmax works in the exp2 domain with a lazy rescale.
 #include "dms_common.h"
 
 namespace dms {
@@ -32,7 +38,29 @@ typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
 constexpr int kThreads = 256;
 constexpr uint32_t kNoKey = 0x7FFFFFFFu;  // key position of padding rows (never visible)
-constexpr float kRescale = 8.0f;
+constexpr float kRescale = 8.0f;          // lazy rescale threshold, log2 units
+constexpr float kMInit = -1.0e30f;        // running max before the first visible key
+
+typedef __attribute__((ext_vector_type(2))) float f32x2;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+
+// LDS tiles keep the pool's tile layout (64-byte rows: key rows of one
+// 32-dim slice, value rows of one dim), with the four 16-byte chunks of row
+// `row` stored in the order c ^ swz(row).  One MFMA operand load reads chunk G
+// of the rows 8(r/4) + r%4 (keys) or r (values) for r = 0..15, G = 0..3; the
+// swizzle puts every 8 and every 16 consecutive lanes on distinct banks.
+__device__ inline int swz_k(int j) { return ((j >> 3) & 3) ^ (((j >> 1) & 1) << 1); }
+__device__ inline int swz_v(int e) { return ((e >> 2) & 3) ^ (((e >> 1) & 1) << 1); }
+
+// max over the four lanes r, r + 16, r + 32, r + 48 (the key rows of one column)
+__device__ inline float col_max(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const uint32_t v = __float_as_uint(y);
+  const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
 
 __device__ inline int load_status(const int32_t* status) {
   return __atomic_load_n(status, __ATOMIC_RELAXED);
@@ -59,9 +87,10 @@ struct PrefillArgs {
   const int32_t* pos;
   int32_t* list;          // [H][total]: chunk-local indices of kept tokens
   int32_t* list_cnt;      // [n * H]
+  char* tiles;            // [2][H][tph] tiles: chunk tokens, then compacted kept tokens
   float* out;             // [T, Hq, D]
   size_t page_bytes;
-  int n, H, g, w, P, log2P, maxp, max_slots, max_seqs, total, max_len, PB;
+  int n, H, g, w, P, log2P, maxp, max_slots, max_seqs, total, max_len, PB, tph;
   float scale_log2;
 };
 
@@ -92,6 +121,56 @@ __global__ __launch_bounds__(kThreads) void prefill_list_kernel(PrefillArgs a) {
   if (threadIdx.x == 0) a.list_cnt[hh] = run;
 }
 
+__device__ inline size_t ws_tile(const PrefillArgs& a, int region, int h, int i, int k) {
+  return ((static_cast<size_t>(region) * a.H + h) * a.tph + a.cu[i] / 32 + i + k);
+}
+
+// Pass 1 (one block per (32-token tile, sequence x head, region)): copy the
+// chunk's keys and values -- region 0: in chunk order; region 1: the kept
+// tokens in list order -- into workspace tiles in the pool's tile layout
+// (keys [d/32][32][32], values transposed [d][32]); rows past the end are 0.
+template <int D>
+__global__ __launch_bounds__(kThreads) void prefill_tile_kernel(PrefillArgs a) {
+  __shared__ uint16_t vrows[32][D + 2];
+  if (load_status(a.status) != 0) return;
+  const int k = blockIdx.x, hh = blockIdx.y, region = blockIdx.z;
+  const int i = hh / a.H, h = hh % a.H;
+  const int tok0 = a.cu[i], C = a.cu[i + 1] - a.cu[i];
+  const int cnt = region ? a.list_cnt[hh] : C;
+  if (k * 32 >= cnt) return;
+  const int32_t* lst = a.list + static_cast<size_t>(h) * a.total + tok0;
+  char* tile = a.tiles + ws_tile(a, region, h, i, k) * (D * 128);
+  const int tid = threadIdx.x;
+  constexpr int kPieces = 32 * D / 8;   // 16-byte pieces of 32 rows
+  for (int pc = tid; pc < kPieces; pc += kThreads) {
+    const int j = pc / (D / 8), e0 = 8 * (pc % (D / 8));
+    const int idx = 32 * k + j;
+    u32x4 kx = {0u, 0u, 0u, 0u}, vx = {0u, 0u, 0u, 0u};
+    if (idx < cnt) {
+      const int c = region ? lst[idx] : idx;
+      const size_t row = (static_cast<size_t>(tok0 + c) * a.H + h) * D + e0;
+      kx = *reinterpret_cast<const u32x4*>(a.k + row);
+      vx = *reinterpret_cast<const u32x4*>(a.v + row);
+    }
+    *reinterpret_cast<u32x4*>(tile + (e0 >> 5) * 2048 + j * 64 + (e0 & 31) * 2) = kx;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      vrows[j][e0 + 2 * e] = static_cast<uint16_t>(vx[e] & 0xFFFFu);
+      vrows[j][e0 + 2 * e + 1] = static_cast<uint16_t>(vx[e] >> 16);
+    }
+  }
+  __syncthreads();
+  // value piece q: dim q / 4, keys 8 (q % 4) .. + 7
+  for (int q = tid; q < kPieces; q += kThreads) {
+    const int e = q >> 2, j0 = 8 * (q & 3);
+    u32x4 x;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      x[t] = static_cast<uint32_t>(vrows[j0 + 2 * t][e]) | (static_cast<uint32_t>(vrows[j0 + 2 * t + 1][e]) << 16);
+    *reinterpret_cast<u32x4*>(tile + D * 64 + q * 16) = x;
+  }
+}
+
 template <int D>
 struct Frag {
   u32x4 ka[D / 32];
@@ -99,12 +178,12 @@ struct Frag {
   u32x4 vt[D / 16];
 };
 
-// Staging of one 32-key tile: each thread moves 16-byte pieces; pool tiles
-// are copied as they are, chunk keys are transposed on the way in.
+// Staging of one 32-key tile: each thread moves 16-byte pieces of a tile in
+// the pool layout (a pool page or a workspace tile) through registers.
 template <int D>
 struct Stage {
   static constexpr int kPieces = (D * 128) / 16 / kThreads;  // 16-byte pieces per thread
-  u32x4 kx[kPieces / 2];   // key pieces (chunk source) or first half (pool source)
+  u32x4 kx[kPieces / 2];   // key pieces
   u32x4 vx[kPieces / 2];   // value pieces
   uint32_t meta;           // this thread's key row (threads 0..31): position | flag << 31
 };
@@ -113,6 +192,7 @@ template <int D, int NQ>
 __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
   __shared__ __attribute__((aligned(16))) char tile_lds[2][D * 128];
   __shared__ uint32_t meta_lds[2][32];
+  __shared__ int masked_lds[2];   // tile has a key hidden from some query of the block
   if (load_status(a.status) != 0) return;
   const int hh = blockIdx.y;
   const int i = hh / a.H, h = hh % a.H;
@@ -125,18 +205,21 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
   const int L0 = a.len[sh];
   const int t0 = p0 + pb0;
   const int t1 = p0 + min(C, pb0 + a.PB);
-  const int band_lo = max(p0, t0 - a.w + 1);
+  // band: chunk tiles from the one holding max(p0, t0 - w + 1) up to t1
+  const int band_c0 = (max(0, t0 - a.w + 1 - p0) >> 5) << 5;
   // kept chunk keys strictly before the band: prefix of the sorted list
   const int32_t* lst = a.list + static_cast<size_t>(h) * a.total + tok0;
   int lo_i = 0, hi_i = a.list_cnt[hh];
   while (lo_i < hi_i) {
     const int mid = (lo_i + hi_i) >> 1;
-    if (lst[mid] < band_lo - p0) lo_i = mid + 1; else hi_i = mid;
+    if (lst[mid] < band_c0) lo_i = mid + 1; else hi_i = mid;
   }
   const int n_pre = lo_i;
   const int nc = (L0 + 31) >> 5;
   const int np = (n_pre + 31) >> 5;
-  const int nb = (t1 - band_lo + 31) >> 5;
+  const int nb = (t1 - p0 - band_c0 + 31) >> 5;
+  const char* pre_tiles = a.tiles + ws_tile(a, 1, h, i, 0) * (D * 128);
+  const char* band_tiles = a.tiles + ws_tile(a, 0, h, i, band_c0 >> 5) * (D * 128);
   const int ntiles = nc + np + nb;
   const int32_t* pt = a.page_table + static_cast<size_t>(sh) * a.maxp;
   const int32_t* smeta = a.slot_meta + static_cast<size_t>(sh) * a.max_slots;
@@ -170,86 +253,70 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
   Stage<D> stg;
   constexpr int KP = Stage<D>::kPieces / 2;
   auto stage_load = [&](int k) {
+    const char* tile;
     if (k < nc) {
       const int sb = k * 32;
-      const char* tile = a.pool + static_cast<size_t>(pt[sb >> a.log2P]) * a.page_bytes +
-                         static_cast<size_t>((sb & (a.P - 1)) >> 5) * (D * 128);
-#pragma unroll
-      for (int m = 0; m < KP; ++m) {
-        stg.kx[m] = *reinterpret_cast<const u32x4*>(tile + (tid + m * kThreads) * 16);
-        stg.vx[m] = *reinterpret_cast<const u32x4*>(tile + D * 64 + (tid + m * kThreads) * 16);
-      }
+      tile = a.pool + static_cast<size_t>(pt[sb >> a.log2P]) * a.page_bytes +
+             static_cast<size_t>((sb & (a.P - 1)) >> 5) * (D * 128);
+      if (tid < 32) stg.meta = sb + tid < L0 ? static_cast<uint32_t>(smeta[sb + tid]) : kNoKey;
+    } else if (k < nc + np) {
+      const int kk = k - nc;
+      tile = pre_tiles + static_cast<size_t>(kk) * (D * 128);
       if (tid < 32) {
-        stg.meta = sb + tid < L0 ? static_cast<uint32_t>(smeta[sb + tid]) : kNoKey;
+        const int idx = kk * 32 + tid;
+        stg.meta = idx < n_pre ? static_cast<uint32_t>(p0 + lst[idx]) : kNoKey;
       }
     } else {
-      // chunk keys: row j of the tile, 16-byte piece e8 of the row
-      const bool pre = k < nc + np;
-      const int base = pre ? (k - nc) * 32 : band_lo - p0 + (k - nc - np) * 32;
-      const int lim = pre ? n_pre : t1 - p0;   // exclusive bound (list index / chunk index)
-#pragma unroll
-      for (int m = 0; m < KP; ++m) {
-        const int pc = tid + m * kThreads;
-        const int j = pc / (D / 8), e8 = pc % (D / 8);
-        const int idx = base + j;
-        const u32x4 z = {0u, 0u, 0u, 0u};
-        if (idx < lim) {
-          const int c = pre ? lst[idx] : idx;
-          const size_t row = (static_cast<size_t>(tok0 + c) * a.H + h) * D + 8 * e8;
-          stg.kx[m] = *reinterpret_cast<const u32x4*>(a.k + row);
-          stg.vx[m] = *reinterpret_cast<const u32x4*>(a.v + row);
-        } else {
-          stg.kx[m] = z;
-          stg.vx[m] = z;
-        }
-      }
+      const int kb = k - nc - np;
+      tile = band_tiles + static_cast<size_t>(kb) * (D * 128);
       if (tid < 32) {
-        const int idx = base + tid;
-        if (idx < lim) {
-          const int c = pre ? lst[idx] : idx;
-          const uint32_t f = pre ? 0u : (a.flags[static_cast<size_t>(tok0 + c) * a.H + h] ? kFlagBit : 0u);
-          stg.meta = static_cast<uint32_t>(p0 + c) | f;
-        } else {
-          stg.meta = kNoKey;
-        }
+        const int c = band_c0 + kb * 32 + tid;
+        stg.meta = c < t1 - p0 ? (static_cast<uint32_t>(p0 + c) |
+                                  (a.flags[static_cast<size_t>(tok0 + c) * a.H + h] ? kFlagBit : 0u))
+                               : kNoKey;
       }
+    }
+#pragma unroll
+    for (int m = 0; m < KP; ++m) {
+      stg.kx[m] = *reinterpret_cast<const u32x4*>(tile + (tid + m * kThreads) * 16);
+      stg.vx[m] = *reinterpret_cast<const u32x4*>(tile + D * 64 + (tid + m * kThreads) * 16);
     }
   };
   auto stage_store = [&](int k, int buf) {
     char* dst = tile_lds[buf];
-    if (k < nc) {
-      const int valid = min(32, L0 - k * 32);
+    // pool slots past L hold stale data: their value elements are zeroed
+    // (workspace tiles are zero past their last row)
+    const int valid = k < nc ? min(32, L0 - k * 32) : 32;
 #pragma unroll
-      for (int m = 0; m < KP; ++m) {
-        const int off = (tid + m * kThreads) * 16;
-        *reinterpret_cast<u32x4*>(dst + off) = stg.kx[m];
-        u32x4 x = stg.vx[m];
-        // value elements of rows >= valid are zeroed (pool slots past L hold
-        // stale data); element i of the piece is row (off % 64) / 2 + i
-        const int j0 = (off & 63) >> 1;
-        if (j0 + 8 > valid) {
+    for (int m = 0; m < KP; ++m) {
+      const int off = (tid + m * kThreads) * 16;
+      const int row = (off & 2047) >> 6, ch = (off & 63) >> 4;
+      *reinterpret_cast<u32x4*>(dst + (off & ~63) + ((ch ^ swz_k(row)) << 4)) = stg.kx[m];
+      u32x4 x = stg.vx[m];
+      // element i of the piece is key row (off % 64) / 2 + i
+      const int j0 = (off & 63) >> 1;
+      if (j0 + 8 > valid) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (j0 + e >= valid) x[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-        }
-        *reinterpret_cast<u32x4*>(dst + D * 64 + off) = x;
+        for (int e = 0; e < 8; ++e)
+          if (j0 + e >= valid) x[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
       }
-    } else {
-#pragma unroll
-      for (int m = 0; m < KP; ++m) {
-        const int pc = tid + m * kThreads;
-        const int j = pc / (D / 8), e8 = pc % (D / 8);
-        const int e0 = 8 * e8;
-        *reinterpret_cast<u32x4*>(dst + (e0 >> 5) * 2048 + j * 64 + (e0 & 31) * 2) = stg.kx[m];
-        const u32x4 x = stg.vx[m];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const uint16_t val = static_cast<uint16_t>((e & 1) ? (x[e >> 1] >> 16) : (x[e >> 1] & 0xFFFFu));
-          *reinterpret_cast<uint16_t*>(dst + D * 64 + (e0 + e) * 64 + j * 2) = val;
-        }
-      }
+      const int vrow = off >> 6;
+      *reinterpret_cast<u32x4*>(dst + D * 64 + (off & ~63) + ((ch ^ swz_v(vrow)) << 4)) = x;
     }
-    if (tid < 32) meta_lds[buf][tid] = stg.meta;
+    if (tid < 64) {
+      // a key row needs the per-element mask iff some query t in [t0, t1)
+      // does not see it: padding, causal (position > t0) or flagged and
+      // expiring by t1 - 1
+      bool need = false;
+      if (tid < 32) {
+        const uint32_t mt = stg.meta;
+        const int kp = static_cast<int>(mt & ~kFlagBit);
+        need = mt == kNoKey || kp > t0 || ((mt & kFlagBit) && kp + a.w <= t1 - 1);
+        meta_lds[buf][tid] = mt;
+      }
+      const uint64_t any = __builtin_amdgcn_ballot_w64(need);
+      if (tid == 0) masked_lds[buf] = any != 0;
+    }
   };
 
   // ---- accumulators
@@ -259,11 +326,13 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
   for (int qb = 0; qb < NQ; ++qb) {
 #pragma unroll
     for (int b = 0; b < D / 16; ++b) o[qb][b] = f32x4{0.f, 0.f, 0.f, 0.f};
-    m_ref[qb] = -INFINITY;
+    m_ref[qb] = kMInit;
     l_run[qb] = 0.f;
   }
-  const uint32_t lo_k = static_cast<uint32_t>((8 * (r >> 2) + (r & 3)) * 64 + 16 * G);
-  const uint32_t lo_v = static_cast<uint32_t>(D * 64 + r * 64 + 16 * G);
+  const int krow = 8 * (r >> 2) + (r & 3);
+  const uint32_t lo_k = static_cast<uint32_t>(krow * 64 + ((G ^ swz_k(krow)) << 4));
+  const uint32_t lo_v = static_cast<uint32_t>(D * 64 + r * 64 + ((G ^ swz_v(r)) << 4));
+  const float thr = kRescale / a.scale_log2;   // rescale threshold in score units
 
   if (ntiles > 0) {
     stage_load(0);
@@ -283,9 +352,16 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
     }
 #pragma unroll
     for (int b = 0; b < D / 16; ++b) f.vt[b] = *reinterpret_cast<const u32x4*>(tl + lo_v + b * 1024);
-    uint32_t km[8];
+    const bool masked = __builtin_amdgcn_readfirstlane(masked_lds[buf]) != 0;
+    int kp[8], kx[8];   // key position and expiry (first query that no longer sees it)
+    if (masked) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) km[j] = meta_lds[buf][8 * G + j];
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t km = meta_lds[buf][8 * G + j];
+        kp[j] = static_cast<int>(km & ~kFlagBit);
+        kx[j] = (km & kFlagBit) ? kp[j] + a.w : 0x7FFFFFFF;
+      }
+    }
 #pragma unroll
     for (int qb = 0; qb < NQ; ++qb) {
       f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
@@ -294,40 +370,46 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
         s0 = mfma_bf16(f.ka[s2], qf[qb][s2], s0);
         s1 = mfma_bf16(f.kb[s2], qf[qb][s2], s1);
       }
-      const int t = tcol[qb];
       float sc[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float raw = j < 4 ? s0[j] : s1[j - 4];
-        const int kp = static_cast<int>(km[j] & ~kFlagBit);
-        const bool kflag = (km[j] & kFlagBit) != 0;
-        const bool vis = (t >= 0) && (km[j] != kNoKey) && kp <= t && (kp > t - a.w || !kflag);
-        sc[j] = vis ? raw * a.scale_log2 : -INFINITY;
+      for (int j = 0; j < 4; ++j) {
+        sc[j] = s0[j];
+        sc[j + 4] = s1[j];
+      }
+      if (masked) {
+        const int t = tcol[qb];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) sc[j] = (kp[j] <= t && t < kx[j]) ? sc[j] : -INFINITY;
       }
       float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
                        fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const bool raise = mx > m_ref[qb] + kRescale;   // false while mx is -inf
+      mx = col_max(mx);
+      const bool raise = mx > m_ref[qb] + thr;   // false while the column has seen no key
       if (__builtin_amdgcn_ballot_w64(raise)) {
         const float m_new = raise ? mx : m_ref[qb];
-        const float alpha = m_ref[qb] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_ref[qb] - m_new);
+        const float alpha = __builtin_amdgcn_exp2f((m_ref[qb] - m_new) * a.scale_log2);
         l_run[qb] *= alpha;
 #pragma unroll
         for (int b = 0; b < D / 16; ++b) o[qb][b] *= alpha;
         m_ref[qb] = m_new;
       }
-      bf16x8 p;
-      float psum = 0.f;
+      // p = 2^((s - m) * scale); hidden keys give exactly 0
+      const float mb = m_ref[qb] * a.scale_log2;
+      float e[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float e = sc[j] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sc[j] - m_ref[qb]);
-        const __bf16 pb = static_cast<__bf16>(e);
-        p[j] = pb;
-        psum += static_cast<float>(pb);
+      for (int j = 0; j < 8; ++j) e[j] = __builtin_amdgcn_exp2f(fmaf(sc[j], a.scale_log2, -mb));
+      // P is rounded to bf16 for the MFMA; the denominator adds the same
+      // rounded values (dot with (1, 1)), so a single dominant key returns
+      // its value row exactly
+      u32x4 pu;
+      const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x2 pr = {e[2 * j], e[2 * j + 1]};
+        const bf16x2 pb = __builtin_convertvector(pr, bf16x2);
+        pu[j] = __builtin_bit_cast(uint32_t, pb);
+        l_run[qb] = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, l_run[qb], false);
       }
-      l_run[qb] += psum;
-      const u32x4 pu = __builtin_bit_cast(u32x4, p);
 #pragma unroll
       for (int b = 0; b < D / 16; ++b) o[qb][b] = mfma_bf16(f.vt[b], pu, o[qb][b]);
     }
@@ -378,6 +460,8 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   a.pos = ls.pos;
   a.list = reinterpret_cast<int32_t*>(w + lo.ws_pf_meta);
   a.list_cnt = reinterpret_cast<int32_t*>(w + lo.ws_pf_cum);
+  a.tiles = w + lo.ws_pf_tiles;
+  a.tph = lo.pf_tiles_per_head;
   a.out = out;
   a.page_bytes = lo.page_bytes;
   a.n = n;
@@ -394,11 +478,16 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   a.PB = 4 * kNQ * (16 / c.group_size);
   a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
   const int NH = n * c.num_kv_heads;
+  // the timing events bracket all three passes
+  if (ev_start) (void)hipEventRecord(ev_start, st);
   hipLaunchKernelGGL(prefill_list_kernel, dim3(NH), dim3(kThreads), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(prefill_tile_kernel<D>, dim3((max_len + 31) / 32, NH, 2), dim3(kThreads), 0,
+                     st, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
   dim3 grid((max_len + a.PB - 1) / a.PB, NH);
-  if (ev_start) (void)hipEventRecord(ev_start, st);
   hipLaunchKernelGGL((prefill_kernel<D, kNQ>), grid, dim3(kThreads), 0, st, a);
   e = hipGetLastError();
   if (ev_stop) (void)hipEventRecord(ev_stop, st);
