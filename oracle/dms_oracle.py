@@ -40,6 +40,19 @@ notes):
 * Softmax scale 1/sqrt(head_dim); query head q reads KV head q // group.
 * A call that would pop more pages than the stack holds fails as a whole
   (OutOfPages) and changes nothing.
+
+Decisions at inference and the eviction-timing ablation:
+
+* Sec. 3.2 rounds the decision to alpha_bin = round(sigmoid(logit)).  The
+  logit of a token for one KV head is the first neuron of the first query
+  head of its group plus the offset b (App. C borrows that neuron; Sec. 3.1
+  adds b, -5 in training).  After the decision is read, App. C sets that
+  neuron to 0 for attention.  Readings: the logit is formed in float32 from
+  the bf16 query value; sigmoid(0) = 1/2 rounds to 0 (the token is kept).
+* Immediate eviction (Sec. 5.3 ablation): the decision made at step t + w
+  evicts token t at that step, so key j is hidden from query t iff
+  j + w <= t and alpha_{j+w} = 1.  In the replay, token t takes token
+  t - w's slot iff t >= w and token t's own decision is 1.
 """
 from __future__ import annotations
 
@@ -49,7 +62,8 @@ from dataclasses import dataclass
 import numpy as np
 
 __all__ = [
-    "visible", "visibility_mask", "additive_mask", "retained_count",
+    "visible", "visible_immediate", "visibility_mask", "additive_mask", "retained_count",
+    "alpha_bin", "query_decisions", "zero_borrowed_neuron",
     "masked_attention", "dense_dms_attention", "dense_dms_attention_head",
     "OutOfPages", "PagedKVOracle",
 ]
@@ -67,12 +81,29 @@ def visible(t, j, flag_j, w):
     return (j <= t) & ((j > t - w) | (flag_j == 0))
 
 
-def visibility_mask(flags: np.ndarray, w: int) -> np.ndarray:
+def visible_immediate(t, j, alpha, w):
+    """Key j visible to query t under immediate eviction (Sec. 5.3): the
+    decision alpha_{j+w}, made at step j + w, evicts token j at that step.
+
+    alpha holds the decisions of positions 0 .. T-1 (T > t); elementwise over
+    arrays of t and j.
+    """
+    alpha = np.asarray(alpha)
+    j = np.asarray(j)
+    at = j + w
+    decided = at <= t
+    evicted = decided & (alpha[np.clip(at, 0, alpha.shape[0] - 1)] == 1)
+    return (j <= t) & ~evicted
+
+
+def visibility_mask(flags: np.ndarray, w: int, mode: str = "delayed") -> np.ndarray:
     """Boolean [T, T] mask, row = query position, column = key position."""
     flags = np.asarray(flags)
     T = flags.shape[0]
     t = np.arange(T)[:, None]
     j = np.arange(T)[None, :]
+    if mode == "immediate":
+        return np.asarray(visible_immediate(t, j, flags, w), dtype=bool)
     return np.asarray(visible(t, j, flags[None, :], w), dtype=bool)
 
 
@@ -92,9 +123,41 @@ def additive_mask(alpha: np.ndarray, w: int) -> np.ndarray:
     return m
 
 
-def retained_count(flags: np.ndarray, w: int, t: int) -> int:
+def retained_count(flags: np.ndarray, w: int, t: int, mode: str = "delayed") -> int:
     """Number of keys visible to query t, counted straight from the predicate."""
+    if mode == "immediate":
+        return sum(1 for j in range(t + 1) if visible_immediate(t, j, flags, w))
     return sum(1 for j in range(t + 1) if visible(t, j, int(flags[j]), w))
+
+
+# ----------------------------------------------------------------------------
+# Decisions from the borrowed query neuron (Sec. 3.2 rounding, App. C)
+# ----------------------------------------------------------------------------
+
+def alpha_bin(logit):
+    """round(sigmoid(logit)) in {0, 1}.  sigmoid is increasing and equals 1/2
+    at 0, so the rounded value is 1 exactly when logit > 0; the tie (logit 0)
+    keeps the token."""
+    return (np.asarray(logit) > 0).astype(np.uint8)
+
+
+def query_decisions(q, group, bias):
+    """Decisions of tokens for every KV head from their queries.
+
+    q [..., Hq, d] (bf16 values as floats): KV head h reads element 0 of query
+    head h * group (the first head of its group) and adds the offset b; the
+    sum is formed in float32.  Returns uint8 [..., Hq // group].
+    """
+    first = np.asarray(q)[..., ::group, 0].astype(np.float32)
+    return alpha_bin(first + np.float32(bias))
+
+
+def zero_borrowed_neuron(q, group):
+    """Copy of q [..., Hq, d] with element 0 of the first query head of every
+    group set to 0 (App. C: the neuron no longer takes part in attention)."""
+    q = np.array(q, dtype=np.float64, copy=True)
+    q[..., ::group, 0] = 0.0
+    return q
 
 
 # ----------------------------------------------------------------------------
@@ -117,13 +180,15 @@ def masked_attention(q, k, v, mask, scale) -> np.ndarray:
     return (p @ v) / p.sum(axis=1, keepdims=True)
 
 
-def dense_dms_attention_head(q_rows, k_hist, v_hist, flags_hist, w, t_query, scale=None):
+def dense_dms_attention_head(q_rows, k_hist, v_hist, flags_hist, w, t_query, scale=None,
+                             mode="delayed"):
     """One KV head, its query group, several query positions, full history.
 
     q_rows [Nq, g, d]: the g query heads of the group at each query position.
     k_hist, v_hist [T, d]: keys / values of positions 0 .. T-1 of this head.
     flags_hist [T]: binary decision of each position.
     t_query [Nq]: position of each query (< T).
+    mode: "delayed" (Sec. 3.1) or "immediate" (Sec. 5.3 ablation).
     Returns [Nq, g, d] float64.
     """
     q_rows = np.asarray(q_rows, np.float64)
@@ -135,13 +200,16 @@ def dense_dms_attention_head(q_rows, k_hist, v_hist, flags_hist, w, t_query, sca
     out = np.empty((Nq, g, d))
     j = np.arange(T)
     for i, t in enumerate(np.asarray(t_query)):
-        row = np.asarray(visible(t, j, flags_hist, w), dtype=bool)
+        if mode == "immediate":
+            row = np.asarray(visible_immediate(t, j, flags_hist, w), dtype=bool)
+        else:
+            row = np.asarray(visible(t, j, flags_hist, w), dtype=bool)
         out[i] = masked_attention(q_rows[i], k_hist, v_hist,
                                   np.broadcast_to(row, (g, T)), scale)
     return out
 
 
-def dense_dms_attention(q, k, v, flags, w, group, t_query=None, scale=None):
+def dense_dms_attention(q, k, v, flags, w, group, t_query=None, scale=None, mode="delayed"):
     """One sequence, all heads.  q [Nq, Hq, d] at positions t_query (default
     0..Nq-1), k / v [T, Hkv, d], flags [T, Hkv].  Returns [Nq, Hq, d]."""
     q = np.asarray(q, np.float64)
@@ -153,7 +221,7 @@ def dense_dms_attention(q, k, v, flags, w, group, t_query=None, scale=None):
     for h in range(Hkv):
         out[:, h * group:(h + 1) * group] = dense_dms_attention_head(
             q[:, h * group:(h + 1) * group], np.asarray(k)[:, h], np.asarray(v)[:, h],
-            np.asarray(flags)[:, h], w, t_query, scale)
+            np.asarray(flags)[:, h], w, t_query, scale, mode)
     return out
 
 
@@ -189,12 +257,17 @@ class PagedKVOracle:
       slot_pos[s, h, slot]      position of the token held by a live slot
       slot_flag[s, h, slot]     its decision
     With ``store_values`` the K / V rows of every live slot are kept too.
+    mode "delayed": token t reuses token t - w's slot iff that token's own
+    decision was 1; mode "immediate": iff token t's decision is 1.
     """
 
     def __init__(self, max_seqs, num_kv_heads, window, page_size, num_pages,
-                 max_pages_per_head, head_dim, store_values=True):
+                 max_pages_per_head, head_dim, store_values=True, mode="delayed"):
         if window < 1:
             raise ValueError("window must be >= 1")
+        if mode not in ("delayed", "immediate"):
+            raise ValueError("mode must be 'delayed' or 'immediate'")
+        self.mode = mode
         self.dims = _Dims(max_seqs, num_kv_heads, window, page_size, num_pages,
                           max_pages_per_head, head_dim)
         S, H, w = max_seqs, num_kv_heads, window
@@ -248,7 +321,10 @@ class PagedKVOracle:
             f = np.stack([flags_all[i][c] for i in act])   # [na, H]
             prev_slot = ring_slot[s[:, None], hs[None, :], e[:, None]]
             prev_flag = ring_flag[s[:, None], hs[None, :], e[:, None]]
-            reuse = (t >= w)[:, None] & (prev_flag == 1)   # token t-w was flagged
+            if self.mode == "immediate":
+                reuse = (t >= w)[:, None] & (f == 1)        # token t evicts token t-w now
+            else:
+                reuse = (t >= w)[:, None] & (prev_flag == 1)   # token t-w was flagged
             slot = np.where(reuse, prev_slot, L[s])
             fresh = ~reuse
             if np.any(slot >= D.max_pages_per_head * P):
