@@ -89,7 +89,37 @@ typedef struct dms_config {
   int32_t max_pages_per_head; /* page-table length of one (seq, head) */
   int32_t max_chunk_tokens;   /* largest total token count of one chunk call */
   float softmax_scale;        /* <= 0 selects 1 / sqrt(head_dim) */
+  int32_t eviction;           /* DMS_EVICT_DELAYED (0, the method) or
+                                 DMS_EVICT_IMMEDIATE (1, the Sec. 5.3 ablation) */
+  int32_t decision_source;    /* DMS_DECIDE_CALLER (0) or DMS_DECIDE_QUERY (1) */
+  float decision_bias;        /* b added to the borrowed neuron (DMS_DECIDE_QUERY);
+                                 -5 is the paper's training offset */
 } dms_config;
+
+/*
+ * Eviction timing (dms_config.eviction).
+ *   DMS_EVICT_DELAYED: token t's own decision alpha_t evicts it at step t + w
+ *     (Sec. 3.1 "Delayed Eviction via Sliding Window").
+ *   DMS_EVICT_IMMEDIATE: the decision made at step t + w evicts token t at
+ *     that step (Sec. 5.3, the ablation the paper compares against): key j
+ *     is visible to query t iff j <= t and (j > t - w or alpha_{j+w} = 0).
+ *     In the cache, token t takes token t - w's slot iff alpha_t = 1.
+ *
+ * Where decisions come from (dms_config.decision_source).
+ *   DMS_DECIDE_CALLER: the caller passes flags (uint8, 0 = keep) to
+ *     dms_append, dms_decode_step, dms_append_chunk and dms_prefill_chunk.
+ *   DMS_DECIDE_QUERY: the decision of a token for KV head h is read from its
+ *     query, as in App. C: alpha = round(sigmoid(x)) = (x > 0), with
+ *     x = q[first query head of the group, h * g][element 0] + decision_bias,
+ *     formed in float32 from the bf16 query (a tie, x = 0, keeps the token);
+ *     that element is then treated as 0 by every attention call (App. C
+ *     removes the borrowed neuron from attention).  Calls with a query use
+ *     dms_decode_step_q / dms_prefill_chunk_q (dms_decode_step and
+ *     dms_prefill_chunk return DMS_ERR_INVALID, and vice versa); appends
+ *     without a query (dms_append, dms_append_chunk) still take flags.
+ */
+enum { DMS_EVICT_DELAYED = 0, DMS_EVICT_IMMEDIATE = 1 };
+enum { DMS_DECIDE_CALLER = 0, DMS_DECIDE_QUERY = 1 };
 
 typedef struct dms_ctx dms_ctx;
 
@@ -159,7 +189,8 @@ int dms_seq_reset(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, vo
  * management).  For each (sequence, KV head), with t = pos:
  *   if t >= w and the token at t - w was flagged, the new token takes that
  *   token's slot (the flagged token leaves the cache now, w steps after its
- *   decision); otherwise it takes the next fresh slot L (L += 1), popping a
+ *   decision; with DMS_EVICT_IMMEDIATE: if the new token is flagged);
+ *   otherwise it takes the next fresh slot L (L += 1), popping a
  *   page when that slot starts a page.  Pops follow call order, then head.
  * Then the ring remembers (slot, flag) for position t and pos += 1.
  * k_dev, v_dev: bf16 [n, Hkv, d]; flags_dev: uint8 [n, Hkv]. */
@@ -167,7 +198,8 @@ int dms_append(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
                const void* k_dev, const void* v_dev, const uint8_t* flags_dev,
                void* stream);
 
-/* Decode attention of one layer over the current cache: every query head
+/* Decode attention of one layer over the current cache (with
+ * DMS_DECIDE_QUERY the borrowed neuron of q is treated as 0): every query head
  * attends to all live slots of its KV head, which are exactly the keys
  * visible to the latest position (decode reads only retained tokens; the
  * cost is the KV bytes read, Sec. 1 and Appendix I).  Split over the
@@ -182,6 +214,14 @@ int dms_decode(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
 int dms_decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
                     const void* q_dev, const void* k_dev, const void* v_dev,
                     const uint8_t* flags_dev, float* out_dev, void* stream);
+
+/* dms_decode_step with decisions read from the queries (DMS_DECIDE_QUERY
+ * only): the decision of each (sequence, KV head) comes from q_dev as
+ * described above, and is also written to decisions_out_dev (uint8 [n, Hkv],
+ * may be NULL). */
+int dms_decode_step_q(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+                      const void* q_dev, const void* k_dev, const void* v_dev,
+                      uint8_t* decisions_out_dev, float* out_dev, void* stream);
 
 /* Append a chunk of tokens per sequence with no attention: the result equals
  * appending them one by one in position order, except that page pops of the
@@ -208,6 +248,14 @@ int dms_prefill_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev
                       const int32_t* cu_seqlens_dev, int total_tokens, int max_seqlen,
                       const void* q_dev, const void* k_dev, const void* v_dev,
                       const uint8_t* flags_dev, float* out_dev, void* stream);
+
+/* dms_prefill_chunk with decisions read from the queries (DMS_DECIDE_QUERY
+ * only); the decisions taken are also written to decisions_out_dev (uint8
+ * [total_tokens, Hkv], may be NULL). */
+int dms_prefill_chunk_q(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+                        const int32_t* cu_seqlens_dev, int total_tokens, int max_seqlen,
+                        const void* q_dev, const void* k_dev, const void* v_dev,
+                        uint8_t* decisions_out_dev, float* out_dev, void* stream);
 
 /* Retained lengths L of the listed sequences of one layer (the paper's
  * per-step "KV-cache token reads", Sec. 5.1): out_dev int32 [n, Hkv]. */

@@ -21,6 +21,10 @@ int validate_config(const dms_config& c) {
   if (c.num_pages < 1 || c.max_pages_per_head < 1 || c.max_chunk_tokens < 0) return DMS_ERR_INVALID;
   if (!(c.softmax_scale <= 0.0f || isfinite(c.softmax_scale))) return DMS_ERR_INVALID;
   if (isnan(c.softmax_scale)) return DMS_ERR_INVALID;
+  if (c.eviction != DMS_EVICT_DELAYED && c.eviction != DMS_EVICT_IMMEDIATE) return DMS_ERR_INVALID;
+  if (c.decision_source != DMS_DECIDE_CALLER && c.decision_source != DMS_DECIDE_QUERY)
+    return DMS_ERR_INVALID;
+  if (c.decision_source == DMS_DECIDE_QUERY && !isfinite(c.decision_bias)) return DMS_ERR_INVALID;
   // slot and page indices are int32 on the device
   if (static_cast<int64_t>(c.max_pages_per_head) * c.page_size >= (int64_t(1) << 31)) return DMS_ERR_INVALID;
   if (static_cast<int64_t>(c.max_seqs) * c.num_kv_heads > (int64_t(1) << 22)) return DMS_ERR_INVALID;
@@ -74,6 +78,7 @@ Layout make_layout(const dms_config& c) {
   // tile layout; sequence i of a call starts at tile cu[i] / 32 + i
   lo.pf_tiles_per_head = static_cast<int>((static_cast<size_t>(c.max_chunk_tokens) + 31) / 32 + S + 1);
   lo.ws_pf_tiles = take(2 * H * static_cast<size_t>(lo.pf_tiles_per_head) * D * 128);
+  lo.ws_pf_flags = take(static_cast<size_t>(c.max_chunk_tokens) * H);  // decisions from q
   lo.workspace_bytes = off;
   return lo;
 }
@@ -226,7 +231,7 @@ int dms_append(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const
   const Ctx& c = ctx->c;
   hipStream_t st = as_stream(stream);
   hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, flags_dev,
-                                  true, 0, nullptr, st);
+                                  nullptr, nullptr, true, 0, nullptr, st);
   if (e == hipSuccess)
     e = dms::launch_scatter(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, k_dev, v_dev, st);
   return hip_rc(e);
@@ -241,7 +246,7 @@ int dms_decode(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const
   const Ctx& c = ctx->c;
   hipStream_t st = as_stream(stream);
   hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, nullptr,
-                                  false, c.decode_waves, out_dev, st);
+                                  nullptr, nullptr, false, c.decode_waves, out_dev, st);
   hipEvent_t e0, e1;
   next_events(ctx->c, DMS_PROFILE_DECODE, &e0, &e1);
   if (e == hipSuccess)
@@ -250,25 +255,83 @@ int dms_decode(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const
   return hip_rc(e);
 }
 
-int dms_decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const void* q_dev,
-                    const void* k_dev, const void* v_dev, const uint8_t* flags_dev,
-                    float* out_dev, void* stream) {
-  int rc = check_call(ctx, layer, n, seq_ids_dev);
-  if (rc) return rc;
-  if (!q_dev || !k_dev || !v_dev || !flags_dev || !out_dev) return DMS_ERR_INVALID;
-  if ((rc = ensure_waves(ctx))) return rc;
+namespace {
+
+// Append + decode of one layer; decisions from flags_dev (caller) or from
+// q_dev (decisions_out_dev receives them, may be null).
+int decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const void* q_dev,
+                const void* k_dev, const void* v_dev, const uint8_t* flags_dev,
+                uint8_t* decisions_out_dev, float* out_dev, void* stream) {
+  const bool from_q = ctx->c.cfg.decision_source == DMS_DECIDE_QUERY;
   const Ctx& c = ctx->c;
   hipStream_t st = as_stream(stream);
   // planner (slot choice, page pops, state, wave ranges) -> decode, which
   // also writes the new K / V into their slots and merges split heads
-  hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, flags_dev,
-                                  true, c.decode_waves, out_dev, st);
+  hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev,
+                                  from_q ? nullptr : flags_dev, from_q ? q_dev : nullptr,
+                                  decisions_out_dev, true, c.decode_waves, out_dev, st);
   hipEvent_t e0, e1;
   next_events(ctx->c, DMS_PROFILE_DECODE, &e0, &e1);
   if (e == hipSuccess)
     e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, k_dev,
                            v_dev, out_dev, c.decode_waves, st, e0, e1);
   return hip_rc(e);
+}
+
+// Masked chunk attention then commit; decisions from flags_dev or from q_dev
+// (written to decisions_out_dev, or to the workspace when that is null).
+int prefill_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+                  const int32_t* cu_seqlens_dev, int total_tokens, int max_seqlen,
+                  const void* q_dev, const void* k_dev, const void* v_dev,
+                  const uint8_t* flags_dev, uint8_t* decisions_out_dev, float* out_dev,
+                  void* stream) {
+  const Ctx& c = ctx->c;
+  hipStream_t st = as_stream(stream);
+  hipError_t e = hipSuccess;
+  const uint8_t* flags = flags_dev;
+  if (c.cfg.decision_source == DMS_DECIDE_QUERY) {
+    uint8_t* buf = decisions_out_dev != nullptr
+                       ? decisions_out_dev
+                       : reinterpret_cast<uint8_t*>(static_cast<char*>(c.ws) + c.lo.ws_pf_flags);
+    e = dms::launch_prefill_decide(c.cfg, q_dev, total_tokens, buf, st);
+    flags = buf;
+  }
+  hipEvent_t e0, e1;
+  next_events(ctx->c, DMS_PROFILE_PREFILL, &e0, &e1);
+  if (e == hipSuccess)
+    e = dms::launch_prefill_attention(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n,
+                                      seq_ids_dev, cu_seqlens_dev, total_tokens, max_seqlen, q_dev,
+                                      k_dev, v_dev, flags, out_dev, st, e0, e1);
+  if (e == hipSuccess)
+    e = dms::launch_chunk_commit(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, seq_ids_dev,
+                                 cu_seqlens_dev, total_tokens, max_seqlen, k_dev, v_dev, flags, st);
+  return hip_rc(e);
+}
+
+}  // namespace
+
+int dms_decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const void* q_dev,
+                    const void* k_dev, const void* v_dev, const uint8_t* flags_dev,
+                    float* out_dev, void* stream) {
+  int rc = check_call(ctx, layer, n, seq_ids_dev);
+  if (rc) return rc;
+  if (ctx->c.cfg.decision_source != DMS_DECIDE_CALLER) return DMS_ERR_INVALID;
+  if (!q_dev || !k_dev || !v_dev || !flags_dev || !out_dev) return DMS_ERR_INVALID;
+  if ((rc = ensure_waves(ctx))) return rc;
+  return decode_step(ctx, layer, n, seq_ids_dev, q_dev, k_dev, v_dev, flags_dev, nullptr, out_dev,
+                     stream);
+}
+
+int dms_decode_step_q(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+                      const void* q_dev, const void* k_dev, const void* v_dev,
+                      uint8_t* decisions_out_dev, float* out_dev, void* stream) {
+  int rc = check_call(ctx, layer, n, seq_ids_dev);
+  if (rc) return rc;
+  if (ctx->c.cfg.decision_source != DMS_DECIDE_QUERY) return DMS_ERR_INVALID;
+  if (!q_dev || !k_dev || !v_dev || !out_dev) return DMS_ERR_INVALID;
+  if ((rc = ensure_waves(ctx))) return rc;
+  return decode_step(ctx, layer, n, seq_ids_dev, q_dev, k_dev, v_dev, nullptr, decisions_out_dev,
+                     out_dev, stream);
 }
 
 int dms_append_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
@@ -292,22 +355,26 @@ int dms_prefill_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev
                       const uint8_t* flags_dev, float* out_dev, void* stream) {
   int rc = check_call(ctx, layer, n, seq_ids_dev);
   if (rc) return rc;
+  if (ctx->c.cfg.decision_source != DMS_DECIDE_CALLER) return DMS_ERR_INVALID;
   if ((rc = check_chunk(ctx, cu_seqlens_dev, total_tokens, max_seqlen))) return rc;
   if (total_tokens == 0) return DMS_OK;
   if (!q_dev || !k_dev || !v_dev || !flags_dev || !out_dev) return DMS_ERR_INVALID;
-  const Ctx& c = ctx->c;
-  hipStream_t st = as_stream(stream);
-  hipEvent_t e0, e1;
-  next_events(ctx->c, DMS_PROFILE_PREFILL, &e0, &e1);
-  hipError_t e = dms::launch_prefill_attention(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer,
-                                               n, seq_ids_dev, cu_seqlens_dev, total_tokens,
-                                               max_seqlen, q_dev, k_dev, v_dev, flags_dev,
-                                               out_dev, st, e0, e1);
-  if (e == hipSuccess)
-    e = dms::launch_chunk_commit(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, seq_ids_dev,
-                                 cu_seqlens_dev, total_tokens, max_seqlen, k_dev, v_dev,
-                                 flags_dev, st);
-  return hip_rc(e);
+  return prefill_chunk(ctx, layer, n, seq_ids_dev, cu_seqlens_dev, total_tokens, max_seqlen, q_dev,
+                       k_dev, v_dev, flags_dev, nullptr, out_dev, stream);
+}
+
+int dms_prefill_chunk_q(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+                        const int32_t* cu_seqlens_dev, int total_tokens, int max_seqlen,
+                        const void* q_dev, const void* k_dev, const void* v_dev,
+                        uint8_t* decisions_out_dev, float* out_dev, void* stream) {
+  int rc = check_call(ctx, layer, n, seq_ids_dev);
+  if (rc) return rc;
+  if (ctx->c.cfg.decision_source != DMS_DECIDE_QUERY) return DMS_ERR_INVALID;
+  if ((rc = check_chunk(ctx, cu_seqlens_dev, total_tokens, max_seqlen))) return rc;
+  if (total_tokens == 0) return DMS_OK;
+  if (!q_dev || !k_dev || !v_dev || !out_dev) return DMS_ERR_INVALID;
+  return prefill_chunk(ctx, layer, n, seq_ids_dev, cu_seqlens_dev, total_tokens, max_seqlen, q_dev,
+                       k_dev, v_dev, nullptr, decisions_out_dev, out_dev, stream);
 }
 
 int dms_retained_lengths(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,

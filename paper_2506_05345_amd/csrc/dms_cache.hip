@@ -149,7 +149,12 @@ struct PlanArgs {
   LayerState st;
   int32_t* status;
   const int32_t* seq_ids;
-  const uint8_t* flags;  // [n, H] or null when not appending
+  const uint8_t* flags;  // [n, H] caller decisions, or null
+  const uint16_t* q;     // [n, Hq, D] bf16: decisions from the borrowed neuron, or null
+  uint8_t* flags_out;    // nullable: decisions taken from q
+  float bias;            // offset added to the borrowed neuron
+  int immediate;         // eviction timing: token t's own decision frees t - w's slot
+  int g, D;
   HeadDesc* desc;        // [n*H]
   int32_t* cum_tiles;    // [n*H + 1]
   int32_t* wave_bounds;  // [W + 1] first tile of every decode wave
@@ -180,8 +185,26 @@ __device__ void wave_ranges(const int32_t* cum, int NH, int W, int32_t* bounds,
   }
 }
 
+// Decision of the token appended for call head hh: the caller's flag, or
+// round(sigmoid(x)) = (x > 0) with x = bf16 element 0 of the first query
+// head of the group plus the offset, in float32 (Sec. 3.2, App. C).
+__device__ inline int decision(const PlanArgs& a, int hh) {
+  if (a.q == nullptr) return a.flags[hh] != 0;
+  const int i = hh / a.H, h = hh % a.H;
+  const uint32_t bits = a.q[(static_cast<size_t>(i) * a.H + h) * a.g * a.D];
+  return (__uint_as_float(bits << 16) + a.bias) > 0.f;
+}
+
+// Whether the incoming token takes the slot of the token that entered w
+// steps ago (ring entry e): delayed eviction -- that token was flagged;
+// immediate eviction -- the incoming token's decision evicts it now.
+__device__ inline bool takes_slot(const PlanArgs& a, int t, int32_t e, int f) {
+  if (t < a.w) return false;
+  return a.immediate ? f != 0 : (static_cast<uint32_t>(e) & kFlagBit) != 0;
+}
+
 struct HeadStep {
-  int sh, t, slot, reuse;
+  int sh, t, slot, reuse, f;
 };
 
 __device__ inline HeadStep r1_step(const PlanArgs& a, int hh) {
@@ -189,10 +212,9 @@ __device__ inline HeadStep r1_step(const PlanArgs& a, int hh) {
   const int s = a.seq_ids[hh / a.H];
   r.sh = s * a.H + hh % a.H;
   r.t = a.st.pos[s];
+  r.f = decision(a, hh);
   const int32_t e = a.st.ring[static_cast<size_t>(r.sh) * a.w + r.t % a.w];
-  // the token that entered w steps ago leaves now if it was flagged; the
-  // incoming token takes its slot
-  r.reuse = (r.t >= a.w) && (static_cast<uint32_t>(e) & kFlagBit);
+  r.reuse = takes_slot(a, r.t, e, r.f);
   r.slot = r.reuse ? static_cast<int>(static_cast<uint32_t>(e) & ~kFlagBit) : a.st.len[r.sh];
   return r;
 }
@@ -233,16 +255,15 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(PlanArgs a) {
     return;
   }
   const int sh = s * a.H + tid % a.H;
-  int t = 0, slot = -1, fresh = 0, need = 0, Lnew = 0, cap = 0;
+  int t = 0, slot = -1, fresh = 0, need = 0, Lnew = 0, cap = 0, f = 0;
   if (a.append && tid < min(NH, top0)) stack_lds[tid] = a.st.stack[top0 - 1 - tid];
   if (act) {
     const int L = a.st.len[sh];
     if (a.append) {
+      f = decision(a, tid);
       t = a.st.pos[s];
       const int32_t e = a.st.ring[static_cast<size_t>(sh) * a.w + t % a.w];
-      // the token that entered w steps ago leaves now if it was flagged; the
-      // incoming token takes its slot
-      const bool reuse = (t >= a.w) && (static_cast<uint32_t>(e) & kFlagBit);
+      const bool reuse = takes_slot(a, t, e, f);
       slot = reuse ? static_cast<int>(static_cast<uint32_t>(e) & ~kFlagBit) : L;
       fresh = !reuse;
       cap = fresh && slot >= a.max_slots;
@@ -263,11 +284,12 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(PlanArgs a) {
   const int c0 = ex.y, c1 = ex.y + tiles;
   if (act) {
     if (a.append) {
-      const uint32_t f = a.flags[tid] ? kFlagBit : 0u;
+      const uint32_t fb = f ? kFlagBit : 0u;
+      if (a.flags_out != nullptr) a.flags_out[tid] = static_cast<uint8_t>(f);
       if (need) a.st.page_table[static_cast<size_t>(sh) * a.maxp + slot / a.P] = stack_lds[ex.x];
       if (fresh) a.st.len[sh] = Lnew;
-      a.st.ring[static_cast<size_t>(sh) * a.w + t % a.w] = static_cast<int32_t>(static_cast<uint32_t>(slot) | f);
-      a.st.slot_meta[static_cast<size_t>(sh) * a.max_slots + slot] = static_cast<int32_t>(static_cast<uint32_t>(t) | f);
+      a.st.ring[static_cast<size_t>(sh) * a.w + t % a.w] = static_cast<int32_t>(static_cast<uint32_t>(slot) | fb);
+      a.st.slot_meta[static_cast<size_t>(sh) * a.max_slots + slot] = static_cast<int32_t>(static_cast<uint32_t>(t) | fb);
       // every head of the sequence read pos before the scan's barriers
       if (tid % a.H == 0) a.st.pos[s] = t + 1;
     }
@@ -332,13 +354,14 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   int run_pop = 0, run_tiles = 0;
   for (int base = 0; base < NH; base += blockDim.x) {
     const int hh = base + threadIdx.x;
-    int need = 0, tiles = 0, Lnew = 0, slot = -1, sh = 0, t = 0, fresh = 0;
+    int need = 0, tiles = 0, Lnew = 0, slot = -1, sh = 0, t = 0, fresh = 0, f = 0;
     if (hh < NH) {
       if (a.append) {
         HeadStep r = r1_step(a, hh);
         sh = r.sh;
         t = r.t;
         slot = r.slot;
+        f = r.f;
         fresh = !r.reuse;
         need = fresh && (slot % a.P) == 0;
         Lnew = a.st.len[sh] + fresh;
@@ -353,11 +376,12 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
     const int ct = run_tiles + block_exclusive_scan(tiles, lds, &tott);
     if (hh < NH) {
       if (a.append) {
-        const uint32_t f = a.flags[hh] ? kFlagBit : 0u;
+        const uint32_t fb = f ? kFlagBit : 0u;
+        if (a.flags_out != nullptr) a.flags_out[hh] = static_cast<uint8_t>(f);
         if (need) a.st.page_table[static_cast<size_t>(sh) * a.maxp + slot / a.P] = a.st.stack[top0 - 1 - pop];
         if (fresh) a.st.len[sh] = Lnew;
-        a.st.ring[static_cast<size_t>(sh) * a.w + t % a.w] = static_cast<int32_t>(static_cast<uint32_t>(slot) | f);
-        a.st.slot_meta[static_cast<size_t>(sh) * a.max_slots + slot] = static_cast<int32_t>(static_cast<uint32_t>(t) | f);
+        a.st.ring[static_cast<size_t>(sh) * a.w + t % a.w] = static_cast<int32_t>(static_cast<uint32_t>(slot) | fb);
+        a.st.slot_meta[static_cast<size_t>(sh) * a.max_slots + slot] = static_cast<int32_t>(static_cast<uint32_t>(t) | fb);
       }
       a.desc[hh] = make_int4(Lnew, sh, slot, 0);
       a.cum_tiles[hh + 1] = ct + tiles;
@@ -445,6 +469,7 @@ struct ChunkArgs {
   int32_t* err;           // call-local error word, err[1] = stack height before the call
   int32_t* slots;         // [T, H] slot of every chunk token
   int n, H, w, P, D, maxp, max_slots, max_seqs, total, max_len;
+  int immediate;          // eviction timing (see chunk_reuse)
 };
 
 __device__ inline int chunk_flag(const ChunkArgs& a, int tok0, int c, int h) {
@@ -452,9 +477,11 @@ __device__ inline int chunk_flag(const ChunkArgs& a, int tok0, int c, int h) {
 }
 
 // Does chunk token c (position pos0 + c) reuse the slot of position pos0 + c - w?
+// Delayed eviction: iff that token was flagged; immediate: iff token c is.
 __device__ inline bool chunk_reuse(const ChunkArgs& a, int sh, int h, int tok0, int pos0, int c) {
   const int t = pos0 + c;
   if (t < a.w) return false;
+  if (a.immediate) return chunk_flag(a, tok0, c, h);
   const int j = c - a.w;
   if (j >= 0) return chunk_flag(a, tok0, j, h);
   const int32_t e = a.st.ring[static_cast<size_t>(sh) * a.w + (t - a.w) % a.w];
@@ -590,7 +617,8 @@ __global__ __launch_bounds__(256) void chunk_commit_kernel(ChunkArgs a) {
     if (c >= ring_from)
       a.st.ring[static_cast<size_t>(sh) * a.w + (pos0 + c) % a.w] =
           static_cast<int32_t>(static_cast<uint32_t>(slot) | fb);
-    const bool survives = (c + a.w >= C) || !fl;
+    // a token keeps its slot unless the token w later in the chunk takes it
+    const bool survives = (c + a.w >= C) || !chunk_reuse(a, sh, h, tok0, pos0, c + a.w);
     if (survives)
       a.st.slot_meta[static_cast<size_t>(sh) * a.max_slots + slot] =
           static_cast<int32_t>(static_cast<uint32_t>(pos0 + c) | fb);
@@ -601,7 +629,7 @@ __global__ __launch_bounds__(256) void chunk_commit_kernel(ChunkArgs a) {
   const int kq = a.D / 8;
   for (int idx = threadIdx.x; idx < C * kq; idx += blockDim.x) {
     const int c = idx / kq, part = idx % kq;
-    if (!((c + a.w >= C) || !chunk_flag(a, tok0, c, h))) continue;
+    if (!((c + a.w >= C) || !chunk_reuse(a, sh, h, tok0, pos0, c + a.w))) continue;
     const int slot = a.slots[static_cast<size_t>(tok0 + c) * a.H + h];
     const int page = a.st.page_table[pt_base + slot / a.P];
     const int row = slot % a.P;
@@ -675,9 +703,15 @@ hipError_t launch_seq_reset(const dms_config& c, const Layout& lo, void* meta, i
 }
 
 hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* ws, int layer,
-                       int n, const int32_t* seq_ids, const uint8_t* flags, bool append,
-                       int waves, float* out, hipStream_t st) {
+                       int n, const int32_t* seq_ids, const uint8_t* flags, const void* q,
+                       uint8_t* flags_out, bool append, int waves, float* out, hipStream_t st) {
   PlanArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.flags_out = flags_out;
+  a.bias = c.decision_bias;
+  a.immediate = c.eviction == DMS_EVICT_IMMEDIATE;
+  a.g = c.group_size;
+  a.D = c.head_dim;
   a.wave_bounds = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_wave_bounds);
   a.wave_head = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_wave_head);
   a.out = out;
@@ -766,6 +800,7 @@ hipError_t launch_chunk_commit(const dms_config& c, const Layout& lo, void* meta
   a.max_seqs = c.max_seqs;
   a.total = total_tokens;
   a.max_len = max_len;
+  a.immediate = c.eviction == DMS_EVICT_IMMEDIATE;
   const int NH = n * c.num_kv_heads;
   hipLaunchKernelGGL(chunk_count_kernel, dim3(NH), dim3(256), 0, st, a);
   hipLaunchKernelGGL(chunk_pages_kernel, dim3(1), dim3(kPlanThreads), 0, st, a);

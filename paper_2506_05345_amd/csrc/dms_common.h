@@ -31,7 +31,7 @@ struct Layout {
   size_t ws_head_desc, ws_cum_tiles, ws_part_ml, ws_part_acc;
   size_t ws_wave_bounds, ws_wave_head, ws_head_cnt;
   size_t ws_ck_need, ws_ck_fresh, ws_ck_base, ws_ck_pos0, ws_ck_err, ws_ck_slot;
-  size_t ws_pf_cum, ws_pf_meta, ws_pf_tiles;
+  size_t ws_pf_cum, ws_pf_meta, ws_pf_tiles, ws_pf_flags;
   int pf_tiles_per_head;   // tiles of one (region, KV head) in ws_pf_tiles
   size_t workspace_bytes;
   int max_heads, max_partials, max_slots;
@@ -177,8 +177,8 @@ hipError_t launch_seq_reset(const dms_config& c, const Layout& lo, void* meta, i
 // tile range and first head of every decode wave.  `out` (nullable) gets zeros
 // for heads with no retained token.
 hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* ws, int layer,
-                       int n, const int32_t* seq_ids, const uint8_t* flags, bool append,
-                       int waves, float* out, hipStream_t st);
+                       int n, const int32_t* seq_ids, const uint8_t* flags, const void* q,
+                       uint8_t* flags_out, bool append, int waves, float* out, hipStream_t st);
 hipError_t launch_scatter(const dms_config& c, const Layout& lo, void* meta, void* ws,
                           void* pool, int layer, int n, const void* k, const void* v,
                           hipStream_t st);
@@ -195,6 +195,8 @@ hipError_t launch_chunk_commit(const dms_config& c, const Layout& lo, void* meta
                                void* pool, int layer, int n, const int32_t* seq_ids,
                                const int32_t* cu, int total_tokens, int max_len, const void* k,
                                const void* v, const uint8_t* flags, hipStream_t st);
+hipError_t launch_prefill_decide(const dms_config& c, const void* q, int total_tokens,
+                                 uint8_t* flags, hipStream_t st);
 hipError_t launch_prefill_attention(const dms_config& c, const Layout& lo, void* meta, void* ws,
                                     void* pool, int layer, int n, const int32_t* seq_ids,
                                     const int32_t* cu, int total_tokens, int max_len,

@@ -71,6 +71,7 @@ struct DecodeParams {
   size_t page_bytes;
   int part_acc_bytes;   // size of the split-K accumulator area (< 2 GiB)
   int NH, g, maxp, P, log2P, W;
+  int zero_neuron;   // element 0 of the group's first query head is read as 0
   float scale_log2;  // softmax scale * log2(e)
 };
 
@@ -391,6 +392,8 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
     const char* qrow = reinterpret_cast<const char*>(q + (static_cast<size_t>(hh) * a.g + r) * D);
 #pragma unroll
     for (int s = 0; s < D / 32; ++s) qf[s] = r < a.g ? ldg16(qrow + (32 * s + 8 * G) * 2) : z;
+    // the borrowed decision neuron takes no part in attention (App. C)
+    if (a.zero_neuron && r == 0 && G == 0) qf[0][0] &= 0xFFFF0000u;
     Acc<D> acc;
 #pragma unroll
     for (int b = 0; b < D / 16; ++b) acc.o[b] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -516,6 +519,7 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
   a.P = c.page_size;
   a.log2P = __builtin_ctz(static_cast<unsigned>(c.page_size));
   a.W = waves;
+  a.zero_neuron = c.decision_source == DMS_DECIDE_QUERY;
   a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
   if (ev_start) (void)hipEventRecord(ev_start, st);
   hipLaunchKernelGGL(decode_kernel<D>, dim3(waves / kWavesPerBlock), dim3(256), 0, st, status,

@@ -91,8 +91,32 @@ struct PrefillArgs {
   float* out;             // [T, Hq, D]
   size_t page_bytes;
   int n, H, g, w, P, log2P, maxp, max_slots, max_seqs, total, max_len, PB, tph;
+  int immediate;    // eviction timing: key j is hidden by the decision of j + w
+  int zero_neuron;  // element 0 of each group's first query head is read as 0
   float scale_log2;
 };
+
+// Decision that hides chunk key c (chunk-local) once it leaves the window:
+// its own (delayed eviction) or that of chunk token c + w (immediate
+// eviction; none yet if c + w is past the chunk).
+__device__ inline bool key_flag(const PrefillArgs& a, int tok0, int C, int c, int h) {
+  const int x = a.immediate ? c + a.w : c;
+  return x < C && a.flags[static_cast<size_t>(tok0 + x) * a.H + h] != 0;
+}
+__device__ inline bool key_kept(const PrefillArgs& a, int tok0, int C, int c, int h) {
+  return !key_flag(a, tok0, C, c, h);
+}
+
+// Decisions from the borrowed query neuron (Sec. 3.2 rounding, App. C):
+// flags[t][h] = (bf16 q[t][h * g][0] + bias > 0) in float32.
+__global__ __launch_bounds__(kThreads) void prefill_decide_kernel(const uint16_t* q, uint8_t* flags,
+                                                                  int total, int H, int g, int D,
+                                                                  float bias) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= static_cast<int64_t>(total) * H) return;
+  const uint32_t bits = q[static_cast<size_t>(idx) * g * D];
+  flags[idx] = (__uint_as_float(bits << 16) + bias) > 0.f;
+}
 
 // Pass 0 (one block per (sequence, head)): validate the chunk boundaries and
 // list the kept tokens of the chunk in position order.
@@ -112,7 +136,7 @@ __global__ __launch_bounds__(kThreads) void prefill_list_kernel(PrefillArgs a) {
   int run = 0;
   for (int c0 = 0; c0 < C; c0 += blockDim.x) {
     const int c = c0 + threadIdx.x;
-    const int kept = (c < C) && a.flags[static_cast<size_t>(tok0 + c) * a.H + h] == 0;
+    const int kept = (c < C) && key_kept(a, tok0, C, c, h);
     int tot;
     const int off = block_exclusive_scan(kept, lds, &tot);
     if (kept) a.list[static_cast<size_t>(h) * a.total + tok0 + run + off] = c;
@@ -247,6 +271,8 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
     for (int s2 = 0; s2 < D / 32; ++s2)
       qf[qb][s2] = ok ? *reinterpret_cast<const u32x4*>(qrow + (32 * s2 + 8 * G) * 2) : z;
+    // the borrowed decision neuron takes no part in attention (App. C)
+    if (a.zero_neuron && qh == 0 && G == 0) qf[qb][0][0] &= 0xFFFF0000u;
   }
 
   // ---- staging: global -> registers (A), registers -> LDS (B)
@@ -258,7 +284,18 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
       const int sb = k * 32;
       tile = a.pool + static_cast<size_t>(pt[sb >> a.log2P]) * a.page_bytes +
              static_cast<size_t>((sb & (a.P - 1)) >> 5) * (D * 128);
-      if (tid < 32) stg.meta = sb + tid < L0 ? static_cast<uint32_t>(smeta[sb + tid]) : kNoKey;
+      if (tid < 32) {
+        uint32_t mt = sb + tid < L0 ? static_cast<uint32_t>(smeta[sb + tid]) : kNoKey;
+        if (a.immediate && mt != kNoKey) {
+          // a cached key j is hidden by the decision of position j + w, which
+          // (for a live key) lies in this chunk or later
+          const int kp = static_cast<int>(mt & ~kFlagBit);
+          const int x = kp + a.w - p0;
+          mt = static_cast<uint32_t>(kp) |
+               ((x >= 0 && x < C && a.flags[static_cast<size_t>(tok0 + x) * a.H + h]) ? kFlagBit : 0u);
+        }
+        stg.meta = mt;
+      }
     } else if (k < nc + np) {
       const int kk = k - nc;
       tile = pre_tiles + static_cast<size_t>(kk) * (D * 128);
@@ -272,7 +309,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
       if (tid < 32) {
         const int c = band_c0 + kb * 32 + tid;
         stg.meta = c < t1 - p0 ? (static_cast<uint32_t>(p0 + c) |
-                                  (a.flags[static_cast<size_t>(tok0 + c) * a.H + h] ? kFlagBit : 0u))
+                                  (key_flag(a, tok0, C, c, h) ? kFlagBit : 0u))
                                : kNoKey;
       }
     }
@@ -462,6 +499,8 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   a.list_cnt = reinterpret_cast<int32_t*>(w + lo.ws_pf_cum);
   a.tiles = w + lo.ws_pf_tiles;
   a.tph = lo.pf_tiles_per_head;
+  a.immediate = c.eviction == DMS_EVICT_IMMEDIATE;
+  a.zero_neuron = c.decision_source == DMS_DECIDE_QUERY;
   a.out = out;
   a.page_bytes = lo.page_bytes;
   a.n = n;
@@ -495,6 +534,16 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
 }
 
 }  // namespace
+
+hipError_t launch_prefill_decide(const dms_config& c, const void* q, int total_tokens,
+                                 uint8_t* flags, hipStream_t st) {
+  const int64_t n = static_cast<int64_t>(total_tokens) * c.num_kv_heads;
+  const int blocks = static_cast<int>((n + kThreads - 1) / kThreads);
+  hipLaunchKernelGGL(prefill_decide_kernel, dim3(blocks), dim3(kThreads), 0, st,
+                     static_cast<const uint16_t*>(q), flags, total_tokens, c.num_kv_heads,
+                     c.group_size, c.head_dim, c.decision_bias);
+  return hipGetLastError();
+}
 
 hipError_t launch_prefill_attention(const dms_config& c, const Layout& lo, void* meta, void* ws,
                                     void* pool, int layer, int n, const int32_t* seq_ids,

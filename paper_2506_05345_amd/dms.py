@@ -41,7 +41,16 @@ class DmsConfig(ctypes.Structure):
         ("max_pages_per_head", ctypes.c_int32),
         ("max_chunk_tokens", ctypes.c_int32),
         ("softmax_scale", ctypes.c_float),
+        ("eviction", ctypes.c_int32),
+        ("decision_source", ctypes.c_int32),
+        ("decision_bias", ctypes.c_float),
     ]
+
+
+DMS_EVICT_DELAYED = 0
+DMS_EVICT_IMMEDIATE = 1
+DMS_DECIDE_CALLER = 0
+DMS_DECIDE_QUERY = 1
 
 
 class DmsStateOffsets(ctypes.Structure):
@@ -75,6 +84,8 @@ _SIGS = {
     "dms_decode_step": (_I, [_VP, _I, _I, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     "dms_append_chunk": (_I, [_VP, _I, _I, _VP, _VP, _I, _I, _VP, _VP, _VP, _VP]),
     "dms_prefill_chunk": (_I, [_VP, _I, _I, _VP, _VP, _I, _I, _VP, _VP, _VP, _VP, _VP, _VP]),
+    "dms_decode_step_q": (_I, [_VP, _I, _I, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
+    "dms_prefill_chunk_q": (_I, [_VP, _I, _I, _VP, _VP, _I, _I, _VP, _VP, _VP, _VP, _VP, _VP]),
     "dms_retained_lengths": (_I, [_VP, _I, _I, _VP, _VP, _VP]),
     "dms_export_state": (_I, [_VP, _I, _VP, _SZ, _VP]),
     "dms_status": (_I, [_VP, _VP]),
@@ -126,10 +137,11 @@ def _check(rc, where):
 
 def make_config(num_layers, max_seqs, num_kv_heads, group_size, head_dim, window,
                 page_size, num_pages, max_pages_per_head, max_chunk_tokens=0,
-                softmax_scale=0.0) -> DmsConfig:
+                softmax_scale=0.0, eviction=DMS_EVICT_DELAYED,
+                decision_source=DMS_DECIDE_CALLER, decision_bias=-5.0) -> DmsConfig:
     return DmsConfig(num_layers, max_seqs, num_kv_heads, group_size, head_dim, window,
                      page_size, num_pages, max_pages_per_head, max_chunk_tokens,
-                     softmax_scale)
+                     softmax_scale, eviction, decision_source, decision_bias)
 
 
 # ---------------------------------------------------------------------------
@@ -184,6 +196,12 @@ def dms_decode_step(ctx, layer, n, seq_ids, q, k, v, flags, out, stream=None):
                                  _ptr(flags), _ptr(out), _stream(stream)), "dms_decode_step")
 
 
+def dms_decode_step_q(ctx, layer, n, seq_ids, q, k, v, decisions_out, out, stream=None):
+    _check(lib().dms_decode_step_q(ctx, layer, n, _ptr(seq_ids), _ptr(q), _ptr(k), _ptr(v),
+                                   _ptr(decisions_out), _ptr(out), _stream(stream)),
+           "dms_decode_step_q")
+
+
 def dms_append_chunk(ctx, layer, n, seq_ids, cu_seqlens, total_tokens, max_seqlen, k, v, flags,
                      stream=None):
     _check(lib().dms_append_chunk(ctx, layer, n, _ptr(seq_ids), _ptr(cu_seqlens), total_tokens,
@@ -196,6 +214,13 @@ def dms_prefill_chunk(ctx, layer, n, seq_ids, cu_seqlens, total_tokens, max_seql
     _check(lib().dms_prefill_chunk(ctx, layer, n, _ptr(seq_ids), _ptr(cu_seqlens), total_tokens,
                                    max_seqlen, _ptr(q), _ptr(k), _ptr(v), _ptr(flags), _ptr(out),
                                    _stream(stream)), "dms_prefill_chunk")
+
+
+def dms_prefill_chunk_q(ctx, layer, n, seq_ids, cu_seqlens, total_tokens, max_seqlen, q, k, v,
+                        decisions_out, out, stream=None):
+    _check(lib().dms_prefill_chunk_q(ctx, layer, n, _ptr(seq_ids), _ptr(cu_seqlens), total_tokens,
+                                     max_seqlen, _ptr(q), _ptr(k), _ptr(v), _ptr(decisions_out),
+                                     _ptr(out), _stream(stream)), "dms_prefill_chunk_q")
 
 
 def dms_retained_lengths(ctx, layer, n, seq_ids, out, stream=None):

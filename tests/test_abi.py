@@ -51,6 +51,11 @@ def _cfg(**kw):
     (dict(max_chunk_tokens=-1), dms.DMS_ERR_INVALID),
     (dict(softmax_scale=float("nan")), dms.DMS_ERR_INVALID),
     (dict(softmax_scale=float("inf")), dms.DMS_ERR_INVALID),
+    (dict(eviction=2), dms.DMS_ERR_INVALID),
+    (dict(eviction=-1), dms.DMS_ERR_INVALID),
+    (dict(decision_source=2), dms.DMS_ERR_INVALID),
+    (dict(decision_source=1, decision_bias=float("nan")), dms.DMS_ERR_INVALID),
+    (dict(decision_source=1, decision_bias=float("inf")), dms.DMS_ERR_INVALID),
 ])
 def test_bad_configuration(kw, code):
     rc = dms.lib().dms_layout(ctypes.byref(_cfg(**kw)), None, None, None, None)
@@ -104,6 +109,31 @@ def test_host_side_argument_errors_change_nothing():
     finally:
         dms.dms_destroy(ctx)
     assert L.dms_destroy(None) == dms.DMS_ERR_INVALID
+
+
+def test_decision_source_selects_the_entry_points():
+    """Caller-flag and query-decision entry points reject the other mode on
+    the host (fake pointers: nothing may be launched or dereferenced)."""
+    L = dms.lib()
+    P = 0x100
+    ctx = dms.dms_create(_cfg(), 0x1000, [0x2000, 0x3000], 0x4000)
+    try:
+        assert L.dms_decode_step_q(ctx, 0, 1, P, P, P, P, None, P, None) == dms.DMS_ERR_INVALID
+        assert L.dms_prefill_chunk_q(ctx, 0, 1, P, P, 10, 10, P, P, P, None, P, None) == dms.DMS_ERR_INVALID
+    finally:
+        dms.dms_destroy(ctx)
+    ctx = dms.dms_create(_cfg(decision_source=dms.DMS_DECIDE_QUERY, eviction=dms.DMS_EVICT_IMMEDIATE),
+                         0x1000, [0x2000, 0x3000], 0x4000)
+    try:
+        assert L.dms_decode_step(ctx, 0, 1, P, P, P, P, P, P, None) == dms.DMS_ERR_INVALID
+        assert L.dms_prefill_chunk(ctx, 0, 1, P, P, 10, 10, P, P, P, P, P, None) == dms.DMS_ERR_INVALID
+        # query mode: q, k, v and out are required; decisions_out may be NULL
+        assert L.dms_decode_step_q(ctx, 0, 1, P, None, P, P, None, P, None) == dms.DMS_ERR_INVALID
+        assert L.dms_decode_step_q(ctx, 0, 1, P, P, P, P, None, None, None) == dms.DMS_ERR_INVALID
+        assert L.dms_prefill_chunk_q(ctx, 0, 1, P, P, 10, 10, None, P, P, None, P, None) == dms.DMS_ERR_INVALID
+        assert L.dms_prefill_chunk_q(ctx, 0, 1, P, P, 0, 0, P, P, P, None, P, None) == dms.DMS_OK
+    finally:
+        dms.dms_destroy(ctx)
 
 
 def test_error_strings():
