@@ -115,8 +115,10 @@ def build(wl, steps_total, chunk_tokens, dev):
         need = torch.div(Lh + steps_total + P - 1, P, rounding_mode="floor")
         max_pages_head = max(max_pages_head, int(need.max()))
         pages_layer = max(pages_layer, int(need.sum()))
+    # the state is built by chunk appends of up to 16 sequences at a time
+    grp = min(B, 16)
     cfg = dms.make_config(nl, B, H, g, D, w, P, pages_layer + 8, max_pages_head + 1,
-                          chunk_tokens * B)
+                          chunk_tokens * grp)
     mb, pb, wb, _ = dms.dms_layout(cfg)
     log(f"pool {pb * nl / 2**30:.1f} GiB ({pages_layer + 8} pages/layer), meta "
         f"{mb / 2**30:.2f} GiB, workspace {wb / 2**20:.1f} MiB")
@@ -126,22 +128,26 @@ def build(wl, steps_total, chunk_tokens, dev):
     t0 = time.perf_counter()
     for layer in range(nl):
         gen.manual_seed(seed * 1000 + layer)
-        done = np.zeros(B, np.int64)
-        while (done < ctx).any():
-            lens = np.minimum(chunk_tokens, ctx - done)
-            cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
-            T = int(cu[-1])
-            k = torch.randn((T, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
-            v = torch.randn((T, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
-            # flags of every sequence's next positions, varlen layout [T, H]
-            seq_of = torch.repeat_interleave(seqs, torch.as_tensor(lens, device=dev))
-            start = torch.as_tensor(cu[:-1], device=dev, dtype=torch.int64)
-            pos = (torch.arange(T, device=dev) - torch.repeat_interleave(start, torch.as_tensor(lens, device=dev))
-                   + torch.as_tensor(done, device=dev)[seq_of])
-            f = sy.flags_torch(seed, p, layer, seq_of[:, None], heads[None, :], pos[:, None], dev)
-            dms.dms_append_chunk(cache.ctx, layer, B, sid, torch.as_tensor(cu, device=dev), T,
-                                 int(lens.max()), k, v, f)
-            done += lens
+        for g0 in range(0, B, grp):
+            ids = np.arange(g0, min(B, g0 + grp))
+            gsid, gseqs = sid[g0:g0 + len(ids)], seqs[g0:g0 + len(ids)]
+            done = np.zeros(len(ids), np.int64)
+            while (done < ctx[ids]).any():
+                lens = np.minimum(chunk_tokens, ctx[ids] - done)
+                cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+                T = int(cu[-1])
+                k = torch.randn((T, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+                v = torch.randn((T, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+                # flags of every sequence's next positions, varlen layout [T, H]
+                lens_t = torch.as_tensor(lens, device=dev)
+                seq_of = torch.repeat_interleave(gseqs, lens_t)
+                start = torch.as_tensor(cu[:-1], device=dev, dtype=torch.int64)
+                pos = (torch.arange(T, device=dev) - torch.repeat_interleave(start, lens_t)
+                       + torch.as_tensor(done, device=dev)[seq_of - g0])
+                f = sy.flags_torch(seed, p, layer, seq_of[:, None], heads[None, :], pos[:, None], dev)
+                dms.dms_append_chunk(cache.ctx, layer, len(ids), gsid, torch.as_tensor(cu, device=dev),
+                                     T, int(lens.max()), k, v, f)
+                done += lens
         if layer % 8 == 7 or layer == nl - 1:
             torch.cuda.synchronize()
             log(f"built layers 0..{layer} ({time.perf_counter() - t0:.1f}s)")
@@ -416,6 +422,131 @@ def run_stress(args):
     print(json.dumps(res), flush=True)
 
 
+# Attention shapes of the paper's models (layers, KV heads, group, head dim)
+# and the dense-model sizes (public model configurations) that the App. I
+# latency estimate needs: hidden size d, MLP width d_ff, vocabulary V.
+SWEEP_SHAPES = {
+    "qwen-r1-1.5b": dict(layers=28, kv_heads=2, group=6, head_dim=128, d=1536, d_ff=8960, V=151936),
+    "qwen-r1-7b": dict(layers=28, kv_heads=4, group=7, head_dim=128, d=3584, d_ff=18944, V=152064),
+    "qwen-r1-32b": dict(layers=64, kv_heads=8, group=5, head_dim=128, d=5120, d_ff=27648, V=152064),
+    "qwen3-8b": dict(layers=36, kv_heads=8, group=4, head_dim=128, d=4096, d_ff=12288, V=151936),
+}
+HBM_BYTES = 288e9
+MFMA_PEAK_FLOPS = 2.5e15
+
+
+def app_i_estimate(sh, B, L):
+    """App. I step model with MI355X peaks: FLOPS(B, L), Reads(B, L) (the
+    "4 d d_ff" read term taken as 4 d d_kv) and latency = max(compute, reads);
+    returns (latency s, share of it that is KV-cache reads, weight bytes)."""
+    n, d, dff, V = sh["layers"], sh["d"], sh["d_ff"], sh["V"]
+    dkv = sh["kv_heads"] * sh["head_dim"]
+    flops = n * B * (6 * d * dff + 4 * d * d + 4 * d * dkv + 4 * d * L) + 2 * B * d * V
+    weights = n * (6 * d * dff + 4 * d * d + 4 * d * dkv) + 2 * d * V
+    kv = n * 4 * B * L * dkv
+    lat = max(flops / MFMA_PEAK_FLOPS, (weights + kv) / (HBM_PEAK_GBS * 1e9))
+    return lat, (kv / (HBM_PEAK_GBS * 1e9)) / lat, weights
+
+
+def measure_decode(wl, steps, warmup, dev):
+    """Build a workload's cache, replay `steps` decode steps of every layer as
+    one HIP graph; returns step ms, KV bytes per step, mean retained length."""
+    import torch
+    from paper_2506_05345_amd import dms
+    S = warmup + steps
+    cache, ctx, L0 = build(wl, S, 4096, dev)
+    q, k, v, flags, fresh = step_inputs(wl, ctx, S, dev)
+    B, nl, D = wl["batch"], wl["layers"], wl["head_dim"]
+    sid = torch.arange(B, dtype=torch.int32, device=dev)
+    out = torch.empty((nl, B, wl["kv_heads"] * wl["group"], D), dtype=torch.float32, device=dev)
+
+    def run_step(s):
+        for layer in range(nl):
+            dms.dms_decode_step(cache.ctx, layer, B, sid, q[s, layer], k[s, layer], v[s, layer],
+                                flags[s, layer], out[layer])
+
+    for s in range(warmup):
+        run_step(s)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for s in range(warmup, S):
+            run_step(s)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    if dms.dms_status(cache.ctx) != 0:
+        raise RuntimeError("decode failed")
+    Lstep = torch.stack(L0)[None] + torch.cumsum(fresh, dim=0)
+    kv = float(Lstep[warmup:].sum()) * 2 * D * 2 / steps
+    mean_L = float(Lstep[warmup:].double().mean())
+    ms = e0.elapsed_time(e1) / steps
+    del graph, q, k, v, flags, fresh, out
+    cache.close()
+    torch.cuda.empty_cache()
+    return ms, kv, mean_L
+
+
+def run_sweep(args):
+    """Attention-only sweeps on one GPU (one JSON line per point):
+    fig4-r1: step latency vs context, Qwen-R1 1.5B / 7B / 32B shapes, batch 32;
+    fig4-qwen3: the same for the Qwen3-8B shape at batch 32 / 64 / 128;
+    maxbatch: the largest batch whose KV cache fits next to the weights in
+    288 GB, at CR 1 / 4 / 8, and its decode tokens/s (attention only).
+    CR c is emulated by eviction probability 1 - 1/c; points whose cache does
+    not fit in HBM are reported as such."""
+    import torch
+    dev = "cuda:0"
+    points = []
+    if args.sweep == "fig4-r1":
+        for name in ("qwen-r1-1.5b", "qwen-r1-7b", "qwen-r1-32b"):
+            for ctxlen in (4096, 8192, 16384, 32768):
+                for cr in (1, 4, 8):
+                    points.append((name, 32, ctxlen, cr, 256))
+    elif args.sweep == "fig4-qwen3":
+        for B in (32, 64, 128):
+            for ctxlen in (4096, 8192, 16384, 32768):
+                for cr in (1, 4, 8):
+                    points.append(("qwen3-8b", B, ctxlen, cr, 512))
+    else:
+        ctxlen = 32768
+        for name in SWEEP_SHAPES:
+            w = 512 if name == "qwen3-8b" else 256
+            sh = SWEEP_SHAPES[name]
+            for cr in (1, 4, 8):
+                p = 1 - 1 / cr
+                Lr = min(w, ctxlen) + (1 - p) * max(0, ctxlen - w)
+                per_seq = sh["layers"] * sh["kv_heads"] * Lr * sh["head_dim"] * 4 * 1.03
+                _, _, weights = app_i_estimate(sh, 1, 0)
+                budget = HBM_BYTES - weights - 24e9       # weights, inputs, workspace, margin
+                points.append((name, int(budget // per_seq), ctxlen, cr, w))
+    for (name, B, ctxlen, cr, w) in points:
+        sh = SWEEP_SHAPES[name]
+        p = 1 - 1 / cr
+        Lr = min(w, ctxlen) + (1 - p) * max(0, ctxlen - w)
+        kv_est = sh["layers"] * B * sh["kv_heads"] * Lr * sh["head_dim"] * 4
+        lat, share, weights = app_i_estimate(sh, B, Lr)
+        rec = {"sweep": args.sweep, "model_shape": name, "batch": B, "context": ctxlen, "cr": cr,
+               "window": w, "kv_cache_gb": round(kv_est / 1e9, 2),
+               "app_i_latency_ms": round(1e3 * lat, 3), "app_i_kv_share": round(share, 3)}
+        if kv_est + weights + 16e9 > HBM_BYTES:
+            rec["status"] = "KV cache does not fit in HBM next to the weights"
+            print(json.dumps(rec), flush=True)
+            continue
+        wl = dict(layers=sh["layers"], batch=B, kv_heads=sh["kv_heads"], group=sh["group"],
+                  head_dim=sh["head_dim"], context=ctxlen, window=w, p_evict=p, seed=11)
+        ms, kv, mean_L = measure_decode(wl, args.steps, args.warmup, dev)
+        rec.update({"status": "measured", "attn_ms_per_step": round(ms, 3),
+                    "kv_gb_per_step": round(kv / 1e9, 3),
+                    "achieved_gbs": round(kv / (ms * 1e-3) / 1e9, 1),
+                    "decode_tok_per_s": round(B / (ms * 1e-3), 1),
+                    "mean_retained": round(mean_L, 1)})
+        print(json.dumps(rec), flush=True)
+        torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -431,6 +562,8 @@ def main():
                     help="run a 1 GiB device copy first (reference kernel for HBM counters)")
     ap.add_argument("--eager", action="store_true",
                     help="launch the timed steps one by one instead of replaying a HIP graph")
+    ap.add_argument("--sweep", choices=["fig4-r1", "fig4-qwen3", "maxbatch"],
+                    help="attention-only sweeps (one JSON line per point) instead of the benchmark")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; the DMS decode path "
@@ -442,6 +575,9 @@ def main():
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.sweep:
+        run_sweep(args)
+        return
     if args.calibrate_copy:
         # plain copy of known size: reads 1 GiB, writes 1 GiB
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
