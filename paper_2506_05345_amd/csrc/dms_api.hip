@@ -64,7 +64,8 @@ Layout make_layout(const dms_config& c) {
   lo.ws_part_ml = take(NP * kMaxGroup * 8);
   lo.ws_part_acc = take(NP * c.group_size * D * 4);
   lo.ws_wave_bounds = take((kMaxWaves + 1) * 4);
-  lo.ws_wave_head = take(kMaxWaves * 4);
+  lo.ws_wave_desc = take(kMaxWaves * 2 * sizeof(int4));   // per decode wave: first segment
+  lo.ws_head_waves = take(NH * sizeof(int4));              // per head: waves holding its tiles
   lo.ws_head_cnt = take(NH * 4);
   lo.ws_ck_need = take(NH * 4);
   lo.ws_ck_fresh = take(NH * 4);

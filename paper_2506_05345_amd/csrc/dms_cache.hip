@@ -158,7 +158,8 @@ struct PlanArgs {
   HeadDesc* desc;        // [n*H]
   int32_t* cum_tiles;    // [n*H + 1]
   int32_t* wave_bounds;  // [W + 1] first tile of every decode wave
-  int32_t* wave_head;    // [W] head holding that tile
+  int4* wave_desc;       // [2W] first segment of every decode wave (see decode kernel)
+  int4* head_waves;      // [n*H] first / last wave holding a tile of the head, live mask
   float* out;            // nullable: zeroed for heads with no retained token
   int n, H, w, P, maxp, max_slots, max_seqs, append, W, gD;
 };
@@ -173,16 +174,56 @@ __device__ inline int upper_index(const int32_t* cum, int NH, int b) {
   return lo;
 }
 
-// Tile range of every decode wave: equal contiguous shares of the flat tile
-// list (heads that straddle a boundary are merged by the decode kernel).
-__device__ void wave_ranges(const int32_t* cum, int NH, int W, int32_t* bounds,
-                            int32_t* first_head) {
-  const int total = cum[NH];
-  for (int w = threadIdx.x; w <= W; w += blockDim.x) {
-    const int b = static_cast<int>(static_cast<int64_t>(w) * total / W);
-    bounds[w] = b;
-    if (w < W) first_head[w] = min(upper_index(cum, NH, b), NH - 1);
+// Descriptor of decode wave w's first segment: its tile range [tb, te), the
+// head hh holding tile tb with that head's tile range [c0, c1), retained
+// length L, state index sh and appended slot z.
+__device__ inline void put_wave_desc(int4* wave_desc, int w, int tb, int te, int hh, int c0,
+                                     int c1, const int4& d) {
+  wave_desc[2 * w] = make_int4(tb, te, hh, c0);
+  wave_desc[2 * w + 1] = make_int4(c1, d.x, d.y, d.z);
+}
+
+// Waves wf .. wl hold the head's tiles [c0, c1) (c1 > c0); bit i of the mask
+// says whether wave wf + i has a non-empty range (waves past 32 are looked up
+// by the merge itself).
+__device__ inline int4 head_waves_of(const int32_t* bounds, int W, int c0, int c1) {
+  int lo = 0, hi = W - 1;            // largest w with bounds[w] <= c0
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (bounds[mid] <= c0) lo = mid; else hi = mid - 1;
   }
+  const int wf = lo;
+  lo = wf; hi = W - 1;               // smallest w with bounds[w + 1] >= c1
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (bounds[mid + 1] >= c1) hi = mid; else lo = mid + 1;
+  }
+  const int wl = lo;
+  int mask = 0;
+  for (int i = 0; i < 32 && wf + i <= wl; ++i)
+    if (bounds[wf + i] < bounds[wf + i + 1]) mask |= 1 << i;
+  return make_int4(wf, wl, mask, 0);
+}
+
+// Tile range of every decode wave: equal contiguous shares of the flat tile
+// list (heads that straddle a boundary are merged by the decode kernel),
+// each wave's first-segment descriptor, and every head's wave span.
+__device__ void wave_ranges(const PlanArgs& a, int NH) {
+  const int32_t* cum = a.cum_tiles;
+  const int total = cum[NH], W = a.W;
+  for (int w = threadIdx.x; w <= W; w += blockDim.x)
+    a.wave_bounds[w] = static_cast<int>(static_cast<int64_t>(w) * total / W);
+  for (int w = threadIdx.x; w < W; w += blockDim.x) {
+    const int tb = static_cast<int>(static_cast<int64_t>(w) * total / W);
+    const int te = static_cast<int>(static_cast<int64_t>(w + 1) * total / W);
+    if (tb < te) {
+      const int hh = min(upper_index(cum, NH, tb), NH - 1);
+      put_wave_desc(a.wave_desc, w, tb, te, hh, cum[hh], cum[hh + 1], a.desc[hh]);
+    }
+  }
+  __syncthreads();  // bounds visible to the searches below
+  for (int hh = threadIdx.x; hh < NH; hh += blockDim.x)
+    if (cum[hh + 1] > cum[hh]) a.head_waves[hh] = head_waves_of(a.wave_bounds, W, cum[hh], cum[hh + 1]);
 }
 
 // Decision of the token appended for call head hh: the caller's flag, or
@@ -303,14 +344,24 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(PlanArgs a) {
     if (a.append) *a.st.top = top0 - tot.x;
   }
   if (a.W > 0) {
-    // wave w starts at tile floor(w * total / W); the head holding tile b
-    // owns every wave w with ceil(c0 * W / total) <= w < ceil(c1 * W / total)
+    // wave w starts at tile floor(w * total / W); the head holding tiles
+    // [c0, c1) is where every wave w with ceil(c0 * W / total) <= w <
+    // ceil(c1 * W / total) starts, and its tiles lie in waves
+    // ceil((c0 + 1) * W / total) - 1 .. ceil(c1 * W / total) - 1
     const int64_t total = tot.y, W = a.W;
-    for (int w = tid; w <= a.W; w += blockDim.x) a.wave_bounds[w] = static_cast<int>(w * total / W);
+    auto bound = [&](int64_t w) { return static_cast<int>(w * total / W); };
+    for (int w = tid; w <= a.W; w += blockDim.x) a.wave_bounds[w] = bound(w);
     if (act && c1 > c0) {
       const int w0 = static_cast<int>((c0 * W + total - 1) / total);
       const int w1 = min(a.W, static_cast<int>((c1 * W + total - 1) / total));
-      for (int w = w0; w < w1; ++w) a.wave_head[w] = tid;
+      const int4 d = make_int4(Lnew, sh, slot, 0);
+      for (int w = w0; w < w1; ++w) put_wave_desc(a.wave_desc, w, bound(w), bound(w + 1), tid, c0, c1, d);
+      const int wf = static_cast<int>(((c0 + 1) * W + total - 1) / total) - 1;
+      const int wl = min(a.W - 1, w1 - 1);
+      int mask = 0;
+      for (int i = 0; i < 32 && wf + i <= wl; ++i)
+        if (bound(wf + i) < bound(wf + i + 1)) mask |= 1 << i;
+      a.head_waves[tid] = make_int4(wf, wl, mask, 0);
     }
   }
 }
@@ -397,7 +448,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
     for (int i = threadIdx.x; i < a.n; i += blockDim.x) a.st.pos[a.seq_ids[i]] += 1;
     if (threadIdx.x == 0) *a.st.top = top0 - total_need;
   }
-  if (a.W > 0) wave_ranges(a.cum_tiles, NH, a.W, a.wave_bounds, a.wave_head);
+  if (a.W > 0) wave_ranges(a, NH);
 }
 
 // Copy each appended token's K row and V column into its slot.
@@ -713,7 +764,8 @@ hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* 
   a.g = c.group_size;
   a.D = c.head_dim;
   a.wave_bounds = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_wave_bounds);
-  a.wave_head = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_wave_head);
+  a.wave_desc = reinterpret_cast<int4*>(static_cast<char*>(ws) + lo.ws_wave_desc);
+  a.head_waves = reinterpret_cast<int4*>(static_cast<char*>(ws) + lo.ws_head_waves);
   a.out = out;
   a.W = waves;
   a.gD = c.group_size * c.head_dim;

@@ -29,7 +29,7 @@ struct Layout {
   size_t page_bytes, pool_bytes;
   // workspace
   size_t ws_head_desc, ws_cum_tiles, ws_part_ml, ws_part_acc;
-  size_t ws_wave_bounds, ws_wave_head, ws_head_cnt;
+  size_t ws_wave_bounds, ws_wave_desc, ws_head_waves, ws_head_cnt;
   size_t ws_ck_need, ws_ck_fresh, ws_ck_base, ws_ck_pos0, ws_ck_err, ws_ck_slot;
   size_t ws_pf_cum, ws_pf_meta, ws_pf_tiles, ws_pf_flags;
   int pf_tiles_per_head;   // tiles of one (region, KV head) in ws_pf_tiles

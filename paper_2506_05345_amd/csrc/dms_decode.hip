@@ -296,12 +296,12 @@ __device__ void merge_head(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsr
 // is issued in one round; weights are passed between lanes by shuffles.
 template <int D>
 __device__ void merge_head_small(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsrc,
-                                 const int32_t* wave_bounds, float* out, int wf, int np, int hh,
+                                 int live_mask, float* out, int wf, int np, int hh,
                                  int g, int lane) {
   constexpr int kMaxPieces = kMaxGroup * D / 4 / 64;
   constexpr int kMaxParts = 4;
   const int pieces = g * D / 4;
-  const bool live = lane < np && wave_bounds[wf + lane] < wave_bounds[wf + lane + 1];
+  const bool live = lane < np && ((live_mask >> lane) & 1);
   const float* ml = reinterpret_cast<const float*>(
       part_ml + (static_cast<size_t>(wf + (lane < np ? lane : 0)) + hh) * kMaxGroup);
   float m[kMaxGroup], l[kMaxGroup];
@@ -359,31 +359,46 @@ template <int D>
 __global__ __launch_bounds__(256, 1) void decode_kernel(
     const int32_t* __restrict__ status, const HeadDesc* __restrict__ desc,
     const int32_t* __restrict__ cum_tiles, const int32_t* __restrict__ wave_bounds,
-    const int32_t* __restrict__ wave_head, int32_t* __restrict__ head_cnt,
+    const int4* __restrict__ wave_desc, const int4* __restrict__ head_waves,
+    int32_t* __restrict__ head_cnt,
     const int32_t* __restrict__ page_table,
     char* __restrict__ pool, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_in,
     const uint16_t* __restrict__ v_in, float2* __restrict__ part_ml, float* __restrict__ part_acc,
     float* __restrict__ out, DecodeParams a) {
   __shared__ float merge_wts[kWavesPerBlock][kMergeBatch][kMaxGroup];
-  if (load_status(status) != 0) return;
   const int lane = threadIdx.x & 63;
   // wave index is uniform across the wave; say so, so that everything derived
   // from it (head, tile, page) lives in scalar registers
   const int wave = blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, G = lane >> 4;
+  // the planner's descriptor of this wave's first segment comes with the
+  // range, so a wave starts after one round of scalar loads
+  const int4 wd0 = wave_desc[2 * wave], wd1 = wave_desc[2 * wave + 1];
   int tb = wave_bounds[wave];
   const int te = wave_bounds[wave + 1];
+  if (load_status(status) != 0) return;
   if (tb >= te) return;
   LaneOff lo;
   lo.k = static_cast<uint32_t>((8 * (r >> 2) + (r & 3)) * 64 + 16 * G);
   lo.v = static_cast<uint32_t>(D * 64 + r * 64 + 16 * G);
-  int hh = wave_head[wave];
+  int hh = wd0.z;
   const int tiles_per_page_log2 = a.log2P - 5;
+  bool first = true;
   while (tb < te) {
-    while (cum_tiles[hh + 1] <= tb) ++hh;
-    const int c0 = cum_tiles[hh], c1 = cum_tiles[hh + 1];
+    int c0, c1;
+    HeadDesc d;
+    if (first) {
+      c0 = wd0.w;
+      c1 = wd1.x;
+      d = make_int4(wd1.y, wd1.z, wd1.w, 0);
+      first = false;
+    } else {
+      while (cum_tiles[hh + 1] <= tb) ++hh;
+      c0 = cum_tiles[hh];
+      c1 = cum_tiles[hh + 1];
+      d = desc[hh];
+    }
     const int seg_end = min(te, c1);
-    const HeadDesc d = desc[hh];
     const int L = d.x;
     const int32_t* pt = page_table + static_cast<size_t>(d.y) * a.maxp;
     // query fragments (B operand): column r = query head r of the group
@@ -480,16 +495,15 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
           __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc.o[b]), acc_rsrc,
                                                  o + 64 * b, 0, kCachePolicySc1);
       }
+      const int4 hw = head_waves[hh];   // waves wf .. wl hold the head's tiles
       __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
       int prev = 0;
       if (lane == 0) prev = atomicAdd(&head_cnt[hh], seg_end - tb);
       prev = __shfl(prev, 0, 64);
       if (prev + (seg_end - tb) == c1 - c0) {
-        int wf = wave, wl = wave;
-        while (wave_bounds[wf] > c0) --wf;
-        while (wave_bounds[wl + 1] < c1) ++wl;
+        const int wf = hw.x, wl = hw.y;
         if (wl - wf < 4)
-          merge_head_small<D>(part_ml, acc_rsrc, wave_bounds, out, wf, wl - wf + 1, hh, a.g, lane);
+          merge_head_small<D>(part_ml, acc_rsrc, hw.z, out, wf, wl - wf + 1, hh, a.g, lane);
         else
           merge_head<D>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, a.g, lane,
                         merge_wts[threadIdx.x >> 6]);
@@ -525,7 +539,8 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
   hipLaunchKernelGGL(decode_kernel<D>, dim3(waves / kWavesPerBlock), dim3(256), 0, st, status,
                      reinterpret_cast<const HeadDesc*>(w + lo.ws_head_desc), cum,
                      reinterpret_cast<const int32_t*>(w + lo.ws_wave_bounds),
-                     reinterpret_cast<const int32_t*>(w + lo.ws_wave_head),
+                     reinterpret_cast<const int4*>(w + lo.ws_wave_desc),
+                     reinterpret_cast<const int4*>(w + lo.ws_head_waves),
                      reinterpret_cast<int32_t*>(w + lo.ws_head_cnt),
                      layer_state(lo, meta, layer).page_table, static_cast<char*>(pool),
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),

@@ -128,6 +128,26 @@ def test_ragged_multi_sequence(d, g, w, P, p):
     compare_pool(cache, 0, cache.export(0), seqs, inp)
 
 
+def test_many_heads_multi_pass_planner():
+    """320 sequences x 4 KV heads = 1280 heads per call: more heads than one
+    planning block has threads, so the multi-pass planner runs; ragged short
+    contexts, some heads longer than one decode wave's share."""
+    H, g, d, w, P = 4, 2, 64, 16, 32
+    rng = np.random.default_rng(77)
+    seqs = [int(s) for s in rng.permutation(320)]
+    lens = {s: int(rng.integers(1, 260)) for s in seqs}
+    lens[seqs[5]] = 3000          # one long sequence: its heads span several waves
+    dms, cfg, cache = _mk(dict(num_layers=1, max_seqs=320, num_kv_heads=H, group_size=g,
+                               head_dim=d, window=w, page_size=P, num_pages=12000,
+                               max_pages_per_head=128, max_chunk_tokens=320 * 256))
+    inp = {s: SeqInputs(13, 0, s, lens[s] + 6, H, g, d, 0.6) for s in seqs}
+    orc = _oracle_for(cfg)
+    _append_chunks(dms, cache, orc, seqs, inp, {s: 0 for s in seqs}, lens, 256)
+    compare_state(cache.export(0), orc, seqs)
+    _decode_steps(dms, cache, orc, seqs, inp, lens, 6, g, check_every=2, dense_check=False)
+    cache.close()
+
+
 def test_decode_from_empty_cache_token_by_token():
     """Every token through dms_decode_step from position 0 (first steps have a
     single visible key, the output is that value exactly up to rounding)."""
