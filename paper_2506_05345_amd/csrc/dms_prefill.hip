@@ -22,9 +22,9 @@
 // Attention pass: a workgroup (4 waves) owns one (sequence, KV head, block of
 // query positions).  Its columns are (position, query head) pairs packed 16
 // to an MFMA column block (16 / g positions x g heads); each wave holds NQ
-// column blocks.  Key tiles of 32 are staged into LDS (16-byte chunks
-// swizzled against bank conflicts), double buffered, and read by every wave
-// with 16-byte LDS loads straight into MFMA operand registers.  A tile is
+// column blocks.  Key tiles of 32 are staged into LDS in the order the MFMA
+// operand loads consume them (no bank conflicts), double buffered, and read
+// by every wave with 16-byte LDS loads straight into operand registers.  A tile is
 // masked per element only when some query of the block does not see one of
 // its keys; the online softmax works in the exp2 domain with a lazy rescale.
 #include "dms_common.h"
@@ -44,13 +44,26 @@ constexpr float kMInit = -1.0e30f;        // running max before the first visibl
 typedef __attribute__((ext_vector_type(2))) float f32x2;
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 
-// LDS tiles keep the pool's tile layout (64-byte rows: key rows of one
-// 32-dim slice, value rows of one dim), with the four 16-byte chunks of row
-// `row` stored in the order c ^ swz(row).  One MFMA operand load reads chunk G
-// of the rows 8(r/4) + r%4 (keys) or r (values) for r = 0..15, G = 0..3; the
-// swizzle puts every 8 and every 16 consecutive lanes on distinct banks.
-__device__ inline int swz_k(int j) { return ((j >> 3) & 3) ^ (((j >> 1) & 1) << 1); }
-__device__ inline int swz_v(int e) { return ((e >> 2) & 3) ^ (((e >> 1) & 1) << 1); }
+// LDS tile layout.  A wave's MFMA operand load -- lane (r, G) = (lane % 16,
+// lane / 16) takes 16 bytes -- is free of bank conflicts when the 64 lanes
+// read one contiguous 1 KB block in lane order (measured on gfx950; rows of
+// 64 bytes read column-wise are not).  So the tile is laid out in LDS in the
+// order the fragment loads consume it:
+//   keys, per 32-dim slice s (2 KB): two 1 KB halves, half h holding tile rows
+//     j = (r % 4) + 8 (r / 4) + 4 h for r = 0..15 (the rows of the first /
+//     second score MFMA), each as [chunk G][r][16 B];
+//   values (V^T), per block of 16 dims b (1 KB): [key chunk G][dim r][16 B].
+// Fragment loads are then base + lane * 16, and staging writes are too: each
+// thread fetches from the pool-layout tile the piece its LDS slot holds.
+__device__ inline int k_src(int P) {   // pool-layout offset of key LDS slot P
+  const int r = P & 15, c = (P >> 4) & 3, h = (P >> 6) & 1;
+  return (P >> 7) * 2048 + ((r & 3) + 8 * (r >> 2) + 4 * h) * 64 + c * 16;
+}
+template <int D>
+__device__ inline int v_src(int P) {   // pool-layout offset of value LDS slot P
+  const int r = P & 15, G = (P >> 4) & 3;
+  return D * 64 + (16 * (P >> 6) + r) * 64 + G * 16;
+}
 
 // max over the four lanes r, r + 16, r + 32, r + 48 (the key rows of one column)
 __device__ inline float col_max(float x) {
@@ -315,8 +328,8 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
     }
 #pragma unroll
     for (int m = 0; m < KP; ++m) {
-      stg.kx[m] = *reinterpret_cast<const u32x4*>(tile + (tid + m * kThreads) * 16);
-      stg.vx[m] = *reinterpret_cast<const u32x4*>(tile + D * 64 + (tid + m * kThreads) * 16);
+      stg.kx[m] = *reinterpret_cast<const u32x4*>(tile + k_src(tid + m * kThreads));
+      stg.vx[m] = *reinterpret_cast<const u32x4*>(tile + v_src<D>(tid + m * kThreads));
     }
   };
   auto stage_store = [&](int k, int buf) {
@@ -326,19 +339,17 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
     const int valid = k < nc ? min(32, L0 - k * 32) : 32;
 #pragma unroll
     for (int m = 0; m < KP; ++m) {
-      const int off = (tid + m * kThreads) * 16;
-      const int row = (off & 2047) >> 6, ch = (off & 63) >> 4;
-      *reinterpret_cast<u32x4*>(dst + (off & ~63) + ((ch ^ swz_k(row)) << 4)) = stg.kx[m];
+      const int P = tid + m * kThreads;
+      *reinterpret_cast<u32x4*>(dst + P * 16) = stg.kx[m];
       u32x4 x = stg.vx[m];
-      // element i of the piece is key row (off % 64) / 2 + i
-      const int j0 = (off & 63) >> 1;
+      // element i of the value piece is key row 8 G + i
+      const int j0 = 8 * ((P >> 4) & 3);
       if (j0 + 8 > valid) {
 #pragma unroll
         for (int e = 0; e < 8; ++e)
           if (j0 + e >= valid) x[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
       }
-      const int vrow = off >> 6;
-      *reinterpret_cast<u32x4*>(dst + D * 64 + (off & ~63) + ((ch ^ swz_v(vrow)) << 4)) = x;
+      *reinterpret_cast<u32x4*>(dst + D * 64 + P * 16) = x;
     }
     if (tid < 64) {
       // a key row needs the per-element mask iff some query t in [t0, t1)
@@ -366,9 +377,8 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
     m_ref[qb] = kMInit;
     l_run[qb] = 0.f;
   }
-  const int krow = 8 * (r >> 2) + (r & 3);
-  const uint32_t lo_k = static_cast<uint32_t>(krow * 64 + ((G ^ swz_k(krow)) << 4));
-  const uint32_t lo_v = static_cast<uint32_t>(D * 64 + r * 64 + ((G ^ swz_v(r)) << 4));
+  const uint32_t lo_k = static_cast<uint32_t>(lane * 16);
+  const uint32_t lo_v = static_cast<uint32_t>(D * 64 + lane * 16);
   const float thr = kRescale / a.scale_log2;   // rescale threshold in score units
 
   if (ntiles > 0) {
@@ -385,7 +395,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
     for (int s2 = 0; s2 < D / 32; ++s2) {
       f.ka[s2] = *reinterpret_cast<const u32x4*>(tl + lo_k + s2 * 2048);
-      f.kb[s2] = *reinterpret_cast<const u32x4*>(tl + lo_k + 256 + s2 * 2048);
+      f.kb[s2] = *reinterpret_cast<const u32x4*>(tl + lo_k + 1024 + s2 * 2048);
     }
 #pragma unroll
     for (int b = 0; b < D / 16; ++b) f.vt[b] = *reinterpret_cast<const u32x4*>(tl + lo_v + b * 1024);
