@@ -18,7 +18,10 @@ Compression", arxiv 2506.05345):
   every query head that reads the KV head; outputs are softmax attention.
 * Gradients of the attention output with respect to q, k, v and alpha, and
   of alpha with respect to its logit, come from automatic differentiation
-  of these plain float64 definitions (torch on the CPU).
+  of these plain float64 definitions (torch on the CPU).  For alpha the
+  attention is written with the mask as weights (1 - alpha_j), the same
+  function, so that at alpha_j = 1 the gradient is the finite derivative
+  from below rather than 0 * inf.
 """
 from __future__ import annotations
 
@@ -103,8 +106,39 @@ def train_attention(q, k, v, alpha, w, group, scale=None):
     return O.numpy(), L.numpy()
 
 
+def _torch_attention_weights(q, k, v, alpha, w, group, scale):
+    """The same attention with the mask applied as weights: softmax with the
+    additive bias log(1 - alpha_j) equals exp(score) * (1 - alpha_j)
+    renormalised.  Automatic differentiation of this form gives the finite
+    one-sided derivative at alpha_j = 1 (where d log(1 - alpha) / d alpha is
+    infinite and the additive form yields 0 * inf)."""
+    import torch
+    B, T, Hq, d = q.shape
+    Hkv = Hq // group
+    t = torch.arange(T)[:, None]
+    j = torch.arange(T)[None, :]
+    causal = j > t
+    window = j > t - w
+    outs = []
+    for h in range(Hkv):
+        a = alpha[:, :, h]
+        keep = (1.0 - a)[:, None, :].expand(B, T, T)
+        mult = torch.where(window, torch.ones_like(keep), keep)
+        mult = torch.where(causal, torch.zeros_like(mult), mult)
+        for qh in range(h * group, (h + 1) * group):
+            s = torch.einsum("btd,bjd->btj", q[:, :, qh], k[:, :, h]) * scale
+            s = torch.where(causal, torch.full_like(s, -math.inf), s)
+            m = s.max(dim=-1, keepdim=True).values.detach()
+            p = torch.exp(s - m) * mult
+            o = torch.einsum("btj,bjd->btd", p, v[:, :, h]) / p.sum(dim=-1, keepdim=True)
+            outs.append((qh, o))
+    outs.sort(key=lambda x: x[0])
+    return torch.stack([o for _, o in outs], dim=2)
+
+
 def train_attention_grads(q, k, v, alpha, dout, w, group, scale=None):
-    """(dq, dk, dv, dalpha) of sum(O * dout) by autograd of the definition."""
+    """(dq, dk, dv, dalpha) of sum(O * dout) by autograd of the definition
+    (weights form; at alpha_j = 1 dalpha_j is the derivative from below)."""
     import torch
     q = torch.tensor(np.asarray(q, np.float64), requires_grad=True)
     k = torch.tensor(np.asarray(k, np.float64), requires_grad=True)
@@ -112,6 +146,6 @@ def train_attention_grads(q, k, v, alpha, dout, w, group, scale=None):
     a = torch.tensor(np.asarray(alpha, np.float64), requires_grad=True)
     if scale is None:
         scale = 1.0 / math.sqrt(q.shape[-1])
-    O, _ = _torch_attention(q, k, v, a, w, group, scale)
+    O = _torch_attention_weights(q, k, v, a, w, group, scale)
     (O * torch.as_tensor(np.asarray(dout, np.float64))).sum().backward()
     return q.grad.numpy(), k.grad.numpy(), v.grad.numpy(), a.grad.numpy()

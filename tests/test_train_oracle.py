@@ -96,6 +96,34 @@ def test_gradients_match_finite_differences(seed):
     assert np.all(da[:, T - w:, :] == 0)
 
 
+def _grad_at_hard_decisions_ok():
+    """At alpha_j in {0, 1} (the ends of its range) the decision gradient is
+    the one-sided derivative of the forward definition: second-order one-sided
+    differences of the output, stepping into [0, 1]."""
+    B, T, H, g, d, w = 1, 10, 1, 2, 4, 2
+    q, k, v, rng = _rand(31, B, T, H, g, d)
+    a = (rng.uniform(size=(B, T, H)) < 0.5).astype(np.float64)
+    dout = rng.normal(size=(B, T, H * g, d))
+    _, _, _, da = oracle.train_attention_grads(q, k, v, a, dout, w, g)
+    if not np.isfinite(da).all():
+        return False
+    f = lambda aa: float((oracle.train_attention(q, k, v, aa, w, g)[0] * dout).sum())
+    h = 1e-4
+    for j in range(T - w):
+        step = -h if a[0, j, 0] == 1.0 else h
+        a1, a2 = a.copy(), a.copy()
+        a1[0, j, 0] += step
+        a2[0, j, 0] += 2 * step
+        fd = (-3 * f(a) + 4 * f(a1) - f(a2)) / (2 * step)
+        if abs(fd - da[0, j, 0]) > 1e-6 * max(1.0, abs(fd)):
+            return False
+    return True
+
+
+def test_gradient_at_hard_decisions_is_the_one_sided_derivative():
+    assert _grad_at_hard_decisions_ok()
+
+
 def test_logistic_noise_inverts_the_logistic_cdf():
     u = (np.arange(1, 2000) + 0.5) / 2001
     L = oracle.logistic_noise(u)
@@ -151,7 +179,7 @@ def test_pins_pass_unmodified():
 
 
 @pytest.mark.parametrize("mutant", ["inclusive_window", "log_alpha", "no_scale", "tau_times",
-                                    "noise_sign"])
+                                    "noise_sign", "weights_alpha"])
 def test_planted_mistake_is_caught(monkeypatch, mutant):
     mod = oracle.train_oracle
     orig_attn = mod._torch_attention
@@ -166,6 +194,12 @@ def test_planted_mistake_is_caught(monkeypatch, mutant):
     elif mutant == "tau_times":
         monkeypatch.setattr(mod, "gumbel_sigmoid", lambda x, u, tau: 1.0 / (1.0 + np.exp(
             -(np.asarray(x, np.float64) + mod.logistic_noise(u)) * tau)))
+    elif mutant == "weights_alpha":
+        orig_w = mod._torch_attention_weights
+        monkeypatch.setattr(mod, "_torch_attention_weights",
+                            lambda q, k, v, a, w, g, s: orig_w(q, k, v, 1.0 - a, w, g, s))
+        assert not _grad_at_hard_decisions_ok()
+        return
     elif mutant == "noise_sign":
         monkeypatch.setattr(mod, "logistic_noise", lambda u: np.log1p(-np.asarray(u, np.float64)) - np.log(u))
     for name in ("gumbel_sigmoid", "logistic_noise", "train_attention"):
