@@ -292,6 +292,62 @@ int dms_profile_stop(dms_ctx* ctx, float* ms_out, int* launches_out);
 /* Static description of an error code. */
 const char* dms_strerror(int code);
 
+/*
+ * Training-time DMS attention (retrofitting, Sec. 3.1)
+ * -----------------------------------------------------
+ * During retrofitting every token j of every KV head carries a continuous
+ * decision alpha_j in [0, 1] (Eq. 1: a Gumbel-sigmoid of the decision
+ * logit), and attention adds the mask M_alpha of Fig. 1b to the scaled
+ * scores: -inf for keys after the query, 0 for the w most recent positions
+ * (j > t - w), log(1 - alpha_j) for older keys (alpha_j = 1 hides the key).
+ * Every sequence of a call has T tokens.  Layouts (row-major, dense):
+ *   q, dout   bf16 [B, T, Hq, d]       k, v      bf16 [B, T, Hkv, d]
+ *   alpha     f32  [B, T, Hkv]         out       f32  [B, T, Hq, d]
+ *   lse       f32  [B, Hq, T]  natural log of each softmax denominator
+ *   dq        f32  [B, T, Hq, d]       dk, dv    f32  [B, T, Hkv, d]
+ *   dalpha    f32  [B, T, Hkv]
+ * Query head q reads KV head q / g.  Gradients are of sum(out * dout) and
+ * overwrite their buffers.  The workspace (dms_train_workspace bytes) holds
+ * tiled copies of the inputs; it and every buffer belong to the caller, and
+ * one workspace serves one stream at a time.  Errors: DMS_ERR_INVALID /
+ * DMS_ERR_UNSUPPORTED (host checks, nothing launched) or DMS_ERR_HIP.
+ */
+typedef struct dms_train_config {
+  int32_t batch;          /* B >= 1 */
+  int32_t seq_len;        /* T >= 1 */
+  int32_t num_kv_heads;   /* Hkv >= 1 */
+  int32_t group_size;     /* g = Hq / Hkv, 1 .. 16 */
+  int32_t head_dim;       /* d: 128 */
+  int32_t window;         /* w >= 1 */
+  float softmax_scale;    /* <= 0 selects 1 / sqrt(head_dim) */
+} dms_train_config;
+
+int dms_train_workspace(const dms_train_config* cfg, size_t* workspace_bytes);
+
+/* Forward: out and lse from q, k, v and the decisions. */
+int dms_train_attention_fwd(const dms_train_config* cfg, const void* q_dev, const void* k_dev,
+                            const void* v_dev, const float* alpha_dev, float* out_dev,
+                            float* lse_dev, void* workspace_dev, void* stream);
+
+/* Backward: dq, dk, dv, dalpha from the forward's inputs, out, lse and dout
+ * (bf16).  The decision gradient is -sum_t exp(s_tj - lse_t) (dP_tj - D_t)
+ * over query positions t >= j + w, finite also where alpha_j = 1. */
+int dms_train_attention_bwd(const dms_train_config* cfg, const void* q_dev, const void* k_dev,
+                            const void* v_dev, const float* alpha_dev, const float* out_dev,
+                            const float* lse_dev, const void* dout_dev, float* dq_dev,
+                            float* dk_dev, float* dv_dev, float* dalpha_dev,
+                            void* workspace_dev, void* stream);
+
+/* Gumbel-sigmoid of Eq. 1: alpha = sigmoid((logit + log u - log(1 - u)) / tau)
+ * for n elements, u in (0, 1) supplied by the caller (u = 0.5 gives the
+ * noise-free sigmoid); tau > 0. */
+int dms_gumbel_sigmoid_fwd(int n, const float* logits_dev, const float* u_dev, float tau,
+                           float* alpha_dev, void* stream);
+
+/* dlogit = dalpha * alpha (1 - alpha) / tau. */
+int dms_gumbel_sigmoid_bwd(int n, const float* alpha_dev, const float* dalpha_dev, float tau,
+                           float* dlogits_dev, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdms.so")
-SOURCES = ["dms_api.hip", "dms_cache.hip", "dms_decode.hip", "dms_prefill.hip"]
+SOURCES = ["dms_api.hip", "dms_cache.hip", "dms_decode.hip", "dms_prefill.hip", "dms_train.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 instructions are kept out of every kernel.
@@ -19,7 +19,7 @@ COMMON = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}", "-Wall",
           "-Wno-unused-function", "-munsafe-fp-atomics"]
 # The prefill softmax never forms a NaN (hidden scores are -inf and give exact
 # zeros), so its max reductions need no NaN quieting.
-PER_SOURCE = {"dms_prefill.hip": ["-fno-honor-nans"]}
+PER_SOURCE = {"dms_prefill.hip": ["-fno-honor-nans"], "dms_train.hip": ["-fno-honor-nans"]}
 
 
 def hipcc() -> str:

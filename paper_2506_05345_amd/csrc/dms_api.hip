@@ -476,4 +476,73 @@ const char* dms_strerror(int code) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Training-time attention
+// ---------------------------------------------------------------------------
+
+static int validate_train_config(const dms_train_config* c) {
+  if (!c) return DMS_ERR_INVALID;
+  if (c->batch < 1 || c->seq_len < 1 || c->num_kv_heads < 1 || c->group_size < 1 || c->window < 1)
+    return DMS_ERR_INVALID;
+  if (c->group_size > dms::kMaxGroup) return DMS_ERR_UNSUPPORTED;
+  if (c->head_dim != dms::kTrainHeadDim) return DMS_ERR_UNSUPPORTED;
+  if (isnan(c->softmax_scale) || (c->softmax_scale > 0.0f && !isfinite(c->softmax_scale)))
+    return DMS_ERR_INVALID;
+  // element offsets of the largest tensors stay below 2^31 rows of head_dim
+  const int64_t rows = static_cast<int64_t>(c->batch) * c->seq_len * c->num_kv_heads * c->group_size;
+  if (rows >= (int64_t(1) << 31) / 8) return DMS_ERR_INVALID;
+  // one grid row per (sequence, KV head)
+  if (static_cast<int64_t>(c->batch) * c->num_kv_heads > 65535) return DMS_ERR_INVALID;
+  return DMS_OK;
+}
+
+int dms_train_workspace(const dms_train_config* cfg, size_t* workspace_bytes) {
+  const int rc = validate_train_config(cfg);
+  if (rc) return rc;
+  if (workspace_bytes) *workspace_bytes = dms::train_workspace_bytes(*cfg);
+  return DMS_OK;
+}
+
+int dms_train_attention_fwd(const dms_train_config* cfg, const void* q_dev, const void* k_dev,
+                            const void* v_dev, const float* alpha_dev, float* out_dev,
+                            float* lse_dev, void* workspace_dev, void* stream) {
+  const int rc = validate_train_config(cfg);
+  if (rc) return rc;
+  if (!q_dev || !k_dev || !v_dev || !alpha_dev || !out_dev || !lse_dev || !workspace_dev)
+    return DMS_ERR_INVALID;
+  return hip_rc(dms::launch_train_fwd(*cfg, q_dev, k_dev, v_dev, alpha_dev, out_dev, lse_dev,
+                                      workspace_dev, as_stream(stream)));
+}
+
+int dms_train_attention_bwd(const dms_train_config* cfg, const void* q_dev, const void* k_dev,
+                            const void* v_dev, const float* alpha_dev, const float* out_dev,
+                            const float* lse_dev, const void* dout_dev, float* dq_dev,
+                            float* dk_dev, float* dv_dev, float* dalpha_dev,
+                            void* workspace_dev, void* stream) {
+  const int rc = validate_train_config(cfg);
+  if (rc) return rc;
+  if (!q_dev || !k_dev || !v_dev || !alpha_dev || !out_dev || !lse_dev || !dout_dev || !dq_dev ||
+      !dk_dev || !dv_dev || !dalpha_dev || !workspace_dev)
+    return DMS_ERR_INVALID;
+  return hip_rc(dms::launch_train_bwd(*cfg, q_dev, k_dev, v_dev, alpha_dev, out_dev, lse_dev,
+                                      dout_dev, dq_dev, dk_dev, dv_dev, dalpha_dev, workspace_dev,
+                                      as_stream(stream)));
+}
+
+int dms_gumbel_sigmoid_fwd(int n, const float* logits_dev, const float* u_dev, float tau,
+                           float* alpha_dev, void* stream) {
+  if (n < 0 || !(tau > 0.f) || !isfinite(tau)) return DMS_ERR_INVALID;
+  if (n == 0) return DMS_OK;
+  if (!logits_dev || !u_dev || !alpha_dev) return DMS_ERR_INVALID;
+  return hip_rc(dms::launch_gumbel_fwd(n, logits_dev, u_dev, tau, alpha_dev, as_stream(stream)));
+}
+
+int dms_gumbel_sigmoid_bwd(int n, const float* alpha_dev, const float* dalpha_dev, float tau,
+                           float* dlogits_dev, void* stream) {
+  if (n < 0 || !(tau > 0.f) || !isfinite(tau)) return DMS_ERR_INVALID;
+  if (n == 0) return DMS_OK;
+  if (!alpha_dev || !dalpha_dev || !dlogits_dev) return DMS_ERR_INVALID;
+  return hip_rc(dms::launch_gumbel_bwd(n, alpha_dev, dalpha_dev, tau, dlogits_dev, as_stream(stream)));
+}
+
 }  // extern "C"

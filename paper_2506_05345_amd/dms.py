@@ -47,6 +47,18 @@ class DmsConfig(ctypes.Structure):
     ]
 
 
+class DmsTrainConfig(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("seq_len", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("group_size", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("window", ctypes.c_int32),
+        ("softmax_scale", ctypes.c_float),
+    ]
+
+
 DMS_EVICT_DELAYED = 0
 DMS_EVICT_IMMEDIATE = 1
 DMS_DECIDE_CALLER = 0
@@ -93,6 +105,13 @@ _SIGS = {
     "dms_profile_start": (_I, [_VP, _I]),
     "dms_profile_stop": (_I, [_VP, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(_I)]),
     "dms_strerror": (ctypes.c_char_p, [_I]),
+    "dms_train_workspace": (_I, [ctypes.POINTER(DmsTrainConfig), ctypes.POINTER(_SZ)]),
+    "dms_train_attention_fwd": (_I, [ctypes.POINTER(DmsTrainConfig), _VP, _VP, _VP, _VP, _VP, _VP,
+                                     _VP, _VP]),
+    "dms_train_attention_bwd": (_I, [ctypes.POINTER(DmsTrainConfig), _VP, _VP, _VP, _VP, _VP, _VP,
+                                     _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
+    "dms_gumbel_sigmoid_fwd": (_I, [_I, _VP, _VP, ctypes.c_float, _VP, _VP]),
+    "dms_gumbel_sigmoid_bwd": (_I, [_I, _VP, _VP, ctypes.c_float, _VP, _VP]),
 }
 
 
@@ -345,3 +364,42 @@ def unpack_page(u16, P, D):
     k = tiles[:, 0].reshape(P // 32, D // 32, 32, 32).transpose(0, 2, 1, 3).reshape(P, D)
     v = tiles[:, 1].reshape(P // 32, D, 32).transpose(0, 2, 1).reshape(P, D)
     return k, v
+
+
+# ---------------------------------------------------------------------------
+# Training-time attention (continuous decisions)
+# ---------------------------------------------------------------------------
+
+def make_train_config(batch, seq_len, num_kv_heads, group_size, head_dim, window,
+                      softmax_scale=0.0) -> DmsTrainConfig:
+    return DmsTrainConfig(batch, seq_len, num_kv_heads, group_size, head_dim, window, softmax_scale)
+
+
+def dms_train_workspace(cfg: DmsTrainConfig) -> int:
+    n = _SZ()
+    _check(lib().dms_train_workspace(ctypes.byref(cfg), ctypes.byref(n)), "dms_train_workspace")
+    return n.value
+
+
+def dms_train_attention_fwd(cfg, q, k, v, alpha, out, lse, workspace, stream=None):
+    _check(lib().dms_train_attention_fwd(ctypes.byref(cfg), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha),
+                                         _ptr(out), _ptr(lse), _ptr(workspace), _stream(stream)),
+           "dms_train_attention_fwd")
+
+
+def dms_train_attention_bwd(cfg, q, k, v, alpha, out, lse, dout, dq, dk, dv, dalpha, workspace,
+                            stream=None):
+    _check(lib().dms_train_attention_bwd(ctypes.byref(cfg), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha),
+                                         _ptr(out), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk),
+                                         _ptr(dv), _ptr(dalpha), _ptr(workspace), _stream(stream)),
+           "dms_train_attention_bwd")
+
+
+def dms_gumbel_sigmoid_fwd(n, logits, u, tau, alpha, stream=None):
+    _check(lib().dms_gumbel_sigmoid_fwd(n, _ptr(logits), _ptr(u), tau, _ptr(alpha), _stream(stream)),
+           "dms_gumbel_sigmoid_fwd")
+
+
+def dms_gumbel_sigmoid_bwd(n, alpha, dalpha, tau, dlogits, stream=None):
+    _check(lib().dms_gumbel_sigmoid_bwd(n, _ptr(alpha), _ptr(dalpha), tau, _ptr(dlogits),
+                                        _stream(stream)), "dms_gumbel_sigmoid_bwd")

@@ -159,3 +159,46 @@ def test_unpack_page_matches_documented_offsets():
         for e in (0, 7, 31, 32, 100, 127):
             assert k[s, e] == 1000 + s * 200 + e
             assert v[s, e] == 3 * (1000 + s * 200 + e)
+
+
+def _tcfg(**kw):
+    base = dict(batch=2, seq_len=100, num_kv_heads=2, group_size=4, head_dim=128, window=16,
+                softmax_scale=0.0)
+    base.update(kw)
+    return dms.make_train_config(**base)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(batch=0), dms.DMS_ERR_INVALID),
+    (dict(seq_len=0), dms.DMS_ERR_INVALID),
+    (dict(num_kv_heads=0), dms.DMS_ERR_INVALID),
+    (dict(group_size=0), dms.DMS_ERR_INVALID),
+    (dict(group_size=17), dms.DMS_ERR_UNSUPPORTED),
+    (dict(head_dim=64), dms.DMS_ERR_UNSUPPORTED),
+    (dict(window=0), dms.DMS_ERR_INVALID),
+    (dict(softmax_scale=float("nan")), dms.DMS_ERR_INVALID),
+    (dict(softmax_scale=float("inf")), dms.DMS_ERR_INVALID),
+    (dict(batch=1 << 20, seq_len=1 << 20), dms.DMS_ERR_INVALID),
+    (dict(batch=40000, num_kv_heads=2, seq_len=1), dms.DMS_ERR_INVALID),
+])
+def test_bad_train_configuration(kw, code):
+    rc = dms.lib().dms_train_workspace(ctypes.byref(_tcfg(**kw)), None)
+    assert rc == code
+
+
+def test_train_workspace_and_host_side_errors():
+    n = dms.dms_train_workspace(_tcfg())
+    # at least the K and V tiles of every head, padded to 32 tokens
+    assert n >= 2 * 2 * 2 * 4 * 128 * 128
+    assert dms.dms_train_workspace(_tcfg(seq_len=200)) > n
+    assert dms.dms_train_workspace(_tcfg(softmax_scale=-1.0)) == n
+    L = dms.lib()
+    assert L.dms_train_attention_fwd(None, *([None] * 8)) == dms.DMS_ERR_INVALID
+    assert L.dms_train_attention_fwd(ctypes.byref(_tcfg()), *([None] * 8)) == dms.DMS_ERR_INVALID
+    assert L.dms_train_attention_bwd(ctypes.byref(_tcfg()), *([None] * 13)) == dms.DMS_ERR_INVALID
+    for fn in (L.dms_gumbel_sigmoid_fwd, L.dms_gumbel_sigmoid_bwd):
+        assert fn(-1, None, None, ctypes.c_float(1.0), None, None) == dms.DMS_ERR_INVALID
+        assert fn(4, None, None, ctypes.c_float(0.0), None, None) == dms.DMS_ERR_INVALID
+        assert fn(4, None, None, ctypes.c_float(float("nan")), None, None) == dms.DMS_ERR_INVALID
+        assert fn(4, None, None, ctypes.c_float(1.0), None, None) == dms.DMS_ERR_INVALID
+        assert fn(0, None, None, ctypes.c_float(1.0), None, None) == dms.DMS_OK
