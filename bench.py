@@ -422,6 +422,113 @@ def run_stress(args):
     print(json.dumps(res), flush=True)
 
 
+TRAIN = dict(batch=2, seq_len=8192, kv_heads=8, group=5, head_dim=128, window=256, tau=0.1,
+             seed=21)
+
+
+def run_train(args):
+    """Training-time DMS attention of one Qwen-R1-32B-shaped layer (8 KV heads,
+    group 5, d = 128) on a micro-batch of 2 sequences x 8192 tokens (the
+    retrofitting context of the R1-distilled models), window 256: Gumbel-
+    sigmoid decisions from synthetic logits, masked attention forward, its
+    backward (dq, dk, dv, dalpha) and the Gumbel-sigmoid backward.  FLOPs are
+    algorithmic over the causal (query, key) pairs: 2 products of 2 d per pair
+    and query head forward, 5 backward; the mask evicts nothing during
+    training, so every causal pair is computed."""
+    import torch
+    from paper_2506_05345_amd import dms
+
+    c = TRAIN
+    B, T, H, g, D, w = c["batch"], c["seq_len"], c["kv_heads"], c["group"], c["head_dim"], c["window"]
+    Hq = H * g
+    dev = "cuda:0"
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(c["seed"])
+    q = torch.randn((B, T, Hq, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    k = torch.randn((B, T, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    v = torch.randn((B, T, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    dout = torch.randn((B, T, Hq, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    logits = torch.randn((B, T, H), generator=gen, device=dev) * 2.0
+    u = torch.rand((B, T, H), generator=gen, device=dev).clamp_(1e-6, 1 - 1e-6)
+    dal_in = torch.randn((B, T, H), generator=gen, device=dev)
+    cfg = dms.make_train_config(B, T, H, g, D, w)
+    ws = torch.empty(dms.dms_train_workspace(cfg), dtype=torch.uint8, device=dev)
+    alpha = torch.empty((B, T, H), device=dev)
+    out = torch.empty((B, T, Hq, D), device=dev)
+    lse = torch.empty((B, Hq, T), device=dev)
+    dq = torch.empty((B, T, Hq, D), device=dev)
+    dk = torch.empty((B, T, H, D), device=dev)
+    dv = torch.empty((B, T, H, D), device=dev)
+    dal = torch.empty((B, T, H), device=dev)
+    dlog = torch.empty((B, T, H), device=dev)
+    n = B * T * H
+    tau = c["tau"]
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+
+    def step(timed=None):
+        if timed is not None:
+            timed[0].record()
+        dms.dms_gumbel_sigmoid_fwd(n, logits, u, tau, alpha)
+        if timed is not None:
+            timed[1].record()
+        dms.dms_train_attention_fwd(cfg, q, k, v, alpha, out, lse, ws)
+        if timed is not None:
+            timed[2].record()
+        dms.dms_train_attention_bwd(cfg, q, k, v, alpha, out, lse, dout, dq, dk, dv, dal, ws)
+        if timed is not None:
+            timed[3].record()
+        # the decision gradient of the step plus an independent upstream term
+        dms.dms_gumbel_sigmoid_bwd(n, alpha, dal, tau, dlog)
+        if timed is not None:
+            timed[4].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    tot = [0.0] * 4
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        step(ev)
+        torch.cuda.synchronize()
+        for i in range(4):
+            tot[i] += ev[i].elapsed_time(ev[i + 1])
+    e1.record()
+    torch.cuda.synchronize()
+    if not (torch.isfinite(dq).all() and torch.isfinite(dal).all() and torch.isfinite(dlog).all()):
+        raise RuntimeError("non-finite training gradients")
+    step_ms = sum(tot) / args.steps
+    pairs = B * Hq * T * (T + 1) / 2
+    f_fwd, f_bwd = 4 * D * pairs, 10 * D * pairs
+    fwd_ms, bwd_ms = tot[1] / args.steps, tot[2] / args.steps
+    peak = MFMA_PEAK_FLOPS / 1e12
+    res = {
+        "metric": "DMS training attention (continuous decisions): fwd+bwd TFLOP/s",
+        "value": round((f_fwd + f_bwd) / (step_ms * 1e-3) / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "Qwen-R1-32B-shaped layer, 2 sequences x 8192 tokens, 8 KV heads "
+                               "x group 5, d=128, w=256, Gumbel-sigmoid tau=0.1 over N(0, 2) logits",
+                   "batch": B, "seq_len": T, "kv_heads": H, "query_heads": Hq, "window": w},
+        "forward": {"ms": round(fwd_ms, 3), "algorithmic_tflop": round(f_fwd / 1e12, 4),
+                    "achieved_tflops": round(f_fwd / (fwd_ms * 1e-3) / 1e12, 2),
+                    "frac": round(f_fwd / (fwd_ms * 1e-3) / 1e12 / peak, 4)},
+        "backward": {"ms": round(bwd_ms, 3), "algorithmic_tflop": round(f_bwd / 1e12, 4),
+                     "achieved_tflops": round(f_bwd / (bwd_ms * 1e-3) / 1e12, 2),
+                     "frac": round(f_bwd / (bwd_ms * 1e-3) / 1e12 / peak, 4)},
+        "gumbel_us": {"fwd": round(1e3 * tot[0] / args.steps, 1),
+                      "bwd": round(1e3 * tot[3] / args.steps, 1)},
+        "roofline": {"bound": "mfma", "peak": peak, "unit": "TFLOP/s",
+                     "achieved": round((f_fwd + f_bwd) / (step_ms * 1e-3) / 1e12, 2),
+                     "frac": round((f_fwd + f_bwd) / (step_ms * 1e-3) / 1e12 / peak, 4),
+                     "traffic": None,
+                     "kernel_timing": "HIP events on the launch stream around each entry point"},
+    }
+    print(json.dumps(res), flush=True)
+
+
 # Attention shapes of the paper's models (layers, KV heads, group, head dim)
 # and the dense-model sizes (public model configurations) that the App. I
 # latency estimate needs: hidden size d, MLP width d_ff, vocabulary V.
@@ -553,7 +660,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="qwen-r1-32b-8x",
-                    choices=sorted(WORKLOADS) + ["qwen-r1-32b-stress"])
+                    choices=sorted(WORKLOADS) + ["qwen-r1-32b-stress", "qwen-r1-32b-train"])
     ap.add_argument("--window", type=int, default=256, choices=[64, 256],
                     help="window of the heterogeneous stress workload")
     ap.add_argument("--chunk", type=int, default=4096)
@@ -587,6 +694,9 @@ def main():
         del src, dst
     if args.workload == "qwen-r1-32b-stress":
         run_stress(args)
+        return
+    if args.workload == "qwen-r1-32b-train":
+        run_train(args)
         return
     wl = WORKLOADS[args.workload]
     S = args.warmup + 2 * args.steps
