@@ -69,6 +69,21 @@ __device__ inline float col_sum(float x) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// The dispatcher deals workgroups to the 8 XCDs round-robin by linear id, and
+// each XCD has its own L2.  Map the linear id so that the workgroups one XCD
+// receives, in dispatch order, are a contiguous range of logical ids
+// (x fastest): the blocks of one (sequence, head) then share an L2 and start
+// together.
+constexpr int kXcds = 8;
+__device__ inline int2 xcd_order() {
+  const int nx = gridDim.x;
+  const int N = nx * gridDim.y;
+  const int id = blockIdx.x + nx * blockIdx.y;
+  const int x = id % kXcds, k = id / kXcds;
+  const int L = x * (N / kXcds) + min(x, N % kXcds) + k;
+  return int2{L % nx, L / nx};
+}
+
 // 8 fp32 values -> 4 packed bf16 pairs (round to nearest even)
 __device__ inline u32x4 pack_bf16(const float* e) {
   u32x4 u;
@@ -181,9 +196,10 @@ template <int D, int NQ>
 __global__ __launch_bounds__(kThreads, 2) void train_fwd_kernel(TrainArgs a) {
   __shared__ __attribute__((aligned(16))) char tile_lds[2][D * 128];
   __shared__ float bias_lds[2][32];
-  const int bh = blockIdx.y;
+  const int2 wg = xcd_order();               // latest (longest) query blocks first
+  const int bh = wg.y;
   const int b = bh / a.H, h = bh % a.H;
-  const int t0 = blockIdx.x * a.PB;
+  const int t0 = (gridDim.x - 1 - wg.x) * a.PB;
   if (t0 >= a.T) return;
   const int t1 = min(a.T, t0 + a.PB);
   const int ntiles = (t1 + 31) >> 5;
@@ -377,9 +393,10 @@ template <int D, int NQ>
 __global__ __launch_bounds__(kThreads, 1) void train_dq_kernel(TrainArgs a) {
   __shared__ __attribute__((aligned(16))) char tile_lds[2][D * 192];
   __shared__ float bias_lds[2][32];
-  const int bh = blockIdx.y;
+  const int2 wg = xcd_order();
+  const int bh = wg.y;
   const int b = bh / a.H, h = bh % a.H;
-  const int t0 = blockIdx.x * a.PB;
+  const int t0 = (gridDim.x - 1 - wg.x) * a.PB;
   if (t0 >= a.T) return;
   const int t1 = min(a.T, t0 + a.PB);
   const int ntiles = (t1 + 31) >> 5;
@@ -524,16 +541,18 @@ __global__ __launch_bounds__(kThreads, 1) void train_dq_kernel(TrainArgs a) {
 // dK / dV / dalpha pass.  Workgroup = (b, KV head h, 64 keys); wave w owns
 // keys j0 + 16 w .. + 15 as the 16 columns of its MFMAs, with those keys' K
 // and V (B operands) in registers.  It walks every query head of the group
-// and every 32-position query tile from the block's first key on; per tile
-// the Q and dO tiles (row and transposed parts), lse and D are staged.
+// and every 32-position query tile from the block's first key on (the last
+// tile first); per tile the Q and dO tiles (row and transposed parts), lse and
+// D are staged.
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void train_dkv_kernel(TrainArgs a) {
   __shared__ __attribute__((aligned(16))) char tile_lds[2][D * 256];
   __shared__ float row_lds[2][2][32];   // lse (log2 units), D of the tile's rows
-  const int bh = blockIdx.y;
+  const int2 wg = xcd_order();               // earliest (longest) key blocks first
+  const int bh = wg.y;
   const int b = bh / a.H, h = bh % a.H;
-  const int j0 = blockIdx.x * 64;
+  const int j0 = wg.x * 64;
   if (j0 >= a.T) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -567,8 +586,11 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_kernel(TrainArgs a) {
   constexpr int KP = D * 4 / kThreads;
   u32x4 sq[KP], sqt[KP], sd[KP], sdt[KP];
   float srow = 0.f;
+  // steps walk the query tiles from the last one down, every query head of
+  // the group per tile: the blocks of one (sequence, head) that run together
+  // read the same tile at about the same time
   auto stage_load = [&](int step) {
-    const int qh = step / nqt, pt = pt0 + step % nqt;
+    const int qh = step % a.g, pt = a.nt - 1 - step / a.g;
     const size_t tix = (static_cast<size_t>(b) * Hq + h * a.g + qh) * a.nt + pt;
     const char* qt = a.qtiles + tix * (D * 128);
     const char* dt = a.dotiles + tix * (D * 128);
@@ -605,7 +627,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_kernel(TrainArgs a) {
     const int buf = step & 1;
     if (step + 1 < nsteps) stage_load(step + 1);
     const char* tl = tile_lds[buf];
-    const int tq = 32 * (pt0 + step % nqt);  // first query position of the tile
+    const int tq = 32 * (a.nt - 1 - step / a.g);  // first query position of the tile
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0, p0 = s0, p1 = s0;
 #pragma unroll
     for (int s2 = 0; s2 < D / 32; ++s2) {
