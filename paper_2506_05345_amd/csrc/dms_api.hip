@@ -7,6 +7,7 @@
 #include <vector>
 
 #include "dms_common.h"
+#include "dms_train.h"
 
 namespace dms {
 

@@ -13,7 +13,6 @@ namespace dms {
 constexpr int kTile = 32;            // tokens per decode tile (k of one PV MFMA)
 constexpr int kMaxWaves = 8192;      // upper bound on decode waves (workspace sizing)
 constexpr int kMaxGroup = 16;        // query heads per KV head (MFMA column count)
-constexpr int kTrainHeadDim = 128;   // head dimension of the training kernels
 constexpr int kMaxSeqs = 65536;      // sequence-id bitmap of the planning kernel
 constexpr uint32_t kFlagBit = 0x80000000u;
 constexpr int kAlign = 256;
@@ -196,18 +195,6 @@ hipError_t launch_chunk_commit(const dms_config& c, const Layout& lo, void* meta
                                void* pool, int layer, int n, const int32_t* seq_ids,
                                const int32_t* cu, int total_tokens, int max_len, const void* k,
                                const void* v, const uint8_t* flags, hipStream_t st);
-// training-time attention (continuous decisions)
-size_t train_workspace_bytes(const dms_train_config& c);
-hipError_t launch_train_fwd(const dms_train_config& c, const void* q, const void* k, const void* v,
-                            const float* alpha, float* out, float* lse, void* ws, hipStream_t st);
-hipError_t launch_train_bwd(const dms_train_config& c, const void* q, const void* k, const void* v,
-                            const float* alpha, const float* out, const float* lse,
-                            const void* dout, float* dq, float* dk, float* dv, float* dalpha,
-                            void* ws, hipStream_t st);
-hipError_t launch_gumbel_fwd(int n, const float* x, const float* u, float tau, float* alpha,
-                             hipStream_t st);
-hipError_t launch_gumbel_bwd(int n, const float* alpha, const float* da, float tau, float* dx,
-                             hipStream_t st);
 hipError_t launch_prefill_decide(const dms_config& c, const void* q, int total_tokens,
                                  uint8_t* flags, hipStream_t st);
 hipError_t launch_prefill_attention(const dms_config& c, const Layout& lo, void* meta, void* ws,

@@ -26,6 +26,7 @@
 #include <cmath>
 
 #include "dms_common.h"
+#include "dms_train.h"
 
 namespace dms {
 namespace {
