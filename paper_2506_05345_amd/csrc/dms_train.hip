@@ -549,7 +549,7 @@ __global__ __launch_bounds__(kThreads, 1) void train_dq_kernel(TrainArgs a) {
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void train_dkv_kernel(TrainArgs a) {
   __shared__ __attribute__((aligned(16))) char tile_lds[2][D * 256];
-  __shared__ float row_lds[2][2][32];   // lse (log2 units), D of the tile's rows
+  __shared__ __attribute__((aligned(16))) float row_lds[2][2][32];   // lse (log2 units), D per row
   const int2 wg = xcd_order();               // earliest (longest) key blocks first
   const int bh = wg.y;
   const int b = bh / a.H, h = bh % a.H;
@@ -582,53 +582,51 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_kernel(TrainArgs a) {
   float dal = 0.f;
 
   const int pt0 = j0 >> 5;
-  const int nqt = a.nt - pt0;                // query tiles per query head
-  const int nsteps = a.g * nqt;
+  const int nsteps = a.g * (a.nt - pt0);     // (query tile, query head) pairs
   constexpr int KP = D * 4 / kThreads;
-  u32x4 sq[KP], sqt[KP], sd[KP], sdt[KP];
-  float srow = 0.f;
+  // Two register sets: the tiles of step s + 2 are loaded while step s is
+  // computed, and step s + 1's are written to LDS at its end.
+  u32x4 ra[4][KP], rb[4][KP];
+  float rowa = 0.f, rowb = 0.f;
   // steps walk the query tiles from the last one down, every query head of
   // the group per tile: the blocks of one (sequence, head) that run together
   // read the same tile at about the same time
-  auto stage_load = [&](int step) {
-    const int qh = step % a.g, pt = a.nt - 1 - step / a.g;
-    const size_t tix = (static_cast<size_t>(b) * Hq + h * a.g + qh) * a.nt + pt;
+  int ld_qh = 0, ld_pt = a.nt - 1;           // next step to load
+  auto stage_load = [&](u32x4 (&rg)[4][KP], float& row) {
+    const size_t tix = (static_cast<size_t>(b) * Hq + h * a.g + ld_qh) * a.nt + ld_pt;
     const char* qt = a.qtiles + tix * (D * 128);
     const char* dt = a.dotiles + tix * (D * 128);
 #pragma unroll
     for (int m = 0; m < KP; ++m) {
       const int P = tid + m * kThreads;
-      sq[m] = ld16(qt + P * 16);
-      sqt[m] = ld16(qt + D * 64 + P * 16);
-      sd[m] = ld16(dt + P * 16);
-      sdt[m] = ld16(dt + D * 64 + P * 16);
+      rg[0][m] = ld16(qt + P * 16);
+      rg[1][m] = ld16(qt + D * 64 + P * 16);
+      rg[2][m] = ld16(dt + P * 16);
+      rg[3][m] = ld16(dt + D * 64 + P * 16);
     }
     if (tid < 64) {
-      const int t = 32 * pt + (tid & 31);
-      const size_t li = (static_cast<size_t>(b) * Hq + h * a.g + qh) * a.T + t;
-      srow = t < a.T ? (tid < 32 ? a.lse[li] * kLog2e : a.dsum[li]) : 0.f;
+      const int t = 32 * ld_pt + (tid & 31);
+      const size_t li = (static_cast<size_t>(b) * Hq + h * a.g + ld_qh) * a.T + t;
+      row = t < a.T ? (tid < 32 ? a.lse[li] * kLog2e : a.dsum[li]) : 0.f;
+    }
+    if (++ld_qh == a.g) {
+      ld_qh = 0;
+      --ld_pt;
     }
   };
-  auto stage_store = [&](int buf) {
+  auto stage_store = [&](int buf, const u32x4 (&rg)[4][KP], float row) {
 #pragma unroll
     for (int m = 0; m < KP; ++m) {
       const int P = tid + m * kThreads;
-      st16(tile_lds[buf] + P * 16, sq[m]);
-      st16(tile_lds[buf] + D * 64 + P * 16, sqt[m]);
-      st16(tile_lds[buf] + D * 128 + P * 16, sd[m]);
-      st16(tile_lds[buf] + D * 192 + P * 16, sdt[m]);
+#pragma unroll
+      for (int part = 0; part < 4; ++part) st16(tile_lds[buf] + part * (D * 64) + P * 16, rg[part][m]);
     }
-    if (tid < 64) row_lds[buf][tid >> 5][tid & 31] = srow;
+    if (tid < 64) row_lds[buf][tid >> 5][tid & 31] = row;
   };
 
-  stage_load(0);
-  stage_store(0);
-  __syncthreads();
-  for (int step = 0; step < nsteps; ++step) {
-    const int buf = step & 1;
-    if (step + 1 < nsteps) stage_load(step + 1);
+  int step_qh = 0, tq = 32 * (a.nt - 1);     // step being computed
+  auto compute = [&](int buf) {
     const char* tl = tile_lds[buf];
-    const int tq = 32 * (a.nt - 1 - step / a.g);  // first query position of the tile
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0, p0 = s0, p1 = s0;
 #pragma unroll
     for (int s2 = 0; s2 < D / 32; ++s2) {
@@ -642,16 +640,18 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_kernel(TrainArgs a) {
       p1 = mfma_bf16(db, vf[s2], p1);
     }
     // lane (key r, G) now holds rows (queries) tq + 8 G + i, i = 0..7
+    const f32x4 l2a = *reinterpret_cast<const f32x4*>(&row_lds[buf][0][8 * G]);
+    const f32x4 l2b = *reinterpret_cast<const f32x4*>(&row_lds[buf][0][8 * G + 4]);
+    const f32x4 dda = *reinterpret_cast<const f32x4*>(&row_lds[buf][1][8 * G]);
+    const f32x4 ddb = *reinterpret_cast<const f32x4*>(&row_lds[buf][1][8 * G + 4]);
     const int cls = mask_class(j0, j0 + 64, tq, tq + 32, a.w, a.T);
     float pr[8], ds[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const float raw = i < 4 ? s0[i] : s1[i - 4];
-      const float dp = i < 4 ? p0[i] : p1[i - 4];
-      const float l2 = row_lds[buf][0][8 * G + i];
-      const float dd = row_lds[buf][1][8 * G + i];
+      const float dpd = (i < 4 ? p0[i] : p1[i - 4]) - (i < 4 ? dda[i] : ddb[i - 4]);
+      const float l2 = i < 4 ? l2a[i] : l2b[i - 4];
       const float pu = __builtin_amdgcn_exp2f(fmaf(raw, a.scale_log2, -l2));   // exp(s - lse) w/o bias
-      const int t = tq + 8 * G + i;
       float p;
       bool old;
       if (cls == 0) {
@@ -661,13 +661,14 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_kernel(TrainArgs a) {
         p = pu;
         old = false;
       } else {
+        const int t = tq + 8 * G + i;
         const bool vis = j <= t && t < a.T && jok;
         old = vis && j <= t - a.w;
         p = vis ? (old ? pu * keep : pu) : 0.f;
       }
       pr[i] = p;
-      ds[i] = p * (dp - dd);
-      if (old) dal += pu * (dp - dd);
+      ds[i] = p * dpd;
+      if (old) dal = fmaf(pu, dpd, dal);
     }
     const u32x4 pu8 = pack_bf16(pr);
     const u32x4 du8 = pack_bf16(ds);
@@ -676,7 +677,25 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_kernel(TrainArgs a) {
       dva[bb] = mfma_bf16(ld16(tl + D * 192 + bb * 1024 + lane * 16), pu8, dva[bb]);
       dka[bb] = mfma_bf16(ld16(tl + D * 64 + bb * 1024 + lane * 16), du8, dka[bb]);
     }
-    if (step + 1 < nsteps) stage_store(buf ^ 1);
+    if (++step_qh == a.g) {
+      step_qh = 0;
+      tq -= 32;
+    }
+  };
+
+  stage_load(ra, rowa);
+  if (nsteps > 1) stage_load(rb, rowb);
+  stage_store(0, ra, rowa);
+  __syncthreads();
+  for (int step = 0; step < nsteps; step += 2) {
+    if (step + 2 < nsteps) stage_load(ra, rowa);
+    compute(0);
+    if (step + 1 < nsteps) stage_store(1, rb, rowb);
+    __syncthreads();
+    if (step + 1 >= nsteps) break;
+    if (step + 3 < nsteps) stage_load(rb, rowb);
+    compute(1);
+    if (step + 2 < nsteps) stage_store(0, ra, rowa);
     __syncthreads();
   }
 
