@@ -7,3 +7,4 @@ calls it and shares no code with it.
 from .dms_oracle import *  # noqa: F401,F403
 from .latency_model import *  # noqa: F401,F403
 from .train_oracle import *  # noqa: F401,F403
+from .kv_fp8 import *  # noqa: F401,F403

@@ -61,6 +61,8 @@ from dataclasses import dataclass
 
 import numpy as np
 
+from .kv_fp8 import dequantize_rows_fp8, quantize_rows_fp8
+
 __all__ = [
     "visible", "visible_immediate", "visibility_mask", "additive_mask", "retained_count",
     "alpha_bin", "query_decisions", "zero_borrowed_neuron",
@@ -259,15 +261,23 @@ class PagedKVOracle:
     With ``store_values`` the K / V rows of every live slot are kept too.
     mode "delayed": token t reuses token t - w's slot iff that token's own
     decision was 1; mode "immediate": iff token t's decision is 1.
+    kv_format "fp8": every stored row is quantized on append (E4M3 codes and
+    a power-of-two row exponent, see ``kv_fp8``); k_codes / k_exp and
+    v_codes / v_exp hold them and k_store / v_store the dequantized rows that
+    attention reads.
     """
 
     def __init__(self, max_seqs, num_kv_heads, window, page_size, num_pages,
-                 max_pages_per_head, head_dim, store_values=True, mode="delayed"):
+                 max_pages_per_head, head_dim, store_values=True, mode="delayed",
+                 kv_format="bf16"):
         if window < 1:
             raise ValueError("window must be >= 1")
         if mode not in ("delayed", "immediate"):
             raise ValueError("mode must be 'delayed' or 'immediate'")
+        if kv_format not in ("bf16", "fp8"):
+            raise ValueError("kv_format must be 'bf16' or 'fp8'")
         self.mode = mode
+        self.kv_format = kv_format
         self.dims = _Dims(max_seqs, num_kv_heads, window, page_size, num_pages,
                           max_pages_per_head, head_dim)
         S, H, w = max_seqs, num_kv_heads, window
@@ -285,6 +295,11 @@ class PagedKVOracle:
         if store_values:
             self.k_store = np.zeros((S, H, max_slots, head_dim), np.float64)
             self.v_store = np.zeros((S, H, max_slots, head_dim), np.float64)
+            if kv_format == "fp8":
+                self.k_codes = np.zeros((S, H, max_slots, head_dim), np.uint8)
+                self.v_codes = np.zeros((S, H, max_slots, head_dim), np.uint8)
+                self.k_exp = np.zeros((S, H, max_slots), np.int64)
+                self.v_exp = np.zeros((S, H, max_slots), np.int64)
 
     # -- the append rule ------------------------------------------------------
     def append_chunk(self, seq_ids, flags_list, k_list=None, v_list=None):
@@ -355,8 +370,19 @@ class PagedKVOracle:
         self.page_table, self.top = page_table, top
         for (s, slot, act, c) in writes:
             for r, i in enumerate(act):
-                self.k_store[s[r], hs, slot[r]] = np.asarray(k_list[i], np.float64).reshape(-1, H, D.head_dim)[c]
-                self.v_store[s[r], hs, slot[r]] = np.asarray(v_list[i], np.float64).reshape(-1, H, D.head_dim)[c]
+                kr = np.asarray(k_list[i], np.float64).reshape(-1, H, D.head_dim)[c]
+                vr = np.asarray(v_list[i], np.float64).reshape(-1, H, D.head_dim)[c]
+                if self.kv_format == "fp8":
+                    kc, ke = quantize_rows_fp8(kr)
+                    vc, ve = quantize_rows_fp8(vr)
+                    self.k_codes[s[r], hs, slot[r]] = kc
+                    self.v_codes[s[r], hs, slot[r]] = vc
+                    self.k_exp[s[r], hs, slot[r]] = ke
+                    self.v_exp[s[r], hs, slot[r]] = ve
+                    kr = dequantize_rows_fp8(kc, ke)
+                    vr = dequantize_rows_fp8(vc, ve)
+                self.k_store[s[r], hs, slot[r]] = kr
+                self.v_store[s[r], hs, slot[r]] = vr
 
     def append(self, seq_ids, flags, k=None, v=None):
         """One token per listed sequence: flags [n, H], k / v [n, H, d]."""
