@@ -94,6 +94,8 @@ typedef struct dms_config {
   int32_t decision_source;    /* DMS_DECIDE_CALLER (0) or DMS_DECIDE_QUERY (1) */
   float decision_bias;        /* b added to the borrowed neuron (DMS_DECIDE_QUERY);
                                  -5 is the paper's training offset */
+  int32_t kv_format;          /* DMS_KV_BF16 (0) or DMS_KV_FP8 (1): how retained
+                                 K / V rows are stored in the page pools */
 } dms_config;
 
 /*
@@ -119,6 +121,24 @@ typedef struct dms_config {
  *     without a query (dms_append, dms_append_chunk) still take flags.
  */
 enum { DMS_EVICT_DELAYED = 0, DMS_EVICT_IMMEDIATE = 1 };
+
+/*
+ * KV storage (dms_config.kv_format).  KV quantization is one of the methods
+ * the paper names as orthogonal to DMS (App. B); this combines the two.
+ *   DMS_KV_BF16: rows are stored as given (bf16), 16 KB per 32-slot tile at
+ *     d = 128.
+ *   DMS_KV_FP8: each retained K row and V row of a (token, KV head) is
+ *     stored as OCP FP8 E4M3 codes with one power-of-two scale 2^e per row,
+ *     e the smallest integer with max|x| * 2^-e <= 448; codes are the
+ *     round-to-nearest-even E4M3 values of x * 2^-e and the stored value is
+ *     code * 2^e.  A 32-slot tile takes 64 d + 256 bytes (8.25 KB at
+ *     d = 128), roughly halving the bytes decode reads.  Every key and value
+ *     is attended in its stored form, including the token a decode step
+ *     appends.  dms_prefill_chunk / dms_prefill_chunk_q return
+ *     DMS_ERR_UNSUPPORTED on an FP8 context; appends, chunk appends and
+ *     decode support it.
+ */
+enum { DMS_KV_BF16 = 0, DMS_KV_FP8 = 1 };
 enum { DMS_DECIDE_CALLER = 0, DMS_DECIDE_QUERY = 1 };
 
 typedef struct dms_ctx dms_ctx;
@@ -148,13 +168,21 @@ typedef struct dms_state_offsets {
 } dms_state_offsets;
 
 /*
- * Page layout in a layer's pool (`page_bytes` = 4 * P * d bytes, page i at
- * i * page_bytes).  A slot s of a head lives in page page_table[s / P], tile
- * (s % P) / 32, row j = s % 32.  A page is P/32 tiles of 128 * d bytes each:
+ * Page layout in a layer's pool (page i at i * page_bytes).  A slot s of a
+ * head lives in page page_table[s / P], tile (s % P) / 32, row j = s % 32.
+ * DMS_KV_BF16: page_bytes = 4 * P * d; a page is P/32 tiles of 128 * d bytes:
  *   keys   bf16 [d/32][32 rows][32 dims]: element (j, e) at byte
  *          (e / 32) * 2048 + j * 64 + (e % 32) * 2 of the tile
  *   values bf16 [d][32 rows] (transposed): element (j, e) at byte
  *          64 * d + e * 64 + j * 2 of the tile
+ * DMS_KV_FP8: page_bytes = P/32 * (64 * d + 256); with
+ *   h = (j / 4) % 2, r = 4 * (j / 8) + j % 4 (row j's place among 16 rows):
+ *   key code (j, e)   at (e / 64) * 2048 + h * 1024 + (16 * ((e / 8) % 4) + r) * 16
+ *                        + 8 * ((e / 32) % 2) + e % 8
+ *   value code (j, e) at 32 * d + (e / 32) * 1024 + (16 * (j / 8) + e % 16) * 16
+ *                        + 8 * ((e / 16) % 2) + j % 8
+ *   key scale of row j (float32)   at 64 * d + (j / 8) * 64 + (j % 8) * 4
+ *   value scale of row j (float32) at 64 * d + (j / 8) * 64 + 32 + (j % 8) * 4
  */
 
 /* Sizes of the caller-owned buffers for `cfg`.  Host only; validates cfg.

@@ -7,6 +7,7 @@
 #include <vector>
 
 #include "dms_common.h"
+#include "dms_fp8.h"
 #include "dms_train.h"
 
 namespace dms {
@@ -26,6 +27,7 @@ int validate_config(const dms_config& c) {
   if (c.decision_source != DMS_DECIDE_CALLER && c.decision_source != DMS_DECIDE_QUERY)
     return DMS_ERR_INVALID;
   if (c.decision_source == DMS_DECIDE_QUERY && !isfinite(c.decision_bias)) return DMS_ERR_INVALID;
+  if (c.kv_format != DMS_KV_BF16 && c.kv_format != DMS_KV_FP8) return DMS_ERR_INVALID;
   // slot and page indices are int32 on the device
   if (static_cast<int64_t>(c.max_pages_per_head) * c.page_size >= (int64_t(1) << 31)) return DMS_ERR_INVALID;
   if (static_cast<int64_t>(c.max_seqs) * c.num_kv_heads > (int64_t(1) << 22)) return DMS_ERR_INVALID;
@@ -55,7 +57,8 @@ Layout make_layout(const dms_config& c) {
   lo.layer_stride = off;
   lo.meta_bytes = lo.layer0 + lo.layer_stride * c.num_layers;
   // pool
-  lo.page_bytes = 2 * P * D * 2;
+  lo.page_bytes = c.kv_format == DMS_KV_FP8 ? P / 32 * fp8_tile_bytes(static_cast<int>(D))
+                                             : 2 * P * D * 2;
   lo.pool_bytes = lo.page_bytes * static_cast<size_t>(c.num_pages);
   // workspace
   off = 0;
@@ -358,6 +361,7 @@ int dms_prefill_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev
   int rc = check_call(ctx, layer, n, seq_ids_dev);
   if (rc) return rc;
   if (ctx->c.cfg.decision_source != DMS_DECIDE_CALLER) return DMS_ERR_INVALID;
+  if (ctx->c.cfg.kv_format != DMS_KV_BF16) return DMS_ERR_UNSUPPORTED;
   if ((rc = check_chunk(ctx, cu_seqlens_dev, total_tokens, max_seqlen))) return rc;
   if (total_tokens == 0) return DMS_OK;
   if (!q_dev || !k_dev || !v_dev || !flags_dev || !out_dev) return DMS_ERR_INVALID;
@@ -372,6 +376,7 @@ int dms_prefill_chunk_q(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_d
   int rc = check_call(ctx, layer, n, seq_ids_dev);
   if (rc) return rc;
   if (ctx->c.cfg.decision_source != DMS_DECIDE_QUERY) return DMS_ERR_INVALID;
+  if (ctx->c.cfg.kv_format != DMS_KV_BF16) return DMS_ERR_UNSUPPORTED;
   if ((rc = check_chunk(ctx, cu_seqlens_dev, total_tokens, max_seqlen))) return rc;
   if (total_tokens == 0) return DMS_OK;
   if (!q_dev || !k_dev || !v_dev || !out_dev) return DMS_ERR_INVALID;

@@ -6,6 +6,7 @@
 // that would exhaust the page pool (or overflow a head's page table) changes
 // nothing and only records the error in the sticky status word.
 #include "dms_common.h"
+#include "dms_fp8.h"
 
 namespace dms {
 namespace {
@@ -461,6 +462,7 @@ struct ScatterArgs {
   const uint16_t* v;
   size_t page_bytes;
   int D, P, maxp;
+  int fp8;   // FP8 pages: rows are quantized on the way in
 };
 
 __global__ __launch_bounds__(64) void scatter_kernel(ScatterArgs a) {
@@ -470,9 +472,16 @@ __global__ __launch_bounds__(64) void scatter_kernel(ScatterArgs a) {
   const int slot = d.z;
   const int page = a.page_table[static_cast<size_t>(d.y) * a.maxp + slot / a.P];
   const int row = slot % a.P;
-  char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * tile_bytes(a.D);
   const int j = row & 31;
   const int lane = threadIdx.x;
+  if (a.fp8) {
+    char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * fp8_tile_bytes(a.D);
+    if (lane < a.D / 8)
+      fp8_store_token(tile, j, a.D, lane, reinterpret_cast<const uint4*>(a.k + static_cast<size_t>(hh) * a.D)[lane],
+                      reinterpret_cast<const uint4*>(a.v + static_cast<size_t>(hh) * a.D)[lane]);
+    return;
+  }
+  char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * tile_bytes(a.D);
   if (lane < a.D / 8)
     *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * lane)) =
         reinterpret_cast<const uint4*>(a.k + static_cast<size_t>(hh) * a.D)[lane];
@@ -521,6 +530,7 @@ struct ChunkArgs {
   int32_t* slots;         // [T, H] slot of every chunk token
   int n, H, w, P, D, maxp, max_slots, max_seqs, total, max_len;
   int immediate;          // eviction timing (see chunk_reuse)
+  int fp8;                // FP8 pages: rows are quantized on the way in
 };
 
 __device__ inline int chunk_flag(const ChunkArgs& a, int tok0, int c, int h) {
@@ -676,7 +686,8 @@ __global__ __launch_bounds__(256) void chunk_commit_kernel(ChunkArgs a) {
   }
   if (threadIdx.x == 0) a.st.len[sh] = L0 + a.fresh[hh];
   __syncthreads();  // page-table entries written above are visible to the copies below
-  // K rows and V columns of surviving tokens: D/8 lanes per token for K
+  // K rows and V columns of surviving tokens: D/8 consecutive lanes per token
+  // (an aligned lane group: blockDim and the loop stride are multiples of it)
   const int kq = a.D / 8;
   for (int idx = threadIdx.x; idx < C * kq; idx += blockDim.x) {
     const int c = idx / kq, part = idx % kq;
@@ -684,9 +695,16 @@ __global__ __launch_bounds__(256) void chunk_commit_kernel(ChunkArgs a) {
     const int slot = a.slots[static_cast<size_t>(tok0 + c) * a.H + h];
     const int page = a.st.page_table[pt_base + slot / a.P];
     const int row = slot % a.P;
-    char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * tile_bytes(a.D);
     const int j = row & 31;
     const size_t src = (static_cast<size_t>(tok0 + c) * a.H + h) * a.D;
+    if (a.fp8) {
+      // the whole group takes this branch together (same token, same test)
+      char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * fp8_tile_bytes(a.D);
+      fp8_store_token(tile, j, a.D, part, reinterpret_cast<const uint4*>(a.k + src)[part],
+                      reinterpret_cast<const uint4*>(a.v + src)[part]);
+      continue;
+    }
+    char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * tile_bytes(a.D);
     *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * part)) =
         reinterpret_cast<const uint4*>(a.k + src)[part];
 #pragma unroll
@@ -804,6 +822,7 @@ hipError_t launch_scatter(const dms_config& c, const Layout& lo, void* meta, voi
   a.D = c.head_dim;
   a.P = c.page_size;
   a.maxp = c.max_pages_per_head;
+  a.fp8 = c.kv_format == DMS_KV_FP8;
   hipLaunchKernelGGL(scatter_kernel, dim3(n * c.num_kv_heads), dim3(64), 0, st, a);
   return hipGetLastError();
 }
@@ -853,6 +872,7 @@ hipError_t launch_chunk_commit(const dms_config& c, const Layout& lo, void* meta
   a.total = total_tokens;
   a.max_len = max_len;
   a.immediate = c.eviction == DMS_EVICT_IMMEDIATE;
+  a.fp8 = c.kv_format == DMS_KV_FP8;
   const int NH = n * c.num_kv_heads;
   hipLaunchKernelGGL(chunk_count_kernel, dim3(NH), dim3(256), 0, st, a);
   hipLaunchKernelGGL(chunk_pages_kernel, dim3(1), dim3(kPlanThreads), 0, st, a);

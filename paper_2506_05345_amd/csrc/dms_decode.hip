@@ -31,6 +31,7 @@
 //  * Online softmax in the exp2 domain: per-lane max over its 8 scores, then
 //    two cross-row shuffles; the running sum stays per lane until the end.
 #include "dms_common.h"
+#include "dms_fp8.h"
 
 namespace dms {
 namespace {
@@ -186,6 +187,135 @@ __device__ inline void compute_tile(Acc<D>& acc, const Frag<D>& f, const u32x4* 
   for (int b = 0; b < D / 16; ++b) acc.o[b] = mfma_bf16(f.vt[b], pu, acc.o[b]);
 }
 
+// ---------------------------------------------------------------------------
+// FP8 pages (layout in dms_fp8.h).  Per tile each lane loads D/64 x 2 key
+// chunks, D/32 value chunks and its 8 slots' key / value scales (16 bytes
+// each); chunks are converted to the same bf16 MFMA operands as above in
+// registers (one conversion per two codes, exact).  Keys: the fp32 scores are
+// multiplied by the key scale; values: the bf16 weights by the value scale
+// (powers of two, so both are exact and the denominator keeps the unscaled
+// weights).
+// ---------------------------------------------------------------------------
+template <int D>
+struct FragF8 {
+  u32x4 k[D / 64][2];  // key chunks of score MFMA rows blocks 0 / 1
+  u32x4 v[D / 32];     // value chunks (two V^T rows each)
+  u32x4 s[4];          // key scales (s[0], s[1]) and value scales (s[2], s[3]) of slots 8G ..
+};
+
+template <int D>
+__device__ inline void load_tile_f8(FragF8<D>& f, const char* tile, int lane, int G) {
+#pragma unroll
+  for (int p = 0; p < D / 64; ++p) {
+    f.k[p][0] = ldg16(tile + p * 2048 + lane * 16);
+    f.k[p][1] = ldg16(tile + p * 2048 + 1024 + lane * 16);
+  }
+#pragma unroll
+  for (int p = 0; p < D / 32; ++p) f.v[p] = ldg16(tile + D * 32 + p * 1024 + lane * 16);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) f.s[i] = ldg16(tile + D * 64 + G * 64 + i * 16);
+}
+
+// Last, partial tile: key rows of missing slots are not read, value codes and
+// scales of missing slots are zeroed (a freed page may hold any bytes).
+template <int D>
+__device__ inline void load_tail_f8(FragF8<D>& f, const char* tile, int lane, int valid, int r, int G) {
+  const int ta = 8 * (r >> 2) + (r & 3);
+  const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int p = 0; p < D / 64; ++p) {
+    f.k[p][0] = ta < valid ? ldg16(tile + p * 2048 + lane * 16) : z;
+    f.k[p][1] = ta + 4 < valid ? ldg16(tile + p * 2048 + 1024 + lane * 16) : z;
+  }
+  const int nv = valid - 8 * G;   // slots of this lane's 8 that exist
+  // byte i of each 8-byte half is slot 8G + i
+  const uint64_t keep8 = nv >= 8 ? ~0ull : (nv <= 0 ? 0ull : (~0ull >> (8 * (8 - nv))));
+  const uint32_t klo = static_cast<uint32_t>(keep8), khi = static_cast<uint32_t>(keep8 >> 32);
+#pragma unroll
+  for (int p = 0; p < D / 32; ++p) {
+    u32x4 x = nv > 0 ? ldg16(tile + D * 32 + p * 1024 + lane * 16) : z;
+    x[0] &= klo;
+    x[1] &= khi;
+    x[2] &= klo;
+    x[3] &= khi;
+    f.v[p] = x;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    u32x4 x = nv > 0 ? ldg16(tile + D * 64 + G * 64 + i * 16) : z;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if ((i & 1) * 4 + c >= nv) x[c] = 0u;
+    f.s[i] = x;
+  }
+}
+
+// 8 E4M3 codes (two words) -> 8 bf16 (exact)
+__device__ inline u32x4 f8_to_bf16x8(uint32_t w0, uint32_t w1) {
+  u32x4 a;
+  a[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w0, 1.0f, false));
+  a[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w0, 1.0f, true));
+  a[2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w1, 1.0f, false));
+  a[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w1, 1.0f, true));
+  return a;
+}
+
+template <int D>
+__device__ inline void compute_tile_f8(Acc<D>& acc, const FragF8<D>& f, const u32x4* qf, float scale,
+                                       int valid, int G) {
+  f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int p = 0; p < D / 64; ++p) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      s0 = mfma_bf16(f8_to_bf16x8(f.k[p][0][2 * j], f.k[p][0][2 * j + 1]), qf[2 * p + j], s0);
+      s1 = mfma_bf16(f8_to_bf16x8(f.k[p][1][2 * j], f.k[p][1][2 * j + 1]), qf[2 * p + j], s1);
+    }
+  }
+  float sc[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    sc[i] = s0[i] * (scale * __uint_as_float(f.s[0][i]));
+    sc[4 + i] = s1[i] * (scale * __uint_as_float(f.s[1][i]));
+  }
+  if (valid < kTile) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (8 * G + j >= valid) sc[j] = -INFINITY;
+  }
+  float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
+                   fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const bool raise = mx > acc.m + kRescale;
+  if (__builtin_amdgcn_ballot_w64(raise)) {
+    const float m_new = raise ? mx : acc.m;
+    const float alpha = __builtin_amdgcn_exp2f(acc.m - m_new);
+    acc.l *= alpha;
+#pragma unroll
+    for (int b = 0; b < D / 16; ++b) acc.o[b] *= alpha;
+    acc.m = m_new;
+  }
+  bf16x8 p;
+  float psum = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const __bf16 pb = static_cast<__bf16>(__builtin_amdgcn_exp2f(sc[j] - acc.m));
+    const float pf = static_cast<float>(pb);
+    psum += pf;
+    // the value scale of slot 8G + j (zero for a missing slot)
+    p[j] = static_cast<__bf16>(pf * __uint_as_float(f.s[2 + (j >> 2)][j & 3]));
+  }
+  acc.l += psum;
+  const u32x4 pu = __builtin_bit_cast(u32x4, p);
+#pragma unroll
+  for (int b = 0; b < D / 16; b += 2) {
+    const u32x4 x = f.v[b / 2];
+    acc.o[b] = mfma_bf16(f8_to_bf16x8(x[0], x[1]), pu, acc.o[b]);
+    acc.o[b + 1] = mfma_bf16(f8_to_bf16x8(x[2], x[3]), pu, acc.o[b + 1]);
+  }
+}
+
 __device__ inline float wave_max(float v) {
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
@@ -258,17 +388,22 @@ __device__ void merge_head(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsr
         if (f < pieces) {
           const int row = 4 * f / D;
           u32x4 x[8];
+          // only partials with a nonzero weight are read: a wave of the span
+          // that got no tiles wrote none, and its slot holds stale bytes
+          float wu[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) wu[u] = i0 + u < nb ? wts[i0 + u][row] : 0.f;
 #pragma unroll
           for (int u = 0; u < 8; ++u) {
             const size_t p2 = static_cast<size_t>(b0 + i0 + u) + hh;
-            x[u] = (i0 + u < nb) ? __builtin_amdgcn_raw_buffer_load_b128(
-                                       acc_rsrc, static_cast<uint32_t>((p2 * g * D + 4 * f) * 4), 0,
-                                       kCachePolicySc1)
-                                 : u32x4{0u, 0u, 0u, 0u};
+            x[u] = wu[u] != 0.f ? __builtin_amdgcn_raw_buffer_load_b128(
+                                      acc_rsrc, static_cast<uint32_t>((p2 * g * D + 4 * f) * 4), 0,
+                                      kCachePolicySc1)
+                                : u32x4{0u, 0u, 0u, 0u};
           }
 #pragma unroll
           for (int u = 0; u < 8; ++u)
-            if (i0 + u < nb) num[j] += wts[i0 + u][row] * __builtin_bit_cast(f32x4, x[u]);
+            if (wu[u] != 0.f) num[j] += wu[u] * __builtin_bit_cast(f32x4, x[u]);
         }
       }
     }
@@ -310,6 +445,8 @@ __device__ void merge_head_small(const float2* part_ml, __amdgpu_buffer_rsrc_t a
     m[r] = (live && r < g) ? load_coherent(ml + 2 * r) : -INFINITY;
     l[r] = (live && r < g) ? load_coherent(ml + 2 * r + 1) : 0.f;
   }
+  // partials of waves that got no tiles were never written (stale bytes):
+  // neither loaded nor added
   u32x4 x[kMaxPieces][kMaxParts];
 #pragma unroll
   for (int j = 0; j < kMaxPieces; ++j) {
@@ -317,7 +454,7 @@ __device__ void merge_head_small(const float2* part_ml, __amdgpu_buffer_rsrc_t a
 #pragma unroll
     for (int u = 0; u < kMaxParts; ++u) {
       const size_t p2 = static_cast<size_t>(wf + u) + hh;
-      x[j][u] = (f < pieces && u < np)
+      x[j][u] = (f < pieces && u < np && ((live_mask >> u) & 1))
                     ? __builtin_amdgcn_raw_buffer_load_b128(
                           acc_rsrc, static_cast<uint32_t>((p2 * g * D + 4 * f) * 4), 0, kCachePolicySc1)
                     : u32x4{0u, 0u, 0u, 0u};
@@ -346,7 +483,7 @@ __device__ void merge_head_small(const float2* part_ml, __amdgpu_buffer_rsrc_t a
 #pragma unroll
         for (int u = 0; u < kMaxParts; ++u) {
           const float wu = __shfl(wgt[r], u, 64);
-          if (r == row && u < np) num += wu * __builtin_bit_cast(f32x4, x[j][u]);
+          if (r == row && u < np && ((live_mask >> u) & 1)) num += wu * __builtin_bit_cast(f32x4, x[j][u]);
         }
         if (r == row) d = den[r];
       }
@@ -355,7 +492,7 @@ __device__ void merge_head_small(const float2* part_ml, __amdgpu_buffer_rsrc_t a
   }
 }
 
-template <int D>
+template <int D, bool FP8>
 __global__ __launch_bounds__(256, 1) void decode_kernel(
     const int32_t* __restrict__ status, const HeadDesc* __restrict__ desc,
     const int32_t* __restrict__ cum_tiles, const int32_t* __restrict__ wave_bounds,
@@ -419,9 +556,10 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
     const int full_hi = (seg_end == c1 && (L & (kTile - 1))) ? t_hi - 1 : t_hi;
     // tile t of the head: page from a scalar load (the whole wave works on
     // one head), then the tile's 16 KB block inside the page
+    constexpr size_t kTileBytes = FP8 ? static_cast<size_t>(D) * 64 + 256 : static_cast<size_t>(D) * 128;
     auto tile_of = [&](int t) -> char* {
       return pool + static_cast<size_t>(pt[t >> tiles_per_page_log2]) * a.page_bytes +
-             static_cast<size_t>(t & ((1 << tiles_per_page_log2) - 1)) * (D * 128);
+             static_cast<size_t>(t & ((1 << tiles_per_page_log2) - 1)) * kTileBytes;
     };
     // The token appended by this call (slot d.z) is written into its tile by
     // the one wave whose segment covers that tile, before the segment's
@@ -429,13 +567,44 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
     if (k_in != nullptr && d.z >= t_lo * kTile && d.z < t_hi * kTile) {
       char* tile = const_cast<char*>(tile_of(d.z >> 5));
       const int j = d.z & 31;
-      if (lane < D / 8)
-        *reinterpret_cast<u32x4*>(tile + k_elem_off(j, 8 * lane)) =
-            reinterpret_cast<const u32x4*>(k_in + static_cast<size_t>(hh) * D)[lane];
+      if constexpr (FP8) {
+        if (lane < D / 8)
+          fp8_store_token(tile, j, D, lane, reinterpret_cast<const uint4*>(k_in + static_cast<size_t>(hh) * D)[lane],
+                          reinterpret_cast<const uint4*>(v_in + static_cast<size_t>(hh) * D)[lane]);
+      } else {
+        if (lane < D / 8)
+          *reinterpret_cast<u32x4*>(tile + k_elem_off(j, 8 * lane)) =
+              reinterpret_cast<const u32x4*>(k_in + static_cast<size_t>(hh) * D)[lane];
 #pragma unroll
-      for (int e = lane; e < D; e += 64)
-        *reinterpret_cast<uint16_t*>(tile + v_elem_off(j, e, D)) = v_in[static_cast<size_t>(hh) * D + e];
+        for (int e = lane; e < D; e += 64)
+          *reinterpret_cast<uint16_t*>(tile + v_elem_off(j, e, D)) = v_in[static_cast<size_t>(hh) * D + e];
+      }
     }
+    if constexpr (FP8) {
+      if (t_lo < full_hi) {
+        FragF8<D> fa, fb;
+        int t = t_lo;
+        load_tile_f8<D>(fa, tile_of(t), lane, G);
+        for (; t + 2 < full_hi; t += 2) {
+          load_tile_f8<D>(fb, tile_of(t + 1), lane, G);
+          compute_tile_f8<D>(acc, fa, qf, a.scale_log2, kTile, G);
+          load_tile_f8<D>(fa, tile_of(t + 2), lane, G);
+          compute_tile_f8<D>(acc, fb, qf, a.scale_log2, kTile, G);
+        }
+        if (t + 1 < full_hi) {
+          load_tile_f8<D>(fb, tile_of(t + 1), lane, G);
+          compute_tile_f8<D>(acc, fa, qf, a.scale_log2, kTile, G);
+          compute_tile_f8<D>(acc, fb, qf, a.scale_log2, kTile, G);
+        } else {
+          compute_tile_f8<D>(acc, fa, qf, a.scale_log2, kTile, G);
+        }
+      }
+      if (full_hi < t_hi) {
+        FragF8<D> ft;
+        load_tail_f8<D>(ft, tile_of(full_hi), lane, L - full_hi * kTile, r, G);
+        compute_tile_f8<D>(acc, ft, qf, a.scale_log2, L - full_hi * kTile, G);
+      }
+    } else {
     if (t_lo < full_hi) {
       // Two register sets; the next tile's loads are always in flight while
       // the current one is computed (the prefetch is unconditional inside the
@@ -461,6 +630,7 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
       Frag<D> ft;
       load_tail<D>(ft, tile_of(full_hi), lo, L - full_hi * kTile, r, G);
       compute_tile<D>(acc, ft, qf, a.scale_log2, L - full_hi * kTile, G);
+    }
     }
     float l = acc.l;
     l += __shfl_xor(l, 16, 64);
@@ -515,7 +685,7 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
   }
 }
 
-template <int D>
+template <int D, bool FP8>
 hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
                            int layer, int n, const void* q, const void* k, const void* v, float* out,
                            int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
@@ -536,7 +706,7 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
   a.zero_neuron = c.decision_source == DMS_DECIDE_QUERY;
   a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
   if (ev_start) (void)hipEventRecord(ev_start, st);
-  hipLaunchKernelGGL(decode_kernel<D>, dim3(waves / kWavesPerBlock), dim3(256), 0, st, status,
+  hipLaunchKernelGGL((decode_kernel<D, FP8>), dim3(waves / kWavesPerBlock), dim3(256), 0, st, status,
                      reinterpret_cast<const HeadDesc*>(w + lo.ws_head_desc), cum,
                      reinterpret_cast<const int32_t*>(w + lo.ws_wave_bounds),
                      reinterpret_cast<const int4*>(w + lo.ws_wave_desc),
@@ -555,11 +725,16 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
 hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
                          int layer, int n, const void* q, const void* k, const void* v, float* out,
                          int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
+  const bool fp8 = c.kv_format == DMS_KV_FP8;
   if (c.head_dim == 128)
-    return launch_decode_d<128>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st, ev_start,
-                                ev_stop);
-  return launch_decode_d<64>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st, ev_start,
-                             ev_stop);
+    return fp8 ? launch_decode_d<128, true>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st,
+                                            ev_start, ev_stop)
+               : launch_decode_d<128, false>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st,
+                                             ev_start, ev_stop);
+  return fp8 ? launch_decode_d<64, true>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st,
+                                         ev_start, ev_stop)
+             : launch_decode_d<64, false>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st,
+                                          ev_start, ev_stop);
 }
 
 // One decode wave per SIMD (a block of 4 waves per CU).  Measured on MI355X
@@ -570,9 +745,12 @@ int decode_resident_waves(const dms_config& c) {
   int dev = 0, cus = 0, blocks = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -1;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
+  const bool fp8 = c.kv_format == DMS_KV_FP8;
   hipError_t e = c.head_dim == 128
-      ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_kernel<128>, 256, 0)
-      : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_kernel<64>, 256, 0);
+      ? (fp8 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_kernel<128, true>, 256, 0)
+             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_kernel<128, false>, 256, 0))
+      : (fp8 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_kernel<64, true>, 256, 0)
+             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_kernel<64, false>, 256, 0));
   if (e != hipSuccess || blocks < 1) return -1;
   int waves = cus * kWavesPerBlock;
   if (waves > kMaxWaves) waves = kMaxWaves / kWavesPerBlock * kWavesPerBlock;

@@ -44,6 +44,7 @@ class DmsConfig(ctypes.Structure):
         ("eviction", ctypes.c_int32),
         ("decision_source", ctypes.c_int32),
         ("decision_bias", ctypes.c_float),
+        ("kv_format", ctypes.c_int32),
     ]
 
 
@@ -63,6 +64,8 @@ DMS_EVICT_DELAYED = 0
 DMS_EVICT_IMMEDIATE = 1
 DMS_DECIDE_CALLER = 0
 DMS_DECIDE_QUERY = 1
+DMS_KV_BF16 = 0
+DMS_KV_FP8 = 1
 
 
 class DmsStateOffsets(ctypes.Structure):
@@ -157,10 +160,11 @@ def _check(rc, where):
 def make_config(num_layers, max_seqs, num_kv_heads, group_size, head_dim, window,
                 page_size, num_pages, max_pages_per_head, max_chunk_tokens=0,
                 softmax_scale=0.0, eviction=DMS_EVICT_DELAYED,
-                decision_source=DMS_DECIDE_CALLER, decision_bias=-5.0) -> DmsConfig:
+                decision_source=DMS_DECIDE_CALLER, decision_bias=-5.0,
+                kv_format=DMS_KV_BF16) -> DmsConfig:
     return DmsConfig(num_layers, max_seqs, num_kv_heads, group_size, head_dim, window,
                      page_size, num_pages, max_pages_per_head, max_chunk_tokens,
-                     softmax_scale, eviction, decision_source, decision_bias)
+                     softmax_scale, eviction, decision_source, decision_bias, kv_format)
 
 
 # ---------------------------------------------------------------------------
@@ -351,11 +355,13 @@ class DmsCache:
         )
 
     def pool_page_kv(self, layer, page):
-        """(K [P, d], V [P, d]) bf16 bit patterns (uint16) of one page, on the host."""
-        import torch
-        raw = self.pools[layer][page * self.page_bytes:(page + 1) * self.page_bytes]
-        return unpack_page(raw.view(torch.int16).cpu().numpy().view(np.uint16),
-                           self.cfg.page_size, self.cfg.head_dim)
+        """One page on the host: bf16 pages give (K [P, d], V [P, d]) bit patterns
+        (uint16); FP8 pages give (K codes, V codes [P, d] uint8, K scales, V scales
+        [P] float32)."""
+        raw = self.pools[layer][page * self.page_bytes:(page + 1) * self.page_bytes].cpu().numpy()
+        if self.cfg.kv_format == DMS_KV_FP8:
+            return unpack_page_fp8(raw, self.cfg.page_size, self.cfg.head_dim)
+        return unpack_page(raw.view(np.uint16), self.cfg.page_size, self.cfg.head_dim)
 
 
 def unpack_page(u16, P, D):
@@ -364,6 +370,26 @@ def unpack_page(u16, P, D):
     k = tiles[:, 0].reshape(P // 32, D // 32, 32, 32).transpose(0, 2, 1, 3).reshape(P, D)
     v = tiles[:, 1].reshape(P // 32, D, 32).transpose(0, 2, 1).reshape(P, D)
     return k, v
+
+
+def unpack_page_fp8(raw, P, D):
+    """Decode one FP8 page (bytes, layout of dms.h) into K codes, V codes [P, D]
+    (uint8) and K scales, V scales [P] (float32)."""
+    tb = 64 * D + 256
+    tiles = np.asarray(raw, np.uint8).reshape(P // 32, tb)
+    j = np.arange(32)[:, None]
+    e = np.arange(D)[None, :]
+    h, r = (j // 4) % 2, 4 * (j // 8) + j % 4
+    koff = (e // 64) * 2048 + h * 1024 + (16 * ((e // 8) % 4) + r) * 16 + 8 * ((e // 32) % 2) + e % 8
+    voff = 32 * D + (e // 32) * 1024 + (16 * (j // 8) + e % 16) * 16 + 8 * ((e // 16) % 2) + j % 8
+    soff = 64 * D + (np.arange(32) // 8) * 64 + (np.arange(32) % 8) * 4
+    k = tiles[:, koff].reshape(P, D)
+    v = tiles[:, voff].reshape(P, D)
+    sc = tiles[:, soff[:, None] + np.arange(4)[None, :]].reshape(P // 32, 32, 4)
+    ks = np.ascontiguousarray(sc).view(np.float32).reshape(P)
+    sv = tiles[:, soff[:, None] + 32 + np.arange(4)[None, :]].reshape(P // 32, 32, 4)
+    vs = np.ascontiguousarray(sv).view(np.float32).reshape(P)
+    return k, v, ks, vs
 
 
 # ---------------------------------------------------------------------------

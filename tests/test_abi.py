@@ -56,6 +56,8 @@ def _cfg(**kw):
     (dict(decision_source=2), dms.DMS_ERR_INVALID),
     (dict(decision_source=1, decision_bias=float("nan")), dms.DMS_ERR_INVALID),
     (dict(decision_source=1, decision_bias=float("inf")), dms.DMS_ERR_INVALID),
+    (dict(kv_format=2), dms.DMS_ERR_INVALID),
+    (dict(kv_format=-1), dms.DMS_ERR_INVALID),
 ])
 def test_bad_configuration(kw, code):
     rc = dms.lib().dms_layout(ctypes.byref(_cfg(**kw)), None, None, None, None)
@@ -202,3 +204,46 @@ def test_train_workspace_and_host_side_errors():
         assert fn(4, None, None, ctypes.c_float(float("nan")), None, None) == dms.DMS_ERR_INVALID
         assert fn(4, None, None, ctypes.c_float(1.0), None, None) == dms.DMS_ERR_INVALID
         assert fn(0, None, None, ctypes.c_float(1.0), None, None) == dms.DMS_OK
+
+
+def test_fp8_pages_layout_and_host_checks():
+    """FP8 pages are P/32 tiles of 64 d + 256 bytes; prefill is rejected on an
+    FP8 context before anything is launched (fake pointers)."""
+    import numpy as np
+    for D in (64, 128):
+        for P in (32, 64, 256):
+            _, pool, _, pg = dms.dms_layout(_cfg(kv_format=dms.DMS_KV_FP8, head_dim=D, page_size=P))
+            assert pg == P // 32 * (64 * D + 256) and pool == pg * _cfg().num_pages
+    # documented offsets (include/dms.h) -> unpack_page_fp8
+    P, D = 64, 128
+    raw = np.zeros(P // 32 * (64 * D + 256), np.uint8)
+    for s_ in (0, 5, 31, 32, 63):
+        t, j = divmod(s_, 32)
+        base = t * (64 * D + 256)
+        h, r = (j // 4) % 2, 4 * (j // 8) + j % 4
+        for e in (0, 7, 31, 32, 64, 100, 127):
+            ko = (e // 64) * 2048 + h * 1024 + (16 * ((e // 8) % 4) + r) * 16 + 8 * ((e // 32) % 2) + e % 8
+            vo = 32 * D + (e // 32) * 1024 + (16 * (j // 8) + e % 16) * 16 + 8 * ((e // 16) % 2) + j % 8
+            raw[base + ko] = (s_ + e) % 251
+            raw[base + vo] = (3 * s_ + e) % 251
+        so = 64 * D + (j // 8) * 64 + (j % 8) * 4
+        raw[base + so: base + so + 4] = np.array([2.0 ** -s_], np.float32).view(np.uint8)
+        raw[base + so + 32: base + so + 36] = np.array([2.0 ** s_], np.float32).view(np.uint8)
+    k, v, ks, vs = dms.unpack_page_fp8(raw, P, D)
+    for s_ in (0, 5, 31, 32, 63):
+        assert ks[s_] == 2.0 ** -s_ and vs[s_] == 2.0 ** s_
+        for e in (0, 7, 31, 32, 64, 100, 127):
+            assert k[s_, e] == (s_ + e) % 251 and v[s_, e] == (3 * s_ + e) % 251
+    L = dms.lib()
+    Pp = 0x100
+    ctx = dms.dms_create(_cfg(kv_format=dms.DMS_KV_FP8), 0x1000, [0x2000, 0x3000], 0x4000)
+    try:
+        assert L.dms_prefill_chunk(ctx, 0, 1, Pp, Pp, 10, 10, Pp, Pp, Pp, Pp, Pp, None) == dms.DMS_ERR_UNSUPPORTED
+    finally:
+        dms.dms_destroy(ctx)
+    ctx = dms.dms_create(_cfg(kv_format=dms.DMS_KV_FP8, decision_source=dms.DMS_DECIDE_QUERY),
+                         0x1000, [0x2000, 0x3000], 0x4000)
+    try:
+        assert L.dms_prefill_chunk_q(ctx, 0, 1, Pp, Pp, 10, 10, Pp, Pp, Pp, None, Pp, None) == dms.DMS_ERR_UNSUPPORTED
+    finally:
+        dms.dms_destroy(ctx)

@@ -260,3 +260,24 @@ def test_seq_reset_returns_pages_in_order():
     # reuse after reset
     _append_chunks(dms, cache, orc, [2], inp, {2: 0}, {2: 120}, 120)
     compare_state(cache.export(0), orc, [0, 1, 2])
+
+
+@pytest.mark.parametrize("lens", [(40, 97, 130), (300, 5, 1)])
+def test_merge_ignores_stale_workspace(lens):
+    """Fewer tiles than decode waves, so heads split over spans that include
+    waves with no tiles (their partial slots are never written): a workspace
+    filled with NaN bytes beforehand must not reach the outputs.  Spans of up
+    to 4 waves take the register merge, longer ones the batched merge."""
+    torch = _torch()
+    dms, cfg, cache = _mk(dict(num_layers=1, max_seqs=3, num_kv_heads=2, group_size=3,
+                               head_dim=128, window=8, page_size=32, num_pages=64,
+                               max_pages_per_head=16, max_chunk_tokens=3 * 300))
+    cache.workspace.fill_(0xFF)
+    dms.dms_init_state(cache.ctx)     # re-zeroes only what the library keeps between calls
+    torch.cuda.synchronize()
+    seqs = [2, 0, 1]
+    ln = dict(zip(seqs, lens))
+    inp = {s: SeqInputs(51, 0, s, ln[s] + 8, 2, 3, 128, 0.5) for s in seqs}
+    orc = _oracle_for(cfg)
+    _append_chunks(dms, cache, orc, seqs, inp, {s: 0 for s in seqs}, ln, 300)
+    _decode_steps(dms, cache, orc, seqs, inp, ln, 8, 3, check_every=4)
