@@ -27,6 +27,7 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0
 # rocprofv3 summary of the decode kernel on the default workload
 TRAFFIC_PROFILE = "decode_kernel_qwen-r1-32b-8x.txt"
+TRAFFIC_PROFILE_FP8 = "decode_kernel_qwen-r1-32b-8x-fp8.txt"
 
 # Synthetic stand-ins for the paper's reasoning-model shapes (Qwen-R1 family).
 WORKLOADS = {
@@ -71,6 +72,13 @@ def profiled_traffic(profile, sources):
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def row_bytes(wl):
+    """Bytes read per retained token of one KV head: K and V rows in bf16, or
+    E4M3 codes plus one float32 scale per row in FP8 pages."""
+    D = wl["head_dim"]
+    return 2 * D + 8 if wl.get("kv_format", 0) == 1 else 2 * D * 2
 
 
 def contexts(wl, rng_seed):
@@ -118,7 +126,7 @@ def build(wl, steps_total, chunk_tokens, dev):
     # the state is built by chunk appends of up to 16 sequences at a time
     grp = min(B, 16)
     cfg = dms.make_config(nl, B, H, g, D, w, P, pages_layer + 8, max_pages_head + 1,
-                          chunk_tokens * grp)
+                          chunk_tokens * grp, kv_format=wl.get("kv_format", dms.DMS_KV_BF16))
     mb, pb, wb, _ = dms.dms_layout(cfg)
     log(f"pool {pb * nl / 2**30:.1f} GiB ({pages_layer + 8} pages/layer), meta "
         f"{mb / 2**30:.2f} GiB, workspace {wb / 2**20:.1f} MiB")
@@ -199,10 +207,11 @@ def cpu_baseline(wl, ctx, budget_s=12.0):
     import numpy as np
 
     import dms_synth as sy
-    from oracle import dense_dms_attention_head
+    from oracle import dense_dms_attention_head, fake_quantize_fp8
 
     B, H, g, D, w, p = (wl["batch"], wl["kv_heads"], wl["group"], wl["head_dim"],
                         wl["window"], wl["p_evict"])
+    fp8 = wl.get("kv_format", 0) == 1
     nl, seed = wl["layers"], wl["seed"]
     rng = np.random.default_rng(12345)
     triples = [(int(rng.integers(nl)), int(rng.integers(B)), int(rng.integers(H))) for _ in range(6)]
@@ -214,6 +223,8 @@ def cpu_baseline(wl, ctx, budget_s=12.0):
         pos = np.arange(T)
         kh = f32(sy.head_sequence_np(seed, sy.STREAM_K, layer, s, h, pos, D))
         vh = f32(sy.head_sequence_np(seed, sy.STREAM_V, layer, s, h, pos, D))
+        if fp8:   # the stored (dequantized) rows
+            kh, vh = fake_quantize_fp8(kh), fake_quantize_fp8(vh)
         fh = sy.flags_np(seed, p, layer, s, h, pos)
         qd = np.arange(D)[None, None, :]
         qh = f32(sy.token_vectors_np(seed, sy.STREAM_Q, layer, s, (h * g + np.arange(g))[None, :, None],
@@ -229,7 +240,7 @@ def cpu_baseline(wl, ctx, budget_s=12.0):
                 elapsed += time.perf_counter() - t0
                 head_steps += 1
                 visible = min(w, t + 1) + int(np.sum(fh[: max(0, t - w + 1)] == 0))
-                bytes_equiv += visible * 2 * D * 2
+                bytes_equiv += visible * row_bytes(wl)
         if time.perf_counter() - t_start > 4 * budget_s:
             break
     threads = os.cpu_count()
@@ -246,7 +257,8 @@ def cpu_baseline(wl, ctx, budget_s=12.0):
         "cores": threads,
         "kind": "oracle",
         "sample": f"{head_steps} head-steps (one KV head, its {g} query heads, one decode "
-                  f"position, dense float64 masked attention over the full history) on "
+                  f"position, dense float64 masked attention over the full history"
+                  f"{' of the dequantized FP8 rows' if fp8 else ''}) on "
                   f"{len(samples)} sampled (layer, sequence, KV head) triples; value = their "
                   f"retained-KV bytes / CPU time",
         "head_steps_per_s": head_steps / elapsed,
@@ -587,7 +599,7 @@ def measure_decode(wl, steps, warmup, dev):
     if dms.dms_status(cache.ctx) != 0:
         raise RuntimeError("decode failed")
     Lstep = torch.stack(L0)[None] + torch.cumsum(fresh, dim=0)
-    kv = float(Lstep[warmup:].sum()) * 2 * D * 2 / steps
+    kv = float(Lstep[warmup:].sum()) * row_bytes(wl) / steps
     mean_L = float(Lstep[warmup:].double().mean())
     ms = e0.elapsed_time(e1) / steps
     del graph, q, k, v, flags, fresh, out
@@ -606,6 +618,7 @@ def run_sweep(args):
     not fit in HBM are reported as such."""
     import torch
     dev = "cuda:0"
+    fmt = 1 if args.kv_format == "fp8" else 0
     points = []
     if args.sweep == "fig4-r1":
         for name in ("qwen-r1-1.5b", "qwen-r1-7b", "qwen-r1-32b"):
@@ -625,7 +638,7 @@ def run_sweep(args):
             for cr in (1, 4, 8):
                 p = 1 - 1 / cr
                 Lr = min(w, ctxlen) + (1 - p) * max(0, ctxlen - w)
-                per_seq = sh["layers"] * sh["kv_heads"] * Lr * sh["head_dim"] * 4 * 1.03
+                per_seq = sh["layers"] * sh["kv_heads"] * Lr * row_bytes(dict(sh, kv_format=fmt)) * 1.03
                 _, _, weights = app_i_estimate(sh, 1, 0)
                 budget = HBM_BYTES - weights - 24e9       # weights, inputs, workspace, margin
                 points.append((name, int(budget // per_seq), ctxlen, cr, w))
@@ -633,17 +646,18 @@ def run_sweep(args):
         sh = SWEEP_SHAPES[name]
         p = 1 - 1 / cr
         Lr = min(w, ctxlen) + (1 - p) * max(0, ctxlen - w)
-        kv_est = sh["layers"] * B * sh["kv_heads"] * Lr * sh["head_dim"] * 4
+        kv_est = sh["layers"] * B * sh["kv_heads"] * Lr * row_bytes(dict(sh, kv_format=fmt))
         lat, share, weights = app_i_estimate(sh, B, Lr)
         rec = {"sweep": args.sweep, "model_shape": name, "batch": B, "context": ctxlen, "cr": cr,
-               "window": w, "kv_cache_gb": round(kv_est / 1e9, 2),
+               "window": w, "kv_format": args.kv_format, "kv_cache_gb": round(kv_est / 1e9, 2),
                "app_i_latency_ms": round(1e3 * lat, 3), "app_i_kv_share": round(share, 3)}
         if kv_est + weights + 16e9 > HBM_BYTES:
             rec["status"] = "KV cache does not fit in HBM next to the weights"
             print(json.dumps(rec), flush=True)
             continue
         wl = dict(layers=sh["layers"], batch=B, kv_heads=sh["kv_heads"], group=sh["group"],
-                  head_dim=sh["head_dim"], context=ctxlen, window=w, p_evict=p, seed=11)
+                  head_dim=sh["head_dim"], context=ctxlen, window=w, p_evict=p, seed=11,
+                  kv_format=fmt)
         ms, kv, mean_L = measure_decode(wl, args.steps, args.warmup, dev)
         rec.update({"status": "measured", "attn_ms_per_step": round(ms, 3),
                     "kv_gb_per_step": round(kv / 1e9, 3),
@@ -664,6 +678,8 @@ def main():
     ap.add_argument("--window", type=int, default=256, choices=[64, 256],
                     help="window of the heterogeneous stress workload")
     ap.add_argument("--chunk", type=int, default=4096)
+    ap.add_argument("--kv-format", choices=["bf16", "fp8"], default="bf16",
+                    help="page format of the decode workloads (fp8: E4M3 rows with power-of-two scales)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run a 1 GiB device copy first (reference kernel for HBM counters)")
@@ -698,7 +714,10 @@ def main():
     if args.workload == "qwen-r1-32b-train":
         run_train(args)
         return
-    wl = WORKLOADS[args.workload]
+    wl = dict(WORKLOADS[args.workload])
+    if args.kv_format == "fp8":
+        wl["kv_format"] = dms.DMS_KV_FP8
+        wl["desc"] += ", FP8 E4M3 KV pages"
     S = args.warmup + 2 * args.steps
     cache, ctx, L0 = build(wl, S, args.chunk, dev)
     q, k, v, flags, fresh = step_inputs(wl, ctx, S, dev)
@@ -707,7 +726,7 @@ def main():
     out = torch.empty((nl, B, H * g, D), dtype=torch.float32, device=dev)
     # retained length of every head when step s attends (after its append)
     Lstep = torch.stack(L0)[None] + torch.cumsum(fresh, dim=0)        # [S, nl, B, H]
-    kv_bytes = Lstep.sum(dim=(1, 2, 3)).to(torch.float64) * 2 * D * 2  # per step, all layers
+    kv_bytes = Lstep.sum(dim=(1, 2, 3)).to(torch.float64) * row_bytes(wl)  # per step, all layers
 
     def run_step(s):
         for layer in range(nl):
@@ -768,7 +787,8 @@ def main():
     mean_L = float(Lstep[t_lo:t_hi].double().mean())
     traffic = None
     if args.workload == "qwen-r1-32b-8x":
-        traffic = profiled_traffic(TRAFFIC_PROFILE, ["dms_common.h", "dms_decode.hip"])
+        traffic = profiled_traffic(TRAFFIC_PROFILE_FP8 if args.kv_format == "fp8" else TRAFFIC_PROFILE,
+                                   ["dms_common.h", "dms_fp8.h", "dms_decode.hip"])
     res = {
         "metric": "DMS decode attn: achieved KV HBM GB/s (% of peak) + decode tok/s at 8x",
         "value": round(value, 1),
@@ -780,10 +800,11 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16" if args.kv_format == "bf16" else "fp8-e4m3 kv, bf16 mfma",
         "data": "synthetic",
         "config": {
             "workload": wl["desc"],
+            "kv_format": args.kv_format,
             "layers": nl, "batch": B, "kv_heads": H, "query_heads": H * g,
             "head_dim": D, "window": wl["window"], "p_evict": wl["p_evict"],
             "context": wl["context"] if not isinstance(wl["context"], tuple) else list(wl["context"]),

@@ -582,6 +582,8 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
     }
     if constexpr (FP8) {
       if (t_lo < full_hi) {
+        // two register sets, as for bf16 (a third set, keeping two FP8 tiles
+        // in flight, measured slower: 235 vs 217 us at the 32B-shaped step)
         FragF8<D> fa, fb;
         int t = t_lo;
         load_tile_f8<D>(fa, tile_of(t), lane, G);
