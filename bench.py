@@ -323,7 +323,9 @@ def run_stress(args):
             need[s] = (min(w, T) + kept + P - 1) // P
         max_pages = max(max_pages, int(need.max()))
         pages = max(pages, int(need.sum()))
-    cfg = dms.make_config(nl, B, H, g, D, w, P, pages + 64, max_pages + 2, C * B)
+    fp8 = args.kv_format == "fp8"
+    cfg = dms.make_config(nl, B, H, g, D, w, P, pages + 64, max_pages + 2, C * B,
+                          kv_format=dms.DMS_KV_FP8 if fp8 else dms.DMS_KV_BF16)
     cache = dms.DmsCache(cfg, device=dev)
     sid = torch.arange(B, dtype=torch.int32, device=dev)
     gen = torch.Generator(device=dev)
@@ -382,7 +384,8 @@ def run_stress(args):
             prev = flags(layer, dseq, dpos - w)
             freshd = ((dpos[:, None] < w) | (prev == 0)).to(torch.int64)
             L[torch.as_tensor(dc, device=dev)] += freshd
-            dbytes[st] += float(L[torch.as_tensor(dc, device=dev)].sum()) * 2 * D * 2
+            dbytes[st] += float(L[torch.as_tensor(dc, device=dev)].sum()) * row_bytes(
+                dict(head_dim=D, kv_format=1 if fp8 else 0))
 
     def step(st):
         for layer in range(nl):
@@ -415,7 +418,8 @@ def run_stress(args):
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(step_ms, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": "32B-shaped heterogeneous stress: 64 layers, 32 sequences x 8 KV "
+        "config": {"kv_format": args.kv_format,
+                   "workload": "32B-shaped heterogeneous stress: 64 layers, 32 sequences x 8 KV "
                                "heads (group 5), per-head eviction rate ~ Beta(7,1), contexts "
                                "log-uniform in [1K, 128K]; per step a 4096-token masked prefill "
                                "for 4 sequences and a decode step for 28",

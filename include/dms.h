@@ -134,9 +134,7 @@ enum { DMS_EVICT_DELAYED = 0, DMS_EVICT_IMMEDIATE = 1 };
  *     code * 2^e.  A 32-slot tile takes 64 d + 256 bytes (8.25 KB at
  *     d = 128), roughly halving the bytes decode reads.  Every key and value
  *     is attended in its stored form, including the token a decode step
- *     appends.  dms_prefill_chunk / dms_prefill_chunk_q return
- *     DMS_ERR_UNSUPPORTED on an FP8 context; appends, chunk appends and
- *     decode support it.
+ *     appends and the chunk's own tokens in a prefill call.
  */
 enum { DMS_KV_BF16 = 0, DMS_KV_FP8 = 1 };
 enum { DMS_DECIDE_CALLER = 0, DMS_DECIDE_QUERY = 1 };

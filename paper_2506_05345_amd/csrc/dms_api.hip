@@ -361,7 +361,6 @@ int dms_prefill_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev
   int rc = check_call(ctx, layer, n, seq_ids_dev);
   if (rc) return rc;
   if (ctx->c.cfg.decision_source != DMS_DECIDE_CALLER) return DMS_ERR_INVALID;
-  if (ctx->c.cfg.kv_format != DMS_KV_BF16) return DMS_ERR_UNSUPPORTED;
   if ((rc = check_chunk(ctx, cu_seqlens_dev, total_tokens, max_seqlen))) return rc;
   if (total_tokens == 0) return DMS_OK;
   if (!q_dev || !k_dev || !v_dev || !flags_dev || !out_dev) return DMS_ERR_INVALID;
@@ -376,7 +375,6 @@ int dms_prefill_chunk_q(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_d
   int rc = check_call(ctx, layer, n, seq_ids_dev);
   if (rc) return rc;
   if (ctx->c.cfg.decision_source != DMS_DECIDE_QUERY) return DMS_ERR_INVALID;
-  if (ctx->c.cfg.kv_format != DMS_KV_BF16) return DMS_ERR_UNSUPPORTED;
   if ((rc = check_chunk(ctx, cu_seqlens_dev, total_tokens, max_seqlen))) return rc;
   if (total_tokens == 0) return DMS_OK;
   if (!q_dev || !k_dev || !v_dev || !out_dev) return DMS_ERR_INVALID;

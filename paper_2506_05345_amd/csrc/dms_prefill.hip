@@ -27,7 +27,10 @@
 // by every wave with 16-byte LDS loads straight into operand registers.  A tile is
 // masked per element only when some query of the block does not see one of
 // its keys; the online softmax works in the exp2 domain with a lazy rescale.
+#include <type_traits>
+
 #include "dms_common.h"
+#include "dms_fp8.h"
 
 namespace dms {
 namespace {
@@ -166,7 +169,7 @@ __device__ inline size_t ws_tile(const PrefillArgs& a, int region, int h, int i,
 // chunk's keys and values -- region 0: in chunk order; region 1: the kept
 // tokens in list order -- into workspace tiles in the pool's tile layout
 // (keys [d/32][32][32], values transposed [d][32]); rows past the end are 0.
-template <int D>
+template <int D, bool FP8>
 __global__ __launch_bounds__(kThreads) void prefill_tile_kernel(PrefillArgs a) {
   __shared__ uint16_t vrows[32][D + 2];
   if (load_status(a.status) != 0) return;
@@ -176,9 +179,28 @@ __global__ __launch_bounds__(kThreads) void prefill_tile_kernel(PrefillArgs a) {
   const int cnt = region ? a.list_cnt[hh] : C;
   if (k * 32 >= cnt) return;
   const int32_t* lst = a.list + static_cast<size_t>(h) * a.total + tok0;
-  char* tile = a.tiles + ws_tile(a, region, h, i, k) * (D * 128);
   const int tid = threadIdx.x;
   constexpr int kPieces = 32 * D / 8;   // 16-byte pieces of 32 rows
+  if constexpr (FP8) {
+    // FP8 pages: the chunk's rows are quantized exactly as the commit will
+    // store them (D/8 consecutive threads per row; rows past the end get
+    // zero codes)
+    char* tile = a.tiles + ws_tile(a, region, h, i, k) * fp8_tile_bytes(D);
+    for (int pc = tid; pc < kPieces; pc += kThreads) {
+      const int j = pc / (D / 8), part = pc % (D / 8);
+      const int idx = 32 * k + j;
+      uint4 kx = make_uint4(0u, 0u, 0u, 0u), vx = make_uint4(0u, 0u, 0u, 0u);
+      if (idx < cnt) {
+        const int c = region ? lst[idx] : idx;
+        const size_t row = (static_cast<size_t>(tok0 + c) * a.H + h) * D + 8 * part;
+        kx = *reinterpret_cast<const uint4*>(a.k + row);
+        vx = *reinterpret_cast<const uint4*>(a.v + row);
+      }
+      fp8_store_token(tile, j, D, part, kx, vx);
+    }
+    return;
+  }
+  char* tile = a.tiles + ws_tile(a, region, h, i, k) * (D * 128);
   for (int pc = tid; pc < kPieces; pc += kThreads) {
     const int j = pc / (D / 8), e0 = 8 * (pc % (D / 8));
     const int idx = 32 * k + j;
@@ -225,9 +247,21 @@ struct Stage {
   uint32_t meta;           // this thread's key row (threads 0..31): position | flag << 31
 };
 
-template <int D, int NQ>
+// FP8 staging: each thread moves 16-byte pieces of the code part (keys then
+// values) and threads 0..15 one 16-byte piece of the scales.
+template <int D>
+struct StageF8 {
+  static constexpr int kPieces = (D * 64) / 16;              // code pieces per tile
+  static constexpr int kPer = (kPieces + kThreads - 1) / kThreads;
+  u32x4 cx[kPer];
+  u32x4 sx;                // scales: [G][key scales (8) | value scales (8)]
+  uint32_t meta;
+};
+
+template <int D, int NQ, bool FP8>
 __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
   __shared__ __attribute__((aligned(16))) char tile_lds[2][D * 128];
+  __shared__ __attribute__((aligned(16))) float scale_lds[2][64];   // FP8: tile scales
   __shared__ uint32_t meta_lds[2][32];
   __shared__ int masked_lds[2];   // tile has a key hidden from some query of the block
   if (load_status(a.status) != 0) return;
@@ -255,8 +289,9 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
   const int nc = (L0 + 31) >> 5;
   const int np = (n_pre + 31) >> 5;
   const int nb = (t1 - p0 - band_c0 + 31) >> 5;
-  const char* pre_tiles = a.tiles + ws_tile(a, 1, h, i, 0) * (D * 128);
-  const char* band_tiles = a.tiles + ws_tile(a, 0, h, i, band_c0 >> 5) * (D * 128);
+  constexpr size_t kTB = FP8 ? static_cast<size_t>(D) * 64 + 256 : static_cast<size_t>(D) * 128;
+  const char* pre_tiles = a.tiles + ws_tile(a, 1, h, i, 0) * kTB;
+  const char* band_tiles = a.tiles + ws_tile(a, 0, h, i, band_c0 >> 5) * kTB;
   const int ntiles = nc + np + nb;
   const int32_t* pt = a.page_table + static_cast<size_t>(sh) * a.maxp;
   const int32_t* smeta = a.slot_meta + static_cast<size_t>(sh) * a.max_slots;
@@ -289,14 +324,14 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
   }
 
   // ---- staging: global -> registers (A), registers -> LDS (B)
-  Stage<D> stg;
-  constexpr int KP = Stage<D>::kPieces / 2;
+  using StageT = typename std::conditional<FP8, StageF8<D>, Stage<D>>::type;
+  StageT stg;
   auto stage_load = [&](int k) {
     const char* tile;
     if (k < nc) {
       const int sb = k * 32;
       tile = a.pool + static_cast<size_t>(pt[sb >> a.log2P]) * a.page_bytes +
-             static_cast<size_t>((sb & (a.P - 1)) >> 5) * (D * 128);
+             static_cast<size_t>((sb & (a.P - 1)) >> 5) * kTB;
       if (tid < 32) {
         uint32_t mt = sb + tid < L0 ? static_cast<uint32_t>(smeta[sb + tid]) : kNoKey;
         if (a.immediate && mt != kNoKey) {
@@ -311,14 +346,14 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
       }
     } else if (k < nc + np) {
       const int kk = k - nc;
-      tile = pre_tiles + static_cast<size_t>(kk) * (D * 128);
+      tile = pre_tiles + static_cast<size_t>(kk) * kTB;
       if (tid < 32) {
         const int idx = kk * 32 + tid;
         stg.meta = idx < n_pre ? static_cast<uint32_t>(p0 + lst[idx]) : kNoKey;
       }
     } else {
       const int kb = k - nc - np;
-      tile = band_tiles + static_cast<size_t>(kb) * (D * 128);
+      tile = band_tiles + static_cast<size_t>(kb) * kTB;
       if (tid < 32) {
         const int c = band_c0 + kb * 32 + tid;
         stg.meta = c < t1 - p0 ? (static_cast<uint32_t>(p0 + c) |
@@ -326,10 +361,20 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
                                : kNoKey;
       }
     }
+    if constexpr (FP8) {
 #pragma unroll
-    for (int m = 0; m < KP; ++m) {
-      stg.kx[m] = *reinterpret_cast<const u32x4*>(tile + k_src(tid + m * kThreads));
-      stg.vx[m] = *reinterpret_cast<const u32x4*>(tile + v_src<D>(tid + m * kThreads));
+      for (int m = 0; m < StageF8<D>::kPer; ++m) {
+        const int Q = tid + m * kThreads;
+        if (Q < StageF8<D>::kPieces) stg.cx[m] = *reinterpret_cast<const u32x4*>(tile + Q * 16);
+      }
+      if (tid < 16) stg.sx = *reinterpret_cast<const u32x4*>(tile + D * 64 + tid * 16);
+    } else {
+      constexpr int KP = Stage<D>::kPieces / 2;
+#pragma unroll
+      for (int m = 0; m < KP; ++m) {
+        stg.kx[m] = *reinterpret_cast<const u32x4*>(tile + k_src(tid + m * kThreads));
+        stg.vx[m] = *reinterpret_cast<const u32x4*>(tile + v_src<D>(tid + m * kThreads));
+      }
     }
   };
   auto stage_store = [&](int k, int buf) {
@@ -337,19 +382,70 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
     // pool slots past L hold stale data: their value elements are zeroed
     // (workspace tiles are zero past their last row)
     const int valid = k < nc ? min(32, L0 - k * 32) : 32;
+    if constexpr (FP8) {
+      // a 16-byte code piece becomes two bf16 LDS slots (exact conversion);
+      // the FP8 tile order matches the LDS fragment order (dms_fp8.h)
 #pragma unroll
-    for (int m = 0; m < KP; ++m) {
-      const int P = tid + m * kThreads;
-      *reinterpret_cast<u32x4*>(dst + P * 16) = stg.kx[m];
-      u32x4 x = stg.vx[m];
-      // element i of the value piece is key row 8 G + i
-      const int j0 = 8 * ((P >> 4) & 3);
-      if (j0 + 8 > valid) {
+      for (int m = 0; m < StageF8<D>::kPer; ++m) {
+        const int Q = tid + m * kThreads;
+        if (Q < StageF8<D>::kPieces) {
+          u32x4 x = stg.cx[m];
+          int P0, step;
+          if (Q < 2 * D) {            // keys: piece (p, h, lane L)
+            P0 = 256 * (Q >> 7) + (Q & 127);
+            step = 128;
+          } else {                    // values: piece (p, lane L), slots 8G .. 8G+7
+            const int Qv = Q - 2 * D;
+            P0 = D * 4 + 128 * (Qv >> 6) + (Qv & 63);
+            step = 64;
+            const int nv = valid - 8 * ((Qv >> 4) & 3);
+            if (nv < 8) {
+              const uint64_t keep8 = nv <= 0 ? 0ull : (~0ull >> (8 * (8 - nv)));
+              const uint32_t klo = static_cast<uint32_t>(keep8), khi = static_cast<uint32_t>(keep8 >> 32);
+              x[0] &= klo;
+              x[1] &= khi;
+              x[2] &= klo;
+              x[3] &= khi;
+            }
+          }
+          u32x4 lo, hi;
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (j0 + e >= valid) x[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+          for (int w2 = 0; w2 < 2; ++w2) {
+            lo[2 * w2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[w2], 1.0f, false));
+            lo[2 * w2 + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[w2], 1.0f, true));
+            hi[2 * w2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[2 + w2], 1.0f, false));
+            hi[2 * w2 + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[2 + w2], 1.0f, true));
+          }
+          *reinterpret_cast<u32x4*>(dst + P0 * 16) = lo;
+          *reinterpret_cast<u32x4*>(dst + (P0 + step) * 16) = hi;
+        }
       }
-      *reinterpret_cast<u32x4*>(dst + D * 64 + P * 16) = x;
+      if (tid < 16) {
+        // scale piece tid: group G = tid / 4, key (tid % 4 < 2) or value scales of
+        // slots 8 G + 4 (tid % 2) .. + 3; missing slots get 0
+        u32x4 x = stg.sx;
+        const int j0 = 8 * (tid >> 2) + 4 * (tid & 1);
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          if (j0 + c >= valid) x[c] = 0u;
+        *reinterpret_cast<u32x4*>(&scale_lds[buf][4 * tid]) = x;
+      }
+    } else {
+      constexpr int KP = Stage<D>::kPieces / 2;
+#pragma unroll
+      for (int m = 0; m < KP; ++m) {
+        const int P = tid + m * kThreads;
+        *reinterpret_cast<u32x4*>(dst + P * 16) = stg.kx[m];
+        u32x4 x = stg.vx[m];
+        // element i of the value piece is key row 8 G + i
+        const int j0 = 8 * ((P >> 4) & 3);
+        if (j0 + 8 > valid) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (j0 + e >= valid) x[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+        }
+        *reinterpret_cast<u32x4*>(dst + D * 64 + P * 16) = x;
+      }
     }
     if (tid < 64) {
       // a key row needs the per-element mask iff some query t in [t0, t1)
@@ -399,6 +495,20 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
     }
 #pragma unroll
     for (int b = 0; b < D / 16; ++b) f.vt[b] = *reinterpret_cast<const u32x4*>(tl + lo_v + b * 1024);
+    float ksc[8], vsc[8];   // FP8: key and value scales of rows 8G .. 8G+7
+    if constexpr (FP8) {
+      const f32x4 k0 = *reinterpret_cast<const f32x4*>(&scale_lds[buf][16 * G]);
+      const f32x4 k1 = *reinterpret_cast<const f32x4*>(&scale_lds[buf][16 * G + 4]);
+      const f32x4 v0 = *reinterpret_cast<const f32x4*>(&scale_lds[buf][16 * G + 8]);
+      const f32x4 v1 = *reinterpret_cast<const f32x4*>(&scale_lds[buf][16 * G + 12]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        ksc[j] = k0[j];
+        ksc[j + 4] = k1[j];
+        vsc[j] = v0[j];
+        vsc[j + 4] = v1[j];
+      }
+    }
     const bool masked = __builtin_amdgcn_readfirstlane(masked_lds[buf]) != 0;
     int kp[8], kx[8];   // key position and expiry (first query that no longer sees it)
     if (masked) {
@@ -422,6 +532,10 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
       for (int j = 0; j < 4; ++j) {
         sc[j] = s0[j];
         sc[j + 4] = s1[j];
+      }
+      if constexpr (FP8) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) sc[j] *= ksc[j];   // exact: a power of two
       }
       if (masked) {
         const int t = tcol[qb];
@@ -456,6 +570,12 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
         const bf16x2 pb = __builtin_convertvector(pr, bf16x2);
         pu[j] = __builtin_bit_cast(uint32_t, pb);
         l_run[qb] = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, l_run[qb], false);
+        if constexpr (FP8) {
+          // PV weights carry the value scale: rounding commutes with a
+          // power-of-two factor, so these are the rounded weights times it
+          const f32x2 pv = {e[2 * j] * vsc[2 * j], e[2 * j + 1] * vsc[2 * j + 1]};
+          pu[j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pv, bf16x2));
+        }
       }
 #pragma unroll
       for (int b = 0; b < D / 16; ++b) o[qb][b] = mfma_bf16(f.vt[b], pu, o[qb][b]);
@@ -483,7 +603,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
 
 constexpr int kNQ = 2;
 
-template <int D>
+template <int D, bool FP8>
 hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
                             int layer, int n, const int32_t* seq_ids, const int32_t* cu,
                             int total_tokens, int max_len, const void* q, const void* k,
@@ -532,12 +652,12 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   hipLaunchKernelGGL(prefill_list_kernel, dim3(NH), dim3(kThreads), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(prefill_tile_kernel<D>, dim3((max_len + 31) / 32, NH, 2), dim3(kThreads), 0,
+  hipLaunchKernelGGL((prefill_tile_kernel<D, FP8>), dim3((max_len + 31) / 32, NH, 2), dim3(kThreads), 0,
                      st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 grid((max_len + a.PB - 1) / a.PB, NH);
-  hipLaunchKernelGGL((prefill_kernel<D, kNQ>), grid, dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((prefill_kernel<D, kNQ, FP8>), grid, dim3(kThreads), 0, st, a);
   e = hipGetLastError();
   if (ev_stop) (void)hipEventRecord(ev_stop, st);
   return e;
@@ -561,11 +681,16 @@ hipError_t launch_prefill_attention(const dms_config& c, const Layout& lo, void*
                                     const void* q, const void* k, const void* v,
                                     const uint8_t* flags, float* out, hipStream_t st,
                                     hipEvent_t ev_start, hipEvent_t ev_stop) {
+  const bool fp8 = c.kv_format == DMS_KV_FP8;
   if (c.head_dim == 128)
-    return launch_prefill_d<128>(c, lo, meta, ws, pool, layer, n, seq_ids, cu, total_tokens,
-                                 max_len, q, k, v, flags, out, st, ev_start, ev_stop);
-  return launch_prefill_d<64>(c, lo, meta, ws, pool, layer, n, seq_ids, cu, total_tokens, max_len,
-                              q, k, v, flags, out, st, ev_start, ev_stop);
+    return fp8 ? launch_prefill_d<128, true>(c, lo, meta, ws, pool, layer, n, seq_ids, cu, total_tokens,
+                                             max_len, q, k, v, flags, out, st, ev_start, ev_stop)
+               : launch_prefill_d<128, false>(c, lo, meta, ws, pool, layer, n, seq_ids, cu, total_tokens,
+                                              max_len, q, k, v, flags, out, st, ev_start, ev_stop);
+  return fp8 ? launch_prefill_d<64, true>(c, lo, meta, ws, pool, layer, n, seq_ids, cu, total_tokens,
+                                          max_len, q, k, v, flags, out, st, ev_start, ev_stop)
+             : launch_prefill_d<64, false>(c, lo, meta, ws, pool, layer, n, seq_ids, cu, total_tokens,
+                                           max_len, q, k, v, flags, out, st, ev_start, ev_stop);
 }
 
 }  // namespace dms

@@ -89,3 +89,25 @@ def compare_pool(cache, layer, view, seqs, inputs_by_seq):
                 owner = view.slot_pos[s, h, slot]
                 assert np.array_equal(kk[slot % P], inp.k[owner, h]), (s, h, slot)
                 assert np.array_equal(vv[slot % P], inp.v[owner, h]), (s, h, slot)
+
+
+def compare_pool_fp8(cache, orc, seqs, layer=0):
+    """FP8 pages: codes and scales of every live slot equal the oracle's
+    quantization of the row its owner appended (bit-exact)."""
+    view = cache.export(layer)
+    c = cache.cfg
+    P = c.page_size
+    pages = {}
+    for s in seqs:
+        for h in range(c.num_kv_heads):
+            L = int(view.L[s, h])
+            for slot in range(L):
+                pg = int(view.page_table[s, h, slot // P])
+                if pg not in pages:
+                    pages[pg] = cache.pool_page_kv(layer, pg)
+                kc, vc, ks, vs = pages[pg]
+                row = slot % P
+                assert np.array_equal(kc[row], orc.k_codes[s, h, slot]), (s, h, slot)
+                assert np.array_equal(vc[row], orc.v_codes[s, h, slot]), (s, h, slot)
+                assert ks[row] == 2.0 ** orc.k_exp[s, h, slot], (s, h, slot)
+                assert vs[row] == 2.0 ** orc.v_exp[s, h, slot], (s, h, slot)

@@ -6,7 +6,7 @@ rows."""
 import numpy as np
 import pytest
 
-from dms_testlib import ATOL, SeqInputs, bf16_to_f32, compare_state, to_dev
+from dms_testlib import ATOL, SeqInputs, bf16_to_f32, compare_pool_fp8, compare_state, to_dev
 from oracle import PagedKVOracle, dense_dms_attention, fake_quantize_fp8
 
 pytestmark = pytest.mark.gpu
@@ -30,25 +30,7 @@ def _mk(**kw):
 
 
 def _compare_pool_fp8(cache, orc, seqs, layer=0):
-    """Codes and scales of every live slot equal the oracle's quantization of
-    the row its owner appended."""
-    view = cache.export(layer)
-    c = cache.cfg
-    P = c.page_size
-    pages = {}
-    for s in seqs:
-        for h in range(c.num_kv_heads):
-            L = int(view.L[s, h])
-            for slot in range(L):
-                pg = int(view.page_table[s, h, slot // P])
-                if pg not in pages:
-                    pages[pg] = cache.pool_page_kv(layer, pg)
-                kc, vc, ks, vs = pages[pg]
-                row = slot % P
-                assert np.array_equal(kc[row], orc.k_codes[s, h, slot]), (s, h, slot)
-                assert np.array_equal(vc[row], orc.v_codes[s, h, slot]), (s, h, slot)
-                assert ks[row] == 2.0 ** orc.k_exp[s, h, slot], (s, h, slot)
-                assert vs[row] == 2.0 ** orc.v_exp[s, h, slot], (s, h, slot)
+    compare_pool_fp8(cache, orc, seqs, layer)
 
 
 def _append_chunks(dms, cache, orc, seqs, inputs, start, stop, chunk):

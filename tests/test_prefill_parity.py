@@ -5,25 +5,36 @@ for several group sizes, head sizes, windows, eviction rates and chunkings."""
 import numpy as np
 import pytest
 
-from dms_testlib import ATOL, SeqInputs, bf16_to_f32, compare_pool, compare_state, to_dev
-from oracle import PagedKVOracle, dense_dms_attention
+from dms_testlib import (ATOL, SeqInputs, bf16_to_f32, compare_pool, compare_pool_fp8, compare_state,
+                         to_dev)
+from oracle import PagedKVOracle, dense_dms_attention, fake_quantize_fp8
 
 pytestmark = pytest.mark.gpu
 
 
-def _run(cfg_kw, seqs, lens, chunks, seed, p, q_scale=1.0, override=None):
+def _run(cfg_kw, seqs, lens, chunks, seed, p, q_scale=1.0, override=None, fp8=False):
     """Prefill every sequence to lens[s] tokens in calls of chunks[c] tokens
-    per sequence; check each call's outputs and the state after it."""
+    per sequence; check each call's outputs and the state after it.  With
+    fp8 the pages are E4M3 and every key and value (cached or in the chunk)
+    is attended in its quantized form; pools and workspace start as NaN
+    bytes."""
     import torch
     from paper_2506_05345_amd import dms
-    cfg = dms.make_config(**cfg_kw)
+    cfg = dms.make_config(kv_format=dms.DMS_KV_FP8 if fp8 else dms.DMS_KV_BF16, **cfg_kw)
     cache = dms.DmsCache(cfg)
+    if fp8:
+        for pl in cache.pools:
+            pl.fill_(0xFF)
+        cache.workspace.fill_(0xFF)
+        dms.dms_init_state(cache.ctx)
+        torch.cuda.synchronize()
+    kvq = fake_quantize_fp8 if fp8 else (lambda x: x)
     H, g, D, w = cfg.num_kv_heads, cfg.group_size, cfg.head_dim, cfg.window
     inp = {s: SeqInputs(seed, 0, s, lens[s], H, g, D, p, q_scale=q_scale) for s in seqs}
     if override:
         override(inp)
     orc = PagedKVOracle(cfg.max_seqs, H, w, cfg.page_size, cfg.num_pages,
-                        cfg.max_pages_per_head, D)
+                        cfg.max_pages_per_head, D, kv_format="fp8" if fp8 else "bf16")
     cur = {s: 0 for s in seqs}
     worst = 0.0
     ci = 0
@@ -48,8 +59,8 @@ def _run(cfg_kw, seqs, lens, chunks, seed, p, q_scale=1.0, override=None):
             if l == 0:
                 continue
             tq = np.arange(cur[s], cur[s] + l)
-            ref = dense_dms_attention(bf16_to_f32(inp[s].q[tq]), bf16_to_f32(inp[s].k[:tq[-1] + 1]),
-                                      bf16_to_f32(inp[s].v[:tq[-1] + 1]), inp[s].flags[:tq[-1] + 1],
+            ref = dense_dms_attention(bf16_to_f32(inp[s].q[tq]), kvq(bf16_to_f32(inp[s].k[:tq[-1] + 1])),
+                                      kvq(bf16_to_f32(inp[s].v[:tq[-1] + 1])), inp[s].flags[:tq[-1] + 1],
                                       w, g, t_query=tq)
             err = np.abs(got[cu[i]:cu[i + 1]] - ref).max()
             worst = max(worst, err)
@@ -60,7 +71,10 @@ def _run(cfg_kw, seqs, lens, chunks, seed, p, q_scale=1.0, override=None):
         for s, l in zip(seqs, ls):
             cur[s] += l
         compare_state(cache.export(0), orc, seqs)
-    compare_pool(cache, 0, cache.export(0), seqs, inp)
+    if fp8:
+        compare_pool_fp8(cache, orc, seqs)
+    else:
+        compare_pool(cache, 0, cache.export(0), seqs, inp)
     cache.close()
     return worst
 
@@ -146,3 +160,24 @@ def test_prefill_then_decode_matches_decode_only_path():
         torch.cuda.synchronize()
         assert torch.equal(outs[0], outs[1])
     cache.close()
+
+
+@pytest.mark.parametrize("d,g,w,P,p,chunks", [
+    (128, 5, 256, 64, 0.875, [400, 77]), (64, 2, 16, 32, 0.5, [37]), (128, 16, 33, 256, 0.75, [200, 1, 311]),
+    (64, 7, 1, 128, 0.9, [400])])
+def test_ragged_prefill_fp8(d, g, w, P, p, chunks):
+    """FP8 pages: cached keys come from E4M3 pages (ragged last tiles over NaN
+    bytes), in-chunk keys from E4M3 workspace tiles; codes of the committed
+    slots bit-exact."""
+    H = 2
+    seqs = [2, 0, 3]
+    lens = {2: 900, 0: 130, 3: 611}
+    _run(dict(num_layers=1, max_seqs=4, num_kv_heads=H, group_size=g, head_dim=d, window=w,
+              page_size=P, num_pages=300, max_pages_per_head=64, max_chunk_tokens=3 * 400),
+         seqs, lens, chunks, 33, p, fp8=True)
+
+
+def test_prefill_fp8_peaked():
+    _run(dict(num_layers=1, max_seqs=1, num_kv_heads=2, group_size=5, head_dim=128, window=64,
+              page_size=64, num_pages=64, max_pages_per_head=16, max_chunk_tokens=512),
+         [0], {0: 600}, [300], 43, 0.875, q_scale=8.0, fp8=True)
