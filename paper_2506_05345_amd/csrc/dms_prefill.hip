@@ -254,6 +254,7 @@ struct StageF8 {
   static constexpr int kPieces = (D * 64) / 16;              // code pieces per tile
   static constexpr int kPer = (kPieces + kThreads - 1) / kThreads;
   u32x4 cx[kPer];
+  float ks[kPer];          // key scale of the token a key piece belongs to
   u32x4 sx;                // scales: [G][key scales (8) | value scales (8)]
   uint32_t meta;
 };
@@ -366,6 +367,11 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
       for (int m = 0; m < StageF8<D>::kPer; ++m) {
         const int Q = tid + m * kThreads;
         if (Q < StageF8<D>::kPieces) stg.cx[m] = *reinterpret_cast<const u32x4*>(tile + Q * 16);
+        if (Q < 2 * D) {
+          // key piece (p, h, lane L): all 16 codes belong to slot 8 (r/4) + r%4 + 4 h
+          const int r = Q & 15, j = 8 * (r >> 2) + (r & 3) + 4 * ((Q >> 6) & 1);
+          stg.ks[m] = *reinterpret_cast<const float*>(tile + D * 64 + (j >> 3) * 64 + (j & 7) * 4);
+        }
       }
       if (tid < 16) stg.sx = *reinterpret_cast<const u32x4*>(tile + D * 64 + tid * 16);
     } else {
@@ -391,9 +397,11 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
         if (Q < StageF8<D>::kPieces) {
           u32x4 x = stg.cx[m];
           int P0, step;
-          if (Q < 2 * D) {            // keys: piece (p, h, lane L)
+          float scale = 1.0f;
+          if (Q < 2 * D) {            // keys: piece (p, h, lane L), dequantized exactly
             P0 = 256 * (Q >> 7) + (Q & 127);
             step = 128;
+            scale = stg.ks[m];
           } else {                    // values: piece (p, lane L), slots 8G .. 8G+7
             const int Qv = Q - 2 * D;
             P0 = D * 4 + 128 * (Qv >> 6) + (Qv & 63);
@@ -411,10 +419,10 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
           u32x4 lo, hi;
 #pragma unroll
           for (int w2 = 0; w2 < 2; ++w2) {
-            lo[2 * w2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[w2], 1.0f, false));
-            lo[2 * w2 + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[w2], 1.0f, true));
-            hi[2 * w2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[2 + w2], 1.0f, false));
-            hi[2 * w2 + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[2 + w2], 1.0f, true));
+            lo[2 * w2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[w2], scale, false));
+            lo[2 * w2 + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[w2], scale, true));
+            hi[2 * w2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[2 + w2], scale, false));
+            hi[2 * w2 + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[2 + w2], scale, true));
           }
           *reinterpret_cast<u32x4*>(dst + P0 * 16) = lo;
           *reinterpret_cast<u32x4*>(dst + (P0 + step) * 16) = hi;
@@ -495,16 +503,12 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
     }
 #pragma unroll
     for (int b = 0; b < D / 16; ++b) f.vt[b] = *reinterpret_cast<const u32x4*>(tl + lo_v + b * 1024);
-    float ksc[8], vsc[8];   // FP8: key and value scales of rows 8G .. 8G+7
+    float vsc[8];   // FP8: value scales of rows 8G .. 8G+7 (keys are staged dequantized)
     if constexpr (FP8) {
-      const f32x4 k0 = *reinterpret_cast<const f32x4*>(&scale_lds[buf][16 * G]);
-      const f32x4 k1 = *reinterpret_cast<const f32x4*>(&scale_lds[buf][16 * G + 4]);
       const f32x4 v0 = *reinterpret_cast<const f32x4*>(&scale_lds[buf][16 * G + 8]);
       const f32x4 v1 = *reinterpret_cast<const f32x4*>(&scale_lds[buf][16 * G + 12]);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        ksc[j] = k0[j];
-        ksc[j + 4] = k1[j];
         vsc[j] = v0[j];
         vsc[j + 4] = v1[j];
       }
@@ -532,10 +536,6 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
       for (int j = 0; j < 4; ++j) {
         sc[j] = s0[j];
         sc[j + 4] = s1[j];
-      }
-      if constexpr (FP8) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) sc[j] *= ksc[j];   // exact: a power of two
       }
       if (masked) {
         const int t = tcol[qb];
