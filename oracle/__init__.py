@@ -8,3 +8,4 @@ from .dms_oracle import *  # noqa: F401,F403
 from .latency_model import *  # noqa: F401,F403
 from .train_oracle import *  # noqa: F401,F403
 from .kv_fp8 import *  # noqa: F401,F403
+from .quest import *  # noqa: F401,F403
