@@ -96,6 +96,9 @@ typedef struct dms_config {
                                  -5 is the paper's training offset */
   int32_t kv_format;          /* DMS_KV_BF16 (0) or DMS_KV_FP8 (1): how retained
                                  K / V rows are stored in the page pools */
+  int32_t quest_page_budget;  /* 0: decode attends every retained slot; B > 0:
+                                 decode attends the B pages of each head that
+                                 Quest's bound ranks highest (see below) */
 } dms_config;
 
 /*
@@ -137,6 +140,22 @@ enum { DMS_EVICT_DELAYED = 0, DMS_EVICT_IMMEDIATE = 1 };
  *     appends and the chunk's own tokens in a prefill call.
  */
 enum { DMS_KV_BF16 = 0, DMS_KV_FP8 = 1 };
+
+/*
+ * Page retrieval within the retained set (dms_config.quest_page_budget).  The
+ * paper names Quest (query-aware page selection) as orthogonal to DMS and
+ * combinable with it (App. A).  With a budget B > 0 the library keeps, for
+ * every cache page, the channel-wise minimum and maximum of the keys in its
+ * live slots (exact, recomputed for every page an append writes; bf16; keys
+ * as stored, i.e. dequantized for FP8 pages).  Each decode call then scores
+ * the pages of a KV head with Quest's bound U = sum_i max(q_i lo_i, q_i hi_i),
+ * taking the maximum over the group's query heads (one selection per KV head,
+ * shared by its group), keeps the B highest (ties: lower page index; every
+ * page when a head has at most B) and attends only their live slots.  Scores
+ * are float32 sums in dimension order.  Prefill attends densely.
+ * dms_quest_selection reports the last decode call's selection.  Requires
+ * max_pages_per_head <= 4096.
+ */
 enum { DMS_DECIDE_CALLER = 0, DMS_DECIDE_QUERY = 1 };
 
 typedef struct dms_ctx dms_ctx;
@@ -163,6 +182,9 @@ typedef struct dms_ctx dms_ctx;
 typedef struct dms_state_offsets {
   size_t status, layer0, layer_stride;
   size_t pos, len, ring, page_table, slot_meta, stack, top;
+  size_t page_bounds;   /* quest_page_budget > 0: bf16 [num_pages][2][d], per
+                           page (by page id) the channel-wise min then max of
+                           the keys in its live slots; 0 otherwise */
 } dms_state_offsets;
 
 /*
@@ -287,6 +309,16 @@ int dms_prefill_chunk_q(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_d
  * per-step "KV-cache token reads", Sec. 5.1): out_dev int32 [n, Hkv]. */
 int dms_retained_lengths(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
                          int32_t* out_dev, void* stream);
+
+/* Page retrieval (quest_page_budget > 0): the selection of the last decode
+ * call on this context, stream-ordered after it.  For its i-th (sequence,
+ * KV head) pair in call order (n pairs of Hkv heads): pages_out_dev[i * B ..]
+ * (int32, B = quest_page_budget) holds the attended page-table indices in
+ * ascending order, and count_out_dev[i] how many (the rest are -1).  Returns
+ * DMS_ERR_INVALID for a context without a budget or n outside 1 .. max_seqs
+ * (pass the n of that decode call). */
+int dms_quest_selection(dms_ctx* ctx, int n, int32_t* pages_out_dev, int32_t* count_out_dev,
+                        void* stream);
 
 /* Copy one layer's state region (dms_state_offsets) plus nothing else into
  * host memory: bytes must be >= layer_stride.  Synchronises `stream`. */

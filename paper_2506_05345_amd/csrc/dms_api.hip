@@ -28,6 +28,8 @@ int validate_config(const dms_config& c) {
     return DMS_ERR_INVALID;
   if (c.decision_source == DMS_DECIDE_QUERY && !isfinite(c.decision_bias)) return DMS_ERR_INVALID;
   if (c.kv_format != DMS_KV_BF16 && c.kv_format != DMS_KV_FP8) return DMS_ERR_INVALID;
+  if (c.quest_page_budget < 0 || c.quest_page_budget > c.max_pages_per_head) return DMS_ERR_INVALID;
+  if (c.quest_page_budget > 0 && c.max_pages_per_head > 4096) return DMS_ERR_UNSUPPORTED;
   // slot and page indices are int32 on the device
   if (static_cast<int64_t>(c.max_pages_per_head) * c.page_size >= (int64_t(1) << 31)) return DMS_ERR_INVALID;
   if (static_cast<int64_t>(c.max_seqs) * c.num_kv_heads > (int64_t(1) << 22)) return DMS_ERR_INVALID;
@@ -54,6 +56,7 @@ Layout make_layout(const dms_config& c) {
   lo.slot_meta = take(S * H * maxp * P * 4);
   lo.stack = take(static_cast<size_t>(c.num_pages) * 4);
   lo.top = take(4);
+  lo.page_bounds = c.quest_page_budget > 0 ? take(static_cast<size_t>(c.num_pages) * 2 * D * 2) : 0;
   lo.layer_stride = off;
   lo.meta_bytes = lo.layer0 + lo.layer_stride * c.num_layers;
   // pool
@@ -84,6 +87,8 @@ Layout make_layout(const dms_config& c) {
   lo.pf_tiles_per_head = static_cast<int>((static_cast<size_t>(c.max_chunk_tokens) + 31) / 32 + S + 1);
   lo.ws_pf_tiles = take(2 * H * static_cast<size_t>(lo.pf_tiles_per_head) * D * 128);
   lo.ws_pf_flags = take(static_cast<size_t>(c.max_chunk_tokens) * H);  // decisions from q
+  lo.ws_q_sel = take(NH * static_cast<size_t>(c.quest_page_budget) * 4);
+  lo.ws_q_len = take(NH * 4);
   lo.workspace_bytes = off;
   return lo;
 }
@@ -143,6 +148,14 @@ int check_chunk(const dms_ctx* ctx, const int32_t* cu, int total, int max_len) {
   return DMS_OK;
 }
 
+// Page retrieval buffers in the workspace.
+const int32_t* quest_lengths(const Ctx& c) {
+  return reinterpret_cast<const int32_t*>(static_cast<char*>(c.ws) + c.lo.ws_q_len);
+}
+const int32_t* quest_pages(const Ctx& c) {
+  return reinterpret_cast<const int32_t*>(static_cast<char*>(c.ws) + c.lo.ws_q_sel);
+}
+
 int ensure_waves(dms_ctx* ctx) {
   if (ctx->c.decode_waves > 0) return DMS_OK;
   int w = dms::decode_resident_waves(ctx->c.cfg);
@@ -183,6 +196,7 @@ int dms_state_layout(const dms_config* cfg, dms_state_offsets* out) {
   out->slot_meta = lo.slot_meta;
   out->stack = lo.stack;
   out->top = lo.top;
+  out->page_bounds = lo.page_bounds;
   return DMS_OK;
 }
 
@@ -239,6 +253,9 @@ int dms_append(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const
                                   nullptr, nullptr, true, 0, nullptr, st);
   if (e == hipSuccess)
     e = dms::launch_scatter(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, k_dev, v_dev, st);
+  if (e == hipSuccess && c.cfg.quest_page_budget > 0)
+    e = dms::launch_quest_bounds(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, false,
+                                 seq_ids_dev, st);
   return hip_rc(e);
 }
 
@@ -250,13 +267,17 @@ int dms_decode(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const
   if ((rc = ensure_waves(ctx))) return rc;
   const Ctx& c = ctx->c;
   hipStream_t st = as_stream(stream);
-  hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, nullptr,
-                                  nullptr, nullptr, false, c.decode_waves, out_dev, st);
+  const bool quest = c.cfg.quest_page_budget > 0;
+  hipError_t e = hipSuccess;
+  if (quest) e = dms::launch_quest_select(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, q_dev, st);
+  if (e == hipSuccess)
+    e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, nullptr, nullptr, nullptr,
+                         false, c.decode_waves, out_dev, st, quest ? quest_lengths(c) : nullptr);
   hipEvent_t e0, e1;
   next_events(ctx->c, DMS_PROFILE_DECODE, &e0, &e1);
   if (e == hipSuccess)
     e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, nullptr,
-                           nullptr, out_dev, c.decode_waves, st, e0, e1);
+                           nullptr, out_dev, c.decode_waves, st, e0, e1, quest ? quest_pages(c) : nullptr);
   return hip_rc(e);
 }
 
@@ -270,6 +291,29 @@ int decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, cons
   const bool from_q = ctx->c.cfg.decision_source == DMS_DECIDE_QUERY;
   const Ctx& c = ctx->c;
   hipStream_t st = as_stream(stream);
+  if (c.cfg.quest_page_budget > 0) {
+    // page retrieval: append (plan, K / V write, bounds of the written
+    // pages), select pages, then plan and decode over the selection
+    hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev,
+                                    from_q ? nullptr : flags_dev, from_q ? q_dev : nullptr,
+                                    decisions_out_dev, true, 0, nullptr, st);
+    if (e == hipSuccess)
+      e = dms::launch_scatter(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, k_dev, v_dev, st);
+    if (e == hipSuccess)
+      e = dms::launch_quest_bounds(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, false,
+                                   seq_ids_dev, st);
+    if (e == hipSuccess)
+      e = dms::launch_quest_select(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, q_dev, st);
+    if (e == hipSuccess)
+      e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, nullptr, nullptr, nullptr,
+                           false, c.decode_waves, out_dev, st, quest_lengths(c));
+    hipEvent_t e0, e1;
+    next_events(ctx->c, DMS_PROFILE_DECODE, &e0, &e1);
+    if (e == hipSuccess)
+      e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, nullptr,
+                             nullptr, out_dev, c.decode_waves, st, e0, e1, quest_pages(c));
+    return hip_rc(e);
+  }
   // planner (slot choice, page pops, state, wave ranges) -> decode, which
   // also writes the new K / V into their slots and merges split heads
   hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev,
@@ -310,6 +354,9 @@ int prefill_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
   if (e == hipSuccess)
     e = dms::launch_chunk_commit(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, seq_ids_dev,
                                  cu_seqlens_dev, total_tokens, max_seqlen, k_dev, v_dev, flags, st);
+  if (e == hipSuccess && c.cfg.quest_page_budget > 0)
+    e = dms::launch_quest_bounds(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, true,
+                                 seq_ids_dev, st);
   return hip_rc(e);
 }
 
@@ -349,9 +396,24 @@ int dms_append_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
   if (total_tokens == 0) return DMS_OK;
   if (!k_dev || !v_dev || !flags_dev) return DMS_ERR_INVALID;
   const Ctx& c = ctx->c;
-  return hip_rc(dms::launch_chunk_commit(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n,
-                                         seq_ids_dev, cu_seqlens_dev, total_tokens, max_seqlen,
-                                         k_dev, v_dev, flags_dev, as_stream(stream)));
+  hipStream_t st = as_stream(stream);
+  hipError_t e = dms::launch_chunk_commit(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n,
+                                          seq_ids_dev, cu_seqlens_dev, total_tokens, max_seqlen,
+                                          k_dev, v_dev, flags_dev, st);
+  // page retrieval: a chunk may write into any page of a head (reused slots)
+  if (e == hipSuccess && c.cfg.quest_page_budget > 0)
+    e = dms::launch_quest_bounds(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, true,
+                                 seq_ids_dev, st);
+  return hip_rc(e);
+}
+
+int dms_quest_selection(dms_ctx* ctx, int n, int32_t* pages_out_dev, int32_t* count_out_dev,
+                        void* stream) {
+  if (!ctx || ctx->c.cfg.quest_page_budget <= 0) return DMS_ERR_INVALID;
+  if (n < 1 || n > ctx->c.cfg.max_seqs || !pages_out_dev || !count_out_dev) return DMS_ERR_INVALID;
+  const Ctx& c = ctx->c;
+  return hip_rc(dms::launch_quest_export(c.cfg, c.lo, c.ws, n, pages_out_dev, count_out_dev,
+                                         as_stream(stream)));
 }
 
 int dms_prefill_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,

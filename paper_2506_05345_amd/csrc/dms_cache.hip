@@ -162,6 +162,7 @@ struct PlanArgs {
   int4* wave_desc;       // [2W] first segment of every decode wave (see decode kernel)
   int4* head_waves;      // [n*H] first / last wave holding a tile of the head, live mask
   float* out;            // nullable: zeroed for heads with no retained token
+  const int32_t* len_override;   // nullable (no append): lengths to plan, per head of the call
   int n, H, w, P, maxp, max_slots, max_seqs, append, W, gD;
 };
 
@@ -300,7 +301,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(PlanArgs a) {
   int t = 0, slot = -1, fresh = 0, need = 0, Lnew = 0, cap = 0, f = 0;
   if (a.append && tid < min(NH, top0)) stack_lds[tid] = a.st.stack[top0 - 1 - tid];
   if (act) {
-    const int L = a.st.len[sh];
+    const int L = (!a.append && a.len_override != nullptr) ? a.len_override[tid] : a.st.len[sh];
     if (a.append) {
       f = decision(a, tid);
       t = a.st.pos[s];
@@ -419,7 +420,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
         Lnew = a.st.len[sh] + fresh;
       } else {
         sh = a.seq_ids[hh / a.H] * a.H + hh % a.H;
-        Lnew = a.st.len[sh];
+        Lnew = a.len_override != nullptr ? a.len_override[hh] : a.st.len[sh];
       }
       tiles = (Lnew + kTile - 1) / kTile;
     }
@@ -773,8 +774,10 @@ hipError_t launch_seq_reset(const dms_config& c, const Layout& lo, void* meta, i
 
 hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* ws, int layer,
                        int n, const int32_t* seq_ids, const uint8_t* flags, const void* q,
-                       uint8_t* flags_out, bool append, int waves, float* out, hipStream_t st) {
+                       uint8_t* flags_out, bool append, int waves, float* out, hipStream_t st,
+                       const int32_t* len_override) {
   PlanArgs a;
+  a.len_override = len_override;
   a.q = static_cast<const uint16_t*>(q);
   a.flags_out = flags_out;
   a.bias = c.decision_bias;

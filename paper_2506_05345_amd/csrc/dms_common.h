@@ -24,6 +24,7 @@ struct Layout {
   // meta
   size_t status, layer0, layer_stride;
   size_t pos, len, ring, page_table, slot_meta, stack, top;
+  size_t page_bounds;      // quest: bf16 [num_pages][2][D] per layer (0 when off)
   size_t meta_bytes;
   // pool of one layer
   size_t page_bytes, pool_bytes;
@@ -32,6 +33,7 @@ struct Layout {
   size_t ws_wave_bounds, ws_wave_desc, ws_head_waves, ws_head_cnt;
   size_t ws_ck_need, ws_ck_fresh, ws_ck_base, ws_ck_pos0, ws_ck_err, ws_ck_slot;
   size_t ws_pf_cum, ws_pf_meta, ws_pf_tiles, ws_pf_flags;
+  size_t ws_q_sel, ws_q_len;   // quest: selection [NH][B], attended lengths [NH]
   int pf_tiles_per_head;   // tiles of one (region, KV head) in ws_pf_tiles
   size_t workspace_bytes;
   int max_heads, max_partials, max_slots;
@@ -50,6 +52,7 @@ struct LayerState {
   int32_t* slot_meta;   // [S][Hkv][max_slots]
   int32_t* stack;       // [num_pages]
   int32_t* top;         // [1]
+  uint16_t* page_bounds;   // quest: [num_pages][2][D] bf16 (null when off)
 };
 
 inline LayerState layer_state(const Layout& lo, void* meta, int layer) {
@@ -58,6 +61,7 @@ inline LayerState layer_state(const Layout& lo, void* meta, int layer) {
   s.pos = reinterpret_cast<int32_t*>(b + lo.pos);
   s.len = reinterpret_cast<int32_t*>(b + lo.len);
   s.ring = reinterpret_cast<int32_t*>(b + lo.ring);
+  s.page_bounds = lo.page_bounds ? reinterpret_cast<uint16_t*>(b + lo.page_bounds) : nullptr;
   s.page_table = reinterpret_cast<int32_t*>(b + lo.page_table);
   s.slot_meta = reinterpret_cast<int32_t*>(b + lo.slot_meta);
   s.stack = reinterpret_cast<int32_t*>(b + lo.stack);
@@ -176,18 +180,35 @@ hipError_t launch_seq_reset(const dms_config& c, const Layout& lo, void* meta, i
 // `append`), per-head descriptors, tile prefix sums and, for `waves` > 0, the
 // tile range and first head of every decode wave.  `out` (nullable) gets zeros
 // for heads with no retained token.
+// `len_override` (nullable, planning without append only): per-head lengths
+// to plan instead of the retained lengths (page retrieval).
 hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* ws, int layer,
                        int n, const int32_t* seq_ids, const uint8_t* flags, const void* q,
-                       uint8_t* flags_out, bool append, int waves, float* out, hipStream_t st);
+                       uint8_t* flags_out, bool append, int waves, float* out, hipStream_t st,
+                       const int32_t* len_override = nullptr);
+// Page retrieval: recompute the bounds of the pages the last planned append
+// wrote (all_pages: every page of every head of the call), then select the
+// pages of each head for query q.
+hipError_t launch_quest_bounds(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                               void* pool, int layer, int n, bool all_pages, const int32_t* seq_ids,
+                               hipStream_t st);
+hipError_t launch_quest_select(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                               int layer, int n, const int32_t* seq_ids, const void* q,
+                               hipStream_t st);
+// Copy the last selection (pages, -1 padded) and per-head page counts out.
+hipError_t launch_quest_export(const dms_config& c, const Layout& lo, void* ws, int n,
+                               int32_t* pages, int32_t* counts, hipStream_t st);
 hipError_t launch_scatter(const dms_config& c, const Layout& lo, void* meta, void* ws,
                           void* pool, int layer, int n, const void* k, const void* v,
                           hipStream_t st);
 // k / v: the tokens appended by this call's planning kernel (written into the
 // pool by the decode kernel itself), or null when nothing was appended.
+// qsel (nullable): per head of the call, the page-table indices to attend
+// (page retrieval), quest_page_budget entries each.
 hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void* ws,
                          void* pool, int layer, int n, const void* q, const void* k,
                          const void* v, float* out, int waves, hipStream_t st,
-                         hipEvent_t ev_start, hipEvent_t ev_stop);
+                         hipEvent_t ev_start, hipEvent_t ev_stop, const int32_t* qsel = nullptr);
 int decode_resident_waves(const dms_config& c);
 hipError_t launch_retained(const dms_config& c, const Layout& lo, void* meta, int layer, int n,
                            const int32_t* seq_ids, int32_t* out, hipStream_t st);

@@ -73,6 +73,7 @@ struct DecodeParams {
   int part_acc_bytes;   // size of the split-K accumulator area (< 2 GiB)
   int NH, g, maxp, P, log2P, W;
   int zero_neuron;   // element 0 of the group's first query head is read as 0
+  int qB;            // page retrieval: pages attended per head (selection stride)
   float scale_log2;  // softmax scale * log2(e)
 };
 
@@ -498,7 +499,7 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
     const int32_t* __restrict__ cum_tiles, const int32_t* __restrict__ wave_bounds,
     const int4* __restrict__ wave_desc, const int4* __restrict__ head_waves,
     int32_t* __restrict__ head_cnt,
-    const int32_t* __restrict__ page_table,
+    const int32_t* __restrict__ page_table, const int32_t* __restrict__ qsel,
     char* __restrict__ pool, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_in,
     const uint16_t* __restrict__ v_in, float2* __restrict__ part_ml, float* __restrict__ part_acc,
     float* __restrict__ out, DecodeParams a) {
@@ -538,6 +539,8 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
     const int seg_end = min(te, c1);
     const int L = d.x;
     const int32_t* pt = page_table + static_cast<size_t>(d.y) * a.maxp;
+    // page retrieval: the head's tiles run over its selected pages only
+    const int32_t* ps = qsel != nullptr ? qsel + static_cast<size_t>(hh) * a.qB : nullptr;
     // query fragments (B operand): column r = query head r of the group
     u32x4 qf[D / 32];
     const u32x4 z = {0u, 0u, 0u, 0u};
@@ -558,7 +561,8 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
     // one head), then the tile's 16 KB block inside the page
     constexpr size_t kTileBytes = FP8 ? static_cast<size_t>(D) * 64 + 256 : static_cast<size_t>(D) * 128;
     auto tile_of = [&](int t) -> char* {
-      return pool + static_cast<size_t>(pt[t >> tiles_per_page_log2]) * a.page_bytes +
+      const int pi = ps != nullptr ? ps[t >> tiles_per_page_log2] : (t >> tiles_per_page_log2);
+      return pool + static_cast<size_t>(pt[pi]) * a.page_bytes +
              static_cast<size_t>(t & ((1 << tiles_per_page_log2) - 1)) * kTileBytes;
     };
     // The token appended by this call (slot d.z) is written into its tile by
@@ -690,7 +694,8 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
 template <int D, bool FP8>
 hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
                            int layer, int n, const void* q, const void* k, const void* v, float* out,
-                           int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
+                           int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop,
+                           const int32_t* qsel) {
   char* w = static_cast<char*>(ws);
   const int32_t* status = reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status);
   const int32_t* cum = reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles);
@@ -706,6 +711,7 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
   a.log2P = __builtin_ctz(static_cast<unsigned>(c.page_size));
   a.W = waves;
   a.zero_neuron = c.decision_source == DMS_DECIDE_QUERY;
+  a.qB = c.quest_page_budget;
   a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
   if (ev_start) (void)hipEventRecord(ev_start, st);
   hipLaunchKernelGGL((decode_kernel<D, FP8>), dim3(waves / kWavesPerBlock), dim3(256), 0, st, status,
@@ -714,7 +720,7 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
                      reinterpret_cast<const int4*>(w + lo.ws_wave_desc),
                      reinterpret_cast<const int4*>(w + lo.ws_head_waves),
                      reinterpret_cast<int32_t*>(w + lo.ws_head_cnt),
-                     layer_state(lo, meta, layer).page_table, static_cast<char*>(pool),
+                     layer_state(lo, meta, layer).page_table, qsel, static_cast<char*>(pool),
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                      static_cast<const uint16_t*>(v), part_ml, part_acc, out, a);
   hipError_t e = hipGetLastError();
@@ -726,17 +732,18 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
 
 hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
                          int layer, int n, const void* q, const void* k, const void* v, float* out,
-                         int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
+                         int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop,
+                         const int32_t* qsel) {
   const bool fp8 = c.kv_format == DMS_KV_FP8;
   if (c.head_dim == 128)
     return fp8 ? launch_decode_d<128, true>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st,
-                                            ev_start, ev_stop)
+                                            ev_start, ev_stop, qsel)
                : launch_decode_d<128, false>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st,
-                                             ev_start, ev_stop);
+                                             ev_start, ev_stop, qsel);
   return fp8 ? launch_decode_d<64, true>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st,
-                                         ev_start, ev_stop)
+                                         ev_start, ev_stop, qsel)
              : launch_decode_d<64, false>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st,
-                                          ev_start, ev_stop);
+                                          ev_start, ev_stop, qsel);
 }
 
 // One decode wave per SIMD (a block of 4 waves per CU).  Measured on MI355X

@@ -45,6 +45,7 @@ class DmsConfig(ctypes.Structure):
         ("decision_source", ctypes.c_int32),
         ("decision_bias", ctypes.c_float),
         ("kv_format", ctypes.c_int32),
+        ("quest_page_budget", ctypes.c_int32),
     ]
 
 
@@ -71,7 +72,7 @@ DMS_KV_FP8 = 1
 class DmsStateOffsets(ctypes.Structure):
     _fields_ = [(n, ctypes.c_size_t) for n in
                 ("status", "layer0", "layer_stride", "pos", "len", "ring", "page_table",
-                 "slot_meta", "stack", "top")]
+                 "slot_meta", "stack", "top", "page_bounds")]
 
 
 class DmsError(RuntimeError):
@@ -102,6 +103,7 @@ _SIGS = {
     "dms_decode_step_q": (_I, [_VP, _I, _I, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     "dms_prefill_chunk_q": (_I, [_VP, _I, _I, _VP, _VP, _I, _I, _VP, _VP, _VP, _VP, _VP, _VP]),
     "dms_retained_lengths": (_I, [_VP, _I, _I, _VP, _VP, _VP]),
+    "dms_quest_selection": (_I, [_VP, _I, _VP, _VP, _VP]),
     "dms_export_state": (_I, [_VP, _I, _VP, _SZ, _VP]),
     "dms_status": (_I, [_VP, _VP]),
     "dms_clear_status": (_I, [_VP, _VP]),
@@ -161,10 +163,11 @@ def make_config(num_layers, max_seqs, num_kv_heads, group_size, head_dim, window
                 page_size, num_pages, max_pages_per_head, max_chunk_tokens=0,
                 softmax_scale=0.0, eviction=DMS_EVICT_DELAYED,
                 decision_source=DMS_DECIDE_CALLER, decision_bias=-5.0,
-                kv_format=DMS_KV_BF16) -> DmsConfig:
+                kv_format=DMS_KV_BF16, quest_page_budget=0) -> DmsConfig:
     return DmsConfig(num_layers, max_seqs, num_kv_heads, group_size, head_dim, window,
                      page_size, num_pages, max_pages_per_head, max_chunk_tokens,
-                     softmax_scale, eviction, decision_source, decision_bias, kv_format)
+                     softmax_scale, eviction, decision_source, decision_bias, kv_format,
+                     quest_page_budget)
 
 
 # ---------------------------------------------------------------------------
@@ -249,6 +252,11 @@ def dms_prefill_chunk_q(ctx, layer, n, seq_ids, cu_seqlens, total_tokens, max_se
 def dms_retained_lengths(ctx, layer, n, seq_ids, out, stream=None):
     _check(lib().dms_retained_lengths(ctx, layer, n, _ptr(seq_ids), _ptr(out), _stream(stream)),
            "dms_retained_lengths")
+
+
+def dms_quest_selection(ctx, n, pages_out, count_out, stream=None):
+    _check(lib().dms_quest_selection(ctx, n, _ptr(pages_out), _ptr(count_out), _stream(stream)),
+           "dms_quest_selection")
 
 
 def dms_export_state(ctx, layer, nbytes, stream=None) -> np.ndarray:

@@ -57,6 +57,9 @@ def _cfg(**kw):
     (dict(decision_source=1, decision_bias=float("nan")), dms.DMS_ERR_INVALID),
     (dict(decision_source=1, decision_bias=float("inf")), dms.DMS_ERR_INVALID),
     (dict(kv_format=2), dms.DMS_ERR_INVALID),
+    (dict(quest_page_budget=-1), dms.DMS_ERR_INVALID),
+    (dict(quest_page_budget=17), dms.DMS_ERR_INVALID),                     # > max_pages_per_head
+    (dict(quest_page_budget=4, max_pages_per_head=5000), dms.DMS_ERR_UNSUPPORTED),
     (dict(kv_format=-1), dms.DMS_ERR_INVALID),
 ])
 def test_bad_configuration(kw, code):
@@ -234,3 +237,28 @@ def test_fp8_pages_layout_and_host_checks():
         assert ks[s_] == 2.0 ** -s_ and vs[s_] == 2.0 ** s_
         for e in (0, 7, 31, 32, 64, 100, 127):
             assert k[s_, e] == (s_ + e) % 251 and v[s_, e] == (3 * s_ + e) % 251
+
+
+def test_quest_layout_and_host_checks():
+    """Page bounds live in each layer's state only with a budget; the
+    selection export rejects contexts without one (fake pointers)."""
+    o0 = dms.dms_state_layout(_cfg())
+    o1 = dms.dms_state_layout(_cfg(quest_page_budget=4))
+    assert o0.page_bounds == 0 and o1.page_bounds > o1.top
+    assert o1.layer_stride - o0.layer_stride >= _cfg().num_pages * 2 * 64 * 2
+    L = dms.lib()
+    P = 0x100
+    ctx = dms.dms_create(_cfg(), 0x1000, [0x2000, 0x3000], 0x4000)
+    try:
+        assert L.dms_quest_selection(ctx, 1, P, P, None) == dms.DMS_ERR_INVALID
+    finally:
+        dms.dms_destroy(ctx)
+    ctx = dms.dms_create(_cfg(quest_page_budget=4), 0x1000, [0x2000, 0x3000], 0x4000)
+    try:
+        assert L.dms_quest_selection(ctx, 0, P, P, None) == dms.DMS_ERR_INVALID
+        assert L.dms_quest_selection(ctx, 5, P, P, None) == dms.DMS_ERR_INVALID   # > max_seqs
+        assert L.dms_quest_selection(ctx, 1, None, P, None) == dms.DMS_ERR_INVALID
+    finally:
+        dms.dms_destroy(ctx)
+    assert L.dms_quest_selection(None, 1, P, P, None) == dms.DMS_ERR_INVALID
+
