@@ -126,7 +126,8 @@ def build(wl, steps_total, chunk_tokens, dev):
     # the state is built by chunk appends of up to 16 sequences at a time
     grp = min(B, 16)
     cfg = dms.make_config(nl, B, H, g, D, w, P, pages_layer + 8, max_pages_head + 1,
-                          chunk_tokens * grp, kv_format=wl.get("kv_format", dms.DMS_KV_BF16))
+                          chunk_tokens * grp, kv_format=wl.get("kv_format", dms.DMS_KV_BF16),
+                          quest_page_budget=wl.get("quest_pages", 0))
     mb, pb, wb, _ = dms.dms_layout(cfg)
     log(f"pool {pb * nl / 2**30:.1f} GiB ({pages_layer + 8} pages/layer), meta "
         f"{mb / 2**30:.2f} GiB, workspace {wb / 2**20:.1f} MiB")
@@ -682,6 +683,9 @@ def main():
     ap.add_argument("--window", type=int, default=256, choices=[64, 256],
                     help="window of the heterogeneous stress workload")
     ap.add_argument("--chunk", type=int, default=4096)
+    ap.add_argument("--quest-pages", type=int, default=0,
+                    help="decode workloads: attend only this many pages (64 slots) per head, chosen "
+                         "by Quest's bound (page retrieval within the retained set)")
     ap.add_argument("--kv-format", choices=["bf16", "fp8"], default="bf16",
                     help="page format of the decode workloads (fp8: E4M3 rows with power-of-two scales)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -722,6 +726,10 @@ def main():
     if args.kv_format == "fp8":
         wl["kv_format"] = dms.DMS_KV_FP8
         wl["desc"] += ", FP8 E4M3 KV pages"
+    quest = args.quest_pages > 0
+    if quest:
+        wl["quest_pages"] = args.quest_pages
+        wl["desc"] += f", Quest page retrieval: {args.quest_pages} pages of 64 slots per head"
     S = args.warmup + 2 * args.steps
     cache, ctx, L0 = build(wl, S, args.chunk, dev)
     q, k, v, flags, fresh = step_inputs(wl, ctx, S, dev)
@@ -767,8 +775,28 @@ def main():
     # a captured graph only mark dependencies on this runtime).
     k_lo, k_hi = t_hi, t_hi + args.steps
     dms.dms_profile_start(cache.ctx, args.steps * nl)
-    for s in range(k_lo, k_hi):
-        run_step(s)
+    if quest:
+        # page retrieval: the bytes a launch reads are the live slots of the
+        # pages it selected, exported after every launch (outside its events)
+        Bq, P = args.quest_pages, 64
+        sel_p = torch.empty((nl, B * H, Bq), dtype=torch.int32, device=dev)
+        sel_c = torch.empty((nl, B * H), dtype=torch.int32, device=dev)
+        attended = []
+        for s in range(k_lo, k_hi):
+            for layer in range(nl):
+                dms.dms_decode_step(cache.ctx, layer, B, sid, q[s, layer], k[s, layer], v[s, layer],
+                                    flags[s, layer], out[layer])
+                dms.dms_quest_selection(cache.ctx, B, sel_p[layer], sel_c[layer])
+            Ls = Lstep[s].reshape(nl, B * H)
+            npg = (Ls + P - 1) // P
+            cnt = sel_c.to(torch.int64)
+            last = torch.gather(sel_p.to(torch.int64), 2, (cnt - 1).clamp(min=0)[..., None])[..., 0]
+            lq = cnt * P - torch.where(last == npg - 1, npg * P - Ls, torch.zeros_like(Ls))
+            attended.append(torch.where(npg <= Bq, Ls, lq).sum(dim=1).to(torch.float64))   # per layer
+        attended = torch.stack(attended)                                                  # [steps, nl]
+    else:
+        for s in range(k_lo, k_hi):
+            run_step(s)
     torch.cuda.synchronize()
     kern_ms, launches = dms.dms_profile_stop(cache.ctx)[dms.DMS_PROFILE_DECODE]
     if launches != args.steps * nl:
@@ -784,13 +812,17 @@ def main():
         if not torch.equal(lens.to(torch.int64), Lstep[-1, layer]):
             raise RuntimeError(f"layer {layer}: retained lengths diverged from the closed form")
     per_step_bytes = float(kv_bytes[t_lo:t_hi].sum()) / args.steps
-    value = per_step_bytes / (step_ms * 1e-3) / 1e9
     per_launch_bytes = float(kv_bytes[k_lo:k_hi].sum()) / (args.steps * nl)
+    if quest:
+        # attended bytes, measured on the eager pass that follows the timed steps
+        per_launch_bytes = float(attended.mean()) * row_bytes(wl)
+        per_step_bytes = per_launch_bytes * nl
+    value = per_step_bytes / (step_ms * 1e-3) / 1e9
     kern_avg_ms = kern_ms / max(launches, 1)
     achieved = per_launch_bytes / (kern_avg_ms * 1e-3) / 1e9
     mean_L = float(Lstep[t_lo:t_hi].double().mean())
     traffic = None
-    if args.workload == "qwen-r1-32b-8x":
+    if args.workload == "qwen-r1-32b-8x" and not quest:
         traffic = profiled_traffic(TRAFFIC_PROFILE_FP8 if args.kv_format == "fp8" else TRAFFIC_PROFILE,
                                    ["dms_common.h", "dms_fp8.h", "dms_decode.hip"])
     res = {
@@ -809,6 +841,7 @@ def main():
         "config": {
             "workload": wl["desc"],
             "kv_format": args.kv_format,
+            "quest_pages": args.quest_pages,
             "layers": nl, "batch": B, "kv_heads": H, "query_heads": H * g,
             "head_dim": D, "window": wl["window"], "p_evict": wl["p_evict"],
             "context": wl["context"] if not isinstance(wl["context"], tuple) else list(wl["context"]),
@@ -835,7 +868,9 @@ def main():
             "bytes_per_launch": int(per_launch_bytes),
         },
     }
-    if not args.no_cpu_baseline:
+    if quest:
+        res["attended_tokens_per_head"] = round(float(attended.mean()) / (B * H), 1)
+    if not args.no_cpu_baseline and not quest:
         log("timing the CPU oracle")
         res["cpu_baseline"] = cpu_baseline(wl, ctx)
     print(json.dumps(res), flush=True)

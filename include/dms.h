@@ -152,7 +152,7 @@ enum { DMS_KV_BF16 = 0, DMS_KV_FP8 = 1 };
  * taking the maximum over the group's query heads (one selection per KV head,
  * shared by its group), keeps the B highest (ties: lower page index; every
  * page when a head has at most B) and attends only their live slots.  Scores
- * are float32 sums in dimension order.  Prefill attends densely.
+ * are float32 sums in a fixed order.  Prefill attends densely.
  * dms_quest_selection reports the last decode call's selection.  Requires
  * max_pages_per_head <= 4096.
  */

@@ -10,7 +10,8 @@
 //     whenever an append writes into it (DMS reuses evicted tokens' slots, so
 //     bounds can shrink as well as grow);
 //   * quest_select_kernel scores every page of a head for its query group
-//     (maximum of U over the group's heads, float32 sums in dimension order),
+//     (maximum of U over the group's heads, one wave per page, float32 sums
+//     in a fixed order),
 //     keeps the B best (ties to the lower page index) in ascending order and
 //     the number of live slots they hold, which the decode planner then
 //     splits into tiles like any retained length.
@@ -19,6 +20,10 @@
 
 namespace dms {
 namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
 constexpr int kQThreads = 256;
 constexpr int kMaxSortPages = 4096;   // max_pages_per_head limit with a budget
@@ -45,24 +50,40 @@ __device__ inline uint16_t f32_to_bf16_exact(float x) {
   return static_cast<uint16_t>(__float_as_uint(x) >> 16);
 }
 
-// Key element (row r of the page, dim d) as stored.
-__device__ inline float key_elem(const QuestArgs& a, const char* page, int r, int d) {
+// Keys of row r, dims e .. e + 7 (e a multiple of 8), as stored.
+__device__ inline void key_elems8(const QuestArgs& a, const char* page, int r, int e, float* x) {
+  const int j = r & 31;
   if (a.fp8) {
     const char* tile = page + static_cast<size_t>(r >> 5) * fp8_tile_bytes(a.D);
-    const int j = r & 31;
-    const uint32_t code = *reinterpret_cast<const uint8_t*>(tile + fp8_k_off(j, d));
+    const uint2 c = *reinterpret_cast<const uint2*>(tile + fp8_k_off(j, e));   // 8 contiguous codes
     const float scale = *reinterpret_cast<const float*>(tile + fp8_ks_off(j, a.D));
-    return __builtin_amdgcn_cvt_pk_f32_fp8(code, false)[0] * scale;   // exact
+    const uint32_t w[2] = {c.x, c.y};
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const auto lo = __builtin_amdgcn_cvt_pk_f32_fp8(w[h], false);
+      const auto hi = __builtin_amdgcn_cvt_pk_f32_fp8(w[h], true);
+      x[4 * h] = lo[0] * scale;       // exact: a code times a power of two
+      x[4 * h + 1] = lo[1] * scale;
+      x[4 * h + 2] = hi[0] * scale;
+      x[4 * h + 3] = hi[1] * scale;
+    }
+    return;
   }
   const char* tile = page + static_cast<size_t>(r >> 5) * tile_bytes(a.D);
-  const uint32_t bits = *reinterpret_cast<const uint16_t*>(tile + k_elem_off(r & 31, d));
-  return __uint_as_float(bits << 16);
+  const uint4 v = *reinterpret_cast<const uint4*>(tile + k_elem_off(j, e));   // 8 contiguous bf16
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __uint_as_float(w[i] << 16);
+    x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+  }
 }
 
 // Grid (pages, heads of the call): page i of head hh -- the page the last
 // planned append wrote (all_pages = 0) or every page (all_pages = 1).
+// Thread t covers dims 8 (t % (D/8)) .. + 7 of rows t / (D/8), + rows_per_pass, ...
 __global__ __launch_bounds__(kQThreads) void quest_bounds_kernel(QuestArgs a) {
-  __shared__ float red[2][kQThreads];
+  __shared__ float red[2][kQThreads][8];
   if (load_status(a.status) != 0) return;
   const int hh = blockIdx.y;
   const int sh = a.seq_ids[hh / a.H] * a.H + hh % a.H;
@@ -73,24 +94,43 @@ __global__ __launch_bounds__(kQThreads) void quest_bounds_kernel(QuestArgs a) {
   const int pg = a.st.page_table[static_cast<size_t>(sh) * a.maxp + i];
   const char* page = a.pool + static_cast<size_t>(pg) * a.page_bytes;
   const int tid = threadIdx.x;
-  const int d = tid % a.D, rg = tid / a.D, nrg = kQThreads / a.D;
-  float lo = INFINITY, hi = -INFINITY;
-  for (int r = rg; r < valid; r += nrg) {
-    const float x = key_elem(a, page, r, d);
-    lo = fminf(lo, x);
-    hi = fmaxf(hi, x);
+  const int per_row = a.D / 8, rows = kQThreads / per_row;
+  const int e = 8 * (tid % per_row), r0 = tid / per_row;
+  float lo[8], hi[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    lo[k] = INFINITY;
+    hi[k] = -INFINITY;
   }
-  red[0][tid] = lo;
-  red[1][tid] = hi;
+  for (int r = r0; r < valid; r += rows) {
+    float x[8];
+    key_elems8(a, page, r, e, x);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      lo[k] = fminf(lo[k], x[k]);
+      hi[k] = fmaxf(hi[k], x[k]);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    red[0][tid][k] = lo[k];
+    red[1][tid][k] = hi[k];
+  }
   __syncthreads();
-  if (rg == 0) {
-    for (int k = 1; k < nrg; ++k) {
-      lo = fminf(lo, red[0][k * a.D + d]);
-      hi = fmaxf(hi, red[1][k * a.D + d]);
+  if (r0 == 0) {
+    for (int g2 = 1; g2 < rows; ++g2) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        lo[k] = fminf(lo[k], red[0][g2 * per_row + tid][k]);
+        hi[k] = fmaxf(hi[k], red[1][g2 * per_row + tid][k]);
+      }
     }
     uint16_t* b = a.st.page_bounds + static_cast<size_t>(pg) * 2 * a.D;
-    b[d] = f32_to_bf16_exact(lo);
-    b[a.D + d] = f32_to_bf16_exact(hi);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      b[e + k] = f32_to_bf16_exact(lo[k]);
+      b[a.D + e + k] = f32_to_bf16_exact(hi[k]);
+    }
   }
 }
 
@@ -102,7 +142,6 @@ __device__ inline uint32_t orderable(float x) {
 
 // One block per head of the call.
 __global__ __launch_bounds__(kQThreads) void quest_select_kernel(QuestArgs a) {
-  __shared__ float qs[kMaxGroup][128];
   __shared__ unsigned long long keys[kMaxSortPages];
   __shared__ int lds[17];
   if (load_status(a.status) != 0) return;
@@ -117,37 +156,79 @@ __global__ __launch_bounds__(kQThreads) void quest_select_kernel(QuestArgs a) {
     if (tid == 0) a.qlen[hh] = L;
     return;
   }
-  // the group's queries, as float (the borrowed neuron read as 0 in query-decision mode)
+  // Scores as one small matrix product: for q_i >= 0 the larger of
+  // q_i lo_i, q_i hi_i is q_i hi_i, else q_i lo_i, so U = [lo | hi] . [q-; q+]
+  // with q- = min(q, 0), q+ = max(q, 0) (exact in bf16; the products are
+  // exact in fp32).  MFMA rows are 16 pages, columns the group's heads, k the
+  // 2 D entries of a page's bounds (lo then hi).  The borrowed neuron is read
+  // as 0 in query-decision mode.
   const int h = hh % a.H;
   const uint16_t* qg = a.q + (static_cast<size_t>(hh / a.H) * a.H * a.g + h * a.g) * a.D;
-  for (int e = tid; e < a.g * a.D; e += kQThreads) {
-    float x = __uint_as_float(static_cast<uint32_t>(qg[e]) << 16);
-    if (a.zero_neuron && e == 0) x = 0.f;
-    qs[e / a.D][e % a.D] = x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int r = lane & 15, G = lane >> 4;
+  const int kbs = a.D / 32;                  // k-blocks per half (lo or hi)
+  u32x4 qneg[4], qpos[4];                    // this lane's column (head r): dims 32 kb + 8 G .. + 7
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) {
+    u32x4 x = {0u, 0u, 0u, 0u};
+    if (r < a.g && kb < kbs) x = *reinterpret_cast<const u32x4*>(qg + r * a.D + 32 * kb + 8 * G);
+    if (a.zero_neuron && r == 0 && G == 0 && kb == 0) x[0] &= 0xFFFF0000u;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      // per bf16 half: negative (sign set) -> q-, else q+
+      const uint32_t neg = ((x[w] >> 15) & 1u) * 0x0000FFFFu | ((x[w] >> 31) & 1u) * 0xFFFF0000u;
+      qneg[kb][w] = x[w] & neg;
+      qpos[kb][w] = x[w] & ~neg;
+    }
   }
   int npow = 1;
   while (npow < npages) npow <<= 1;
   for (int p = tid; p < npow; p += kQThreads) keys[p] = 0ull;
   __syncthreads();
-  for (int p = tid; p < npages; p += kQThreads) {
-    const int pg = a.st.page_table[static_cast<size_t>(sh) * a.maxp + p];
-    const uint16_t* b = a.st.page_bounds + static_cast<size_t>(pg) * 2 * a.D;
-    float best = -INFINITY;
-    for (int hq = 0; hq < a.g; ++hq) {
-      float u = 0.f;
-      for (int d = 0; d < a.D; ++d) {
-        const float lo = __uint_as_float(static_cast<uint32_t>(b[d]) << 16);
-        const float hi = __uint_as_float(static_cast<uint32_t>(b[a.D + d]) << 16);
-        const float x = qs[hq][d];
-        u += fmaxf(x * lo, x * hi);
+  for (int pb = 16 * wave; pb < npages; pb += kQThreads / 4) {
+    // A operand: lane (page pb + r, G) loads bound entries 32 kb + 8 G .. + 7
+    const int p = pb + r;
+    const uint16_t* b = p < npages
+        ? a.st.page_bounds + static_cast<size_t>(a.st.page_table[static_cast<size_t>(sh) * a.maxp + p]) * 2 * a.D
+        : nullptr;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      if (kb < kbs) {
+        const u32x4 lo = b ? *reinterpret_cast<const u32x4*>(b + 32 * kb + 8 * G) : u32x4{0u, 0u, 0u, 0u};
+        const u32x4 hi = b ? *reinterpret_cast<const u32x4*>(b + a.D + 32 * kb + 8 * G) : u32x4{0u, 0u, 0u, 0u};
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, lo),
+                                                      __builtin_bit_cast(bf16x8, qneg[kb]), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, hi),
+                                                      __builtin_bit_cast(bf16x8, qpos[kb]), acc, 0, 0, 0);
       }
-      best = fmaxf(best, u);
     }
-    // larger score first; equal scores: lower page index first
-    keys[p] = (static_cast<unsigned long long>(orderable(best)) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(p));
+    // lane (head r, G) holds pages pb + 4 G + i; maximum over the group's heads
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float u = r < a.g ? acc[i] : -INFINITY;
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) u = fmaxf(u, __shfl_xor(u, off, 16));
+      const int pp = pb + 4 * G + i;
+      // larger score first; equal scores: lower page index first
+      if (r == 0 && pp < npages)
+        keys[pp] = (static_cast<unsigned long long>(orderable(u)) << 32) |
+                   (0xFFFFFFFFu - static_cast<uint32_t>(pp));
+    }
   }
   __syncthreads();
-  // bitonic sort, descending
+  __shared__ int chosen[kMaxSortPages];
+  if (npages <= kQThreads) {
+    // rank of each page among all of them (keys are distinct)
+    if (tid < npages) {
+      const unsigned long long k0 = keys[tid];
+      int rank = 0;
+      for (int p = 0; p < npages; ++p) rank += keys[p] > k0;
+      chosen[tid] = rank < a.B;
+    }
+    __syncthreads();
+  } else {
+  // bitonic sort, descending, then the B best marked
   for (int k = 2; k <= npow; k <<= 1) {
     for (int j = k >> 1; j > 0; j >>= 1) {
       for (int x = tid; x < npow; x += kQThreads) {
@@ -164,13 +245,13 @@ __global__ __launch_bounds__(kQThreads) void quest_select_kernel(QuestArgs a) {
       __syncthreads();
     }
   }
-  // the B best pages, listed in ascending page order
-  __shared__ int chosen[kMaxSortPages];
   for (int p = tid; p < npages; p += kQThreads) chosen[p] = 0;
   __syncthreads();
   for (int i = tid; i < a.B; i += kQThreads)
     chosen[0xFFFFFFFFu - static_cast<uint32_t>(keys[i] & 0xFFFFFFFFull)] = 1;
   __syncthreads();
+  }
+  // the B best pages, listed in ascending page order
   int run = 0;
   for (int p0 = 0; p0 < npages; p0 += kQThreads) {
     const int p = p0 + tid;
