@@ -10,11 +10,15 @@ from dms_testlib import SeqInputs, to_dev
 pytestmark = pytest.mark.gpu
 
 
-def test_graph_replays_match_eager():
+@pytest.mark.parametrize("fp8,budget", [(False, 0), (True, 0), (False, 2), (True, 2)])
+def test_graph_replays_match_eager(fp8, budget):
+    """Dense and page-retrieval steps (budget 2 of ~3 pages per head), bf16 and
+    FP8 pages: the retrieval step is six launches per layer, all captured."""
     import torch
     from paper_2506_05345_amd import dms
     kw = dict(num_layers=2, max_seqs=3, num_kv_heads=2, group_size=5, head_dim=128, window=16,
-              page_size=64, num_pages=200, max_pages_per_head=32, max_chunk_tokens=3 * 600)
+              page_size=64, num_pages=200, max_pages_per_head=32, max_chunk_tokens=3 * 600,
+              kv_format=dms.DMS_KV_FP8 if fp8 else dms.DMS_KV_BF16, quest_page_budget=budget)
     cfg = dms.make_config(**kw)
     eager, graphed = dms.DmsCache(cfg), dms.DmsCache(cfg)
     seqs = [2, 0, 1]

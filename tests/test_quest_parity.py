@@ -203,3 +203,54 @@ def test_budget_covering_every_page_is_dense_decode():
     dmsmod.dms_decode(dense.ctx, 0, 2, sid, q, b)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+def test_many_heads_multi_pass_planner():
+    """320 sequences x 4 KV heads: more heads than one planning block has
+    threads, so the multi-pass planner plans over the selected pages."""
+    H, g, d, P, B = 4, 2, 64, 32, 2
+    rng = np.random.default_rng(71)
+    seqs = [int(s) for s in rng.permutation(320)]
+    lens = {s: int(rng.integers(1, 300)) for s in seqs}
+    dms, cfg, cache, orc = _mk(B, num_layers=1, max_seqs=320, num_kv_heads=H, group_size=g, head_dim=d,
+                               window=8, page_size=P, num_pages=12000, max_pages_per_head=32,
+                               max_chunk_tokens=320 * 300)
+    inp = {s: SeqInputs(72, 0, s, lens[s] + 3, H, g, d, 0.5) for s in seqs}
+    _append_chunks(dms, cache, orc, seqs, inp, lens, 300)
+    exact, amb = _decode_steps(dms, cache, orc, seqs, inp, lens, 3, g, check_bounds_every=2)
+    assert exact > 100
+
+
+def test_query_decisions_read_the_zeroed_neuron():
+    """Decisions from the borrowed neuron (App. C): selection scores and
+    attention both read that element as 0."""
+    import torch
+    from oracle import query_decisions, zero_borrowed_neuron
+    H, g, d, P, B = 2, 4, 128, 32, 2
+    dms, cfg, cache, orc = _mk(B, num_layers=1, max_seqs=2, num_kv_heads=H, group_size=g, head_dim=d,
+                               window=8, page_size=P, num_pages=64, max_pages_per_head=16,
+                               max_chunk_tokens=600, decision_source=1, decision_bias=0.0)
+    seqs = [1, 0]
+    lens = {1: 300, 0: 180}
+    inp = {s: SeqInputs(73, 0, s, lens[s] + 10, H, g, d, 0.5) for s in seqs}
+    for s in seqs:   # decisions as the library will take them: from q
+        inp[s].flags[:] = query_decisions(bf16_to_f32(inp[s].q), g, 0.0)
+    _append_chunks(dms, cache, orc, seqs, inp, lens, 300)
+    sid = to_dev(np.array(seqs, np.int32))
+    for step in range(10):
+        ts = {s: lens[s] + step for s in seqs}
+        q = np.stack([inp[s].q[ts[s]] for s in seqs])
+        k = np.stack([inp[s].k[ts[s]] for s in seqs])
+        v = np.stack([inp[s].v[ts[s]] for s in seqs])
+        out = torch.full((2, H * g, d), float("nan"), device="cuda")
+        dec = torch.empty((2, H), dtype=torch.uint8, device="cuda")
+        dms.dms_decode_step_q(cache.ctx, 0, 2, sid, to_dev(q), to_dev(k), to_dev(v), dec, out)
+        torch.cuda.synchronize()
+        assert dms.dms_status(cache.ctx) == 0
+        f = np.stack([inp[s].flags[ts[s]] for s in seqs])
+        assert np.array_equal(dec.cpu().numpy(), f)
+        orc.append(seqs, f, bf16_to_f32(k), bf16_to_f32(v))
+        qz = zero_borrowed_neuron(bf16_to_f32(q), g)
+        from dms_synth import f32_to_bf16_bits_np
+        _check_step(dms, cache, orc, seqs, f32_to_bf16_bits_np(qz.astype(np.float32)), out, g)
+
