@@ -860,7 +860,8 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "traffic_source": "profiles/" + TRAFFIC_PROFILE if traffic is not None else None,
+            "traffic_source": ("profiles/" + (TRAFFIC_PROFILE_FP8 if args.kv_format == "fp8" else TRAFFIC_PROFILE)
+                               if traffic is not None else None),
             "kernel": "decode_kernel<128>",
             "kernel_timing": "HIP events around each decode launch, eager pass of the next "
                              f"{args.steps} steps",

@@ -190,13 +190,15 @@ typedef struct dms_state_offsets {
 /*
  * Page layout in a layer's pool (page i at i * page_bytes).  A slot s of a
  * head lives in page page_table[s / P], tile (s % P) / 32, row j = s % 32.
+ * With h = (j / 4) % 2 and r = 4 * (j / 8) + j % 4 (row j's place among 16
+ * rows), both formats store a tile in the order of the decode kernel's MFMA
+ * operand loads (16-byte pieces, one contiguous 1 KB per load instruction):
  * DMS_KV_BF16: page_bytes = 4 * P * d; a page is P/32 tiles of 128 * d bytes:
- *   keys   bf16 [d/32][32 rows][32 dims]: element (j, e) at byte
- *          (e / 32) * 2048 + j * 64 + (e % 32) * 2 of the tile
- *   values bf16 [d][32 rows] (transposed): element (j, e) at byte
- *          64 * d + e * 64 + j * 2 of the tile
- * DMS_KV_FP8: page_bytes = P/32 * (64 * d + 256); with
- *   h = (j / 4) % 2, r = 4 * (j / 8) + j % 4 (row j's place among 16 rows):
+ *   key (j, e)   bf16 at byte ((((e / 32) * 2 + h) * 4 + (e / 8) % 4) * 16 + r) * 16
+ *                         + (e % 8) * 2 of the tile
+ *   value (j, e) bf16 at byte 64 * d + (((e / 16) * 4 + j / 8) * 16 + e % 16) * 16
+ *                         + (j % 8) * 2 of the tile
+ * DMS_KV_FP8: page_bytes = P/32 * (64 * d + 256):
  *   key code (j, e)   at (e / 64) * 2048 + h * 1024 + (16 * ((e / 8) % 4) + r) * 16
  *                        + 8 * ((e / 32) % 2) + e % 8
  *   value code (j, e) at 32 * d + (e / 32) * 1024 + (16 * (j / 8) + e % 16) * 16

@@ -88,6 +88,7 @@ Layout make_layout(const dms_config& c) {
   lo.ws_pf_tiles = take(2 * H * static_cast<size_t>(lo.pf_tiles_per_head) * D * 128);
   lo.ws_pf_flags = take(static_cast<size_t>(c.max_chunk_tokens) * H);  // decisions from q
   lo.ws_q_sel = take(NH * static_cast<size_t>(c.quest_page_budget) * 4);
+  lo.ws_q_page = take(NH * static_cast<size_t>(c.quest_page_budget) * 4);
   lo.ws_q_len = take(NH * 4);
   lo.workspace_bytes = off;
   return lo;
@@ -154,6 +155,9 @@ const int32_t* quest_lengths(const Ctx& c) {
 }
 const int32_t* quest_pages(const Ctx& c) {
   return reinterpret_cast<const int32_t*>(static_cast<char*>(c.ws) + c.lo.ws_q_sel);
+}
+const int32_t* quest_phys_pages(const Ctx& c) {
+  return reinterpret_cast<const int32_t*>(static_cast<char*>(c.ws) + c.lo.ws_q_page);
 }
 
 int ensure_waves(dms_ctx* ctx) {
@@ -277,7 +281,7 @@ int dms_decode(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const
   next_events(ctx->c, DMS_PROFILE_DECODE, &e0, &e1);
   if (e == hipSuccess)
     e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, nullptr,
-                           nullptr, out_dev, c.decode_waves, st, e0, e1, quest ? quest_pages(c) : nullptr);
+                           nullptr, out_dev, c.decode_waves, st, e0, e1, quest ? quest_phys_pages(c) : nullptr);
   return hip_rc(e);
 }
 
@@ -311,7 +315,7 @@ int decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, cons
     next_events(ctx->c, DMS_PROFILE_DECODE, &e0, &e1);
     if (e == hipSuccess)
       e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, nullptr,
-                             nullptr, out_dev, c.decode_waves, st, e0, e1, quest_pages(c));
+                             nullptr, out_dev, c.decode_waves, st, e0, e1, quest_phys_pages(c));
     return hip_rc(e);
   }
   // planner (slot choice, page pops, state, wave ranges) -> decode, which

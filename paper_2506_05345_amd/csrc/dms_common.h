@@ -33,7 +33,8 @@ struct Layout {
   size_t ws_wave_bounds, ws_wave_desc, ws_head_waves, ws_head_cnt;
   size_t ws_ck_need, ws_ck_fresh, ws_ck_base, ws_ck_pos0, ws_ck_err, ws_ck_slot;
   size_t ws_pf_cum, ws_pf_meta, ws_pf_tiles, ws_pf_flags;
-  size_t ws_q_sel, ws_q_len;   // quest: selection [NH][B], attended lengths [NH]
+  size_t ws_q_sel, ws_q_page, ws_q_len;   // quest: selection [NH][B] (page-table
+                                          // indices, physical pages), attended lengths [NH]
   int pf_tiles_per_head;   // tiles of one (region, KV head) in ws_pf_tiles
   size_t workspace_bytes;
   int max_heads, max_partials, max_slots;
@@ -70,17 +71,23 @@ inline LayerState layer_state(const Layout& lo, void* meta, int layer) {
 }
 
 // Pool page layout.  A page holds P/32 tiles of 32 consecutive slots; each
-// tile is 128*D bytes, keys first, then values:
-//   K part [D/32][32 slots][32 dims] bf16  -- element (j, e) at (e/32)*2048 + j*64 + (e%32)*2
-//   V part [D][32 slots] bf16 (transposed) -- element (j, e) at 64*D + e*64 + j*2
-// so the 32 tokens a decode tile reads are one contiguous 16 KB block (D = 128)
-// and every 16-byte lane load of the decode kernel covers whole cache lines.
+// tile is 128*D bytes, keys first, then values, both in the order the decode
+// MFMAs consume them, as 16-byte pieces of 8 bf16:
+//   K part: D/32 x 2 blocks of 1 KB.  Block (s, h) holds dims 32 s .. 32 s + 31
+//     of the 16 slots j with (j / 4) % 2 == h, as [G = dims / 8 % 4][r][8 dims]
+//     with r = 4 (j / 8) + j % 4 (the rows of the first / second score MFMA);
+//   V part: D/16 blocks of 1 KB.  Block b holds dims 16 b .. 16 b + 15 as
+//     [G = slots / 8][r = dim % 16][8 slots] (rows of V^T).
+// Every load instruction of a decode wave then reads one contiguous 1 KB with
+// lane l taking bytes 16 l .. 16 l + 15.
 __host__ __device__ inline size_t tile_bytes(int D) { return static_cast<size_t>(D) * 128; }
 __host__ __device__ inline size_t k_elem_off(int j, int e) {
-  return static_cast<size_t>(e >> 5) * 2048 + j * 64 + (e & 31) * 2;
+  return (static_cast<size_t>(((e >> 5) * 2 + ((j >> 2) & 1)) * 4 + ((e >> 3) & 3)) * 16 +
+          4 * (j >> 3) + (j & 3)) * 16 + (e & 7) * 2;
 }
 __host__ __device__ inline size_t v_elem_off(int j, int e, int D) {
-  return static_cast<size_t>(D) * 64 + e * 64 + j * 2;
+  return static_cast<size_t>(D) * 64 + (static_cast<size_t>((e >> 4) * 4 + (j >> 3)) * 16 + (e & 15)) * 16 +
+         (j & 7) * 2;
 }
 
 // Per-head descriptor written by the planning kernels, one per (seq in call,
@@ -203,12 +210,12 @@ hipError_t launch_scatter(const dms_config& c, const Layout& lo, void* meta, voi
                           hipStream_t st);
 // k / v: the tokens appended by this call's planning kernel (written into the
 // pool by the decode kernel itself), or null when nothing was appended.
-// qsel (nullable): per head of the call, the page-table indices to attend
-// (page retrieval), quest_page_budget entries each.
+// qpage (nullable): per head of the call, the physical pages to attend (page
+// retrieval), quest_page_budget entries each.
 hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void* ws,
                          void* pool, int layer, int n, const void* q, const void* k,
                          const void* v, float* out, int waves, hipStream_t st,
-                         hipEvent_t ev_start, hipEvent_t ev_stop, const int32_t* qsel = nullptr);
+                         hipEvent_t ev_start, hipEvent_t ev_stop, const int32_t* qpage = nullptr);
 int decode_resident_waves(const dms_config& c);
 hipError_t launch_retained(const dms_config& c, const Layout& lo, void* meta, int layer, int n,
                            const int32_t* seq_ids, int32_t* out, hipStream_t st);

@@ -13,14 +13,16 @@
 //    ragged per-head lengths (Sec. 3.1: heads compress at different rates) do
 //    not unbalance the chip.  A wave covering a whole head writes the final
 //    output; a head split over several waves gets partials (running max, sum,
-//    accumulator) and the wave that completes the head's tile count merges
-//    them with log-sum-exp weights (device-coherent accesses, no L2 flush).
+//    accumulator).  At the end of its range a wave adds its tile counts to
+//    the heads it shares, and the wave that completes a head's count merges
+//    its partials with log-sum-exp weights (device-coherent accesses, no L2
+//    flush), so no wait interrupts the tile stream.
 //  * Pages are stored tile-major: the 32 tokens of a tile are one contiguous
-//    block (keys as D/32 sub-blocks of 32 x 32 dims, then values transposed,
-//    D rows of 32 tokens).  Per tile each lane issues 16-byte loads straight
-//    into MFMA operand registers -- keys as the A operand of S^T = K Q^T,
-//    transposed values as the A operand of O^T = V^T P^T -- and every load
-//    instruction covers whole 128-byte lines.  No LDS round trip is needed.
+//    block, in the order the MFMAs consume it (keys as the A operand of
+//    S^T = K Q^T, transposed values as the A operand of O^T = V^T P^T; layout
+//    in dms_common.h).  Per tile each lane issues 16-byte loads straight into
+//    operand registers, and every load instruction of a wave reads one
+//    contiguous 1 KB.  No LDS round trip is needed.
 //    The group's g query heads fill g of the 16 MFMA columns.
 //  * The 16x16 accumulator layout puts rows 4*(lane/16) .. +3 of column
 //    lane%16 in each lane.  Tile rows of the first / second score MFMA are
@@ -52,6 +54,21 @@ __device__ inline f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
 }
 
 __device__ inline u32x4 ldg16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
+// Reads of tables that no kernel running with this one writes (planner
+// output, page tables): through the constant address space, so that a
+// wave-uniform index becomes a scalar load even inside loops that store to
+// the pool (a vector load there would need vmcnt(0) before its value is used
+// and drain the wave's tile pipeline).
+__device__ inline int ldc(const int32_t* p, size_t i) {
+  typedef const int32_t __attribute__((address_space(4))) CT;
+  return ((CT*)p)[i];
+}
+__device__ inline int4 ldc(const int4* p, size_t i) {
+  typedef int __attribute__((ext_vector_type(4))) i32x4;
+  typedef const i32x4 __attribute__((address_space(4))) CT;
+  const i32x4 v = ((CT*)p)[i];
+  return make_int4(v[0], v[1], v[2], v[3]);
+}
 // Cache-tile reads: every byte is read once per step, so the loads are
 // non-temporal (measured on MI355X: a shuffled 32 KB-page stream reaches
 // 7.1 TB/s this way against 6.3 TB/s with ordinary loads).
@@ -95,40 +112,37 @@ struct Frag {
   u32x4 vt[D / 16];  // V^T rows d = 16b + r, tokens 8G .. 8G+7
 };
 
-// Per-lane byte offsets inside a 32-token tile (constant for the whole
-// kernel); see the page layout in dms_common.h.
-struct LaneOff {
-  uint32_t k;  // K row 8*(r/4) + r%4 of sub-block 0, elements 8G .. 8G+7
-  uint32_t v;  // V^T row r, tokens 8G .. 8G+7
-};
-
-// Load one full 32-token tile starting at `tile` (wave-uniform address).
+// Load one full 32-slot tile (wave-uniform address).  The tile is stored in
+// fragment order (see dms_common.h), so load instruction i of the wave reads
+// the contiguous 1 KB block i and lane l takes bytes 16 l .. 16 l + 15.
 template <int D>
-__device__ inline void load_tile(Frag<D>& f, const char* tile, LaneOff lo) {
+__device__ inline void load_tile(Frag<D>& f, const char* tile, int lane) {
+  const char* p = tile + lane * 16;
 #pragma unroll
   for (int s = 0; s < D / 32; ++s) {
-    f.ka[s] = ldkv(tile + lo.k + s * 2048);
-    f.kb[s] = ldkv(tile + lo.k + 256 + s * 2048);
+    f.ka[s] = ldkv(p + s * 2048);
+    f.kb[s] = ldkv(p + s * 2048 + 1024);
   }
 #pragma unroll
-  for (int b = 0; b < D / 16; ++b) f.vt[b] = ldkv(tile + lo.v + b * 1024);
+  for (int b = 0; b < D / 16; ++b) f.vt[b] = ldkv(p + D * 64 + b * 1024);
 }
 
 // Last, partial tile of a head: rows at or past L are not read and the value
 // elements of those tokens are zero.
 template <int D>
-__device__ inline void load_tail(Frag<D>& f, const char* tile, LaneOff lo, int valid, int r, int G) {
+__device__ inline void load_tail(Frag<D>& f, const char* tile, int lane, int valid, int r, int G) {
   const int ta = 8 * (r >> 2) + (r & 3);
   const u32x4 z = {0u, 0u, 0u, 0u};
+  const char* p = tile + lane * 16;
 #pragma unroll
   for (int s = 0; s < D / 32; ++s) {
-    f.ka[s] = ta < valid ? ldkv(tile + lo.k + s * 2048) : z;
-    f.kb[s] = ta + 4 < valid ? ldkv(tile + lo.k + 256 + s * 2048) : z;
+    f.ka[s] = ta < valid ? ldkv(p + s * 2048) : z;
+    f.kb[s] = ta + 4 < valid ? ldkv(p + s * 2048 + 1024) : z;
   }
   const int nv = valid - 8 * G;  // tokens of this lane's 8 that exist
 #pragma unroll
   for (int b = 0; b < D / 16; ++b) {
-    u32x4 x = nv > 0 ? ldkv(tile + lo.v + b * 1024) : z;
+    u32x4 x = nv > 0 ? ldkv(p + D * 64 + b * 1024) : z;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       if (j >= nv) {  // element j holds token 8G + j
@@ -505,7 +519,7 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
     const int32_t* __restrict__ cum_tiles, const int32_t* __restrict__ wave_bounds,
     const int4* __restrict__ wave_desc, const int4* __restrict__ head_waves,
     int32_t* __restrict__ head_cnt,
-    const int32_t* __restrict__ page_table, const int32_t* __restrict__ qsel,
+    const int32_t* __restrict__ page_table, const int32_t* __restrict__ qpage,
     char* __restrict__ pool, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_in,
     const uint16_t* __restrict__ v_in, float2* __restrict__ part_ml, float* __restrict__ part_acc,
     float* __restrict__ out, DecodeParams a) {
@@ -517,17 +531,17 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
   const int r = lane & 15, G = lane >> 4;
   // the planner's descriptor of this wave's first segment comes with the
   // range, so a wave starts after one round of scalar loads
-  const int4 wd0 = wave_desc[2 * wave], wd1 = wave_desc[2 * wave + 1];
-  int tb = wave_bounds[wave];
-  const int te = wave_bounds[wave + 1];
+  const int4 wd0 = ldc(wave_desc, 2 * wave), wd1 = ldc(wave_desc, 2 * wave + 1);
+  int tb = ldc(wave_bounds, wave);
+  const int te = ldc(wave_bounds, wave + 1);
   if (load_status(status) != 0) return;
   if (tb >= te) return;
-  LaneOff lo;
-  lo.k = static_cast<uint32_t>((8 * (r >> 2) + (r & 3)) * 64 + 16 * G);
-  lo.v = static_cast<uint32_t>(D * 64 + r * 64 + 16 * G);
   int hh = wd0.z;
   const int tiles_per_page_log2 = a.log2P - 5;
   bool first = true;
+  // heads shared with other waves, published at the end: head, tiles, total
+  int p_hh[2] = {0, 0}, p_cnt[2] = {0, 0}, p_tot[2] = {0, 0};
+  int npend = 0;
   while (tb < te) {
     int c0, c1;
     HeadDesc d;
@@ -537,16 +551,17 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
       d = make_int4(wd1.y, wd1.z, wd1.w, 0);
       first = false;
     } else {
-      while (cum_tiles[hh + 1] <= tb) ++hh;
-      c0 = cum_tiles[hh];
-      c1 = cum_tiles[hh + 1];
-      d = desc[hh];
+      while (ldc(cum_tiles, hh + 1) <= tb) ++hh;
+      c0 = ldc(cum_tiles, hh);
+      c1 = ldc(cum_tiles, hh + 1);
+      d = ldc(desc, hh);
     }
     const int seg_end = min(te, c1);
     const int L = d.x;
     const int32_t* pt = page_table + static_cast<size_t>(d.y) * a.maxp;
-    // page retrieval: the head's tiles run over its selected pages only
-    const int32_t* ps = qsel != nullptr ? qsel + static_cast<size_t>(hh) * a.qB : nullptr;
+    // page retrieval: the head's tiles run over the physical pages of its
+    // selection only
+    const int32_t* pages = qpage != nullptr ? qpage + static_cast<size_t>(hh) * a.qB : pt;
     // query fragments (B operand): column r = query head r of the group
     u32x4 qf[D / 32];
     const u32x4 z = {0u, 0u, 0u, 0u};
@@ -566,16 +581,16 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
     // tile t of the head: page from a scalar load (the whole wave works on
     // one head), then the tile's 16 KB block inside the page
     constexpr size_t kTileBytes = FP8 ? static_cast<size_t>(D) * 64 + 256 : static_cast<size_t>(D) * 128;
-    auto tile_of = [&](int t) -> char* {
-      const int pi = ps != nullptr ? ps[t >> tiles_per_page_log2] : (t >> tiles_per_page_log2);
-      return pool + static_cast<size_t>(pt[pi]) * a.page_bytes +
+    auto tile_in = [&](const int32_t* pl, int t) -> char* {
+      return pool + static_cast<size_t>(ldc(pl, t >> tiles_per_page_log2)) * a.page_bytes +
              static_cast<size_t>(t & ((1 << tiles_per_page_log2) - 1)) * kTileBytes;
     };
+    auto tile_of = [&](int t) -> char* { return tile_in(pages, t); };
     // The token appended by this call (slot d.z) is written into its tile by
     // the one wave whose segment covers that tile, before the segment's
     // loads: same-wave stores and loads to one address stay in order.
     if (k_in != nullptr && d.z >= t_lo * kTile && d.z < t_hi * kTile) {
-      char* tile = const_cast<char*>(tile_of(d.z >> 5));
+      char* tile = tile_in(pt, d.z >> 5);
       const int j = d.z & 31;
       if constexpr (FP8) {
         if (lane < D / 8)
@@ -623,15 +638,15 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
       // loop so the compiler's wait counts only cover the older tile).
       Frag<D> fa, fb;
       int t = t_lo;
-      load_tile<D>(fa, tile_of(t), lo);
+      load_tile<D>(fa, tile_of(t), lane);
       for (; t + 2 < full_hi; t += 2) {
-        load_tile<D>(fb, tile_of(t + 1), lo);
+        load_tile<D>(fb, tile_of(t + 1), lane);
         compute_tile<D>(acc, fa, qf, a.scale_log2, kTile, G);
-        load_tile<D>(fa, tile_of(t + 2), lo);
+        load_tile<D>(fa, tile_of(t + 2), lane);
         compute_tile<D>(acc, fb, qf, a.scale_log2, kTile, G);
       }
       if (t + 1 < full_hi) {
-        load_tile<D>(fb, tile_of(t + 1), lo);
+        load_tile<D>(fb, tile_of(t + 1), lane);
         compute_tile<D>(acc, fa, qf, a.scale_log2, kTile, G);
         compute_tile<D>(acc, fb, qf, a.scale_log2, kTile, G);
       } else {
@@ -640,7 +655,7 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
     }
     if (full_hi < t_hi) {
       Frag<D> ft;
-      load_tail<D>(ft, tile_of(full_hi), lo, L - full_hi * kTile, r, G);
+      load_tail<D>(ft, tile_of(full_hi), lane, L - full_hi * kTile, r, G);
       compute_tile<D>(acc, ft, qf, a.scale_log2, L - full_hi * kTile, G);
     }
     }
@@ -677,23 +692,38 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
           __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc.o[b]), acc_rsrc,
                                                  o + 64 * b, 0, kCachePolicySc1);
       }
-      const int4 hw = head_waves[hh];   // waves wf .. wl hold the head's tiles
-      __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-      int prev = 0;
-      if (lane == 0) prev = atomicAdd(&head_cnt[hh], seg_end - tb);
-      prev = __shfl(prev, 0, 64);
-      if (prev + (seg_end - tb) == c1 - c0) {
-        const int wf = hw.x, wl = hw.y;
-        if (wl - wf < 4)
-          merge_head_small<D>(part_ml, acc_rsrc, hw.z, out, wf, wl - wf + 1, hh, a.g, lane);
-        else
-          merge_head<D>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, a.g, lane,
-                        merge_wts[threadIdx.x >> 6]);
-        if (lane == 0) __hip_atomic_store(&head_cnt[hh], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
+      p_hh[npend] = hh;
+      p_cnt[npend] = seg_end - tb;
+      p_tot[npend] = c1 - c0;
+      ++npend;
     }
     tb = seg_end;
     ++hh;
+  }
+  // Heads shared with other waves (at most the first and the last segment):
+  // once this wave's partial stores are complete, add its tile counts to
+  // the heads' arrival counters; the wave that completes a head's count
+  // merges all its partials by log-sum-exp and writes the output.  Deferring
+  // this to the end of the range keeps the tile stream free of waits.
+  if (npend > 0) {
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    int prev = 0;
+    if (lane < npend) prev = atomicAdd(&head_cnt[lane == 0 ? p_hh[0] : p_hh[1]], lane == 0 ? p_cnt[0] : p_cnt[1]);
+    const int prev0 = __shfl(prev, 0, 64), prev1 = __shfl(prev, 1, 64);
+    const __amdgpu_buffer_rsrc_t acc_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        part_acc, static_cast<short>(0), a.part_acc_bytes, kBufferDword3);
+    for (int i = 0; i < npend; ++i) {
+      if ((i == 0 ? prev0 : prev1) + p_cnt[i] != p_tot[i]) continue;
+      const int mh = p_hh[i];
+      const int4 hw = ldc(head_waves, mh);   // waves wf .. wl hold the head's tiles
+      const int wf = hw.x, wl = hw.y;
+      if (wl - wf < 4)
+        merge_head_small<D>(part_ml, acc_rsrc, hw.z, out, wf, wl - wf + 1, mh, a.g, lane);
+      else
+        merge_head<D>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, mh, a.g, lane,
+                      merge_wts[threadIdx.x >> 6]);
+      if (lane == 0) __hip_atomic_store(&head_cnt[mh], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
 }
 
@@ -701,7 +731,7 @@ template <int D, bool FP8>
 hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
                            int layer, int n, const void* q, const void* k, const void* v, float* out,
                            int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop,
-                           const int32_t* qsel) {
+                           const int32_t* qpage) {
   char* w = static_cast<char*>(ws);
   const int32_t* status = reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status);
   const int32_t* cum = reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles);
@@ -726,7 +756,7 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
                      reinterpret_cast<const int4*>(w + lo.ws_wave_desc),
                      reinterpret_cast<const int4*>(w + lo.ws_head_waves),
                      reinterpret_cast<int32_t*>(w + lo.ws_head_cnt),
-                     layer_state(lo, meta, layer).page_table, qsel, static_cast<char*>(pool),
+                     layer_state(lo, meta, layer).page_table, qpage, static_cast<char*>(pool),
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                      static_cast<const uint16_t*>(v), part_ml, part_acc, out, a);
   hipError_t e = hipGetLastError();
@@ -739,17 +769,17 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
 hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
                          int layer, int n, const void* q, const void* k, const void* v, float* out,
                          int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop,
-                         const int32_t* qsel) {
+                         const int32_t* qpage) {
   const bool fp8 = c.kv_format == DMS_KV_FP8;
   if (c.head_dim == 128)
     return fp8 ? launch_decode_d<128, true>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st,
-                                            ev_start, ev_stop, qsel)
+                                            ev_start, ev_stop, qpage)
                : launch_decode_d<128, false>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st,
-                                             ev_start, ev_stop, qsel);
+                                             ev_start, ev_stop, qpage);
   return fp8 ? launch_decode_d<64, true>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st,
-                                         ev_start, ev_stop, qsel)
+                                         ev_start, ev_stop, qpage)
              : launch_decode_d<64, false>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st,
-                                          ev_start, ev_stop, qsel);
+                                          ev_start, ev_stop, qpage);
 }
 
 // One decode wave per SIMD (a block of 4 waves per CU).  Measured on MI355X

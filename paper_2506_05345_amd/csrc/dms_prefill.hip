@@ -50,23 +50,10 @@ typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 // LDS tile layout.  A wave's MFMA operand load -- lane (r, G) = (lane % 16,
 // lane / 16) takes 16 bytes -- is free of bank conflicts when the 64 lanes
 // read one contiguous 1 KB block in lane order (measured on gfx950; rows of
-// 64 bytes read column-wise are not).  So the tile is laid out in LDS in the
-// order the fragment loads consume it:
-//   keys, per 32-dim slice s (2 KB): two 1 KB halves, half h holding tile rows
-//     j = (r % 4) + 8 (r / 4) + 4 h for r = 0..15 (the rows of the first /
-//     second score MFMA), each as [chunk G][r][16 B];
-//   values (V^T), per block of 16 dims b (1 KB): [key chunk G][dim r][16 B].
-// Fragment loads are then base + lane * 16, and staging writes are too: each
-// thread fetches from the pool-layout tile the piece its LDS slot holds.
-__device__ inline int k_src(int P) {   // pool-layout offset of key LDS slot P
-  const int r = P & 15, c = (P >> 4) & 3, h = (P >> 6) & 1;
-  return (P >> 7) * 2048 + ((r & 3) + 8 * (r >> 2) + 4 * h) * 64 + c * 16;
-}
-template <int D>
-__device__ inline int v_src(int P) {   // pool-layout offset of value LDS slot P
-  const int r = P & 15, G = (P >> 4) & 3;
-  return D * 64 + (16 * (P >> 6) + r) * 64 + G * 16;
-}
+// 64 bytes read column-wise are not).  The pool's tile layout is already in
+// that order (dms_common.h): keys as 1 KB blocks per (32-dim slice, score
+// MFMA row set), values (V^T) as 1 KB blocks per 16 dims, lane-ordered pieces
+// inside each.  So staging copies a tile's 16-byte piece P to LDS slot P.
 
 // max over the four lanes r, r + 16, r + 32, r + 48 (the key rows of one column)
 __device__ inline float col_max(float x) {
@@ -211,7 +198,7 @@ __global__ __launch_bounds__(kThreads) void prefill_tile_kernel(PrefillArgs a) {
       kx = *reinterpret_cast<const u32x4*>(a.k + row);
       vx = *reinterpret_cast<const u32x4*>(a.v + row);
     }
-    *reinterpret_cast<u32x4*>(tile + (e0 >> 5) * 2048 + j * 64 + (e0 & 31) * 2) = kx;
+    *reinterpret_cast<u32x4*>(tile + k_elem_off(j, e0)) = kx;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       vrows[j][e0 + 2 * e] = static_cast<uint16_t>(vx[e] & 0xFFFFu);
@@ -219,14 +206,14 @@ __global__ __launch_bounds__(kThreads) void prefill_tile_kernel(PrefillArgs a) {
     }
   }
   __syncthreads();
-  // value piece q: dim q / 4, keys 8 (q % 4) .. + 7
+  // value piece q: dim q / 4, keys 8 (q % 4) .. + 7 (contiguous in the tile)
   for (int q = tid; q < kPieces; q += kThreads) {
     const int e = q >> 2, j0 = 8 * (q & 3);
     u32x4 x;
 #pragma unroll
     for (int t = 0; t < 4; ++t)
       x[t] = static_cast<uint32_t>(vrows[j0 + 2 * t][e]) | (static_cast<uint32_t>(vrows[j0 + 2 * t + 1][e]) << 16);
-    *reinterpret_cast<u32x4*>(tile + D * 64 + q * 16) = x;
+    *reinterpret_cast<u32x4*>(tile + v_elem_off(j0, e, D)) = x;
   }
 }
 
@@ -378,8 +365,8 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
       constexpr int KP = Stage<D>::kPieces / 2;
 #pragma unroll
       for (int m = 0; m < KP; ++m) {
-        stg.kx[m] = *reinterpret_cast<const u32x4*>(tile + k_src(tid + m * kThreads));
-        stg.vx[m] = *reinterpret_cast<const u32x4*>(tile + v_src<D>(tid + m * kThreads));
+        stg.kx[m] = *reinterpret_cast<const u32x4*>(tile + (tid + m * kThreads) * 16);
+        stg.vx[m] = *reinterpret_cast<const u32x4*>(tile + D * 64 + (tid + m * kThreads) * 16);
       }
     }
   };

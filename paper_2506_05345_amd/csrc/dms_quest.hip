@@ -36,6 +36,7 @@ struct QuestArgs {
   const char* pool;
   const uint16_t* q;        // [n, Hq, D] bf16
   int32_t* sel;             // [NH][B] attended page-table indices, ascending
+  int32_t* qpage;           // [NH][B] their physical pages (what decode reads)
   int32_t* qlen;            // [NH] live slots in the attended pages
   size_t page_bytes;
   int n, H, g, D, P, maxp, B, fp8, zero_neuron, all_pages;
@@ -151,8 +152,13 @@ __global__ __launch_bounds__(kQThreads) void quest_select_kernel(QuestArgs a) {
   const int npages = (L + a.P - 1) / a.P;
   const int tid = threadIdx.x;
   int32_t* sel = a.sel + static_cast<size_t>(hh) * a.B;
+  int32_t* qpage = a.qpage + static_cast<size_t>(hh) * a.B;
+  const int32_t* pt = a.st.page_table + static_cast<size_t>(sh) * a.maxp;
   if (npages <= a.B) {
-    for (int i = tid; i < a.B; i += kQThreads) sel[i] = i < npages ? i : -1;
+    for (int i = tid; i < a.B; i += kQThreads) {
+      sel[i] = i < npages ? i : -1;
+      qpage[i] = i < npages ? pt[i] : -1;
+    }
     if (tid == 0) a.qlen[hh] = L;
     return;
   }
@@ -258,7 +264,10 @@ __global__ __launch_bounds__(kQThreads) void quest_select_kernel(QuestArgs a) {
     const int f = p < npages ? chosen[p] : 0;
     int tot;
     const int off = block_exclusive_scan(f, lds, &tot);
-    if (f) sel[run + off] = p;
+    if (f) {
+      sel[run + off] = p;
+      qpage[run + off] = pt[p];
+    }
     run += tot;
   }
   if (tid == 0) a.qlen[hh] = a.B * a.P - (chosen[npages - 1] ? npages * a.P - L : 0);
@@ -285,6 +294,7 @@ QuestArgs quest_args(const dms_config& c, const Layout& lo, void* meta, void* ws
   a.status = reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status);
   a.desc = reinterpret_cast<const HeadDesc*>(w + lo.ws_head_desc);
   a.sel = reinterpret_cast<int32_t*>(w + lo.ws_q_sel);
+  a.qpage = reinterpret_cast<int32_t*>(w + lo.ws_q_page);
   a.qlen = reinterpret_cast<int32_t*>(w + lo.ws_q_len);
   a.page_bytes = lo.page_bytes;
   a.n = n;

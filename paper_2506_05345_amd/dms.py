@@ -373,10 +373,15 @@ class DmsCache:
 
 
 def unpack_page(u16, P, D):
-    """Decode one page (uint16 words, tile-major layout of dms.h) into K, V [P, D]."""
+    """Decode one page (uint16 words, fragment-ordered tiles of dms.h) into K, V [P, D]."""
     tiles = np.asarray(u16).reshape(P // 32, 2, D * 32)
-    k = tiles[:, 0].reshape(P // 32, D // 32, 32, 32).transpose(0, 2, 1, 3).reshape(P, D)
-    v = tiles[:, 1].reshape(P // 32, D, 32).transpose(0, 2, 1).reshape(P, D)
+    j = np.arange(32)[:, None]
+    e = np.arange(D)[None, :]
+    h, r = (j // 4) % 2, 4 * (j // 8) + j % 4
+    koff = ((((e // 32) * 2 + h) * 4 + (e // 8) % 4) * 16 + r) * 8 + e % 8
+    voff = (((e // 16) * 4 + j // 8) * 16 + e % 16) * 8 + j % 8
+    k = tiles[:, 0][:, koff].reshape(P, D)
+    v = tiles[:, 1][:, voff].reshape(P, D)
     return k, v
 
 

@@ -147,21 +147,45 @@ def test_error_strings():
     assert dms.dms_strerror(-99) == "unknown error code"
 
 
+def _bf16_offsets(j, e, D):
+    """Byte offsets of key and value element (j, e) in a bf16 tile (include/dms.h)."""
+    h, r = (j // 4) % 2, 4 * (j // 8) + j % 4
+    k = ((((e // 32) * 2 + h) * 4 + (e // 8) % 4) * 16 + r) * 16 + (e % 8) * 2
+    v = 64 * D + (((e // 16) * 4 + j // 8) * 16 + e % 16) * 16 + (j % 8) * 2
+    return k, v
+
+
+def test_bf16_tile_offsets_are_a_bijection():
+    # every key and value element of a tile has its own 2-byte cell, and the
+    # cells fill the 128 * D bytes exactly
+    import numpy as np
+    for D in (64, 128):
+        j = np.arange(32)[:, None]
+        e = np.arange(D)[None, :]
+        k, v = _bf16_offsets(j, e, D)
+        cells = np.concatenate([k.ravel(), v.ravel()])
+        assert (cells % 2 == 0).all()
+        assert np.array_equal(np.sort(cells), np.arange(0, 128 * D, 2))
+        # the 8 dims of one key piece (and 8 slots of one value piece) are contiguous
+        assert (np.diff(k.reshape(32, D // 8, 8), axis=2) == 2).all()
+        assert (np.diff(v.T.reshape(D, 4, 8), axis=2) == 2).all()
+
+
 def test_unpack_page_matches_documented_offsets():
-    # element (j, e) of tile t: key at (e/32)*2048 + j*64 + (e%32)*2 bytes,
-    # value at 64*D + e*64 + j*2 bytes (include/dms.h)
+    # element (j, e) of tile t at the documented key / value offsets
     import numpy as np
     P, D = 64, 128
     words = np.zeros(P * D * 2, np.uint16)
-    for s in (0, 5, 31, 32, 63):
+    for s in (0, 5, 12, 31, 32, 45, 63):
         t, j = divmod(s, 32)
-        for e in (0, 7, 31, 32, 100, 127):
+        for e in (0, 7, 9, 31, 32, 100, 127):
             base = t * 128 * D
-            words[(base + (e // 32) * 2048 + j * 64 + (e % 32) * 2) // 2] = 1000 + s * 200 + e
-            words[(base + 64 * D + e * 64 + j * 2) // 2] = 3 * (1000 + s * 200 + e)
+            ko, vo = _bf16_offsets(j, e, D)
+            words[(base + ko) // 2] = 1000 + s * 200 + e
+            words[(base + vo) // 2] = 3 * (1000 + s * 200 + e)
     k, v = dms.unpack_page(words, P, D)
-    for s in (0, 5, 31, 32, 63):
-        for e in (0, 7, 31, 32, 100, 127):
+    for s in (0, 5, 12, 31, 32, 45, 63):
+        for e in (0, 7, 9, 31, 32, 100, 127):
             assert k[s, e] == 1000 + s * 200 + e
             assert v[s, e] == 3 * (1000 + s * 200 + e)
 
