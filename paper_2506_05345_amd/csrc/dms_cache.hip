@@ -550,7 +550,13 @@ __device__ inline bool chunk_reuse(const ChunkArgs& a, int sh, int h, int tok0, 
   return (static_cast<uint32_t>(e) & kFlagBit) != 0;
 }
 
-// Pass 1 (one block per head): count fresh tokens and the pages they need.
+constexpr int kChunkTPT = 16;   // consecutive chunk tokens per thread in the scans
+
+// Pass 1 (one block per head): count fresh tokens and the pages they need,
+// and give every fresh token its slot (L0 + its index among the fresh ones;
+// the slot array is scratch, so writing it before validation is harmless).
+// Each thread takes kChunkTPT consecutive tokens (their flags are loaded
+// together), so a 4096-token chunk needs one block scan.
 __global__ __launch_bounds__(256) void chunk_count_kernel(ChunkArgs a) {
   __shared__ int lds[17];
   if (load_status(a.status) != 0) return;
@@ -566,16 +572,26 @@ __global__ __launch_bounds__(256) void chunk_count_kernel(ChunkArgs a) {
   }
   const int sh = s * a.H + h;
   const int pos0 = a.st.pos[s];
+  const int L0 = a.st.len[sh];
+  int32_t* slots = a.slots + static_cast<size_t>(tok0) * a.H + h;   // token c at c * H
   int cnt = 0;
-  for (int c0 = 0; c0 < C; c0 += blockDim.x) {
-    const int c = c0 + threadIdx.x;
-    int f = (c < C) && !chunk_reuse(a, sh, h, tok0, pos0, c);
+  for (int base = 0; base < C; base += blockDim.x * kChunkTPT) {
+    const int c0 = base + threadIdx.x * kChunkTPT;
+    bool f[kChunkTPT];
+    int mine = 0;
+#pragma unroll
+    for (int u = 0; u < kChunkTPT; ++u) {
+      f[u] = c0 + u < C && !chunk_reuse(a, sh, h, tok0, pos0, c0 + u);
+      mine += f[u];
+    }
     int tot;
-    block_exclusive_scan(f, lds, &tot);
+    int k = L0 + cnt + block_exclusive_scan(mine, lds, &tot);
+#pragma unroll
+    for (int u = 0; u < kChunkTPT; ++u)
+      if (f[u]) slots[static_cast<size_t>(c0 + u) * a.H] = k++;
     cnt += tot;
   }
   if (threadIdx.x == 0) {
-    const int L0 = a.st.len[sh];
     const int L1 = L0 + cnt;
     if (L1 > a.max_slots) atomicCAS(reinterpret_cast<int*>(a.err), 0, DMS_ERR_CAPACITY);
     a.fresh[hh] = cnt;
@@ -628,9 +644,8 @@ __global__ __launch_bounds__(kPlanThreads) void chunk_pages_kernel(ChunkArgs a) 
       a.st.pos[a.seq_ids[i]] = a.pos0[i] + (a.cu[i + 1] - a.cu[i]);
 }
 
-// Pass 3 (one block per head): slots, page table, ring, slot metadata, K/V.
+// Pass 3 (one block per head): reused slots, page table, ring, slot metadata.
 __global__ __launch_bounds__(256) void chunk_commit_kernel(ChunkArgs a) {
-  __shared__ int lds[17];
   if (load_status(a.status) != 0) return;
   const int top_before = a.err[1];
   const int hh = blockIdx.x;
@@ -641,41 +656,47 @@ __global__ __launch_bounds__(256) void chunk_commit_kernel(ChunkArgs a) {
   const int pos0 = a.pos0[i];
   const int L0 = a.st.len[sh];
   const size_t pt_base = static_cast<size_t>(sh) * a.maxp;
+  int32_t* slots = a.slots + static_cast<size_t>(tok0) * a.H + h;   // token c at c * H
   // new pages, popped in page-index order from this head's reserved range
   const int first_new_page = (L0 + a.P - 1) / a.P;
   for (int k = threadIdx.x; k < a.need[hh]; k += blockDim.x)
     a.st.page_table[pt_base + first_new_page + k] = a.st.stack[top_before - 1 - (a.base[hh] + k)];
-  // fresh slot numbers
-  int run = 0;
-  for (int c0 = 0; c0 < C; c0 += blockDim.x) {
-    const int c = c0 + threadIdx.x;
-    const int f = (c < C) && !chunk_reuse(a, sh, h, tok0, pos0, c);
-    int tot;
-    const int off = block_exclusive_scan(f, lds, &tot);
-    if (f) a.slots[static_cast<size_t>(tok0 + c) * a.H + h] = L0 + run + off;
-    run += tot;
-  }
-  __syncthreads();
-  // reused slots: follow the stride-w chain back to a fresh token or the ring
-  for (int c = threadIdx.x; c < C; c += blockDim.x) {
-    if (!chunk_reuse(a, sh, h, tok0, pos0, c)) continue;
-    int x = c;
-    while (x >= 0 && chunk_reuse(a, sh, h, tok0, pos0, x)) x -= a.w;
-    int slot;
-    if (x >= 0) {
-      slot = a.slots[static_cast<size_t>(tok0 + x) * a.H + h];
-    } else {
-      const int32_t e = a.st.ring[static_cast<size_t>(sh) * a.w + (pos0 + x) % a.w];
-      slot = static_cast<int>(static_cast<uint32_t>(e) & ~kFlagBit);
+  // Reused slots (fresh ones were assigned by pass 1).  A token that reuses
+  // takes the slot of the token w before it, so along one residue class
+  // c = r, r + w, r + 2w, ... every token holds the slot of the latest fresh
+  // token of the class before it, or, for the first ones, the slot the ring
+  // gives for position pos0 + r - w.  One forward walk per class, its flags
+  // and fresh slots loaded kChunkTPT members at a time.
+  for (int r = threadIdx.x; r < min(a.w, C); r += blockDim.x) {
+    int carried = -1;
+    if (pos0 + r >= a.w) {
+      const int32_t e = a.st.ring[static_cast<size_t>(sh) * a.w + (pos0 + r) % a.w];
+      carried = static_cast<int>(static_cast<uint32_t>(e) & ~kFlagBit);
     }
-    a.slots[static_cast<size_t>(tok0 + c) * a.H + h] = slot;
+    for (int c0 = r; c0 < C; c0 += kChunkTPT * a.w) {
+      bool ru[kChunkTPT];
+      int sl[kChunkTPT];
+#pragma unroll
+      for (int u = 0; u < kChunkTPT; ++u) {
+        const int c = c0 + u * a.w;
+        ru[u] = c < C && chunk_reuse(a, sh, h, tok0, pos0, c);
+        sl[u] = (c < C && !ru[u]) ? slots[static_cast<size_t>(c) * a.H] : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < kChunkTPT; ++u) {
+        const int c = c0 + u * a.w;
+        if (c >= C) break;
+        if (ru[u]) slots[static_cast<size_t>(c) * a.H] = carried;
+        else carried = sl[u];
+      }
+    }
   }
   __syncthreads();  // ring reads above complete before the ring is rewritten
   const int ring_from = C > a.w ? C - a.w : 0;
   for (int c = threadIdx.x; c < C; c += blockDim.x) {
     const int fl = chunk_flag(a, tok0, c, h);
     const uint32_t fb = fl ? kFlagBit : 0u;
-    const int slot = a.slots[static_cast<size_t>(tok0 + c) * a.H + h];
+    const int slot = slots[static_cast<size_t>(c) * a.H];
     if (c >= ring_from)
       a.st.ring[static_cast<size_t>(sh) * a.w + (pos0 + c) % a.w] =
           static_cast<int32_t>(static_cast<uint32_t>(slot) | fb);
@@ -686,32 +707,45 @@ __global__ __launch_bounds__(256) void chunk_commit_kernel(ChunkArgs a) {
           static_cast<int32_t>(static_cast<uint32_t>(pos0 + c) | fb);
   }
   if (threadIdx.x == 0) a.st.len[sh] = L0 + a.fresh[hh];
-  __syncthreads();  // page-table entries written above are visible to the copies below
-  // K rows and V columns of surviving tokens: D/8 consecutive lanes per token
-  // (an aligned lane group: blockDim and the loop stride are multiples of it)
+}
+
+// Pass 4 (blocks of 256 / (D/8) tokens of one head): K rows and V columns of
+// the surviving tokens into their slots, D/8 consecutive lanes per token (an
+// aligned lane group: the block size is a multiple of it, so a group is
+// entirely inside or outside the chunk and takes every branch together).
+// The page table entries of pass 3 are complete: separate launch.
+__global__ __launch_bounds__(256) void chunk_copy_kernel(ChunkArgs a) {
+  if (load_status(a.status) != 0) return;
+  const int hh = blockIdx.y;
+  const int i = hh / a.H, h = hh % a.H;
+  const int tok0 = a.cu[i], C = a.cu[i + 1] - a.cu[i];
   const int kq = a.D / 8;
-  for (int idx = threadIdx.x; idx < C * kq; idx += blockDim.x) {
-    const int c = idx / kq, part = idx % kq;
-    if (!((c + a.w >= C) || !chunk_reuse(a, sh, h, tok0, pos0, c + a.w))) continue;
-    const int slot = a.slots[static_cast<size_t>(tok0 + c) * a.H + h];
-    const int page = a.st.page_table[pt_base + slot / a.P];
-    const int row = slot % a.P;
-    const int j = row & 31;
-    const size_t src = (static_cast<size_t>(tok0 + c) * a.H + h) * a.D;
-    if (a.fp8) {
-      // the whole group takes this branch together (same token, same test)
-      char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * fp8_tile_bytes(a.D);
-      fp8_store_token(tile, j, a.D, part, reinterpret_cast<const uint4*>(a.k + src)[part],
-                      reinterpret_cast<const uint4*>(a.v + src)[part]);
-      continue;
-    }
-    char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * tile_bytes(a.D);
-    *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * part)) =
-        reinterpret_cast<const uint4*>(a.k + src)[part];
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      *reinterpret_cast<uint16_t*>(tile + v_elem_off(j, part * 8 + e, a.D)) = a.v[src + part * 8 + e];
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= C * kq) return;
+  const int c = idx / kq, part = idx % kq;
+  const int s = a.seq_ids[i];
+  const int sh = s * a.H + h;
+  const int pos0 = a.pos0[i];
+  if (!((c + a.w >= C) || !chunk_reuse(a, sh, h, tok0, pos0, c + a.w))) return;
+  const int slot = a.slots[static_cast<size_t>(tok0 + c) * a.H + h];
+  const int page = a.st.page_table[static_cast<size_t>(sh) * a.maxp + slot / a.P];
+  const int row = slot % a.P;
+  const int j = row & 31;
+  const size_t src = (static_cast<size_t>(tok0 + c) * a.H + h) * a.D;
+  const uint4 kx = reinterpret_cast<const uint4*>(a.k + src)[part];
+  const uint4 vx = reinterpret_cast<const uint4*>(a.v + src)[part];
+  if (a.fp8) {
+    char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * fp8_tile_bytes(a.D);
+    fp8_store_token(tile, j, a.D, part, kx, vx);
+    return;
   }
+  char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * tile_bytes(a.D);
+  *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * part)) = kx;
+  const uint32_t vw[4] = {vx.x, vx.y, vx.z, vx.w};
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    *reinterpret_cast<uint16_t*>(tile + v_elem_off(j, part * 8 + e, a.D)) =
+        static_cast<uint16_t>(vw[e >> 1] >> (16 * (e & 1)));
 }
 
 }  // namespace
@@ -880,6 +914,11 @@ hipError_t launch_chunk_commit(const dms_config& c, const Layout& lo, void* meta
   hipLaunchKernelGGL(chunk_count_kernel, dim3(NH), dim3(256), 0, st, a);
   hipLaunchKernelGGL(chunk_pages_kernel, dim3(1), dim3(kPlanThreads), 0, st, a);
   hipLaunchKernelGGL(chunk_commit_kernel, dim3(NH), dim3(256), 0, st, a);
+  if (max_len > 0) {
+    const int per_block = 256 / (c.head_dim / 8);   // tokens per copy block
+    hipLaunchKernelGGL(chunk_copy_kernel, dim3((max_len + per_block - 1) / per_block, NH), dim3(256), 0,
+                       st, a);
+  }
   return hipGetLastError();
 }
 
