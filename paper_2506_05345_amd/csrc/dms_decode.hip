@@ -608,18 +608,30 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
     if constexpr (FP8) {
       if (t_lo < full_hi) {
         // two register sets, as for bf16 (a third set, keeping two FP8 tiles
-        // in flight, measured slower: 235 vs 217 us at the 32B-shaped step)
+        // in flight, measured slower)
         FragF8<D> fa, fb;
+        // the next tile's address is formed a tile ahead and a scheduling
+        // barrier keeps its loads ahead of this tile's waits (1.5% faster
+        // than leaving the order to the compiler, which waited for part of
+        // the current tile first)
         int t = t_lo;
+        const int last = full_hi - 1;
         load_tile_f8<D>(fa, tile_of(t), lane, G);
+        __builtin_amdgcn_sched_barrier(0);
+        const char* pb = tile_of(min(t + 1, last));
         for (; t + 2 < full_hi; t += 2) {
-          load_tile_f8<D>(fb, tile_of(t + 1), lane, G);
+          load_tile_f8<D>(fb, pb, lane, G);
+          __builtin_amdgcn_sched_barrier(0);
+          const char* pa = tile_of(t + 2);
           compute_tile_f8<D>(acc, fa, qf, a.scale_log2, kTile, G);
-          load_tile_f8<D>(fa, tile_of(t + 2), lane, G);
+          load_tile_f8<D>(fa, pa, lane, G);
+          __builtin_amdgcn_sched_barrier(0);
+          pb = tile_of(min(t + 3, last));
           compute_tile_f8<D>(acc, fb, qf, a.scale_log2, kTile, G);
         }
         if (t + 1 < full_hi) {
-          load_tile_f8<D>(fb, tile_of(t + 1), lane, G);
+          load_tile_f8<D>(fb, pb, lane, G);
+          __builtin_amdgcn_sched_barrier(0);
           compute_tile_f8<D>(acc, fa, qf, a.scale_log2, kTile, G);
           compute_tile_f8<D>(acc, fb, qf, a.scale_log2, kTile, G);
         } else {
