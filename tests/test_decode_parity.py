@@ -281,3 +281,36 @@ def test_merge_ignores_stale_workspace(lens):
     orc = _oracle_for(cfg)
     _append_chunks(dms, cache, orc, seqs, inp, {s: 0 for s in seqs}, ln, 300)
     _decode_steps(dms, cache, orc, seqs, inp, ln, 8, 3, check_every=4)
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+def test_long_heads_split_over_hundreds_of_waves(fmt):
+    """Two heads of ~24K retained tokens each: ~1500 tiles over the 1024 decode
+    waves, so every head is split over hundreds of waves and its merge runs
+    the batched path over several batches of 64 partials, at the end of the
+    waves that complete it.  Flags mostly 0 so the heads stay long.  Pools and
+    workspace start as NaN bytes, so a stale partial or slot would show."""
+    torch = _torch()
+    from paper_2506_05345_amd import dms as dmsmod
+    H, g, d, w, P = 2, 4, 128, 64, 64
+    T = 26000
+    kw = dict(num_layers=1, max_seqs=1, num_kv_heads=H, group_size=g, head_dim=d, window=w,
+              page_size=P, num_pages=2 * (T // P + 8), max_pages_per_head=T // P + 8,
+              max_chunk_tokens=4096)
+    if fmt == "fp8":
+        kw["kv_format"] = dmsmod.DMS_KV_FP8
+    dms, cfg, cache = _mk(kw)
+    for p in cache.pools:
+        p.fill_(0xFF)
+    cache.workspace.fill_(0xFF)
+    dms.dms_init_state(cache.ctx)
+    torch.cuda.synchronize()
+    inp = {0: SeqInputs(29, 0, 0, T + 4, H, g, d, 0.05)}
+    orc = PagedKVOracle(cfg.max_seqs, H, w, P, cfg.num_pages, cfg.max_pages_per_head, d,
+                        kv_format=fmt)
+    _append_chunks(dms, cache, orc, [0], inp, {0: 0}, {0: T}, 4096)
+    view = cache.export(0)
+    assert view.L[0].min() > 20000
+    compare_state(view, orc, [0])
+    _decode_steps(dms, cache, orc, [0], inp, {0: T}, 3, g, dense_check=False)
+    cache.close()
