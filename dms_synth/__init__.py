@@ -162,6 +162,15 @@ def token_vectors_np(seed, stream, layer, seq, head, pos, dim) -> np.ndarray:
     return normal_bf16_bits_np(seed, stream, idx)
 
 
+def wide_coords(head, dim, width):
+    """Coordinates of element ``dim`` of a vector of ``width`` > 256 elements
+    (rows of a latent-attention cache, 576 wide): the dim field holds 8 bits,
+    so the vector is split into ceil(width / 256) sub-heads.  Works on ints,
+    NumPy arrays and torch tensors; returns (head, dim) for the generators."""
+    nsub = -(-width // (1 << DIM_BITS))
+    return head * nsub + dim // (1 << DIM_BITS), dim % (1 << DIM_BITS)
+
+
 def head_sequence_np(seed, stream, layer, seq, head, positions, head_dim) -> np.ndarray:
     """[len(positions), head_dim] bf16 bits of one head's vectors at the given positions."""
     pos = np.asarray(positions, np.uint64)[:, None]

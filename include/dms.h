@@ -82,7 +82,7 @@ typedef struct dms_config {
   int32_t max_seqs;           /* sequence ids are 0 .. max_seqs-1 (<= 65536) */
   int32_t num_kv_heads;       /* Hkv >= 1 */
   int32_t group_size;         /* g = Hq / Hkv, 1 .. 16 */
-  int32_t head_dim;           /* d: 64 or 128 */
+  int32_t head_dim;           /* d: 64 or 128 (576 for DMS_KV_MLA) */
   int32_t window;             /* w >= 1: eviction delay = sliding window */
   int32_t page_size;          /* P tokens per page: 32, 64, 128 or 256 */
   int32_t num_pages;          /* pages in each layer's pool */
@@ -94,8 +94,8 @@ typedef struct dms_config {
   int32_t decision_source;    /* DMS_DECIDE_CALLER (0) or DMS_DECIDE_QUERY (1) */
   float decision_bias;        /* b added to the borrowed neuron (DMS_DECIDE_QUERY);
                                  -5 is the paper's training offset */
-  int32_t kv_format;          /* DMS_KV_BF16 (0) or DMS_KV_FP8 (1): how retained
-                                 K / V rows are stored in the page pools */
+  int32_t kv_format;          /* DMS_KV_BF16 (0), DMS_KV_FP8 (1) or DMS_KV_MLA (2):
+                                 how retained rows are stored in the page pools */
   int32_t quest_page_budget;  /* 0: decode attends every retained slot; B > 0:
                                  decode attends the B pages of each head that
                                  Quest's bound ranks highest (see below) */
@@ -138,8 +138,23 @@ enum { DMS_EVICT_DELAYED = 0, DMS_EVICT_IMMEDIATE = 1 };
  *     d = 128), roughly halving the bytes decode reads.  Every key and value
  *     is attended in its stored form, including the token a decode step
  *     appends and the chunk's own tokens in a prefill call.
+ *   DMS_KV_MLA: a multi-head latent attention cache, the direction the paper
+ *     names for future work (Sec. 6).  Each token caches one bf16 row of
+ *     d = 576 shared by all query heads: the compressed latent (dims
+ *     0 .. 511) then the decoupled rotary key (dims 512 .. 575).  The cache
+ *     is one KV head (num_kv_heads = 1) whose group is every query head
+ *     (group_size <= 16), and DMS evicts its rows by the same rule.  Decode
+ *     works in the absorbed form: q (per query head, 576 dims) is the query
+ *     already mapped into the latent space followed by its rotary part; a
+ *     head scores row j by q . row_j over all 576 dims and its output is the
+ *     softmax-weighted sum of the rows' latent dims, so `out` holds
+ *     [n][group_size][512] float32 (the up-projection of values is the
+ *     caller's).  The `v` arguments are ignored (may be NULL).  Requires
+ *     decision_source = DMS_DECIDE_CALLER and quest_page_budget = 0;
+ *     dms_prefill_chunk and dms_prefill_chunk_q return DMS_ERR_UNSUPPORTED
+ *     (chunks are appended with dms_append_chunk).
  */
-enum { DMS_KV_BF16 = 0, DMS_KV_FP8 = 1 };
+enum { DMS_KV_BF16 = 0, DMS_KV_FP8 = 1, DMS_KV_MLA = 2 };
 
 /*
  * Page retrieval within the retained set (dms_config.quest_page_budget).  The
@@ -205,6 +220,9 @@ typedef struct dms_state_offsets {
  *                        + 8 * ((e / 16) % 2) + j % 8
  *   key scale of row j (float32)   at 64 * d + (j / 8) * 64 + (j % 8) * 4
  *   value scale of row j (float32) at 64 * d + (j / 8) * 64 + 32 + (j % 8) * 4
+ * DMS_KV_MLA: page_bytes = 2 * P * d (d = 576); a page is P/32 tiles of
+ *   64 * d bytes holding the rows only, element (j, e) at the DMS_KV_BF16
+ *   key offset above.
  */
 
 /* Sizes of the caller-owned buffers for `cfg`.  Host only; validates cfg.
@@ -254,7 +272,8 @@ int dms_append(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
  * visible to the latest position (decode reads only retained tokens; the
  * cost is the KV bytes read, Sec. 1 and Appendix I).  Split over the
  * retained tokens of all heads, merged by log-sum-exp.
- * q_dev: bf16 [n, Hq, d]; out_dev: float32 [n, Hq, d]. */
+ * q_dev: bf16 [n, Hq, d]; out_dev: float32 [n, Hq, d] ([n, Hq, 512] for
+ * DMS_KV_MLA). */
 int dms_decode(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
                const void* q_dev, float* out_dev, void* stream);
 

@@ -41,6 +41,18 @@ notes):
 * A call that would pop more pages than the stack holds fails as a whole
   (OutOfPages) and changes nothing.
 
+Latent attention (MLA; the paper names it as a direction for DMS, Sec. 6,
+without a scheme).  Reading: an MLA layer caches one row per token shared by
+all query heads -- the compressed latent c_t followed by the decoupled rotary
+key -- so DMS treats it as a single KV head whose group is every query head
+and evicts rows by the same rule.  Decode is the absorbed form of
+DeepSeek-V2's attention: the query arrives already mapped into the latent
+space (W_UK^T q_nope) and followed by its rotary part; a head scores row j
+by q . row_j over the full row and outputs the softmax-weighted sum of the
+rows' latent parts (W_UV is applied afterwards by the model).  ``mla_attention``
+writes that out; the tests pin it to the non-absorbed form with explicit
+per-head keys [W_UK c_j ; k_rope_j] and values W_UV c_j.
+
 Decisions at inference and the eviction-timing ablation:
 
 * Sec. 3.2 rounds the decision to alpha_bin = round(sigmoid(logit)).  The
@@ -67,7 +79,7 @@ __all__ = [
     "visible", "visible_immediate", "visibility_mask", "additive_mask", "retained_count",
     "alpha_bin", "query_decisions", "zero_borrowed_neuron",
     "masked_attention", "dense_dms_attention", "dense_dms_attention_head",
-    "OutOfPages", "PagedKVOracle",
+    "mla_attention", "OutOfPages", "PagedKVOracle",
 ]
 
 
@@ -180,6 +192,17 @@ def masked_attention(q, k, v, mask, scale) -> np.ndarray:
     m = s.max(axis=1, keepdims=True)
     p = np.where(mask, np.exp(s - m), 0.0)
     return (p @ v) / p.sum(axis=1, keepdims=True)
+
+
+def mla_attention(q, rows, mask, latent, scale) -> np.ndarray:
+    """Absorbed-form latent attention, float64: softmax(scale * q rows^T
+    restricted to mask) rows[:, :latent].
+
+    q [Tq, d] (latent-space query then rotary query), rows [Tk, d] (latent
+    then rotary key), mask bool [Tq, Tk].  Returns [Tq, latent].
+    """
+    rows = np.asarray(rows, np.float64)
+    return masked_attention(q, rows, rows[:, :latent], mask, scale)
 
 
 def dense_dms_attention_head(q_rows, k_hist, v_hist, flags_hist, w, t_query, scale=None,
@@ -423,6 +446,19 @@ class PagedKVOracle:
         k = self.k_store[s, h, :n]
         v = self.v_store[s, h, :n]
         return masked_attention(q, k, v, np.ones((q.shape[0], n), bool), scale)
+
+    def decode_latent(self, seq_ids, q, latent, scale=None):
+        """Latent-attention decode (one KV head holding the rows, every query
+        head in its group): q [n, Hq, d] -> [n, Hq, latent]."""
+        q = np.asarray(q, np.float64)
+        n, Hq, d = q.shape
+        if scale is None:
+            scale = 1.0 / math.sqrt(d)
+        out = np.empty((n, Hq, latent))
+        for i, s in enumerate(seq_ids):
+            L = int(self.L[s, 0])
+            out[i] = mla_attention(q[i], self.k_store[s, 0, :L], np.ones((Hq, L), bool), latent, scale)
+        return out
 
     def decode(self, seq_ids, q, group, scale=None):
         """q [n, Hq, d] -> [n, Hq, d]: each query head over its KV head's live slots."""

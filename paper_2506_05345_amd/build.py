@@ -10,8 +10,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdms.so")
-SOURCES = ["dms_api.hip", "dms_cache.hip", "dms_decode.hip", "dms_prefill.hip", "dms_quest.hip",
-           "dms_train.hip"]
+SOURCES = ["dms_api.hip", "dms_cache.hip", "dms_decode.hip", "dms_mla.hip", "dms_prefill.hip",
+           "dms_quest.hip", "dms_train.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 instructions are kept out of every kernel.

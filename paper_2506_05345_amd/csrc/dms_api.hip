@@ -17,7 +17,17 @@ int validate_config(const dms_config& c) {
   if (c.num_kv_heads < 1 || c.group_size < 1 || c.window < 1) return DMS_ERR_INVALID;
   if (c.group_size > kMaxGroup) return DMS_ERR_UNSUPPORTED;
   if (c.head_dim < 1) return DMS_ERR_INVALID;
-  if (c.head_dim != 64 && c.head_dim != 128) return DMS_ERR_UNSUPPORTED;
+  if (c.kv_format == DMS_KV_MLA) {
+    // latent rows: one KV head, caller decisions, no page retrieval
+    if (c.head_dim != kMlaDim) return DMS_ERR_UNSUPPORTED;
+    if (c.num_kv_heads != 1 || c.decision_source != DMS_DECIDE_CALLER || c.quest_page_budget != 0)
+      return DMS_ERR_UNSUPPORTED;
+    // split partials are addressed with 32-bit byte offsets
+    if (static_cast<int64_t>(kMaxWaves + c.max_seqs) * c.group_size * kMlaLatent * 4 >= (int64_t(1) << 31))
+      return DMS_ERR_UNSUPPORTED;
+  } else if (c.head_dim != 64 && c.head_dim != 128) {
+    return DMS_ERR_UNSUPPORTED;
+  }
   if (c.page_size != 32 && c.page_size != 64 && c.page_size != 128 && c.page_size != 256)
     return DMS_ERR_INVALID;
   if (c.num_pages < 1 || c.max_pages_per_head < 1 || c.max_chunk_tokens < 0) return DMS_ERR_INVALID;
@@ -27,7 +37,8 @@ int validate_config(const dms_config& c) {
   if (c.decision_source != DMS_DECIDE_CALLER && c.decision_source != DMS_DECIDE_QUERY)
     return DMS_ERR_INVALID;
   if (c.decision_source == DMS_DECIDE_QUERY && !isfinite(c.decision_bias)) return DMS_ERR_INVALID;
-  if (c.kv_format != DMS_KV_BF16 && c.kv_format != DMS_KV_FP8) return DMS_ERR_INVALID;
+  if (c.kv_format != DMS_KV_BF16 && c.kv_format != DMS_KV_FP8 && c.kv_format != DMS_KV_MLA)
+    return DMS_ERR_INVALID;
   if (c.quest_page_budget < 0 || c.quest_page_budget > c.max_pages_per_head) return DMS_ERR_INVALID;
   if (c.quest_page_budget > 0 && c.max_pages_per_head > 4096) return DMS_ERR_UNSUPPORTED;
   // slot and page indices are int32 on the device
@@ -60,8 +71,9 @@ Layout make_layout(const dms_config& c) {
   lo.layer_stride = off;
   lo.meta_bytes = lo.layer0 + lo.layer_stride * c.num_layers;
   // pool
-  lo.page_bytes = c.kv_format == DMS_KV_FP8 ? P / 32 * fp8_tile_bytes(static_cast<int>(D))
-                                             : 2 * P * D * 2;
+  lo.page_bytes = c.kv_format == DMS_KV_FP8   ? P / 32 * fp8_tile_bytes(static_cast<int>(D))
+                  : c.kv_format == DMS_KV_MLA ? P / 32 * mla_tile_bytes(static_cast<int>(D))
+                                              : 2 * P * D * 2;
   lo.pool_bytes = lo.page_bytes * static_cast<size_t>(c.num_pages);
   // workspace
   off = 0;
@@ -69,7 +81,8 @@ Layout make_layout(const dms_config& c) {
   lo.ws_head_desc = take(NH * sizeof(HeadDesc));
   lo.ws_cum_tiles = take((NH + 1) * 4);
   lo.ws_part_ml = take(NP * kMaxGroup * 8);
-  lo.ws_part_acc = take(NP * c.group_size * D * 4);
+  const size_t Dout = c.kv_format == DMS_KV_MLA ? kMlaLatent : D;   // output row width
+  lo.ws_part_acc = take(NP * c.group_size * Dout * 4);
   lo.ws_wave_bounds = take((kMaxWaves + 1) * 4);
   lo.ws_wave_desc = take(kMaxWaves * 2 * sizeof(int4));   // per decode wave: first segment
   lo.ws_head_waves = take(NH * sizeof(int4));              // per head: waves holding its tiles
@@ -84,7 +97,10 @@ Layout make_layout(const dms_config& c) {
   lo.ws_pf_meta = take(static_cast<size_t>(c.max_chunk_tokens) * H * 4);
   // prefill: chunk keys / values and the compacted kept ones, in the pool's
   // tile layout; sequence i of a call starts at tile cu[i] / 32 + i
-  lo.pf_tiles_per_head = static_cast<int>((static_cast<size_t>(c.max_chunk_tokens) + 31) / 32 + S + 1);
+  // (no chunk attention over latent rows)
+  lo.pf_tiles_per_head = c.kv_format == DMS_KV_MLA
+                             ? 0
+                             : static_cast<int>((static_cast<size_t>(c.max_chunk_tokens) + 31) / 32 + S + 1);
   lo.ws_pf_tiles = take(2 * H * static_cast<size_t>(lo.pf_tiles_per_head) * D * 128);
   lo.ws_pf_flags = take(static_cast<size_t>(c.max_chunk_tokens) * H);  // decisions from q
   lo.ws_q_sel = take(NH * static_cast<size_t>(c.quest_page_budget) * 4);
@@ -121,6 +137,9 @@ namespace {
 inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
 inline int hip_rc(hipError_t e) { return e == hipSuccess ? DMS_OK : DMS_ERR_HIP; }
+
+// Latent-attention cache: keys only (the values are part of the key row).
+inline bool mla(const dms_ctx* ctx) { return ctx->c.cfg.kv_format == DMS_KV_MLA; }
 
 // Event pair for the next timed launch of a session (or nulls).
 void next_events(Ctx& c, int kind, hipEvent_t* a, hipEvent_t* b) {
@@ -250,7 +269,7 @@ int dms_append(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const
                const void* v_dev, const uint8_t* flags_dev, void* stream) {
   int rc = check_call(ctx, layer, n, seq_ids_dev);
   if (rc) return rc;
-  if (!k_dev || !v_dev || !flags_dev) return DMS_ERR_INVALID;
+  if (!k_dev || !(v_dev || mla(ctx)) || !flags_dev) return DMS_ERR_INVALID;
   const Ctx& c = ctx->c;
   hipStream_t st = as_stream(stream);
   hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, flags_dev,
@@ -372,7 +391,7 @@ int dms_decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, 
   int rc = check_call(ctx, layer, n, seq_ids_dev);
   if (rc) return rc;
   if (ctx->c.cfg.decision_source != DMS_DECIDE_CALLER) return DMS_ERR_INVALID;
-  if (!q_dev || !k_dev || !v_dev || !flags_dev || !out_dev) return DMS_ERR_INVALID;
+  if (!q_dev || !k_dev || !(v_dev || mla(ctx)) || !flags_dev || !out_dev) return DMS_ERR_INVALID;
   if ((rc = ensure_waves(ctx))) return rc;
   return decode_step(ctx, layer, n, seq_ids_dev, q_dev, k_dev, v_dev, flags_dev, nullptr, out_dev,
                      stream);
@@ -398,7 +417,7 @@ int dms_append_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
   if (rc) return rc;
   if ((rc = check_chunk(ctx, cu_seqlens_dev, total_tokens, max_seqlen))) return rc;
   if (total_tokens == 0) return DMS_OK;
-  if (!k_dev || !v_dev || !flags_dev) return DMS_ERR_INVALID;
+  if (!k_dev || !(v_dev || mla(ctx)) || !flags_dev) return DMS_ERR_INVALID;
   const Ctx& c = ctx->c;
   hipStream_t st = as_stream(stream);
   hipError_t e = dms::launch_chunk_commit(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n,
@@ -426,6 +445,7 @@ int dms_prefill_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev
                       const uint8_t* flags_dev, float* out_dev, void* stream) {
   int rc = check_call(ctx, layer, n, seq_ids_dev);
   if (rc) return rc;
+  if (mla(ctx)) return DMS_ERR_UNSUPPORTED;
   if (ctx->c.cfg.decision_source != DMS_DECIDE_CALLER) return DMS_ERR_INVALID;
   if ((rc = check_chunk(ctx, cu_seqlens_dev, total_tokens, max_seqlen))) return rc;
   if (total_tokens == 0) return DMS_OK;
@@ -440,6 +460,7 @@ int dms_prefill_chunk_q(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_d
                         uint8_t* decisions_out_dev, float* out_dev, void* stream) {
   int rc = check_call(ctx, layer, n, seq_ids_dev);
   if (rc) return rc;
+  if (mla(ctx)) return DMS_ERR_UNSUPPORTED;
   if (ctx->c.cfg.decision_source != DMS_DECIDE_QUERY) return DMS_ERR_INVALID;
   if ((rc = check_chunk(ctx, cu_seqlens_dev, total_tokens, max_seqlen))) return rc;
   if (total_tokens == 0) return DMS_OK;

@@ -464,6 +464,7 @@ struct ScatterArgs {
   size_t page_bytes;
   int D, P, maxp;
   int fp8;   // FP8 pages: rows are quantized on the way in
+  int mla;   // latent-attention pages: the key row only
 };
 
 __global__ __launch_bounds__(64) void scatter_kernel(ScatterArgs a) {
@@ -480,6 +481,13 @@ __global__ __launch_bounds__(64) void scatter_kernel(ScatterArgs a) {
     if (lane < a.D / 8)
       fp8_store_token(tile, j, a.D, lane, reinterpret_cast<const uint4*>(a.k + static_cast<size_t>(hh) * a.D)[lane],
                       reinterpret_cast<const uint4*>(a.v + static_cast<size_t>(hh) * a.D)[lane]);
+    return;
+  }
+  if (a.mla) {
+    char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * mla_tile_bytes(a.D);
+    for (int part = lane; part < a.D / 8; part += 64)
+      *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * part)) =
+          reinterpret_cast<const uint4*>(a.k + static_cast<size_t>(hh) * a.D)[part];
     return;
   }
   char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * tile_bytes(a.D);
@@ -532,6 +540,7 @@ struct ChunkArgs {
   int n, H, w, P, D, maxp, max_slots, max_seqs, total, max_len;
   int immediate;          // eviction timing (see chunk_reuse)
   int fp8;                // FP8 pages: rows are quantized on the way in
+  int mla;                // latent-attention pages: the key row only
 };
 
 __device__ inline int chunk_flag(const ChunkArgs& a, int tok0, int c, int h) {
@@ -733,6 +742,11 @@ __global__ __launch_bounds__(256) void chunk_copy_kernel(ChunkArgs a) {
   const int j = row & 31;
   const size_t src = (static_cast<size_t>(tok0 + c) * a.H + h) * a.D;
   const uint4 kx = reinterpret_cast<const uint4*>(a.k + src)[part];
+  if (a.mla) {
+    char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * mla_tile_bytes(a.D);
+    *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * part)) = kx;
+    return;
+  }
   const uint4 vx = reinterpret_cast<const uint4*>(a.v + src)[part];
   if (a.fp8) {
     char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * fp8_tile_bytes(a.D);
@@ -823,7 +837,9 @@ hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* 
   a.head_waves = reinterpret_cast<int4*>(static_cast<char*>(ws) + lo.ws_head_waves);
   a.out = out;
   a.W = waves;
-  a.gD = c.group_size * c.head_dim;
+  // output row of a call head: g query heads of head_dim (of the latent width
+  // for a latent-attention cache)
+  a.gD = c.group_size * (c.kv_format == DMS_KV_MLA ? kMlaLatent : c.head_dim);
   a.st = layer_state(lo, meta, layer);
   a.status = reinterpret_cast<int32_t*>(static_cast<char*>(meta) + lo.status);
   a.seq_ids = seq_ids;
@@ -860,6 +876,7 @@ hipError_t launch_scatter(const dms_config& c, const Layout& lo, void* meta, voi
   a.P = c.page_size;
   a.maxp = c.max_pages_per_head;
   a.fp8 = c.kv_format == DMS_KV_FP8;
+  a.mla = c.kv_format == DMS_KV_MLA;
   hipLaunchKernelGGL(scatter_kernel, dim3(n * c.num_kv_heads), dim3(64), 0, st, a);
   return hipGetLastError();
 }
@@ -910,6 +927,7 @@ hipError_t launch_chunk_commit(const dms_config& c, const Layout& lo, void* meta
   a.max_len = max_len;
   a.immediate = c.eviction == DMS_EVICT_IMMEDIATE;
   a.fp8 = c.kv_format == DMS_KV_FP8;
+  a.mla = c.kv_format == DMS_KV_MLA;
   const int NH = n * c.num_kv_heads;
   hipLaunchKernelGGL(chunk_count_kernel, dim3(NH), dim3(256), 0, st, a);
   hipLaunchKernelGGL(chunk_pages_kernel, dim3(1), dim3(kPlanThreads), 0, st, a);

@@ -13,6 +13,8 @@ namespace dms {
 constexpr int kTile = 32;            // tokens per decode tile (k of one PV MFMA)
 constexpr int kMaxWaves = 8192;      // upper bound on decode waves (workspace sizing)
 constexpr int kMaxGroup = 16;        // query heads per KV head (MFMA column count)
+constexpr int kMlaDim = 576;         // latent attention row: 512 latent + 64 rotary key dims
+constexpr int kMlaLatent = 512;      // of which the latent (the values)
 constexpr int kMaxSeqs = 65536;      // sequence-id bitmap of the planning kernel
 constexpr uint32_t kFlagBit = 0x80000000u;
 constexpr int kAlign = 256;
@@ -81,6 +83,9 @@ inline LayerState layer_state(const Layout& lo, void* meta, int layer) {
 // Every load instruction of a decode wave then reads one contiguous 1 KB with
 // lane l taking bytes 16 l .. 16 l + 15.
 __host__ __device__ inline size_t tile_bytes(int D) { return static_cast<size_t>(D) * 128; }
+// Latent-attention pages: a 32-slot tile holds only the key part (the values
+// are the first kMlaLatent dims of each row), in the same fragment order.
+__host__ __device__ inline size_t mla_tile_bytes(int D) { return static_cast<size_t>(D) * 64; }
 __host__ __device__ inline size_t k_elem_off(int j, int e) {
   return (static_cast<size_t>(((e >> 5) * 2 + ((j >> 2) & 1)) * 4 + ((e >> 3) & 3)) * 16 +
           4 * (j >> 3) + (j & 3)) * 16 + (e & 7) * 2;
@@ -217,6 +222,13 @@ hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void
                          const void* v, float* out, int waves, hipStream_t st,
                          hipEvent_t ev_start, hipEvent_t ev_stop, const int32_t* qpage = nullptr);
 int decode_resident_waves(const dms_config& c);
+// Decode over a latent-attention cache (kv_format DMS_KV_MLA): rows of
+// kMlaDim bf16, outputs [n, g, kMlaLatent] float32.
+hipError_t launch_decode_mla(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                             void* pool, int layer, int n, const void* q, const void* k,
+                             float* out, int waves, hipStream_t st, hipEvent_t ev_start,
+                             hipEvent_t ev_stop);
+int decode_mla_resident_waves();
 hipError_t launch_retained(const dms_config& c, const Layout& lo, void* meta, int layer, int n,
                            const int32_t* seq_ids, int32_t* out, hipStream_t st);
 hipError_t launch_chunk_commit(const dms_config& c, const Layout& lo, void* meta, void* ws,

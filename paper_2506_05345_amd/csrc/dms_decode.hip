@@ -782,6 +782,8 @@ hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void
                          int layer, int n, const void* q, const void* k, const void* v, float* out,
                          int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop,
                          const int32_t* qpage) {
+  if (c.kv_format == DMS_KV_MLA)
+    return launch_decode_mla(c, lo, meta, ws, pool, layer, n, q, k, out, waves, st, ev_start, ev_stop);
   const bool fp8 = c.kv_format == DMS_KV_FP8;
   if (c.head_dim == 128)
     return fp8 ? launch_decode_d<128, true>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st,
@@ -799,6 +801,7 @@ hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void
 // heads to merge, same bandwidth); the launch must fit entirely, so the
 // occupancy of the kernel is checked.
 int decode_resident_waves(const dms_config& c) {
+  if (c.kv_format == DMS_KV_MLA) return decode_mla_resident_waves();
   int dev = 0, cus = 0, blocks = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -1;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;

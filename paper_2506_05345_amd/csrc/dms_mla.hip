@@ -1,0 +1,463 @@
+// DMS decode over a multi-head latent attention (MLA) cache, gfx950.
+//
+// The paper names MLA (DeepSeek-V2) as a direction for DMS (Sec. 6) without
+// a scheme.  Reading taken here: an MLA layer caches, per token, one row
+// shared by all query heads -- the compressed latent c_t (512 dims) followed
+// by the decoupled rotary key (64 dims) -- so it is one KV head with
+// g = all query heads.  DMS gives that row one decision per token and evicts
+// it by the same delayed rule (Sec. 3.1), so the bookkeeping (planner, slots,
+// pages, chunk commit) is the standard path's with Hkv = 1.  Decode works in
+// the absorbed form: with the query already multiplied into the latent space
+// (q~ = W_UK^T q_nope, 512 dims) and its rotary part (64 dims), a head scores
+// a row by q . row over all 576 dims and its output is the softmax-weighted
+// sum of the rows' first 512 dims (the latent; W_UV is applied by the caller).
+//
+// The kernel follows decode_kernel (dms_decode.hip): the planner's equal
+// tile ranges per wave, one wave per SIMD, split heads merged by the wave
+// that completes them at the end of its range.  Per 32-slot tile:
+//  * keys: the row is stored in the fragment order of the 16x16x32 score
+//    MFMA (A operand: tile rows, k = 32 dims); the tile is read in two halves
+//    of 16 rows, half h holding slots 8(r/4) + r%4 + 4h, with the next half's
+//    loads always in flight while the current one is computed;
+//  * values: the 16x16x32 PV MFMA needs, per lane, 8 consecutive slots of one
+//    latent dim -- the transpose of how the rows arrive.  Each wave writes the
+//    latent part of its tile to its own LDS area as [dim][slot] (2-byte
+//    stores) and reads the V^T operands back as 16-byte pieces;
+//  * the two score halves of a lane hold slots 8G .. 8G+3 and 8G+4 .. 8G+7,
+//    exactly the k slice of the PV B operand, so probabilities stay in
+//    registers (as in the standard kernel).
+#include "dms_common.h"
+
+namespace dms {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
+
+constexpr int kWavesPerBlock = 4;
+constexpr int kD = kMlaDim;             // row: latent + rotary key
+constexpr int kDv = kMlaLatent;         // latent (value) dims
+constexpr int kKBlocks = kD / 32;       // 32-dim k-steps of the score MFMA (18)
+constexpr int kLBlocks = kDv / 32;      // of them latent (16)
+constexpr int kOBlocks = kDv / 16;      // 16-dim row blocks of O^T (32)
+constexpr int kVtStride = 72;           // LDS bytes per latent dim: 32 slots + pad
+constexpr float kRescale = 8.0f;        // lazy rescale threshold, log2 units
+constexpr int kMergeWidth = 4;          // partials whose pieces are in flight together
+constexpr int kMergeBlocks = 8;         // output blocks merged per pass
+constexpr int kPvGroup = 4;             // PV blocks whose V^T reads are in flight together
+
+__device__ inline int load_status(const int32_t* status) {
+  return __atomic_load_n(status, __ATOMIC_RELAXED);
+}
+__device__ inline int ldc(const int32_t* p, size_t i) {
+  typedef const int32_t __attribute__((address_space(4))) CT;
+  return ((CT*)p)[i];
+}
+__device__ inline int4 ldc(const int4* p, size_t i) {
+  typedef int __attribute__((ext_vector_type(4))) i32x4;
+  typedef const i32x4 __attribute__((address_space(4))) CT;
+  const i32x4 v = ((CT*)p)[i];
+  return make_int4(v[0], v[1], v[2], v[3]);
+}
+// A wave-uniform pointer taken into scalar registers: a table read through it
+// is a scalar load, which the vector loads in flight do not wait behind.
+template <typename T>
+__device__ inline const T* uniform_ptr(const T* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+  return reinterpret_cast<const T*>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+__device__ inline f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+__device__ inline u32x4 ldkv(const char* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+__device__ inline void store_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline float load_coherent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+constexpr int kWaitVmcnt0 = 0x0F70;
+constexpr int kBufferDword3 = 0x00020000;
+constexpr int kCachePolicySc1 = 0x10;
+
+struct MlaParams {
+  size_t page_bytes;
+  int part_acc_bytes;
+  int g, maxp, log2P;
+  float scale_log2;
+};
+
+// Latent piece s of this lane's row (dims 32s + 8G .. +7 of slot `slot`)
+// into the wave's [dim][slot] LDS area; a slot at or past the valid rows is
+// written as zeros (a freed page may hold any bytes).
+__device__ inline void piece_to_lds(u32x4 x, char* vt, int s, int slot, bool live, int G) {
+  if (!live) x = u32x4{0u, 0u, 0u, 0u};
+  char* base = vt + (32 * s + 8 * G) * kVtStride + slot * 2;
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    *reinterpret_cast<uint16_t*>(base + e * kVtStride) = static_cast<uint16_t>(x[e >> 1] >> (16 * (e & 1)));
+}
+
+// The wave's LDS area passes between its lanes (written by the lanes that
+// loaded a slot, read by the lanes that multiply a latent dim): the wave's
+// LDS operations complete in order, and these fences keep the compiler from
+// moving accesses across the hand-over.
+__device__ inline void lds_handoff() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+struct Acc {
+  f32x4 o[kOBlocks];   // O^T rows 16b + 4G .. +3 of column r (query head r)
+  float m, l;
+};
+
+// Softmax of one tile (scores of slots 8G .. 8G+3 in sa, 8G+4 .. 8G+7 in sb)
+// and its PV products with the transposed latent in LDS.
+__device__ inline void finish_tile(Acc& acc, f32x4 sa, f32x4 sb, const char* vt, float scale,
+                                   int valid, int r, int G) {
+  float sc[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    sc[i] = sa[i] * scale;
+    sc[4 + i] = sb[i] * scale;
+  }
+  const int nv = valid - 8 * G;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) sc[j] = j < nv ? sc[j] : -INFINITY;
+  float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
+                   fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const bool raise = mx > acc.m + kRescale;
+  if (__builtin_amdgcn_ballot_w64(raise)) {
+    const float m_new = raise ? mx : acc.m;
+    const float alpha = __builtin_amdgcn_exp2f(acc.m - m_new);
+    acc.l *= alpha;
+#pragma unroll
+    for (int b = 0; b < kOBlocks; ++b) acc.o[b] *= alpha;
+    acc.m = m_new;
+  }
+  bf16x8 p;
+  float psum = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const __bf16 pb = static_cast<__bf16>(__builtin_amdgcn_exp2f(sc[j] - acc.m));
+    p[j] = pb;
+    psum += static_cast<float>(pb);
+  }
+  acc.l += psum;
+  const u32x4 pu = __builtin_bit_cast(u32x4, p);
+  // V^T operand of row block b: latent dim 16b + r, slots 8G .. 8G+7; read
+  // kPvGroup blocks ahead of the products that use them (reading all 32
+  // first would not fit in registers)
+  const char* vrow = vt + r * kVtStride + 16 * G;
+  auto read_v = [&](int b) {
+    const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow + 16 * b * kVtStride);
+    const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16 * b * kVtStride + 8);
+    return u32x4{lo[0], lo[1], hi[0], hi[1]};
+  };
+  u32x4 v[2][kPvGroup];
+#pragma unroll
+  for (int i = 0; i < kPvGroup; ++i) v[0][i] = read_v(i);
+#pragma unroll
+  for (int b0 = 0; b0 < kOBlocks; b0 += kPvGroup) {
+    const int cur = (b0 / kPvGroup) & 1;
+    if (b0 + kPvGroup < kOBlocks) {
+#pragma unroll
+      for (int i = 0; i < kPvGroup; ++i) v[cur ^ 1][i] = read_v(b0 + kPvGroup + i);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < kPvGroup; ++i) acc.o[b0 + i] = mfma_bf16(v[cur][i], pu, acc.o[b0 + i]);
+  }
+}
+
+// Log-sum-exp merge of the partials of head hh written by waves wf .. wl
+// (index w + hh; waves with an empty range wrote none).  Each lane owns the
+// pieces its stores wrote: query head r, latent dims 16b + 4G .. +3, taken
+// kMergeBlocks blocks at a time so the pieces in flight stay in registers.
+__device__ void merge_head_mla(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsrc,
+                               const int32_t* wave_bounds, float* out, int wf, int wl, int hh,
+                               int g, int r, int G) {
+  auto live = [&](int w2) {
+    return w2 <= wl && ldc(wave_bounds, w2) < ldc(wave_bounds, w2 + 1) && r < g;
+  };
+  auto ml_of = [&](int w2) {
+    return reinterpret_cast<const float*>(part_ml + (static_cast<size_t>(w2) + hh) * kMaxGroup + r);
+  };
+  float M = -INFINITY;
+  for (int w2 = wf; w2 <= wl; ++w2)
+    if (live(w2)) M = fmaxf(M, load_coherent(ml_of(w2)));
+  float den = 0.f;
+  for (int w2 = wf; w2 <= wl; ++w2)
+    if (live(w2)) den += __builtin_amdgcn_exp2f(load_coherent(ml_of(w2)) - M) * load_coherent(ml_of(w2) + 1);
+  const float inv = 1.0f / den;
+  float* o = out + (static_cast<size_t>(hh) * g + r) * kDv + 4 * G;
+  for (int b0 = 0; b0 < kOBlocks; b0 += kMergeBlocks) {
+    f32x4 num[kMergeBlocks];
+#pragma unroll
+    for (int b = 0; b < kMergeBlocks; ++b) num[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int w0 = wf; w0 <= wl; w0 += kMergeWidth) {
+      float wt[kMergeWidth];
+      u32x4 x[kMergeWidth][kMergeBlocks];
+#pragma unroll
+      for (int u = 0; u < kMergeWidth; ++u) {
+        const int w2 = w0 + u;
+        const bool lv = live(w2);
+        const size_t pid = static_cast<size_t>(w2) + hh;
+        wt[u] = lv ? __builtin_amdgcn_exp2f(load_coherent(ml_of(w2)) - M) : 0.f;
+        const uint32_t off = static_cast<uint32_t>(((pid * g + (lv ? r : 0)) * kDv + 16 * b0 + 4 * G) * 4);
+#pragma unroll
+        for (int b = 0; b < kMergeBlocks; ++b)
+          x[u][b] = lv ? __builtin_amdgcn_raw_buffer_load_b128(acc_rsrc, off + 64 * b, 0, kCachePolicySc1)
+                       : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int u = 0; u < kMergeWidth; ++u)
+#pragma unroll
+        for (int b = 0; b < kMergeBlocks; ++b) num[b] += wt[u] * __builtin_bit_cast(f32x4, x[u][b]);
+    }
+    if (r < g) {
+#pragma unroll
+      for (int b = 0; b < kMergeBlocks; ++b) *reinterpret_cast<f32x4*>(o + 16 * (b0 + b)) = num[b] * inv;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256, 1) void decode_mla_kernel(
+    const int32_t* __restrict__ status, const HeadDesc* __restrict__ desc,
+    const int32_t* __restrict__ cum_tiles, const int32_t* __restrict__ wave_bounds,
+    const int4* __restrict__ wave_desc, const int4* __restrict__ head_waves,
+    int32_t* __restrict__ head_cnt, const int32_t* __restrict__ page_table,
+    char* __restrict__ pool, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_in,
+    float2* __restrict__ part_ml, float* __restrict__ part_acc, float* __restrict__ out,
+    MlaParams a) {
+  __shared__ __attribute__((aligned(16))) char vt_lds[kWavesPerBlock][kDv * kVtStride];
+  const int lane = threadIdx.x & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wave = blockIdx.x * kWavesPerBlock + wid;
+  const int r = lane & 15, G = lane >> 4;
+  char* vt = vt_lds[wid];
+  const int4 wd0 = ldc(wave_desc, 2 * wave), wd1 = ldc(wave_desc, 2 * wave + 1);
+  int tb = ldc(wave_bounds, wave);
+  const int te = ldc(wave_bounds, wave + 1);
+  if (load_status(status) != 0) return;
+  if (tb >= te) return;
+  const int tpp_log2 = a.log2P - 5;
+  const int tpp_mask = (1 << tpp_log2) - 1;
+  constexpr size_t kTileBytes = static_cast<size_t>(kD) * 64;
+  const __amdgpu_buffer_rsrc_t acc_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      part_acc, static_cast<short>(0), a.part_acc_bytes, kBufferDword3);
+  int p_hh[2] = {0, 0}, p_cnt[2] = {0, 0}, p_tot[2] = {0, 0};
+  int npend = 0;
+  int hh = wd0.z;
+  bool first = true;
+  const int qr = min(r, a.g - 1);
+  while (tb < te) {
+    int c0, c1;
+    HeadDesc d;
+    if (first) {
+      c0 = wd0.w;
+      c1 = wd1.x;
+      d = make_int4(wd1.y, wd1.z, wd1.w, 0);
+      first = false;
+    } else {
+      while (ldc(cum_tiles, hh + 1) <= tb) ++hh;
+      c0 = ldc(cum_tiles, hh);
+      c1 = ldc(cum_tiles, hh + 1);
+      d = ldc(desc, hh);
+    }
+    const int seg_end = min(te, c1);
+    const int L = d.x;
+    const int32_t* pt = page_table + static_cast<size_t>(d.y) * a.maxp;
+    auto tile_of = [&](int t) -> const char* {
+      return pool + static_cast<size_t>(ldc(uniform_ptr(pt), t >> tpp_log2)) * a.page_bytes +
+             static_cast<size_t>(t & tpp_mask) * kTileBytes;
+    };
+    // query fragments (B operand of the score MFMA): column r = query head r
+    u32x4 qf[kKBlocks];
+    const char* qrow = reinterpret_cast<const char*>(q + (static_cast<size_t>(hh) * a.g + qr) * kD);
+#pragma unroll
+    for (int s = 0; s < kKBlocks; ++s) {
+      const u32x4 x = *reinterpret_cast<const u32x4*>(qrow + (32 * s + 8 * G) * 2);
+      qf[s] = r < a.g ? x : u32x4{0u, 0u, 0u, 0u};
+    }
+    const int t_lo = tb - c0;
+    const int t_hi = seg_end - c0;
+    // the token appended by this call (slot d.z) is written into its tile by
+    // the wave whose segment covers it, before the segment's loads
+    if (k_in != nullptr && d.z >= t_lo * kTile && d.z < t_hi * kTile) {
+      char* tile = const_cast<char*>(tile_of(d.z >> 5));
+      const int j = d.z & 31;
+      const uint4* src = reinterpret_cast<const uint4*>(k_in + static_cast<size_t>(hh) * kD);
+      // 72 pieces: one per lane, then 8 more (no lane loop, whose divergent
+      // exit would push the uniform values used after it into VGPRs)
+      *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * lane)) = src[lane];
+      if (lane < kD / 8 - 64)
+        *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * (64 + lane))) = src[64 + lane];
+    }
+    Acc acc;
+#pragma unroll
+    for (int b = 0; b < kOBlocks; ++b) acc.o[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    acc.m = -INFINITY;
+    acc.l = 0.f;
+    // slot of this lane's row in half h: 8 (r / 4) + r % 4 + 4 h
+    const int row0 = 8 * (r >> 2) + (r & 3);
+    // The tile's 36 pieces (half h, k-step s: 1 KB at h * 1024 + s * 2048)
+    // stream through 18 registers sets: piece s of a half is consumed (score
+    // MFMA, latent to LDS) and its register set refilled with the piece 18
+    // positions later -- the other half, or the next tile -- so 17 to 18
+    // pieces (18 KB) stay in flight with 72 registers.
+    u32x4 kr[kKBlocks];
+    const char* cur = tile_of(t_lo) + lane * 16;
+    // issued in piece order (the waits below count on it)
+#pragma unroll
+    for (int s = 0; s < kKBlocks; ++s) {
+      kr[s] = ldkv(cur + s * 2048);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    int t = t_lo;
+    for (; t + 1 < t_hi; ++t) {
+      const char* nxt = tile_of(t + 1) + lane * 16;
+      f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < kKBlocks; ++s) {
+        sa = mfma_bf16(kr[s], qf[s], sa);
+        if (s < kLBlocks) piece_to_lds(kr[s], vt, s, row0, true, G);
+        kr[s] = ldkv(cur + 1024 + s * 2048);
+        if (s % 3 == 2) __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int s = 0; s < kKBlocks; ++s) {
+        sb = mfma_bf16(kr[s], qf[s], sb);
+        if (s < kLBlocks) piece_to_lds(kr[s], vt, s, row0 + 4, true, G);
+        kr[s] = ldkv(nxt + s * 2048);
+        if (s % 3 == 2) __builtin_amdgcn_sched_barrier(0);
+      }
+      lds_handoff();
+      finish_tile(acc, sa, sb, vt, a.scale_log2, kTile, r, G);
+      lds_handoff();
+      cur = nxt;
+    }
+    {
+      // last tile of the segment: rows at or past L are stale
+      const int valid = (seg_end == c1) ? L - t * kTile : kTile;
+      f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < kKBlocks; ++s) {
+        sa = mfma_bf16(kr[s], qf[s], sa);
+        if (s < kLBlocks) piece_to_lds(kr[s], vt, s, row0, row0 < valid, G);
+        kr[s] = ldkv(cur + 1024 + s * 2048);
+        if (s % 3 == 2) __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int s = 0; s < kKBlocks; ++s) {
+        sb = mfma_bf16(kr[s], qf[s], sb);
+        if (s < kLBlocks) piece_to_lds(kr[s], vt, s, row0 + 4, row0 + 4 < valid, G);
+      }
+      lds_handoff();
+      finish_tile(acc, sa, sb, vt, a.scale_log2, valid, r, G);
+      lds_handoff();
+    }
+    float l = acc.l;
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    if (tb == c0 && seg_end == c1) {
+      if (r < a.g) {
+        const float inv = 1.0f / l;
+        float* o = out + (static_cast<size_t>(hh) * a.g + r) * kDv + 4 * G;
+#pragma unroll
+        for (int b = 0; b < kOBlocks; ++b) *reinterpret_cast<f32x4*>(o + 16 * b) = acc.o[b] * inv;
+      }
+    } else {
+      // split head: publish this wave's partial (agent-coherent stores), counted at the end
+      const size_t pid = static_cast<size_t>(wave) + hh;
+      if (r < a.g) {
+        float* ml = reinterpret_cast<float*>(part_ml + pid * kMaxGroup + r);
+        if (G == 0) {
+          store_coherent(ml, acc.m);
+          store_coherent(ml + 1, l);
+        }
+        const uint32_t o = static_cast<uint32_t>(((pid * a.g + r) * kDv + 4 * G) * 4);
+#pragma unroll
+        for (int b = 0; b < kOBlocks; ++b)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc.o[b]), acc_rsrc,
+                                                 o + 64 * b, 0, kCachePolicySc1);
+      }
+      p_hh[npend] = hh;
+      p_cnt[npend] = seg_end - tb;
+      p_tot[npend] = c1 - c0;
+      ++npend;
+    }
+    tb = seg_end;
+    ++hh;
+  }
+  if (npend > 0) {
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    int prev = 0;
+    if (lane < npend) prev = atomicAdd(&head_cnt[lane == 0 ? p_hh[0] : p_hh[1]], lane == 0 ? p_cnt[0] : p_cnt[1]);
+    const int prev0 = __shfl(prev, 0, 64), prev1 = __shfl(prev, 1, 64);
+    for (int i = 0; i < npend; ++i) {
+      if ((i == 0 ? prev0 : prev1) + p_cnt[i] != p_tot[i]) continue;
+      const int mh = p_hh[i];
+      const int4 hw = ldc(head_waves, mh);
+      merge_head_mla(part_ml, acc_rsrc, wave_bounds, out, hw.x, hw.y, mh, a.g, r, G);
+      if (lane == 0) __hip_atomic_store(&head_cnt[mh], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_decode_mla(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                             void* pool, int layer, int n, const void* q, const void* k,
+                             float* out, int waves, hipStream_t st, hipEvent_t ev_start,
+                             hipEvent_t ev_stop) {
+  char* w = static_cast<char*>(ws);
+  MlaParams a;
+  a.page_bytes = lo.page_bytes;
+  a.part_acc_bytes = static_cast<int>(static_cast<size_t>(lo.max_partials) * c.group_size * kDv * 4);
+  a.g = c.group_size;
+  a.maxp = c.max_pages_per_head;
+  a.log2P = __builtin_ctz(static_cast<unsigned>(c.page_size));
+  a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
+  if (ev_start) (void)hipEventRecord(ev_start, st);
+  hipLaunchKernelGGL(decode_mla_kernel, dim3(waves / kWavesPerBlock), dim3(256), 0, st,
+                     reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status),
+                     reinterpret_cast<const HeadDesc*>(w + lo.ws_head_desc),
+                     reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles),
+                     reinterpret_cast<const int32_t*>(w + lo.ws_wave_bounds),
+                     reinterpret_cast<const int4*>(w + lo.ws_wave_desc),
+                     reinterpret_cast<const int4*>(w + lo.ws_head_waves),
+                     reinterpret_cast<int32_t*>(w + lo.ws_head_cnt),
+                     layer_state(lo, meta, layer).page_table, static_cast<char*>(pool),
+                     static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                     reinterpret_cast<float2*>(w + lo.ws_part_ml),
+                     reinterpret_cast<float*>(w + lo.ws_part_acc), out, a);
+  hipError_t e = hipGetLastError();
+  if (ev_stop) (void)hipEventRecord(ev_stop, st);
+  return e;
+}
+
+int decode_mla_resident_waves() {
+  int dev = 0, cus = 0, blocks = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return -1;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_mla_kernel, 256, 0) != hipSuccess ||
+      blocks < 1)
+    return -1;
+  int waves = cus * kWavesPerBlock;
+  if (waves > kMaxWaves) waves = kMaxWaves / kWavesPerBlock * kWavesPerBlock;
+  return waves;
+}
+
+}  // namespace dms

@@ -67,6 +67,9 @@ DMS_DECIDE_CALLER = 0
 DMS_DECIDE_QUERY = 1
 DMS_KV_BF16 = 0
 DMS_KV_FP8 = 1
+DMS_KV_MLA = 2
+MLA_ROW_DIM = 576      # latent (512) + rotary key (64)
+MLA_LATENT_DIM = 512
 
 
 class DmsStateOffsets(ctypes.Structure):
@@ -364,11 +367,15 @@ class DmsCache:
 
     def pool_page_kv(self, layer, page):
         """One page on the host: bf16 pages give (K [P, d], V [P, d]) bit patterns
-        (uint16); FP8 pages give (K codes, V codes [P, d] uint8, K scales, V scales
+        (uint16); latent pages give (rows [P, d], their latent part [P, 512]);
+        FP8 pages give (K codes, V codes [P, d] uint8, K scales, V scales
         [P] float32)."""
         raw = self.pools[layer][page * self.page_bytes:(page + 1) * self.page_bytes].cpu().numpy()
         if self.cfg.kv_format == DMS_KV_FP8:
             return unpack_page_fp8(raw, self.cfg.page_size, self.cfg.head_dim)
+        if self.cfg.kv_format == DMS_KV_MLA:
+            rows = unpack_page_mla(raw.view(np.uint16), self.cfg.page_size, self.cfg.head_dim)
+            return rows, rows[:, :MLA_LATENT_DIM]
         return unpack_page(raw.view(np.uint16), self.cfg.page_size, self.cfg.head_dim)
 
 
@@ -383,6 +390,17 @@ def unpack_page(u16, P, D):
     k = tiles[:, 0][:, koff].reshape(P, D)
     v = tiles[:, 1][:, voff].reshape(P, D)
     return k, v
+
+
+def unpack_page_mla(u16, P, D):
+    """Decode one latent-attention page (uint16 words) into its rows [P, D]:
+    tiles of 32 rows in the key order of the bf16 pages, no value part."""
+    tiles = np.asarray(u16).reshape(P // 32, D * 32)
+    j = np.arange(32)[:, None]
+    e = np.arange(D)[None, :]
+    h, r = (j // 4) % 2, 4 * (j // 8) + j % 4
+    koff = ((((e // 32) * 2 + h) * 4 + (e // 8) % 4) * 16 + r) * 8 + e % 8
+    return tiles[:, koff].reshape(P, D)
 
 
 def unpack_page_fp8(raw, P, D):

@@ -56,7 +56,7 @@ def _cfg(**kw):
     (dict(decision_source=2), dms.DMS_ERR_INVALID),
     (dict(decision_source=1, decision_bias=float("nan")), dms.DMS_ERR_INVALID),
     (dict(decision_source=1, decision_bias=float("inf")), dms.DMS_ERR_INVALID),
-    (dict(kv_format=2), dms.DMS_ERR_INVALID),
+    (dict(kv_format=3), dms.DMS_ERR_INVALID),
     (dict(quest_page_budget=-1), dms.DMS_ERR_INVALID),
     (dict(quest_page_budget=17), dms.DMS_ERR_INVALID),                     # > max_pages_per_head
     (dict(quest_page_budget=4, max_pages_per_head=5000), dms.DMS_ERR_UNSUPPORTED),
@@ -286,3 +286,46 @@ def test_quest_layout_and_host_checks():
         dms.dms_destroy(ctx)
     assert L.dms_quest_selection(None, 1, P, P, None) == dms.DMS_ERR_INVALID
 
+
+
+def test_latent_pages_layout_and_host_checks():
+    """Latent-attention pools: one KV head of 576-dim rows, P/32 tiles of
+    64 * 576 bytes in the bf16 key order; the unsupported combinations are
+    refused on the host."""
+    import numpy as np
+    mla = dict(kv_format=dms.DMS_KV_MLA, head_dim=dms.MLA_ROW_DIM, num_kv_heads=1, group_size=16)
+    for P in (32, 64, 256):
+        _, pool, ws, pg = dms.dms_layout(_cfg(page_size=P, **mla))
+        assert pg == P * dms.MLA_ROW_DIM * 2 and pool == pg * _cfg().num_pages
+    for kw in (dict(head_dim=128), dict(num_kv_heads=2), dict(quest_page_budget=2),
+               dict(decision_source=dms.DMS_DECIDE_QUERY)):
+        rc = dms.lib().dms_layout(ctypes.byref(_cfg(**{**mla, **kw})), None, None, None, None)
+        assert rc == dms.DMS_ERR_UNSUPPORTED, kw
+    # 576-dim rows only exist in latent pools
+    rc = dms.lib().dms_layout(ctypes.byref(_cfg(head_dim=dms.MLA_ROW_DIM)), None, None, None, None)
+    assert rc == dms.DMS_ERR_UNSUPPORTED
+    rc = dms.lib().dms_layout(ctypes.byref(_cfg(group_size=17, **{k: v for k, v in mla.items() if k != "group_size"})),
+                              None, None, None, None)
+    assert rc == dms.DMS_ERR_UNSUPPORTED
+    # documented offsets (include/dms.h): the bf16 key formula, tiles of 64 d bytes
+    P, D = 64, dms.MLA_ROW_DIM
+    words = np.zeros(P * D, np.uint16)
+    for s_ in (0, 5, 31, 32, 63):
+        t, j = divmod(s_, 32)
+        h, r = (j // 4) % 2, 4 * (j // 8) + j % 4
+        for e in (0, 7, 31, 32, 100, 511, 512, 575):
+            off = t * 64 * D + ((((e // 32) * 2 + h) * 4 + (e // 8) % 4) * 16 + r) * 16 + (e % 8) * 2
+            words[off // 2] = 1 + s_ * 1000 + e
+    rows = dms.unpack_page_mla(words, P, D)
+    for s_ in (0, 5, 31, 32, 63):
+        for e in (0, 7, 31, 32, 100, 511, 512, 575):
+            assert rows[s_, e] == 1 + s_ * 1000 + e
+    # the prefill entry points refuse latent pools before any device work
+    L = dms.lib()
+    ctx = dms.dms_create(_cfg(**mla), 0x1000, [0x2000, 0x3000], 0x4000)
+    try:
+        X = 0x100
+        assert L.dms_prefill_chunk(ctx, 0, 1, X, X, 4, 4, X, X, None, X, X, None) == dms.DMS_ERR_UNSUPPORTED
+        assert L.dms_prefill_chunk_q(ctx, 0, 1, X, X, 4, 4, X, X, None, X, X, None) == dms.DMS_ERR_UNSUPPORTED
+    finally:
+        dms.dms_destroy(ctx)

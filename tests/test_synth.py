@@ -71,3 +71,18 @@ def test_beta71_rates():
     r = sy.beta71_rates_np(4, 0, np.arange(256)[:, None], np.arange(8)[None, :]) / 2**24
     # Beta(7, 1) has mean 7/8
     assert abs(r.mean() - 0.875) < 0.02 and r.min() > 0.2 and r.max() < 1.0
+
+
+def test_wide_vectors_have_distinct_coordinates():
+    """576-wide rows: every (head, element) pair of up to 16 heads maps to its
+    own generator coordinate, so no two elements of any rows share a draw."""
+    import numpy as np
+    import dms_synth as sy
+    heads = np.arange(16)[:, None]
+    dims = np.arange(576)[None, :]
+    h, d = sy.wide_coords(heads, dims, 576)
+    assert d.max() < 256 and h.max() < (1 << sy.HEAD_BITS)
+    keys = (h << sy.DIM_BITS) + d
+    assert len(np.unique(keys)) == 16 * 576
+    v = sy.token_vectors_np(5, sy.STREAM_K, 0, 0, h, 7, d)
+    assert len(np.unique(v)) > 1000
