@@ -43,7 +43,17 @@ WORKLOADS = {
                           context=(4096, 32768), window=256, p_evict=3 / 4, seed=2,
                           desc="Qwen-R1-7B-shaped DMS decode, contexts uniform in "
                                "[4096, 32768], w=256, flags Bernoulli(3/4)"),
+    # latent attention: one cached row of 512 latent + 64 rotary dims per
+    # token, shared by all 16 query heads (DeepSeek-V2-Lite's attention shape)
+    "deepseek-v2-lite-8x": dict(layers=27, batch=128, kv_heads=1, group=16, head_dim=576,
+                                context=32768, window=256, p_evict=7 / 8, seed=4, kv_format=2,
+                                desc="DeepSeek-V2-Lite-shaped latent-attention (MLA) DMS decode, "
+                                     "absorbed form, 8 prompts x 16 chains, context 32768, w=256, "
+                                     "flags Bernoulli(7/8)"),
 }
+MLA = 2            # kv_format of latent-attention pools
+MLA_LATENT = 512   # output (value) dims of a latent-attention row
+TRAFFIC_PROFILE_MLA = "decode_mla_kernel_deepseek-v2-lite-8x.txt"
 
 
 def profiled_traffic(profile, sources):
@@ -75,10 +85,12 @@ def log(msg):
 
 
 def row_bytes(wl):
-    """Bytes read per retained token of one KV head: K and V rows in bf16, or
-    E4M3 codes plus one float32 scale per row in FP8 pages."""
+    """Bytes read per retained token of one KV head: K and V rows in bf16,
+    E4M3 codes plus one float32 scale per row in FP8 pages, or the one bf16
+    row of a latent-attention cache."""
     D = wl["head_dim"]
-    return 2 * D + 8 if wl.get("kv_format", 0) == 1 else 2 * D * 2
+    fmt = wl.get("kv_format", 0)
+    return 2 * D + 8 if fmt == 1 else 2 * D if fmt == MLA else 2 * D * 2
 
 
 def contexts(wl, rng_seed):
@@ -146,7 +158,8 @@ def build(wl, steps_total, chunk_tokens, dev):
                 cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
                 T = int(cu[-1])
                 k = torch.randn((T, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
-                v = torch.randn((T, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+                v = (None if wl.get("kv_format", 0) == MLA
+                     else torch.randn((T, H, D), generator=gen, device=dev, dtype=torch.bfloat16))
                 # flags of every sequence's next positions, varlen layout [T, H]
                 lens_t = torch.as_tensor(lens, device=dev)
                 seq_of = torch.repeat_interleave(gseqs, lens_t)
@@ -185,7 +198,8 @@ def step_inputs(wl, ctx, steps_total, dev):
     gen.manual_seed(seed * 7919 + 17)
     q = torch.randn((steps_total, nl, B, H * g, D), generator=gen, device=dev, dtype=torch.bfloat16)
     k = torch.randn((steps_total, nl, B, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
-    v = torch.randn((steps_total, nl, B, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    v = (None if wl.get("kv_format", 0) == MLA
+         else torch.randn((steps_total, nl, B, H, D), generator=gen, device=dev, dtype=torch.bfloat16))
     ctx_t = torch.as_tensor(ctx, device=dev)
     seqs = torch.arange(B, device=dev, dtype=torch.int64)
     heads = torch.arange(H, device=dev, dtype=torch.int64)
@@ -208,13 +222,20 @@ def cpu_baseline(wl, ctx, budget_s=12.0):
     import numpy as np
 
     import dms_synth as sy
-    from oracle import dense_dms_attention_head, fake_quantize_fp8
+    from oracle import dense_dms_attention_head, fake_quantize_fp8, mla_attention
+    from oracle import visible as key_visible
 
     B, H, g, D, w, p = (wl["batch"], wl["kv_heads"], wl["group"], wl["head_dim"],
                         wl["window"], wl["p_evict"])
     fp8 = wl.get("kv_format", 0) == 1
+    mla = wl.get("kv_format", 0) == MLA
     nl, seed = wl["layers"], wl["seed"]
     rng = np.random.default_rng(12345)
+
+    def _wide(heads, dims, width, positions):
+        hh, dd = sy.wide_coords(heads, dims, width)
+        return hh, positions, dd
+
     triples = [(int(rng.integers(nl)), int(rng.integers(B)), int(rng.integers(H))) for _ in range(6)]
     f32 = sy.bf16_bits_to_f32_np
     head_steps, bytes_equiv, elapsed = 0, 0, 0.0
@@ -222,14 +243,21 @@ def cpu_baseline(wl, ctx, budget_s=12.0):
     for (layer, s, h) in triples:
         T = int(ctx[s]) + 8
         pos = np.arange(T)
-        kh = f32(sy.head_sequence_np(seed, sy.STREAM_K, layer, s, h, pos, D))
-        vh = f32(sy.head_sequence_np(seed, sy.STREAM_V, layer, s, h, pos, D))
-        if fp8:   # the stored (dequantized) rows
-            kh, vh = fake_quantize_fp8(kh), fake_quantize_fp8(vh)
         fh = sy.flags_np(seed, p, layer, s, h, pos)
         qd = np.arange(D)[None, None, :]
-        qh = f32(sy.token_vectors_np(seed, sy.STREAM_Q, layer, s, (h * g + np.arange(g))[None, :, None],
-                                     pos[-8:][:, None, None], qd))
+        qh_ = (h * g + np.arange(g))[None, :, None]
+        if mla:   # 576-wide rows and queries
+            kh = f32(sy.token_vectors_np(seed, sy.STREAM_K, layer, s,
+                                         *_wide(np.full((1, 1), h), np.arange(D)[None, :], D, pos[:, None])))
+            vh = None
+            qh = f32(sy.token_vectors_np(seed, sy.STREAM_Q, layer, s,
+                                         *_wide(qh_, qd, D, pos[-8:][:, None, None])))
+        else:
+            kh = f32(sy.head_sequence_np(seed, sy.STREAM_K, layer, s, h, pos, D))
+            vh = f32(sy.head_sequence_np(seed, sy.STREAM_V, layer, s, h, pos, D))
+            if fp8:   # the stored (dequantized) rows
+                kh, vh = fake_quantize_fp8(kh), fake_quantize_fp8(vh)
+            qh = f32(sy.token_vectors_np(seed, sy.STREAM_Q, layer, s, qh_, pos[-8:][:, None, None], qd))
         samples.append((kh, vh, fh, qh, T))
     t_start = time.perf_counter()
     while elapsed < budget_s:
@@ -237,7 +265,12 @@ def cpu_baseline(wl, ctx, budget_s=12.0):
             for i in range(4):
                 t = T - 8 + i
                 t0 = time.perf_counter()
-                dense_dms_attention_head(qh[i:i + 1], kh[:t + 1], vh[:t + 1], fh[:t + 1], w, [t])
+                if mla:
+                    mask = np.asarray(key_visible(t, np.arange(t + 1), fh[:t + 1], w), dtype=bool)
+                    mla_attention(qh[i], kh[:t + 1], np.broadcast_to(mask, (g, t + 1)), MLA_LATENT,
+                                  1.0 / math.sqrt(D))
+                else:
+                    dense_dms_attention_head(qh[i:i + 1], kh[:t + 1], vh[:t + 1], fh[:t + 1], w, [t])
                 elapsed += time.perf_counter() - t0
                 head_steps += 1
                 visible = min(w, t + 1) + int(np.sum(fh[: max(0, t - w + 1)] == 0))
@@ -258,8 +291,8 @@ def cpu_baseline(wl, ctx, budget_s=12.0):
         "cores": threads,
         "kind": "oracle",
         "sample": f"{head_steps} head-steps (one KV head, its {g} query heads, one decode "
-                  f"position, dense float64 masked attention over the full history"
-                  f"{' of the dequantized FP8 rows' if fp8 else ''}) on "
+                  f"position, dense float64 masked {'absorbed latent ' if mla else ''}attention over "
+                  f"the full history{' of the dequantized FP8 rows' if fp8 else ''}) on "
                   f"{len(samples)} sampled (layer, sequence, KV head) triples; value = their "
                   f"retained-KV bytes / CPU time",
         "head_steps_per_s": head_steps / elapsed,
@@ -582,11 +615,13 @@ def measure_decode(wl, steps, warmup, dev):
     q, k, v, flags, fresh = step_inputs(wl, ctx, S, dev)
     B, nl, D = wl["batch"], wl["layers"], wl["head_dim"]
     sid = torch.arange(B, dtype=torch.int32, device=dev)
-    out = torch.empty((nl, B, wl["kv_heads"] * wl["group"], D), dtype=torch.float32, device=dev)
+    Dout = MLA_LATENT if wl.get("kv_format", 0) == MLA else D
+    out = torch.empty((nl, B, wl["kv_heads"] * wl["group"], Dout), dtype=torch.float32, device=dev)
 
     def run_step(s):
         for layer in range(nl):
-            dms.dms_decode_step(cache.ctx, layer, B, sid, q[s, layer], k[s, layer], v[s, layer],
+            dms.dms_decode_step(cache.ctx, layer, B, sid, q[s, layer], k[s, layer],
+                                None if v is None else v[s, layer],
                                 flags[s, layer], out[layer])
 
     for s in range(warmup):
@@ -723,6 +758,10 @@ def main():
         run_train(args)
         return
     wl = dict(WORKLOADS[args.workload])
+    if wl.get("kv_format", 0) == MLA and (args.kv_format != "bf16" or args.quest_pages > 0):
+        print(json.dumps({"error": "latent-attention pools hold bf16 rows and attend every "
+                                   "retained row (no --kv-format fp8, no --quest-pages)"}))
+        sys.exit(2)
     if args.kv_format == "fp8":
         wl["kv_format"] = dms.DMS_KV_FP8
         wl["desc"] += ", FP8 E4M3 KV pages"
@@ -735,14 +774,16 @@ def main():
     q, k, v, flags, fresh = step_inputs(wl, ctx, S, dev)
     B, H, g, D, nl = wl["batch"], wl["kv_heads"], wl["group"], wl["head_dim"], wl["layers"]
     sid = torch.arange(B, dtype=torch.int32, device=dev)
-    out = torch.empty((nl, B, H * g, D), dtype=torch.float32, device=dev)
+    mla = wl.get("kv_format", 0) == MLA
+    out = torch.empty((nl, B, H * g, MLA_LATENT if mla else D), dtype=torch.float32, device=dev)
     # retained length of every head when step s attends (after its append)
     Lstep = torch.stack(L0)[None] + torch.cumsum(fresh, dim=0)        # [S, nl, B, H]
     kv_bytes = Lstep.sum(dim=(1, 2, 3)).to(torch.float64) * row_bytes(wl)  # per step, all layers
 
     def run_step(s):
         for layer in range(nl):
-            dms.dms_decode_step(cache.ctx, layer, B, sid, q[s, layer], k[s, layer], v[s, layer],
+            dms.dms_decode_step(cache.ctx, layer, B, sid, q[s, layer], k[s, layer],
+                                None if v is None else v[s, layer],
                                 flags[s, layer], out[layer])
 
     for s in range(args.warmup):
@@ -784,7 +825,8 @@ def main():
         attended = []
         for s in range(k_lo, k_hi):
             for layer in range(nl):
-                dms.dms_decode_step(cache.ctx, layer, B, sid, q[s, layer], k[s, layer], v[s, layer],
+                dms.dms_decode_step(cache.ctx, layer, B, sid, q[s, layer], k[s, layer],
+                                None if v is None else v[s, layer],
                                     flags[s, layer], out[layer])
                 dms.dms_quest_selection(cache.ctx, B, sel_p[layer], sel_c[layer])
             Ls = Lstep[s].reshape(nl, B * H)
@@ -821,10 +863,13 @@ def main():
     kern_avg_ms = kern_ms / max(launches, 1)
     achieved = per_launch_bytes / (kern_avg_ms * 1e-3) / 1e9
     mean_L = float(Lstep[t_lo:t_hi].double().mean())
-    traffic = None
+    traffic, traffic_profile = None, None
     if args.workload == "qwen-r1-32b-8x" and not quest:
-        traffic = profiled_traffic(TRAFFIC_PROFILE_FP8 if args.kv_format == "fp8" else TRAFFIC_PROFILE,
-                                   ["dms_common.h", "dms_fp8.h", "dms_decode.hip"])
+        traffic_profile = TRAFFIC_PROFILE_FP8 if args.kv_format == "fp8" else TRAFFIC_PROFILE
+        traffic = profiled_traffic(traffic_profile, ["dms_common.h", "dms_fp8.h", "dms_decode.hip"])
+    elif mla:
+        traffic_profile = TRAFFIC_PROFILE_MLA
+        traffic = profiled_traffic(traffic_profile, ["dms_common.h", "dms_mla.hip"])
     res = {
         "metric": "DMS decode attn: achieved KV HBM GB/s (% of peak) + decode tok/s at 8x",
         "value": round(value, 1),
@@ -840,10 +885,10 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": wl["desc"],
-            "kv_format": args.kv_format,
+            "kv_format": "mla (bf16 rows)" if mla else args.kv_format,
             "quest_pages": args.quest_pages,
             "layers": nl, "batch": B, "kv_heads": H, "query_heads": H * g,
-            "head_dim": D, "window": wl["window"], "p_evict": wl["p_evict"],
+            "head_dim": D, **({"latent_dim": MLA_LATENT, "rope_dim": D - MLA_LATENT} if mla else {}), "window": wl["window"], "p_evict": wl["p_evict"],
             "context": wl["context"] if not isinstance(wl["context"], tuple) else list(wl["context"]),
             "mean_retained_tokens": round(mean_L, 1),
             "effective_compression": round(float((ctx.mean() + t_lo + args.steps / 2) / mean_L), 2),
@@ -860,9 +905,8 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "traffic_source": ("profiles/" + (TRAFFIC_PROFILE_FP8 if args.kv_format == "fp8" else TRAFFIC_PROFILE)
-                               if traffic is not None else None),
-            "kernel": "decode_kernel<128>",
+            "traffic_source": "profiles/" + traffic_profile if traffic is not None else None,
+            "kernel": "decode_mla_kernel" if mla else f"decode_kernel<{D}>",
             "kernel_timing": "HIP events around each decode launch, eager pass of the next "
                              f"{args.steps} steps",
             "kernel_avg_us": round(1e3 * kern_avg_ms, 2),

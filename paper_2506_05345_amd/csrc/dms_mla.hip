@@ -12,9 +12,12 @@
 // a row by q . row over all 576 dims and its output is the softmax-weighted
 // sum of the rows' first 512 dims (the latent; W_UV is applied by the caller).
 //
-// The kernel follows decode_kernel (dms_decode.hip): the planner's equal
-// tile ranges per wave, one wave per SIMD, split heads merged by the wave
-// that completes them at the end of its range.  Per 32-slot tile:
+// The kernel follows decode_kernel (dms_decode.hip) in its work split: the
+// planner's equal tile ranges per wave, one wave per SIMD.  A split head's
+// partials (16 heads x 512 float32 per wave, 16x the standard kernel's) are
+// combined by a second launch with one wave per output row, not by the last
+// arriving wave, whose lone merge of a head's partials would be a
+// latency-bound tail.  Per 32-slot tile:
 //  * keys: the row is stored in the fragment order of the 16x16x32 score
 //    MFMA (A operand: tile rows, k = 32 dims); the tile is read in two halves
 //    of 16 rows, half h holding slots 8(r/4) + r%4 + 4h, with the next half's
@@ -44,8 +47,7 @@ constexpr int kLBlocks = kDv / 32;      // of them latent (16)
 constexpr int kOBlocks = kDv / 16;      // 16-dim row blocks of O^T (32)
 constexpr int kVtStride = 72;           // LDS bytes per latent dim: 32 slots + pad
 constexpr float kRescale = 8.0f;        // lazy rescale threshold, log2 units
-constexpr int kMergeWidth = 4;          // partials whose pieces are in flight together
-constexpr int kMergeBlocks = 8;         // output blocks merged per pass
+constexpr int kCombineBatch = 8;        // partials whose rows a combine wave loads together
 constexpr int kPvGroup = 4;             // PV blocks whose V^T reads are in flight together
 
 __device__ inline int load_status(const int32_t* status) {
@@ -77,19 +79,9 @@ __device__ inline f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
 __device__ inline u32x4 ldkv(const char* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 }
-__device__ inline void store_coherent(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ inline float load_coherent(const float* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-constexpr int kWaitVmcnt0 = 0x0F70;
-constexpr int kBufferDword3 = 0x00020000;
-constexpr int kCachePolicySc1 = 0x10;
 
 struct MlaParams {
   size_t page_bytes;
-  int part_acc_bytes;
   int g, maxp, log2P;
   float scale_log2;
 };
@@ -181,63 +173,10 @@ __device__ inline void finish_tile(Acc& acc, f32x4 sa, f32x4 sb, const char* vt,
   }
 }
 
-// Log-sum-exp merge of the partials of head hh written by waves wf .. wl
-// (index w + hh; waves with an empty range wrote none).  Each lane owns the
-// pieces its stores wrote: query head r, latent dims 16b + 4G .. +3, taken
-// kMergeBlocks blocks at a time so the pieces in flight stay in registers.
-__device__ void merge_head_mla(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsrc,
-                               const int32_t* wave_bounds, float* out, int wf, int wl, int hh,
-                               int g, int r, int G) {
-  auto live = [&](int w2) {
-    return w2 <= wl && ldc(wave_bounds, w2) < ldc(wave_bounds, w2 + 1) && r < g;
-  };
-  auto ml_of = [&](int w2) {
-    return reinterpret_cast<const float*>(part_ml + (static_cast<size_t>(w2) + hh) * kMaxGroup + r);
-  };
-  float M = -INFINITY;
-  for (int w2 = wf; w2 <= wl; ++w2)
-    if (live(w2)) M = fmaxf(M, load_coherent(ml_of(w2)));
-  float den = 0.f;
-  for (int w2 = wf; w2 <= wl; ++w2)
-    if (live(w2)) den += __builtin_amdgcn_exp2f(load_coherent(ml_of(w2)) - M) * load_coherent(ml_of(w2) + 1);
-  const float inv = 1.0f / den;
-  float* o = out + (static_cast<size_t>(hh) * g + r) * kDv + 4 * G;
-  for (int b0 = 0; b0 < kOBlocks; b0 += kMergeBlocks) {
-    f32x4 num[kMergeBlocks];
-#pragma unroll
-    for (int b = 0; b < kMergeBlocks; ++b) num[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int w0 = wf; w0 <= wl; w0 += kMergeWidth) {
-      float wt[kMergeWidth];
-      u32x4 x[kMergeWidth][kMergeBlocks];
-#pragma unroll
-      for (int u = 0; u < kMergeWidth; ++u) {
-        const int w2 = w0 + u;
-        const bool lv = live(w2);
-        const size_t pid = static_cast<size_t>(w2) + hh;
-        wt[u] = lv ? __builtin_amdgcn_exp2f(load_coherent(ml_of(w2)) - M) : 0.f;
-        const uint32_t off = static_cast<uint32_t>(((pid * g + (lv ? r : 0)) * kDv + 16 * b0 + 4 * G) * 4);
-#pragma unroll
-        for (int b = 0; b < kMergeBlocks; ++b)
-          x[u][b] = lv ? __builtin_amdgcn_raw_buffer_load_b128(acc_rsrc, off + 64 * b, 0, kCachePolicySc1)
-                       : u32x4{0u, 0u, 0u, 0u};
-      }
-#pragma unroll
-      for (int u = 0; u < kMergeWidth; ++u)
-#pragma unroll
-        for (int b = 0; b < kMergeBlocks; ++b) num[b] += wt[u] * __builtin_bit_cast(f32x4, x[u][b]);
-    }
-    if (r < g) {
-#pragma unroll
-      for (int b = 0; b < kMergeBlocks; ++b) *reinterpret_cast<f32x4*>(o + 16 * (b0 + b)) = num[b] * inv;
-    }
-  }
-}
-
 __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
     const int32_t* __restrict__ status, const HeadDesc* __restrict__ desc,
     const int32_t* __restrict__ cum_tiles, const int32_t* __restrict__ wave_bounds,
-    const int4* __restrict__ wave_desc, const int4* __restrict__ head_waves,
-    int32_t* __restrict__ head_cnt, const int32_t* __restrict__ page_table,
+    const int4* __restrict__ wave_desc, const int32_t* __restrict__ page_table,
     char* __restrict__ pool, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_in,
     float2* __restrict__ part_ml, float* __restrict__ part_acc, float* __restrict__ out,
     MlaParams a) {
@@ -255,10 +194,6 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
   const int tpp_log2 = a.log2P - 5;
   const int tpp_mask = (1 << tpp_log2) - 1;
   constexpr size_t kTileBytes = static_cast<size_t>(kD) * 64;
-  const __amdgpu_buffer_rsrc_t acc_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      part_acc, static_cast<short>(0), a.part_acc_bytes, kBufferDword3);
-  int p_hh[2] = {0, 0}, p_cnt[2] = {0, 0}, p_tot[2] = {0, 0};
-  int npend = 0;
   int hh = wd0.z;
   bool first = true;
   const int qr = min(r, a.g - 1);
@@ -379,41 +314,68 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
         for (int b = 0; b < kOBlocks; ++b) *reinterpret_cast<f32x4*>(o + 16 * b) = acc.o[b] * inv;
       }
     } else {
-      // split head: publish this wave's partial (agent-coherent stores), counted at the end
+      // split head: this wave's partial, combined by the next launch
       const size_t pid = static_cast<size_t>(wave) + hh;
       if (r < a.g) {
-        float* ml = reinterpret_cast<float*>(part_ml + pid * kMaxGroup + r);
-        if (G == 0) {
-          store_coherent(ml, acc.m);
-          store_coherent(ml + 1, l);
-        }
-        const uint32_t o = static_cast<uint32_t>(((pid * a.g + r) * kDv + 4 * G) * 4);
+        if (G == 0) part_ml[pid * kMaxGroup + r] = make_float2(acc.m, l);
+        float* o = part_acc + (pid * a.g + r) * kDv + 4 * G;
 #pragma unroll
-        for (int b = 0; b < kOBlocks; ++b)
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc.o[b]), acc_rsrc,
-                                                 o + 64 * b, 0, kCachePolicySc1);
+        for (int b = 0; b < kOBlocks; ++b) *reinterpret_cast<f32x4*>(o + 16 * b) = acc.o[b];
       }
-      p_hh[npend] = hh;
-      p_cnt[npend] = seg_end - tb;
-      p_tot[npend] = c1 - c0;
-      ++npend;
     }
     tb = seg_end;
     ++hh;
   }
-  if (npend > 0) {
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-    int prev = 0;
-    if (lane < npend) prev = atomicAdd(&head_cnt[lane == 0 ? p_hh[0] : p_hh[1]], lane == 0 ? p_cnt[0] : p_cnt[1]);
-    const int prev0 = __shfl(prev, 0, 64), prev1 = __shfl(prev, 1, 64);
-    for (int i = 0; i < npend; ++i) {
-      if ((i == 0 ? prev0 : prev1) + p_cnt[i] != p_tot[i]) continue;
-      const int mh = p_hh[i];
-      const int4 hw = ldc(head_waves, mh);
-      merge_head_mla(part_ml, acc_rsrc, wave_bounds, out, hw.x, hw.y, mh, a.g, r, G);
-      if (lane == 0) __hip_atomic_store(&head_cnt[mh], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Log-sum-exp combine of the split heads, after the decode kernel: one wave
+// per (call head, query head) row, lane l owning latent dims 8l .. 8l+7.  A
+// head whose tiles one wave covered was written by that wave; a head without
+// tiles was zero-filled by the planner.  Partials of head hh are those of the
+// waves wf .. wl spanning its tiles (index w + hh), skipping empty waves.
+__global__ __launch_bounds__(64) void combine_mla_kernel(
+    const int32_t* __restrict__ status, const int32_t* __restrict__ cum_tiles,
+    const int4* __restrict__ head_waves, const int32_t* __restrict__ wave_bounds,
+    const float2* __restrict__ part_ml, const float* __restrict__ part_acc,
+    float* __restrict__ out, int g) {
+  if (load_status(status) != 0) return;
+  const int hh = blockIdx.y, r = blockIdx.x, lane = threadIdx.x;
+  if (ldc(cum_tiles, hh + 1) <= ldc(cum_tiles, hh)) return;
+  const int4 hw = ldc(head_waves, hh);
+  const int wf = hw.x, wl = hw.y;
+  if (wf == wl) return;
+  auto live = [&](int w) { return ldc(wave_bounds, w) < ldc(wave_bounds, w + 1); };
+  const float* ml = reinterpret_cast<const float*>(part_ml) + 2 * r;
+  float M = -INFINITY;
+  for (int w = wf; w <= wl; ++w)
+    if (live(w)) M = fmaxf(M, ml[(static_cast<size_t>(w) + hh) * 2 * kMaxGroup]);
+  float den = 0.f;
+  f32x4 n0 = {0.f, 0.f, 0.f, 0.f}, n1 = {0.f, 0.f, 0.f, 0.f};
+  for (int w0 = wf; w0 <= wl; w0 += kCombineBatch) {
+    float wt[kCombineBatch];
+    f32x4 x0[kCombineBatch], x1[kCombineBatch];
+#pragma unroll
+    for (int u = 0; u < kCombineBatch; ++u) {
+      const int w = w0 + u;
+      const bool lv = w <= wl && live(w);
+      const size_t pid = static_cast<size_t>(lv ? w : wf) + hh;
+      const float* pm = ml + pid * 2 * kMaxGroup;
+      wt[u] = lv ? __builtin_amdgcn_exp2f(pm[0] - M) : 0.f;
+      if (lv) den += wt[u] * pm[1];
+      const f32x4* src = reinterpret_cast<const f32x4*>(part_acc + (pid * g + r) * kDv) + 2 * lane;
+      x0[u] = lv ? src[0] : f32x4{0.f, 0.f, 0.f, 0.f};
+      x1[u] = lv ? src[1] : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int u = 0; u < kCombineBatch; ++u) {
+      n0 += wt[u] * x0[u];
+      n1 += wt[u] * x1[u];
     }
   }
+  const float inv = 1.0f / den;
+  f32x4* o = reinterpret_cast<f32x4*>(out + (static_cast<size_t>(hh) * g + r) * kDv) + 2 * lane;
+  o[0] = n0 * inv;
+  o[1] = n1 * inv;
 }
 
 }  // namespace
@@ -425,7 +387,6 @@ hipError_t launch_decode_mla(const dms_config& c, const Layout& lo, void* meta, 
   char* w = static_cast<char*>(ws);
   MlaParams a;
   a.page_bytes = lo.page_bytes;
-  a.part_acc_bytes = static_cast<int>(static_cast<size_t>(lo.max_partials) * c.group_size * kDv * 4);
   a.g = c.group_size;
   a.maxp = c.max_pages_per_head;
   a.log2P = __builtin_ctz(static_cast<unsigned>(c.page_size));
@@ -437,13 +398,21 @@ hipError_t launch_decode_mla(const dms_config& c, const Layout& lo, void* meta, 
                      reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles),
                      reinterpret_cast<const int32_t*>(w + lo.ws_wave_bounds),
                      reinterpret_cast<const int4*>(w + lo.ws_wave_desc),
-                     reinterpret_cast<const int4*>(w + lo.ws_head_waves),
-                     reinterpret_cast<int32_t*>(w + lo.ws_head_cnt),
                      layer_state(lo, meta, layer).page_table, static_cast<char*>(pool),
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                      reinterpret_cast<float2*>(w + lo.ws_part_ml),
                      reinterpret_cast<float*>(w + lo.ws_part_acc), out, a);
   hipError_t e = hipGetLastError();
+  if (e == hipSuccess && n > 0) {
+    hipLaunchKernelGGL(combine_mla_kernel, dim3(c.group_size, n), dim3(64), 0, st,
+                       reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status),
+                       reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles),
+                       reinterpret_cast<const int4*>(w + lo.ws_head_waves),
+                       reinterpret_cast<const int32_t*>(w + lo.ws_wave_bounds),
+                       reinterpret_cast<const float2*>(w + lo.ws_part_ml),
+                       reinterpret_cast<const float*>(w + lo.ws_part_acc), out, c.group_size);
+    e = hipGetLastError();
+  }
   if (ev_stop) (void)hipEventRecord(ev_stop, st);
   return e;
 }
