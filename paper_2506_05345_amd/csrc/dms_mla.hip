@@ -181,14 +181,15 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
     float2* __restrict__ part_ml, float* __restrict__ part_acc, float* __restrict__ out,
     MlaParams a) {
   __shared__ __attribute__((aligned(16))) char vt_lds[kWavesPerBlock][kDv * kVtStride];
+  __shared__ float2 ml_lds[kWavesPerBlock][kMaxGroup];
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wave = blockIdx.x * kWavesPerBlock + wid;
+  const int unit = blockIdx.x;   // the planner's unit: this block's tile range
   const int r = lane & 15, G = lane >> 4;
   char* vt = vt_lds[wid];
-  const int4 wd0 = ldc(wave_desc, 2 * wave), wd1 = ldc(wave_desc, 2 * wave + 1);
-  int tb = ldc(wave_bounds, wave);
-  const int te = ldc(wave_bounds, wave + 1);
+  const int4 wd0 = ldc(wave_desc, 2 * unit), wd1 = ldc(wave_desc, 2 * unit + 1);
+  int tb = ldc(wave_bounds, unit);
+  const int te = ldc(wave_bounds, unit + 1);
   if (load_status(status) != 0) return;
   if (tb >= te) return;
   const int tpp_log2 = a.log2P - 5;
@@ -218,111 +219,149 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
       return pool + static_cast<size_t>(ldc(uniform_ptr(pt), t >> tpp_log2)) * a.page_bytes +
              static_cast<size_t>(t & tpp_mask) * kTileBytes;
     };
-    // query fragments (B operand of the score MFMA): column r = query head r
-    u32x4 qf[kKBlocks];
-    const char* qrow = reinterpret_cast<const char*>(q + (static_cast<size_t>(hh) * a.g + qr) * kD);
-#pragma unroll
-    for (int s = 0; s < kKBlocks; ++s) {
-      const u32x4 x = *reinterpret_cast<const u32x4*>(qrow + (32 * s + 8 * G) * 2);
-      qf[s] = r < a.g ? x : u32x4{0u, 0u, 0u, 0u};
-    }
     const int t_lo = tb - c0;
     const int t_hi = seg_end - c0;
-    // the token appended by this call (slot d.z) is written into its tile by
-    // the wave whose segment covers it, before the segment's loads
-    if (k_in != nullptr && d.z >= t_lo * kTile && d.z < t_hi * kTile) {
-      char* tile = const_cast<char*>(tile_of(d.z >> 5));
-      const int j = d.z & 31;
-      const uint4* src = reinterpret_cast<const uint4*>(k_in + static_cast<size_t>(hh) * kD);
-      // 72 pieces: one per lane, then 8 more (no lane loop, whose divergent
-      // exit would push the uniform values used after it into VGPRs)
-      *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * lane)) = src[lane];
-      if (lane < kD / 8 - 64)
-        *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * (64 + lane))) = src[64 + lane];
-    }
+    // the segment's tiles are dealt to the block's waves in turn: this wave
+    // takes t_lo + wid, t_lo + wid + 4, ...
+    const int t_first = t_lo + wid;
     Acc acc;
 #pragma unroll
     for (int b = 0; b < kOBlocks; ++b) acc.o[b] = f32x4{0.f, 0.f, 0.f, 0.f};
     acc.m = -INFINITY;
     acc.l = 0.f;
-    // slot of this lane's row in half h: 8 (r / 4) + r % 4 + 4 h
-    const int row0 = 8 * (r >> 2) + (r & 3);
-    // The tile's 36 pieces (half h, k-step s: 1 KB at h * 1024 + s * 2048)
-    // stream through 18 registers sets: piece s of a half is consumed (score
-    // MFMA, latent to LDS) and its register set refilled with the piece 18
-    // positions later -- the other half, or the next tile -- so 17 to 18
-    // pieces (18 KB) stay in flight with 72 registers.
-    u32x4 kr[kKBlocks];
-    const char* cur = tile_of(t_lo) + lane * 16;
-    // issued in piece order (the waits below count on it)
+    if (t_first < t_hi) {
+      // query fragments (B operand of the score MFMA): column r = query head r
+      u32x4 qf[kKBlocks];
+      const char* qrow = reinterpret_cast<const char*>(q + (static_cast<size_t>(hh) * a.g + qr) * kD);
 #pragma unroll
-    for (int s = 0; s < kKBlocks; ++s) {
-      kr[s] = ldkv(cur + s * 2048);
-      __builtin_amdgcn_sched_barrier(0);
+      for (int s = 0; s < kKBlocks; ++s) {
+        const u32x4 x = *reinterpret_cast<const u32x4*>(qrow + (32 * s + 8 * G) * 2);
+        qf[s] = r < a.g ? x : u32x4{0u, 0u, 0u, 0u};
+      }
+      // the token appended by this call (slot d.z) is written into its tile
+      // by the wave that reads that tile, before its loads
+      const int tz = d.z >> 5;
+      if (k_in != nullptr && tz >= t_first && tz < t_hi && ((tz - t_first) & 3) == 0) {
+        char* tile = const_cast<char*>(tile_of(tz));
+        const int j = d.z & 31;
+        const uint4* src = reinterpret_cast<const uint4*>(k_in + static_cast<size_t>(hh) * kD);
+        // 72 pieces: one per lane, then 8 more (no lane loop, whose divergent
+        // exit would push the uniform values used after it into VGPRs)
+        *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * lane)) = src[lane];
+        if (lane < kD / 8 - 64)
+          *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * (64 + lane))) = src[64 + lane];
+      }
+      // slot of this lane's row in half h: 8 (r / 4) + r % 4 + 4 h
+      const int row0 = 8 * (r >> 2) + (r & 3);
+      // The tile's 36 pieces (half h, k-step s: 1 KB at h * 1024 + s * 2048)
+      // stream through 18 registers sets: piece s of a half is consumed
+      // (score MFMA, latent to LDS) and its register set refilled with the
+      // piece 18 positions later -- the other half, or the wave's next tile
+      // -- so 17 to 18 pieces (18 KB) stay in flight with 72 registers.
+      u32x4 kr[kKBlocks];
+      const char* cur = tile_of(t_first) + lane * 16;
+      // issued in piece order (the waits below count on it)
+#pragma unroll
+      for (int s = 0; s < kKBlocks; ++s) {
+        kr[s] = ldkv(cur + s * 2048);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      int t = t_first;
+      for (; t + kWavesPerBlock < t_hi; t += kWavesPerBlock) {
+        const char* nxt = tile_of(t + kWavesPerBlock) + lane * 16;
+        f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < kKBlocks; ++s) {
+          sa = mfma_bf16(kr[s], qf[s], sa);
+          if (s < kLBlocks) piece_to_lds(kr[s], vt, s, row0, true, G);
+          kr[s] = ldkv(cur + 1024 + s * 2048);
+          if (s % 3 == 2) __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int s = 0; s < kKBlocks; ++s) {
+          sb = mfma_bf16(kr[s], qf[s], sb);
+          if (s < kLBlocks) piece_to_lds(kr[s], vt, s, row0 + 4, true, G);
+          kr[s] = ldkv(nxt + s * 2048);
+          if (s % 3 == 2) __builtin_amdgcn_sched_barrier(0);
+        }
+        lds_handoff();
+        finish_tile(acc, sa, sb, vt, a.scale_log2, kTile, r, G);
+        lds_handoff();
+        cur = nxt;
+      }
+      {
+        // the wave's last tile: rows at or past L are stale in the head's last tile
+        const int valid = (t == t_hi - 1 && seg_end == c1) ? L - t * kTile : kTile;
+        f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < kKBlocks; ++s) {
+          sa = mfma_bf16(kr[s], qf[s], sa);
+          if (s < kLBlocks) piece_to_lds(kr[s], vt, s, row0, row0 < valid, G);
+          kr[s] = ldkv(cur + 1024 + s * 2048);
+          if (s % 3 == 2) __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int s = 0; s < kKBlocks; ++s) {
+          sb = mfma_bf16(kr[s], qf[s], sb);
+          if (s < kLBlocks) piece_to_lds(kr[s], vt, s, row0 + 4, row0 + 4 < valid, G);
+        }
+        lds_handoff();
+        finish_tile(acc, sa, sb, vt, a.scale_log2, valid, r, G);
+        lds_handoff();
+      }
     }
-    int t = t_lo;
-    for (; t + 1 < t_hi; ++t) {
-      const char* nxt = tile_of(t + 1) + lane * 16;
-      f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < kKBlocks; ++s) {
-        sa = mfma_bf16(kr[s], qf[s], sa);
-        if (s < kLBlocks) piece_to_lds(kr[s], vt, s, row0, true, G);
-        kr[s] = ldkv(cur + 1024 + s * 2048);
-        if (s % 3 == 2) __builtin_amdgcn_sched_barrier(0);
-      }
-#pragma unroll
-      for (int s = 0; s < kKBlocks; ++s) {
-        sb = mfma_bf16(kr[s], qf[s], sb);
-        if (s < kLBlocks) piece_to_lds(kr[s], vt, s, row0 + 4, true, G);
-        kr[s] = ldkv(nxt + s * 2048);
-        if (s % 3 == 2) __builtin_amdgcn_sched_barrier(0);
-      }
-      lds_handoff();
-      finish_tile(acc, sa, sb, vt, a.scale_log2, kTile, r, G);
-      lds_handoff();
-      cur = nxt;
-    }
-    {
-      // last tile of the segment: rows at or past L are stale
-      const int valid = (seg_end == c1) ? L - t * kTile : kTile;
-      f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < kKBlocks; ++s) {
-        sa = mfma_bf16(kr[s], qf[s], sa);
-        if (s < kLBlocks) piece_to_lds(kr[s], vt, s, row0, row0 < valid, G);
-        kr[s] = ldkv(cur + 1024 + s * 2048);
-        if (s % 3 == 2) __builtin_amdgcn_sched_barrier(0);
-      }
-#pragma unroll
-      for (int s = 0; s < kKBlocks; ++s) {
-        sb = mfma_bf16(kr[s], qf[s], sb);
-        if (s < kLBlocks) piece_to_lds(kr[s], vt, s, row0 + 4, row0 + 4 < valid, G);
-      }
-      lds_handoff();
-      finish_tile(acc, sa, sb, vt, a.scale_log2, valid, r, G);
-      lds_handoff();
-    }
+    // Block combine of the four waves' partials of this head, through LDS:
+    // each wave stages (m, l) and its accumulators in its own area, then
+    // folds the four for 8 of the 32 row blocks.  The result is the head's
+    // output when the block covered all its tiles, else the block's partial
+    // for the combine launch.
     float l = acc.l;
     l += __shfl_xor(l, 16, 64);
     l += __shfl_xor(l, 32, 64);
-    if (tb == c0 && seg_end == c1) {
-      if (r < a.g) {
-        const float inv = 1.0f / l;
+#pragma unroll
+    for (int b = 0; b < kOBlocks; ++b)
+      *reinterpret_cast<f32x4*>(vt + (b * 64 + lane) * 16) = acc.o[b];
+    if (G == 0) ml_lds[wid][r] = make_float2(acc.m, l);
+    __syncthreads();
+    float mj[kWavesPerBlock], M = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kWavesPerBlock; ++j) {
+      mj[j] = ml_lds[j][r].x;
+      M = fmaxf(M, mj[j]);
+    }
+    float den = 0.f, wj[kWavesPerBlock];
+#pragma unroll
+    for (int j = 0; j < kWavesPerBlock; ++j) {
+      wj[j] = __builtin_amdgcn_exp2f(mj[j] - M);   // 0 for a wave without tiles (m = -inf)
+      den += wj[j] * ml_lds[j][r].y;
+    }
+    constexpr int kBlocksPerWave = kOBlocks / kWavesPerBlock;
+    f32x4 num[kBlocksPerWave];
+#pragma unroll
+    for (int i = 0; i < kBlocksPerWave; ++i) {
+      const int b = wid * kBlocksPerWave + i;
+      num[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < kWavesPerBlock; ++j)
+        num[i] += wj[j] * *reinterpret_cast<const f32x4*>(vt_lds[j] + (b * 64 + lane) * 16);
+    }
+    if (r < a.g) {
+      if (tb == c0 && seg_end == c1) {
+        const float inv = 1.0f / den;
         float* o = out + (static_cast<size_t>(hh) * a.g + r) * kDv + 4 * G;
 #pragma unroll
-        for (int b = 0; b < kOBlocks; ++b) *reinterpret_cast<f32x4*>(o + 16 * b) = acc.o[b] * inv;
-      }
-    } else {
-      // split head: this wave's partial, combined by the next launch
-      const size_t pid = static_cast<size_t>(wave) + hh;
-      if (r < a.g) {
-        if (G == 0) part_ml[pid * kMaxGroup + r] = make_float2(acc.m, l);
+        for (int i = 0; i < kBlocksPerWave; ++i)
+          *reinterpret_cast<f32x4*>(o + 16 * (wid * kBlocksPerWave + i)) = num[i] * inv;
+      } else {
+        const size_t pid = static_cast<size_t>(unit) + hh;
+        if (wid == 0 && G == 0) part_ml[pid * kMaxGroup + r] = make_float2(M, den);
         float* o = part_acc + (pid * a.g + r) * kDv + 4 * G;
 #pragma unroll
-        for (int b = 0; b < kOBlocks; ++b) *reinterpret_cast<f32x4*>(o + 16 * b) = acc.o[b];
+        for (int i = 0; i < kBlocksPerWave; ++i)
+          *reinterpret_cast<f32x4*>(o + 16 * (wid * kBlocksPerWave + i)) = num[i];
       }
     }
+    __syncthreads();   // the staged partials are read before the next segment's tiles reuse the areas
     tb = seg_end;
     ++hh;
   }
@@ -345,31 +384,41 @@ __global__ __launch_bounds__(64) void combine_mla_kernel(
   const int wf = hw.x, wl = hw.y;
   if (wf == wl) return;
   auto live = [&](int w) { return ldc(wave_bounds, w) < ldc(wave_bounds, w + 1); };
-  const float* ml = reinterpret_cast<const float*>(part_ml) + 2 * r;
-  float M = -INFINITY;
-  for (int w = wf; w <= wl; ++w)
-    if (live(w)) M = fmaxf(M, ml[(static_cast<size_t>(w) + hh) * 2 * kMaxGroup]);
-  float den = 0.f;
+  // batches of partials: each batch's (m, l) and rows are loaded together
+  // (one round trip), folded into a running maximum, rescaled when it rises
+  float M = -INFINITY, den = 0.f;
   f32x4 n0 = {0.f, 0.f, 0.f, 0.f}, n1 = {0.f, 0.f, 0.f, 0.f};
   for (int w0 = wf; w0 <= wl; w0 += kCombineBatch) {
-    float wt[kCombineBatch];
+    bool lv[kCombineBatch];
+    float2 mv[kCombineBatch];
     f32x4 x0[kCombineBatch], x1[kCombineBatch];
 #pragma unroll
     for (int u = 0; u < kCombineBatch; ++u) {
       const int w = w0 + u;
-      const bool lv = w <= wl && live(w);
-      const size_t pid = static_cast<size_t>(lv ? w : wf) + hh;
-      const float* pm = ml + pid * 2 * kMaxGroup;
-      wt[u] = lv ? __builtin_amdgcn_exp2f(pm[0] - M) : 0.f;
-      if (lv) den += wt[u] * pm[1];
+      lv[u] = w <= wl && live(w);
+      const size_t pid = static_cast<size_t>(lv[u] ? w : wf) + hh;
+      const float2 m = part_ml[pid * kMaxGroup + r];
+      mv[u] = lv[u] ? m : make_float2(-INFINITY, 0.f);
       const f32x4* src = reinterpret_cast<const f32x4*>(part_acc + (pid * g + r) * kDv) + 2 * lane;
-      x0[u] = lv ? src[0] : f32x4{0.f, 0.f, 0.f, 0.f};
-      x1[u] = lv ? src[1] : f32x4{0.f, 0.f, 0.f, 0.f};
+      x0[u] = lv[u] ? src[0] : f32x4{0.f, 0.f, 0.f, 0.f};
+      x1[u] = lv[u] ? src[1] : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    float bm = mv[0].x;
+#pragma unroll
+    for (int u = 1; u < kCombineBatch; ++u) bm = fmaxf(bm, mv[u].x);
+    if (bm > M) {   // the first batch always raises M from -inf (weight 0 for the zero sums)
+      const float sc = __builtin_amdgcn_exp2f(M - bm);
+      den *= sc;
+      n0 *= sc;
+      n1 *= sc;
+      M = bm;
     }
 #pragma unroll
     for (int u = 0; u < kCombineBatch; ++u) {
-      n0 += wt[u] * x0[u];
-      n1 += wt[u] * x1[u];
+      const float wt = lv[u] ? __builtin_amdgcn_exp2f(mv[u].x - M) : 0.f;
+      den += wt * mv[u].y;
+      n0 += wt * x0[u];
+      n1 += wt * x1[u];
     }
   }
   const float inv = 1.0f / den;
@@ -392,7 +441,7 @@ hipError_t launch_decode_mla(const dms_config& c, const Layout& lo, void* meta, 
   a.log2P = __builtin_ctz(static_cast<unsigned>(c.page_size));
   a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
   if (ev_start) (void)hipEventRecord(ev_start, st);
-  hipLaunchKernelGGL(decode_mla_kernel, dim3(waves / kWavesPerBlock), dim3(256), 0, st,
+  hipLaunchKernelGGL(decode_mla_kernel, dim3(waves), dim3(256), 0, st,
                      reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status),
                      reinterpret_cast<const HeadDesc*>(w + lo.ws_head_desc),
                      reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles),
@@ -424,9 +473,9 @@ int decode_mla_resident_waves() {
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_mla_kernel, 256, 0) != hipSuccess ||
       blocks < 1)
     return -1;
-  int waves = cus * kWavesPerBlock;
-  if (waves > kMaxWaves) waves = kMaxWaves / kWavesPerBlock * kWavesPerBlock;
-  return waves;
+  // the planner's units are blocks (one per CU): each block's four waves
+  // share its tile range
+  return cus < kMaxWaves ? cus : kMaxWaves;
 }
 
 }  // namespace dms
