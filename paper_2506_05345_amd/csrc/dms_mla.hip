@@ -12,12 +12,15 @@
 // a row by q . row over all 576 dims and its output is the softmax-weighted
 // sum of the rows' first 512 dims (the latent; W_UV is applied by the caller).
 //
-// The kernel follows decode_kernel (dms_decode.hip) in its work split: the
-// planner's equal tile ranges per wave, one wave per SIMD.  A split head's
-// partials (16 heads x 512 float32 per wave, 16x the standard kernel's) are
-// combined by a second launch with one wave per output row, not by the last
-// arriving wave, whose lone merge of a head's partials would be a
-// latency-bound tail.  Per 32-slot tile:
+// Work split: the planner's units are blocks (one per CU), each taking an
+// equal contiguous share of the call's tiles; a block deals each segment's
+// tiles (the part of one head in its share) to its four waves in turn, and at
+// the segment's end the four fold their partials through LDS -- into the
+// head's output when the block covered the whole head, else into one partial
+// per (block, head).  Those partials (16 heads x 512 float32, 16x the
+// standard kernel's per split) are merged by a second launch with one wave
+// per output row rather than by the last block to finish, whose lone merge
+// would be a latency-bound tail.  Per 32-slot tile:
 //  * keys: the row is stored in the fragment order of the 16x16x32 score
 //    MFMA (A operand: tile rows, k = 32 dims); the tile is read in two halves
 //    of 16 rows, half h holding slots 8(r/4) + r%4 + 4h, with the next half's
