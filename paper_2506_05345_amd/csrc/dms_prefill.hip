@@ -16,8 +16,9 @@
 //
 // Pass 0 lists the kept chunk tokens; pass 1 copies the chunk's keys and
 // values, in chunk order and in kept order, into workspace tiles in the
-// pool's tile layout (keys [d/32][32][32], values transposed [d][32]), so the
-// attention pass stages every source the same way.
+// pool's tile layout (16-byte pieces in the decode MFMAs' fragment order:
+// keys by (k-step, half, lane), values transposed), so the attention pass
+// stages every source the same way.
 //
 // Attention pass: a workgroup (4 waves) owns one (sequence, KV head, block of
 // query positions).  Its columns are (position, query head) pairs packed 16
@@ -155,7 +156,7 @@ __device__ inline size_t ws_tile(const PrefillArgs& a, int region, int h, int i,
 // Pass 1 (one block per (32-token tile, sequence x head, region)): copy the
 // chunk's keys and values -- region 0: in chunk order; region 1: the kept
 // tokens in list order -- into workspace tiles in the pool's tile layout
-// (keys [d/32][32][32], values transposed [d][32]); rows past the end are 0.
+// (fragment order, values transposed); rows past the end are 0.
 template <int D, bool FP8>
 __global__ __launch_bounds__(kThreads) void prefill_tile_kernel(PrefillArgs a) {
   __shared__ uint16_t vrows[32][D + 2];
