@@ -906,8 +906,7 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
             "traffic_source": "profiles/" + traffic_profile if traffic is not None else None,
-            "kernel": ("decode_mla_kernel + combine_mla_kernel (split-head combine launch)" if mla
-                       else f"decode_kernel<{D}>"),
+            "kernel": "decode_mla_kernel" if mla else f"decode_kernel<{D}>",
             "kernel_timing": "HIP events around each decode launch, eager pass of the next "
                              f"{args.steps} steps",
             "kernel_avg_us": round(1e3 * kern_avg_ms, 2),

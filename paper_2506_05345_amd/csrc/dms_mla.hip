@@ -17,10 +17,12 @@
 // tiles (the part of one head in its share) to its four waves in turn, and at
 // the segment's end the four fold their partials through LDS -- into the
 // head's output when the block covered the whole head, else into one partial
-// per (block, head).  Those partials (16 heads x 512 float32, 16x the
-// standard kernel's per split) are merged by a second launch with one wave
-// per output row rather than by the last block to finish, whose lone merge
-// would be a latency-bound tail.  Per 32-slot tile:
+// per (block, head), a few per head.  The block that completes a split
+// head's tile count merges its partials (each wave folding a quarter of the
+// dims, partials loaded in batches), as the standard kernel's last arriving
+// wave does; with one partial per wave (16 heads x 512 float32 each, 16x the
+// standard kernel's) that lone merge was a latency-bound tail, and a separate
+// combine launch cost more than folding in LDS first.  Per 32-slot tile:
 //  * keys: the row is stored in the fragment order of the 16x16x32 score
 //    MFMA (A operand: tile rows, k = 32 dims); the tile is read in two halves
 //    of 16 rows, half h holding slots 8(r/4) + r%4 + 4h, with the next half's
@@ -50,7 +52,7 @@ constexpr int kLBlocks = kDv / 32;      // of them latent (16)
 constexpr int kOBlocks = kDv / 16;      // 16-dim row blocks of O^T (32)
 constexpr int kVtStride = 72;           // LDS bytes per latent dim: 32 slots + pad
 constexpr float kRescale = 8.0f;        // lazy rescale threshold, log2 units
-constexpr int kCombineBatch = 8;        // partials whose rows a combine wave loads together
+constexpr int kMergeBatch = 4;             // partials a merge loads together
 constexpr int kPvGroup = 4;             // PV blocks whose V^T reads are in flight together
 
 __device__ inline int load_status(const int32_t* status) {
@@ -83,8 +85,19 @@ __device__ inline u32x4 ldkv(const char* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 }
 
+__device__ inline void store_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline float load_coherent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+constexpr int kWaitVmcnt0 = 0x0F70;       // s_waitcnt vmcnt(0)
+constexpr int kBufferDword3 = 0x00020000;
+constexpr int kCachePolicySc1 = 0x10;     // coherent at the device level (past the die's L2)
+
 struct MlaParams {
   size_t page_bytes;
+  int part_acc_bytes;   // size of the partial accumulator area (< 2 GiB)
   int g, maxp, log2P;
   float scale_log2;
 };
@@ -179,12 +192,14 @@ __device__ inline void finish_tile(Acc& acc, f32x4 sa, f32x4 sb, const char* vt,
 __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
     const int32_t* __restrict__ status, const HeadDesc* __restrict__ desc,
     const int32_t* __restrict__ cum_tiles, const int32_t* __restrict__ wave_bounds,
-    const int4* __restrict__ wave_desc, const int32_t* __restrict__ page_table,
+    const int4* __restrict__ wave_desc, const int4* __restrict__ head_waves,
+    int32_t* __restrict__ head_cnt, const int32_t* __restrict__ page_table,
     char* __restrict__ pool, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_in,
     float2* __restrict__ part_ml, float* __restrict__ part_acc, float* __restrict__ out,
     MlaParams a) {
   __shared__ __attribute__((aligned(16))) char vt_lds[kWavesPerBlock][kDv * kVtStride];
   __shared__ float2 ml_lds[kWavesPerBlock][kMaxGroup];
+  __shared__ int s_last;
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int unit = blockIdx.x;   // the planner's unit: this block's tile range
@@ -201,6 +216,8 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
   int hh = wd0.z;
   bool first = true;
   const int qr = min(r, a.g - 1);
+  const __amdgpu_buffer_rsrc_t acc_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      part_acc, static_cast<short>(0), a.part_acc_bytes, kBufferDword3);
   while (tb < te) {
     int c0, c1;
     HeadDesc d;
@@ -317,7 +334,7 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
     // each wave stages (m, l) and its accumulators in its own area, then
     // folds the four for 8 of the 32 row blocks.  The result is the head's
     // output when the block covered all its tiles, else the block's partial
-    // for the combine launch.
+    // of a split head.
     float l = acc.l;
     l += __shfl_xor(l, 16, 64);
     l += __shfl_xor(l, 32, 64);
@@ -356,78 +373,92 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
         for (int i = 0; i < kBlocksPerWave; ++i)
           *reinterpret_cast<f32x4*>(o + 16 * (wid * kBlocksPerWave + i)) = num[i] * inv;
       } else {
+        // the block's partial, with stores that are complete at the device's
+        // coherence point once this wave's vmcnt drains
         const size_t pid = static_cast<size_t>(unit) + hh;
-        if (wid == 0 && G == 0) part_ml[pid * kMaxGroup + r] = make_float2(M, den);
-        float* o = part_acc + (pid * a.g + r) * kDv + 4 * G;
+        if (wid == 0 && G == 0) {
+          float* ml = reinterpret_cast<float*>(part_ml + pid * kMaxGroup + r);
+          store_coherent(ml, M);
+          store_coherent(ml + 1, den);
+        }
+        const uint32_t o = static_cast<uint32_t>(((pid * a.g + r) * kDv + 4 * G) * 4);
 #pragma unroll
         for (int i = 0; i < kBlocksPerWave; ++i)
-          *reinterpret_cast<f32x4*>(o + 16 * (wid * kBlocksPerWave + i)) = num[i];
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, num[i]), acc_rsrc,
+                                                 o + 64 * (wid * kBlocksPerWave + i), 0, kCachePolicySc1);
+      }
+    }
+    if (!(tb == c0 && seg_end == c1)) {
+      // Split head: once the block's partial is stored, add its tiles to the
+      // head's arrival counter; the block that completes the count merges
+      // the head's partials (one per block, a few per head), each wave
+      // folding its 8 row blocks, and resets the counter.
+      __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        const int prev = atomicAdd(&head_cnt[hh], seg_end - tb);
+        s_last = prev + (seg_end - tb) == c1 - c0;
+      }
+      __syncthreads();
+      if (s_last) {
+        // batches of kMergeBatch partials: their (m, l) and rows are loaded
+        // together (one round trip) and folded into a running maximum
+        const int4 hw = ldc(head_waves, hh);
+        float Mh = -INFINITY, dh = 0.f;
+        f32x4 nh[kBlocksPerWave];
+#pragma unroll
+        for (int i = 0; i < kBlocksPerWave; ++i) nh[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int u0 = hw.x; u0 <= hw.y; u0 += kMergeBatch) {
+          bool lv[kMergeBatch];
+          float mv[kMergeBatch], lv_l[kMergeBatch];
+          u32x4 x[kMergeBatch][kBlocksPerWave];
+#pragma unroll
+          for (int j = 0; j < kMergeBatch; ++j) {
+            const int u = u0 + j;
+            lv[j] = u <= hw.y && ldc(wave_bounds, u) < ldc(wave_bounds, u + 1);
+            const size_t pid = static_cast<size_t>(lv[j] ? u : hw.x) + hh;
+            const float* ml = reinterpret_cast<const float*>(part_ml + pid * kMaxGroup + r);
+            mv[j] = lv[j] ? load_coherent(ml) : -INFINITY;
+            lv_l[j] = lv[j] ? load_coherent(ml + 1) : 0.f;
+            const uint32_t o = static_cast<uint32_t>(((pid * a.g + (r < a.g ? r : 0)) * kDv + 4 * G) * 4);
+#pragma unroll
+            for (int i = 0; i < kBlocksPerWave; ++i)
+              x[j][i] = lv[j] ? __builtin_amdgcn_raw_buffer_load_b128(acc_rsrc, o + 64 * (wid * kBlocksPerWave + i), 0,
+                                                                       kCachePolicySc1)
+                              : u32x4{0u, 0u, 0u, 0u};
+          }
+          float bm = mv[0];
+#pragma unroll
+          for (int j = 1; j < kMergeBatch; ++j) bm = fmaxf(bm, mv[j]);
+          if (bm > Mh) {   // the first batch always raises Mh from -inf (its sums are 0)
+            const float sc = __builtin_amdgcn_exp2f(Mh - bm);
+            dh *= sc;
+#pragma unroll
+            for (int i = 0; i < kBlocksPerWave; ++i) nh[i] *= sc;
+            Mh = bm;
+          }
+#pragma unroll
+          for (int j = 0; j < kMergeBatch; ++j) {
+            const float wt = lv[j] ? __builtin_amdgcn_exp2f(mv[j] - Mh) : 0.f;
+            dh += wt * lv_l[j];
+#pragma unroll
+            for (int i = 0; i < kBlocksPerWave; ++i) nh[i] += wt * __builtin_bit_cast(f32x4, x[j][i]);
+          }
+        }
+        if (r < a.g) {
+          const float inv = 1.0f / dh;
+          float* o = out + (static_cast<size_t>(hh) * a.g + r) * kDv + 4 * G;
+#pragma unroll
+          for (int i = 0; i < kBlocksPerWave; ++i)
+            *reinterpret_cast<f32x4*>(o + 16 * (wid * kBlocksPerWave + i)) = nh[i] * inv;
+        }
+        if (threadIdx.x == 0) __hip_atomic_store(&head_cnt[hh], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
     __syncthreads();   // the staged partials are read before the next segment's tiles reuse the areas
     tb = seg_end;
     ++hh;
   }
-}
-
-// Log-sum-exp combine of the split heads, after the decode kernel: one wave
-// per (call head, query head) row, lane l owning latent dims 8l .. 8l+7.  A
-// head whose tiles one wave covered was written by that wave; a head without
-// tiles was zero-filled by the planner.  Partials of head hh are those of the
-// waves wf .. wl spanning its tiles (index w + hh), skipping empty waves.
-__global__ __launch_bounds__(64) void combine_mla_kernel(
-    const int32_t* __restrict__ status, const int32_t* __restrict__ cum_tiles,
-    const int4* __restrict__ head_waves, const int32_t* __restrict__ wave_bounds,
-    const float2* __restrict__ part_ml, const float* __restrict__ part_acc,
-    float* __restrict__ out, int g) {
-  if (load_status(status) != 0) return;
-  const int hh = blockIdx.y, r = blockIdx.x, lane = threadIdx.x;
-  if (ldc(cum_tiles, hh + 1) <= ldc(cum_tiles, hh)) return;
-  const int4 hw = ldc(head_waves, hh);
-  const int wf = hw.x, wl = hw.y;
-  if (wf == wl) return;
-  auto live = [&](int w) { return ldc(wave_bounds, w) < ldc(wave_bounds, w + 1); };
-  // batches of partials: each batch's (m, l) and rows are loaded together
-  // (one round trip), folded into a running maximum, rescaled when it rises
-  float M = -INFINITY, den = 0.f;
-  f32x4 n0 = {0.f, 0.f, 0.f, 0.f}, n1 = {0.f, 0.f, 0.f, 0.f};
-  for (int w0 = wf; w0 <= wl; w0 += kCombineBatch) {
-    bool lv[kCombineBatch];
-    float2 mv[kCombineBatch];
-    f32x4 x0[kCombineBatch], x1[kCombineBatch];
-#pragma unroll
-    for (int u = 0; u < kCombineBatch; ++u) {
-      const int w = w0 + u;
-      lv[u] = w <= wl && live(w);
-      const size_t pid = static_cast<size_t>(lv[u] ? w : wf) + hh;
-      const float2 m = part_ml[pid * kMaxGroup + r];
-      mv[u] = lv[u] ? m : make_float2(-INFINITY, 0.f);
-      const f32x4* src = reinterpret_cast<const f32x4*>(part_acc + (pid * g + r) * kDv) + 2 * lane;
-      x0[u] = lv[u] ? src[0] : f32x4{0.f, 0.f, 0.f, 0.f};
-      x1[u] = lv[u] ? src[1] : f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-    float bm = mv[0].x;
-#pragma unroll
-    for (int u = 1; u < kCombineBatch; ++u) bm = fmaxf(bm, mv[u].x);
-    if (bm > M) {   // the first batch always raises M from -inf (weight 0 for the zero sums)
-      const float sc = __builtin_amdgcn_exp2f(M - bm);
-      den *= sc;
-      n0 *= sc;
-      n1 *= sc;
-      M = bm;
-    }
-#pragma unroll
-    for (int u = 0; u < kCombineBatch; ++u) {
-      const float wt = lv[u] ? __builtin_amdgcn_exp2f(mv[u].x - M) : 0.f;
-      den += wt * mv[u].y;
-      n0 += wt * x0[u];
-      n1 += wt * x1[u];
-    }
-  }
-  const float inv = 1.0f / den;
-  f32x4* o = reinterpret_cast<f32x4*>(out + (static_cast<size_t>(hh) * g + r) * kDv) + 2 * lane;
-  o[0] = n0 * inv;
-  o[1] = n1 * inv;
 }
 
 }  // namespace
@@ -439,6 +470,7 @@ hipError_t launch_decode_mla(const dms_config& c, const Layout& lo, void* meta, 
   char* w = static_cast<char*>(ws);
   MlaParams a;
   a.page_bytes = lo.page_bytes;
+  a.part_acc_bytes = static_cast<int>(static_cast<size_t>(lo.max_partials) * c.group_size * kDv * 4);
   a.g = c.group_size;
   a.maxp = c.max_pages_per_head;
   a.log2P = __builtin_ctz(static_cast<unsigned>(c.page_size));
@@ -450,21 +482,13 @@ hipError_t launch_decode_mla(const dms_config& c, const Layout& lo, void* meta, 
                      reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles),
                      reinterpret_cast<const int32_t*>(w + lo.ws_wave_bounds),
                      reinterpret_cast<const int4*>(w + lo.ws_wave_desc),
+                     reinterpret_cast<const int4*>(w + lo.ws_head_waves),
+                     reinterpret_cast<int32_t*>(w + lo.ws_head_cnt),
                      layer_state(lo, meta, layer).page_table, static_cast<char*>(pool),
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                      reinterpret_cast<float2*>(w + lo.ws_part_ml),
                      reinterpret_cast<float*>(w + lo.ws_part_acc), out, a);
   hipError_t e = hipGetLastError();
-  if (e == hipSuccess && n > 0) {
-    hipLaunchKernelGGL(combine_mla_kernel, dim3(c.group_size, n), dim3(64), 0, st,
-                       reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status),
-                       reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles),
-                       reinterpret_cast<const int4*>(w + lo.ws_head_waves),
-                       reinterpret_cast<const int32_t*>(w + lo.ws_wave_bounds),
-                       reinterpret_cast<const float2*>(w + lo.ws_part_ml),
-                       reinterpret_cast<const float*>(w + lo.ws_part_acc), out, c.group_size);
-    e = hipGetLastError();
-  }
   if (ev_stop) (void)hipEventRecord(ev_stop, st);
   return e;
 }
