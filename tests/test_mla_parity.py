@@ -200,3 +200,66 @@ def test_mla_prefill_is_refused():
     with pytest.raises(dms.DmsError):
         dms.dms_prefill_chunk(cache.ctx, 0, 1, sid, cu, 4, 4, x, x, None, fl, out)
     cache.close()
+
+
+def test_mla_graph_replays_match_eager():
+    """Latent-attention decode steps (two layers) captured once into a HIP
+    graph and replayed with eager work in between: every replay equals an
+    eager run of the same step on an identical cache, outputs bitwise and
+    state bit-exact (split heads merge partials in unit order whichever
+    block completes them)."""
+    torch = _torch()
+    from paper_2506_05345_amd import dms
+    g, w, P, T0, REPLAYS = 16, 16, 64, 700, 4
+    seqs = [2, 0, 1]
+    kw = dict(num_layers=2, max_seqs=3, num_kv_heads=1, group_size=g, head_dim=ROW, window=w,
+              page_size=P, num_pages=120, max_pages_per_head=32, max_chunk_tokens=3 * T0,
+              kv_format=dms.DMS_KV_MLA)
+    cfg = dms.make_config(**kw)
+    eager, graphed = dms.DmsCache(cfg), dms.DmsCache(cfg)
+    inp = {s: MlaInputs(67, s, T0 + REPLAYS, g, 0.6) for s in seqs}
+    sid = to_dev(np.array(seqs, np.int32))
+    cu = to_dev(np.array([0, T0, 2 * T0, 3 * T0], np.int32))
+    kk = to_dev(np.concatenate([inp[s].k[:T0] for s in seqs]))
+    ff = to_dev(np.concatenate([inp[s].flags[:T0] for s in seqs]))
+    for c in (eager, graphed):
+        for layer in (0, 1):
+            dms.dms_append_chunk(c.ctx, layer, 3, sid, cu, 3 * T0, T0, kk, None, ff)
+    torch.cuda.synchronize()
+    qb = torch.empty((3, g, ROW), dtype=torch.bfloat16, device="cuda")
+    kb = torch.empty((3, 1, ROW), dtype=torch.bfloat16, device="cuda")
+    fb = torch.empty((3, 1), dtype=torch.uint8, device="cuda")
+    outs = [torch.empty((3, g, LATENT), device="cuda") for _ in range(2)]
+
+    def fill(t):
+        qb.copy_(to_dev(np.stack([inp[s].q[t] for s in seqs])))
+        kb.copy_(to_dev(np.stack([inp[s].k[t] for s in seqs])))
+        fb.copy_(to_dev(np.stack([inp[s].flags[t] for s in seqs])))
+
+    def step(c):
+        for layer in (0, 1):
+            dms.dms_decode_step(c.ctx, layer, 3, sid, qb, kb, None, fb, outs[layer])
+
+    fill(T0)
+    torch.cuda.synchronize()
+    gr = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gr):
+        step(graphed)
+    torch.cuda.synchronize()
+    for r in range(REPLAYS):
+        fill(T0 + r)
+        torch.cuda.synchronize()
+        gr.replay()
+        torch.cuda.synchronize()
+        got = [o.clone() for o in outs]
+        step(eager)
+        torch.cuda.synchronize()
+        for layer in (0, 1):
+            assert torch.equal(got[layer], outs[layer]), (r, layer)
+            a, b = eager.export(layer), graphed.export(layer)
+            for f in ("pos", "L", "ring_slot", "ring_flag", "page_table", "stack"):
+                assert np.array_equal(getattr(a, f), getattr(b, f)), (r, layer, f)
+        assert dms.dms_status(graphed.ctx) == 0 and dms.dms_status(eager.ctx) == 0
+        _ = torch.ones(1000, device="cuda").sum().item()
+    eager.close()
+    graphed.close()
