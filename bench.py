@@ -300,6 +300,27 @@ def cpu_baseline(wl, ctx, budget_s=12.0):
     }
 
 
+def chunk_visible_counts(L0, pos, flags_back, w):
+    """Keys visible to every query of a prefill chunk, per KV head.
+
+    After a token's append the live slots of its head are exactly the keys
+    visible to it, so the count at chunk token c is the head's retained count
+    after appending tokens 0 .. c: the count before the chunk, L0 [n, H], plus
+    one for every chunk token that took a fresh slot (position < w, or the
+    token w positions earlier was kept).  pos [n, C] positions of the chunk
+    tokens; flags_back [n, C, H] decisions of the tokens at pos - w (ignored
+    where pos < w).  Returns int64 [n, C, H]."""
+    import torch
+    fresh = ((pos[..., None] < w) | (flags_back == 0)).to(torch.int64)
+    return L0.to(torch.int64)[:, None, :] + torch.cumsum(fresh, dim=1)
+
+
+def prefill_flops(visible_counts, group, head_dim):
+    """Algorithmic flops of masked prefill: q.k and p.v over every visible
+    (query, key) pair of every query head of the group, 4 d flops each."""
+    return float(visible_counts.sum()) * group * 4 * head_dim
+
+
 STRESS = dict(layers=64, batch=32, kv_heads=8, group=5, head_dim=128, prefill_seqs=4,
               chunk=4096, ctx_lo=1024, ctx_hi=131072)
 
@@ -407,10 +428,9 @@ def run_stress(args):
                               for s in pf])
             pseq = torch.as_tensor(np.repeat(pf, C), device=dev)
             fp[layer, st] = flags(layer, pseq, ppos)
-            prev = flags(layer, pseq, ppos - w)
-            fresh = ((ppos[:, None] < w) | (prev == 0)).to(torch.int64).view(npf, C, H)
-            Lq = L[torch.as_tensor(pf, device=dev)][:, None, :] + torch.cumsum(fresh, dim=1)
-            flops[st] += float(Lq.sum()) * g * 4 * D
+            prev = flags(layer, pseq, ppos - w).view(npf, C, H)
+            Lq = chunk_visible_counts(L[torch.as_tensor(pf, device=dev)], ppos.view(npf, C), prev, w)
+            flops[st] += prefill_flops(Lq, g, D)
             L[torch.as_tensor(pf, device=dev)] = Lq[:, -1]
             dpos = torch.as_tensor(ctx[dc] + st, device=dev)
             dseq = torch.as_tensor(dc, device=dev)

@@ -30,7 +30,7 @@ import math
 import numpy as np
 
 __all__ = ["logistic_noise", "gumbel_sigmoid", "gumbel_sigmoid_grad", "train_attention",
-           "train_attention_grads", "dms_additive_bias"]
+           "train_attention_grads"]
 
 
 def logistic_noise(u):
@@ -50,18 +50,6 @@ def gumbel_sigmoid_grad(alpha, dalpha, tau):
     """d loss / d logit = d loss / d alpha * alpha (1 - alpha) / tau."""
     a = np.asarray(alpha, np.float64)
     return np.asarray(dalpha, np.float64) * a * (1.0 - a) / tau
-
-
-def dms_additive_bias(alpha_h, w):
-    """M_alpha of one KV head, [T, T] float64 (row = query, column = key)."""
-    a = np.asarray(alpha_h, np.float64)
-    T = a.shape[0]
-    t = np.arange(T)[:, None]
-    j = np.arange(T)[None, :]
-    with np.errstate(divide="ignore"):
-        outside = np.log1p(-a)[None, :] * np.ones((T, 1))
-    m = np.where(j > t, -np.inf, np.where(j > t - w, 0.0, outside))
-    return m
 
 
 def _torch_attention(q, k, v, alpha, w, group, scale):

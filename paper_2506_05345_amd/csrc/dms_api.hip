@@ -22,11 +22,17 @@ int validate_config(const dms_config& c) {
     if (c.head_dim != kMlaDim) return DMS_ERR_UNSUPPORTED;
     if (c.num_kv_heads != 1 || c.decision_source != DMS_DECIDE_CALLER || c.quest_page_budget != 0)
       return DMS_ERR_UNSUPPORTED;
-    // split partials are addressed with 32-bit byte offsets
-    if (static_cast<int64_t>(kMaxWaves + c.max_seqs) * c.group_size * kMlaLatent * 4 >= (int64_t(1) << 31))
-      return DMS_ERR_UNSUPPORTED;
   } else if (c.head_dim != 64 && c.head_dim != 128) {
     return DMS_ERR_UNSUPPORTED;
+  }
+  // Split-K partial accumulators (one g x row-width float32 block per
+  // partial, kMaxWaves + max_seqs * Hkv partials) are addressed through a
+  // buffer resource with 32-bit byte offsets, so their area must stay below
+  // 2 GiB for every page format.
+  {
+    const int64_t row = c.kv_format == DMS_KV_MLA ? kMlaLatent : c.head_dim;
+    const int64_t partials = kMaxWaves + static_cast<int64_t>(c.max_seqs) * c.num_kv_heads;
+    if (partials * c.group_size * row * 4 >= (int64_t(1) << 31)) return DMS_ERR_UNSUPPORTED;
   }
   if (c.page_size != 32 && c.page_size != 64 && c.page_size != 128 && c.page_size != 256)
     return DMS_ERR_INVALID;

@@ -93,7 +93,7 @@ constexpr int kCachePolicySc1 = 0x10;
 
 struct DecodeParams {
   size_t page_bytes;
-  int part_acc_bytes;   // size of the split-K accumulator area (< 2 GiB)
+  int part_acc_bytes;   // size of the split-K accumulator area (< 2 GiB: validate_config)
   int NH, g, maxp, P, log2P, W;
   int zero_neuron;   // element 0 of the group's first query head is read as 0
   int qB;            // page retrieval: pages attended per head (selection stride)

@@ -61,10 +61,31 @@ def _cfg(**kw):
     (dict(quest_page_budget=17), dms.DMS_ERR_INVALID),                     # > max_pages_per_head
     (dict(quest_page_budget=4, max_pages_per_head=5000), dms.DMS_ERR_UNSUPPORTED),
     (dict(kv_format=-1), dms.DMS_ERR_INVALID),
+    # split-K partial accumulators past 2 GiB (32-bit buffer offsets), for every page format
+    (dict(max_seqs=65536, num_kv_heads=8, group_size=16, head_dim=128), dms.DMS_ERR_UNSUPPORTED),
+    (dict(max_seqs=65536, num_kv_heads=8, group_size=16, head_dim=128, kv_format=1),
+     dms.DMS_ERR_UNSUPPORTED),
+    (dict(max_seqs=32768, num_kv_heads=16, group_size=16, head_dim=64), dms.DMS_ERR_UNSUPPORTED),
+    (dict(max_seqs=65536, num_kv_heads=1, group_size=16, head_dim=576, kv_format=2),
+     dms.DMS_ERR_UNSUPPORTED),
 ])
 def test_bad_configuration(kw, code):
     rc = dms.lib().dms_layout(ctypes.byref(_cfg(**kw)), None, None, None, None)
     assert rc == code
+
+
+# Largest-partials configurations below the 2 GiB bound: (8192 + S * Hkv) * g * row * 4 bytes.
+@pytest.mark.parametrize("kw", [
+    dict(max_seqs=4096, num_kv_heads=8, group_size=16, head_dim=128),
+    dict(max_seqs=65536, num_kv_heads=8, group_size=1, head_dim=128, kv_format=1),
+    dict(max_seqs=8192, num_kv_heads=1, group_size=16, head_dim=576, kv_format=2),
+])
+def test_partial_area_just_below_the_bound_is_accepted(kw):
+    cfg = _cfg(**kw)
+    row = 512 if kw.get("kv_format") == 2 else kw["head_dim"]
+    assert (8192 + cfg.max_seqs * cfg.num_kv_heads) * cfg.group_size * row * 4 < 2 ** 31
+    m, p, w, pg = dms.dms_layout(cfg)
+    assert w >= (8192 + cfg.max_seqs * cfg.num_kv_heads) * cfg.group_size * row * 4
 
 
 def test_layout_sizes():
