@@ -162,6 +162,70 @@ def _check(rc, where):
         raise DmsError(rc, where)
 
 
+# Configuration of every live context (by handle), for the argument checks.
+_CTX_CFG = {}
+
+_BF16 = "bf16"
+_U8 = "uint8"
+_I32 = "int32"
+_F32 = "float32"
+
+
+def _args(where, *specs):
+    """Check tensor arguments before their addresses are handed to the library.
+    Each spec is (tensor, name, element type, minimum element count).  Element
+    types of all arguments are checked first, then that each is a contiguous
+    GPU tensor with enough elements.  Integers (raw device addresses) and None
+    pass through; the library checks null pointers itself."""
+    import torch
+    kinds = {_BF16: torch.bfloat16, _U8: torch.uint8, _I32: torch.int32, _F32: torch.float32}
+    live = []
+    for x, name, kind, count in specs:
+        if x is None or isinstance(x, int):
+            continue
+        if not isinstance(x, torch.Tensor):
+            raise TypeError(f"{where}: {name} must be a tensor or a device address, got {type(x)}")
+        if x.dtype != kinds[kind]:
+            raise DmsError(DMS_ERR_INVALID, f"{where}: {name} must be {kind}, got {x.dtype}")
+        live.append((x, name, count))
+    for x, name, count in live:
+        if not x.is_cuda:
+            raise DmsError(DMS_ERR_INVALID, f"{where}: {name} must be a GPU tensor")
+        if not x.is_contiguous():
+            raise DmsError(DMS_ERR_INVALID, f"{where}: {name} must be contiguous")
+        if x.numel() < count:
+            raise DmsError(DMS_ERR_INVALID,
+                           f"{where}: {name} holds {x.numel()} elements, needs {count}")
+
+
+def _arg(x, name, kind, count, where):
+    _args(where, (x, name, kind, count))
+
+
+def _dims(ctx):
+    """(Hkv, Hq, d, output row width) of a context's configuration, or None for
+    a handle this module did not create."""
+    c = _CTX_CFG.get(ctx)
+    if c is None:
+        return None
+    out_d = MLA_LATENT_DIM if c.kv_format == DMS_KV_MLA else c.head_dim
+    return c.num_kv_heads, c.num_kv_heads * c.group_size, c.head_dim, out_d
+
+
+def _check_kv_args(ctx, where, n, rows, seq_ids=None, cu=None, k=None, v=None, flags=None,
+                   q=None, out=None, decisions=None):
+    """seq_ids [n] and cu_seqlens [n + 1] int32; per-row tensors for `rows`
+    rows (tokens of a chunk, or one per sequence)."""
+    specs = [(seq_ids, "seq_ids", _I32, n), (cu, "cu_seqlens", _I32, n + 1)]
+    dims = _dims(ctx)
+    if dims is not None:
+        H, Hq, D, Dout = dims
+        specs += [(k, "k", _BF16, rows * H * D), (v, "v", _BF16, rows * H * D),
+                  (flags, "flags", _U8, rows * H), (decisions, "decisions_out", _U8, rows * H),
+                  (q, "q", _BF16, rows * Hq * D), (out, "out", _F32, rows * Hq * Dout)]
+    _args(where, *specs)
+
+
 def make_config(num_layers, max_seqs, num_kv_heads, group_size, head_dim, window,
                 page_size, num_pages, max_pages_per_head, max_chunk_tokens=0,
                 softmax_scale=0.0, eviction=DMS_EVICT_DELAYED,
@@ -195,11 +259,13 @@ def dms_create(cfg: DmsConfig, meta, pools, workspace):
     out = _VP()
     _check(lib().dms_create(ctypes.byref(cfg), _ptr(meta), arr, _ptr(workspace),
                             ctypes.byref(out)), "dms_create")
+    _CTX_CFG[out.value] = DmsConfig.from_buffer_copy(cfg)
     return out.value
 
 
 def dms_destroy(ctx):
     _check(lib().dms_destroy(ctx), "dms_destroy")
+    _CTX_CFG.pop(ctx, None)
 
 
 def dms_init_state(ctx, stream=None):
@@ -207,25 +273,32 @@ def dms_init_state(ctx, stream=None):
 
 
 def dms_seq_reset(ctx, layer, n, seq_ids, stream=None):
+    _arg(seq_ids, "seq_ids", _I32, n, "dms_seq_reset")
     _check(lib().dms_seq_reset(ctx, layer, n, _ptr(seq_ids), _stream(stream)), "dms_seq_reset")
 
 
 def dms_append(ctx, layer, n, seq_ids, k, v, flags, stream=None):
+    _check_kv_args(ctx, "dms_append", n, n, seq_ids=seq_ids, k=k, v=v, flags=flags)
     _check(lib().dms_append(ctx, layer, n, _ptr(seq_ids), _ptr(k), _ptr(v), _ptr(flags),
                             _stream(stream)), "dms_append")
 
 
 def dms_decode(ctx, layer, n, seq_ids, q, out, stream=None):
+    _check_kv_args(ctx, "dms_decode", n, n, seq_ids=seq_ids, q=q, out=out)
     _check(lib().dms_decode(ctx, layer, n, _ptr(seq_ids), _ptr(q), _ptr(out), _stream(stream)),
            "dms_decode")
 
 
 def dms_decode_step(ctx, layer, n, seq_ids, q, k, v, flags, out, stream=None):
+    _check_kv_args(ctx, "dms_decode_step", n, n, seq_ids=seq_ids, k=k, v=v, flags=flags, q=q,
+                   out=out)
     _check(lib().dms_decode_step(ctx, layer, n, _ptr(seq_ids), _ptr(q), _ptr(k), _ptr(v),
                                  _ptr(flags), _ptr(out), _stream(stream)), "dms_decode_step")
 
 
 def dms_decode_step_q(ctx, layer, n, seq_ids, q, k, v, decisions_out, out, stream=None):
+    _check_kv_args(ctx, "dms_decode_step_q", n, n, seq_ids=seq_ids, k=k, v=v, q=q, out=out,
+                   decisions=decisions_out)
     _check(lib().dms_decode_step_q(ctx, layer, n, _ptr(seq_ids), _ptr(q), _ptr(k), _ptr(v),
                                    _ptr(decisions_out), _ptr(out), _stream(stream)),
            "dms_decode_step_q")
@@ -233,6 +306,8 @@ def dms_decode_step_q(ctx, layer, n, seq_ids, q, k, v, decisions_out, out, strea
 
 def dms_append_chunk(ctx, layer, n, seq_ids, cu_seqlens, total_tokens, max_seqlen, k, v, flags,
                      stream=None):
+    _check_kv_args(ctx, "dms_append_chunk", n, total_tokens, seq_ids=seq_ids, cu=cu_seqlens, k=k,
+                   v=v, flags=flags)
     _check(lib().dms_append_chunk(ctx, layer, n, _ptr(seq_ids), _ptr(cu_seqlens), total_tokens,
                                   max_seqlen, _ptr(k), _ptr(v), _ptr(flags), _stream(stream)),
            "dms_append_chunk")
@@ -240,6 +315,8 @@ def dms_append_chunk(ctx, layer, n, seq_ids, cu_seqlens, total_tokens, max_seqle
 
 def dms_prefill_chunk(ctx, layer, n, seq_ids, cu_seqlens, total_tokens, max_seqlen, q, k, v,
                       flags, out, stream=None):
+    _check_kv_args(ctx, "dms_prefill_chunk", n, total_tokens, seq_ids=seq_ids, cu=cu_seqlens, k=k,
+                   v=v, flags=flags, q=q, out=out)
     _check(lib().dms_prefill_chunk(ctx, layer, n, _ptr(seq_ids), _ptr(cu_seqlens), total_tokens,
                                    max_seqlen, _ptr(q), _ptr(k), _ptr(v), _ptr(flags), _ptr(out),
                                    _stream(stream)), "dms_prefill_chunk")
@@ -247,17 +324,27 @@ def dms_prefill_chunk(ctx, layer, n, seq_ids, cu_seqlens, total_tokens, max_seql
 
 def dms_prefill_chunk_q(ctx, layer, n, seq_ids, cu_seqlens, total_tokens, max_seqlen, q, k, v,
                         decisions_out, out, stream=None):
+    _check_kv_args(ctx, "dms_prefill_chunk_q", n, total_tokens, seq_ids=seq_ids, cu=cu_seqlens,
+                   k=k, v=v, q=q, out=out, decisions=decisions_out)
     _check(lib().dms_prefill_chunk_q(ctx, layer, n, _ptr(seq_ids), _ptr(cu_seqlens), total_tokens,
                                      max_seqlen, _ptr(q), _ptr(k), _ptr(v), _ptr(decisions_out),
                                      _ptr(out), _stream(stream)), "dms_prefill_chunk_q")
 
 
 def dms_retained_lengths(ctx, layer, n, seq_ids, out, stream=None):
+    dims = _dims(ctx)
+    _args("dms_retained_lengths", (seq_ids, "seq_ids", _I32, n),
+          (out, "out", _I32, n * dims[0] if dims else 0))
     _check(lib().dms_retained_lengths(ctx, layer, n, _ptr(seq_ids), _ptr(out), _stream(stream)),
            "dms_retained_lengths")
 
 
 def dms_quest_selection(ctx, n, pages_out, count_out, stream=None):
+    c = _CTX_CFG.get(ctx)
+    if c is not None:
+        _args("dms_quest_selection",
+              (pages_out, "pages_out", _I32, n * c.num_kv_heads * max(c.quest_page_budget, 1)),
+              (count_out, "count_out", _I32, n * c.num_kv_heads))
     _check(lib().dms_quest_selection(ctx, n, _ptr(pages_out), _ptr(count_out), _stream(stream)),
            "dms_quest_selection")
 
@@ -438,7 +525,25 @@ def dms_train_workspace(cfg: DmsTrainConfig) -> int:
     return n.value
 
 
+def _check_train_args(cfg, where, **t):
+    B, T, H, g, D = cfg.batch, cfg.seq_len, cfg.num_kv_heads, cfg.group_size, cfg.head_dim
+    rows_q, rows_k = B * T * H * g, B * T * H
+    spec = {"q": (_BF16, rows_q * D), "dout": (_BF16, rows_q * D), "k": (_BF16, rows_k * D),
+            "v": (_BF16, rows_k * D), "alpha": (_F32, rows_k), "out": (_F32, rows_q * D),
+            "lse": (_F32, rows_q), "dq": (_F32, rows_q * D), "dk": (_F32, rows_k * D),
+            "dv": (_F32, rows_k * D), "dalpha": (_F32, rows_k)}
+    specs = [(x, name, *spec[name]) for name, x in t.items() if name != "workspace"]
+    ws = t.get("workspace")
+    if ws is not None and not isinstance(ws, int):
+        # the size is only known for a valid configuration (else the library refuses it)
+        need = dms_train_workspace(cfg) if cfg.batch >= 1 and cfg.seq_len >= 1 else 0
+        specs.append((ws, "workspace", _U8, need))
+    _args(where, *specs)
+
+
 def dms_train_attention_fwd(cfg, q, k, v, alpha, out, lse, workspace, stream=None):
+    _check_train_args(cfg, "dms_train_attention_fwd", q=q, k=k, v=v, alpha=alpha, out=out,
+                      lse=lse, workspace=workspace)
     _check(lib().dms_train_attention_fwd(ctypes.byref(cfg), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha),
                                          _ptr(out), _ptr(lse), _ptr(workspace), _stream(stream)),
            "dms_train_attention_fwd")
@@ -446,6 +551,8 @@ def dms_train_attention_fwd(cfg, q, k, v, alpha, out, lse, workspace, stream=Non
 
 def dms_train_attention_bwd(cfg, q, k, v, alpha, out, lse, dout, dq, dk, dv, dalpha, workspace,
                             stream=None):
+    _check_train_args(cfg, "dms_train_attention_bwd", q=q, k=k, v=v, alpha=alpha, out=out,
+                      lse=lse, dout=dout, dq=dq, dk=dk, dv=dv, dalpha=dalpha, workspace=workspace)
     _check(lib().dms_train_attention_bwd(ctypes.byref(cfg), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha),
                                          _ptr(out), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk),
                                          _ptr(dv), _ptr(dalpha), _ptr(workspace), _stream(stream)),
@@ -453,10 +560,14 @@ def dms_train_attention_bwd(cfg, q, k, v, alpha, out, lse, dout, dq, dk, dv, dal
 
 
 def dms_gumbel_sigmoid_fwd(n, logits, u, tau, alpha, stream=None):
+    _args("dms_gumbel_sigmoid_fwd", (logits, "logits", _F32, n), (u, "u", _F32, n),
+          (alpha, "alpha", _F32, n))
     _check(lib().dms_gumbel_sigmoid_fwd(n, _ptr(logits), _ptr(u), tau, _ptr(alpha), _stream(stream)),
            "dms_gumbel_sigmoid_fwd")
 
 
 def dms_gumbel_sigmoid_bwd(n, alpha, dalpha, tau, dlogits, stream=None):
+    _args("dms_gumbel_sigmoid_bwd", (alpha, "alpha", _F32, n), (dalpha, "dalpha", _F32, n),
+          (dlogits, "dlogits", _F32, n))
     _check(lib().dms_gumbel_sigmoid_bwd(n, _ptr(alpha), _ptr(dalpha), tau, _ptr(dlogits),
                                         _stream(stream)), "dms_gumbel_sigmoid_bwd")

@@ -350,3 +350,71 @@ def test_latent_pages_layout_and_host_checks():
         assert L.dms_prefill_chunk_q(ctx, 0, 1, X, X, 4, 4, X, X, None, X, X, None) == dms.DMS_ERR_UNSUPPORTED
     finally:
         dms.dms_destroy(ctx)
+
+
+def test_binding_checks_tensor_arguments_before_the_call():
+    """The Python binding refuses tensors of the wrong element type, on the
+    host, non-contiguous or too small before handing their addresses to the
+    library (which cannot see them); raw integer addresses pass through."""
+    import torch
+    cfg = _cfg()    # Hkv = 2, g = 2, d = 64
+    ctx = dms.dms_create(cfg, 0x1000, [0x2000, 0x3000], 0x4000)
+    try:
+        n = 2
+        sid = torch.zeros(n, dtype=torch.int32)
+        q = torch.zeros((n, 4, 64), dtype=torch.bfloat16)
+        k = torch.zeros((n, 2, 64), dtype=torch.bfloat16)
+        fl = torch.zeros((n, 2), dtype=torch.uint8)
+        out = torch.zeros((n, 4, 64), dtype=torch.float32)
+
+        def code(fn, *a):
+            with pytest.raises(dms.DmsError) as e:
+                fn(*a)
+            return e.value.code, str(e.value)
+
+        # element types
+        c, msg = code(dms.dms_decode_step, ctx, 0, n, sid.to(torch.int64), q, k, k, fl, out, 0)
+        assert c == dms.DMS_ERR_INVALID and "seq_ids must be int32" in msg
+        c, msg = code(dms.dms_decode_step, ctx, 0, n, sid, q.float(), k, k, fl, out, 0)
+        assert c == dms.DMS_ERR_INVALID and ": q must be bf16" in msg
+        c, msg = code(dms.dms_decode_step, ctx, 0, n, sid, q, k, k, fl.to(torch.int32), out, 0)
+        assert "flags must be uint8" in msg
+        c, msg = code(dms.dms_decode_step, ctx, 0, n, sid, q, k, k, fl, out.to(torch.bfloat16), 0)
+        assert "out must be float32" in msg
+        c, msg = code(dms.dms_train_attention_fwd, dms.make_train_config(1, 4, 2, 2, 128, 2),
+                      q, k, k, out, out, out.to(torch.bfloat16), 0x100)
+        assert "lse must be float32" in msg
+        # right types, but host memory
+        c, msg = code(dms.dms_decode_step, ctx, 0, n, sid, q, k, k, fl, out, 0)
+        assert c == dms.DMS_ERR_INVALID and "GPU" in msg
+        # raw addresses are not inspected (the library validates nulls and sizes it can see)
+        assert dms.lib().dms_decode_step(ctx, 0, n, 0x100, 0x100, 0x100, 0x100, 0x100, None,
+                                         None) == dms.DMS_ERR_INVALID
+    finally:
+        dms.dms_destroy(ctx)
+    assert ctx not in dms._CTX_CFG
+
+
+@pytest.mark.gpu
+def test_binding_refuses_small_or_strided_gpu_tensors():
+    import torch
+    cfg = _cfg()
+    cache = dms.DmsCache(cfg, device="cuda")
+    try:
+        n = 2
+        sid = torch.arange(n, dtype=torch.int32, device="cuda")
+        q = torch.zeros((n, 4, 64), dtype=torch.bfloat16, device="cuda")
+        k = torch.zeros((n, 2, 64), dtype=torch.bfloat16, device="cuda")
+        fl = torch.zeros((n, 2), dtype=torch.uint8, device="cuda")
+        out = torch.zeros((n, 4, 64), dtype=torch.float32, device="cuda")
+        with pytest.raises(dms.DmsError, match="needs"):
+            dms.dms_decode_step(cache.ctx, 0, n, sid, q[:1], k, k, fl, out)
+        with pytest.raises(dms.DmsError, match="contiguous"):
+            dms.dms_decode_step(cache.ctx, 0, n, sid, q, k, k, fl,
+                                torch.zeros((n, 64, 4), device="cuda").transpose(1, 2))
+        with pytest.raises(dms.DmsError, match="needs"):
+            dms.dms_append_chunk(cache.ctx, 0, 1, sid[:1], sid[:1], 2, 2, k, k, fl)  # cu too short
+        torch.cuda.synchronize()
+        assert dms.dms_status(cache.ctx) == 0
+    finally:
+        cache.close()

@@ -128,6 +128,29 @@ def test_ragged_multi_sequence(d, g, w, P, p):
     compare_pool(cache, 0, cache.export(0), seqs, inp)
 
 
+def test_qwen3_8b_shape_window_512():
+    """The Qwen3-8B attention shape of the sweeps (8 KV heads x group 4,
+    head_dim 128) with its window w = 512 (Sec. 5.2): contexts below, at and
+    well past the window, chunks that are not multiples of the page, then
+    decode steps across the window boundary of the shortest sequence."""
+    H, g, d, w, P = 8, 4, 128, 512, 64
+    seqs = [4, 1, 0, 3, 2]
+    lens = {4: 300, 1: 511, 0: 512, 3: 1900, 2: 3700}
+    dms, cfg, cache = _mk(dict(num_layers=1, max_seqs=5, num_kv_heads=H, group_size=g,
+                               head_dim=d, window=w, page_size=P, num_pages=5 * H * 70,
+                               max_pages_per_head=70, max_chunk_tokens=5 * 700))
+    inp = {s: SeqInputs(29, 0, s, lens[s] + 240, H, g, d, 0.875) for s in seqs}
+    orc = _oracle_for(cfg)
+    _append_chunks(dms, cache, orc, seqs, inp, {s: 0 for s in seqs}, lens, 700)
+    view = cache.export(0)
+    compare_state(view, orc, seqs)
+    compare_pool(cache, 0, view, seqs, inp)
+    # 230 steps take sequence 4 from 300 past the window (512) and the others further
+    _decode_steps(dms, cache, orc, seqs, inp, lens, 230, g, check_every=23)
+    compare_pool(cache, 0, cache.export(0), seqs, inp)
+    cache.close()
+
+
 def test_many_heads_multi_pass_planner():
     """320 sequences x 4 KV heads = 1280 heads per call: more heads than one
     planning block has threads, so the multi-pass planner runs; ragged short

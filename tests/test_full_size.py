@@ -4,10 +4,12 @@ head_dim 128), 32768 context tokens appended in 4096-token chunks, w=256,
 flags Bernoulli(7/8), then decode steps.
 
 Checked: every head's bookkeeping bit-exactly against the oracle's replay
-(retained lengths, positions, rings, page tables, slot owners, free stack),
+(retained lengths, positions, rings, page tables, slot owners, free stack);
+the decode outputs of every query head of 16 sequences spread over the batch
+and of every head whose tiles the planner spreads over three or more decode
+waves, against dense masked attention over the full history (max-abs 1e-2);
 and, on sampled (sequence, KV head) pairs, the pool contents at every live
-slot and the decode outputs against dense masked attention over the full
-history (max-abs 1e-2)."""
+slot."""
 import numpy as np
 import pytest
 
@@ -21,6 +23,20 @@ SEED, LAYER = 3, 5
 B, H, G, D, W, P, CTX, CHUNK, P_EVICT = 128, 8, 5, 128, 256, 64, 32768, 4096, 7 / 8
 STEPS = 3
 SAMPLES = [(0, 0), (17, 3), (64, 7), (127, 5), (90, 1), (33, 6)]
+FULL_SEQS = list(range(0, B, 8))   # every query head of these sequences
+
+
+def wave_spans(L, waves):
+    """Decode waves holding each head's tiles, as the planner splits the call:
+    the heads' 32-slot tiles laid end to end in call order, wave w taking
+    tiles [w * total / W, (w + 1) * total / W).  L [n, H] retained lengths."""
+    tiles = (L.reshape(-1).astype(np.int64) + 31) // 32
+    cum = np.concatenate([[0], np.cumsum(tiles)])
+    total = int(cum[-1])
+    bounds = np.arange(waves + 1, dtype=np.int64) * total // waves
+    first = np.searchsorted(bounds, cum[:-1], side="right") - 1          # bounds[w] <= c0
+    last = np.searchsorted(bounds[1:], cum[1:], side="left")             # bounds[w + 1] >= c1
+    return (last - first + 1).reshape(L.shape)
 
 
 def test_full_size_layer():
@@ -83,6 +99,32 @@ def test_full_size_layer():
         view = cache.export(0)
         compare_state(view, orc, range(B))
         if step == STEPS - 1:
+            # every query head of FULL_SEQS, every head spread over >= 3 waves
+            props = torch.cuda.get_device_properties(0)
+            n_waves = min(props.multi_processor_count * 4, 8192)
+            span = wave_spans(view.L, n_waves)
+            check = sorted({(s, h) for s in FULL_SEQS for h in range(H)} |
+                           {(int(s), int(h)) for s, h in zip(*np.nonzero(span >= 3))} |
+                           set(SAMPLES))
+            print(f"[full-size] comparing {len(check)} KV heads ({int((span >= 3).sum())} over "
+                  f">= 3 waves, widest {int(span.max())}) at t={t}", flush=True)
+            worst = 0.0
+            by_seq = {}
+            for (s, h) in check:
+                by_seq.setdefault(s, []).append(h)
+            for s, hs in by_seq.items():
+                kd = sy.seq_chunk_vectors_torch(SEED, sy.STREAM_K, LAYER, [s], H, 0, t + 1, D, dev)
+                vd = sy.seq_chunk_vectors_torch(SEED, sy.STREAM_V, LAYER, [s], H, 0, t + 1, D, dev)
+                ks, vs = kd[0].float().cpu().numpy(), vd[0].float().cpu().numpy()
+                del kd, vd
+                for h in hs:
+                    ref = dense_dms_attention_head(bf16_to_f32(q[s, h * G:(h + 1) * G])[None],
+                                                   ks[:, h], vs[:, h], flags_host[s, : t + 1, h],
+                                                   W, [t])[0]
+                    err = float(np.abs(got[s, h * G:(h + 1) * G] - ref).max())
+                    assert err <= ATOL, (s, h, int(span[s, h]), err)
+                    worst = max(worst, err)
+            print(f"[full-size] worst max-abs error {worst:.2e}", flush=True)
             for (s, h) in SAMPLES:
                 hist = np.arange(t + 1)
                 kh = sy.head_sequence_np(SEED, sy.STREAM_K, LAYER, s, h, hist, D)
