@@ -74,7 +74,9 @@ enum {
   DMS_ERR_HIP = -3,           /* a HIP runtime call or launch failed */
   DMS_ERR_OUT_OF_PAGES = -4,  /* device: free-page stack exhausted */
   DMS_ERR_CAPACITY = -5,      /* device: a head needs more than max_pages_per_head */
-  DMS_ERR_BAD_SEQ = -6        /* device: sequence id out of range or repeated */
+  DMS_ERR_BAD_SEQ = -6,       /* device: sequence id out of range or repeated */
+  DMS_ERR_SCRATCH = -7        /* host: call too large for the static scratch of
+                                 dms_decode_step_static */
 };
 
 typedef struct dms_config {
@@ -283,6 +285,32 @@ int dms_decode(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
 int dms_decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
                     const void* q_dev, const void* k_dev, const void* v_dev,
                     const uint8_t* flags_dev, float* out_dev, void* stream);
+
+/* dms_decode_step for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same append, split-K decode and merge, with everything the call needs
+ * beyond its inputs, outputs and the context's state and pools (planner
+ * output, split-K partials, arrival counters) kept in a static 32 MiB device
+ * array inside libdms instead of the context's workspace.  The array exists
+ * once per GPU (its address is resolved by dms_init_state, or by this call
+ * on a device where that has not happened) and is held until the process
+ * ends; the call allocates and frees nothing.
+ *   Limit: with W decode waves (4 per compute unit: 1024 on MI355X) and
+ *   NH = n * num_kv_heads, the call needs about
+ *   (W + NH) * (128 + 4 * group_size * head_dim) + 40 * W + 40 * NH bytes;
+ *   a call above 32 MiB returns DMS_ERR_SCRATCH and changes nothing (e.g.
+ *   group 16, head_dim 128: up to ~3000 KV heads per call).
+ *   Supported: DMS_DECIDE_CALLER, DMS_KV_BF16 or DMS_KV_FP8 pages,
+ *   quest_page_budget = 0 (DMS_ERR_UNSUPPORTED otherwise).
+ *   Every call on one GPU shares that GPU's array: calls that may overlap in
+ *   time on one GPU (different streams, or different contexts on streams not
+ *   ordered with each other) race and must not be issued; calls ordered on
+ *   one stream are safe.  The array keeps the last call's contents; what must
+ *   start at zero is cleared by each call.
+ * Arguments, outputs and errors as for dms_decode_step. */
+int dms_decode_step_static(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+                           const void* q_dev, const void* k_dev, const void* v_dev,
+                           const uint8_t* flags_dev, float* out_dev, void* stream);
 
 /* dms_decode_step with decisions read from the queries (DMS_DECIDE_QUERY
  * only): the decision of each (sequence, KV head) comes from q_dev as

@@ -4,6 +4,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <vector>
 
 #include "dms_common.h"
@@ -138,6 +139,11 @@ struct dms_ctx {
   Ctx c;
 };
 
+// Scratch of dms_decode_step_static (see static_scratch below): one copy per
+// GPU, held until the process ends.
+constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+
 namespace {
 
 inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
@@ -183,6 +189,53 @@ const int32_t* quest_pages(const Ctx& c) {
 }
 const int32_t* quest_phys_pages(const Ctx& c) {
   return reinterpret_cast<const int32_t*>(static_cast<char*>(c.ws) + c.lo.ws_q_page);
+}
+
+// ---------------------------------------------------------------------------
+// Static scratch of dms_decode_step_static
+// ---------------------------------------------------------------------------
+
+// Device memory that dms_decode_step_static works in instead of the caller's
+// workspace: planner output (head descriptors, tile prefix sums, per-wave
+// ranges, per-head wave spans), split-K partials and arrival counters.  Every
+// GPU the library runs on holds its own copy until the process ends.  In host
+// code the name is only a stand-in for the symbol; kernels get the device
+// address that hipGetSymbolAddress returns for the current device.
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxScratchDevices] = {};
+
+// Device address of the current device's scratch, resolved once per device.
+int static_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxScratchDevices) return DMS_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_dev[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return DMS_ERR_HIP;
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return DMS_OK;
+}
+
+// Offsets of the decode buffers for a call of `n` sequences over `waves`
+// decode waves, packed from offset 0 of the scratch (the meta and pool
+// offsets of `lo` are kept).  Returns the bytes used.
+size_t static_layout(const dms_config& c, int n, int waves, dms::Layout* lo) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = dms::align_up(off + bytes, dms::kAlign); return o; };
+  const size_t NH = static_cast<size_t>(n) * c.num_kv_heads, W = static_cast<size_t>(waves);
+  lo->ws_head_desc = take(NH * sizeof(dms::HeadDesc));
+  lo->ws_cum_tiles = take((NH + 1) * 4);
+  lo->ws_part_ml = take((W + NH) * dms::kMaxGroup * 8);
+  lo->ws_part_acc = take((W + NH) * c.group_size * c.head_dim * 4);
+  lo->ws_wave_bounds = take((W + 1) * 4);
+  lo->ws_wave_desc = take(W * 2 * sizeof(int4));
+  lo->ws_head_waves = take(NH * sizeof(int4));
+  lo->ws_head_cnt = take(NH * 4);
+  lo->max_partials = static_cast<int>(W + NH);   // partial index = wave + call head
+  return off;
 }
 
 int ensure_waves(dms_ctx* ctx) {
@@ -259,6 +312,9 @@ int dms_destroy(dms_ctx* ctx) {
 
 int dms_init_state(dms_ctx* ctx, void* stream) {
   if (!ctx) return DMS_ERR_INVALID;
+  // set-up of the current device's static scratch (dms_decode_step_static)
+  void* sp = nullptr;
+  if (int rc = static_scratch(&sp)) return rc;
   return hip_rc(dms::launch_init_state(ctx->c.cfg, ctx->c.lo, ctx->c.meta, ctx->c.ws,
                                        as_stream(stream)));
 }
@@ -401,6 +457,35 @@ int dms_decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, 
   if ((rc = ensure_waves(ctx))) return rc;
   return decode_step(ctx, layer, n, seq_ids_dev, q_dev, k_dev, v_dev, flags_dev, nullptr, out_dev,
                      stream);
+}
+
+int dms_decode_step_static(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
+                           const void* q_dev, const void* k_dev, const void* v_dev,
+                           const uint8_t* flags_dev, float* out_dev, void* stream) {
+  int rc = check_call(ctx, layer, n, seq_ids_dev);
+  if (rc) return rc;
+  const dms_config& cfg = ctx->c.cfg;
+  if (cfg.decision_source != DMS_DECIDE_CALLER) return DMS_ERR_INVALID;
+  if (cfg.kv_format == DMS_KV_MLA || cfg.quest_page_budget > 0) return DMS_ERR_UNSUPPORTED;
+  if (!q_dev || !k_dev || !v_dev || !flags_dev || !out_dev) return DMS_ERR_INVALID;
+  if ((rc = ensure_waves(ctx))) return rc;
+  const Ctx& c = ctx->c;
+  dms::Layout slo = c.lo;
+  if (static_layout(cfg, n, c.decode_waves, &slo) > kStaticScratchBytes) return DMS_ERR_SCRATCH;
+  void* sp = nullptr;
+  if ((rc = static_scratch(&sp))) return rc;
+  hipStream_t st = as_stream(stream);
+  // the same planner and decode kernels as dms_decode_step; the planner also
+  // clears the arrival counters of the call's heads, which an earlier call
+  // (of any context) may have left in the scratch
+  hipError_t e = dms::launch_plan(cfg, slo, c.meta, sp, layer, n, seq_ids_dev, flags_dev, nullptr,
+                                  nullptr, true, c.decode_waves, out_dev, st, nullptr, true);
+  hipEvent_t e0, e1;
+  next_events(ctx->c, DMS_PROFILE_DECODE, &e0, &e1);
+  if (e == hipSuccess)
+    e = dms::launch_decode(cfg, slo, c.meta, sp, c.pools[layer], layer, n, q_dev, k_dev, v_dev,
+                           out_dev, c.decode_waves, st, e0, e1);
+  return hip_rc(e);
 }
 
 int dms_decode_step_q(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
@@ -569,6 +654,7 @@ const char* dms_strerror(int code) {
     case DMS_ERR_OUT_OF_PAGES: return "KV page pool exhausted";
     case DMS_ERR_CAPACITY: return "a head exceeds max_pages_per_head";
     case DMS_ERR_BAD_SEQ: return "sequence id out of range or repeated in one call";
+    case DMS_ERR_SCRATCH: return "call too large for the library's static scratch";
     default: return "unknown error code";
   }
 }

@@ -163,6 +163,7 @@ struct PlanArgs {
   int4* head_waves;      // [n*H] first / last wave holding a tile of the head, live mask
   float* out;            // nullable: zeroed for heads with no retained token
   const int32_t* len_override;   // nullable (no append): lengths to plan, per head of the call
+  int32_t* zero_cnt;     // nullable: split-head arrival counters of the call's heads, cleared
   int n, H, w, P, maxp, max_slots, max_seqs, append, W, gD;
 };
 
@@ -338,6 +339,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(PlanArgs a) {
     }
     a.desc[tid] = make_int4(Lnew, sh, slot, 0);
     a.cum_tiles[tid + 1] = c1;
+    if (a.zero_cnt != nullptr) a.zero_cnt[tid] = 0;
     if (a.out != nullptr && Lnew == 0)
       for (int e = 0; e < a.gD; ++e) a.out[static_cast<size_t>(tid) * a.gD + e] = 0.f;
   }
@@ -438,6 +440,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
       }
       a.desc[hh] = make_int4(Lnew, sh, slot, 0);
       a.cum_tiles[hh + 1] = ct + tiles;
+      if (a.zero_cnt != nullptr) a.zero_cnt[hh] = 0;
       if (a.out != nullptr && Lnew == 0)
         for (int e = 0; e < a.gD; ++e) a.out[static_cast<size_t>(hh) * a.gD + e] = 0.f;
     }
@@ -823,9 +826,12 @@ hipError_t launch_seq_reset(const dms_config& c, const Layout& lo, void* meta, i
 hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* ws, int layer,
                        int n, const int32_t* seq_ids, const uint8_t* flags, const void* q,
                        uint8_t* flags_out, bool append, int waves, float* out, hipStream_t st,
-                       const int32_t* len_override) {
+                       const int32_t* len_override, bool clear_head_counts) {
   PlanArgs a;
   a.len_override = len_override;
+  a.zero_cnt = clear_head_counts
+                   ? reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_head_cnt)
+                   : nullptr;
   a.q = static_cast<const uint16_t*>(q);
   a.flags_out = flags_out;
   a.bias = c.decision_bias;

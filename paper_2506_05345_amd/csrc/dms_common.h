@@ -194,10 +194,12 @@ hipError_t launch_seq_reset(const dms_config& c, const Layout& lo, void* meta, i
 // for heads with no retained token.
 // `len_override` (nullable, planning without append only): per-head lengths
 // to plan instead of the retained lengths (page retrieval).
+// `clear_head_counts`: also zero the split-head arrival counters of the
+// call's heads (scratch whose earlier contents are unknown).
 hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* ws, int layer,
                        int n, const int32_t* seq_ids, const uint8_t* flags, const void* q,
                        uint8_t* flags_out, bool append, int waves, float* out, hipStream_t st,
-                       const int32_t* len_override = nullptr);
+                       const int32_t* len_override = nullptr, bool clear_head_counts = false);
 // Page retrieval: recompute the bounds of the pages the last planned append
 // wrote (all_pages: every page of every head of the call), then select the
 // pages of each head for query q.

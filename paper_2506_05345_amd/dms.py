@@ -26,6 +26,7 @@ DMS_ERR_HIP = -3
 DMS_ERR_OUT_OF_PAGES = -4
 DMS_ERR_CAPACITY = -5
 DMS_ERR_BAD_SEQ = -6
+DMS_ERR_SCRATCH = -7
 
 
 class DmsConfig(ctypes.Structure):
@@ -104,6 +105,7 @@ _SIGS = {
     "dms_append_chunk": (_I, [_VP, _I, _I, _VP, _VP, _I, _I, _VP, _VP, _VP, _VP]),
     "dms_prefill_chunk": (_I, [_VP, _I, _I, _VP, _VP, _I, _I, _VP, _VP, _VP, _VP, _VP, _VP]),
     "dms_decode_step_q": (_I, [_VP, _I, _I, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
+    "dms_decode_step_static": (_I, [_VP, _I, _I, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     "dms_prefill_chunk_q": (_I, [_VP, _I, _I, _VP, _VP, _I, _I, _VP, _VP, _VP, _VP, _VP, _VP]),
     "dms_retained_lengths": (_I, [_VP, _I, _I, _VP, _VP, _VP]),
     "dms_quest_selection": (_I, [_VP, _I, _VP, _VP, _VP]),
@@ -294,6 +296,14 @@ def dms_decode_step(ctx, layer, n, seq_ids, q, k, v, flags, out, stream=None):
                    out=out)
     _check(lib().dms_decode_step(ctx, layer, n, _ptr(seq_ids), _ptr(q), _ptr(k), _ptr(v),
                                  _ptr(flags), _ptr(out), _stream(stream)), "dms_decode_step")
+
+
+def dms_decode_step_static(ctx, layer, n, seq_ids, q, k, v, flags, out, stream=None):
+    _check_kv_args(ctx, "dms_decode_step_static", n, n, seq_ids=seq_ids, k=k, v=v, flags=flags,
+                   q=q, out=out)
+    _check(lib().dms_decode_step_static(ctx, layer, n, _ptr(seq_ids), _ptr(q), _ptr(k), _ptr(v),
+                                        _ptr(flags), _ptr(out), _stream(stream)),
+           "dms_decode_step_static")
 
 
 def dms_decode_step_q(ctx, layer, n, seq_ids, q, k, v, decisions_out, out, stream=None):
