@@ -348,83 +348,109 @@ __device__ inline float wave_sum(float v) {
   return v;
 }
 
-constexpr int kMergeBatch = 64;   // partials handled per merge round (one per lane)
+constexpr int kMergeBatch = 64;   // partials whose (max, sum) one round of loads fetches (one per lane)
+constexpr int kMergeLoads = 32;   // 16-byte accumulator loads in flight per lane in the merge
 
 // Log-sum-exp merge of the partials a head got from waves wf .. wl (index
-// w + hh; waves with an empty range wrote none).  All reads are
-// agent-coherent and issued in parallel: each lane fetches one partial's
-// (max, sum) for every row, row maxima and sums are wave reductions, the
-// weights go through LDS, and the head's g x D outputs are spread over the
-// 64 lanes as 16-byte pieces whose loads for a batch of partials are in
-// flight together.
-template <int D>
-__device__ void merge_head(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsrc,
+// w + hh; waves with an empty range wrote none).  Every access is
+// agent-coherent, and the merge is bound by the round trips of one wave, so
+// as many loads as possible are in flight together: lane i fetches partial
+// b0 + i's (max, sum) for every row, the head's g x D outputs are spread
+// over the lanes as PPL 16-byte pieces each, and the pieces of U partials
+// (U * PPL <= kMergeLoads) are all requested before any is used -- the first
+// U together with the (max, sum) loads.  Loads of partials that turn out
+// dead (no tiles) or that lie past the span read in-range stale bytes and
+// are discarded by a select, never multiplied.
+template <int D, int PPL>
+__device__ __forceinline__ void merge_head(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsrc,
                            const int32_t* wave_bounds, float* out, int wf, int wl, int hh, int g,
                            int lane, float (*wts)[kMaxGroup]) {
-  constexpr int kMaxPieces = kMaxGroup * D / 4 / 64;   // 16-byte pieces per lane
+  constexpr int U = kMergeLoads / PPL > 0 ? kMergeLoads / PPL : 1;
   const int pieces = g * D / 4;
-  // pass 1: row maxima
-  float M[kMaxGroup];
+  const int nparts = wl - wf + 1;
+  int row[PPL];
+#pragma unroll
+  for (int j = 0; j < PPL; ++j) row[j] = min(4 * (lane + 64 * j) / D, kMaxGroup - 1);
+  auto acc_load = [&](int u, int j) -> u32x4 {
+    // partial wf + min(u, nparts - 1): always inside the written span's slots
+    const size_t p2 = static_cast<size_t>(wf + min(u, nparts - 1)) + hh;
+    const int f = min(lane + 64 * j, pieces - 1);
+    return __builtin_amdgcn_raw_buffer_load_b128(
+        acc_rsrc, static_cast<uint32_t>((p2 * g * D + 4 * f) * 4), 0, kCachePolicySc1);
+  };
+  f32x4 num[PPL];
+#pragma unroll
+  for (int j = 0; j < PPL; ++j) num[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float den[kMaxGroup];
+#pragma unroll
+  for (int r = 0; r < kMaxGroup; ++r) den[r] = 0.f;
+  // pass 1: row maxima; the lane's (max, sum) of the last batch stay in registers
+  float M[kMaxGroup], ml_m[kMaxGroup], ml_l[kMaxGroup];
 #pragma unroll
   for (int r = 0; r < kMaxGroup; ++r) M[r] = -INFINITY;
-  for (int b0 = wf; b0 <= wl; b0 += kMergeBatch) {
-    const int w2 = b0 + lane;
-    if (w2 <= wl && wave_bounds[w2] < wave_bounds[w2 + 1]) {
-      const float* ml = reinterpret_cast<const float*>(part_ml + (static_cast<size_t>(w2) + hh) * kMaxGroup);
+  u32x4 x[U][PPL];    // accumulator pieces in flight; the first batch goes out with the (max, sum) loads
+  bool live = false;
+  for (int b0 = 0; b0 < nparts; b0 += kMergeBatch) {
+    const int w2 = wf + b0 + lane;
+    live = b0 + lane < nparts && wave_bounds[w2] < wave_bounds[w2 + 1];
+    const float* ml = reinterpret_cast<const float*>(part_ml + (static_cast<size_t>(live ? w2 : wf) + hh) * kMaxGroup);
 #pragma unroll
-      for (int r = 0; r < kMaxGroup; ++r)
-        if (r < g) M[r] = fmaxf(M[r], load_coherent(ml + 2 * r));
+    for (int r = 0; r < kMaxGroup; ++r) {
+      ml_m[r] = (live && r < g) ? load_coherent(ml + 2 * r) : -INFINITY;
+      ml_l[r] = (live && r < g) ? load_coherent(ml + 2 * r + 1) : 0.f;
     }
+    if (b0 == 0) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < PPL; ++j) x[u][j] = acc_load(u, j);
+    }
+#pragma unroll
+    for (int r = 0; r < kMaxGroup; ++r) M[r] = fmaxf(M[r], ml_m[r]);
   }
 #pragma unroll
   for (int r = 0; r < kMaxGroup; ++r)
     if (r < g) M[r] = wave_max(M[r]);
-  // pass 2: weights, sums and weighted accumulators, one batch of partials at a time
-  float den[kMaxGroup];
+  // pass 2: weights through LDS, then the accumulators U partials at a time
+  for (int b0 = 0; b0 < nparts; b0 += kMergeBatch) {
+    if (nparts > kMergeBatch) {   // only the last batch's (max, sum) were kept
+      const int w2 = wf + b0 + lane;
+      live = b0 + lane < nparts && wave_bounds[w2] < wave_bounds[w2 + 1];
+      const float* ml = reinterpret_cast<const float*>(part_ml + (static_cast<size_t>(live ? w2 : wf) + hh) * kMaxGroup);
 #pragma unroll
-  for (int r = 0; r < kMaxGroup; ++r) den[r] = 0.f;
-  f32x4 num[kMaxPieces];
-#pragma unroll
-  for (int j = 0; j < kMaxPieces; ++j) num[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int b0 = wf; b0 <= wl; b0 += kMergeBatch) {
-    const int w2 = b0 + lane;
-    const bool live = w2 <= wl && wave_bounds[w2] < wave_bounds[w2 + 1];
-    const float* ml = reinterpret_cast<const float*>(part_ml + (static_cast<size_t>(w2) + hh) * kMaxGroup);
+      for (int r = 0; r < kMaxGroup; ++r) {
+        ml_m[r] = (live && r < g) ? load_coherent(ml + 2 * r) : -INFINITY;
+        ml_l[r] = (live && r < g) ? load_coherent(ml + 2 * r + 1) : 0.f;
+      }
+    }
 #pragma unroll
     for (int r = 0; r < kMaxGroup; ++r) {
       if (r < g) {
-        const float sc = live ? __builtin_amdgcn_exp2f(load_coherent(ml + 2 * r) - M[r]) : 0.f;
+        const float sc = live ? __builtin_amdgcn_exp2f(ml_m[r] - M[r]) : 0.f;
         wts[lane][r] = sc;
-        if (live) den[r] += sc * load_coherent(ml + 2 * r + 1);
+        den[r] += sc * ml_l[r];
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    const int nb = min(kMergeBatch, wl - b0 + 1);
-    for (int i0 = 0; i0 < nb; i0 += 8) {
+    const int nb = min(kMergeBatch, nparts - b0);
+    for (int i0 = 0; i0 < nb; i0 += U) {
+      if (b0 != 0 || i0 != 0) {
 #pragma unroll
-      for (int j = 0; j < kMaxPieces; ++j) {
-        const int f = lane + 64 * j;
-        if (f < pieces) {
-          const int row = 4 * f / D;
-          u32x4 x[8];
-          // only partials with a nonzero weight are read: a wave of the span
-          // that got no tiles wrote none, and its slot holds stale bytes
-          float wu[8];
+        for (int u = 0; u < U; ++u)
 #pragma unroll
-          for (int u = 0; u < 8; ++u) wu[u] = i0 + u < nb ? wts[i0 + u][row] : 0.f;
+          for (int j = 0; j < PPL; ++j) x[u][j] = acc_load(b0 + i0 + u, j);
+      }
 #pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            const size_t p2 = static_cast<size_t>(b0 + i0 + u) + hh;
-            x[u] = wu[u] != 0.f ? __builtin_amdgcn_raw_buffer_load_b128(
-                                      acc_rsrc, static_cast<uint32_t>((p2 * g * D + 4 * f) * 4), 0,
-                                      kCachePolicySc1)
-                                : u32x4{0u, 0u, 0u, 0u};
-          }
+      for (int u = 0; u < U; ++u) {
 #pragma unroll
-          for (int u = 0; u < 8; ++u)
-            if (wu[u] != 0.f) num[j] += wu[u] * __builtin_bit_cast(f32x4, x[u]);
+        for (int j = 0; j < PPL; ++j) {
+          // a zero weight marks a partial past the span or of a wave without
+          // tiles (stale bytes), or one that underflowed: it adds nothing
+          const float wu = i0 + u < nb ? wts[i0 + u][row[j]] : 0.f;
+          const f32x4 v = __builtin_bit_cast(f32x4, x[u][j]);
+          num[j] += wu != 0.f ? wu * v : f32x4{0.f, 0.f, 0.f, 0.f};
         }
       }
     }
@@ -435,15 +461,36 @@ __device__ void merge_head(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsr
     if (r < g) den[r] = wave_sum(den[r]);
   float* o = out + static_cast<size_t>(hh) * g * D;
 #pragma unroll
-  for (int j = 0; j < kMaxPieces; ++j) {
+  for (int j = 0; j < PPL; ++j) {
     const int f = lane + 64 * j;
     if (f < pieces) {
-      const int row = 4 * f / D;
       float d = den[0];
 #pragma unroll
-      for (int r = 1; r < kMaxGroup; ++r) if (r == row) d = den[r];
+      for (int r = 1; r < kMaxGroup; ++r) if (r == row[j]) d = den[r];
       *reinterpret_cast<f32x4*>(o + 4 * f) = num[j] * (1.0f / d);
     }
+  }
+}
+
+// merge_head with the piece count per lane, PPL = ceil(g * D / 256), fixed at
+// compile time (the in-flight load batch is sized by it).
+template <int D>
+__device__ __forceinline__ void merge_head_any(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsrc,
+                               const int32_t* wave_bounds, float* out, int wf, int wl, int hh,
+                               int g, int lane, float (*wts)[kMaxGroup]) {
+  switch ((g * D / 4 + 63) / 64) {
+    case 1: merge_head<D, 1>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, g, lane, wts); break;
+    case 2: merge_head<D, 2>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, g, lane, wts); break;
+    case 3: merge_head<D, 3>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, g, lane, wts); break;
+    case 4: merge_head<D, 4>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, g, lane, wts); break;
+    default:
+      if constexpr (D > 64) {
+        if ((g * D / 4 + 63) / 64 <= 6)
+          merge_head<D, 6>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, g, lane, wts);
+        else
+          merge_head<D, 8>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, g, lane, wts);
+      }
+      break;
   }
 }
 
@@ -451,7 +498,7 @@ __device__ void merge_head(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsr
 // partial (max, sum) and all 16-byte accumulator pieces of all partials --
 // is issued in one round; weights are passed between lanes by shuffles.
 template <int D>
-__device__ void merge_head_small(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsrc,
+__device__ __forceinline__ void merge_head_small(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsrc,
                                  int live_mask, float* out, int wf, int np, int hh,
                                  int g, int lane) {
   constexpr int kMaxPieces = kMaxGroup * D / 4 / 64;
@@ -732,8 +779,8 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
       if (wl - wf < 4)
         merge_head_small<D>(part_ml, acc_rsrc, hw.z, out, wf, wl - wf + 1, mh, a.g, lane);
       else
-        merge_head<D>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, mh, a.g, lane,
-                      merge_wts[threadIdx.x >> 6]);
+        merge_head_any<D>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, mh, a.g, lane,
+                          merge_wts[threadIdx.x >> 6]);
       if (lane == 0) __hip_atomic_store(&head_cnt[mh], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
