@@ -94,6 +94,7 @@ Layout make_layout(const dms_config& c) {
   lo.ws_wave_desc = take(kMaxWaves * 2 * sizeof(int4));   // per decode wave: first segment
   lo.ws_head_waves = take(NH * sizeof(int4));              // per head: waves holding its tiles
   lo.ws_head_cnt = take(NH * 4);
+  lo.ws_plan_ctr = take(16);
   lo.ws_ck_need = take(NH * 4);
   lo.ws_ck_fresh = take(NH * 4);
   lo.ws_ck_base = take(NH * 4);
@@ -398,6 +399,16 @@ int decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, cons
       e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, nullptr,
                              nullptr, out_dev, c.decode_waves, st, e0, e1, quest_phys_pages(c));
     return hip_rc(e);
+  }
+  if (dms::decode_step_fusable(c.cfg, n)) {
+    // one launch: every workgroup plans the append in LDS, the last one to
+    // read the state writes it, and the waves decode (writing the new K / V
+    // into their slots and merging split heads)
+    hipEvent_t e0, e1;
+    next_events(ctx->c, DMS_PROFILE_DECODE, &e0, &e1);
+    return hip_rc(dms::launch_decode_step(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n,
+                                          seq_ids_dev, flags_dev, q_dev, k_dev, v_dev,
+                                          decisions_out_dev, out_dev, c.decode_waves, st, e0, e1));
   }
   // planner (slot choice, page pops, state, wave ranges) -> decode, which
   // also writes the new K / V into their slots and merges split heads

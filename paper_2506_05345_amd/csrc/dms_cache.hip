@@ -25,6 +25,7 @@ struct InitArgs {
   char* meta;
   int32_t* ck_err;
   int32_t* head_cnt;
+  int32_t* plan_ctr;
   int64_t n_heads;
   size_t layer0, layer_stride, pos, len, ring, page_table, stack, top;
   int64_t n_pos, n_len, n_ring, n_pt;
@@ -53,6 +54,7 @@ __global__ void init_state_kernel(InitArgs a) {
       *reinterpret_cast<int32_t*>(a.meta) = 0;  // status
       a.ck_err[0] = 0;
       a.ck_err[1] = 0;
+      a.plan_ctr[0] = 0;
     }
   }
 }
@@ -233,18 +235,14 @@ __device__ void wave_ranges(const PlanArgs& a, int NH) {
 // round(sigmoid(x)) = (x > 0) with x = bf16 element 0 of the first query
 // head of the group plus the offset, in float32 (Sec. 3.2, App. C).
 __device__ inline int decision(const PlanArgs& a, int hh) {
-  if (a.q == nullptr) return a.flags[hh] != 0;
-  const int i = hh / a.H, h = hh % a.H;
-  const uint32_t bits = a.q[(static_cast<size_t>(i) * a.H + h) * a.g * a.D];
-  return (__uint_as_float(bits << 16) + a.bias) > 0.f;
+  return token_decision(a.flags, a.q, hh, a.H, a.g, a.D, a.bias);
 }
 
 // Whether the incoming token takes the slot of the token that entered w
 // steps ago (ring entry e): delayed eviction -- that token was flagged;
 // immediate eviction -- the incoming token's decision evicts it now.
 __device__ inline bool takes_slot(const PlanArgs& a, int t, int32_t e, int f) {
-  if (t < a.w) return false;
-  return a.immediate ? f != 0 : (static_cast<uint32_t>(e) & kFlagBit) != 0;
+  return takes_old_slot(t, a.w, e, f, a.immediate);
 }
 
 struct HeadStep {
@@ -773,6 +771,7 @@ hipError_t launch_init_state(const dms_config& c, const Layout& lo, void* meta, 
   a.meta = static_cast<char*>(meta);
   a.ck_err = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_ck_err);
   a.head_cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_head_cnt);
+  a.plan_ctr = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_plan_ctr);
   a.n_heads = lo.max_heads;
   a.layer0 = lo.layer0;
   a.layer_stride = lo.layer_stride;

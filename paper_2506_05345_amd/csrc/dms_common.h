@@ -33,6 +33,7 @@ struct Layout {
   // workspace
   size_t ws_head_desc, ws_cum_tiles, ws_part_ml, ws_part_acc;
   size_t ws_wave_bounds, ws_wave_desc, ws_head_waves, ws_head_cnt;
+  size_t ws_plan_ctr;   // fused decode: workgroups that have read the state this launch
   size_t ws_ck_need, ws_ck_fresh, ws_ck_base, ws_ck_pos0, ws_ck_err, ws_ck_slot;
   size_t ws_pf_cum, ws_pf_meta, ws_pf_tiles, ws_pf_flags;
   size_t ws_q_sel, ws_q_page, ws_q_len;   // quest: selection [NH][B] (page-table
@@ -93,6 +94,25 @@ __host__ __device__ inline size_t k_elem_off(int j, int e) {
 __host__ __device__ inline size_t v_elem_off(int j, int e, int D) {
   return static_cast<size_t>(D) * 64 + (static_cast<size_t>((e >> 4) * 4 + (j >> 3)) * 16 + (e & 15)) * 16 +
          (j & 7) * 2;
+}
+
+// Decision of a token appended for call head hh (sequence hh / H, KV head
+// hh % H): the caller's flag, or round(sigmoid(x)) = (x > 0) with x = bf16
+// element 0 of the first query head of the group plus the offset, in float32
+// (Sec. 3.2, App. C).
+__device__ inline int token_decision(const uint8_t* flags, const uint16_t* q, int hh, int H, int g,
+                                     int D, float bias) {
+  if (q == nullptr) return flags[hh] != 0;
+  const uint32_t bits = q[static_cast<size_t>(hh) * g * D];   // (i * H + h) * g * D
+  return (__uint_as_float(bits << 16) + bias) > 0.f;
+}
+
+// Whether the token at position t takes the slot of the token that entered
+// w steps ago (ring entry e): delayed eviction -- that token was flagged;
+// immediate eviction -- the incoming token's own decision evicts it now.
+__device__ inline bool takes_old_slot(int t, int w, int32_t e, int f, int immediate) {
+  if (t < w) return false;
+  return immediate ? f != 0 : (static_cast<uint32_t>(e) & kFlagBit) != 0;
 }
 
 // Per-head descriptor written by the planning kernels, one per (seq in call,
@@ -224,6 +244,14 @@ hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void
                          const void* v, float* out, int waves, hipStream_t st,
                          hipEvent_t ev_start, hipEvent_t ev_stop, const int32_t* qpage = nullptr);
 int decode_resident_waves(const dms_config& c);
+// dms_decode_step in one launch (the append planning runs inside the decode
+// kernel); for calls where decode_step_fusable holds.
+bool decode_step_fusable(const dms_config& c, int n);
+hipError_t launch_decode_step(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
+                              int layer, int n, const int32_t* seq_ids, const uint8_t* flags,
+                              const void* q, const void* k, const void* v, uint8_t* flags_out,
+                              float* out, int waves, hipStream_t st, hipEvent_t ev_start,
+                              hipEvent_t ev_stop);
 // Decode over a latent-attention cache (kv_format DMS_KV_MLA): rows of
 // kMlaDim bf16, outputs [n, g, kMlaLatent] float32.
 hipError_t launch_decode_mla(const dms_config& c, const Layout& lo, void* meta, void* ws,

@@ -348,6 +348,34 @@ __device__ inline float wave_sum(float v) {
   return v;
 }
 
+// First tile of wave w when `total` tiles are split over W waves in equal
+// contiguous shares (w = W gives `total`); the planner and the fused decode
+// launch split a call this way.
+__device__ inline int wave_start(int64_t w, int total, int W) {
+  return static_cast<int>(w * total / W);
+}
+
+// Waves wf .. wl hold tiles [c0, c1) of a head (c1 > c0): wave_start(wf) <= c0 <
+// wave_start(wf + 1) and wave_start(wl) < c1 <= wave_start(wl + 1); bit i of the
+// mask says whether wave wf + i has a non-empty range (i < 32).
+__device__ inline int4 head_span(int c0, int c1, int total, int W) {
+  const int64_t T = total, Wl = W;
+  const int wf = static_cast<int>(((c0 + 1) * Wl + T - 1) / T) - 1;
+  const int wl = min(W - 1, static_cast<int>((c1 * Wl + T - 1) / T) - 1);
+  // wave_start(w) = floor(w T / W), stepped through the span: each step adds
+  // T / W and carries the remainder
+  const int q = total / W, rstep = total % W;
+  int rem = static_cast<int>(static_cast<int64_t>(wf) * T % Wl);
+  int mask = 0;
+  for (int i = 0; i < 32 && wf + i <= wl; ++i) {
+    rem += rstep;
+    const int grow = q + (rem >= W ? 1 : 0);   // tiles of wave wf + i
+    if (rem >= W) rem -= W;
+    if (grow > 0) mask |= 1 << i;
+  }
+  return make_int4(wf, wl, mask, 0);
+}
+
 constexpr int kMergeBatch = 64;   // partials whose (max, sum) one round of loads fetches (one per lane)
 constexpr int kMergeLoads = 32;   // 16-byte accumulator loads in flight per lane in the merge
 
@@ -363,7 +391,7 @@ constexpr int kMergeLoads = 32;   // 16-byte accumulator loads in flight per lan
 // are discarded by a select, never multiplied.
 template <int D, int PPL>
 __device__ __forceinline__ void merge_head(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsrc,
-                           const int32_t* wave_bounds, float* out, int wf, int wl, int hh, int g,
+                           int total, int W, float* out, int wf, int wl, int hh, int g,
                            int lane, float (*wts)[kMaxGroup]) {
   constexpr int U = kMergeLoads / PPL > 0 ? kMergeLoads / PPL : 1;
   const int pieces = g * D / 4;
@@ -392,7 +420,7 @@ __device__ __forceinline__ void merge_head(const float2* part_ml, __amdgpu_buffe
   bool live = false;
   for (int b0 = 0; b0 < nparts; b0 += kMergeBatch) {
     const int w2 = wf + b0 + lane;
-    live = b0 + lane < nparts && wave_bounds[w2] < wave_bounds[w2 + 1];
+    live = b0 + lane < nparts && wave_start(w2, total, W) < wave_start(w2 + 1, total, W);
     const float* ml = reinterpret_cast<const float*>(part_ml + (static_cast<size_t>(live ? w2 : wf) + hh) * kMaxGroup);
 #pragma unroll
     for (int r = 0; r < kMaxGroup; ++r) {
@@ -415,7 +443,7 @@ __device__ __forceinline__ void merge_head(const float2* part_ml, __amdgpu_buffe
   for (int b0 = 0; b0 < nparts; b0 += kMergeBatch) {
     if (nparts > kMergeBatch) {   // only the last batch's (max, sum) were kept
       const int w2 = wf + b0 + lane;
-      live = b0 + lane < nparts && wave_bounds[w2] < wave_bounds[w2 + 1];
+      live = b0 + lane < nparts && wave_start(w2, total, W) < wave_start(w2 + 1, total, W);
       const float* ml = reinterpret_cast<const float*>(part_ml + (static_cast<size_t>(live ? w2 : wf) + hh) * kMaxGroup);
 #pragma unroll
       for (int r = 0; r < kMaxGroup; ++r) {
@@ -476,19 +504,19 @@ __device__ __forceinline__ void merge_head(const float2* part_ml, __amdgpu_buffe
 // compile time (the in-flight load batch is sized by it).
 template <int D>
 __device__ __forceinline__ void merge_head_any(const float2* part_ml, __amdgpu_buffer_rsrc_t acc_rsrc,
-                               const int32_t* wave_bounds, float* out, int wf, int wl, int hh,
+                               int total, int W, float* out, int wf, int wl, int hh,
                                int g, int lane, float (*wts)[kMaxGroup]) {
   switch ((g * D / 4 + 63) / 64) {
-    case 1: merge_head<D, 1>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, g, lane, wts); break;
-    case 2: merge_head<D, 2>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, g, lane, wts); break;
-    case 3: merge_head<D, 3>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, g, lane, wts); break;
-    case 4: merge_head<D, 4>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, g, lane, wts); break;
+    case 1: merge_head<D, 1>(part_ml, acc_rsrc, total, W, out, wf, wl, hh, g, lane, wts); break;
+    case 2: merge_head<D, 2>(part_ml, acc_rsrc, total, W, out, wf, wl, hh, g, lane, wts); break;
+    case 3: merge_head<D, 3>(part_ml, acc_rsrc, total, W, out, wf, wl, hh, g, lane, wts); break;
+    case 4: merge_head<D, 4>(part_ml, acc_rsrc, total, W, out, wf, wl, hh, g, lane, wts); break;
     default:
       if constexpr (D > 64) {
         if ((g * D / 4 + 63) / 64 <= 6)
-          merge_head<D, 6>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, g, lane, wts);
+          merge_head<D, 6>(part_ml, acc_rsrc, total, W, out, wf, wl, hh, g, lane, wts);
         else
-          merge_head<D, 8>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, hh, g, lane, wts);
+          merge_head<D, 8>(part_ml, acc_rsrc, total, W, out, wf, wl, hh, g, lane, wts);
       }
       break;
   }
@@ -560,49 +588,102 @@ __device__ __forceinline__ void merge_head_small(const float2* part_ml, __amdgpu
   }
 }
 
-template <int D, bool FP8>
-__global__ __launch_bounds__(256, 1) void decode_kernel(
-    const int32_t* __restrict__ status, const HeadDesc* __restrict__ desc,
-    const int32_t* __restrict__ cum_tiles, const int32_t* __restrict__ wave_bounds,
-    const int4* __restrict__ wave_desc, const int4* __restrict__ head_waves,
-    int32_t* __restrict__ head_cnt,
+// Where a decode launch finds the call's work split: the planning kernel's
+// output in the workspace (GlobalPlan) or the plan every workgroup of a fused
+// launch builds in LDS (LdsPlan).  Both give, for call head hh, its tile range
+// [cum(hh), cum(hh + 1)) in the flat tile list and its descriptor (retained
+// length, state head, slot appended by this call, and the page popped for
+// that slot when the page table may not hold it yet, else -1); every value is
+// uniform across the wave.
+struct GlobalPlan {
+  const HeadDesc* desc;
+  const int32_t* cum;
+  const int32_t* wave_bounds;
+  const int4* wave_desc;
+  const int4* head_waves;   // per head: first / last wave holding its tiles, live mask
+  int total;
+  // the planner's descriptor of wave w's first segment comes with its range,
+  // so a wave starts after one round of scalar loads
+  __device__ __forceinline__ bool first(int w, int& tb, int& te, int& hh, int& c0, int& c1, HeadDesc& d) const {
+    const int4 wd0 = ldc(wave_desc, 2 * w), wd1 = ldc(wave_desc, 2 * w + 1);
+    tb = ldc(wave_bounds, w);
+    te = ldc(wave_bounds, w + 1);
+    hh = wd0.z;
+    c0 = wd0.w;
+    c1 = wd1.x;
+    d = make_int4(wd1.y, wd1.z, wd1.w, -1);
+    return tb < te;
+  }
+  __device__ __forceinline__ void next(int& hh, int tb, int& c0, int& c1, HeadDesc& d) const {
+    while (ldc(cum, hh + 1) <= tb) ++hh;
+    c0 = ldc(cum, hh);
+    c1 = ldc(cum, hh + 1);
+    d = ldc(desc, hh);
+    d.w = -1;   // the planner has written the page table
+  }
+  __device__ __forceinline__ int4 span(int hh, int) const { return ldc(head_waves, hh); }
+};
+
+struct LdsPlan {
+  const int* cum;      // [NH + 1]
+  const int4* desc;    // [NH]
+  int total, W, NH;
+  __device__ __forceinline__ int cum_at(int i) const { return __builtin_amdgcn_readfirstlane(cum[i]); }
+  __device__ __forceinline__ HeadDesc head(int hh) const {
+    const int4 v = desc[hh];
+    return make_int4(__builtin_amdgcn_readfirstlane(v.x), __builtin_amdgcn_readfirstlane(v.y),
+                     __builtin_amdgcn_readfirstlane(v.z), __builtin_amdgcn_readfirstlane(v.w));
+  }
+  __device__ __forceinline__ bool first(int w, int& tb, int& te, int& hh, int& c0, int& c1, HeadDesc& d) const {
+    tb = wave_start(w, total, W);
+    te = wave_start(w + 1, total, W);
+    if (tb >= te) return false;
+    int lo = 0, hi = NH - 1;   // the head holding tile tb: largest hh with cum[hh] <= tb
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (cum_at(mid) <= tb) lo = mid; else hi = mid - 1;
+    }
+    hh = lo;
+    c0 = cum_at(hh);
+    c1 = cum_at(hh + 1);
+    d = head(hh);
+    return true;
+  }
+  __device__ __forceinline__ void next(int& hh, int tb, int& c0, int& c1, HeadDesc& d) const {
+    while (cum_at(hh + 1) <= tb) ++hh;
+    c0 = cum_at(hh);
+    c1 = cum_at(hh + 1);
+    d = head(hh);
+  }
+  __device__ __forceinline__ int4 span(int hh, int W_) const {
+    return head_span(cum_at(hh), cum_at(hh + 1), total, W_);
+  }
+};
+
+// One decode wave's work: stream its tile range (split-K over the retained
+// slots of the heads it covers), write whole heads' outputs, publish partials
+// of heads it shares, and merge the heads whose tile count it completes.
+template <int D, bool FP8, class Plan>
+__device__ __forceinline__ void decode_wave(
+    const Plan& plan, int wave, int W, int32_t* __restrict__ head_cnt,
     const int32_t* __restrict__ page_table, const int32_t* __restrict__ qpage,
     char* __restrict__ pool, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_in,
     const uint16_t* __restrict__ v_in, float2* __restrict__ part_ml, float* __restrict__ part_acc,
-    float* __restrict__ out, DecodeParams a) {
-  __shared__ float merge_wts[kWavesPerBlock][kMergeBatch][kMaxGroup];
+    float* __restrict__ out, const DecodeParams& a, float (*merge_wts)[kMaxGroup]) {
   const int lane = threadIdx.x & 63;
-  // wave index is uniform across the wave; say so, so that everything derived
-  // from it (head, tile, page) lives in scalar registers
-  const int wave = blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, G = lane >> 4;
-  // the planner's descriptor of this wave's first segment comes with the
-  // range, so a wave starts after one round of scalar loads
-  const int4 wd0 = ldc(wave_desc, 2 * wave), wd1 = ldc(wave_desc, 2 * wave + 1);
-  int tb = ldc(wave_bounds, wave);
-  const int te = ldc(wave_bounds, wave + 1);
-  if (load_status(status) != 0) return;
-  if (tb >= te) return;
-  int hh = wd0.z;
+  int tb, te, hh, c0, c1;
+  HeadDesc d;
+  if (!plan.first(wave, tb, te, hh, c0, c1, d)) return;
   const int tiles_per_page_log2 = a.log2P - 5;
   bool first = true;
-  // heads shared with other waves, published at the end: head, tiles, total
-  int p_hh[2] = {0, 0}, p_cnt[2] = {0, 0}, p_tot[2] = {0, 0};
+  // heads shared with other waves (at most the first and the last segment),
+  // published at the end: head, tiles of this wave, tiles of the head
+  int p_hh0 = 0, p_cnt0 = 0, p_tot0 = 0, p_hh1 = 0, p_cnt1 = 0, p_tot1 = 0;
   int npend = 0;
   while (tb < te) {
-    int c0, c1;
-    HeadDesc d;
-    if (first) {
-      c0 = wd0.w;
-      c1 = wd1.x;
-      d = make_int4(wd1.y, wd1.z, wd1.w, 0);
-      first = false;
-    } else {
-      while (ldc(cum_tiles, hh + 1) <= tb) ++hh;
-      c0 = ldc(cum_tiles, hh);
-      c1 = ldc(cum_tiles, hh + 1);
-      d = ldc(desc, hh);
-    }
+    if (!first) plan.next(hh, tb, c0, c1, d);
+    first = false;
     const int seg_end = min(te, c1);
     const int L = d.x;
     const int32_t* pt = page_table + static_cast<size_t>(d.y) * a.maxp;
@@ -628,8 +709,13 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
     // tile t of the head: page from a scalar load (the whole wave works on
     // one head), then the tile's 16 KB block inside the page
     constexpr size_t kTileBytes = FP8 ? static_cast<size_t>(D) * 64 + 256 : static_cast<size_t>(D) * 128;
+    // a page this call popped (fused launch) is taken from the plan: its
+    // page-table entry may not be written yet
+    const int new_pi = d.w >= 0 ? (d.z >> 5) >> tiles_per_page_log2 : -1;
     auto tile_in = [&](const int32_t* pl, int t) -> char* {
-      return pool + static_cast<size_t>(ldc(pl, t >> tiles_per_page_log2)) * a.page_bytes +
+      const int pi = t >> tiles_per_page_log2;
+      const int pg = pi == new_pi ? d.w : ldc(pl, pi);
+      return pool + static_cast<size_t>(pg) * a.page_bytes +
              static_cast<size_t>(t & ((1 << tiles_per_page_log2) - 1)) * kTileBytes;
     };
     auto tile_of = [&](int t) -> char* { return tile_in(pages, t); };
@@ -751,9 +837,15 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
           __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc.o[b]), acc_rsrc,
                                                  o + 64 * b, 0, kCachePolicySc1);
       }
-      p_hh[npend] = hh;
-      p_cnt[npend] = seg_end - tb;
-      p_tot[npend] = c1 - c0;
+      if (npend == 0) {
+        p_hh0 = hh;
+        p_cnt0 = seg_end - tb;
+        p_tot0 = c1 - c0;
+      } else {
+        p_hh1 = hh;
+        p_cnt1 = seg_end - tb;
+        p_tot1 = c1 - c0;
+      }
       ++npend;
     }
     tb = seg_end;
@@ -767,35 +859,251 @@ __global__ __launch_bounds__(256, 1) void decode_kernel(
   if (npend > 0) {
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     int prev = 0;
-    if (lane < npend) prev = atomicAdd(&head_cnt[lane == 0 ? p_hh[0] : p_hh[1]], lane == 0 ? p_cnt[0] : p_cnt[1]);
+    if (lane < npend) prev = atomicAdd(&head_cnt[lane == 0 ? p_hh0 : p_hh1], lane == 0 ? p_cnt0 : p_cnt1);
     const int prev0 = __shfl(prev, 0, 64), prev1 = __shfl(prev, 1, 64);
     const __amdgpu_buffer_rsrc_t acc_rsrc = __builtin_amdgcn_make_buffer_rsrc(
         part_acc, static_cast<short>(0), a.part_acc_bytes, kBufferDword3);
     for (int i = 0; i < npend; ++i) {
-      if ((i == 0 ? prev0 : prev1) + p_cnt[i] != p_tot[i]) continue;
-      const int mh = p_hh[i];
-      const int4 hw = ldc(head_waves, mh);   // waves wf .. wl hold the head's tiles
+      if (i == 0 ? prev0 + p_cnt0 != p_tot0 : prev1 + p_cnt1 != p_tot1) continue;
+      const int mh = i == 0 ? p_hh0 : p_hh1;
+      const int4 hw = plan.span(mh, W);   // waves wf .. wl hold the head's tiles
       const int wf = hw.x, wl = hw.y;
       if (wl - wf < 4)
         merge_head_small<D>(part_ml, acc_rsrc, hw.z, out, wf, wl - wf + 1, mh, a.g, lane);
       else
-        merge_head_any<D>(part_ml, acc_rsrc, wave_bounds, out, wf, wl, mh, a.g, lane,
-                          merge_wts[threadIdx.x >> 6]);
+        merge_head_any<D>(part_ml, acc_rsrc, plan.total, W, out, wf, wl, mh, a.g, lane, merge_wts);
       if (lane == 0) __hip_atomic_store(&head_cnt[mh], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
 
+// Decode launch after the planning kernel (workspace plan).
 template <int D, bool FP8>
-hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
-                           int layer, int n, const void* q, const void* k, const void* v, float* out,
-                           int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop,
-                           const int32_t* qpage) {
-  char* w = static_cast<char*>(ws);
-  const int32_t* status = reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status);
-  const int32_t* cum = reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles);
-  float2* part_ml = reinterpret_cast<float2*>(w + lo.ws_part_ml);
-  float* part_acc = reinterpret_cast<float*>(w + lo.ws_part_acc);
+__global__ __launch_bounds__(256, 1) void decode_kernel(
+    const int32_t* __restrict__ status, const HeadDesc* __restrict__ desc,
+    const int32_t* __restrict__ cum_tiles, const int32_t* __restrict__ wave_bounds,
+    const int4* __restrict__ wave_desc, const int4* __restrict__ head_waves,
+    int32_t* __restrict__ head_cnt,
+    const int32_t* __restrict__ page_table, const int32_t* __restrict__ qpage,
+    char* __restrict__ pool, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_in,
+    const uint16_t* __restrict__ v_in, float2* __restrict__ part_ml, float* __restrict__ part_acc,
+    float* __restrict__ out, DecodeParams a) {
+  __shared__ float merge_wts[kWavesPerBlock][kMergeBatch][kMaxGroup];
+  if (load_status(status) != 0) return;
+  // wave index is uniform across the wave; say so, so that everything derived
+  // from it (head, tile, page) lives in scalar registers
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const GlobalPlan plan{desc, cum_tiles, wave_bounds, wave_desc, head_waves, ldc(cum_tiles, a.NH)};
+  decode_wave<D, FP8>(plan, blockIdx.x * kWavesPerBlock + wid, a.W, head_cnt, page_table, qpage,
+                      pool, q, k_in, v_in, part_ml, part_acc, out, a, merge_wts[wid]);
+}
+
+// ---------------------------------------------------------------------------
+// Fused decode step: append planning inside the decode launch
+// ---------------------------------------------------------------------------
+
+constexpr int kFuseMaxHeads = 1024;   // call heads a fused launch plans in LDS
+constexpr int kFuseHeadsPerThread = kFuseMaxHeads / 256;
+
+struct FusedArgs {
+  LayerState st;
+  int32_t* status;
+  const int32_t* seq_ids;
+  const uint8_t* flags;    // [n, H] caller decisions, or null (decisions from q)
+  const uint16_t* q_dec;   // queries for the borrowed-neuron decisions, or null
+  uint8_t* flags_out;      // nullable: decisions taken from q
+  int32_t* plan_ctr;       // workgroups of this launch that have read the state
+  float bias;
+  int immediate, n, H, w, P, maxp, max_slots, max_seqs, g, D;
+};
+
+// Rule R1 for one appended token per (sequence, KV head) of the call, done by
+// every workgroup of the launch into its LDS: each head's slot (the slot of
+// the token w positions back when that one leaves the cache, else the next
+// fresh one), the pages popped in call order, the retained lengths and the
+// tile prefix sums of the work split.  The loads form three dependent rounds
+// (sequence ids and decisions; positions and lengths, issued for clamped ids
+// before the ids are validated; ring entries and stack).  Nothing is written
+// to the state here: once a workgroup has read it, its first thread adds one
+// to a launch counter in the workspace without waiting for the result, and
+// the workgroup whose add completes the count writes the new state after its
+// decode work (write_state), when every other workgroup has finished reading.
+// Returns false in every thread when the call does nothing (a sticky error was
+// set before, or this call sets one; all workgroups take the same decision
+// from the same data).  *total gets the call's tile count, *new_top the stack
+// height after the call's pops; *ticket, in thread 0, the counter value before
+// its add.
+__device__ __forceinline__ bool fused_plan(const FusedArgs& f, int* s_cum, int4* s_desc, int2* s_aux,
+                                           uint32_t* s_seen, int32_t* s_stack, int* s_scan,
+                                           int* total, int* ticket, int* new_top) {
+  const int tid = threadIdx.x;
+  const int NH = f.n * f.H;
+  // round 1: status and stack height (one thread reads them for the whole
+  // workgroup: another workgroup may set the status meanwhile, and every
+  // thread must take the same exit), sequence ids, decisions
+  if (tid == 0) {
+    s_scan[0] = load_status(f.status);
+    s_scan[1] = *f.st.top;
+  }
+  for (int i = tid; i < ((f.max_seqs + 31) >> 5); i += blockDim.x) s_seen[i] = 0;
+  int seq[kFuseHeadsPerThread], dec[kFuseHeadsPerThread], pos[kFuseHeadsPerThread];
+  int L[kFuseHeadsPerThread];
+#pragma unroll
+  for (int k = 0; k < kFuseHeadsPerThread; ++k) {
+    const int hh = kFuseHeadsPerThread * tid + k;
+    seq[k] = hh < NH ? f.seq_ids[hh / f.H] : 0;
+    dec[k] = hh < NH ? token_decision(f.flags, f.q_dec, hh, f.H, f.g, f.D, f.bias) : 0;
+  }
+  // round 2, issued before the ids are validated (clamped into range; the
+  // values are only used once the ids are known to be valid)
+#pragma unroll
+  for (int k = 0; k < kFuseHeadsPerThread; ++k) {
+    const int hh = kFuseHeadsPerThread * tid + k;
+    const int s = min(max(seq[k], 0), f.max_seqs - 1);
+    pos[k] = hh < NH ? f.st.pos[s] : 0;
+    L[k] = hh < NH ? f.st.len[s * f.H + hh % f.H] : 0;
+  }
+  __syncthreads();
+  const int status = s_scan[0];
+  const int top0 = s_scan[1];
+  // sequence ids in range and not repeated
+  int bad = 0;
+  if (status == 0) {
+#pragma unroll
+    for (int k = 0; k < kFuseHeadsPerThread; ++k) {
+      const int hh = kFuseHeadsPerThread * tid + k;
+      if (hh < NH && hh % f.H == 0) {
+        const int s = seq[k];
+        if (s < 0 || s >= f.max_seqs) {
+          bad = 1;
+        } else {
+          const uint32_t bit = 1u << (s & 31);
+          if (atomicOr(&s_seen[s >> 5], bit) & bit) bad = 1;
+        }
+      }
+    }
+  }
+  bad = __syncthreads_or(bad);   // also orders s_scan's reads above before its reuse
+  if (status != 0) return false;
+  if (bad) {
+    if (tid == 0) set_status(f.status, DMS_ERR_BAD_SEQ);
+    return false;
+  }
+  // round 3: ring entries, and the pages this call may pop in pop order
+  for (int i = tid; i < min(NH, top0); i += blockDim.x) s_stack[i] = f.st.stack[top0 - 1 - i];
+  int sh[kFuseHeadsPerThread], slot[kFuseHeadsPerThread], fresh[kFuseHeadsPerThread];
+  int need[kFuseHeadsPerThread];
+  int cap = 0, my_need = 0, my_tiles = 0;
+#pragma unroll
+  for (int k = 0; k < kFuseHeadsPerThread; ++k) {
+    const int hh = kFuseHeadsPerThread * tid + k;
+    sh[k] = slot[k] = fresh[k] = need[k] = 0;
+    if (hh < NH) {
+      sh[k] = seq[k] * f.H + hh % f.H;
+      const int32_t e = f.st.ring[static_cast<size_t>(sh[k]) * f.w + pos[k] % f.w];
+      const bool reuse = takes_old_slot(pos[k], f.w, e, dec[k], f.immediate);
+      slot[k] = reuse ? static_cast<int>(static_cast<uint32_t>(e) & ~kFlagBit) : L[k];
+      fresh[k] = !reuse;
+      cap |= fresh[k] && slot[k] >= f.max_slots;
+      need[k] = fresh[k] && (slot[k] % f.P) == 0;
+      L[k] += fresh[k];
+    }
+    my_need += need[k];
+    my_tiles += (L[k] + kTile - 1) / kTile;
+  }
+  int2 tot;
+  const int2 ex = block_exclusive_scan2(make_int2(my_need, my_tiles), s_scan, &tot);
+  cap = __syncthreads_or(cap);
+  if (cap || tot.x > top0) {
+    if (tid == 0) set_status(f.status, cap ? DMS_ERR_CAPACITY : DMS_ERR_OUT_OF_PAGES);
+    return false;
+  }
+  int pop = ex.x, ct = ex.y;
+#pragma unroll
+  for (int k = 0; k < kFuseHeadsPerThread; ++k) {
+    const int hh = kFuseHeadsPerThread * tid + k;
+    if (hh < NH) {
+      const int pg = need[k] ? s_stack[pop] : -1;
+      pop += need[k];
+      ct += (L[k] + kTile - 1) / kTile;
+      s_desc[hh] = make_int4(L[k], sh[k], slot[k], pg);
+      s_aux[hh] = make_int2(pos[k], dec[k] | (fresh[k] << 1));
+      s_cum[hh + 1] = ct;
+    }
+  }
+  if (tid == 0) s_cum[0] = 0;
+  *total = tot.y;
+  *new_top = top0 - tot.x;
+  // every load of the state above has returned (its values are in LDS or
+  // registers): count this workgroup as done reading; the last to count
+  // writes the new state
+  __syncthreads();
+  if (tid == 0) *ticket = atomicAdd(f.plan_ctr, 1);
+  return true;
+}
+
+// The new state of the call's heads (one wave of the workgroup that read the
+// state last): rings, slot owners, lengths, new page-table entries, positions,
+// stack height, decisions taken; then the launch counter is reset.
+__device__ __forceinline__ void write_state(const FusedArgs& f, const int4* s_desc, const int2* s_aux,
+                                            int top0_minus_pops, int lane) {
+  const int NH = f.n * f.H;
+  for (int hh = lane; hh < NH; hh += 64) {
+    const int4 d = s_desc[hh];       // Lnew, state head, slot, page popped (-1: none)
+    const int2 x = s_aux[hh];        // position, decision | fresh << 1
+    const int dec = x.y & 1;
+    const uint32_t fb = dec ? kFlagBit : 0u;
+    if (f.flags_out != nullptr) f.flags_out[hh] = static_cast<uint8_t>(dec);
+    if (d.w >= 0) f.st.page_table[static_cast<size_t>(d.y) * f.maxp + d.z / f.P] = d.w;
+    if (x.y & 2) f.st.len[d.y] = d.x;
+    f.st.ring[static_cast<size_t>(d.y) * f.w + x.x % f.w] = static_cast<int32_t>(static_cast<uint32_t>(d.z) | fb);
+    f.st.slot_meta[static_cast<size_t>(d.y) * f.max_slots + d.z] = static_cast<int32_t>(static_cast<uint32_t>(x.x) | fb);
+    if (hh % f.H == 0) f.st.pos[f.seq_ids[hh / f.H]] = x.x + 1;
+  }
+  if (lane == 0) {
+    *f.st.top = top0_minus_pops;
+    __hip_atomic_store(f.plan_ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Decode waves of a fused launch: at least kFuseMinTiles tiles per wave and at
+// least one wave per workgroup (so every compute unit streams), at most all
+// resident waves.  Fewer, longer waves split small calls into fewer parts.
+constexpr int kFuseMinTiles = 8;
+
+// dms_decode_step in one launch (calls of up to kFuseMaxHeads heads without
+// page retrieval): fused planning, then the decode waves.  With fewer active
+// waves than resident ones, logical wave lw runs as wave lw / B of workgroup
+// lw % B (B workgroups), spreading the active waves over all compute units.
+template <int D, bool FP8>
+__global__ __launch_bounds__(256, 1) void decode_step_kernel(
+    FusedArgs f, int32_t* __restrict__ head_cnt, char* __restrict__ pool,
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_in,
+    const uint16_t* __restrict__ v_in, float2* __restrict__ part_ml, float* __restrict__ part_acc,
+    float* __restrict__ out, DecodeParams a) {
+  __shared__ float merge_wts[kWavesPerBlock][kMergeBatch][kMaxGroup];
+  __shared__ int s_cum[kFuseMaxHeads + 1];
+  __shared__ int4 s_desc[kFuseMaxHeads];
+  __shared__ int2 s_aux[kFuseMaxHeads];
+  __shared__ uint32_t s_seen[kMaxSeqs / 32];
+  __shared__ int32_t s_stack[kFuseMaxHeads];
+  __shared__ int s_scan[34];
+  int total = 0, ticket = 0, new_top = 0;
+  if (!fused_plan(f, s_cum, s_desc, s_aux, s_seen, s_stack, s_scan, &total, &ticket, &new_top)) return;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nb = gridDim.x;
+  const int T = __builtin_amdgcn_readfirstlane(total);
+  const int W = min(a.W, max(nb, (T + kFuseMinTiles - 1) / kFuseMinTiles));
+  const int lw = W == a.W ? blockIdx.x * kWavesPerBlock + wid : wid * nb + blockIdx.x;
+  const LdsPlan plan{s_cum, s_desc, T, W, a.NH};
+  if (lw < W)
+    decode_wave<D, FP8>(plan, lw, W, head_cnt, f.st.page_table, nullptr, pool, q, k_in, v_in,
+                        part_ml, part_acc, out, a, merge_wts[wid]);
+  // the workgroup whose count completed the launch's writes the new state
+  if (wid == 0 && __shfl(ticket, 0, 64) == nb - 1) write_state(f, s_desc, s_aux, new_top, threadIdx.x & 63);
+}
+
+DecodeParams decode_params(const dms_config& c, const Layout& lo, int D, int n, int waves) {
   DecodeParams a;
   a.page_bytes = lo.page_bytes;
   a.part_acc_bytes = static_cast<int>(static_cast<size_t>(lo.max_partials) * c.group_size * D * 4);
@@ -808,6 +1116,59 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
   a.zero_neuron = c.decision_source == DMS_DECIDE_QUERY;
   a.qB = c.quest_page_budget;
   a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
+  return a;
+}
+
+template <int D, bool FP8>
+hipError_t launch_decode_step_d(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                                void* pool, int layer, int n, const int32_t* seq_ids,
+                                const uint8_t* flags, const void* q, const void* k, const void* v,
+                                uint8_t* flags_out, float* out, int waves, hipStream_t st,
+                                hipEvent_t ev_start, hipEvent_t ev_stop) {
+  char* w = static_cast<char*>(ws);
+  FusedArgs f;
+  f.st = layer_state(lo, meta, layer);
+  f.status = reinterpret_cast<int32_t*>(static_cast<char*>(meta) + lo.status);
+  f.seq_ids = seq_ids;
+  const bool from_q = c.decision_source == DMS_DECIDE_QUERY;
+  f.flags = from_q ? nullptr : flags;
+  f.q_dec = from_q ? static_cast<const uint16_t*>(q) : nullptr;
+  f.flags_out = flags_out;
+  f.plan_ctr = reinterpret_cast<int32_t*>(w + lo.ws_plan_ctr);
+  f.bias = c.decision_bias;
+  f.immediate = c.eviction == DMS_EVICT_IMMEDIATE;
+  f.n = n;
+  f.H = c.num_kv_heads;
+  f.w = c.window;
+  f.P = c.page_size;
+  f.maxp = c.max_pages_per_head;
+  f.max_slots = lo.max_slots;
+  f.max_seqs = c.max_seqs;
+  f.g = c.group_size;
+  f.D = D;
+  const DecodeParams a = decode_params(c, lo, D, n, waves);
+  if (ev_start) (void)hipEventRecord(ev_start, st);
+  hipLaunchKernelGGL((decode_step_kernel<D, FP8>), dim3(waves / kWavesPerBlock), dim3(256), 0, st, f,
+                     reinterpret_cast<int32_t*>(w + lo.ws_head_cnt), static_cast<char*>(pool),
+                     static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                     static_cast<const uint16_t*>(v), reinterpret_cast<float2*>(w + lo.ws_part_ml),
+                     reinterpret_cast<float*>(w + lo.ws_part_acc), out, a);
+  hipError_t e = hipGetLastError();
+  if (ev_stop) (void)hipEventRecord(ev_stop, st);
+  return e;
+}
+
+template <int D, bool FP8>
+hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
+                           int layer, int n, const void* q, const void* k, const void* v, float* out,
+                           int waves, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop,
+                           const int32_t* qpage) {
+  char* w = static_cast<char*>(ws);
+  const int32_t* status = reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status);
+  const int32_t* cum = reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles);
+  float2* part_ml = reinterpret_cast<float2*>(w + lo.ws_part_ml);
+  float* part_acc = reinterpret_cast<float*>(w + lo.ws_part_acc);
+  const DecodeParams a = decode_params(c, lo, D, n, waves);
   if (ev_start) (void)hipEventRecord(ev_start, st);
   hipLaunchKernelGGL((decode_kernel<D, FP8>), dim3(waves / kWavesPerBlock), dim3(256), 0, st, status,
                      reinterpret_cast<const HeadDesc*>(w + lo.ws_head_desc), cum,
@@ -843,6 +1204,39 @@ hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void
                                           ev_start, ev_stop, qpage);
 }
 
+// Calls of at most this many KV heads take the fused launch.  Measured on
+// MI355X (step time, fused / planner + decode): 1.5B-shaped 32 x 2 heads 1.00
+// / 1.15 ms (the fused launch also splits the call over fewer, longer waves,
+// so heads are merged from ~6 partials instead of ~16-33); 7B-shaped 64 x 4
+// heads 3.75 / 3.71 ms; 32B-shaped 128 x 8 heads 24.36 / 24.37 ms.  The
+// in-kernel planning costs about what the planning kernel does (three
+// dependent rounds of loads of cold state, ~8-10 us), so it only pays where
+// the smaller split does.
+constexpr int kFuseCallHeads = 128;
+
+bool decode_step_fusable(const dms_config& c, int n) {
+  static_assert(kFuseCallHeads <= kFuseMaxHeads, "fused calls are planned in LDS");
+  return c.kv_format != DMS_KV_MLA && c.quest_page_budget == 0 &&
+         static_cast<int64_t>(n) * c.num_kv_heads <= kFuseCallHeads;
+}
+
+hipError_t launch_decode_step(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
+                              int layer, int n, const int32_t* seq_ids, const uint8_t* flags,
+                              const void* q, const void* k, const void* v, uint8_t* flags_out,
+                              float* out, int waves, hipStream_t st, hipEvent_t ev_start,
+                              hipEvent_t ev_stop) {
+  const bool fp8 = c.kv_format == DMS_KV_FP8;
+  if (c.head_dim == 128)
+    return fp8 ? launch_decode_step_d<128, true>(c, lo, meta, ws, pool, layer, n, seq_ids, flags, q, k, v,
+                                                 flags_out, out, waves, st, ev_start, ev_stop)
+               : launch_decode_step_d<128, false>(c, lo, meta, ws, pool, layer, n, seq_ids, flags, q, k, v,
+                                                  flags_out, out, waves, st, ev_start, ev_stop);
+  return fp8 ? launch_decode_step_d<64, true>(c, lo, meta, ws, pool, layer, n, seq_ids, flags, q, k, v,
+                                              flags_out, out, waves, st, ev_start, ev_stop)
+             : launch_decode_step_d<64, false>(c, lo, meta, ws, pool, layer, n, seq_ids, flags, q, k, v,
+                                               flags_out, out, waves, st, ev_start, ev_stop);
+}
+
 // One decode wave per SIMD (a block of 4 waves per CU).  Measured on MI355X
 // at the Qwen-R1-32B-shaped workload this beats two per SIMD (fewer split
 // heads to merge, same bandwidth); the launch must fit entirely, so the
@@ -859,6 +1253,13 @@ int decode_resident_waves(const dms_config& c) {
       : (fp8 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_kernel<64, true>, 256, 0)
              : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_kernel<64, false>, 256, 0));
   if (e != hipSuccess || blocks < 1) return -1;
+  int fblocks = 0;
+  e = c.head_dim == 128
+      ? (fp8 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&fblocks, decode_step_kernel<128, true>, 256, 0)
+             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&fblocks, decode_step_kernel<128, false>, 256, 0))
+      : (fp8 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&fblocks, decode_step_kernel<64, true>, 256, 0)
+             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&fblocks, decode_step_kernel<64, false>, 256, 0));
+  if (e != hipSuccess || fblocks < 1) return -1;
   int waves = cus * kWavesPerBlock;
   if (waves > kMaxWaves) waves = kMaxWaves / kWavesPerBlock * kWavesPerBlock;
   return waves;

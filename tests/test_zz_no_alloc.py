@@ -1,10 +1,11 @@
 """dms_decode_step_static (planner output, split-K partials and arrival
 counters in the library's static device scratch, nothing allocated) against
-dms_decode_step (the same kernels over the context's workspace) and against
-the CPU oracle: two contexts with identical state take identical decode
-steps, one through each entry point.  Outputs must be identical bit for bit
-(same kernels, same work split) and within 1e-2 of the oracle's replay;
-bookkeeping bit-exact on both sides.  Two calls in a row, the second with
+dms_decode_step (over the context's workspace) and against the CPU oracle:
+two contexts with identical state take identical decode steps, one through
+each entry point.  dms_decode_step may split a call differently (its fused
+launch sizes the wave count to the call), so the two outputs agree up to
+float32 reassociation: both within 1e-2 of each other and of the oracle's
+replay; bookkeeping bit-exact on both sides.  Two calls in a row, the second with
 fewer sequences, then a call from a third context of another shape on the
 same GPU (the scratch keeps the last call's contents)."""
 import numpy as np
@@ -80,11 +81,11 @@ def _step_both(dms, cfg, caches, inputs, orc, seqs, pos):
         outs.append(out.cpu().numpy())
     orc.append(seqs, f, bf16_to_f32(k), bf16_to_f32(v))
     ref = orc.decode(seqs, bf16_to_f32(q), g)
-    assert np.array_equal(outs[0], outs[1], equal_nan=False), \
-        float(np.nanmax(np.abs(outs[0] - outs[1])))
-    assert np.isfinite(outs[1]).all()
+    assert np.isfinite(outs[0]).all() and np.isfinite(outs[1]).all()
+    assert float(np.abs(outs[0] - outs[1]).max()) <= ATOL
     err = float(np.abs(outs[1] - ref).max())
     assert err <= ATOL, err
+    assert float(np.abs(outs[0] - ref).max()) <= ATOL
     v0, v1 = caches[0].export(0), caches[1].export(0)
     compare_state(v1, orc, range(cfg.max_seqs))
     compare_state(v0, orc, range(cfg.max_seqs))
