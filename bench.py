@@ -26,8 +26,14 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 # rocprofv3 summary of the decode kernel on the default workload
-TRAFFIC_PROFILE = "decode_kernel_qwen-r1-32b-8x.txt"
-TRAFFIC_PROFILE_FP8 = "decode_kernel_qwen-r1-32b-8x-fp8.txt"
+# rocprofv3 summaries of the decode kernel by (workload, page format)
+TRAFFIC_PROFILES = {
+    ("qwen-r1-32b-8x", "bf16"): "decode_kernel_qwen-r1-32b-8x.txt",
+    ("qwen-r1-32b-8x", "fp8"): "decode_kernel_qwen-r1-32b-8x-fp8.txt",
+    ("qwen-r1-7b-4x", "bf16"): "decode_kernel_qwen-r1-7b-4x.txt",
+    ("qwen-r1-1.5b-8x", "bf16"): "decode_step_kernel_qwen-r1-1.5b-8x.txt",
+}
+LATENCY_STEPS = 50   # default steps timed one by one for the per-step distribution
 
 # Synthetic stand-ins for the paper's reasoning-model shapes (Qwen-R1 family).
 WORKLOADS = {
@@ -278,17 +284,23 @@ def cpu_baseline(wl, ctx, budget_s=12.0):
         if time.perf_counter() - t_start > 4 * budget_s:
             break
     threads = os.cpu_count()
+    blas = None
     try:
         from threadpoolctl import threadpool_info
         info = threadpool_info()
         if info:
             threads = max(int(x.get("num_threads", 1)) for x in info)
+            blas = ", ".join(sorted({f"{x.get('internal_api')} {x.get('version')}" for x in info
+                                     if x.get("user_api") == "blas"})) or None
     except Exception:
         pass
     return {
         "value": bytes_equiv / elapsed / 1e9,
         "unit": "GB/s",
         "cores": threads,
+        "host_cpus": os.cpu_count(),
+        "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
+        "numpy_blas": blas,
         "kind": "oracle",
         "sample": f"{head_steps} head-steps (one KV head, its {g} query heads, one decode "
                   f"position, dense float64 masked {'absorbed latent ' if mla else ''}attention over "
@@ -744,6 +756,9 @@ def main():
     ap.add_argument("--kv-format", choices=["bf16", "fp8"], default="bf16",
                     help="page format of the decode workloads (fp8: E4M3 rows with power-of-two scales)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--latency-steps", type=int, default=LATENCY_STEPS,
+                    help="decode workloads: further steps timed one by one (own HIP graph each) for "
+                         "the per-step p10/p50/p90; 0 skips them")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run a 1 GiB device copy first (reference kernel for HBM counters)")
     ap.add_argument("--eager", action="store_true",
@@ -756,6 +771,7 @@ def main():
                                    "has no multi-GPU mode (--gpus must be 1)"}))
         sys.exit(2)
 
+    import numpy as np
     import torch
     from paper_2506_05345_amd import dms
 
@@ -789,7 +805,7 @@ def main():
     if quest:
         wl["quest_pages"] = args.quest_pages
         wl["desc"] += f", Quest page retrieval: {args.quest_pages} pages of 64 slots per head"
-    S = args.warmup + 2 * args.steps
+    S = args.warmup + 2 * args.steps + args.latency_steps
     cache, ctx, L0 = build(wl, S, args.chunk, dev)
     q, k, v, flags, fresh = step_inputs(wl, ctx, S, dev)
     B, H, g, D, nl = wl["batch"], wl["kv_heads"], wl["group"], wl["head_dim"], wl["layers"]
@@ -821,6 +837,7 @@ def main():
                 run_step(s)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    log("timed steps captured" if graph is not None else "timed steps: eager")
     t0 = time.perf_counter()
     ev0.record()
     if graph is not None:
@@ -831,6 +848,7 @@ def main():
     ev1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    log("timed steps done; kernel-timing pass")
     # Decode-kernel duration: HIP events recorded by the library around every
     # decode launch of an eager pass over the next `steps` steps (events inside
     # a captured graph only mark dependencies on this runtime).
@@ -861,6 +879,7 @@ def main():
             run_step(s)
     torch.cuda.synchronize()
     kern_ms, launches = dms.dms_profile_stop(cache.ctx)[dms.DMS_PROFILE_DECODE]
+    log("kernel-timing pass done")
     if launches != args.steps * nl:
         raise RuntimeError(f"timing events recorded {launches} of {args.steps * nl} decode launches")
     step_ms = ev0.elapsed_time(ev1) / args.steps
@@ -871,7 +890,7 @@ def main():
     lens = torch.empty((B, H), dtype=torch.int32, device=dev)
     for layer in range(nl):
         dms.dms_retained_lengths(cache.ctx, layer, B, sid, lens)
-        if not torch.equal(lens.to(torch.int64), Lstep[-1, layer]):
+        if not torch.equal(lens.to(torch.int64), Lstep[k_hi - 1, layer]):
             raise RuntimeError(f"layer {layer}: retained lengths diverged from the closed form")
     per_step_bytes = float(kv_bytes[t_lo:t_hi].sum()) / args.steps
     per_launch_bytes = float(kv_bytes[k_lo:k_hi].sum()) / (args.steps * nl)
@@ -883,9 +902,38 @@ def main():
     kern_avg_ms = kern_ms / max(launches, 1)
     achieved = per_launch_bytes / (kern_avg_ms * 1e-3) / 1e9
     mean_L = float(Lstep[t_lo:t_hi].double().mean())
+    # per-step latency distribution: args.latency_steps further steps, each
+    # captured as its own graph and replayed once between HIP events
+    lat_ms = []
+    n_lat = args.latency_steps
+    if not args.eager and n_lat > 0:
+        l_lo = k_hi
+        graphs = []
+        for s in range(l_lo, l_lo + n_lat):
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr):
+                run_step(s)
+            graphs.append(gr)
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n_lat + 1)]
+        torch.cuda.synchronize()
+        evs[0].record()
+        for i, gr in enumerate(graphs):
+            gr.replay()
+            evs[i + 1].record()
+        torch.cuda.synchronize()
+        lat_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(n_lat)]
+        log(f"per-step latency of {n_lat} steps done")
+        del graphs
+        st = dms.dms_status(cache.ctx)
+        if st != 0:
+            raise RuntimeError(f"decode failed: {dms.dms_strerror(st)}")
+        for layer in range(nl):
+            dms.dms_retained_lengths(cache.ctx, layer, B, sid, lens)
+            if not torch.equal(lens.to(torch.int64), Lstep[l_lo + n_lat - 1, layer]):
+                raise RuntimeError(f"layer {layer}: retained lengths diverged from the closed form")
     traffic, traffic_profile = None, None
-    if args.workload == "qwen-r1-32b-8x" and not quest:
-        traffic_profile = TRAFFIC_PROFILE_FP8 if args.kv_format == "fp8" else TRAFFIC_PROFILE
+    if not quest and not mla and (args.workload, args.kv_format) in TRAFFIC_PROFILES:
+        traffic_profile = TRAFFIC_PROFILES[(args.workload, args.kv_format)]
         traffic = profiled_traffic(traffic_profile, ["dms_common.h", "dms_fp8.h", "dms_decode.hip"])
     elif mla:
         traffic_profile = TRAFFIC_PROFILE_MLA
@@ -918,6 +966,10 @@ def main():
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 1),
         "decode_tok_per_s": round(B / (step_ms * 1e-3), 1),
         "wall_ms_per_step": round(1e3 * wall / args.steps, 4),
+        "step_latency_ms": ({"steps": len(lat_ms), "how": "one HIP graph per step, HIP events between replays",
+                             "p10": round(float(np.percentile(lat_ms, 10)), 4),
+                             "p50": round(float(np.percentile(lat_ms, 50)), 4),
+                             "p90": round(float(np.percentile(lat_ms, 90)), 4)} if lat_ms else None),
         "roofline": {
             "bound": "hbm",
             "achieved": round(achieved, 1),
