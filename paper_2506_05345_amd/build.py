@@ -67,5 +67,56 @@ def build(verbose: bool = False, extra_flags=()) -> str:
     return LIB
 
 
+# Host-side sanitizers for the C-ABI layer (argument checks, layout, context):
+# AddressSanitizer and UndefinedBehaviorSanitizer instrument the host code of
+# dms_api.hip only (the device code and the kernel translation units are
+# built as usual); the library then needs the sanitizer runtime preloaded
+# (sanitizer_runtime()).
+SAN_BUILD = os.path.join(HERE, "_build_san")
+SAN_LIB = os.path.join(SAN_BUILD, "libdms_san.so")
+HOST_SAN = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-fno-sanitize-recover=all"]
+
+
+def sanitizer_runtime() -> str:
+    """The shared AddressSanitizer runtime of hipcc's clang (to preload)."""
+    import glob
+    root = os.path.dirname(os.path.dirname(os.path.realpath(hipcc())))
+    cands = sorted(glob.glob(os.path.join(root, "llvm", "lib", "clang", "*", "lib", "linux",
+                                          "libclang_rt.asan-x86_64.so")))
+    cands += sorted(glob.glob("/opt/rocm/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so"))
+    if not cands:
+        raise RuntimeError("libclang_rt.asan-x86_64.so not found")
+    return cands[0]
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    """libdms_san.so: dms_api.hip with host ASan/UBSan, linked with the other
+    objects of the regular build (built first if missing)."""
+    objs = [os.path.join(BUILD, s.replace(".hip", ".o")) for s in SOURCES if s != "dms_api.hip"]
+    if not all(os.path.exists(o) for o in objs):
+        build(verbose)
+    os.makedirs(SAN_BUILD, exist_ok=True)
+    cc = hipcc()
+    api = os.path.join(SAN_BUILD, "dms_api.o")
+    cmd = [cc, *COMMON, *GPU_FLAGS, *HOST_SAN, "-c", os.path.join(CSRC, "dms_api.hip"), "-o", api]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)
+    if r.returncode != 0:
+        raise RuntimeError("hipcc failed:\n" + r.stdout.decode(errors="replace"))
+    tmp = SAN_LIB + ".tmp"
+    cmd = [cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *HOST_SAN, "-shared-libasan", api, *objs,
+           "-o", tmp]
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)
+    if r.returncode != 0:
+        raise RuntimeError("link failed:\n" + r.stdout.decode(errors="replace"))
+    os.replace(tmp, SAN_LIB)
+    return SAN_LIB
+
+
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    if "--sanitize" in sys.argv:
+        print(build_sanitized(verbose="-v" in sys.argv))
+    else:
+        print(build(verbose="-v" in sys.argv))

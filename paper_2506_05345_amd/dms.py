@@ -179,6 +179,8 @@ def _args(where, *specs):
     types of all arguments are checked first, then that each is a contiguous
     GPU tensor with enough elements.  Integers (raw device addresses) and None
     pass through; the library checks null pointers itself."""
+    if all(x is None or isinstance(x, int) for x, *_ in specs):
+        return
     import torch
     kinds = {_BF16: torch.bfloat16, _U8: torch.uint8, _I32: torch.int32, _F32: torch.float32}
     live = []

@@ -9,6 +9,12 @@ if ROOT not in sys.path:
 
 
 def pytest_configure(config):
+    # DMS_TEST_LIBRARY: run the tests against another build of libdms (the
+    # host-sanitizer build of tests/test_abi_sanitized.py)
+    alt = os.environ.get("DMS_TEST_LIBRARY")
+    if alt:
+        from paper_2506_05345_amd import dms
+        dms.LIB_PATH = alt
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: long-running CPU test")
 
