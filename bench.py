@@ -56,10 +56,20 @@ WORKLOADS = {
                                 desc="DeepSeek-V2-Lite-shaped latent-attention (MLA) DMS decode, "
                                      "absorbed form, 8 prompts x 16 chains, context 32768, w=256, "
                                      "flags Bernoulli(7/8)"),
+    # the same rows shared by 128 query heads (DeepSeek-V2's attention shape)
+    "deepseek-v2-8x": dict(layers=60, batch=128, kv_heads=1, group=128, head_dim=576,
+                           context=32768, window=256, p_evict=7 / 8, seed=5, kv_format=2,
+                           desc="DeepSeek-V2-shaped latent-attention (MLA) DMS decode, absorbed "
+                                "form, 128 query heads, 8 prompts x 16 chains, context 32768, "
+                                "w=256, flags Bernoulli(7/8)"),
 }
 MLA = 2            # kv_format of latent-attention pools
 MLA_LATENT = 512   # output (value) dims of a latent-attention row
-TRAFFIC_PROFILE_MLA = "decode_mla_kernel_deepseek-v2-lite-8x.txt"
+TRAFFIC_PROFILES_MLA = {
+    "deepseek-v2-lite-8x": "decode_mla_kernel_deepseek-v2-lite-8x.txt",
+    "deepseek-v2-8x": "decode_mla_kernel_deepseek-v2-8x.txt",
+}
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
 def profiled_traffic(profile, sources):
@@ -97,6 +107,14 @@ def row_bytes(wl):
     D = wl["head_dim"]
     fmt = wl.get("kv_format", 0)
     return 2 * D + 8 if fmt == 1 else 2 * D if fmt == MLA else 2 * D * 2
+
+
+def attend_flops(wl):
+    """Matrix flops per retained token of one KV head in a decode step: each
+    query head of the group scores the key (2 d) and adds the weighted value
+    (2 d; the 512 latent dims of a latent row)."""
+    D, g = wl["head_dim"], wl["group"]
+    return g * (2 * D + 2 * (MLA_LATENT if wl.get("kv_format", 0) == MLA else D))
 
 
 def contexts(wl, rng_seed):
@@ -191,6 +209,16 @@ def build(wl, steps_total, chunk_tokens, dev):
     return cache, ctx, L0
 
 
+class _Cycled:
+    """Per-step inputs indexed [step, ...] over a smaller pool of steps."""
+
+    def __init__(self, pool):
+        self.pool, self.n = pool, pool.shape[0]
+
+    def __getitem__(self, idx):
+        return self.pool[(idx[0] % self.n, *idx[1:])]
+
+
 def step_inputs(wl, ctx, steps_total, dev):
     """Per (step, layer) decode inputs and the retained length of every head
     at every step (closed form from the flags)."""
@@ -202,7 +230,11 @@ def step_inputs(wl, ctx, steps_total, dev):
     nl, seed = wl["layers"], wl["seed"]
     gen = torch.Generator(device=dev)
     gen.manual_seed(seed * 7919 + 17)
-    q = torch.randn((steps_total, nl, B, H * g, D), generator=gen, device=dev, dtype=torch.bfloat16)
+    # queries: distinct for every step up to about 8 GB of them, then taken
+    # again in turn (their values change neither the rows read nor the work;
+    # 128-head latent queries are 1.1 GB per step)
+    nq = max(1, min(steps_total, int(8e9 // (nl * B * H * g * D * 2))))
+    q = _Cycled(torch.randn((nq, nl, B, H * g, D), generator=gen, device=dev, dtype=torch.bfloat16))
     k = torch.randn((steps_total, nl, B, H, D), generator=gen, device=dev, dtype=torch.bfloat16)
     v = (None if wl.get("kv_format", 0) == MLA
          else torch.randn((steps_total, nl, B, H, D), generator=gen, device=dev, dtype=torch.bfloat16))
@@ -935,9 +967,11 @@ def main():
     if not quest and not mla and (args.workload, args.kv_format) in TRAFFIC_PROFILES:
         traffic_profile = TRAFFIC_PROFILES[(args.workload, args.kv_format)]
         traffic = profiled_traffic(traffic_profile, ["dms_common.h", "dms_fp8.h", "dms_decode.hip"])
-    elif mla:
-        traffic_profile = TRAFFIC_PROFILE_MLA
+    elif mla and args.workload in TRAFFIC_PROFILES_MLA:
+        traffic_profile = TRAFFIC_PROFILES_MLA[args.workload]
         traffic = profiled_traffic(traffic_profile, ["dms_common.h", "dms_mla.hip"])
+    # the same launches' matrix work (the roofline's other axis)
+    launch_tflops = per_launch_bytes / row_bytes(wl) * attend_flops(wl) / (kern_avg_ms * 1e-3) / 1e12
     res = {
         "metric": "DMS decode attn: achieved KV HBM GB/s (% of peak) + decode tok/s at 8x",
         "value": round(value, 1),
@@ -983,6 +1017,9 @@ def main():
                              f"{args.steps} steps",
             "kernel_avg_us": round(1e3 * kern_avg_ms, 2),
             "bytes_per_launch": int(per_launch_bytes),
+            "flops_per_byte": round(attend_flops(wl) / row_bytes(wl), 1),
+            "mfma_tflops": round(launch_tflops, 1),
+            "mfma_frac": round(launch_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
         },
     }
     if quest:

@@ -83,7 +83,7 @@ typedef struct dms_config {
   int32_t num_layers;         /* >= 1; layers are independent caches */
   int32_t max_seqs;           /* sequence ids are 0 .. max_seqs-1 (<= 65536) */
   int32_t num_kv_heads;       /* Hkv >= 1 */
-  int32_t group_size;         /* g = Hq / Hkv, 1 .. 16 */
+  int32_t group_size;         /* g = Hq / Hkv, 1 .. 16 (1 .. 128 for DMS_KV_MLA) */
   int32_t head_dim;           /* d: 64 or 128 (576 for DMS_KV_MLA) */
   int32_t window;             /* w >= 1: eviction delay = sliding window */
   int32_t page_size;          /* P tokens per page: 32, 64, 128 or 256 */
@@ -145,7 +145,11 @@ enum { DMS_EVICT_DELAYED = 0, DMS_EVICT_IMMEDIATE = 1 };
  *     d = 576 shared by all query heads: the compressed latent (dims
  *     0 .. 511) then the decoupled rotary key (dims 512 .. 575).  The cache
  *     is one KV head (num_kv_heads = 1) whose group is every query head
- *     (group_size <= 16), and DMS evicts its rows by the same rule.  Decode
+ *     (group_size <= 128: DeepSeek-V2-Lite has 16, DeepSeek-V2 128; decode
+ *     attends groups of 16 query heads, each re-reading the rows, which
+ *     the groups of one call read close together in time so that the
+ *     re-reads mostly hit the L2), and DMS evicts its rows by the same
+ *     rule.  Decode
  *     works in the absorbed form: q (per query head, 576 dims) is the query
  *     already mapped into the latent space followed by its rotary part; a
  *     head scores row j by q . row_j over all 576 dims and its output is the

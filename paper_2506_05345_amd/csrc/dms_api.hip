@@ -16,7 +16,7 @@ namespace dms {
 int validate_config(const dms_config& c) {
   if (c.num_layers < 1 || c.max_seqs < 1 || c.max_seqs > kMaxSeqs) return DMS_ERR_INVALID;
   if (c.num_kv_heads < 1 || c.group_size < 1 || c.window < 1) return DMS_ERR_INVALID;
-  if (c.group_size > kMaxGroup) return DMS_ERR_UNSUPPORTED;
+  if (c.group_size > (c.kv_format == DMS_KV_MLA ? kMlaMaxGroup : kMaxGroup)) return DMS_ERR_UNSUPPORTED;
   if (c.head_dim < 1) return DMS_ERR_INVALID;
   if (c.kv_format == DMS_KV_MLA) {
     // latent rows: one KV head, caller decisions, no page retrieval
@@ -27,12 +27,14 @@ int validate_config(const dms_config& c) {
     return DMS_ERR_UNSUPPORTED;
   }
   // Split-K partial accumulators (one g x row-width float32 block per
-  // partial, kMaxWaves + max_seqs * Hkv partials) are addressed through a
-  // buffer resource with 32-bit byte offsets, so their area must stay below
-  // 2 GiB for every page format.
+  // partial, kMaxWaves + max_seqs * Hkv partials, kMaxMlaUnits + max_seqs for
+  // latent rows) are addressed through a buffer resource with 32-bit byte
+  // offsets, so their area must stay below 2 GiB for every page format.
   {
-    const int64_t row = c.kv_format == DMS_KV_MLA ? kMlaLatent : c.head_dim;
-    const int64_t partials = kMaxWaves + static_cast<int64_t>(c.max_seqs) * c.num_kv_heads;
+    const bool mla_rows = c.kv_format == DMS_KV_MLA;
+    const int64_t row = mla_rows ? kMlaLatent : c.head_dim;
+    const int64_t partials = (mla_rows ? kMaxMlaUnits : kMaxWaves) +
+                             static_cast<int64_t>(c.max_seqs) * c.num_kv_heads;
     if (partials * c.group_size * row * 4 >= (int64_t(1) << 31)) return DMS_ERR_UNSUPPORTED;
   }
   if (c.page_size != 32 && c.page_size != 64 && c.page_size != 128 && c.page_size != 256)
@@ -61,7 +63,10 @@ Layout make_layout(const dms_config& c) {
   const size_t maxp = c.max_pages_per_head, P = c.page_size, D = c.head_dim;
   lo.max_slots = static_cast<int>(maxp * P);
   lo.max_heads = static_cast<int>(S * H);
-  lo.max_partials = kMaxWaves + lo.max_heads;
+  const bool mla_rows = c.kv_format == DMS_KV_MLA;
+  lo.max_partials = (mla_rows ? kMaxMlaUnits : kMaxWaves) + lo.max_heads;
+  lo.ml_stride = mla_rows ? (c.group_size + kMaxGroup - 1) / kMaxGroup * kMaxGroup : kMaxGroup;
+  lo.head_groups = mla_rows ? (c.group_size + kMaxGroup - 1) / kMaxGroup : 1;
   // meta
   lo.status = 0;
   lo.layer0 = kAlign;
@@ -87,13 +92,13 @@ Layout make_layout(const dms_config& c) {
   const size_t NH = lo.max_heads, NP = lo.max_partials;
   lo.ws_head_desc = take(NH * sizeof(HeadDesc));
   lo.ws_cum_tiles = take((NH + 1) * 4);
-  lo.ws_part_ml = take(NP * kMaxGroup * 8);
+  lo.ws_part_ml = take(NP * lo.ml_stride * 8);
   const size_t Dout = c.kv_format == DMS_KV_MLA ? kMlaLatent : D;   // output row width
   lo.ws_part_acc = take(NP * c.group_size * Dout * 4);
   lo.ws_wave_bounds = take((kMaxWaves + 1) * 4);
   lo.ws_wave_desc = take(kMaxWaves * 2 * sizeof(int4));   // per decode wave: first segment
   lo.ws_head_waves = take(NH * sizeof(int4));              // per head: waves holding its tiles
-  lo.ws_head_cnt = take(NH * 4);
+  lo.ws_head_cnt = take(NH * lo.head_groups * 4);
   lo.ws_plan_ctr = take(16);
   lo.ws_ck_need = take(NH * 4);
   lo.ws_ck_fresh = take(NH * 4);
@@ -229,12 +234,15 @@ size_t static_layout(const dms_config& c, int n, int waves, dms::Layout* lo) {
   const size_t NH = static_cast<size_t>(n) * c.num_kv_heads, W = static_cast<size_t>(waves);
   lo->ws_head_desc = take(NH * sizeof(dms::HeadDesc));
   lo->ws_cum_tiles = take((NH + 1) * 4);
-  lo->ws_part_ml = take((W + NH) * dms::kMaxGroup * 8);
+  // (the entry point takes standard-row formats only: one head group)
+  lo->ml_stride = dms::kMaxGroup;
+  lo->head_groups = 1;
+  lo->ws_part_ml = take((W + NH) * lo->ml_stride * 8);
   lo->ws_part_acc = take((W + NH) * c.group_size * c.head_dim * 4);
   lo->ws_wave_bounds = take((W + 1) * 4);
   lo->ws_wave_desc = take(W * 2 * sizeof(int4));
   lo->ws_head_waves = take(NH * sizeof(int4));
-  lo->ws_head_cnt = take(NH * 4);
+  lo->ws_head_cnt = take(NH * lo->head_groups * 4);
   lo->max_partials = static_cast<int>(W + NH);   // partial index = wave + call head
   return off;
 }

@@ -772,7 +772,7 @@ hipError_t launch_init_state(const dms_config& c, const Layout& lo, void* meta, 
   a.ck_err = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_ck_err);
   a.head_cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_head_cnt);
   a.plan_ctr = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + lo.ws_plan_ctr);
-  a.n_heads = lo.max_heads;
+  a.n_heads = static_cast<int64_t>(lo.max_heads) * lo.head_groups;
   a.layer0 = lo.layer0;
   a.layer_stride = lo.layer_stride;
   a.pos = lo.pos;

@@ -15,6 +15,8 @@ constexpr int kMaxWaves = 8192;      // upper bound on decode waves (workspace s
 constexpr int kMaxGroup = 16;        // query heads per KV head (MFMA column count)
 constexpr int kMlaDim = 576;         // latent attention row: 512 latent + 64 rotary key dims
 constexpr int kMlaLatent = 512;      // of which the latent (the values)
+constexpr int kMlaMaxGroup = 128;    // query heads sharing one latent row (groups of kMaxGroup)
+constexpr int kMaxMlaUnits = 1024;   // upper bound on latent-attention work units (workspace sizing)
 constexpr int kMaxSeqs = 65536;      // sequence-id bitmap of the planning kernel
 constexpr uint32_t kFlagBit = 0x80000000u;
 constexpr int kAlign = 256;
@@ -41,6 +43,8 @@ struct Layout {
   int pf_tiles_per_head;   // tiles of one (region, KV head) in ws_pf_tiles
   size_t workspace_bytes;
   int max_heads, max_partials, max_slots;
+  int ml_stride;     // (max, sum) pairs per split-K partial: kMaxGroup, or the latent group rounded up
+  int head_groups;   // arrival counters per call head: query-head groups of kMaxGroup (latent rows)
 };
 
 // Host-side validation; returns DMS_OK or an error code.

@@ -12,8 +12,12 @@
 // a row by q . row over all 576 dims and its output is the softmax-weighted
 // sum of the rows' first 512 dims (the latent; W_UV is applied by the caller).
 //
-// Work split: the planner's units are blocks (one per CU), each taking an
-// equal contiguous share of the call's tiles; a block deals each segment's
+// Work split: the planner's units are tile ranges (one per CU), each taking
+// an equal contiguous share of the call's tiles.  A query group wider than 16
+// heads (DeepSeek-V2: 128) is attended as groups of 16, one block per (unit,
+// head group): every group's block reads the unit's tiles, and the blocks of
+// one unit are dispatched to the same XCD close together so that the later
+// readers mostly hit that XCD's L2.  A block deals each segment's
 // tiles (the part of one head in its share) to its four waves in turn, and at
 // the segment's end the four fold their partials through LDS -- into the
 // head's output when the block covered the whole head, else into one partial
@@ -99,8 +103,17 @@ struct MlaParams {
   size_t page_bytes;
   int part_acc_bytes;   // size of the partial accumulator area (< 2 GiB)
   int g, maxp, log2P;
+  int W;                // the planner's units (tile ranges)
+  int ngroups;          // query-head groups of kMaxGroup (one workgroup per unit and group)
+  int ml_stride;        // (max, sum) pairs per partial
   float scale_log2;
 };
+
+// Workgroups per dispatch batch: a multiple of the eight XCDs, so that the
+// workgroups of every head group of one unit share an XCD (workgroup i runs
+// on XCD i % 8) and read that unit's tiles close together in time -- the
+// later groups' reads then mostly hit that XCD's L2.
+constexpr int kUnitBatch = 32;
 
 // Latent piece s of this lane's row (dims 32s + 8G .. +7 of slot `slot`)
 // into the wave's [dim][slot] LDS area; a slot at or past the valid rows is
@@ -202,7 +215,14 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
   __shared__ int s_last;
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int unit = blockIdx.x;   // the planner's unit: this block's tile range
+  // the planner's unit (this block's tile range) and the group of kMaxGroup
+  // query heads this block attends for
+  const int per = kUnitBatch * a.ngroups;
+  const int unit = static_cast<int>(blockIdx.x) / per * kUnitBatch + static_cast<int>(blockIdx.x) % kUnitBatch;
+  const int grp = static_cast<int>(blockIdx.x) % per / kUnitBatch;
+  if (unit >= a.W) return;
+  const int h0 = grp * kMaxGroup;                    // first query head of the group
+  const int gq = min(kMaxGroup, a.g - h0);           // query heads in the group
   const int r = lane & 15, G = lane >> 4;
   char* vt = vt_lds[wid];
   const int4 wd0 = ldc(wave_desc, 2 * unit), wd1 = ldc(wave_desc, 2 * unit + 1);
@@ -215,7 +235,7 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
   constexpr size_t kTileBytes = static_cast<size_t>(kD) * 64;
   int hh = wd0.z;
   bool first = true;
-  const int qr = min(r, a.g - 1);
+  const int qr = min(r, gq - 1);
   const __amdgpu_buffer_rsrc_t acc_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       part_acc, static_cast<short>(0), a.part_acc_bytes, kBufferDword3);
   while (tb < te) {
@@ -252,14 +272,16 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
     if (t_first < t_hi) {
       // query fragments (B operand of the score MFMA): column r = query head r
       u32x4 qf[kKBlocks];
-      const char* qrow = reinterpret_cast<const char*>(q + (static_cast<size_t>(hh) * a.g + qr) * kD);
+      const char* qrow = reinterpret_cast<const char*>(q + (static_cast<size_t>(hh) * a.g + h0 + qr) * kD);
 #pragma unroll
       for (int s = 0; s < kKBlocks; ++s) {
         const u32x4 x = *reinterpret_cast<const u32x4*>(qrow + (32 * s + 8 * G) * 2);
-        qf[s] = r < a.g ? x : u32x4{0u, 0u, 0u, 0u};
+        qf[s] = r < gq ? x : u32x4{0u, 0u, 0u, 0u};
       }
       // the token appended by this call (slot d.z) is written into its tile
-      // by the wave that reads that tile, before its loads
+      // by the wave that reads that tile, before its loads (by that wave of
+      // every head group's block: the same bytes, each block's own store
+      // ordered before its own loads)
       const int tz = d.z >> 5;
       if (k_in != nullptr && tz >= t_first && tz < t_hi && ((tz - t_first) & 3) == 0) {
         char* tile = const_cast<char*>(tile_of(tz));
@@ -365,10 +387,10 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
       for (int j = 0; j < kWavesPerBlock; ++j)
         num[i] += wj[j] * *reinterpret_cast<const f32x4*>(vt_lds[j] + (b * 64 + lane) * 16);
     }
-    if (r < a.g) {
+    if (r < gq) {
       if (tb == c0 && seg_end == c1) {
         const float inv = 1.0f / den;
-        float* o = out + (static_cast<size_t>(hh) * a.g + r) * kDv + 4 * G;
+        float* o = out + (static_cast<size_t>(hh) * a.g + h0 + r) * kDv + 4 * G;
 #pragma unroll
         for (int i = 0; i < kBlocksPerWave; ++i)
           *reinterpret_cast<f32x4*>(o + 16 * (wid * kBlocksPerWave + i)) = num[i] * inv;
@@ -377,11 +399,11 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
         // coherence point once this wave's vmcnt drains
         const size_t pid = static_cast<size_t>(unit) + hh;
         if (wid == 0 && G == 0) {
-          float* ml = reinterpret_cast<float*>(part_ml + pid * kMaxGroup + r);
+          float* ml = reinterpret_cast<float*>(part_ml + pid * a.ml_stride + h0 + r);
           store_coherent(ml, M);
           store_coherent(ml + 1, den);
         }
-        const uint32_t o = static_cast<uint32_t>(((pid * a.g + r) * kDv + 4 * G) * 4);
+        const uint32_t o = static_cast<uint32_t>(((pid * a.g + h0 + r) * kDv + 4 * G) * 4);
 #pragma unroll
         for (int i = 0; i < kBlocksPerWave; ++i)
           __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, num[i]), acc_rsrc,
@@ -396,7 +418,7 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
       __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
       __syncthreads();
       if (threadIdx.x == 0) {
-        const int prev = atomicAdd(&head_cnt[hh], seg_end - tb);
+        const int prev = atomicAdd(&head_cnt[hh * a.ngroups + grp], seg_end - tb);
         s_last = prev + (seg_end - tb) == c1 - c0;
       }
       __syncthreads();
@@ -417,10 +439,10 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
             const int u = u0 + j;
             lv[j] = u <= hw.y && ldc(wave_bounds, u) < ldc(wave_bounds, u + 1);
             const size_t pid = static_cast<size_t>(lv[j] ? u : hw.x) + hh;
-            const float* ml = reinterpret_cast<const float*>(part_ml + pid * kMaxGroup + r);
+            const float* ml = reinterpret_cast<const float*>(part_ml + pid * a.ml_stride + h0 + r);
             mv[j] = lv[j] ? load_coherent(ml) : -INFINITY;
             lv_l[j] = lv[j] ? load_coherent(ml + 1) : 0.f;
-            const uint32_t o = static_cast<uint32_t>(((pid * a.g + (r < a.g ? r : 0)) * kDv + 4 * G) * 4);
+            const uint32_t o = static_cast<uint32_t>(((pid * a.g + h0 + (r < gq ? r : 0)) * kDv + 4 * G) * 4);
 #pragma unroll
             for (int i = 0; i < kBlocksPerWave; ++i)
               x[j][i] = lv[j] ? __builtin_amdgcn_raw_buffer_load_b128(acc_rsrc, o + 64 * (wid * kBlocksPerWave + i), 0,
@@ -445,14 +467,15 @@ __global__ __launch_bounds__(256, 1) void decode_mla_kernel(
             for (int i = 0; i < kBlocksPerWave; ++i) nh[i] += wt * __builtin_bit_cast(f32x4, x[j][i]);
           }
         }
-        if (r < a.g) {
+        if (r < gq) {
           const float inv = 1.0f / dh;
-          float* o = out + (static_cast<size_t>(hh) * a.g + r) * kDv + 4 * G;
+          float* o = out + (static_cast<size_t>(hh) * a.g + h0 + r) * kDv + 4 * G;
 #pragma unroll
           for (int i = 0; i < kBlocksPerWave; ++i)
             *reinterpret_cast<f32x4*>(o + 16 * (wid * kBlocksPerWave + i)) = nh[i] * inv;
         }
-        if (threadIdx.x == 0) __hip_atomic_store(&head_cnt[hh], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (threadIdx.x == 0)
+          __hip_atomic_store(&head_cnt[hh * a.ngroups + grp], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
     __syncthreads();   // the staged partials are read before the next segment's tiles reuse the areas
@@ -475,9 +498,13 @@ hipError_t launch_decode_mla(const dms_config& c, const Layout& lo, void* meta, 
   a.g = c.group_size;
   a.maxp = c.max_pages_per_head;
   a.log2P = __builtin_ctz(static_cast<unsigned>(c.page_size));
+  a.W = waves;
+  a.ngroups = lo.head_groups;
+  a.ml_stride = lo.ml_stride;
   a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
+  const int blocks = (waves + kUnitBatch - 1) / kUnitBatch * kUnitBatch * a.ngroups;
   if (ev_start) (void)hipEventRecord(ev_start, st);
-  hipLaunchKernelGGL(decode_mla_kernel, dim3(waves), dim3(256), 0, st,
+  hipLaunchKernelGGL(decode_mla_kernel, dim3(blocks), dim3(256), 0, st,
                      reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status),
                      reinterpret_cast<const HeadDesc*>(w + lo.ws_head_desc),
                      reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles),
@@ -502,8 +529,8 @@ int decode_mla_resident_waves() {
       blocks < 1)
     return -1;
   // the planner's units are blocks (one per CU): each block's four waves
-  // share its tile range
-  return cus < kMaxWaves ? cus : kMaxWaves;
+  // share its tile range (one block per unit and query-head group)
+  return cus < kMaxMlaUnits ? cus : kMaxMlaUnits;
 }
 
 }  // namespace dms

@@ -68,24 +68,31 @@ def _cfg(**kw):
     (dict(max_seqs=32768, num_kv_heads=16, group_size=16, head_dim=64), dms.DMS_ERR_UNSUPPORTED),
     (dict(max_seqs=65536, num_kv_heads=1, group_size=16, head_dim=576, kv_format=2),
      dms.DMS_ERR_UNSUPPORTED),
+    (dict(max_seqs=8192, num_kv_heads=1, group_size=128, head_dim=576, kv_format=2),
+     dms.DMS_ERR_UNSUPPORTED),
 ])
 def test_bad_configuration(kw, code):
     rc = dms.lib().dms_layout(ctypes.byref(_cfg(**kw)), None, None, None, None)
     assert rc == code
 
 
-# Largest-partials configurations below the 2 GiB bound: (8192 + S * Hkv) * g * row * 4 bytes.
+# Largest-partials configurations below the 2 GiB bound: (U + S * Hkv) * g * row * 4
+# bytes, U = 8192 decode waves (1024 work units for latent rows).
 @pytest.mark.parametrize("kw", [
     dict(max_seqs=4096, num_kv_heads=8, group_size=16, head_dim=128),
     dict(max_seqs=65536, num_kv_heads=8, group_size=1, head_dim=128, kv_format=1),
     dict(max_seqs=8192, num_kv_heads=1, group_size=16, head_dim=576, kv_format=2),
+    dict(max_seqs=60000, num_kv_heads=1, group_size=16, head_dim=576, kv_format=2),
+    dict(max_seqs=4096, num_kv_heads=1, group_size=128, head_dim=576, kv_format=2),
 ])
 def test_partial_area_just_below_the_bound_is_accepted(kw):
     cfg = _cfg(**kw)
-    row = 512 if kw.get("kv_format") == 2 else kw["head_dim"]
-    assert (8192 + cfg.max_seqs * cfg.num_kv_heads) * cfg.group_size * row * 4 < 2 ** 31
+    latent = kw.get("kv_format") == 2
+    row, units = (512, 1024) if latent else (kw["head_dim"], 8192)
+    need = (units + cfg.max_seqs * cfg.num_kv_heads) * cfg.group_size * row * 4
+    assert need < 2 ** 31
     m, p, w, pg = dms.dms_layout(cfg)
-    assert w >= (8192 + cfg.max_seqs * cfg.num_kv_heads) * cfg.group_size * row * 4
+    assert w >= need
 
 
 def test_layout_sizes():
@@ -325,9 +332,18 @@ def test_latent_pages_layout_and_host_checks():
     # 576-dim rows only exist in latent pools
     rc = dms.lib().dms_layout(ctypes.byref(_cfg(head_dim=dms.MLA_ROW_DIM)), None, None, None, None)
     assert rc == dms.DMS_ERR_UNSUPPORTED
-    rc = dms.lib().dms_layout(ctypes.byref(_cfg(group_size=17, **{k: v for k, v in mla.items() if k != "group_size"})),
-                              None, None, None, None)
+    # up to 128 query heads share a latent row (DeepSeek-V2), in groups of 16
+    lat = {k: v for k, v in mla.items() if k != "group_size"}
+    for g in (17, 40, 128):
+        rc = dms.lib().dms_layout(ctypes.byref(_cfg(group_size=g, **lat)), None, None, None, None)
+        assert rc == dms.DMS_OK, g
+    rc = dms.lib().dms_layout(ctypes.byref(_cfg(group_size=129, **lat)), None, None, None, None)
     assert rc == dms.DMS_ERR_UNSUPPORTED
+    # the workspace grows with the group: partial rows, (max, sum) slots of
+    # the group rounded up to 16, one arrival counter per head group
+    ws16 = dms.dms_layout(_cfg(group_size=16, **lat))[2]
+    ws128 = dms.dms_layout(_cfg(group_size=128, **lat))[2]
+    assert ws128 > 7 * ws16
     # documented offsets (include/dms.h): the bf16 key formula, tiles of 64 d bytes
     P, D = 64, dms.MLA_ROW_DIM
     words = np.zeros(P * D, np.uint16)

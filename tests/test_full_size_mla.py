@@ -1,8 +1,9 @@
-"""Parity of latent-attention (MLA) decode at the benchmark's full size, one
+"""Parity of latent-attention (MLA) decode at the benchmark's full sizes, one
 layer, in the launch configuration the benchmark times: 128 sequences, one
-latent KV head of 576-dim rows shared by 16 query heads, 32768 context
-tokens appended in 4096-token chunks, w=256, flags Bernoulli(7/8), then
-decode steps.
+latent KV head of 576-dim rows shared by 16 query heads (DeepSeek-V2-Lite)
+or 128 (DeepSeek-V2: eight head groups of 16), 32768 context tokens
+appended in 4096-token chunks, w=256, flags Bernoulli(7/8), then decode
+steps.
 
 Checked: the bookkeeping of every sequence bit-exactly against the oracle's
 replay, and, on sampled sequences, the stored rows at every live slot and the
@@ -20,7 +21,7 @@ from oracle import PagedKVOracle, mla_attention, visible
 pytestmark = pytest.mark.gpu
 
 SEED, LAYER = 4, 11
-B, G, ROW, LATENT, W, P, CTX, CHUNK, P_EVICT = 128, 16, 576, 512, 256, 64, 32768, 4096, 7 / 8
+B, ROW, LATENT, W, P, CTX, CHUNK, P_EVICT = 128, 576, 512, 256, 64, 32768, 4096, 7 / 8
 STEPS = 3
 SAMPLES = [0, 17, 64, 127, 90, 33]
 
@@ -30,7 +31,8 @@ def _rows_np(seq, positions):
     return sy.token_vectors_np(SEED, sy.STREAM_K, LAYER, seq, hh, np.asarray(positions)[:, None], dd)
 
 
-def test_full_size_latent_layer():
+@pytest.mark.parametrize("G", [16, 128], ids=["deepseek-v2-lite", "deepseek-v2"])
+def test_full_size_latent_layer(G):
     import torch
     from paper_2506_05345_amd import dms
 

@@ -117,7 +117,7 @@ def _compare_rows(cache, orc, seqs):
     return view
 
 
-@pytest.mark.parametrize("g", [16, 5, 1])
+@pytest.mark.parametrize("g", [128, 40, 16, 5, 1])
 def test_mla_ragged_chunks_then_decode(g):
     """Ragged histories (1 token .. a few thousand) appended in chunks, then
     decode steps that append one row each: state, rows and outputs."""
@@ -167,12 +167,14 @@ def test_mla_decode_without_append_and_separate_appends():
     cache.close()
 
 
-def test_mla_long_heads_split_over_many_waves():
+@pytest.mark.parametrize("g", [16, 128])
+def test_mla_long_heads_split_over_many_waves(g):
     """Two sequences of ~24K retained rows each (~750 tiles apiece over the
-    decode waves): every head is split over hundreds of waves and merged by
-    the wave that completes it.  Pools and workspace start as NaN bytes."""
+    decode units): every head is split over hundreds of units and merged, per
+    group of 16 query heads, by the block that completes it.  Pools and
+    workspace start as NaN bytes."""
     torch = _torch()
-    g, w, P, T = 16, 64, 64, 25000
+    w, P, T = 64, 64, 25000
     dms, cfg, cache, orc = _mk(2, g, w, P, num_pages=2 * (T // P + 8), maxp=T // P + 8)
     for p in cache.pools:
         p.fill_(0xFF)

@@ -52,7 +52,8 @@ def _absorbed(c, k_rope, w_uk, w_uv, q_nope, q_rope, mask, scale):
     return np.einsum("hvl,hl->hv", w_uv, lat)
 
 
-@pytest.mark.parametrize("T,H,w,p", [(1, 4, 4, 0.0), (40, 16, 8, 0.5), (300, 16, 16, 0.9)])
+@pytest.mark.parametrize("T,H,w,p", [(1, 4, 4, 0.0), (40, 16, 8, 0.5), (300, 16, 16, 0.9),
+                                     (200, 128, 32, 0.7)])
 def test_absorbed_form_equals_explicit_mla(T, H, w, p):
     c, k_rope, w_uk, w_uv, q_nope, q_rope = _mla_inputs(T * 7 + H, T, H)
     flags = (np.random.default_rng(T).random(T) < p).astype(np.uint8)
