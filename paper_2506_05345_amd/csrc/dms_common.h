@@ -262,7 +262,7 @@ hipError_t launch_decode_mla(const dms_config& c, const Layout& lo, void* meta, 
                              void* pool, int layer, int n, const void* q, const void* k,
                              float* out, int waves, hipStream_t st, hipEvent_t ev_start,
                              hipEvent_t ev_stop);
-int decode_mla_resident_waves();
+int decode_mla_resident_waves(const dms_config& c);
 hipError_t launch_retained(const dms_config& c, const Layout& lo, void* meta, int layer, int n,
                            const int32_t* seq_ids, int32_t* out, hipStream_t st);
 hipError_t launch_chunk_commit(const dms_config& c, const Layout& lo, void* meta, void* ws,

@@ -1242,7 +1242,7 @@ hipError_t launch_decode_step(const dms_config& c, const Layout& lo, void* meta,
 // heads to merge, same bandwidth); the launch must fit entirely, so the
 // occupancy of the kernel is checked.
 int decode_resident_waves(const dms_config& c) {
-  if (c.kv_format == DMS_KV_MLA) return decode_mla_resident_waves();
+  if (c.kv_format == DMS_KV_MLA) return decode_mla_resident_waves(c);
   int dev = 0, cus = 0, blocks = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -1;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
