@@ -345,11 +345,13 @@ int dms_append(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, const
   hipStream_t st = as_stream(stream);
   hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, flags_dev,
                                   nullptr, nullptr, true, 0, nullptr, st);
-  if (e == hipSuccess)
-    e = dms::launch_scatter(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, k_dev, v_dev, st);
-  if (e == hipSuccess && c.cfg.quest_page_budget > 0)
-    e = dms::launch_quest_bounds(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, false,
-                                 seq_ids_dev, st);
+  if (e == hipSuccess) {
+    // with page retrieval the written pages' bounds are recomputed in the
+    // same launch as the K / V writes
+    e = c.cfg.quest_page_budget > 0
+            ? dms::launch_quest_append(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, k_dev, v_dev, st)
+            : dms::launch_scatter(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, k_dev, v_dev, st);
+  }
   return hip_rc(e);
 }
 
@@ -386,18 +388,15 @@ int decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, cons
   const Ctx& c = ctx->c;
   hipStream_t st = as_stream(stream);
   if (c.cfg.quest_page_budget > 0) {
-    // page retrieval: append (plan, K / V write, bounds of the written
-    // pages), select pages, then plan and decode over the selection
+    // page retrieval: plan the append; write K / V, recompute the written
+    // pages' bounds and select every head's pages (one launch); then plan
+    // and decode over the selection
     hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev,
                                     from_q ? nullptr : flags_dev, from_q ? q_dev : nullptr,
                                     decisions_out_dev, true, 0, nullptr, st);
     if (e == hipSuccess)
-      e = dms::launch_scatter(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, k_dev, v_dev, st);
-    if (e == hipSuccess)
-      e = dms::launch_quest_bounds(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, false,
-                                   seq_ids_dev, st);
-    if (e == hipSuccess)
-      e = dms::launch_quest_select(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, q_dev, st);
+      e = dms::launch_quest_append_select(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, k_dev,
+                                          v_dev, st);
     if (e == hipSuccess)
       e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, nullptr, nullptr, nullptr,
                            false, c.decode_waves, out_dev, st, quest_lengths(c));

@@ -477,13 +477,6 @@ __global__ __launch_bounds__(64) void scatter_kernel(ScatterArgs a) {
   const int row = slot % a.P;
   const int j = row & 31;
   const int lane = threadIdx.x;
-  if (a.fp8) {
-    char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * fp8_tile_bytes(a.D);
-    if (lane < a.D / 8)
-      fp8_store_token(tile, j, a.D, lane, reinterpret_cast<const uint4*>(a.k + static_cast<size_t>(hh) * a.D)[lane],
-                      reinterpret_cast<const uint4*>(a.v + static_cast<size_t>(hh) * a.D)[lane]);
-    return;
-  }
   if (a.mla) {
     char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * mla_tile_bytes(a.D);
     for (int part = lane; part < a.D / 8; part += 64)
@@ -491,12 +484,9 @@ __global__ __launch_bounds__(64) void scatter_kernel(ScatterArgs a) {
           reinterpret_cast<const uint4*>(a.k + static_cast<size_t>(hh) * a.D)[part];
     return;
   }
-  char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes + (row >> 5) * tile_bytes(a.D);
-  if (lane < a.D / 8)
-    *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * lane)) =
-        reinterpret_cast<const uint4*>(a.k + static_cast<size_t>(hh) * a.D)[lane];
-  for (int e = lane; e < a.D; e += 64)
-    *reinterpret_cast<uint16_t*>(tile + v_elem_off(j, e, a.D)) = a.v[static_cast<size_t>(hh) * a.D + e];
+  char* tile = a.pool + static_cast<size_t>(page) * a.page_bytes +
+               (row >> 5) * (a.fp8 ? fp8_tile_bytes(a.D) : tile_bytes(a.D));
+  store_token_kv(tile, j, a.D, lane, a.fp8, a.k + static_cast<size_t>(hh) * a.D, a.v + static_cast<size_t>(hh) * a.D);
 }
 
 struct RetainedArgs {

@@ -227,6 +227,13 @@ hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* 
 // Page retrieval: recompute the bounds of the pages the last planned append
 // wrote (all_pages: every page of every head of the call), then select the
 // pages of each head for query q.
+// Quest: an append's K / V written and the written pages' bounds recomputed.
+hipError_t launch_quest_append(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                               void* pool, int layer, int n, const void* k, const void* v, hipStream_t st);
+// Quest, decode step: the append's K / V and bounds, then every head's selection.
+hipError_t launch_quest_append_select(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                                      void* pool, int layer, int n, const void* q, const void* k,
+                                      const void* v, hipStream_t st);
 hipError_t launch_quest_bounds(const dms_config& c, const Layout& lo, void* meta, void* ws,
                                void* pool, int layer, int n, bool all_pages, const int32_t* seq_ids,
                                hipStream_t st);

@@ -98,4 +98,19 @@ __device__ inline void fp8_store_token(char* tile, int j, int D, int i, uint4 k8
   }
 }
 
+// Write one token's K row and V column into slot j of its tile, bf16 or FP8
+// pages (`tile`: the 32-slot tile holding the slot).  Called by the 64 lanes
+// of one wave; lane i < D/8 holds dims 8 i .. 8 i + 7 of both rows.
+__device__ inline void store_token_kv(char* tile, int j, int D, int lane, bool fp8, const uint16_t* k,
+                                      const uint16_t* v) {
+  if (fp8) {
+    if (lane < D / 8)
+      fp8_store_token(tile, j, D, lane, reinterpret_cast<const uint4*>(k)[lane],
+                      reinterpret_cast<const uint4*>(v)[lane]);
+    return;
+  }
+  if (lane < D / 8) *reinterpret_cast<uint4*>(tile + k_elem_off(j, 8 * lane)) = reinterpret_cast<const uint4*>(k)[lane];
+  for (int e = lane; e < D; e += 64) *reinterpret_cast<uint16_t*>(tile + v_elem_off(j, e, D)) = v[e];
+}
+
 }  // namespace dms

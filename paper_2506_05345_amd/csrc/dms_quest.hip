@@ -6,9 +6,10 @@
 // the channel-wise min / max of the page's keys, and attends only the pages
 // with the largest bounds.  Here the unit is the cache's own page (P slots of
 // one KV head holding retained tokens of any positions):
-//   * quest_bounds_kernel recomputes lo / hi exactly over a page's live slots
-//     whenever an append writes into it (DMS reuses evicted tokens' slots, so
-//     bounds can shrink as well as grow);
+//   * quest_append_kernel writes an appended token's K / V into its slot and
+//     recomputes lo / hi exactly over that page's live slots (DMS reuses
+//     evicted tokens' slots, so bounds can shrink as well as grow);
+//     quest_bounds_kernel does the same for every page after a chunk commit;
 //   * quest_select_kernel scores every page of a head for its query group
 //     (maximum of U over the group's heads, one wave per page, float32 sums
 //     in a fixed order),
@@ -27,6 +28,9 @@ typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
 constexpr int kQThreads = 256;
 constexpr int kMaxSortPages = 4096;   // max_pages_per_head limit with a budget
+// the select kernel's sort keys and page marks at that limit fit the LDS a
+// launch may request
+static_assert(kMaxSortPages * (8 + 4) <= 65536, "select LDS");
 
 struct QuestArgs {
   LayerState st;
@@ -35,11 +39,14 @@ struct QuestArgs {
   const int32_t* seq_ids;
   const char* pool;
   const uint16_t* q;        // [n, Hq, D] bf16
+  const uint16_t* k;        // [n, Hkv, D] bf16: appended keys (quest_append_kernel)
+  const uint16_t* v;        // [n, Hkv, D] bf16: appended values
   int32_t* sel;             // [NH][B] attended page-table indices, ascending
   int32_t* qpage;           // [NH][B] their physical pages (what decode reads)
   int32_t* qlen;            // [NH] live slots in the attended pages
   size_t page_bytes;
   int n, H, g, D, P, maxp, B, fp8, zero_neuron, all_pages;
+  int sort_pages;           // power of two >= maxp: sort keys in the select kernel's LDS
 };
 
 __device__ inline int load_status(const int32_t* status) {
@@ -80,19 +87,11 @@ __device__ inline void key_elems8(const QuestArgs& a, const char* page, int r, i
   }
 }
 
-// Grid (pages, heads of the call): page i of head hh -- the page the last
-// planned append wrote (all_pages = 0) or every page (all_pages = 1).
-// Thread t covers dims 8 (t % (D/8)) .. + 7 of rows t / (D/8), + rows_per_pass, ...
-__global__ __launch_bounds__(kQThreads) void quest_bounds_kernel(QuestArgs a) {
+// lo / hi of page `pg` over its first `valid` rows, written to the page's
+// bounds.  Thread t covers dims 8 (t % (D/8)) .. + 7 of rows t / (D/8),
+// + rows_per_pass, ...
+__device__ void page_bounds(const QuestArgs& a, int pg, int valid) {
   __shared__ float red[2][kQThreads][8];
-  if (load_status(a.status) != 0) return;
-  const int hh = blockIdx.y;
-  const int sh = a.seq_ids[hh / a.H] * a.H + hh % a.H;
-  const int L = a.st.len[sh];
-  const int i = a.all_pages ? static_cast<int>(blockIdx.x) : a.desc[hh].z / a.P;
-  if (i * a.P >= L) return;
-  const int valid = min(a.P, L - i * a.P);
-  const int pg = a.st.page_table[static_cast<size_t>(sh) * a.maxp + i];
   const char* page = a.pool + static_cast<size_t>(pg) * a.page_bytes;
   const int tid = threadIdx.x;
   const int per_row = a.D / 8, rows = kQThreads / per_row;
@@ -135,20 +134,66 @@ __global__ __launch_bounds__(kQThreads) void quest_bounds_kernel(QuestArgs a) {
   }
 }
 
+// Grid (pages, heads of the call): every page of head hh (after a chunk
+// commit), or the page the last planned append wrote (all_pages = 0).
+__global__ __launch_bounds__(kQThreads) void quest_bounds_kernel(QuestArgs a) {
+  if (load_status(a.status) != 0) return;
+  const int hh = blockIdx.y;
+  const int sh = a.seq_ids[hh / a.H] * a.H + hh % a.H;
+  const int L = a.st.len[sh];
+  const int i = a.all_pages ? static_cast<int>(blockIdx.x) : a.desc[hh].z / a.P;
+  if (i * a.P >= L) return;
+  page_bounds(a, a.st.page_table[static_cast<size_t>(sh) * a.maxp + i], min(a.P, L - i * a.P));
+}
+
+// One block per head of the call, after the append's plan: the token's K / V
+// into its slot (wave 0), then the bounds of that page over its live slots,
+// the new row read back after the barrier (its stores are complete and
+// visible to the block's other waves there).
+__device__ void select_head(const QuestArgs& a, int hh, int sh, int L, unsigned long long* keys, int* chosen);
+
+__device__ inline void append_head(const QuestArgs& a, int hh, const HeadDesc& d) {
+  const int i = d.z / a.P, row = d.z % a.P;
+  const int pg = a.st.page_table[static_cast<size_t>(d.y) * a.maxp + i];
+  if (threadIdx.x < 64) {
+    char* tile = const_cast<char*>(a.pool) + static_cast<size_t>(pg) * a.page_bytes +
+                 (row >> 5) * (a.fp8 ? fp8_tile_bytes(a.D) : tile_bytes(a.D));
+    store_token_kv(tile, row & 31, a.D, threadIdx.x, a.fp8, a.k + static_cast<size_t>(hh) * a.D,
+                   a.v + static_cast<size_t>(hh) * a.D);
+  }
+  __syncthreads();
+  page_bounds(a, pg, min(a.P, d.x - i * a.P));
+}
+
+__global__ __launch_bounds__(kQThreads) void quest_append_kernel(QuestArgs a) {
+  if (load_status(a.status) != 0) return;
+  const int hh = blockIdx.x;
+  append_head(a, hh, a.desc[hh]);   // desc: (L after the append, state index, slot)
+}
+
+// A decode step's append and page selection for one head per block: the
+// selection reads every page's bounds, the written page's from this block's
+// own stores (visible after the barrier).
+__global__ __launch_bounds__(kQThreads) void quest_append_select_kernel(QuestArgs a) {
+  extern __shared__ unsigned long long q_dyn[];
+  if (load_status(a.status) != 0) return;
+  const int hh = blockIdx.x;
+  const HeadDesc d = a.desc[hh];
+  append_head(a, hh, d);
+  __syncthreads();
+  select_head(a, hh, d.y, d.x, q_dyn, reinterpret_cast<int*>(q_dyn + a.sort_pages));
+}
+
 // Sortable bits of a float (larger float -> larger unsigned).
 __device__ inline uint32_t orderable(float x) {
   const uint32_t u = __float_as_uint(x);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// One block per head of the call.
-__global__ __launch_bounds__(kQThreads) void quest_select_kernel(QuestArgs a) {
-  __shared__ unsigned long long keys[kMaxSortPages];
+// Selection of call head hh by one block: keys (sort_pages of them) and
+// page marks (maxp) in the caller's LDS.
+__device__ void select_head(const QuestArgs& a, int hh, int sh, int L, unsigned long long* keys, int* chosen) {
   __shared__ int lds[17];
-  if (load_status(a.status) != 0) return;
-  const int hh = blockIdx.x;
-  const int sh = a.seq_ids[hh / a.H] * a.H + hh % a.H;
-  const int L = a.st.len[sh];
   const int npages = (L + a.P - 1) / a.P;
   const int tid = threadIdx.x;
   int32_t* sel = a.sel + static_cast<size_t>(hh) * a.B;
@@ -223,7 +268,6 @@ __global__ __launch_bounds__(kQThreads) void quest_select_kernel(QuestArgs a) {
     }
   }
   __syncthreads();
-  __shared__ int chosen[kMaxSortPages];
   if (npages <= kQThreads) {
     // rank of each page among all of them (keys are distinct)
     if (tid < npages) {
@@ -273,6 +317,17 @@ __global__ __launch_bounds__(kQThreads) void quest_select_kernel(QuestArgs a) {
   if (tid == 0) a.qlen[hh] = a.B * a.P - (chosen[npages - 1] ? npages * a.P - L : 0);
 }
 
+// One block per head of the call.
+__global__ __launch_bounds__(kQThreads) void quest_select_kernel(QuestArgs a) {
+  // sort keys then page marks, sized at launch so that small page tables
+  // leave room for many blocks per CU
+  extern __shared__ unsigned long long q_dyn[];
+  if (load_status(a.status) != 0) return;
+  const int hh = blockIdx.x;
+  const int sh = a.seq_ids[hh / a.H] * a.H + hh % a.H;
+  select_head(a, hh, sh, a.st.len[sh], q_dyn, reinterpret_cast<int*>(q_dyn + a.sort_pages));
+}
+
 // Selection of the last decode call -> caller buffers (one thread per head).
 __global__ __launch_bounds__(kQThreads) void quest_export_kernel(const int32_t* sel, int NH, int B,
                                                                  int32_t* pages, int32_t* counts) {
@@ -306,6 +361,8 @@ QuestArgs quest_args(const dms_config& c, const Layout& lo, void* meta, void* ws
   a.B = c.quest_page_budget;
   a.fp8 = c.kv_format == DMS_KV_FP8;
   a.zero_neuron = c.decision_source == DMS_DECIDE_QUERY;
+  a.sort_pages = 1;
+  while (a.sort_pages < c.max_pages_per_head) a.sort_pages <<= 1;
   return a;
 }
 
@@ -320,6 +377,29 @@ hipError_t launch_quest_bounds(const dms_config& c, const Layout& lo, void* meta
   a.all_pages = all_pages;
   const dim3 grid(all_pages ? c.max_pages_per_head : 1, n * c.num_kv_heads);
   hipLaunchKernelGGL(quest_bounds_kernel, grid, dim3(kQThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_quest_append(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                               void* pool, int layer, int n, const void* k, const void* v, hipStream_t st) {
+  QuestArgs a = quest_args(c, lo, meta, ws, layer, n);
+  a.pool = static_cast<const char*>(pool);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  hipLaunchKernelGGL(quest_append_kernel, dim3(n * c.num_kv_heads), dim3(kQThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_quest_append_select(const dms_config& c, const Layout& lo, void* meta, void* ws,
+                                      void* pool, int layer, int n, const void* q, const void* k,
+                                      const void* v, hipStream_t st) {
+  QuestArgs a = quest_args(c, lo, meta, ws, layer, n);
+  a.pool = static_cast<const char*>(pool);
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  const size_t lds = static_cast<size_t>(a.sort_pages) * 8 + static_cast<size_t>(c.max_pages_per_head) * 4;
+  hipLaunchKernelGGL(quest_append_select_kernel, dim3(n * c.num_kv_heads), dim3(kQThreads), lds, st, a);
   return hipGetLastError();
 }
 
@@ -338,7 +418,8 @@ hipError_t launch_quest_select(const dms_config& c, const Layout& lo, void* meta
   QuestArgs a = quest_args(c, lo, meta, ws, layer, n);
   a.seq_ids = seq_ids;
   a.q = static_cast<const uint16_t*>(q);
-  hipLaunchKernelGGL(quest_select_kernel, dim3(n * c.num_kv_heads), dim3(kQThreads), 0, st, a);
+  const size_t lds = static_cast<size_t>(a.sort_pages) * 8 + static_cast<size_t>(c.max_pages_per_head) * 4;
+  hipLaunchKernelGGL(quest_select_kernel, dim3(n * c.num_kv_heads), dim3(kQThreads), lds, st, a);
   return hipGetLastError();
 }
 
