@@ -660,6 +660,138 @@ struct LdsPlan {
   }
 };
 
+// Tiles [t_lo, t_hi) of call head hh (descriptor d; `head_end`: the range
+// ends with the head's last tile) streamed into acc: query fragments, the
+// appended token written into its tile by the wave whose range covers it
+// (before the range's loads: same-wave stores and loads to one address stay
+// in order), then the tiles, two register sets in flight.
+template <int D, bool FP8>
+__device__ __forceinline__ void stream_segment(
+  Acc<D>& acc, int hh, const HeadDesc& d, int t_lo, int t_hi, bool head_end,
+  const int32_t* __restrict__ page_table, const int32_t* __restrict__ qpage, char* __restrict__ pool,
+  const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_in, const uint16_t* __restrict__ v_in,
+  const DecodeParams& a) {
+  const int lane = threadIdx.x & 63;
+  const int r = lane & 15, G = lane >> 4;
+  const int tiles_per_page_log2 = a.log2P - 5;
+  const int L = d.x;
+  const int32_t* pt = page_table + static_cast<size_t>(d.y) * a.maxp;
+  // page retrieval: the head's tiles run over the physical pages of its
+  // selection only
+  const int32_t* pages = qpage != nullptr ? qpage + static_cast<size_t>(hh) * a.qB : pt;
+  // query fragments (B operand): column r = query head r of the group
+  u32x4 qf[D / 32];
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  const char* qrow = reinterpret_cast<const char*>(q + (static_cast<size_t>(hh) * a.g + r) * D);
+#pragma unroll
+  for (int s = 0; s < D / 32; ++s) qf[s] = r < a.g ? ldg16(qrow + (32 * s + 8 * G) * 2) : z;
+  // the borrowed decision neuron takes no part in attention (App. C)
+  if (a.zero_neuron && r == 0 && G == 0) qf[0][0] &= 0xFFFF0000u;
+#pragma unroll
+  for (int b = 0; b < D / 16; ++b) acc.o[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  acc.m = -INFINITY;
+  acc.l = 0.f;
+  const int full_hi = (head_end && (L & (kTile - 1))) ? t_hi - 1 : t_hi;
+  // tile t of the head: page from a scalar load (the whole wave works on
+  // one head), then the tile's 16 KB block inside the page
+  constexpr size_t kTileBytes = FP8 ? static_cast<size_t>(D) * 64 + 256 : static_cast<size_t>(D) * 128;
+  // a page this call popped (fused launch) is taken from the plan: its
+  // page-table entry may not be written yet
+  const int new_pi = d.w >= 0 ? (d.z >> 5) >> tiles_per_page_log2 : -1;
+  auto tile_in = [&](const int32_t* pl, int t) -> char* {
+    const int pi = t >> tiles_per_page_log2;
+    const int pg = pi == new_pi ? d.w : ldc(pl, pi);
+    return pool + static_cast<size_t>(pg) * a.page_bytes +
+           static_cast<size_t>(t & ((1 << tiles_per_page_log2) - 1)) * kTileBytes;
+  };
+  auto tile_of = [&](int t) -> char* { return tile_in(pages, t); };
+  // The token appended by this call (slot d.z) is written into its tile by
+  // the one wave whose segment covers that tile, before the segment's
+  // loads: same-wave stores and loads to one address stay in order.
+  if (k_in != nullptr && d.z >= t_lo * kTile && d.z < t_hi * kTile) {
+    char* tile = tile_in(pt, d.z >> 5);
+    const int j = d.z & 31;
+    if constexpr (FP8) {
+      if (lane < D / 8)
+        fp8_store_token(tile, j, D, lane, reinterpret_cast<const uint4*>(k_in + static_cast<size_t>(hh) * D)[lane],
+                        reinterpret_cast<const uint4*>(v_in + static_cast<size_t>(hh) * D)[lane]);
+    } else {
+      if (lane < D / 8)
+        *reinterpret_cast<u32x4*>(tile + k_elem_off(j, 8 * lane)) =
+            reinterpret_cast<const u32x4*>(k_in + static_cast<size_t>(hh) * D)[lane];
+#pragma unroll
+      for (int e = lane; e < D; e += 64)
+        *reinterpret_cast<uint16_t*>(tile + v_elem_off(j, e, D)) = v_in[static_cast<size_t>(hh) * D + e];
+    }
+  }
+  if constexpr (FP8) {
+    if (t_lo < full_hi) {
+      // two register sets, as for bf16 (a third set, keeping two FP8 tiles
+      // in flight, measured slower)
+      FragF8<D> fa, fb;
+      // the next tile's address is formed a tile ahead and a scheduling
+      // barrier keeps its loads ahead of this tile's waits (1.5% faster
+      // than leaving the order to the compiler, which waited for part of
+      // the current tile first)
+      int t = t_lo;
+      const int last = full_hi - 1;
+      load_tile_f8<D>(fa, tile_of(t), lane, G);
+      __builtin_amdgcn_sched_barrier(0);
+      const char* pb = tile_of(min(t + 1, last));
+      for (; t + 2 < full_hi; t += 2) {
+        load_tile_f8<D>(fb, pb, lane, G);
+        __builtin_amdgcn_sched_barrier(0);
+        const char* pa = tile_of(t + 2);
+        compute_tile_f8<D>(acc, fa, qf, a.scale_log2, kTile, G);
+        load_tile_f8<D>(fa, pa, lane, G);
+        __builtin_amdgcn_sched_barrier(0);
+        pb = tile_of(min(t + 3, last));
+        compute_tile_f8<D>(acc, fb, qf, a.scale_log2, kTile, G);
+      }
+      if (t + 1 < full_hi) {
+        load_tile_f8<D>(fb, pb, lane, G);
+        __builtin_amdgcn_sched_barrier(0);
+        compute_tile_f8<D>(acc, fa, qf, a.scale_log2, kTile, G);
+        compute_tile_f8<D>(acc, fb, qf, a.scale_log2, kTile, G);
+      } else {
+        compute_tile_f8<D>(acc, fa, qf, a.scale_log2, kTile, G);
+      }
+    }
+    if (full_hi < t_hi) {
+      FragF8<D> ft;
+      load_tail_f8<D>(ft, tile_of(full_hi), lane, L - full_hi * kTile, r, G);
+      compute_tile_f8<D>(acc, ft, qf, a.scale_log2, L - full_hi * kTile, G);
+    }
+  } else {
+  if (t_lo < full_hi) {
+    // Two register sets; the next tile's loads are always in flight while
+    // the current one is computed (the prefetch is unconditional inside the
+    // loop so the compiler's wait counts only cover the older tile).
+    Frag<D> fa, fb;
+    int t = t_lo;
+    load_tile<D>(fa, tile_of(t), lane);
+    for (; t + 2 < full_hi; t += 2) {
+      load_tile<D>(fb, tile_of(t + 1), lane);
+      compute_tile<D>(acc, fa, qf, a.scale_log2, kTile, G);
+      load_tile<D>(fa, tile_of(t + 2), lane);
+      compute_tile<D>(acc, fb, qf, a.scale_log2, kTile, G);
+    }
+    if (t + 1 < full_hi) {
+      load_tile<D>(fb, tile_of(t + 1), lane);
+      compute_tile<D>(acc, fa, qf, a.scale_log2, kTile, G);
+      compute_tile<D>(acc, fb, qf, a.scale_log2, kTile, G);
+    } else {
+      compute_tile<D>(acc, fa, qf, a.scale_log2, kTile, G);
+    }
+  }
+  if (full_hi < t_hi) {
+    Frag<D> ft;
+    load_tail<D>(ft, tile_of(full_hi), lane, L - full_hi * kTile, r, G);
+    compute_tile<D>(acc, ft, qf, a.scale_log2, L - full_hi * kTile, G);
+  }
+  }
+}
+
 // One decode wave's work: stream its tile range (split-K over the retained
 // slots of the heads it covers), write whole heads' outputs, publish partials
 // of heads it shares, and merge the heads whose tile count it completes.
@@ -675,7 +807,6 @@ __device__ __forceinline__ void decode_wave(
   int tb, te, hh, c0, c1;
   HeadDesc d;
   if (!plan.first(wave, tb, te, hh, c0, c1, d)) return;
-  const int tiles_per_page_log2 = a.log2P - 5;
   bool first = true;
   // heads shared with other waves (at most the first and the last segment),
   // published at the end: head, tiles of this wave, tiles of the head
@@ -685,125 +816,9 @@ __device__ __forceinline__ void decode_wave(
     if (!first) plan.next(hh, tb, c0, c1, d);
     first = false;
     const int seg_end = min(te, c1);
-    const int L = d.x;
-    const int32_t* pt = page_table + static_cast<size_t>(d.y) * a.maxp;
-    // page retrieval: the head's tiles run over the physical pages of its
-    // selection only
-    const int32_t* pages = qpage != nullptr ? qpage + static_cast<size_t>(hh) * a.qB : pt;
-    // query fragments (B operand): column r = query head r of the group
-    u32x4 qf[D / 32];
-    const u32x4 z = {0u, 0u, 0u, 0u};
-    const char* qrow = reinterpret_cast<const char*>(q + (static_cast<size_t>(hh) * a.g + r) * D);
-#pragma unroll
-    for (int s = 0; s < D / 32; ++s) qf[s] = r < a.g ? ldg16(qrow + (32 * s + 8 * G) * 2) : z;
-    // the borrowed decision neuron takes no part in attention (App. C)
-    if (a.zero_neuron && r == 0 && G == 0) qf[0][0] &= 0xFFFF0000u;
     Acc<D> acc;
-#pragma unroll
-    for (int b = 0; b < D / 16; ++b) acc.o[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-    acc.m = -INFINITY;
-    acc.l = 0.f;
-    const int t_lo = tb - c0;
-    const int t_hi = seg_end - c0;
-    const int full_hi = (seg_end == c1 && (L & (kTile - 1))) ? t_hi - 1 : t_hi;
-    // tile t of the head: page from a scalar load (the whole wave works on
-    // one head), then the tile's 16 KB block inside the page
-    constexpr size_t kTileBytes = FP8 ? static_cast<size_t>(D) * 64 + 256 : static_cast<size_t>(D) * 128;
-    // a page this call popped (fused launch) is taken from the plan: its
-    // page-table entry may not be written yet
-    const int new_pi = d.w >= 0 ? (d.z >> 5) >> tiles_per_page_log2 : -1;
-    auto tile_in = [&](const int32_t* pl, int t) -> char* {
-      const int pi = t >> tiles_per_page_log2;
-      const int pg = pi == new_pi ? d.w : ldc(pl, pi);
-      return pool + static_cast<size_t>(pg) * a.page_bytes +
-             static_cast<size_t>(t & ((1 << tiles_per_page_log2) - 1)) * kTileBytes;
-    };
-    auto tile_of = [&](int t) -> char* { return tile_in(pages, t); };
-    // The token appended by this call (slot d.z) is written into its tile by
-    // the one wave whose segment covers that tile, before the segment's
-    // loads: same-wave stores and loads to one address stay in order.
-    if (k_in != nullptr && d.z >= t_lo * kTile && d.z < t_hi * kTile) {
-      char* tile = tile_in(pt, d.z >> 5);
-      const int j = d.z & 31;
-      if constexpr (FP8) {
-        if (lane < D / 8)
-          fp8_store_token(tile, j, D, lane, reinterpret_cast<const uint4*>(k_in + static_cast<size_t>(hh) * D)[lane],
-                          reinterpret_cast<const uint4*>(v_in + static_cast<size_t>(hh) * D)[lane]);
-      } else {
-        if (lane < D / 8)
-          *reinterpret_cast<u32x4*>(tile + k_elem_off(j, 8 * lane)) =
-              reinterpret_cast<const u32x4*>(k_in + static_cast<size_t>(hh) * D)[lane];
-#pragma unroll
-        for (int e = lane; e < D; e += 64)
-          *reinterpret_cast<uint16_t*>(tile + v_elem_off(j, e, D)) = v_in[static_cast<size_t>(hh) * D + e];
-      }
-    }
-    if constexpr (FP8) {
-      if (t_lo < full_hi) {
-        // two register sets, as for bf16 (a third set, keeping two FP8 tiles
-        // in flight, measured slower)
-        FragF8<D> fa, fb;
-        // the next tile's address is formed a tile ahead and a scheduling
-        // barrier keeps its loads ahead of this tile's waits (1.5% faster
-        // than leaving the order to the compiler, which waited for part of
-        // the current tile first)
-        int t = t_lo;
-        const int last = full_hi - 1;
-        load_tile_f8<D>(fa, tile_of(t), lane, G);
-        __builtin_amdgcn_sched_barrier(0);
-        const char* pb = tile_of(min(t + 1, last));
-        for (; t + 2 < full_hi; t += 2) {
-          load_tile_f8<D>(fb, pb, lane, G);
-          __builtin_amdgcn_sched_barrier(0);
-          const char* pa = tile_of(t + 2);
-          compute_tile_f8<D>(acc, fa, qf, a.scale_log2, kTile, G);
-          load_tile_f8<D>(fa, pa, lane, G);
-          __builtin_amdgcn_sched_barrier(0);
-          pb = tile_of(min(t + 3, last));
-          compute_tile_f8<D>(acc, fb, qf, a.scale_log2, kTile, G);
-        }
-        if (t + 1 < full_hi) {
-          load_tile_f8<D>(fb, pb, lane, G);
-          __builtin_amdgcn_sched_barrier(0);
-          compute_tile_f8<D>(acc, fa, qf, a.scale_log2, kTile, G);
-          compute_tile_f8<D>(acc, fb, qf, a.scale_log2, kTile, G);
-        } else {
-          compute_tile_f8<D>(acc, fa, qf, a.scale_log2, kTile, G);
-        }
-      }
-      if (full_hi < t_hi) {
-        FragF8<D> ft;
-        load_tail_f8<D>(ft, tile_of(full_hi), lane, L - full_hi * kTile, r, G);
-        compute_tile_f8<D>(acc, ft, qf, a.scale_log2, L - full_hi * kTile, G);
-      }
-    } else {
-    if (t_lo < full_hi) {
-      // Two register sets; the next tile's loads are always in flight while
-      // the current one is computed (the prefetch is unconditional inside the
-      // loop so the compiler's wait counts only cover the older tile).
-      Frag<D> fa, fb;
-      int t = t_lo;
-      load_tile<D>(fa, tile_of(t), lane);
-      for (; t + 2 < full_hi; t += 2) {
-        load_tile<D>(fb, tile_of(t + 1), lane);
-        compute_tile<D>(acc, fa, qf, a.scale_log2, kTile, G);
-        load_tile<D>(fa, tile_of(t + 2), lane);
-        compute_tile<D>(acc, fb, qf, a.scale_log2, kTile, G);
-      }
-      if (t + 1 < full_hi) {
-        load_tile<D>(fb, tile_of(t + 1), lane);
-        compute_tile<D>(acc, fa, qf, a.scale_log2, kTile, G);
-        compute_tile<D>(acc, fb, qf, a.scale_log2, kTile, G);
-      } else {
-        compute_tile<D>(acc, fa, qf, a.scale_log2, kTile, G);
-      }
-    }
-    if (full_hi < t_hi) {
-      Frag<D> ft;
-      load_tail<D>(ft, tile_of(full_hi), lane, L - full_hi * kTile, r, G);
-      compute_tile<D>(acc, ft, qf, a.scale_log2, L - full_hi * kTile, G);
-    }
-    }
+    stream_segment<D, FP8>(acc, hh, d, tb - c0, seg_end - c0, seg_end == c1, page_table, qpage, pool, q, k_in,
+                           v_in, a);
     float l = acc.l;
     l += __shfl_xor(l, 16, 64);
     l += __shfl_xor(l, 32, 64);
@@ -1066,6 +1081,72 @@ __device__ __forceinline__ void write_state(const FusedArgs& f, const int4* s_de
   }
 }
 
+// Calls whose every head has at most kHeadBlockTiles tiles run one workgroup
+// per head: its four waves take contiguous quarters of the head's tiles and
+// fold their results through LDS, so no split-K partial goes through memory
+// and no arrival counter is taken.  Measured at a 1.5B-shaped step (64 heads
+// of ~40 tiles spread over ~320 waves) the global merges -- partial stores,
+// the arrival atomic, then the merging wave's coherent loads -- held the
+// launch for up to 18 us of its 36.
+constexpr int kHeadBlockTiles = 64;
+
+template <int D, bool FP8>
+__device__ __forceinline__ void decode_head_block(const LdsPlan& plan, int hh, const int32_t* __restrict__ page_table,
+                                                  char* __restrict__ pool, const uint16_t* __restrict__ q,
+                                                  const uint16_t* __restrict__ k_in, const uint16_t* __restrict__ v_in,
+                                                  float* __restrict__ out, const DecodeParams& a,
+                                                  f32x4 (*fold)[D / 16][64], float2 (*fold_ml)[kMaxGroup]) {
+  const int lane = threadIdx.x & 63;
+  const int r = lane & 15, G = lane >> 4;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int c0 = plan.cum_at(hh), c1 = plan.cum_at(hh + 1);
+  const int n = c1 - c0;
+  const HeadDesc d = plan.head(hh);
+  const int t_lo = wid * n / kWavesPerBlock, t_hi = (wid + 1) * n / kWavesPerBlock;
+  Acc<D> acc;
+  if (t_lo < t_hi) {
+    stream_segment<D, FP8>(acc, hh, d, t_lo, t_hi, t_hi == n, page_table, nullptr, pool, q, k_in, v_in, a);
+  } else {
+#pragma unroll
+    for (int b = 0; b < D / 16; ++b) acc.o[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    acc.m = -INFINITY;
+    acc.l = 0.f;
+  }
+  float l = acc.l;
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+#pragma unroll
+  for (int b = 0; b < D / 16; ++b) fold[wid][b][lane] = acc.o[b];
+  if (G == 0) fold_ml[wid][r] = make_float2(acc.m, l);
+  __syncthreads();
+  // wave wid folds row blocks wid * D/64 .. of the four waves' results
+  float mj[kWavesPerBlock], M = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < kWavesPerBlock; ++j) {
+    mj[j] = fold_ml[j][r].x;
+    M = fmaxf(M, mj[j]);
+  }
+  float den = 0.f, wj[kWavesPerBlock];
+#pragma unroll
+  for (int j = 0; j < kWavesPerBlock; ++j) {
+    wj[j] = __builtin_amdgcn_exp2f(mj[j] - M);   // 0 for a wave without tiles (m = -inf)
+    den += wj[j] * fold_ml[j][r].y;
+  }
+  constexpr int kBlocks = D / 16 / kWavesPerBlock;
+  if (r < a.g) {
+    const float inv = 1.0f / den;
+    float* o = out + (static_cast<size_t>(hh) * a.g + r) * D + 4 * G;
+#pragma unroll
+    for (int i = 0; i < kBlocks; ++i) {
+      const int b = wid * kBlocks + i;
+      f32x4 num = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < kWavesPerBlock; ++j) num += wj[j] * fold[j][b][lane];
+      *reinterpret_cast<f32x4*>(o + 16 * b) = num * inv;
+    }
+  }
+}
+
 // Decode waves of a fused launch: at least kFuseMinTiles tiles per wave and at
 // least one wave per workgroup (so every compute unit streams), at most all
 // resident waves.  Fewer, longer waves split small calls into fewer parts.
@@ -1088,17 +1169,29 @@ __global__ __launch_bounds__(256, 1) void decode_step_kernel(
   __shared__ uint32_t s_seen[kMaxSeqs / 32];
   __shared__ int32_t s_stack[kFuseMaxHeads];
   __shared__ int s_scan[34];
+  __shared__ f32x4 s_fold[kWavesPerBlock][D / 16][64];
+  __shared__ float2 s_fold_ml[kWavesPerBlock][kMaxGroup];
   int total = 0, ticket = 0, new_top = 0;
   if (!fused_plan(f, s_cum, s_desc, s_aux, s_seen, s_stack, s_scan, &total, &ticket, &new_top)) return;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nb = gridDim.x;
   const int T = __builtin_amdgcn_readfirstlane(total);
-  const int W = min(a.W, max(nb, (T + kFuseMinTiles - 1) / kFuseMinTiles));
-  const int lw = W == a.W ? blockIdx.x * kWavesPerBlock + wid : wid * nb + blockIdx.x;
-  const LdsPlan plan{s_cum, s_desc, T, W, a.NH};
-  if (lw < W)
-    decode_wave<D, FP8>(plan, lw, W, head_cnt, f.st.page_table, nullptr, pool, q, k_in, v_in,
-                        part_ml, part_acc, out, a, merge_wts[wid]);
+  // every workgroup takes the same decision from the same plan
+  int wide = 0;
+  for (int hh = threadIdx.x; hh < a.NH; hh += blockDim.x) wide |= s_cum[hh + 1] - s_cum[hh] > kHeadBlockTiles;
+  wide = __syncthreads_or(wide);
+  if (!wide && a.NH <= nb) {
+    if (static_cast<int>(blockIdx.x) < a.NH)
+      decode_head_block<D, FP8>(LdsPlan{s_cum, s_desc, T, 1, a.NH}, blockIdx.x, f.st.page_table, pool, q, k_in,
+                                v_in, out, a, s_fold, s_fold_ml);
+  } else {
+    const int W = min(a.W, max(nb, (T + kFuseMinTiles - 1) / kFuseMinTiles));
+    const int lw = W == a.W ? blockIdx.x * kWavesPerBlock + wid : wid * nb + blockIdx.x;
+    const LdsPlan plan{s_cum, s_desc, T, W, a.NH};
+    if (lw < W)
+      decode_wave<D, FP8>(plan, lw, W, head_cnt, f.st.page_table, nullptr, pool, q, k_in, v_in,
+                          part_ml, part_acc, out, a, merge_wts[wid]);
+  }
   // the workgroup whose count completed the launch's writes the new state
   if (wid == 0 && __shfl(ticket, 0, 64) == nb - 1) write_state(f, s_desc, s_aux, new_top, threadIdx.x & 63);
 }
