@@ -41,6 +41,15 @@ typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
 constexpr int kThreads = 256;
+// Attention pass workgroup: eight waves for FP8 pages at d = 128 (one
+// workgroup per CU, two waves per SIMD), else four.  Each of a chunk's query
+// blocks stages every cached tile of its head, so more waves per workgroup
+// means fewer stagings per query: with FP8 pages a staging dequantizes the
+// tile, and eight waves ran 3229 vs 3747 us per call at the 32B-shaped stress
+// step; with bf16 pages eight waves ran slower (2585 vs 2480 us: more waves
+// at every barrier).
+template <int D, bool FP8>
+constexpr int attn_threads() { return FP8 && D == 128 ? 512 : 256; }
 constexpr uint32_t kNoKey = 0x7FFFFFFFu;  // key position of padding rows (never visible)
 constexpr float kRescale = 8.0f;          // lazy rescale threshold, log2 units
 constexpr float kMInit = -1.0e30f;        // running max before the first visible key
@@ -229,7 +238,7 @@ struct Frag {
 // the pool layout (a pool page or a workspace tile) through registers.
 template <int D>
 struct Stage {
-  static constexpr int kPieces = (D * 128) / 16 / kThreads;  // 16-byte pieces per thread
+  static constexpr int kPieces = (D * 128) / 16 / attn_threads<D, false>();  // 16-byte pieces per thread
   u32x4 kx[kPieces / 2];   // key pieces
   u32x4 vx[kPieces / 2];   // value pieces
   uint32_t meta;           // this thread's key row (threads 0..31): position | flag << 31
@@ -240,7 +249,7 @@ struct Stage {
 template <int D>
 struct StageF8 {
   static constexpr int kPieces = (D * 64) / 16;              // code pieces per tile
-  static constexpr int kPer = (kPieces + kThreads - 1) / kThreads;
+  static constexpr int kPer = (kPieces + attn_threads<D, true>() - 1) / attn_threads<D, true>();
   u32x4 cx[kPer];
   float ks[kPer];          // key scale of the token a key piece belongs to
   u32x4 sx;                // scales: [G][key scales (8) | value scales (8)]
@@ -248,7 +257,8 @@ struct StageF8 {
 };
 
 template <int D, int NQ, bool FP8>
-__global__ __launch_bounds__(kThreads, 2) void prefill_kernel(PrefillArgs a) {
+__global__ __launch_bounds__((attn_threads<D, FP8>()), (512 / attn_threads<D, FP8>())) void prefill_kernel(PrefillArgs a) {
+  constexpr int kThreads = attn_threads<D, FP8>();
   __shared__ __attribute__((aligned(16))) char tile_lds[2][D * 128];
   __shared__ __attribute__((aligned(16))) float scale_lds[2][64];   // FP8: tile scales
   __shared__ uint32_t meta_lds[2][32];
@@ -632,7 +642,7 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   a.max_seqs = c.max_seqs;
   a.total = total_tokens;
   a.max_len = max_len;
-  a.PB = 4 * kNQ * (16 / c.group_size);
+  a.PB = attn_threads<D, FP8>() / 64 * kNQ * (16 / c.group_size);
   a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
   const int NH = n * c.num_kv_heads;
   // the timing events bracket all three passes
@@ -645,7 +655,7 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 grid((max_len + a.PB - 1) / a.PB, NH);
-  hipLaunchKernelGGL((prefill_kernel<D, kNQ, FP8>), grid, dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((prefill_kernel<D, kNQ, FP8>), grid, dim3(attn_threads<D, FP8>()), 0, st, a);
   e = hipGetLastError();
   if (ev_stop) (void)hipEventRecord(ev_stop, st);
   return e;
