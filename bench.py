@@ -365,6 +365,112 @@ def prefill_flops(visible_counts, group, head_dim):
     return float(visible_counts.sum()) * group * 4 * head_dim
 
 
+def mla_prefill_flops(visible_counts, group):
+    """Algorithmic flops of latent-attention prefill: for every visible
+    (query, key) pair of every query head, q . row over 576 dims and the
+    weighted sum of the 512 latent dims, 2 flops per multiply-add."""
+    return float(visible_counts.sum()) * group * 2 * (576 + MLA_LATENT)
+
+
+def run_mla_prefill(args):
+    """Latent-attention chunked prefill: a 4096-token DMS-masked chunk for each
+    of 4 sequences on every layer, after 32768 tokens of context (flags
+    Bernoulli(7/8), w = 256), DeepSeek-V2-Lite (16 query heads) or -V2 (128)
+    shapes.  Queries and rows are random and shared by the layers of a step;
+    flags are per layer and position."""
+    import numpy as np
+    import torch
+
+    import dms_synth as sy
+    from paper_2506_05345_amd import dms
+
+    base = WORKLOADS[args.workload.replace("-prefill", "-8x")]
+    C, B = 4096, 4
+    wl = dict(base, batch=B)
+    desc = (base["desc"].split(",")[0] + ": masked chunked prefill, a 4096-token chunk for each of 4 "
+            "sequences on every layer after 32768 tokens of context, w=256, flags Bernoulli(7/8)")
+    nl, g, w, p, seed = wl["layers"], wl["group"], wl["window"], wl["p_evict"], wl["seed"]
+    dev = "cuda"
+    S = args.warmup + args.steps
+    cache, ctx, L0 = build(wl, S * C, C, dev)
+    sid = torch.arange(B, dtype=torch.int32, device=dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seed * 31 + 7)
+    q = torch.randn((B * C, g, 576), generator=gen, device=dev, dtype=torch.bfloat16)
+    k = torch.randn((B * C, 1, 576), generator=gen, device=dev, dtype=torch.bfloat16)
+    out = torch.empty((B * C, g, MLA_LATENT), dtype=torch.float32, device=dev)
+    cu = torch.arange(B + 1, dtype=torch.int32, device=dev) * C
+    seqs = torch.arange(B, device=dev)
+    zero = torch.zeros(1, dtype=torch.int64, device=dev)
+    ctx_t = torch.as_tensor(ctx, device=dev)
+
+    def positions(st):
+        return ctx_t[:, None] + st * C + torch.arange(C, device=dev)[None, :]      # [B, C]
+
+    def flags_at(layer, pos):
+        return sy.flags_torch(seed, p, layer, seqs[:, None, None], zero[None, None, :], pos[:, :, None], dev)
+
+    flags = [[flags_at(layer, positions(st)).reshape(B * C, 1) for layer in range(nl)] for st in range(S)]
+    for st in range(args.warmup):
+        for layer in range(nl):
+            dms.dms_prefill_chunk(cache.ctx, layer, B, sid, cu, B * C, C, q, k, None, flags[st][layer], out)
+    torch.cuda.synchronize()
+    log("warmup done")
+    # algorithmic work of the timed steps: visible keys of every chunk query
+    # (the retained count after its own append), stepping the closed form
+    # from the device's retained lengths before the first timed chunk
+    lens = torch.empty((B, 1), dtype=torch.int32, device=dev)
+    Ls, flops = [], 0.0
+    for layer in range(nl):
+        dms.dms_retained_lengths(cache.ctx, layer, B, sid, lens)
+        Ls.append(lens.to(torch.int64).clone())
+    for st in range(args.warmup, S):
+        pos = positions(st)
+        for layer in range(nl):
+            vis = chunk_visible_counts(Ls[layer], pos, flags_at(layer, pos - w), w)
+            flops += mla_prefill_flops(vis, g)
+            Ls[layer] = vis[:, -1, :]
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    dms.dms_profile_start(cache.ctx, args.steps * nl)
+    torch.cuda.synchronize()
+    ev0.record()
+    for st in range(args.warmup, S):
+        for layer in range(nl):
+            dms.dms_prefill_chunk(cache.ctx, layer, B, sid, cu, B * C, C, q, k, None, flags[st][layer], out)
+    ev1.record()
+    torch.cuda.synchronize()
+    kern_ms, launches = dms.dms_profile_stop(cache.ctx)[dms.DMS_PROFILE_PREFILL]
+    st_code = dms.dms_status(cache.ctx)
+    if st_code != 0:
+        raise RuntimeError(f"prefill failed: {dms.dms_strerror(st_code)}")
+    for layer in range(nl):
+        dms.dms_retained_lengths(cache.ctx, layer, B, sid, lens)
+        if not torch.equal(lens.to(torch.int64), Ls[layer]):
+            raise RuntimeError(f"layer {layer}: retained lengths diverged from the closed form")
+    if not torch.isfinite(out).all():
+        raise RuntimeError("non-finite prefill output")
+    step_ms = ev0.elapsed_time(ev1) / args.steps
+    tflops = flops / args.steps / (step_ms * 1e-3) / 1e12
+    call_us = 1e3 * kern_ms / max(launches, 1)
+    res = {
+        "metric": "DMS latent-attention chunked prefill: algorithmic TFLOP/s",
+        "value": round(tflops, 1), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(step_ms, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": desc, "layers": nl, "batch": B, "chunk": C, "query_heads": g,
+                   "row_dim": 576, "latent_dim": MLA_LATENT, "context": 32768, "window": w,
+                   "p_evict": p},
+        "prefill_tokens_per_s": round(B * C / (step_ms * 1e-3 / nl), 1),
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "call_avg_us": round(call_us, 1),
+                     "call_timing": "HIP events around each dms_prefill_chunk (list, tile copy and "
+                                    "attention passes)",
+                     "flops_per_call": round(flops / (args.steps * nl))},
+    }
+    print(json.dumps(res), flush=True)
+
+
 STRESS = dict(layers=64, batch=32, kv_heads=8, group=5, head_dim=128, prefill_seqs=4,
               chunk=4096, ctx_lo=1024, ctx_hi=131072)
 
@@ -778,7 +884,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="qwen-r1-32b-8x",
-                    choices=sorted(WORKLOADS) + ["qwen-r1-32b-stress", "qwen-r1-32b-train"])
+                    choices=sorted(WORKLOADS) + ["qwen-r1-32b-stress", "qwen-r1-32b-train",
+                                                 "deepseek-v2-lite-prefill", "deepseek-v2-prefill"])
     ap.add_argument("--window", type=int, default=256, choices=[64, 256],
                     help="window of the heterogeneous stress workload")
     ap.add_argument("--chunk", type=int, default=4096)
@@ -821,6 +928,9 @@ def main():
         del src, dst
     if args.workload == "qwen-r1-32b-stress":
         run_stress(args)
+        return
+    if args.workload.endswith("-prefill"):
+        run_mla_prefill(args)
         return
     if args.workload == "qwen-r1-32b-train":
         run_train(args)

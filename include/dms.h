@@ -157,8 +157,10 @@ enum { DMS_EVICT_DELAYED = 0, DMS_EVICT_IMMEDIATE = 1 };
  *     [n][group_size][512] float32 (the up-projection of values is the
  *     caller's).  The `v` arguments are ignored (may be NULL).  Requires
  *     decision_source = DMS_DECIDE_CALLER and quest_page_budget = 0;
- *     dms_prefill_chunk and dms_prefill_chunk_q return DMS_ERR_UNSUPPORTED
- *     (chunks are appended with dms_append_chunk).
+ *     dms_prefill_chunk attends the chunk's queries ([T][group_size][576])
+ *     to the retained rows and the chunk's own rows under the DMS mask,
+ *     writes [T][group_size][512] float32 and commits the rows;
+ *     dms_prefill_chunk_q returns DMS_ERR_UNSUPPORTED.
  */
 enum { DMS_KV_BF16 = 0, DMS_KV_FP8 = 1, DMS_KV_MLA = 2 };
 
@@ -344,7 +346,8 @@ int dms_append_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
  * flagged within the last w positions expire inside the chunk by the same
  * rule.  Then the chunk is committed as by dms_append_chunk.
  * Arguments as for dms_append_chunk, plus q_dev: bf16 [total_tokens, Hq, d]
- * and out_dev: float32 [total_tokens, Hq, d]. */
+ * and out_dev: float32 [total_tokens, Hq, d] (latent rows, DMS_KV_MLA: d = 576
+ * for q and the rows, 512 for out; v_dev is ignored and may be NULL). */
 int dms_prefill_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev,
                       const int32_t* cu_seqlens_dev, int total_tokens, int max_seqlen,
                       const void* q_dev, const void* k_dev, const void* v_dev,

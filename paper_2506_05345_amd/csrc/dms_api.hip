@@ -108,13 +108,12 @@ Layout make_layout(const dms_config& c) {
   lo.ws_ck_slot = take(static_cast<size_t>(c.max_chunk_tokens) * H * 4);
   lo.ws_pf_cum = take((NH + 1) * 4);
   lo.ws_pf_meta = take(static_cast<size_t>(c.max_chunk_tokens) * H * 4);
-  // prefill: chunk keys / values and the compacted kept ones, in the pool's
-  // tile layout; sequence i of a call starts at tile cu[i] / 32 + i
-  // (no chunk attention over latent rows)
-  lo.pf_tiles_per_head = c.kv_format == DMS_KV_MLA
-                             ? 0
-                             : static_cast<int>((static_cast<size_t>(c.max_chunk_tokens) + 31) / 32 + S + 1);
-  lo.ws_pf_tiles = take(2 * H * static_cast<size_t>(lo.pf_tiles_per_head) * D * 128);
+  // prefill: chunk keys / values (latent rows) and the compacted kept ones,
+  // in the pool's tile layout; sequence i of a call starts at tile
+  // cu[i] / 32 + i
+  lo.pf_tiles_per_head = static_cast<int>((static_cast<size_t>(c.max_chunk_tokens) + 31) / 32 + S + 1);
+  lo.ws_pf_tiles = take(2 * H * static_cast<size_t>(lo.pf_tiles_per_head) * D *
+                        (c.kv_format == DMS_KV_MLA ? 64 : 128));
   lo.ws_pf_flags = take(static_cast<size_t>(c.max_chunk_tokens) * H);  // decisions from q
   lo.ws_q_sel = take(NH * static_cast<size_t>(c.quest_page_budget) * 4);
   lo.ws_q_page = take(NH * static_cast<size_t>(c.quest_page_budget) * 4);
@@ -554,11 +553,10 @@ int dms_prefill_chunk(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev
                       const uint8_t* flags_dev, float* out_dev, void* stream) {
   int rc = check_call(ctx, layer, n, seq_ids_dev);
   if (rc) return rc;
-  if (mla(ctx)) return DMS_ERR_UNSUPPORTED;
   if (ctx->c.cfg.decision_source != DMS_DECIDE_CALLER) return DMS_ERR_INVALID;
   if ((rc = check_chunk(ctx, cu_seqlens_dev, total_tokens, max_seqlen))) return rc;
   if (total_tokens == 0) return DMS_OK;
-  if (!q_dev || !k_dev || !v_dev || !flags_dev || !out_dev) return DMS_ERR_INVALID;
+  if (!q_dev || !k_dev || !(v_dev || mla(ctx)) || !flags_dev || !out_dev) return DMS_ERR_INVALID;
   return prefill_chunk(ctx, layer, n, seq_ids_dev, cu_seqlens_dev, total_tokens, max_seqlen, q_dev,
                        k_dev, v_dev, flags_dev, nullptr, out_dev, stream);
 }

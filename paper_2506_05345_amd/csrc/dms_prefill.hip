@@ -661,6 +661,374 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   return e;
 }
 
+
+// ---------------------------------------------------------------------------
+// Chunked prefill over a latent-attention (MLA) cache: one KV head of
+// 576-dim rows shared by the g query heads, in the absorbed form of the
+// latent decode: column (position t, query head h) scores row j by q . row
+// over all 576 dims and sums the rows' first 512 (latent) dims.  The mask and
+// the three key sources are the standard prefill's.  Columns are packed 16
+// per MFMA block -- 16 / g positions x g heads for g <= 16, else one position
+// x 16 of its heads -- and each of a workgroup's four waves takes one column
+// block (its 16 x 512 float32 accumulators fill most of a wave's registers).
+// Per 32-row tile staged in LDS a wave runs 36 score MFMAs, reading the rows
+// in their stored fragment order, and 32 PV MFMAs whose V^T operand (8 rows
+// of one latent dim per lane) comes from the LDS transpose read.
+// ---------------------------------------------------------------------------
+typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+constexpr int kMlaThreads = 256;
+constexpr int kMlaKSteps = kMlaDim / 32;                         // 18
+constexpr int kMlaTileBytes = kMlaDim * 64;                      // 32 rows of 576 bf16
+constexpr int kMlaPieces = kMlaTileBytes / 16 / kMlaThreads;     // staged 16-byte pieces per thread (9)
+constexpr int kMlaOBlocks = kMlaLatent / 16;                     // 16-dim row blocks of O^T (32)
+constexpr int kMlaScoreBatch = 3;                                // score k-steps whose operands are read together
+static_assert(kMlaTileBytes % (16 * kMlaThreads) == 0, "tile staged evenly");
+
+__device__ inline u32x2 tr_read16(const char* p) {
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                       (__attribute__((address_space(3))) v4i16*)(p)));
+}
+
+// Pass 1 for latent rows (one block per (32-token tile, sequence, region)):
+// the chunk's rows in chunk order (region 0) and the kept ones in list order
+// (region 1) into workspace tiles in the pool's layout; rows past the end
+// are 0.
+__global__ __launch_bounds__(kThreads) void prefill_tile_mla_kernel(PrefillArgs a) {
+  if (load_status(a.status) != 0) return;
+  const int k = blockIdx.x, i = blockIdx.y, region = blockIdx.z;
+  const int tok0 = a.cu[i], C = a.cu[i + 1] - a.cu[i];
+  const int cnt = region ? a.list_cnt[i] : C;
+  if (k * 32 >= cnt) return;
+  const int32_t* lst = a.list + tok0;
+  char* tile = a.tiles + ws_tile(a, region, 0, i, k) * kMlaTileBytes;
+  constexpr int kRow = kMlaDim / 8;   // 16-byte pieces per row
+  for (int pc = threadIdx.x; pc < 32 * kRow; pc += kThreads) {
+    const int j = pc / kRow, e0 = 8 * (pc % kRow);
+    const int idx = 32 * k + j;
+    u32x4 x = {0u, 0u, 0u, 0u};
+    if (idx < cnt) {
+      const int c = region ? lst[idx] : idx;
+      x = *reinterpret_cast<const u32x4*>(a.k + static_cast<size_t>(tok0 + c) * kMlaDim + e0);
+    }
+    *reinterpret_cast<u32x4*>(tile + k_elem_off(j, e0)) = x;
+  }
+}
+
+__global__ __launch_bounds__(kMlaThreads, 1) void prefill_mla_kernel(PrefillArgs a) {
+  __shared__ __attribute__((aligned(16))) char tile_lds[2][kMlaTileBytes];
+  __shared__ uint32_t meta_lds[2][32];
+  __shared__ int masked_lds[2];
+  if (load_status(a.status) != 0) return;
+  const int i = blockIdx.y;   // sequence of the call (one KV head)
+  const int tok0 = a.cu[i], C = a.cu[i + 1] - a.cu[i];
+  const int g = a.g;
+  const int pcb = g <= kMaxGroup ? kMaxGroup / g : 1;     // positions per column block
+  const int cgs = (g + kMaxGroup - 1) / kMaxGroup;        // column blocks per position set
+  const int ncb = (C + pcb - 1) / pcb * cgs;
+  const int cb0 = blockIdx.x * (kMlaThreads / 64);
+  if (cb0 >= ncb) return;
+  const int cb1 = min(cb0 + kMlaThreads / 64, ncb) - 1;
+  const int s = a.seq_ids[i];
+  const int sh = s;
+  const int p0 = a.pos[s];
+  const int L0 = a.len[sh];
+  // the block's positions [t0, t1)
+  const int t0 = p0 + (cb0 / cgs) * pcb;
+  const int t1 = p0 + min(C, (cb1 / cgs + 1) * pcb);
+  // band: chunk tiles from the one holding max(p0, t0 - w + 1) up to t1
+  const int band_c0 = (max(0, t0 - a.w + 1 - p0) >> 5) << 5;
+  // kept chunk keys strictly before the band: prefix of the sorted list
+  const int32_t* lst = a.list + tok0;
+  int lo_i = 0, hi_i = a.list_cnt[i];
+  while (lo_i < hi_i) {
+    const int mid = (lo_i + hi_i) >> 1;
+    if (lst[mid] < band_c0) lo_i = mid + 1; else hi_i = mid;
+  }
+  const int n_pre = lo_i;
+  const int nc = (L0 + 31) >> 5;
+  const int np = (n_pre + 31) >> 5;
+  const int nb = (t1 - p0 - band_c0 + 31) >> 5;
+  const char* pre_tiles = a.tiles + ws_tile(a, 1, 0, i, 0) * kMlaTileBytes;
+  const char* band_tiles = a.tiles + ws_tile(a, 0, 0, i, band_c0 >> 5) * kMlaTileBytes;
+  const int ntiles = nc + np + nb;
+  const int32_t* pt = a.page_table + static_cast<size_t>(sh) * a.maxp;
+  const int32_t* smeta = a.slot_meta + static_cast<size_t>(sh) * a.max_slots;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 15, G = lane >> 4;
+  // ---- this wave's column block and this lane's column (position, head)
+  const int cb = cb0 + wave;
+  const bool active = cb < ncb;
+  const int pbk = cb / cgs, hg = cb % cgs;
+  int pl, qh;
+  bool ok;
+  if (g <= kMaxGroup) {
+    pl = r / g;
+    qh = r % g;
+    ok = pl < pcb;
+  } else {
+    pl = 0;
+    qh = kMaxGroup * hg + r;
+    ok = qh < g;
+  }
+  const int cpos = pbk * pcb + pl;   // chunk-local position
+  ok = ok && active && cpos < C;
+  const int tcol = ok ? p0 + cpos : -1;
+  u32x4 qf[kMlaKSteps];
+  {
+    const char* qrow = reinterpret_cast<const char*>(
+        a.q + (static_cast<size_t>(tok0 + (ok ? cpos : 0)) * g + (ok ? qh : 0)) * kMlaDim);
+#pragma unroll
+    for (int s2 = 0; s2 < kMlaKSteps; ++s2)
+      qf[s2] = ok ? *reinterpret_cast<const u32x4*>(qrow + (32 * s2 + 8 * G) * 2) : u32x4{0u, 0u, 0u, 0u};
+  }
+
+  // ---- staging: global -> registers, registers -> LDS (the tile as stored)
+  u32x4 kx[kMlaPieces];
+  uint32_t smt = kNoKey;
+  auto stage_load = [&](int k) {
+    const char* tile;
+    if (k < nc) {
+      const int sb = k * 32;
+      tile = a.pool + static_cast<size_t>(pt[sb >> a.log2P]) * a.page_bytes +
+             static_cast<size_t>((sb & (a.P - 1)) >> 5) * kMlaTileBytes;
+      if (tid < 32) {
+        uint32_t mt = sb + tid < L0 ? static_cast<uint32_t>(smeta[sb + tid]) : kNoKey;
+        if (a.immediate && mt != kNoKey) {
+          const int kp = static_cast<int>(mt & ~kFlagBit);
+          const int x = kp + a.w - p0;
+          mt = static_cast<uint32_t>(kp) |
+               ((x >= 0 && x < C && a.flags[static_cast<size_t>(tok0 + x)]) ? kFlagBit : 0u);
+        }
+        smt = mt;
+      }
+    } else if (k < nc + np) {
+      const int kk = k - nc;
+      tile = pre_tiles + static_cast<size_t>(kk) * kMlaTileBytes;
+      if (tid < 32) {
+        const int idx = kk * 32 + tid;
+        smt = idx < n_pre ? static_cast<uint32_t>(p0 + lst[idx]) : kNoKey;
+      }
+    } else {
+      const int kb = k - nc - np;
+      tile = band_tiles + static_cast<size_t>(kb) * kMlaTileBytes;
+      if (tid < 32) {
+        const int c = band_c0 + kb * 32 + tid;
+        smt = c < t1 - p0 ? (static_cast<uint32_t>(p0 + c) | (key_flag(a, tok0, C, c, 0) ? kFlagBit : 0u))
+                          : kNoKey;
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < kMlaPieces; ++m) kx[m] = *reinterpret_cast<const u32x4*>(tile + (tid + m * kMlaThreads) * 16);
+  };
+  auto stage_store = [&](int k, int buf) {
+    char* dst = tile_lds[buf];
+    // pool slots past L hold stale bits (a freed page may hold NaNs): their
+    // rows are zeroed, which zeroes them in the V^T operand too
+    const int valid = k < nc ? min(32, L0 - k * 32) : 32;
+#pragma unroll
+    for (int m = 0; m < kMlaPieces; ++m) {
+      const int P = tid + m * kMlaThreads;
+      // piece P: 1 KB block P / 64 of half (P / 64) % 2, lane row P % 16
+      const int pr = P & 15, row = 8 * (pr >> 2) + (pr & 3) + 4 * ((P >> 6) & 1);
+      const u32x4 x = row < valid ? kx[m] : u32x4{0u, 0u, 0u, 0u};
+      *reinterpret_cast<u32x4*>(dst + P * 16) = x;
+    }
+    if (tid < 64) {
+      // a key row needs the per-element mask iff some query of the block does
+      // not see it: padding, causal (position > t0) or flagged and expiring
+      // by t1 - 1
+      bool need = false;
+      if (tid < 32) {
+        const uint32_t mt = smt;
+        const int kp = static_cast<int>(mt & ~kFlagBit);
+        need = mt == kNoKey || kp > t0 || ((mt & kFlagBit) && kp + a.w <= t1 - 1);
+        meta_lds[buf][tid] = mt;
+      }
+      const uint64_t any = __builtin_amdgcn_ballot_w64(need);
+      if (tid == 0) masked_lds[buf] = any != 0;
+    }
+  };
+
+  // ---- accumulators: O^T rows 16 b + 4G .. + 3 of column r
+  f32x4 o[kMlaOBlocks];
+#pragma unroll
+  for (int b = 0; b < kMlaOBlocks; ++b) o[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_ref = kMInit, l_run = 0.f;
+  const float thr = kRescale / a.scale_log2;   // rescale threshold in score units
+  // transpose-read address of this lane in a tile (row block 0, rows 0-3 of
+  // each 8): lane 16 G' + 4 j + q reads dims 4q .. 4q + 3 of row 8 G' + j
+  const int tr_j = (lane & 15) >> 2, tr_q = lane & 3;
+  const int tr_off = (tr_q >> 1) * 256 + (4 * G + tr_j) * 16 + 8 * (tr_q & 1);
+
+  if (ntiles > 0) {
+    stage_load(0);
+    stage_store(0, 0);
+  }
+  __syncthreads();
+  for (int k = 0; k < ntiles; ++k) {
+    const int buf = k & 1;
+    if (k + 1 < ntiles) stage_load(k + 1);
+    const char* tl = tile_lds[buf];
+    if (active) {
+      // scores: the 36 A pieces (piece 2s + h: half h, k-step s) read in
+      // batches, the next batch in flight while one is multiplied
+      f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+      u32x4 kp2[2][2 * kMlaScoreBatch];
+      const char* kl = tl + lane * 16;
+#pragma unroll
+      for (int e = 0; e < 2 * kMlaScoreBatch; ++e) kp2[0][e] = *reinterpret_cast<const u32x4*>(kl + e * 1024);
+#pragma unroll
+      for (int bt = 0; bt < kMlaKSteps / kMlaScoreBatch; ++bt) {
+        if (bt + 1 < kMlaKSteps / kMlaScoreBatch) {
+#pragma unroll
+          for (int e = 0; e < 2 * kMlaScoreBatch; ++e)
+            kp2[(bt + 1) & 1][e] = *reinterpret_cast<const u32x4*>(kl + (2 * kMlaScoreBatch * (bt + 1) + e) * 1024);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int e = 0; e < kMlaScoreBatch; ++e) {
+          s0 = mfma_bf16(kp2[bt & 1][2 * e], qf[kMlaScoreBatch * bt + e], s0);
+          s1 = mfma_bf16(kp2[bt & 1][2 * e + 1], qf[kMlaScoreBatch * bt + e], s1);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // lane (r, G): keys 8G .. 8G+3 (s0) and 8G+4 .. 8G+7 (s1) of column r
+      float sc[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        sc[j] = s0[j];
+        sc[j + 4] = s1[j];
+      }
+      if (__builtin_amdgcn_readfirstlane(masked_lds[buf]) != 0) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const uint32_t km = meta_lds[buf][8 * G + j];
+          const int kpos = static_cast<int>(km & ~kFlagBit);
+          const int kexp = (km & kFlagBit) ? kpos + a.w : 0x7FFFFFFF;
+          sc[j] = (kpos <= tcol && tcol < kexp) ? sc[j] : -INFINITY;
+        }
+      }
+      float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
+                       fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
+      mx = col_max(mx);
+      const bool raise = mx > m_ref + thr;   // false while the column has seen no key
+      if (__builtin_amdgcn_ballot_w64(raise)) {
+        const float m_new = raise ? mx : m_ref;
+        const float alpha = __builtin_amdgcn_exp2f((m_ref - m_new) * a.scale_log2);
+        l_run *= alpha;
+#pragma unroll
+        for (int b = 0; b < kMlaOBlocks; ++b) o[b] *= alpha;
+        m_ref = m_new;
+      }
+      const float mb = m_ref * a.scale_log2;
+      u32x4 pu;
+      const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x2 pr = {__builtin_amdgcn_exp2f(fmaf(sc[2 * j], a.scale_log2, -mb)),
+                          __builtin_amdgcn_exp2f(fmaf(sc[2 * j + 1], a.scale_log2, -mb))};
+        const bf16x2 pb = __builtin_convertvector(pr, bf16x2);
+        pu[j] = __builtin_bit_cast(uint32_t, pb);
+        l_run = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, l_run, false);
+      }
+      // PV: V^T of latent row block b (dims 16 b ..), rows 8G .. 8G+7, from
+      // the transpose read; four blocks' reads ahead of their products
+#pragma unroll
+      for (int b0 = 0; b0 < kMlaOBlocks; b0 += 4) {
+        u32x4 vt[4];
+#pragma unroll
+        for (int i2 = 0; i2 < 4; ++i2) {
+          const int b = b0 + i2;
+          const char* base = tl + (b >> 1) * 2048 + (b & 1) * 512 + tr_off;
+          const u32x2 lo = tr_read16(base), hi = tr_read16(base + 1024);
+          vt[i2] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+        }
+#pragma unroll
+        for (int i2 = 0; i2 < 4; ++i2) o[b0 + i2] = mfma_bf16(vt[i2], pu, o[b0 + i2]);
+      }
+    }
+    if (k + 1 < ntiles) stage_store(k + 1, buf ^ 1);
+    __syncthreads();
+  }
+
+  // ---- outputs
+  float l = l_run;
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  if (tcol >= 0) {
+    const float inv = 1.0f / l;
+    float* dst = a.out + (static_cast<size_t>(tok0 + cpos) * g + qh) * kMlaLatent + 4 * G;
+#pragma unroll
+    for (int b = 0; b < kMlaOBlocks; ++b) *reinterpret_cast<f32x4*>(dst + 16 * b) = o[b] * inv;
+  }
+}
+
+hipError_t launch_prefill_mla(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
+                              int layer, int n, const int32_t* seq_ids, const int32_t* cu,
+                              int total_tokens, int max_len, const void* q, const void* k,
+                              const uint8_t* flags, float* out, hipStream_t st, hipEvent_t ev_start,
+                              hipEvent_t ev_stop) {
+  char* w = static_cast<char*>(ws);
+  LayerState ls = layer_state(lo, meta, layer);
+  PrefillArgs a;
+  a.status = reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status);
+  a.status_w = reinterpret_cast<int32_t*>(static_cast<char*>(meta) + lo.status);
+  a.seq_ids = seq_ids;
+  a.cu = cu;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = nullptr;
+  a.flags = flags;
+  a.pool = static_cast<const char*>(pool);
+  a.page_table = ls.page_table;
+  a.slot_meta = ls.slot_meta;
+  a.len = ls.len;
+  a.pos = ls.pos;
+  a.list = reinterpret_cast<int32_t*>(w + lo.ws_pf_meta);
+  a.list_cnt = reinterpret_cast<int32_t*>(w + lo.ws_pf_cum);
+  a.tiles = w + lo.ws_pf_tiles;
+  a.tph = lo.pf_tiles_per_head;
+  a.immediate = c.eviction == DMS_EVICT_IMMEDIATE;
+  a.zero_neuron = 0;
+  a.out = out;
+  a.page_bytes = lo.page_bytes;
+  a.n = n;
+  a.H = 1;
+  a.g = c.group_size;
+  a.w = c.window;
+  a.P = c.page_size;
+  a.log2P = __builtin_ctz(static_cast<unsigned>(c.page_size));
+  a.maxp = c.max_pages_per_head;
+  a.max_slots = lo.max_slots;
+  a.max_seqs = c.max_seqs;
+  a.total = total_tokens;
+  a.max_len = max_len;
+  a.PB = 0;
+  a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
+  // the timing events bracket all three passes
+  if (ev_start) (void)hipEventRecord(ev_start, st);
+  hipLaunchKernelGGL(prefill_list_kernel, dim3(n), dim3(kThreads), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(prefill_tile_mla_kernel, dim3((max_len + 31) / 32, n, 2), dim3(kThreads), 0, st, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int g = c.group_size;
+  const int pcb = g <= kMaxGroup ? kMaxGroup / g : 1;
+  const int cgs = (g + kMaxGroup - 1) / kMaxGroup;
+  const int ncb = (max_len + pcb - 1) / pcb * cgs;
+  const int per_block = kMlaThreads / 64;
+  hipLaunchKernelGGL(prefill_mla_kernel, dim3((ncb + per_block - 1) / per_block, n), dim3(kMlaThreads), 0, st, a);
+  e = hipGetLastError();
+  if (ev_stop) (void)hipEventRecord(ev_stop, st);
+  return e;
+}
+
 }  // namespace
 
 hipError_t launch_prefill_decide(const dms_config& c, const void* q, int total_tokens,
@@ -679,6 +1047,9 @@ hipError_t launch_prefill_attention(const dms_config& c, const Layout& lo, void*
                                     const void* q, const void* k, const void* v,
                                     const uint8_t* flags, float* out, hipStream_t st,
                                     hipEvent_t ev_start, hipEvent_t ev_stop) {
+  if (c.kv_format == DMS_KV_MLA)
+    return launch_prefill_mla(c, lo, meta, ws, pool, layer, n, seq_ids, cu, total_tokens, max_len, q, k, flags,
+                              out, st, ev_start, ev_stop);
   const bool fp8 = c.kv_format == DMS_KV_FP8;
   if (c.head_dim == 128)
     return fp8 ? launch_prefill_d<128, true>(c, lo, meta, ws, pool, layer, n, seq_ids, cu, total_tokens,

@@ -357,12 +357,15 @@ def test_latent_pages_layout_and_host_checks():
     for s_ in (0, 5, 31, 32, 63):
         for e in (0, 7, 31, 32, 100, 511, 512, 575):
             assert rows[s_, e] == 1 + s_ * 1000 + e
-    # the prefill entry points refuse latent pools before any device work
+    # latent pools: prefill with caller decisions takes no value rows (v may be
+    # NULL, the other arguments may not); decisions from q are refused, all
+    # before any device work
     L = dms.lib()
     ctx = dms.dms_create(_cfg(**mla), 0x1000, [0x2000, 0x3000], 0x4000)
     try:
         X = 0x100
-        assert L.dms_prefill_chunk(ctx, 0, 1, X, X, 4, 4, X, X, None, X, X, None) == dms.DMS_ERR_UNSUPPORTED
+        assert L.dms_prefill_chunk(ctx, 0, 1, X, X, 4, 4, None, X, None, X, X, None) == dms.DMS_ERR_INVALID
+        assert L.dms_prefill_chunk(ctx, 0, 1, X, X, 4, 4, X, None, None, X, X, None) == dms.DMS_ERR_INVALID
         assert L.dms_prefill_chunk_q(ctx, 0, 1, X, X, 4, 4, X, X, None, X, X, None) == dms.DMS_ERR_UNSUPPORTED
     finally:
         dms.dms_destroy(ctx)

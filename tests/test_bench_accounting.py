@@ -51,3 +51,20 @@ def test_app_i_estimate_matches_oracle_model(name):
         assert weights == lm.reads(B, 0, **params)
         kv = lm.reads(B, L, **params) - lm.reads(B, 0, **params)
         assert share == pytest.approx(kv / peak_bw / lat, rel=1e-12)
+
+
+def test_latent_prefill_and_decode_flops_decompose_into_the_pinned_accountant():
+    # the oracle's accountant counts 4 d flops per visible (query, key) pair
+    # and query head: 2 d for q . k and 2 d for p . v.  A latent row scores
+    # over all 576 dims and contributes its 512 latent dims as the value.
+    rng = np.random.default_rng(7)
+    vis = torch.as_tensor(rng.integers(0, 5000, size=(3, 17, 1)))
+    for g in (1, 16, 40, 128):
+        want = lm.prefill_attention_flops(vis.numpy(), g, 576) / 2 + lm.prefill_attention_flops(vis.numpy(), g, 512) / 2
+        assert bench.mla_prefill_flops(vis, g) == want
+        # per retained row of one decode step: the same per-pair count
+        wl = dict(head_dim=576, group=g, kv_format=bench.MLA)
+        assert bench.attend_flops(wl) == lm.prefill_attention_flops(np.ones(1), g, 576) / 2 + \
+            lm.prefill_attention_flops(np.ones(1), g, 512) / 2
+    # standard rows: 4 d per pair
+    assert bench.attend_flops(dict(head_dim=128, group=5)) == lm.prefill_attention_flops(np.ones(1), 5, 128)

@@ -190,17 +190,95 @@ def test_mla_long_heads_split_over_many_waves(g):
     cache.close()
 
 
-def test_mla_prefill_is_refused():
+def _prefill_run(g, seqs, lens, chunks, seed, p, w, P, nan_fill=False, then_decode=0):
+    """Prefill every sequence to lens[s] tokens in calls of chunks[c] tokens
+    per sequence (dms_prefill_chunk over latent rows): each call's outputs
+    against dense masked absorbed attention over the full history, the state
+    and stored rows after it against the oracle replay; then decode steps."""
+    torch = _torch()
+    maxp = max(lens.values()) // P + 4 + then_decode // P
+    dms, cfg, cache, orc = _mk(max(seqs) + 1, g, w, P, num_pages=len(seqs) * maxp, maxp=maxp,
+                               max_chunk=len(seqs) * max(chunks))
+    if nan_fill:
+        for pl in cache.pools:
+            pl.fill_(0xFF)
+        cache.workspace.fill_(0xFF)
+        dms.dms_init_state(cache.ctx)
+        torch.cuda.synchronize()
+    inp = {s: MlaInputs(seed, s, lens[s] + then_decode, g, p) for s in seqs}
+    scale = 1.0 / math.sqrt(ROW)
+    cur = {s: 0 for s in seqs}
+    ci = 0
+    worst = 0.0
+    while any(cur[s] < lens[s] for s in seqs):
+        C = chunks[ci % len(chunks)]
+        ci += 1
+        ls = [min(C, lens[s] - cur[s]) for s in seqs]
+        cu = np.concatenate([[0], np.cumsum(ls)]).astype(np.int32)
+        q = np.concatenate([inp[s].q[cur[s]:cur[s] + l] for s, l in zip(seqs, ls)])
+        k = np.concatenate([inp[s].k[cur[s]:cur[s] + l] for s, l in zip(seqs, ls)])
+        f = np.concatenate([inp[s].flags[cur[s]:cur[s] + l] for s, l in zip(seqs, ls)])
+        out = torch.full((int(cu[-1]), g, LATENT), float("nan"), device="cuda")
+        dms.dms_prefill_chunk(cache.ctx, 0, len(seqs), to_dev(np.array(seqs, np.int32)), to_dev(cu),
+                              int(cu[-1]), int(max(ls)), to_dev(q), to_dev(k), None, to_dev(f), out)
+        torch.cuda.synchronize()
+        assert dms.dms_status(cache.ctx) == 0
+        got = out.cpu().numpy()
+        for i, (s, l) in enumerate(zip(seqs, ls)):
+            if l == 0:
+                continue
+            T = cur[s] + l
+            rows = bf16_to_f32(inp[s].k[:T, 0]).astype(np.float64)
+            qs = bf16_to_f32(inp[s].q[cur[s]:T]).astype(np.float64)
+            for x in range(l):
+                t = cur[s] + x
+                mask = np.asarray(visible(t, np.arange(t + 1), inp[s].flags[:t + 1, 0], w), dtype=bool)
+                ref = mla_attention(qs[x], rows[:t + 1], np.broadcast_to(mask, (g, t + 1)), LATENT, scale)
+                err = float(np.abs(got[cu[i] + x] - ref).max())
+                worst = max(worst, err)
+                assert err <= ATOL, (s, t, err)
+        rows_f = [bf16_to_f32(inp[s].k[cur[s]:cur[s] + l]) for s, l in zip(seqs, ls)]
+        orc.append_chunk(seqs, [inp[s].flags[cur[s]:cur[s] + l] for s, l in zip(seqs, ls)], rows_f, rows_f)
+        for s, l in zip(seqs, ls):
+            cur[s] += l
+        view = _compare_rows(cache, orc, seqs)
+        compare_state(view, orc, seqs)
+    if then_decode:
+        _decode_steps(dms, cache, orc, seqs, inp, {s: lens[s] for s in seqs}, then_decode, g, dense_every=4)
+    cache.close()
+    return worst
+
+
+@pytest.mark.parametrize("g,w,P,p,chunks", [
+    (16, 32, 64, 0.75, [256, 37]), (5, 16, 32, 0.5, [300]), (1, 8, 64, 0.9, [129, 64]),
+    (40, 64, 64, 0.875, [200]), (128, 24, 64, 0.75, [96, 160])])
+def test_mla_prefill_ragged_chunks(g, w, P, p, chunks):
+    """Chunked prefill over latent rows: ragged histories, several chunkings,
+    query groups below, at and above 16 heads (ragged groups of 16)."""
+    lens = {2: 700, 0: 131, 1: 402} if g <= 40 else {1: 300, 0: 97}
+    worst = _prefill_run(g, sorted(lens), lens, chunks, 53 + g, p, w, P)
+    print(f"[mla prefill] g={g} max abs err {worst:.2e}", flush=True)
+
+
+def test_mla_prefill_on_nan_pools_then_decode():
+    """Pools and workspace start as NaN bytes (stale rows of freed pages and
+    the workspace's unused tiles must never reach an output); decode steps
+    after the prefill continue from the committed state."""
+    _prefill_run(16, [0, 1], {0: 500, 1: 260}, [200], 71, 0.8, 32, 64, nan_fill=True, then_decode=12)
+
+
+def test_mla_prefill_q_is_refused():
+    """Decisions from the query are not combined with latent rows."""
     from paper_2506_05345_amd import dms
     _, cfg, cache, _ = _mk(1, 16, 16, 32, 8, 4)
     torch = _torch()
     x = torch.zeros(16 * ROW, dtype=torch.bfloat16, device="cuda")
     cu = torch.tensor([0, 4], dtype=torch.int32, device="cuda")
-    fl = torch.zeros(4, dtype=torch.uint8, device="cuda")
+    dec = torch.zeros(4, dtype=torch.uint8, device="cuda")
     out = torch.zeros(4 * 16 * LATENT, dtype=torch.float32, device="cuda")
     sid = torch.zeros(1, dtype=torch.int32, device="cuda")
     with pytest.raises(dms.DmsError):
-        dms.dms_prefill_chunk(cache.ctx, 0, 1, sid, cu, 4, 4, x, x, None, fl, out)
+        dms.dms_prefill_chunk_q(cache.ctx, 0, 1, sid, cu, 4, 4, x, x, None, dec, out)
     cache.close()
 
 
