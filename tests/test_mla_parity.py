@@ -10,7 +10,7 @@ import pytest
 
 import dms_synth as sy
 from dms_testlib import ATOL, bf16_to_f32, compare_state, to_dev
-from oracle import PagedKVOracle, mla_attention, visible
+from oracle import PagedKVOracle, mla_attention, visible, visible_immediate
 
 pytestmark = pytest.mark.gpu
 
@@ -36,14 +36,15 @@ def _torch():
     return torch
 
 
-def _mk(max_seqs, g, w, P, num_pages, maxp, max_chunk=4096):
+def _mk(max_seqs, g, w, P, num_pages, maxp, max_chunk=4096, mode="delayed"):
     from paper_2506_05345_amd import dms
     cfg = dms.make_config(num_layers=1, max_seqs=max_seqs, num_kv_heads=1, group_size=g,
                           head_dim=ROW, window=w, page_size=P, num_pages=num_pages,
                           max_pages_per_head=maxp, max_chunk_tokens=max_chunk,
+                          eviction=dms.DMS_EVICT_IMMEDIATE if mode == "immediate" else dms.DMS_EVICT_DELAYED,
                           kv_format=dms.DMS_KV_MLA)
     cache = dms.DmsCache(cfg)
-    orc = PagedKVOracle(max_seqs, 1, w, P, num_pages, maxp, ROW)
+    orc = PagedKVOracle(max_seqs, 1, w, P, num_pages, maxp, ROW, mode=mode)
     return dms, cfg, cache, orc
 
 
@@ -190,7 +191,7 @@ def test_mla_long_heads_split_over_many_waves(g):
     cache.close()
 
 
-def _prefill_run(g, seqs, lens, chunks, seed, p, w, P, nan_fill=False, then_decode=0):
+def _prefill_run(g, seqs, lens, chunks, seed, p, w, P, nan_fill=False, then_decode=0, mode="delayed"):
     """Prefill every sequence to lens[s] tokens in calls of chunks[c] tokens
     per sequence (dms_prefill_chunk over latent rows): each call's outputs
     against dense masked absorbed attention over the full history, the state
@@ -198,7 +199,7 @@ def _prefill_run(g, seqs, lens, chunks, seed, p, w, P, nan_fill=False, then_deco
     torch = _torch()
     maxp = max(lens.values()) // P + 4 + then_decode // P
     dms, cfg, cache, orc = _mk(max(seqs) + 1, g, w, P, num_pages=len(seqs) * maxp, maxp=maxp,
-                               max_chunk=len(seqs) * max(chunks))
+                               max_chunk=len(seqs) * max(chunks), mode=mode)
     if nan_fill:
         for pl in cache.pools:
             pl.fill_(0xFF)
@@ -232,7 +233,10 @@ def _prefill_run(g, seqs, lens, chunks, seed, p, w, P, nan_fill=False, then_deco
             qs = bf16_to_f32(inp[s].q[cur[s]:T]).astype(np.float64)
             for x in range(l):
                 t = cur[s] + x
-                mask = np.asarray(visible(t, np.arange(t + 1), inp[s].flags[:t + 1, 0], w), dtype=bool)
+                if mode == "immediate":
+                    mask = np.asarray(visible_immediate(t, np.arange(t + 1), inp[s].flags[:, 0], w), dtype=bool)
+                else:
+                    mask = np.asarray(visible(t, np.arange(t + 1), inp[s].flags[:t + 1, 0], w), dtype=bool)
                 ref = mla_attention(qs[x], rows[:t + 1], np.broadcast_to(mask, (g, t + 1)), LATENT, scale)
                 err = float(np.abs(got[cu[i] + x] - ref).max())
                 worst = max(worst, err)
@@ -258,6 +262,14 @@ def test_mla_prefill_ragged_chunks(g, w, P, p, chunks):
     lens = {2: 700, 0: 131, 1: 402} if g <= 40 else {1: 300, 0: 97}
     worst = _prefill_run(g, sorted(lens), lens, chunks, 53 + g, p, w, P)
     print(f"[mla prefill] g={g} max abs err {worst:.2e}", flush=True)
+
+
+def test_mla_prefill_immediate_eviction():
+    """The immediate-eviction timing (a token's own decision evicts the token
+    w positions back, Sec. 5.3): cached keys hidden by decisions inside the
+    chunk, chunk keys by later chunk decisions."""
+    lens = {0: 600, 1: 333}
+    _prefill_run(16, [0, 1], lens, [150, 64], 81, 0.7, 32, 64, mode="immediate")
 
 
 def test_mla_prefill_on_nan_pools_then_decode():
