@@ -114,6 +114,7 @@ Layout make_layout(const dms_config& c) {
   lo.pf_tiles_per_head = static_cast<int>((static_cast<size_t>(c.max_chunk_tokens) + 31) / 32 + S + 1);
   lo.ws_pf_tiles = take(2 * H * static_cast<size_t>(lo.pf_tiles_per_head) * D *
                         (c.kv_format == DMS_KV_MLA ? 64 : 128));
+  lo.ws_pf_tmeta = take(2 * H * static_cast<size_t>(lo.pf_tiles_per_head) * 32 * 4);   // their key rows
   lo.ws_pf_flags = take(static_cast<size_t>(c.max_chunk_tokens) * H);  // decisions from q
   lo.ws_q_sel = take(NH * static_cast<size_t>(c.quest_page_budget) * 4);
   lo.ws_q_page = take(NH * static_cast<size_t>(c.quest_page_budget) * 4);

@@ -101,6 +101,7 @@ struct PrefillArgs {
   int32_t* list;          // [H][total]: chunk-local indices of kept tokens
   int32_t* list_cnt;      // [n * H]
   char* tiles;            // [2][H][tph] tiles: chunk tokens, then compacted kept tokens
+  uint32_t* tmeta;        // [2][H][tph][32]: key rows of those tiles (position | flag << 31)
   float* out;             // [T, Hq, D]
   size_t page_bytes;
   int n, H, g, w, P, log2P, maxp, max_slots, max_seqs, total, max_len, PB, tph;
@@ -178,6 +179,17 @@ __global__ __launch_bounds__(kThreads) void prefill_tile_kernel(PrefillArgs a) {
   const int32_t* lst = a.list + static_cast<size_t>(h) * a.total + tok0;
   const int tid = threadIdx.x;
   constexpr int kPieces = 32 * D / 8;   // 16-byte pieces of 32 rows
+  if (tid < 32) {
+    // the tile's key rows as the pool's slot metadata has them: position |
+    // flag << 31 (kept-list rows carry no flag); rows past the end: no key
+    const int idx = 32 * k + tid;
+    const int p0 = a.pos[a.seq_ids[i]];
+    uint32_t mt = kNoKey;
+    if (idx < cnt)
+      mt = region ? static_cast<uint32_t>(p0 + lst[idx])
+                  : (static_cast<uint32_t>(p0 + idx) | (key_flag(a, tok0, C, idx, h) ? kFlagBit : 0u));
+    a.tmeta[ws_tile(a, region, h, i, k) * 32 + tid] = mt;
+  }
   if constexpr (FP8) {
     // FP8 pages: the chunk's rows are quantized exactly as the commit will
     // store them (D/8 consecutive threads per row; rows past the end get
@@ -255,6 +267,88 @@ struct StageF8 {
   u32x4 sx;                // scales: [G][key scales (8) | value scales (8)]
   uint32_t meta;
 };
+
+// Online-softmax weights of one key tile for one column block: s0 / s1 are
+// the scores of key rows 8 G .. 8 G + 3 and 8 G + 4 .. 8 G + 7 of the lane's
+// column t.  kp / kx (read only when masked): position and expiry (first
+// query that no longer sees it) of those rows; vsc (FP8): their value scales.
+// Rescales o and l_run when the column's max rises past the threshold;
+// returns the weights rounded to bf16 for the PV MFMAs.
+template <int D, bool FP8>
+__device__ __forceinline__ u32x4 col_weights(f32x4 s0, f32x4 s1, const float (&vsc)[8], bool masked,
+                                             const int (&kp)[8], const int (&kx)[8], int t,
+                                             f32x4 (&o)[D / 16], float& m_ref, float& l_run, float thr,
+                                             float scale_log2) {
+  float sc[8];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    sc[j] = s0[j];
+    sc[j + 4] = s1[j];
+  }
+  if (masked) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sc[j] = (kp[j] <= t && t < kx[j]) ? sc[j] : -INFINITY;
+  }
+  float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
+                   fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
+  mx = col_max(mx);
+  const bool raise = mx > m_ref + thr;   // false while the column has seen no key
+  if (__builtin_amdgcn_ballot_w64(raise)) {
+    const float m_new = raise ? mx : m_ref;
+    const float alpha = __builtin_amdgcn_exp2f((m_ref - m_new) * scale_log2);
+    l_run *= alpha;
+#pragma unroll
+    for (int b = 0; b < D / 16; ++b) o[b] *= alpha;
+    m_ref = m_new;
+  }
+  // p = 2^((s - m) * scale); hidden keys give exactly 0
+  const float mb = m_ref * scale_log2;
+  float e[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) e[j] = __builtin_amdgcn_exp2f(fmaf(sc[j], scale_log2, -mb));
+  // P is rounded to bf16 for the MFMA; the denominator adds the same
+  // rounded values (dot with (1, 1)), so a single dominant key returns its
+  // value row exactly
+  u32x4 pu;
+  const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const f32x2 pr = {e[2 * j], e[2 * j + 1]};
+    const bf16x2 pb = __builtin_convertvector(pr, bf16x2);
+    pu[j] = __builtin_bit_cast(uint32_t, pb);
+    l_run = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, l_run, false);
+    if constexpr (FP8) {
+      // PV weights carry the value scale: rounding commutes with a
+      // power-of-two factor, so these are the rounded weights times it
+      const f32x2 pv = {e[2 * j] * vsc[2 * j], e[2 * j + 1] * vsc[2 * j + 1]};
+      pu[j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pv, bf16x2));
+    }
+  }
+  return pu;
+}
+
+// Scores, online softmax and PV of one key tile for the NQ column blocks of a
+// wave.
+template <int D, int NQ, bool FP8>
+__device__ __forceinline__ void attend_tile(const Frag<D>& f, const float (&vsc)[8], bool masked,
+                                            const int (&kp)[8], const int (&kx)[8],
+                                            const int (&tcol)[NQ], const u32x4 (&qf)[NQ][D / 32],
+                                            f32x4 (&o)[NQ][D / 16], float (&m_ref)[NQ],
+                                            float (&l_run)[NQ], float thr, float scale_log2) {
+#pragma unroll
+  for (int qb = 0; qb < NQ; ++qb) {
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s2 = 0; s2 < D / 32; ++s2) {
+      s0 = mfma_bf16(f.ka[s2], qf[qb][s2], s0);
+      s1 = mfma_bf16(f.kb[s2], qf[qb][s2], s1);
+    }
+    const u32x4 pu = col_weights<D, FP8>(s0, s1, vsc, masked, kp, kx, tcol[qb], o[qb], m_ref[qb], l_run[qb],
+                                         thr, scale_log2);
+#pragma unroll
+    for (int b = 0; b < D / 16; ++b) o[qb][b] = mfma_bf16(f.vt[b], pu, o[qb][b]);
+  }
+}
 
 template <int D, int NQ, bool FP8>
 __global__ __launch_bounds__((attn_threads<D, FP8>()), (512 / attn_threads<D, FP8>())) void prefill_kernel(PrefillArgs a) {
@@ -521,65 +615,278 @@ __global__ __launch_bounds__((attn_threads<D, FP8>()), (512 / attn_threads<D, FP
         kx[j] = (km & kFlagBit) ? kp[j] + a.w : 0x7FFFFFFF;
       }
     }
-#pragma unroll
-    for (int qb = 0; qb < NQ; ++qb) {
-      f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s2 = 0; s2 < D / 32; ++s2) {
-        s0 = mfma_bf16(f.ka[s2], qf[qb][s2], s0);
-        s1 = mfma_bf16(f.kb[s2], qf[qb][s2], s1);
-      }
-      float sc[8];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        sc[j] = s0[j];
-        sc[j + 4] = s1[j];
-      }
-      if (masked) {
-        const int t = tcol[qb];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) sc[j] = (kp[j] <= t && t < kx[j]) ? sc[j] : -INFINITY;
-      }
-      float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
-                       fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
-      mx = col_max(mx);
-      const bool raise = mx > m_ref[qb] + thr;   // false while the column has seen no key
-      if (__builtin_amdgcn_ballot_w64(raise)) {
-        const float m_new = raise ? mx : m_ref[qb];
-        const float alpha = __builtin_amdgcn_exp2f((m_ref[qb] - m_new) * a.scale_log2);
-        l_run[qb] *= alpha;
-#pragma unroll
-        for (int b = 0; b < D / 16; ++b) o[qb][b] *= alpha;
-        m_ref[qb] = m_new;
-      }
-      // p = 2^((s - m) * scale); hidden keys give exactly 0
-      const float mb = m_ref[qb] * a.scale_log2;
-      float e[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) e[j] = __builtin_amdgcn_exp2f(fmaf(sc[j], a.scale_log2, -mb));
-      // P is rounded to bf16 for the MFMA; the denominator adds the same
-      // rounded values (dot with (1, 1)), so a single dominant key returns
-      // its value row exactly
-      u32x4 pu;
-      const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3F803F80u);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const f32x2 pr = {e[2 * j], e[2 * j + 1]};
-        const bf16x2 pb = __builtin_convertvector(pr, bf16x2);
-        pu[j] = __builtin_bit_cast(uint32_t, pb);
-        l_run[qb] = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, l_run[qb], false);
-        if constexpr (FP8) {
-          // PV weights carry the value scale: rounding commutes with a
-          // power-of-two factor, so these are the rounded weights times it
-          const f32x2 pv = {e[2 * j] * vsc[2 * j], e[2 * j + 1] * vsc[2 * j + 1]};
-          pu[j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pv, bf16x2));
-        }
-      }
-#pragma unroll
-      for (int b = 0; b < D / 16; ++b) o[qb][b] = mfma_bf16(f.vt[b], pu, o[qb][b]);
-    }
+    attend_tile<D, NQ, FP8>(f, vsc, masked, kp, kx, tcol, qf, o, m_ref, l_run, thr, a.scale_log2);
     if (k + 1 < ntiles) stage_store(k + 1, buf ^ 1);
     __syncthreads();
+  }
+
+  // ---- outputs
+#pragma unroll
+  for (int qb = 0; qb < NQ; ++qb) {
+    float l = l_run[qb];
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    const int t = tcol[qb];
+    if (t >= 0) {
+      const int qh = r % a.g;
+      const float inv = 1.0f / l;
+      float* dst = a.out + (static_cast<size_t>(tok0 + (t - p0)) * Hq + h * a.g + qh) * D + 4 * G;
+#pragma unroll
+      for (int b = 0; b < D / 16; ++b) *reinterpret_cast<f32x4*>(dst + 16 * b) = o[qb][b] * inv;
+    }
+  }
+}
+
+// ---- bf16 pages under delayed eviction: tiles copied by the hardware.
+// Every key source is a plain copy -- pool tiles with their slot metadata,
+// workspace tiles with the metadata pass 1 wrote -- so global -> LDS loads
+// (global_load_lds) move tiles and key rows two tiles ahead of the one being
+// attended, into three LDS buffers, with no staging registers, LDS stores or
+// waits for them in the loop.  Rows past a source's end are fixed up when
+// read: pool slots past the live length hold stale data (values zeroed in
+// registers, keys hidden), kept-list rows from the band on are hidden.
+//
+// The LDS destination of a copy goes in M0, written by the same inline
+// assembly statement as the load; nothing else in this kernel reads M0.  The
+// compiler does not count these loads, so the kernel waits for them itself
+// (vmcnt, oldest first) before the barrier that publishes a tile.
+#define DMS_LDS __attribute__((address_space(3)))
+#define DMS_CONST __attribute__((address_space(4)))
+
+constexpr int wait_vm(int n) { return 0x0F70 | (n & 15) | ((n >> 4) << 14); }
+constexpr int kWaitLgkm0 = 0xC07F;   // s_waitcnt lgkmcnt(0)
+
+__device__ inline uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((DMS_LDS const char*)p));
+}
+
+// 64 lanes x 16 bytes from g (per lane) to LDS m0 + 16 lane
+__device__ inline void lds_copy16(const char* g, uint32_t m0) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" : : "s"(m0), "v"(g) : "memory", "m0");
+}
+// 64 lanes x 4 bytes from g (per lane) to LDS m0 + 4 lane
+__device__ inline void lds_copy4(const char* g, uint32_t m0) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" : : "s"(m0), "v"(g) : "memory", "m0");
+}
+
+template <int D, int NQ>
+__global__ __launch_bounds__(256, 2) void prefill_copy_kernel(PrefillArgs a) {
+  constexpr int kBuf = 3;
+  constexpr int kTB = D * 128;
+  constexpr int kLoads = D / 32;   // 1 KB copies per wave and tile (four waves)
+  __shared__ __attribute__((aligned(16))) char tile_lds[kBuf][kTB];
+  __shared__ __attribute__((aligned(16))) uint32_t meta_lds[kBuf][64];   // rows 0..31, twice
+  if (load_status(a.status) != 0) return;
+  const int hh = blockIdx.y;
+  const int i = hh / a.H, h = hh % a.H;
+  const int tok0 = a.cu[i], C = a.cu[i + 1] - a.cu[i];
+  const int pb0 = blockIdx.x * a.PB;
+  if (pb0 >= C) return;
+  const int s = a.seq_ids[i];
+  const int sh = s * a.H + h;
+  const int p0 = a.pos[s];
+  const int L0 = a.len[sh];
+  const int t0 = p0 + pb0;
+  const int t1 = p0 + min(C, pb0 + a.PB);
+  // band: chunk tiles from the one holding max(p0, t0 - w + 1) up to t1
+  const int band_c0 = (max(0, t0 - a.w + 1 - p0) >> 5) << 5;
+  // kept chunk keys strictly before the band: prefix of the sorted list
+  const int32_t* lst = a.list + static_cast<size_t>(h) * a.total + tok0;
+  int lo_i = 0, hi_i = a.list_cnt[hh];
+  while (lo_i < hi_i) {
+    const int mid = (lo_i + hi_i) >> 1;
+    if (lst[mid] < band_c0) lo_i = mid + 1; else hi_i = mid;
+  }
+  const int n_pre = lo_i;
+  const int nc = (L0 + 31) >> 5;
+  const int np = (n_pre + 31) >> 5;
+  const int nb = (t1 - p0 - band_c0 + 31) >> 5;
+  const int ntiles = nc + np + nb;
+  const char* pre_tiles = a.tiles + ws_tile(a, 1, h, i, 0) * kTB;
+  const char* band_tiles = a.tiles + ws_tile(a, 0, h, i, band_c0 >> 5) * kTB;
+  const uint32_t* pre_meta = a.tmeta + ws_tile(a, 1, h, i, 0) * 32;
+  const uint32_t* band_meta = a.tmeta + ws_tile(a, 0, h, i, band_c0 >> 5) * 32;
+  // the page table does not change during the kernel: scalar loads
+  const DMS_CONST int32_t* pt = (const DMS_CONST int32_t*)(a.page_table + static_cast<size_t>(sh) * a.maxp);
+  const uint32_t* smeta = reinterpret_cast<const uint32_t*>(a.slot_meta + static_cast<size_t>(sh) * a.max_slots);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 15, G = lane >> 4;
+  const int Hq = a.H * a.g;
+  const int pcb = 16 / a.g;  // positions per column block
+
+  // ---- columns of this lane: (position, query head) in each column block
+  int tcol[NQ];
+  u32x4 qf[NQ][D / 32];
+#pragma unroll
+  for (int qb = 0; qb < NQ; ++qb) {
+    const int cb = wave * NQ + qb;
+    const int pl = r / a.g, qh = r % a.g;
+    const int t = t0 + cb * pcb + pl;
+    const bool ok = (pl < pcb) && (t < t1);
+    tcol[qb] = ok ? t : -1;
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    const char* qrow = reinterpret_cast<const char*>(
+        a.q + (static_cast<size_t>(tok0 + (t - p0)) * Hq + h * a.g + qh) * D);
+#pragma unroll
+    for (int s2 = 0; s2 < D / 32; ++s2)
+      qf[qb][s2] = ok ? *reinterpret_cast<const u32x4*>(qrow + (32 * s2 + 8 * G) * 2) : z;
+    // the borrowed decision neuron takes no part in attention (App. C)
+    if (a.zero_neuron && qh == 0 && G == 0) qf[qb][0][0] &= 0xFFFF0000u;
+  }
+  // the query loads complete before the first copy, so that no wait the
+  // compiler places for them can fall inside the loop
+  __builtin_amdgcn_s_waitcnt(wait_vm(0));
+
+  // ---- copies of tile k into buffer b: kLoads 1 KB blocks per wave; wave 0
+  // also copies the 32 key rows (both halves of the wave read the same rows)
+  int page = nc > 0 ? pt[0] : 0;   // page of the next pool tile to copy
+  auto issue = [&](int k, int b) {
+    const char* tile;
+    const uint32_t* mt;
+    if (k < nc) {
+      const int sb = 32 * k;
+      tile = a.pool + static_cast<size_t>(page) * a.page_bytes + static_cast<size_t>((sb & (a.P - 1)) >> 5) * kTB;
+      mt = smeta + sb;
+      if (k + 1 < nc) page = pt[(sb + 32) >> a.log2P];
+    } else if (k < nc + np) {
+      tile = pre_tiles + static_cast<size_t>(k - nc) * kTB;
+      mt = pre_meta + (k - nc) * 32;
+    } else {
+      tile = band_tiles + static_cast<size_t>(k - nc - np) * kTB;
+      mt = band_meta + (k - nc - np) * 32;
+    }
+    const uint32_t dst = lds_addr(tile_lds[b]);
+#pragma unroll
+    for (int m = 0; m < kLoads; ++m) {
+      const int blk = m * 4 + wave;
+      lds_copy16(tile + blk * 1024 + lane * 16, __builtin_amdgcn_readfirstlane(dst + blk * 1024));
+    }
+    if (wave == 0) lds_copy4(reinterpret_cast<const char*>(mt + (lane & 31)), lds_addr(meta_lds[b]));
+  };
+
+  // ---- accumulators
+  f32x4 o[NQ][D / 16];
+  float m_ref[NQ], l_run[NQ];
+#pragma unroll
+  for (int qb = 0; qb < NQ; ++qb) {
+#pragma unroll
+    for (int b = 0; b < D / 16; ++b) o[qb][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m_ref[qb] = kMInit;
+    l_run[qb] = 0.f;
+  }
+  const uint32_t lo_k = static_cast<uint32_t>(lane * 16);
+  const uint32_t lo_v = static_cast<uint32_t>(D * 64 + lane * 16);
+  const float thr = kRescale / a.scale_log2;   // rescale threshold in score units
+
+  // Pipeline: tile k's keys (and key rows) are in registers when iteration
+  // k starts; its value operands are read while its scores and weights are
+  // formed, and tile k + 1's keys while its PV MFMAs run.  The copy of tile
+  // k + 3 goes into tile k's buffer once every wave holds tile k's values.
+  for (int j = 0; j < min(kBuf, ntiles); ++j) issue(j, j);
+  Frag<D> f;
+  uint32_t mrow_l = 0;
+  u32x4 m0, m1;
+  // key operands and key rows of tile k (in LDS) into registers
+  auto read_keys = [&](int k) {
+    const char* tl = tile_lds[k % kBuf];
+    mrow_l = meta_lds[k % kBuf][lane];
+    m0 = *reinterpret_cast<const u32x4*>(&meta_lds[k % kBuf][8 * G]);
+    m1 = *reinterpret_cast<const u32x4*>(&meta_lds[k % kBuf][8 * G + 4]);
+#pragma unroll
+    for (int s2 = 0; s2 < D / 32; ++s2) {
+      f.ka[s2] = *reinterpret_cast<const u32x4*>(tl + lo_k + s2 * 2048);
+      f.kb[s2] = *reinterpret_cast<const u32x4*>(tl + lo_k + 1024 + s2 * 2048);
+    }
+  };
+  // wait until tile k has landed (the copies of up to `ahead` later tiles
+  // may still be in flight), then publish it to every wave
+  auto publish = [&](int ahead) {
+    if (ahead >= 2) {
+      if (wave == 0) __builtin_amdgcn_s_waitcnt(wait_vm(2 * (kLoads + 1)));
+      else __builtin_amdgcn_s_waitcnt(wait_vm(2 * kLoads));
+    } else if (ahead == 1) {
+      if (wave == 0) __builtin_amdgcn_s_waitcnt(wait_vm(kLoads + 1));
+      else __builtin_amdgcn_s_waitcnt(wait_vm(kLoads));
+    } else {
+      __builtin_amdgcn_s_waitcnt(wait_vm(0));
+    }
+    __syncthreads();
+  };
+  if (ntiles > 0) {
+    publish(min(2, ntiles - 1));
+    read_keys(0);
+  }
+  for (int k = 0; k < ntiles; ++k) {
+    // rows of the tile that hold keys: pool slots below the live length,
+    // kept-list rows before the band
+    const int rows = k < nc ? L0 - 32 * k : (k < nc + np ? n_pre - 32 * (k - nc) : 32);
+    // a key row needs the per-element mask iff some query t in [t0, t1)
+    // does not see it: no key, causal (position > t0) or flagged and
+    // expiring by t1 - 1
+    const uint32_t mrow = (lane & 31) < rows ? mrow_l : kNoKey;
+    const int kpr = static_cast<int>(mrow & ~kFlagBit);
+    const bool need = mrow == kNoKey || kpr > t0 || ((mrow & kFlagBit) && kpr + a.w <= t1 - 1);
+    const bool masked = __builtin_amdgcn_ballot_w64(need) != 0;
+    int kp[8], kx[8];   // key position and expiry (first query that no longer sees it)
+    if (masked) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t km = 8 * G + j < rows ? (j < 4 ? m0[j] : m1[j - 4]) : kNoKey;
+        kp[j] = static_cast<int>(km & ~kFlagBit);
+        kx[j] = (km & kFlagBit) ? kp[j] + a.w : 0x7FFFFFFF;
+      }
+    }
+    // scores of every column block
+    f32x4 s0[NQ], s1[NQ];
+#pragma unroll
+    for (int qb = 0; qb < NQ; ++qb) {
+      s0[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      s1[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s2 = 0; s2 < D / 32; ++s2) {
+        s0[qb] = mfma_bf16(f.ka[s2], qf[qb][s2], s0[qb]);
+        s1[qb] = mfma_bf16(f.kb[s2], qf[qb][s2], s1[qb]);
+      }
+    }
+    // value operands of tile k
+    const char* tl = tile_lds[k % kBuf];
+#pragma unroll
+    for (int b = 0; b < D / 16; ++b) f.vt[b] = *reinterpret_cast<const u32x4*>(tl + lo_v + b * 1024);
+    // weights
+    float vsc[8];   // (FP8 only)
+    u32x4 pu[NQ];
+#pragma unroll
+    for (int qb = 0; qb < NQ; ++qb)
+      pu[qb] = col_weights<D, false>(s0[qb], s1[qb], vsc, masked, kp, kx, tcol[qb], o[qb], m_ref[qb],
+                                     l_run[qb], thr, a.scale_log2);
+    if (rows < 32) {
+      // stale pool slots: value elements of rows 8 G + e >= rows are zeroed
+      // (element e of a value piece is key row 8 G + e)
+      u32x4 keep;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        keep[e] = (8 * G + 2 * e < rows ? 0x0000FFFFu : 0u) | (8 * G + 2 * e + 1 < rows ? 0xFFFF0000u : 0u);
+#pragma unroll
+      for (int b = 0; b < D / 16; ++b) f.vt[b] &= keep;
+    }
+    if (k + 1 < ntiles) {
+      // every wave holds tile k's operands (the barrier waits for the reads);
+      // tile k + 1 is in LDS.  Its keys replace tile k's in registers.
+      publish(min(1, ntiles - 2 - k));
+      read_keys(k + 1);
+      if (k + 3 < ntiles) issue(k + 3, k % kBuf);
+    } else {
+      // (the value reads complete on this path too, so that the PV MFMAs
+      // below wait for nothing on the other)
+      __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    }
+#pragma unroll
+    for (int qb = 0; qb < NQ; ++qb)
+#pragma unroll
+      for (int b = 0; b < D / 16; ++b) o[qb][b] = mfma_bf16(f.vt[b], pu[qb], o[qb][b]);
   }
 
   // ---- outputs
@@ -626,6 +933,7 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   a.list = reinterpret_cast<int32_t*>(w + lo.ws_pf_meta);
   a.list_cnt = reinterpret_cast<int32_t*>(w + lo.ws_pf_cum);
   a.tiles = w + lo.ws_pf_tiles;
+  a.tmeta = reinterpret_cast<uint32_t*>(w + lo.ws_pf_tmeta);
   a.tph = lo.pf_tiles_per_head;
   a.immediate = c.eviction == DMS_EVICT_IMMEDIATE;
   a.zero_neuron = c.decision_source == DMS_DECIDE_QUERY;
@@ -655,7 +963,10 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 grid((max_len + a.PB - 1) / a.PB, NH);
-  hipLaunchKernelGGL((prefill_kernel<D, kNQ, FP8>), grid, dim3(attn_threads<D, FP8>()), 0, st, a);
+  if (!FP8 && !a.immediate)
+    hipLaunchKernelGGL((prefill_copy_kernel<D, kNQ>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((prefill_kernel<D, kNQ, FP8>), grid, dim3(attn_threads<D, FP8>()), 0, st, a);
   e = hipGetLastError();
   if (ev_stop) (void)hipEventRecord(ev_stop, st);
   return e;
@@ -992,6 +1303,7 @@ hipError_t launch_prefill_mla(const dms_config& c, const Layout& lo, void* meta,
   a.list = reinterpret_cast<int32_t*>(w + lo.ws_pf_meta);
   a.list_cnt = reinterpret_cast<int32_t*>(w + lo.ws_pf_cum);
   a.tiles = w + lo.ws_pf_tiles;
+  a.tmeta = reinterpret_cast<uint32_t*>(w + lo.ws_pf_tmeta);
   a.tph = lo.pf_tiles_per_head;
   a.immediate = c.eviction == DMS_EVICT_IMMEDIATE;
   a.zero_neuron = 0;

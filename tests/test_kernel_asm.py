@@ -1,9 +1,9 @@
-"""Checks on the gfx950 assembly of the latent-attention kernel (CPU only:
-hipcc cross-compiles).
+"""Checks on the gfx950 assembly of the kernels that copy tiles global -> LDS
+(latent-attention decode, bf16 prefill; CPU only: hipcc cross-compiles).
 
-The kernel copies tiles into LDS with global->LDS loads written as inline
+These kernels copy tiles into LDS with global->LDS loads written as inline
 assembly, each preceded by its own write of M0 (the LDS destination); the
-compiler does not preserve M0 across inline assembly, so the kernel relies on
+compiler does not preserve M0 across inline assembly, so the kernels rely on
 no other instruction reading M0.  The test pins that: every instruction that
 names M0 is one of those writes, immediately followed by its load."""
 import os
@@ -24,11 +24,13 @@ def _hipcc():
     return exe
 
 
-def test_m0_is_only_the_lds_copy_destination(tmp_path):
+@pytest.mark.parametrize("src", ["dms_mla.hip", "dms_prefill.hip"])
+def test_m0_is_only_the_lds_copy_destination(tmp_path, src):
     from paper_2506_05345_amd import build
-    out = tmp_path / "mla.s"
+    out = tmp_path / (src + ".s")
     cmd = [_hipcc(), "-O3", "-std=c++17", f"--offload-arch={build.ARCH}", *build.GPU_FLAGS,
-           "-munsafe-fp-atomics", "--cuda-device-only", "-S", os.path.join(CSRC, "dms_mla.hip"), "-o", str(out)]
+           *build.PER_SOURCE.get(src, []), "-munsafe-fp-atomics", "--cuda-device-only", "-S",
+           os.path.join(CSRC, src), "-o", str(out)]
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)
     assert r.returncode == 0, r.stdout.decode(errors="replace")
     lines = [l.split(";")[0].strip() for l in out.read_text().splitlines()]
@@ -37,7 +39,7 @@ def test_m0_is_only_the_lds_copy_destination(tmp_path):
     for i, l in enumerate(lines):
         if re.search(r"\bm0\b", l):
             assert re.fullmatch(r"s_mov_b32 m0, s\d+", l), l
-            assert lines[i + 1].startswith("global_load_lds_dwordx4"), (l, lines[i + 1])
+            assert lines[i + 1].startswith("global_load_lds_dword"), (l, lines[i + 1])
             copies += 1
     assert copies > 0
     # and every global->LDS load has its own M0 write just before it
