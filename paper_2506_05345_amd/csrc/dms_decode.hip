@@ -1081,28 +1081,39 @@ __device__ __forceinline__ void write_state(const FusedArgs& f, const int4* s_de
   }
 }
 
-// Calls whose every head has at most kHeadBlockTiles tiles run one workgroup
-// per head: its four waves take contiguous quarters of the head's tiles and
-// fold their results through LDS, so no split-K partial goes through memory
-// and no arrival counter is taken.  Measured at a 1.5B-shaped step (64 heads
-// of ~40 tiles spread over ~320 waves) the global merges -- partial stores,
-// the arrival atomic, then the merging wave's coherent loads -- held the
-// launch for up to 18 us of its 36.
+// Calls whose every head has at most kHeadBlockTiles tiles run S workgroups
+// per head (S = 1 .. kHeadBlockParts, as many as the launch has workgroups
+// for): workgroup s takes the s-th of S contiguous parts of the head's
+// tiles, its four waves quarters of that part, and the waves fold their
+// results through LDS.  With S = 1 the fold writes the output: no split-K
+// partial goes through memory and no arrival counter is taken.  Measured at
+// a 1.5B-shaped step (64 heads of ~40 tiles spread over ~320 waves) the
+// per-wave global merges -- partial stores, the arrival atomic, then the
+// merging wave's coherent loads -- held the launch for up to 18 us of its
+// 36.  With S > 1 each workgroup publishes one folded partial and the last
+// of the S merges them (at most four partials, one coherent round trip).
 constexpr int kHeadBlockTiles = 64;
+constexpr int kHeadBlockParts = 4;
 
 template <int D, bool FP8>
-__device__ __forceinline__ void decode_head_block(const LdsPlan& plan, int hh, const int32_t* __restrict__ page_table,
+__device__ __forceinline__ void decode_head_block(const LdsPlan& plan, int hh, int S, int s,
+                                                  const int32_t* __restrict__ page_table,
                                                   char* __restrict__ pool, const uint16_t* __restrict__ q,
                                                   const uint16_t* __restrict__ k_in, const uint16_t* __restrict__ v_in,
-                                                  float* __restrict__ out, const DecodeParams& a,
-                                                  f32x4 (*fold)[D / 16][64], float2 (*fold_ml)[kMaxGroup]) {
+                                                  int32_t* __restrict__ head_cnt, float2* __restrict__ part_ml,
+                                                  float* __restrict__ part_acc, float* __restrict__ out,
+                                                  const DecodeParams& a, f32x4 (*fold)[D / 16][64],
+                                                  float2 (*fold_ml)[kMaxGroup]) {
   const int lane = threadIdx.x & 63;
   const int r = lane & 15, G = lane >> 4;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c0 = plan.cum_at(hh), c1 = plan.cum_at(hh + 1);
   const int n = c1 - c0;
   const HeadDesc d = plan.head(hh);
-  const int t_lo = wid * n / kWavesPerBlock, t_hi = (wid + 1) * n / kWavesPerBlock;
+  // this workgroup's part of the head's tiles, then this wave's quarter of it
+  const int p_lo = s * n / S, p_hi = (s + 1) * n / S;
+  const int t_lo = p_lo + wid * (p_hi - p_lo) / kWavesPerBlock;
+  const int t_hi = p_lo + (wid + 1) * (p_hi - p_lo) / kWavesPerBlock;
   Acc<D> acc;
   if (t_lo < t_hi) {
     stream_segment<D, FP8>(acc, hh, d, t_lo, t_hi, t_hi == n, page_table, nullptr, pool, q, k_in, v_in, a);
@@ -1129,20 +1140,61 @@ __device__ __forceinline__ void decode_head_block(const LdsPlan& plan, int hh, c
   float den = 0.f, wj[kWavesPerBlock];
 #pragma unroll
   for (int j = 0; j < kWavesPerBlock; ++j) {
-    wj[j] = __builtin_amdgcn_exp2f(mj[j] - M);   // 0 for a wave without tiles (m = -inf)
+    // 0 for a wave without tiles (m = -inf); a part without tiles (S > 1,
+    // fewer tiles than parts) folds to m = -inf, l = 0, accumulators 0
+    wj[j] = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mj[j] - M);
     den += wj[j] * fold_ml[j][r].y;
   }
   constexpr int kBlocks = D / 16 / kWavesPerBlock;
+  if (S == 1) {
+    if (r < a.g) {
+      const float inv = 1.0f / den;
+      float* o = out + (static_cast<size_t>(hh) * a.g + r) * D + 4 * G;
+#pragma unroll
+      for (int i = 0; i < kBlocks; ++i) {
+        const int b = wid * kBlocks + i;
+        f32x4 num = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < kWavesPerBlock; ++j) num += wj[j] * fold[j][b][lane];
+        *reinterpret_cast<f32x4*>(o + 16 * b) = num * inv;
+      }
+    }
+    return;
+  }
+  // Part s of S: publish the folded partial (max, denominator, unnormalized
+  // accumulators) at index hh * S + s with agent-coherent stores; once every
+  // wave's stores are complete, count the part in; the workgroup that
+  // completes the count merges the S partials.
+  const size_t pid = static_cast<size_t>(hh) * S + s;
+  const __amdgpu_buffer_rsrc_t acc_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      part_acc, static_cast<short>(0), a.part_acc_bytes, kBufferDword3);
   if (r < a.g) {
-    const float inv = 1.0f / den;
-    float* o = out + (static_cast<size_t>(hh) * a.g + r) * D + 4 * G;
+    if (wid == 0 && G == 0) {
+      float* ml = reinterpret_cast<float*>(part_ml + pid * kMaxGroup + r);
+      store_coherent(ml, M);
+      store_coherent(ml + 1, den);
+    }
+    const uint32_t o = static_cast<uint32_t>(((pid * a.g + r) * D + 4 * G) * 4);
 #pragma unroll
     for (int i = 0; i < kBlocks; ++i) {
       const int b = wid * kBlocks + i;
       f32x4 num = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int j = 0; j < kWavesPerBlock; ++j) num += wj[j] * fold[j][b][lane];
-      *reinterpret_cast<f32x4*>(o + 16 * b) = num * inv;
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, num), acc_rsrc, o + 64 * b, 0,
+                                             kCachePolicySc1);
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  __syncthreads();
+  if (wid == 0) {
+    int prev = 0;
+    if (lane == 0) prev = atomicAdd(&head_cnt[hh], 1);
+    prev = __shfl(prev, 0, 64);
+    if (prev == S - 1) {
+      // partial u of the head sits at index (wf + u) + hh = hh * S + u
+      merge_head_small<D>(part_ml, acc_rsrc, (1 << S) - 1, out, hh * S - hh, S, hh, a.g, lane);
+      if (lane == 0) __hip_atomic_store(&head_cnt[hh], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -1181,9 +1233,11 @@ __global__ __launch_bounds__(256, 1) void decode_step_kernel(
   for (int hh = threadIdx.x; hh < a.NH; hh += blockDim.x) wide |= s_cum[hh + 1] - s_cum[hh] > kHeadBlockTiles;
   wide = __syncthreads_or(wide);
   if (!wide && a.NH <= nb) {
-    if (static_cast<int>(blockIdx.x) < a.NH)
-      decode_head_block<D, FP8>(LdsPlan{s_cum, s_desc, T, 1, a.NH}, blockIdx.x, f.st.page_table, pool, q, k_in,
-                                v_in, out, a, s_fold, s_fold_ml);
+    const int S = min(kHeadBlockParts, nb / a.NH);
+    if (static_cast<int>(blockIdx.x) < a.NH * S)
+      decode_head_block<D, FP8>(LdsPlan{s_cum, s_desc, T, 1, a.NH}, blockIdx.x / S, S, blockIdx.x % S,
+                                f.st.page_table, pool, q, k_in, v_in, head_cnt, part_ml, part_acc, out, a, s_fold,
+                                s_fold_ml);
   } else {
     const int W = min(a.W, max(nb, (T + kFuseMinTiles - 1) / kFuseMinTiles));
     const int lw = W == a.W ? blockIdx.x * kWavesPerBlock + wid : wid * nb + blockIdx.x;
