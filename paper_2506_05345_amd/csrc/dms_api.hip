@@ -389,15 +389,16 @@ int decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, cons
   hipStream_t st = as_stream(stream);
   if (c.cfg.quest_page_budget > 0) {
     // page retrieval: plan the append; write K / V, recompute the written
-    // pages' bounds and select every head's pages (one launch); then plan
-    // and decode over the selection
+    // pages' bounds, select every head's pages and (up to 1024 heads) plan
+    // the decode over the selection, in one launch; then decode
     hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev,
                                     from_q ? nullptr : flags_dev, from_q ? q_dev : nullptr,
                                     decisions_out_dev, true, 0, nullptr, st);
+    bool planned = false;
     if (e == hipSuccess)
       e = dms::launch_quest_append_select(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, k_dev,
-                                          v_dev, st);
-    if (e == hipSuccess)
+                                          v_dev, c.decode_waves, out_dev, &planned, st);
+    if (e == hipSuccess && !planned)
       e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, nullptr, nullptr, nullptr,
                            false, c.decode_waves, out_dev, st, quest_lengths(c));
     hipEvent_t e0, e1;

@@ -230,10 +230,13 @@ hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* 
 // Quest: an append's K / V written and the written pages' bounds recomputed.
 hipError_t launch_quest_append(const dms_config& c, const Layout& lo, void* meta, void* ws,
                                void* pool, int layer, int n, const void* k, const void* v, hipStream_t st);
-// Quest, decode step: the append's K / V and bounds, then every head's selection.
+// Quest, decode step: the append's K / V and bounds, then every head's
+// selection; for calls of up to 1024 heads the launch also writes the decode
+// plan over the attended lengths for `waves` decode waves (*planned set), as
+// launch_plan would with those lengths.
 hipError_t launch_quest_append_select(const dms_config& c, const Layout& lo, void* meta, void* ws,
                                       void* pool, int layer, int n, const void* q, const void* k,
-                                      const void* v, hipStream_t st);
+                                      const void* v, int waves, float* out, bool* planned, hipStream_t st);
 hipError_t launch_quest_bounds(const dms_config& c, const Layout& lo, void* meta, void* ws,
                                void* pool, int layer, int n, bool all_pages, const int32_t* seq_ids,
                                hipStream_t st);
