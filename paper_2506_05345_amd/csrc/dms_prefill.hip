@@ -823,18 +823,26 @@ __global__ __launch_bounds__(256, 2) void prefill_copy_kernel(PrefillArgs a) {
     // rows of the tile that hold keys: pool slots below the live length,
     // kept-list rows before the band
     const int rows = k < nc ? L0 - 32 * k : (k < nc + np ? n_pre - 32 * (k - nc) : 32);
+    if (rows < 32) {
+      // rows past the source's end hold no key
+      if ((lane & 31) >= rows) mrow_l = kNoKey;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (8 * G + j >= rows) m0[j] = kNoKey;
+        if (8 * G + 4 + j >= rows) m1[j] = kNoKey;
+      }
+    }
     // a key row needs the per-element mask iff some query t in [t0, t1)
     // does not see it: no key, causal (position > t0) or flagged and
     // expiring by t1 - 1
-    const uint32_t mrow = (lane & 31) < rows ? mrow_l : kNoKey;
-    const int kpr = static_cast<int>(mrow & ~kFlagBit);
-    const bool need = mrow == kNoKey || kpr > t0 || ((mrow & kFlagBit) && kpr + a.w <= t1 - 1);
+    const int kpr = static_cast<int>(mrow_l & ~kFlagBit);
+    const bool need = mrow_l == kNoKey || kpr > t0 || ((mrow_l & kFlagBit) && kpr + a.w <= t1 - 1);
     const bool masked = __builtin_amdgcn_ballot_w64(need) != 0;
     int kp[8], kx[8];   // key position and expiry (first query that no longer sees it)
     if (masked) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const uint32_t km = 8 * G + j < rows ? (j < 4 ? m0[j] : m1[j - 4]) : kNoKey;
+        const uint32_t km = j < 4 ? m0[j] : m1[j - 4];
         kp[j] = static_cast<int>(km & ~kFlagBit);
         kx[j] = (km & kFlagBit) ? kp[j] + a.w : 0x7FFFFFFF;
       }
