@@ -52,7 +52,6 @@ struct QuestArgs {
   int32_t* wave_bounds;     // [W + 1]
   int4* wave_desc;          // [2W]
   int4* head_waves;         // [NH]
-  int32_t* head_cnt;        // [NH] split-head arrival counters, cleared
   float* out;               // [NH][gD] rows of heads that attend nothing are zeroed
   int W, gD, plan_tail;
   size_t page_bytes;
@@ -201,13 +200,15 @@ constexpr int kPlanMaxHeads = kPlanPer * kQThreads;
 __device__ void plan_attended(const QuestArgs& a, int NH) {
   __shared__ int lds[17];
   const int tid = threadIdx.x;
-  int len[kPlanPer], mine = 0;
+  int len[kPlanPer], shd[kPlanPer], mine = 0;
 #pragma unroll
   for (int k = 0; k < kPlanPer; ++k) {
     const int hh = kPlanPer * tid + k;
     len[k] = hh < NH ? __hip_atomic_load(a.qlen + hh, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
-    mine += (len[k] + kTile - 1) / kTile;
+    shd[k] = hh < NH ? a.desc[hh].y : 0;   // state head (the append plan's descriptor)
   }
+#pragma unroll
+  for (int k = 0; k < kPlanPer; ++k) mine += (len[k] + kTile - 1) / kTile;
   int total = 0;
   int c = block_exclusive_scan(mine, lds, &total);
   const int64_t T = total, W = a.W;
@@ -220,10 +221,9 @@ __device__ void plan_attended(const QuestArgs& a, int NH) {
     if (hh >= NH) break;
     const int c0 = c, c1 = c + (len[k] + kTile - 1) / kTile;
     c = c1;
-    const int4 d = make_int4(len[k], a.desc[hh].y, -1, 0);
+    const int4 d = make_int4(len[k], shd[k], -1, 0);
     a.plan_desc[hh] = d;
     a.cum_tiles[hh + 1] = c1;
-    a.head_cnt[hh] = 0;
     if (len[k] == 0)
       for (int e = 0; e < a.gD; ++e) a.out[static_cast<size_t>(hh) * a.gD + e] = 0.f;
     if (c1 > c0 && total > 0) {
@@ -489,7 +489,6 @@ hipError_t launch_quest_append_select(const dms_config& c, const Layout& lo, voi
   a.wave_bounds = reinterpret_cast<int32_t*>(w + lo.ws_wave_bounds);
   a.wave_desc = reinterpret_cast<int4*>(w + lo.ws_wave_desc);
   a.head_waves = reinterpret_cast<int4*>(w + lo.ws_head_waves);
-  a.head_cnt = reinterpret_cast<int32_t*>(w + lo.ws_head_cnt);
   a.out = out;
   a.W = waves;
   a.gD = c.group_size * c.head_dim;

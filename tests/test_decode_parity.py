@@ -171,6 +171,30 @@ def test_many_heads_multi_pass_planner():
     cache.close()
 
 
+@pytest.mark.parametrize("nseq", [3, 20, 25])
+def test_short_heads_split_over_workgroups(nseq):
+    """Small calls whose heads all fit one workgroup's share: 12, 80 and 100
+    call heads are split over 4, 3 and 2 workgroups per head (one folded
+    partial each, merged by the last); heads of 1-3 tiles leave parts without
+    tiles."""
+    H, g, d, w, P = 4, 2, 64, 16, 32
+    rng = np.random.default_rng(90 + nseq)
+    seqs = [int(s) for s in rng.permutation(nseq)]
+    lens = {s: int(rng.integers(1, 600)) for s in seqs}
+    for s in seqs[:3]:
+        lens[s] = int(rng.integers(1, 90))   # one to three tiles
+    dms, cfg, cache = _mk(dict(num_layers=1, max_seqs=nseq, num_kv_heads=H, group_size=g,
+                               head_dim=d, window=w, page_size=P, num_pages=4000,
+                               max_pages_per_head=64, max_chunk_tokens=nseq * 600))
+    inp = {s: SeqInputs(91, 0, s, lens[s] + 8, H, g, d, 0.7) for s in seqs}
+    orc = _oracle_for(cfg)
+    _append_chunks(dms, cache, orc, seqs, inp, {s: 0 for s in seqs}, lens, 600)
+    compare_state(cache.export(0), orc, seqs)
+    _decode_steps(dms, cache, orc, seqs, inp, lens, 8, g, check_every=3, dense_check=False)
+    compare_pool(cache, 0, cache.export(0), seqs, inp)
+    cache.close()
+
+
 def test_decode_from_empty_cache_token_by_token():
     """Every token through dms_decode_step from position 0 (first steps have a
     single visible key, the output is that value exactly up to rounding)."""
