@@ -389,23 +389,27 @@ int decode_step(dms_ctx* ctx, int layer, int n, const int32_t* seq_ids_dev, cons
   hipStream_t st = as_stream(stream);
   if (c.cfg.quest_page_budget > 0) {
     // page retrieval: plan the append; write K / V, recompute the written
-    // pages' bounds, select every head's pages and (up to 1024 heads) plan
-    // the decode over the selection, in one launch; then decode
+    // pages' bounds and select every head's pages (one launch); then decode
+    // over the selection, planning its tiles inside the decode launch (up to
+    // 1024 heads) or with the planner
     hipError_t e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev,
                                     from_q ? nullptr : flags_dev, from_q ? q_dev : nullptr,
                                     decisions_out_dev, true, 0, nullptr, st);
-    bool planned = false;
     if (e == hipSuccess)
       e = dms::launch_quest_append_select(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, k_dev,
-                                          v_dev, c.decode_waves, out_dev, &planned, st);
-    if (e == hipSuccess && !planned)
+                                          v_dev, st);
+    const bool in_launch = n * c.cfg.num_kv_heads <= dms::decode_attended_max_heads();
+    if (e == hipSuccess && !in_launch)
       e = dms::launch_plan(c.cfg, c.lo, c.meta, c.ws, layer, n, seq_ids_dev, nullptr, nullptr, nullptr,
                            false, c.decode_waves, out_dev, st, quest_lengths(c));
     hipEvent_t e0, e1;
     next_events(ctx->c, DMS_PROFILE_DECODE, &e0, &e1);
     if (e == hipSuccess)
-      e = dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, nullptr,
-                             nullptr, out_dev, c.decode_waves, st, e0, e1, quest_phys_pages(c));
+      e = in_launch ? dms::launch_decode_attended(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev,
+                                                  out_dev, c.decode_waves, st, e0, e1, quest_phys_pages(c),
+                                                  quest_lengths(c))
+                    : dms::launch_decode(c.cfg, c.lo, c.meta, c.ws, c.pools[layer], layer, n, q_dev, nullptr,
+                                         nullptr, out_dev, c.decode_waves, st, e0, e1, quest_phys_pages(c));
     return hip_rc(e);
   }
   if (dms::decode_step_fusable(c.cfg, n)) {

@@ -54,8 +54,7 @@ __global__ void init_state_kernel(InitArgs a) {
       *reinterpret_cast<int32_t*>(a.meta) = 0;  // status
       a.ck_err[0] = 0;
       a.ck_err[1] = 0;
-      a.plan_ctr[0] = 0;   // fused decode: workgroups that read the state
-      a.plan_ctr[1] = 0;   // page retrieval: heads whose selection is done
+      a.plan_ctr[0] = 0;
     }
   }
 }

@@ -230,13 +230,18 @@ hipError_t launch_plan(const dms_config& c, const Layout& lo, void* meta, void* 
 // Quest: an append's K / V written and the written pages' bounds recomputed.
 hipError_t launch_quest_append(const dms_config& c, const Layout& lo, void* meta, void* ws,
                                void* pool, int layer, int n, const void* k, const void* v, hipStream_t st);
-// Quest, decode step: the append's K / V and bounds, then every head's
-// selection; for calls of up to 1024 heads the launch also writes the decode
-// plan over the attended lengths for `waves` decode waves (*planned set), as
-// launch_plan would with those lengths.
+// Quest, decode step: the append's K / V and bounds, then every head's selection.
 hipError_t launch_quest_append_select(const dms_config& c, const Layout& lo, void* meta, void* ws,
                                       void* pool, int layer, int n, const void* q, const void* k,
-                                      const void* v, int waves, float* out, bool* planned, hipStream_t st);
+                                      const void* v, hipStream_t st);
+// Page retrieval, calls of up to decode_attended_max_heads() heads: decode over
+// the selected pages, every workgroup planning the tiles over the attended
+// lengths (qlen [n * Hkv]) in LDS (no planner launch).
+int decode_attended_max_heads();
+hipError_t launch_decode_attended(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
+                                  int layer, int n, const void* q, float* out, int waves, hipStream_t st,
+                                  hipEvent_t ev_start, hipEvent_t ev_stop, const int32_t* qpage,
+                                  const int32_t* qlen);
 hipError_t launch_quest_bounds(const dms_config& c, const Layout& lo, void* meta, void* ws,
                                void* pool, int layer, int n, bool all_pages, const int32_t* seq_ids,
                                hipStream_t st);

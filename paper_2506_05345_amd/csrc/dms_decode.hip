@@ -1250,6 +1250,56 @@ __global__ __launch_bounds__(256, 1) void decode_step_kernel(
   if (wid == 0 && __shfl(ticket, 0, 64) == nb - 1) write_state(f, s_desc, s_aux, new_top, threadIdx.x & 63);
 }
 
+// Decode over Quest's selection (page retrieval) with the work split planned
+// in every workgroup: the tile prefix sums over the call's attended lengths
+// (qlen) and the head descriptors go to LDS, then the waves decode as with
+// the planner's split.  Replaces the planner launch between the selection and
+// the decode for calls of up to kFuseMaxHeads heads.
+template <int D, bool FP8>
+__global__ __launch_bounds__(256, 1) void decode_attended_kernel(
+    const int32_t* __restrict__ status, const HeadDesc* __restrict__ desc, const int32_t* __restrict__ qlen,
+    int32_t* __restrict__ head_cnt, const int32_t* __restrict__ page_table, const int32_t* __restrict__ qpage,
+    char* __restrict__ pool, const uint16_t* __restrict__ q, float2* __restrict__ part_ml,
+    float* __restrict__ part_acc, float* __restrict__ out, DecodeParams a) {
+  __shared__ float merge_wts[kWavesPerBlock][kMergeBatch][kMaxGroup];
+  __shared__ int s_cum[kFuseMaxHeads + 1];
+  __shared__ int4 s_desc[kFuseMaxHeads];
+  __shared__ int s_scan[17];
+  if (load_status(status) != 0) return;
+  constexpr int kPer = kFuseMaxHeads / 256;   // heads per thread
+  const int tid = threadIdx.x;
+  const int NH = a.NH;
+  int len[kPer], sh[kPer], mine = 0;
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int hh = kPer * tid + k;
+    len[k] = hh < NH ? qlen[hh] : 0;
+    sh[k] = hh < NH ? desc[hh].y : 0;   // state head (the append plan's descriptor)
+  }
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) mine += (len[k] + kTile - 1) / kTile;
+  int total = 0;
+  int c = block_exclusive_scan(mine, s_scan, &total);
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int hh = kPer * tid + k;
+    if (hh < NH) {
+      c += (len[k] + kTile - 1) / kTile;
+      s_cum[hh + 1] = c;
+      s_desc[hh] = make_int4(len[k], sh[k], -1, -1);   // no appended slot, no pending page
+      // a head that attends nothing (never after an append) gets zero rows
+      if (len[k] == 0 && blockIdx.x == 0)
+        for (int e = 0; e < a.g * D; ++e) out[static_cast<size_t>(hh) * a.g * D + e] = 0.f;
+    }
+  }
+  if (tid == 0) s_cum[0] = 0;
+  __syncthreads();
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const LdsPlan plan{s_cum, s_desc, __builtin_amdgcn_readfirstlane(total), a.W, NH};
+  decode_wave<D, FP8>(plan, blockIdx.x * kWavesPerBlock + wid, a.W, head_cnt, page_table, qpage, pool, q,
+                      nullptr, nullptr, part_ml, part_acc, out, a, merge_wts[wid]);
+}
+
 DecodeParams decode_params(const dms_config& c, const Layout& lo, int D, int n, int waves) {
   DecodeParams a;
   a.page_bytes = lo.page_bytes;
@@ -1349,6 +1399,44 @@ hipError_t launch_decode(const dms_config& c, const Layout& lo, void* meta, void
                                          ev_start, ev_stop, qpage)
              : launch_decode_d<64, false>(c, lo, meta, ws, pool, layer, n, q, k, v, out, waves, st,
                                           ev_start, ev_stop, qpage);
+}
+
+template <int D, bool FP8>
+hipError_t launch_decode_attended_d(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
+                                    int layer, int n, const void* q, float* out, int waves, hipStream_t st,
+                                    hipEvent_t ev_start, hipEvent_t ev_stop, const int32_t* qpage,
+                                    const int32_t* qlen) {
+  char* w = static_cast<char*>(ws);
+  const DecodeParams a = decode_params(c, lo, D, n, waves);
+  if (ev_start) (void)hipEventRecord(ev_start, st);
+  hipLaunchKernelGGL((decode_attended_kernel<D, FP8>), dim3(waves / kWavesPerBlock), dim3(256), 0, st,
+                     reinterpret_cast<const int32_t*>(static_cast<char*>(meta) + lo.status),
+                     reinterpret_cast<const HeadDesc*>(w + lo.ws_head_desc), qlen,
+                     reinterpret_cast<int32_t*>(w + lo.ws_head_cnt), layer_state(lo, meta, layer).page_table, qpage,
+                     static_cast<char*>(pool), static_cast<const uint16_t*>(q),
+                     reinterpret_cast<float2*>(w + lo.ws_part_ml), reinterpret_cast<float*>(w + lo.ws_part_acc),
+                     out, a);
+  hipError_t e = hipGetLastError();
+  if (ev_stop) (void)hipEventRecord(ev_stop, st);
+  return e;
+}
+
+int decode_attended_max_heads() { return kFuseMaxHeads; }
+
+hipError_t launch_decode_attended(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
+                                  int layer, int n, const void* q, float* out, int waves, hipStream_t st,
+                                  hipEvent_t ev_start, hipEvent_t ev_stop, const int32_t* qpage,
+                                  const int32_t* qlen) {
+  const bool fp8 = c.kv_format == DMS_KV_FP8;
+  if (c.head_dim == 128)
+    return fp8 ? launch_decode_attended_d<128, true>(c, lo, meta, ws, pool, layer, n, q, out, waves, st, ev_start,
+                                                     ev_stop, qpage, qlen)
+               : launch_decode_attended_d<128, false>(c, lo, meta, ws, pool, layer, n, q, out, waves, st, ev_start,
+                                                      ev_stop, qpage, qlen);
+  return fp8 ? launch_decode_attended_d<64, true>(c, lo, meta, ws, pool, layer, n, q, out, waves, st, ev_start,
+                                                  ev_stop, qpage, qlen)
+             : launch_decode_attended_d<64, false>(c, lo, meta, ws, pool, layer, n, q, out, waves, st, ev_start,
+                                                   ev_stop, qpage, qlen);
 }
 
 // Calls of at most this many KV heads take the fused launch.  Measured on

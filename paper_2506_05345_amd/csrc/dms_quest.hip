@@ -44,16 +44,6 @@ struct QuestArgs {
   int32_t* sel;             // [NH][B] attended page-table indices, ascending
   int32_t* qpage;           // [NH][B] their physical pages (what decode reads)
   int32_t* qlen;            // [NH] live slots in the attended pages
-  // decode plan over the attended lengths, built by the last block of the
-  // append + select launch (plan_tail); the same arrays the planner writes
-  int32_t* done;            // blocks of the launch that finished their selection
-  HeadDesc* plan_desc;      // [NH] (attended length, state head, -1, 0)
-  int32_t* cum_tiles;       // [NH + 1]
-  int32_t* wave_bounds;     // [W + 1]
-  int4* wave_desc;          // [2W]
-  int4* head_waves;         // [NH]
-  float* out;               // [NH][gD] rows of heads that attend nothing are zeroed
-  int W, gD, plan_tail;
   size_t page_bytes;
   int n, H, g, D, P, maxp, B, fp8, zero_neuron, all_pages;
   int sort_pages;           // power of two >= maxp: sort keys in the select kernel's LDS
@@ -61,12 +51,6 @@ struct QuestArgs {
 
 __device__ inline int load_status(const int32_t* status) {
   return __atomic_load_n(status, __ATOMIC_RELAXED);
-}
-
-// Attended lengths are stored and read at device coherence: the block that
-// plans reads every other block's length within the same launch.
-__device__ inline void put_qlen(const QuestArgs& a, int hh, int L) {
-  __hip_atomic_store(a.qlen + hh, L, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ inline uint16_t f32_to_bf16_exact(float x) {
@@ -190,83 +174,14 @@ __global__ __launch_bounds__(kQThreads) void quest_append_kernel(QuestArgs a) {
 // A decode step's append and page selection for one head per block: the
 // selection reads every page's bounds, the written page's from this block's
 // own stores (visible after the barrier).
-// Decode plan over the attended lengths (what the planner writes for a call
-// without append, lengths overridden): tile prefix sums, every decode wave's
-// equal share of the flat tile list with its first segment, and every
-// head's wave span.  One block; kPlanPer heads per thread.
-constexpr int kPlanPer = 4;
-constexpr int kPlanMaxHeads = kPlanPer * kQThreads;
-
-__device__ void plan_attended(const QuestArgs& a, int NH) {
-  __shared__ int lds[17];
-  const int tid = threadIdx.x;
-  int len[kPlanPer], shd[kPlanPer], mine = 0;
-#pragma unroll
-  for (int k = 0; k < kPlanPer; ++k) {
-    const int hh = kPlanPer * tid + k;
-    len[k] = hh < NH ? __hip_atomic_load(a.qlen + hh, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
-    shd[k] = hh < NH ? a.desc[hh].y : 0;   // state head (the append plan's descriptor)
-  }
-#pragma unroll
-  for (int k = 0; k < kPlanPer; ++k) mine += (len[k] + kTile - 1) / kTile;
-  int total = 0;
-  int c = block_exclusive_scan(mine, lds, &total);
-  const int64_t T = total, W = a.W;
-  auto bound = [&](int64_t w) { return static_cast<int>(w * T / W); };
-  for (int w = tid; w <= a.W; w += kQThreads) a.wave_bounds[w] = bound(w);
-  if (tid == 0) a.cum_tiles[0] = 0;
-#pragma unroll
-  for (int k = 0; k < kPlanPer; ++k) {
-    const int hh = kPlanPer * tid + k;
-    if (hh >= NH) break;
-    const int c0 = c, c1 = c + (len[k] + kTile - 1) / kTile;
-    c = c1;
-    const int4 d = make_int4(len[k], shd[k], -1, 0);
-    a.plan_desc[hh] = d;
-    a.cum_tiles[hh + 1] = c1;
-    if (len[k] == 0)
-      for (int e = 0; e < a.gD; ++e) a.out[static_cast<size_t>(hh) * a.gD + e] = 0.f;
-    if (c1 > c0 && total > 0) {
-      // wave w starts at tile bound(w); head hh's tiles [c0, c1) are where
-      // waves ceil(c0 W / T) .. ceil(c1 W / T) - 1 start, and lie in waves
-      // ceil((c0 + 1) W / T) - 1 .. ceil(c1 W / T) - 1
-      const int w0 = static_cast<int>((c0 * W + T - 1) / T);
-      const int w1 = min(a.W, static_cast<int>((c1 * W + T - 1) / T));
-      for (int w = w0; w < w1; ++w) {
-        a.wave_desc[2 * w] = make_int4(bound(w), bound(w + 1), hh, c0);
-        a.wave_desc[2 * w + 1] = make_int4(c1, d.x, d.y, d.z);
-      }
-      const int wf = static_cast<int>(((c0 + 1) * W + T - 1) / T) - 1;
-      const int wl = min(a.W - 1, w1 - 1);
-      int mask = 0;
-      for (int i = 0; i < 32 && wf + i <= wl; ++i)
-        if (bound(wf + i) < bound(wf + i + 1)) mask |= 1 << i;
-      a.head_waves[hh] = make_int4(wf, wl, mask, 0);
-    }
-  }
-}
-
 __global__ __launch_bounds__(kQThreads) void quest_append_select_kernel(QuestArgs a) {
   extern __shared__ unsigned long long q_dyn[];
-  __shared__ int s_last;
   if (load_status(a.status) != 0) return;
   const int hh = blockIdx.x;
   const HeadDesc d = a.desc[hh];
   append_head(a, hh, d);
   __syncthreads();
   select_head(a, hh, d.y, d.x, q_dyn, reinterpret_cast<int*>(q_dyn + a.sort_pages));
-  if (!a.plan_tail) return;
-  // count this head's selection in once its length is stored; the block that
-  // completes the count plans the decode over every head's attended length
-  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this thread's stores are complete
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const int prev = atomicAdd(a.done, 1);
-    s_last = prev == static_cast<int>(gridDim.x) - 1;
-    if (s_last) __hip_atomic_store(a.done, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  __syncthreads();
-  if (s_last) plan_attended(a, gridDim.x);
 }
 
 // Sortable bits of a float (larger float -> larger unsigned).
@@ -289,7 +204,7 @@ __device__ void select_head(const QuestArgs& a, int hh, int sh, int L, unsigned 
       sel[i] = i < npages ? i : -1;
       qpage[i] = i < npages ? pt[i] : -1;
     }
-    if (tid == 0) put_qlen(a, hh, L);
+    if (tid == 0) a.qlen[hh] = L;
     return;
   }
   // Scores as one small matrix product: for q_i >= 0 the larger of
@@ -399,7 +314,7 @@ __device__ void select_head(const QuestArgs& a, int hh, int sh, int L, unsigned 
     }
     run += tot;
   }
-  if (tid == 0) put_qlen(a, hh, a.B * a.P - (chosen[npages - 1] ? npages * a.P - L : 0));
+  if (tid == 0) a.qlen[hh] = a.B * a.P - (chosen[npages - 1] ? npages * a.P - L : 0);
 }
 
 // One block per head of the call.
@@ -477,21 +392,8 @@ hipError_t launch_quest_append(const dms_config& c, const Layout& lo, void* meta
 
 hipError_t launch_quest_append_select(const dms_config& c, const Layout& lo, void* meta, void* ws,
                                       void* pool, int layer, int n, const void* q, const void* k,
-                                      const void* v, int waves, float* out, bool* planned, hipStream_t st) {
+                                      const void* v, hipStream_t st) {
   QuestArgs a = quest_args(c, lo, meta, ws, layer, n);
-  char* w = static_cast<char*>(ws);
-  // calls of up to kPlanMaxHeads heads get their decode plan from this launch
-  a.plan_tail = waves > 0 && n * c.num_kv_heads <= kPlanMaxHeads;
-  *planned = a.plan_tail != 0;
-  a.done = reinterpret_cast<int32_t*>(w + lo.ws_plan_ctr) + 1;
-  a.plan_desc = reinterpret_cast<HeadDesc*>(w + lo.ws_head_desc);
-  a.cum_tiles = reinterpret_cast<int32_t*>(w + lo.ws_cum_tiles);
-  a.wave_bounds = reinterpret_cast<int32_t*>(w + lo.ws_wave_bounds);
-  a.wave_desc = reinterpret_cast<int4*>(w + lo.ws_wave_desc);
-  a.head_waves = reinterpret_cast<int4*>(w + lo.ws_head_waves);
-  a.out = out;
-  a.W = waves;
-  a.gD = c.group_size * c.head_dim;
   a.pool = static_cast<const char*>(pool);
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);
