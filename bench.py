@@ -96,6 +96,19 @@ def profiled_traffic(profile, sources):
     return int(val) if val else None
 
 
+def decode_kernel_name(wl, quest_pages):
+    """The launch that the decode kernel timing covers for this workload: the
+    latent-attention kernel, the decode over Quest's selection (planned in the
+    launch up to 1024 call heads), the fused small-call step (up to 128 call
+    heads), or the planned decode kernel."""
+    D, NH = wl["head_dim"], wl["batch"] * wl["kv_heads"]
+    if wl.get("kv_format", 0) == MLA:
+        return "decode_mla_kernel"
+    if quest_pages > 0:
+        return f"decode_attended_kernel<{D}>" if NH <= 1024 else f"decode_kernel<{D}>"
+    return f"decode_step_kernel<{D}>" if NH <= 128 else f"decode_kernel<{D}>"
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -1122,7 +1135,7 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
             "traffic_source": "profiles/" + traffic_profile if traffic is not None else None,
-            "kernel": "decode_mla_kernel" if mla else f"decode_kernel<{D}>",
+            "kernel": decode_kernel_name(wl, args.quest_pages),
             "kernel_timing": "HIP events around each decode launch, eager pass of the next "
                              f"{args.steps} steps",
             "kernel_avg_us": round(1e3 * kern_avg_ms, 2),
