@@ -98,6 +98,7 @@ struct DecodeParams {
   int zero_neuron;   // element 0 of the group's first query head is read as 0
   int qB;            // page retrieval: pages attended per head (selection stride)
   float scale_log2;  // softmax scale * log2(e)
+  int defer_merge;   // split heads are merged by merge_kernel after the launch
 };
 
 // Scores are exponentiated against a per-lane reference max that is only
@@ -870,8 +871,9 @@ __device__ __forceinline__ void decode_wave(
   // once this wave's partial stores are complete, add its tile counts to
   // the heads' arrival counters; the wave that completes a head's count
   // merges all its partials by log-sum-exp and writes the output.  Deferring
-  // this to the end of the range keeps the tile stream free of waits.
-  if (npend > 0) {
+  // this to the end of the range keeps the tile stream free of waits.  In
+  // a planned launch (defer_merge) the merges run after it instead.
+  if (npend > 0 && !a.defer_merge) {
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     int prev = 0;
     if (lane < npend) prev = atomicAdd(&head_cnt[lane == 0 ? p_hh0 : p_hh1], lane == 0 ? p_cnt0 : p_cnt1);
@@ -1250,6 +1252,36 @@ __global__ __launch_bounds__(256, 1) void decode_step_kernel(
   if (wid == 0 && __shfl(ticket, 0, 64) == nb - 1) write_state(f, s_desc, s_aux, new_top, threadIdx.x & 63);
 }
 
+// Split heads of a planned decode launch, merged after it: one wave per call
+// head whose tiles span several waves; its partials are complete and visible
+// at the launch boundary.  Merging inside the decode launch put the merges'
+// coherent loads behind the stream's requests in the memory queues: at the
+// 32B-shaped stress step a merge after its arrival count took 7-25 us while
+// the count itself took ~1 us.
+template <int D>
+__global__ __launch_bounds__(256) void merge_kernel(const int32_t* __restrict__ status,
+                                                    const int32_t* __restrict__ cum_tiles,
+                                                    const int4* __restrict__ head_waves,
+                                                    const float2* __restrict__ part_ml, float* __restrict__ part_acc,
+                                                    float* __restrict__ out, DecodeParams a) {
+  __shared__ float merge_wts[kWavesPerBlock][kMergeBatch][kMaxGroup];
+  if (load_status(status) != 0) return;
+  const int lane = threadIdx.x & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int hh = blockIdx.x * kWavesPerBlock + wid;
+  if (hh >= a.NH) return;
+  if (ldc(cum_tiles, hh + 1) <= ldc(cum_tiles, hh)) return;   // no tiles (the planner zeroed its output)
+  const int4 hw = ldc(head_waves, hh);
+  const int wf = hw.x, wl = hw.y;
+  if (wf == wl) return;   // one wave held the whole head and wrote its output
+  const __amdgpu_buffer_rsrc_t acc_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      part_acc, static_cast<short>(0), a.part_acc_bytes, kBufferDword3);
+  if (wl - wf < 4)
+    merge_head_small<D>(part_ml, acc_rsrc, hw.z, out, wf, wl - wf + 1, hh, a.g, lane);
+  else
+    merge_head_any<D>(part_ml, acc_rsrc, ldc(cum_tiles, a.NH), a.W, out, wf, wl, hh, a.g, lane, merge_wts[wid]);
+}
+
 // Decode over Quest's selection (page retrieval) with the work split planned
 // in every workgroup: the tile prefix sums over the call's attended lengths
 // (qlen) and the head descriptors go to LDS, then the waves decode as with
@@ -1313,6 +1345,7 @@ DecodeParams decode_params(const dms_config& c, const Layout& lo, int D, int n, 
   a.zero_neuron = c.decision_source == DMS_DECIDE_QUERY;
   a.qB = c.quest_page_budget;
   a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
+  a.defer_merge = 0;
   return a;
 }
 
@@ -1365,7 +1398,8 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
   const int32_t* cum = reinterpret_cast<const int32_t*>(w + lo.ws_cum_tiles);
   float2* part_ml = reinterpret_cast<float2*>(w + lo.ws_part_ml);
   float* part_acc = reinterpret_cast<float*>(w + lo.ws_part_acc);
-  const DecodeParams a = decode_params(c, lo, D, n, waves);
+  DecodeParams a = decode_params(c, lo, D, n, waves);
+  a.defer_merge = 1;
   if (ev_start) (void)hipEventRecord(ev_start, st);
   hipLaunchKernelGGL((decode_kernel<D, FP8>), dim3(waves / kWavesPerBlock), dim3(256), 0, st, status,
                      reinterpret_cast<const HeadDesc*>(w + lo.ws_head_desc), cum,
@@ -1377,6 +1411,11 @@ hipError_t launch_decode_d(const dms_config& c, const Layout& lo, void* meta, vo
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                      static_cast<const uint16_t*>(v), part_ml, part_acc, out, a);
   hipError_t e = hipGetLastError();
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL((merge_kernel<D>), dim3((a.NH + kWavesPerBlock - 1) / kWavesPerBlock), dim3(256), 0, st,
+                       status, cum, reinterpret_cast<const int4*>(w + lo.ws_head_waves), part_ml, part_acc, out, a);
+    e = hipGetLastError();
+  }
   if (ev_stop) (void)hipEventRecord(ev_stop, st);
   return e;
 }
