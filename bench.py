@@ -100,13 +100,14 @@ def decode_kernel_name(wl, quest_pages):
     """The launch that the decode kernel timing covers for this workload: the
     latent-attention kernel, the decode over Quest's selection (planned in the
     launch up to 1024 call heads), the fused small-call step (up to 128 call
-    heads), or the planned decode kernel."""
+    heads), or the planned decode kernel with the merge launch after it."""
     D, NH = wl["head_dim"], wl["batch"] * wl["kv_heads"]
     if wl.get("kv_format", 0) == MLA:
         return "decode_mla_kernel"
+    planned = f"decode_kernel<{D}> + merge_kernel<{D}>"
     if quest_pages > 0:
-        return f"decode_attended_kernel<{D}>" if NH <= 1024 else f"decode_kernel<{D}>"
-    return f"decode_step_kernel<{D}>" if NH <= 128 else f"decode_kernel<{D}>"
+        return f"decode_attended_kernel<{D}>" if NH <= 1024 else planned
+    return f"decode_step_kernel<{D}>" if NH <= 128 else planned
 
 
 def log(msg):
