@@ -12,17 +12,18 @@ from oracle import PagedKVOracle, dense_dms_attention, fake_quantize_fp8
 pytestmark = pytest.mark.gpu
 
 
-def _run(cfg_kw, seqs, lens, chunks, seed, p, q_scale=1.0, override=None, fp8=False):
+def _run(cfg_kw, seqs, lens, chunks, seed, p, q_scale=1.0, override=None, fp8=False, nan_pools=False):
     """Prefill every sequence to lens[s] tokens in calls of chunks[c] tokens
     per sequence; check each call's outputs and the state after it.  With
     fp8 the pages are E4M3 and every key and value (cached or in the chunk)
     is attended in its quantized form; pools and workspace start as NaN
-    bytes."""
+    bytes (also with nan_pools for bf16 pages: the slots past a head's live
+    length, read with its last cached tile, then hold NaNs)."""
     import torch
     from paper_2506_05345_amd import dms
     cfg = dms.make_config(kv_format=dms.DMS_KV_FP8 if fp8 else dms.DMS_KV_BF16, **cfg_kw)
     cache = dms.DmsCache(cfg)
-    if fp8:
+    if fp8 or nan_pools:
         for pl in cache.pools:
             pl.fill_(0xFF)
         cache.workspace.fill_(0xFF)
@@ -99,6 +100,19 @@ def test_ragged_prefill(d, g, w, P, p):
     _run(dict(num_layers=1, max_seqs=4, num_kv_heads=H, group_size=g, head_dim=d, window=w,
               page_size=P, num_pages=300, max_pages_per_head=64, max_chunk_tokens=3 * 400),
          seqs, lens, [400, 77], 31, p)
+
+
+@pytest.mark.parametrize("d,g,w,P,chunks", [(128, 5, 256, 64, [400, 77]), (64, 3, 5, 32, [37, 200]),
+                                            (128, 8, 16, 256, [129])])
+def test_ragged_prefill_nan_pools(d, g, w, P, chunks):
+    """bf16 pages over NaN bytes: every ragged last cache tile brings stale
+    NaN rows into LDS, which must leave no trace in the outputs."""
+    H = 2
+    seqs = [2, 0, 3]
+    lens = {2: 700, 0: 95, 3: 411}
+    _run(dict(num_layers=1, max_seqs=4, num_kv_heads=H, group_size=g, head_dim=d, window=w,
+              page_size=P, num_pages=300, max_pages_per_head=64, max_chunk_tokens=3 * 400),
+         seqs, lens, chunks, 57, 0.75, nan_pools=True)
 
 
 def test_prefill_peaked_and_needle():
