@@ -640,9 +640,9 @@ __global__ __launch_bounds__((attn_threads<D, FP8>()), (512 / attn_threads<D, FP
 // ---- bf16 pages under delayed eviction: tiles copied by the hardware.
 // Every key source is a plain copy -- pool tiles with their slot metadata,
 // workspace tiles with the metadata pass 1 wrote -- so global -> LDS loads
-// (global_load_lds) move tiles and key rows two tiles ahead of the one being
-// attended, into three LDS buffers, with no staging registers, LDS stores or
-// waits for them in the loop.  Rows past a source's end are fixed up when
+// (global_load_lds) move tiles and key rows into three LDS buffers, each
+// copy issued as soon as its buffer is free (two to three tiles ahead of the
+// one being attended), with no staging registers or LDS stores.  Rows past a source's end are fixed up when
 // read: pool slots past the live length hold stale data (values zeroed in
 // registers, keys hidden), kept-list rows from the band on are hidden.
 //
@@ -654,7 +654,6 @@ __global__ __launch_bounds__((attn_threads<D, FP8>()), (512 / attn_threads<D, FP
 #define DMS_CONST __attribute__((address_space(4)))
 
 constexpr int wait_vm(int n) { return 0x0F70 | (n & 15) | ((n >> 4) << 14); }
-constexpr int kWaitLgkm0 = 0xC07F;   // s_waitcnt lgkmcnt(0)
 
 __device__ inline uint32_t lds_addr(const void* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((DMS_LDS const char*)p));
@@ -886,10 +885,6 @@ __global__ __launch_bounds__(256, 2) void prefill_copy_kernel(PrefillArgs a) {
       publish(min(1, ntiles - 2 - k));
       read_keys(k + 1);
       if (k + 3 < ntiles) issue(k + 3, k % kBuf);
-    } else {
-      // (the value reads complete on this path too, so that the PV MFMAs
-      // below wait for nothing on the other)
-      __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     }
 #pragma unroll
     for (int qb = 0; qb < NQ; ++qb)
