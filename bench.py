@@ -485,6 +485,122 @@ def run_mla_prefill(args):
     print(json.dumps(res), flush=True)
 
 
+TINY = dict(layers=1, batch=1, kv_heads=2, group=2, head_dim=64, window=16, page=64, context=512,
+            decode=64, p_evict=0.5, seed=0)
+
+
+def run_tiny(args):
+    """The tiny configuration timed whole: one sequence (2 KV heads x group 2,
+    d = 64, w = 16, flags Bernoulli(1/2)) prefilled with a 512-token masked
+    chunk (dms_prefill_chunk: attention over the chunk and its commit), then
+    64 decode steps (dms_decode_step), from an empty cache.  Each timed job
+    starts with dms_seq_reset; HIP events around the whole job on the launch
+    stream; eager launches (every call of the job is timed, host work
+    included)."""
+    import numpy as np
+    import torch
+
+    import dms_synth as sy
+    from paper_2506_05345_amd import dms
+
+    t = TINY
+    H, g, D, w, C, ND = t["kv_heads"], t["group"], t["head_dim"], t["window"], t["context"], t["decode"]
+    seed, p = t["seed"], t["p_evict"]
+    T = C + ND
+    pos = np.arange(T)
+    flags = sy.flags_np(seed, p, 0, 0, np.arange(H)[None, :], pos[:, None]).astype(np.uint8)
+    dim = np.arange(D)[None, None, :]
+    pp = pos[:, None, None]
+    k = sy.token_vectors_np(seed, sy.STREAM_K, 0, 0, np.arange(H)[None, :, None], pp, dim)
+    v = sy.token_vectors_np(seed, sy.STREAM_V, 0, 0, np.arange(H)[None, :, None], pp, dim)
+    q = sy.token_vectors_np(seed, sy.STREAM_Q, 0, 0, np.arange(H * g)[None, :, None], pp, dim)
+    dev = "cuda:0"
+
+    def bf16(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    qd, kd, vd = bf16(q), bf16(k), bf16(v)
+    fd = torch.from_numpy(flags).to(dev)
+    cfg = dms.make_config(num_layers=1, max_seqs=1, num_kv_heads=H, group_size=g, head_dim=D, window=w,
+                          page_size=t["page"], num_pages=32, max_pages_per_head=16, max_chunk_tokens=C)
+    cache = dms.DmsCache(cfg)
+    sid = torch.zeros(1, dtype=torch.int32, device=dev)
+    cu = torch.tensor([0, C], dtype=torch.int32, device=dev)
+    out_pf = torch.empty((C, H * g, D), dtype=torch.float32, device=dev)
+    out_dc = torch.empty((ND, 1, H * g, D), dtype=torch.float32, device=dev)
+    st = torch.cuda.current_stream()
+
+    def job():
+        dms.dms_seq_reset(cache.ctx, 0, 1, sid)
+        dms.dms_prefill_chunk(cache.ctx, 0, 1, sid, cu, C, C, qd[:C], kd[:C], vd[:C], fd[:C], out_pf)
+        for j in range(ND):
+            x = C + j
+            dms.dms_decode_step(cache.ctx, 0, 1, sid, qd[x:x + 1], kd[x:x + 1], vd[x:x + 1], fd[x:x + 1],
+                                out_dc[j])
+
+    for _ in range(args.warmup):
+        job()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    times = []
+    for _ in range(args.steps):
+        e0.record(st)
+        job()
+        e1.record(st)
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1))
+    if dms.dms_status(cache.ctx) != 0:
+        raise RuntimeError(f"device status {dms.dms_status(cache.ctx)}")
+    if not (torch.isfinite(out_pf).all() and torch.isfinite(out_dc).all()):
+        raise RuntimeError("non-finite outputs")
+    ms = float(np.mean(times))
+    res = {
+        "metric": "tiny configuration timed whole: 512-token masked prefill + 64 decode steps, ms per job",
+        "value": round(ms, 4), "unit": "ms", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "tiny: 1 sequence, 2 KV heads x group 2, d=64, w=16, flags Bernoulli(1/2), "
+                               "seed 0; 512-token prefill chunk then 64 decode steps", "layers": 1, "batch": 1,
+                   "kv_heads": H, "query_heads": H * g, "head_dim": D, "window": w, "context": C,
+                   "decode_steps": ND, "parallelism": "single GPU", "launch": "eager (every call of the job)"},
+        "job_ms": {"mean": round(ms, 4), "p10": round(float(np.percentile(times, 10)), 4),
+                   "p50": round(float(np.percentile(times, 50)), 4),
+                   "p90": round(float(np.percentile(times, 90)), 4)},
+        "decode_tok_per_s": round(ND / (ms * 1e-3), 1),
+    }
+    cnt = torch.zeros(H, dtype=torch.int32, device=dev)
+    dms.dms_retained_lengths(cache.ctx, 0, 1, sid, cnt)
+    torch.cuda.synchronize()
+    res["retained_after_job"] = [int(x) for x in cnt.cpu()]
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = tiny_cpu_baseline(q, k, v, flags, g, w, C, ND)
+    print(json.dumps(res), flush=True)
+
+
+def tiny_cpu_baseline(q, k, v, flags, g, w, C, ND):
+    """The oracle's dense float64 masked attention for the same job: every
+    chunk query, then every decode query over the full history."""
+    import os
+    import time
+
+    import numpy as np
+
+    import dms_synth as sy
+    from oracle import dense_dms_attention
+
+    f32 = sy.bf16_bits_to_f32_np
+    qf, kf, vf = f32(q), f32(k), f32(v)
+    t0 = time.perf_counter()
+    dense_dms_attention(qf[:C], kf[:C], vf[:C], flags[:C], w, g)
+    for j in range(ND):
+        x = C + j
+        dense_dms_attention(qf[x:x + 1], kf[:x + 1], vf[:x + 1], flags[:x + 1], w, g, t_query=np.array([x]))
+    sec = time.perf_counter() - t0
+    return {"value": round(1e3 * sec, 3), "unit": "ms", "cores": 1, "kind": "oracle",
+            "sample": "the whole job once (512 chunk queries, then 64 decode queries over the full history)",
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
+
+
 STRESS = dict(layers=64, batch=32, kv_heads=8, group=5, head_dim=128, prefill_seqs=4,
               chunk=4096, ctx_lo=1024, ctx_hi=131072)
 
@@ -898,7 +1014,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="qwen-r1-32b-8x",
-                    choices=sorted(WORKLOADS) + ["qwen-r1-32b-stress", "qwen-r1-32b-train",
+                    choices=sorted(WORKLOADS) + ["tiny", "qwen-r1-32b-stress", "qwen-r1-32b-train",
                                                  "deepseek-v2-lite-prefill", "deepseek-v2-prefill"])
     ap.add_argument("--window", type=int, default=256, choices=[64, 256],
                     help="window of the heterogeneous stress workload")
@@ -940,6 +1056,9 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.workload == "tiny":
+        run_tiny(args)
+        return
     if args.workload == "qwen-r1-32b-stress":
         run_stress(args)
         return
