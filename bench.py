@@ -572,6 +572,10 @@ def run_tiny(args):
     dms.dms_retained_lengths(cache.ctx, 0, 1, sid, cnt)
     torch.cuda.synchronize()
     res["retained_after_job"] = [int(x) for x in cnt.cpu()]
+    # after token T - 1: the last w tokens plus every unflagged older one
+    expect = [int(((pos > T - 1 - w) | (flags[:, h] == 0)).sum()) for h in range(H)]
+    if res["retained_after_job"] != expect:
+        raise RuntimeError(f"retained lengths {res['retained_after_job']} differ from the closed form {expect}")
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = tiny_cpu_baseline(q, k, v, flags, g, w, C, ND)
     print(json.dumps(res), flush=True)
