@@ -116,6 +116,10 @@ Layout make_layout(const dms_config& c) {
                         (c.kv_format == DMS_KV_MLA ? 64 : 128));
   lo.ws_pf_tmeta = take(2 * H * static_cast<size_t>(lo.pf_tiles_per_head) * 32 * 4);   // their key rows
   lo.ws_pf_flags = take(static_cast<size_t>(c.max_chunk_tokens) * H);  // decisions from q
+  // kept chunk tokens before every 32-aligned chunk position, per KV head
+  // (same indexing as the tiles of one region)
+  lo.ws_pf_kb = take(H * static_cast<size_t>(lo.pf_tiles_per_head) * 4);
+  lo.ws_pf_order = take(NH * 4);   // attention workgroup rows, heaviest head first
   lo.ws_q_sel = take(NH * static_cast<size_t>(c.quest_page_budget) * 4);
   lo.ws_q_page = take(NH * static_cast<size_t>(c.quest_page_budget) * 4);
   lo.ws_q_len = take(NH * 4);

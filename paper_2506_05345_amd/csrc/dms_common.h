@@ -37,7 +37,7 @@ struct Layout {
   size_t ws_wave_bounds, ws_wave_desc, ws_head_waves, ws_head_cnt;
   size_t ws_plan_ctr;   // fused decode: workgroups that have read the state this launch
   size_t ws_ck_need, ws_ck_fresh, ws_ck_base, ws_ck_pos0, ws_ck_err, ws_ck_slot;
-  size_t ws_pf_cum, ws_pf_meta, ws_pf_tiles, ws_pf_tmeta, ws_pf_flags;
+  size_t ws_pf_cum, ws_pf_meta, ws_pf_tiles, ws_pf_tmeta, ws_pf_flags, ws_pf_kb, ws_pf_order;
   size_t ws_q_sel, ws_q_page, ws_q_len;   // quest: selection [NH][B] (page-table
                                           // indices, physical pages), attended lengths [NH]
   int pf_tiles_per_head;   // tiles of one (region, KV head) in ws_pf_tiles

@@ -100,6 +100,8 @@ struct PrefillArgs {
   const int32_t* pos;
   int32_t* list;          // [H][total]: chunk-local indices of kept tokens
   int32_t* list_cnt;      // [n * H]
+  int32_t* kept_before;   // [H][tph]: kept chunk tokens before chunk position 32 j (tile indexing)
+  int32_t* order;         // [n * H]: (sequence, head) of attention grid row y, or null (row y itself)
   char* tiles;            // [2][H][tph] tiles: chunk tokens, then compacted kept tokens
   uint32_t* tmeta;        // [2][H][tph][32]: key rows of those tiles (position | flag << 31)
   float* out;             // [T, Hq, D]
@@ -132,8 +134,17 @@ __global__ __launch_bounds__(kThreads) void prefill_decide_kernel(const uint16_t
   flags[idx] = (__uint_as_float(bits << 16) + bias) > 0.f;
 }
 
-// Pass 0 (one block per (sequence, head)): validate the chunk boundaries and
-// list the kept tokens of the chunk in position order.
+__device__ inline size_t ws_tile(const PrefillArgs& a, int region, int h, int i, int k) {
+  return ((static_cast<size_t>(region) * a.H + h) * a.tph + a.cu[i] / 32 + i + k);
+}
+// kept_before entry of chunk position 32 j of sequence i, head h
+__device__ inline size_t ws_kb(const PrefillArgs& a, int h, int i, int j) {
+  return static_cast<size_t>(h) * a.tph + a.cu[i] / 32 + i + j;
+}
+
+// Pass 0 (one block per (sequence, head)): validate the chunk boundaries,
+// list the kept tokens of the chunk in position order and count them before
+// every 32-aligned position.
 __global__ __launch_bounds__(kThreads) void prefill_list_kernel(PrefillArgs a) {
   __shared__ int lds[17];
   if (load_status(a.status) != 0) return;
@@ -154,13 +165,34 @@ __global__ __launch_bounds__(kThreads) void prefill_list_kernel(PrefillArgs a) {
     int tot;
     const int off = block_exclusive_scan(kept, lds, &tot);
     if (kept) a.list[static_cast<size_t>(h) * a.total + tok0 + run + off] = c;
+    if (c < C && (c & 31) == 0) a.kept_before[ws_kb(a, h, i, c >> 5)] = run + off;
     run += tot;
   }
   if (threadIdx.x == 0) a.list_cnt[hh] = run;
 }
 
-__device__ inline size_t ws_tile(const PrefillArgs& a, int region, int h, int i, int k) {
-  return ((static_cast<size_t>(region) * a.H + h) * a.tph + a.cu[i] / 32 + i + k);
+
+// Attention grid rows by decreasing work (rows are dispatched in order, so
+// the longest heads start first and the short ones fill the tail): one
+// workgroup ranks the n * H (sequence, head) rows by their live length plus
+// half their kept chunk tokens (the cached keys every block of the row
+// attends to, and the mean of its kept-prefix keys); ties keep row order.
+constexpr int kOrderMax = 512;
+__global__ __launch_bounds__(kThreads) void prefill_order_kernel(PrefillArgs a) {
+  __shared__ int work[kOrderMax];
+  if (load_status(a.status) != 0) return;
+  const int NH = a.n * a.H;
+  for (int x = threadIdx.x; x < NH; x += kThreads) {
+    const int i = x / a.H, h = x % a.H;
+    work[x] = a.len[a.seq_ids[i] * a.H + h] + a.list_cnt[x] / 2;
+  }
+  __syncthreads();
+  for (int x = threadIdx.x; x < NH; x += kThreads) {
+    const int wx = work[x];
+    int rank = 0;
+    for (int y = 0; y < NH; ++y) rank += work[y] > wx || (work[y] == wx && y < x);
+    a.order[rank] = x;
+  }
 }
 
 // Pass 1 (one block per (32-token tile, sequence x head, region)): copy the
@@ -640,16 +672,17 @@ __global__ __launch_bounds__((attn_threads<D, FP8>()), (512 / attn_threads<D, FP
 // ---- bf16 pages under delayed eviction: tiles copied by the hardware.
 // Every key source is a plain copy -- pool tiles with their slot metadata,
 // workspace tiles with the metadata pass 1 wrote -- so global -> LDS loads
-// (global_load_lds) move tiles and key rows into three LDS buffers, each
-// copy issued as soon as its buffer is free (two to three tiles ahead of the
-// one being attended), with no staging registers or LDS stores.  Rows past a source's end are fixed up when
-// read: pool slots past the live length hold stale data (values zeroed in
-// registers, keys hidden), kept-list rows from the band on are hidden.
+// (global_load_lds) move tiles and key rows into four LDS buffers, each tile
+// by one wave (the address work is done once per tile) two tiles ahead of
+// the one being attended, with no staging registers or LDS stores.  Rows
+// past a source's end are fixed up when read: pool slots past the live
+// length hold stale data (values zeroed in registers, keys hidden),
+// kept-list rows from the band on are hidden.
 //
 // The LDS destination of a copy goes in M0, written by the same inline
 // assembly statement as the load; nothing else in this kernel reads M0.  The
 // compiler does not count these loads, so the kernel waits for them itself
-// (vmcnt, oldest first) before the barrier that publishes a tile.
+// (vmcnt) before the barrier that publishes a tile.
 #define DMS_LDS __attribute__((address_space(3)))
 #define DMS_CONST __attribute__((address_space(4)))
 
@@ -668,15 +701,47 @@ __device__ inline void lds_copy4(const char* g, uint32_t m0) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" : : "s"(m0), "v"(g) : "memory", "m0");
 }
 
-template <int D, int NQ>
-__global__ __launch_bounds__(256, 2) void prefill_copy_kernel(PrefillArgs a) {
-  constexpr int kBuf = 3;
+// ---- attention pass, the two column blocks of a wave half a tile apart.
+// With every step of a tile in one order (scores, weights, PV) the weights'
+// VALU work (maxima, exponentials, bf16 rounding, denominators) waits for the
+// score MFMAs and the PV MFMAs wait for it.  Here a tile k is attended in two
+// halves, each pairing one block's weights with MFMAs of the other block:
+//   A(k): weights of block 0 on tile k   | scores of block 1 on tile k, then
+//                                        | PV of block 1 on tile k - 1
+//   B(k): weights of block 1 on tile k   | scores of block 0 on tile k + 1,
+//                                        | then PV of block 0 on tile k
+// A half starts with its block's mask, column maxima and (rare, wave-uniform)
+// rescale; the rest is one straight stretch in which scheduling groups
+// alternate single MFMAs with a share of the VALU work and of the LDS operand
+// reads.  Tile k + 1's keys and key rows are read during A(k) (after the
+// score MFMAs of tile k have taken theirs), tile k's values at its end, so
+// one register set holds each operand.  Four LDS buffers: at the start of
+// A(k) one barrier publishes tile k + 1 and frees the buffer of tile k - 1,
+// into which tile k + 3 is copied.
+template <int M, int V, int R, int I = 0>
+__device__ __forceinline__ void interleave() {
+  if constexpr (I < M) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+    constexpr int nr = R / M + (I < R % M ? 1 : 0);
+    if constexpr (nr > 0) __builtin_amdgcn_sched_group_barrier(0x100, nr, 0);   // LDS reads
+    constexpr int nv = V / M + (I < V % M ? 1 : 0);
+    if constexpr (nv > 0) __builtin_amdgcn_sched_group_barrier(0x002, nv, 0);   // VALU
+    interleave<M, V, R, I + 1>();
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void prefill_pipe_kernel(PrefillArgs a) {
+  constexpr int NQ = 2;
+  constexpr int kBuf = 4;
   constexpr int kTB = D * 128;
   constexpr int kLoads = D / 32;   // 1 KB copies per wave and tile (four waves)
+  constexpr int KS = D / 32;       // k-steps of a score MFMA chain
+  constexpr int OB = D / 16;       // 16-dim output blocks
   __shared__ __attribute__((aligned(16))) char tile_lds[kBuf][kTB];
   __shared__ __attribute__((aligned(16))) uint32_t meta_lds[kBuf][64];   // rows 0..31, twice
   if (load_status(a.status) != 0) return;
-  const int hh = blockIdx.y;
+  const int hh = a.order ? a.order[blockIdx.y] : blockIdx.y;
   const int i = hh / a.H, h = hh % a.H;
   const int tok0 = a.cu[i], C = a.cu[i + 1] - a.cu[i];
   const int pb0 = blockIdx.x * a.PB;
@@ -687,16 +752,9 @@ __global__ __launch_bounds__(256, 2) void prefill_copy_kernel(PrefillArgs a) {
   const int L0 = a.len[sh];
   const int t0 = p0 + pb0;
   const int t1 = p0 + min(C, pb0 + a.PB);
-  // band: chunk tiles from the one holding max(p0, t0 - w + 1) up to t1
-  const int band_c0 = (max(0, t0 - a.w + 1 - p0) >> 5) << 5;
-  // kept chunk keys strictly before the band: prefix of the sorted list
-  const int32_t* lst = a.list + static_cast<size_t>(h) * a.total + tok0;
-  int lo_i = 0, hi_i = a.list_cnt[hh];
-  while (lo_i < hi_i) {
-    const int mid = (lo_i + hi_i) >> 1;
-    if (lst[mid] < band_c0) lo_i = mid + 1; else hi_i = mid;
-  }
-  const int n_pre = lo_i;
+  const int band_c0 = (max(0, pb0 - a.w + 1) >> 5) << 5;   // chunk-local, < C
+  // kept chunk keys strictly before the band, counted by pass 0
+  const int n_pre = a.kept_before[ws_kb(a, h, i, band_c0 >> 5)];
   const int nc = (L0 + 31) >> 5;
   const int np = (n_pre + 31) >> 5;
   const int nb = (t1 - p0 - band_c0 + 31) >> 5;
@@ -705,7 +763,6 @@ __global__ __launch_bounds__(256, 2) void prefill_copy_kernel(PrefillArgs a) {
   const char* band_tiles = a.tiles + ws_tile(a, 0, h, i, band_c0 >> 5) * kTB;
   const uint32_t* pre_meta = a.tmeta + ws_tile(a, 1, h, i, 0) * 32;
   const uint32_t* band_meta = a.tmeta + ws_tile(a, 0, h, i, band_c0 >> 5) * 32;
-  // the page table does not change during the kernel: scalar loads
   const DMS_CONST int32_t* pt = (const DMS_CONST int32_t*)(a.page_table + static_cast<size_t>(sh) * a.maxp);
   const uint32_t* smeta = reinterpret_cast<const uint32_t*>(a.slot_meta + static_cast<size_t>(sh) * a.max_slots);
 
@@ -714,11 +771,10 @@ __global__ __launch_bounds__(256, 2) void prefill_copy_kernel(PrefillArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 15, G = lane >> 4;
   const int Hq = a.H * a.g;
-  const int pcb = 16 / a.g;  // positions per column block
+  const int pcb = 16 / a.g;
 
-  // ---- columns of this lane: (position, query head) in each column block
   int tcol[NQ];
-  u32x4 qf[NQ][D / 32];
+  u32x4 qf[NQ][KS];
 #pragma unroll
   for (int qb = 0; qb < NQ; ++qb) {
     const int cb = wave * NQ + qb;
@@ -730,26 +786,24 @@ __global__ __launch_bounds__(256, 2) void prefill_copy_kernel(PrefillArgs a) {
     const char* qrow = reinterpret_cast<const char*>(
         a.q + (static_cast<size_t>(tok0 + (t - p0)) * Hq + h * a.g + qh) * D);
 #pragma unroll
-    for (int s2 = 0; s2 < D / 32; ++s2)
+    for (int s2 = 0; s2 < KS; ++s2)
       qf[qb][s2] = ok ? *reinterpret_cast<const u32x4*>(qrow + (32 * s2 + 8 * G) * 2) : z;
-    // the borrowed decision neuron takes no part in attention (App. C)
     if (a.zero_neuron && qh == 0 && G == 0) qf[qb][0][0] &= 0xFFFF0000u;
   }
-  // the query loads complete before the first copy, so that no wait the
-  // compiler places for them can fall inside the loop
   __builtin_amdgcn_s_waitcnt(wait_vm(0));
 
-  // ---- copies of tile k into buffer b: kLoads 1 KB blocks per wave; wave 0
-  // also copies the 32 key rows (both halves of the wave read the same rows)
-  int page = nc > 0 ? pt[0] : 0;   // page of the next pool tile to copy
-  auto issue = [&](int k, int b) {
+  // pool page of tile k (only read for k < nc)
+  auto page_of = [&](int k) { return k < nc ? pt[(32 * k) >> a.log2P] : 0; };
+  // tile k is copied by wave k % 4 alone (the address work is done once per
+  // tile), 1 KB per instruction
+  auto issue = [&](int k, int page) {
+    if (wave != (k & 3)) return;
     const char* tile;
     const uint32_t* mt;
     if (k < nc) {
       const int sb = 32 * k;
       tile = a.pool + static_cast<size_t>(page) * a.page_bytes + static_cast<size_t>((sb & (a.P - 1)) >> 5) * kTB;
       mt = smeta + sb;
-      if (k + 1 < nc) page = pt[(sb + 32) >> a.log2P];
     } else if (k < nc + np) {
       tile = pre_tiles + static_cast<size_t>(k - nc) * kTB;
       mt = pre_meta + (k - nc) * 32;
@@ -757,74 +811,137 @@ __global__ __launch_bounds__(256, 2) void prefill_copy_kernel(PrefillArgs a) {
       tile = band_tiles + static_cast<size_t>(k - nc - np) * kTB;
       mt = band_meta + (k - nc - np) * 32;
     }
+    const int b = k % kBuf;
     const uint32_t dst = lds_addr(tile_lds[b]);
 #pragma unroll
-    for (int m = 0; m < kLoads; ++m) {
-      const int blk = m * 4 + wave;
-      lds_copy16(tile + blk * 1024 + lane * 16, __builtin_amdgcn_readfirstlane(dst + blk * 1024));
-    }
-    if (wave == 0) lds_copy4(reinterpret_cast<const char*>(mt + (lane & 31)), lds_addr(meta_lds[b]));
+    for (int m = 0; m < 4 * kLoads; ++m) lds_copy16(tile + m * 1024 + lane * 16, dst + m * 1024);
+    lds_copy4(reinterpret_cast<const char*>(mt + (lane & 31)), lds_addr(meta_lds[b]));
+  };
+  // tile k has landed once the wave that copied it has no copy in flight
+  // (its next copy is issued after tile k is published)
+  auto wait_tile = [&](int k) {
+    if (wave == (k & 3)) __builtin_amdgcn_s_waitcnt(wait_vm(0));
   };
 
-  // ---- accumulators
-  f32x4 o[NQ][D / 16];
+  f32x4 o[NQ][OB];
   float m_ref[NQ], l_run[NQ];
 #pragma unroll
   for (int qb = 0; qb < NQ; ++qb) {
 #pragma unroll
-    for (int b = 0; b < D / 16; ++b) o[qb][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int b = 0; b < OB; ++b) o[qb][b] = f32x4{0.f, 0.f, 0.f, 0.f};
     m_ref[qb] = kMInit;
     l_run[qb] = 0.f;
   }
   const uint32_t lo_k = static_cast<uint32_t>(lane * 16);
   const uint32_t lo_v = static_cast<uint32_t>(D * 64 + lane * 16);
-  const float thr = kRescale / a.scale_log2;   // rescale threshold in score units
+  const float thr = kRescale / a.scale_log2;
+  const float sl2 = a.scale_log2;
 
-  // Pipeline: tile k's keys (and key rows) are in registers when iteration
-  // k starts; its value operands are read while its scores and weights are
-  // formed, and tile k + 1's keys while its PV MFMAs run.  The copy of tile
-  // k + 3 goes into tile k's buffer once every wave holds tile k's values.
-  for (int j = 0; j < min(kBuf, ntiles); ++j) issue(j, j);
-  Frag<D> f;
-  uint32_t mrow_l = 0;
-  u32x4 m0, m1;
-  // key operands and key rows of tile k (in LDS) into registers
-  auto read_keys = [&](int k) {
+  // operand registers: keys (and key rows) of one tile, values of one tile
+  u32x4 ka[KS], kb[KS], vt[OB];
+  uint32_t nrow = 0;
+  u32x4 nm0, nm1;
+  auto read_k = [&](int k) {
     const char* tl = tile_lds[k % kBuf];
-    mrow_l = meta_lds[k % kBuf][lane];
-    m0 = *reinterpret_cast<const u32x4*>(&meta_lds[k % kBuf][8 * G]);
-    m1 = *reinterpret_cast<const u32x4*>(&meta_lds[k % kBuf][8 * G + 4]);
 #pragma unroll
-    for (int s2 = 0; s2 < D / 32; ++s2) {
-      f.ka[s2] = *reinterpret_cast<const u32x4*>(tl + lo_k + s2 * 2048);
-      f.kb[s2] = *reinterpret_cast<const u32x4*>(tl + lo_k + 1024 + s2 * 2048);
+    for (int s2 = 0; s2 < KS; ++s2) {
+      ka[s2] = *reinterpret_cast<const u32x4*>(tl + lo_k + s2 * 2048);
+      kb[s2] = *reinterpret_cast<const u32x4*>(tl + lo_k + 1024 + s2 * 2048);
+    }
+    nrow = meta_lds[k % kBuf][lane];
+    nm0 = *reinterpret_cast<const u32x4*>(&meta_lds[k % kBuf][8 * G]);
+    nm1 = *reinterpret_cast<const u32x4*>(&meta_lds[k % kBuf][8 * G + 4]);
+  };
+  auto read_v = [&](int k) {
+    const char* tl = tile_lds[k % kBuf];
+#pragma unroll
+    for (int b = 0; b < OB; ++b) vt[b] = *reinterpret_cast<const u32x4*>(tl + lo_v + b * 1024);
+  };
+  auto scores = [&](int qb, float (&sc)[8]) {
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s2 = 0; s2 < KS; ++s2) {
+      s0 = mfma_bf16(ka[s2], qf[qb][s2], s0);
+      s1 = mfma_bf16(kb[s2], qf[qb][s2], s1);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      sc[j] = s0[j];
+      sc[j + 4] = s1[j];
     }
   };
-  // wait until tile k has landed (the copies of up to `ahead` later tiles
-  // may still be in flight), then publish it to every wave
-  auto publish = [&](int ahead) {
-    if (ahead >= 2) {
-      if (wave == 0) __builtin_amdgcn_s_waitcnt(wait_vm(2 * (kLoads + 1)));
-      else __builtin_amdgcn_s_waitcnt(wait_vm(2 * kLoads));
-    } else if (ahead == 1) {
-      if (wave == 0) __builtin_amdgcn_s_waitcnt(wait_vm(kLoads + 1));
-      else __builtin_amdgcn_s_waitcnt(wait_vm(kLoads));
-    } else {
-      __builtin_amdgcn_s_waitcnt(wait_vm(0));
-    }
-    __syncthreads();
+  auto pv = [&](int qb, u32x4 pu) {
+#pragma unroll
+    for (int b = 0; b < OB; ++b) o[qb][b] = mfma_bf16(vt[b], pu, o[qb][b]);
   };
+  // mask, column max and lazy rescale of one block's scores
+  auto head = [&](int qb, float (&sc)[8], bool masked, const int (&kp)[8], const int (&kx)[8]) {
+    if (masked) {
+      const int t = tcol[qb];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) sc[j] = (kp[j] <= t && t < kx[j]) ? sc[j] : -INFINITY;
+    }
+    float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
+                     fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
+    mx = col_max(mx);
+    const bool raise = mx > m_ref[qb] + thr;
+    if (__builtin_amdgcn_ballot_w64(raise)) {
+      const float m_new = raise ? mx : m_ref[qb];
+      const float alpha = __builtin_amdgcn_exp2f((m_ref[qb] - m_new) * sl2);
+      l_run[qb] *= alpha;
+#pragma unroll
+      for (int b = 0; b < OB; ++b) o[qb][b] *= alpha;
+      m_ref[qb] = m_new;
+    }
+  };
+  // weights p = 2^((s - m) scale) rounded to bf16, in two parts: the first
+  // forms half of the exponentials, the second the rest, the rounding and
+  // the denominator (which adds the rounded values, dot with (1, 1))
+  auto weights1 = [&](int qb, const float (&sc)[8], float (&e)[8]) {
+    const float mb = m_ref[qb] * sl2;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) e[j] = fmaf(sc[j], sl2, -mb);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) e[j] = __builtin_amdgcn_exp2f(e[j]);
+  };
+  auto weights2 = [&](int qb, float (&e)[8]) {
+#pragma unroll
+    for (int j = 4; j < 8; ++j) e[j] = __builtin_amdgcn_exp2f(e[j]);
+    u32x4 pu;
+    const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const f32x2 pr = {e[2 * j], e[2 * j + 1]};
+      const bf16x2 pb = __builtin_convertvector(pr, bf16x2);
+      pu[j] = __builtin_bit_cast(uint32_t, pb);
+      l_run[qb] = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, l_run[qb], false);
+    }
+    return pu;
+  };
+
+  for (int j = 0; j < min(kBuf - 1, ntiles); ++j) issue(j, page_of(j));
+  int page = page_of(kBuf - 1);   // page of the next tile to copy
+  float sc0[8], sc1[8];
+  u32x4 pu1 = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int b = 0; b < OB; ++b) vt[b] = u32x4{0u, 0u, 0u, 0u};
   if (ntiles > 0) {
-    publish(min(2, ntiles - 1));
-    read_keys(0);
+    wait_tile(0);
+    __syncthreads();
+    read_k(0);
+    scores(0, sc0);
   }
   for (int k = 0; k < ntiles; ++k) {
-    // rows of the tile that hold keys: pool slots below the live length,
-    // kept-list rows before the band
+    // ---- A(k) head: publish tile k + 1, copy tile k + 3 into tile k - 1's buffer
+    if (k + 1 < ntiles) wait_tile(k + 1);
+    __syncthreads();
+    if (k + 3 < ntiles) issue(k + 3, page);
+    // key rows of tile k; rows past the source's end hold no key
     const int rows = k < nc ? L0 - 32 * k : (k < nc + np ? n_pre - 32 * (k - nc) : 32);
+    uint32_t mrow = nrow;
+    u32x4 m0 = nm0, m1 = nm1;
     if (rows < 32) {
-      // rows past the source's end hold no key
-      if ((lane & 31) >= rows) mrow_l = kNoKey;
+      if ((lane & 31) >= rows) mrow = kNoKey;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         if (8 * G + j >= rows) m0[j] = kNoKey;
@@ -834,10 +951,10 @@ __global__ __launch_bounds__(256, 2) void prefill_copy_kernel(PrefillArgs a) {
     // a key row needs the per-element mask iff some query t in [t0, t1)
     // does not see it: no key, causal (position > t0) or flagged and
     // expiring by t1 - 1
-    const int kpr = static_cast<int>(mrow_l & ~kFlagBit);
-    const bool need = mrow_l == kNoKey || kpr > t0 || ((mrow_l & kFlagBit) && kpr + a.w <= t1 - 1);
+    const int kpr = static_cast<int>(mrow & ~kFlagBit);
+    const bool need = mrow == kNoKey || kpr > t0 || ((mrow & kFlagBit) && kpr + a.w <= t1 - 1);
     const bool masked = __builtin_amdgcn_ballot_w64(need) != 0;
-    int kp[8], kx[8];   // key position and expiry (first query that no longer sees it)
+    int kp[8], kx[8];
     if (masked) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
@@ -846,51 +963,51 @@ __global__ __launch_bounds__(256, 2) void prefill_copy_kernel(PrefillArgs a) {
         kx[j] = (km & kFlagBit) ? kp[j] + a.w : 0x7FFFFFFF;
       }
     }
-    // scores of every column block
-    f32x4 s0[NQ], s1[NQ];
-#pragma unroll
-    for (int qb = 0; qb < NQ; ++qb) {
-      s0[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      s1[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s2 = 0; s2 < D / 32; ++s2) {
-        s0[qb] = mfma_bf16(f.ka[s2], qf[qb][s2], s0[qb]);
-        s1[qb] = mfma_bf16(f.kb[s2], qf[qb][s2], s1[qb]);
-      }
-    }
-    // value operands of tile k
-    const char* tl = tile_lds[k % kBuf];
-#pragma unroll
-    for (int b = 0; b < D / 16; ++b) f.vt[b] = *reinterpret_cast<const u32x4*>(tl + lo_v + b * 1024);
-    // weights
-    float vsc[8];   // (FP8 only)
-    u32x4 pu[NQ];
-#pragma unroll
-    for (int qb = 0; qb < NQ; ++qb)
-      pu[qb] = col_weights<D, false>(s0[qb], s1[qb], vsc, masked, kp, kx, tcol[qb], o[qb], m_ref[qb],
-                                     l_run[qb], thr, a.scale_log2);
+    head(0, sc0, masked, kp, kx);
+    // ---- A(k) stretch
+    float e[8];
+    __builtin_amdgcn_sched_barrier(0);
+    scores(1, sc1);
+    weights1(0, sc0, e);
+    interleave<2 * KS, 12, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    pv(1, pu1);
+    read_k(k + 1);
+    const u32x4 pu0 = weights2(0, e);
+    interleave<OB, 12, 2 * KS + 3>();
+    __builtin_amdgcn_sched_barrier(0);
+    // the weights are formed here, beside the MFMAs above, not next to their
+    // first use in B(k)
+    asm volatile("" : : "v"(pu0), "v"(l_run[0]));
+    read_v(k);
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- B(k) head
     if (rows < 32) {
       // stale pool slots: value elements of rows 8 G + e >= rows are zeroed
-      // (element e of a value piece is key row 8 G + e)
       u32x4 keep;
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        keep[e] = (8 * G + 2 * e < rows ? 0x0000FFFFu : 0u) | (8 * G + 2 * e + 1 < rows ? 0xFFFF0000u : 0u);
+      for (int q = 0; q < 4; ++q)
+        keep[q] = (8 * G + 2 * q < rows ? 0x0000FFFFu : 0u) | (8 * G + 2 * q + 1 < rows ? 0xFFFF0000u : 0u);
 #pragma unroll
-      for (int b = 0; b < D / 16; ++b) f.vt[b] &= keep;
+      for (int b = 0; b < OB; ++b) vt[b] &= keep;
     }
-    if (k + 1 < ntiles) {
-      // every wave holds tile k's operands (the barrier waits for the reads);
-      // tile k + 1 is in LDS.  Its keys replace tile k's in registers.
-      publish(min(1, ntiles - 2 - k));
-      read_keys(k + 1);
-      if (k + 3 < ntiles) issue(k + 3, k % kBuf);
-    }
-#pragma unroll
-    for (int qb = 0; qb < NQ; ++qb)
-#pragma unroll
-      for (int b = 0; b < D / 16; ++b) o[qb][b] = mfma_bf16(f.vt[b], pu[qb], o[qb][b]);
+    head(1, sc1, masked, kp, kx);
+    // ---- B(k) stretch
+    __builtin_amdgcn_sched_barrier(0);
+    scores(0, sc0);
+    weights1(1, sc1, e);
+    interleave<2 * KS, 12, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    pv(0, pu0);
+    pu1 = weights2(1, e);
+    interleave<OB, 12, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("" : : "v"(pu1), "v"(l_run[1]));
+    // after this iteration's last LDS operand use: a scalar load in flight
+    // would turn every LDS wait before it into a full one
+    if (k + 4 < nc) page = pt[(32 * (k + 4)) >> a.log2P];
   }
+  if (ntiles > 0) pv(1, pu1);
 
   // ---- outputs
 #pragma unroll
@@ -904,7 +1021,7 @@ __global__ __launch_bounds__(256, 2) void prefill_copy_kernel(PrefillArgs a) {
       const float inv = 1.0f / l;
       float* dst = a.out + (static_cast<size_t>(tok0 + (t - p0)) * Hq + h * a.g + qh) * D + 4 * G;
 #pragma unroll
-      for (int b = 0; b < D / 16; ++b) *reinterpret_cast<f32x4*>(dst + 16 * b) = o[qb][b] * inv;
+      for (int b = 0; b < OB; ++b) *reinterpret_cast<f32x4*>(dst + 16 * b) = o[qb][b] * inv;
     }
   }
 }
@@ -937,6 +1054,8 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   a.list_cnt = reinterpret_cast<int32_t*>(w + lo.ws_pf_cum);
   a.tiles = w + lo.ws_pf_tiles;
   a.tmeta = reinterpret_cast<uint32_t*>(w + lo.ws_pf_tmeta);
+  a.kept_before = reinterpret_cast<int32_t*>(w + lo.ws_pf_kb);
+  a.order = nullptr;
   a.tph = lo.pf_tiles_per_head;
   a.immediate = c.eviction == DMS_EVICT_IMMEDIATE;
   a.zero_neuron = c.decision_source == DMS_DECIDE_QUERY;
@@ -956,18 +1075,25 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   a.PB = attn_threads<D, FP8>() / 64 * kNQ * (16 / c.group_size);
   a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
   const int NH = n * c.num_kv_heads;
-  // the timing events bracket all three passes
+  // the timing events bracket every pass
   if (ev_start) (void)hipEventRecord(ev_start, st);
   hipLaunchKernelGGL(prefill_list_kernel, dim3(NH), dim3(kThreads), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const bool pipe = !FP8 && !a.immediate;
+  if (pipe && NH > 1 && NH <= kOrderMax) {
+    a.order = reinterpret_cast<int32_t*>(w + lo.ws_pf_order);
+    hipLaunchKernelGGL(prefill_order_kernel, dim3(1), dim3(kThreads), 0, st, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL((prefill_tile_kernel<D, FP8>), dim3((max_len + 31) / 32, NH, 2), dim3(kThreads), 0,
                      st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 grid((max_len + a.PB - 1) / a.PB, NH);
-  if (!FP8 && !a.immediate)
-    hipLaunchKernelGGL((prefill_copy_kernel<D, kNQ>), grid, dim3(256), 0, st, a);
+  if (pipe)
+    hipLaunchKernelGGL((prefill_pipe_kernel<D>), grid, dim3(256), 0, st, a);
   else
     hipLaunchKernelGGL((prefill_kernel<D, kNQ, FP8>), grid, dim3(attn_threads<D, FP8>()), 0, st, a);
   e = hipGetLastError();
@@ -1307,6 +1433,8 @@ hipError_t launch_prefill_mla(const dms_config& c, const Layout& lo, void* meta,
   a.list_cnt = reinterpret_cast<int32_t*>(w + lo.ws_pf_cum);
   a.tiles = w + lo.ws_pf_tiles;
   a.tmeta = reinterpret_cast<uint32_t*>(w + lo.ws_pf_tmeta);
+  a.kept_before = reinterpret_cast<int32_t*>(w + lo.ws_pf_kb);
+  a.order = nullptr;
   a.tph = lo.pf_tiles_per_head;
   a.immediate = c.eviction == DMS_EVICT_IMMEDIATE;
   a.zero_neuron = 0;
@@ -1325,7 +1453,7 @@ hipError_t launch_prefill_mla(const dms_config& c, const Layout& lo, void* meta,
   a.max_len = max_len;
   a.PB = 0;
   a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
-  // the timing events bracket all three passes
+  // the timing events bracket every pass
   if (ev_start) (void)hipEventRecord(ev_start, st);
   hipLaunchKernelGGL(prefill_list_kernel, dim3(n), dim3(kThreads), 0, st, a);
   hipError_t e = hipGetLastError();
