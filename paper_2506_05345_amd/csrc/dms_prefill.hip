@@ -21,9 +21,10 @@
 // stages every source the same way.
 //
 // Attention pass: a workgroup (4 waves) owns one (sequence, KV head, block of
-// query positions).  Its columns are (position, query head) pairs packed 16
-// to an MFMA column block (16 / g positions x g heads); each wave holds NQ
-// column blocks.  Key tiles of 32 are staged into LDS in the order the MFMA
+// query positions).  Its columns are (position, query head) pairs, the g
+// heads of a position consecutive, packed 16 to an MFMA column block (a
+// position's heads may straddle two blocks); each wave holds NQ column
+// blocks.  Key tiles of 32 are staged into LDS in the order the MFMA
 // operand loads consume them (no bank conflicts), double buffered, and read
 // by every wave with 16-byte LDS loads straight into operand registers.  A tile is
 // masked per element only when some query of the block does not see one of
@@ -426,17 +427,18 @@ __global__ __launch_bounds__((attn_threads<D, FP8>()), (512 / attn_threads<D, FP
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 15, G = lane >> 4;
   const int Hq = a.H * a.g;
-  const int pcb = 16 / a.g;  // positions per column block
 
-  // ---- columns of this lane: (position, query head) in each column block
+  // ---- columns of this lane: column c of the workgroup's (wave, block,
+  // lane r) is query head c % g at position t0 + c / g (a position's heads
+  // may straddle two column blocks)
   int tcol[NQ];
   u32x4 qf[NQ][D / 32];
 #pragma unroll
   for (int qb = 0; qb < NQ; ++qb) {
-    const int cb = wave * NQ + qb;
-    const int pl = r / a.g, qh = r % a.g;
-    const int t = t0 + cb * pcb + pl;
-    const bool ok = (pl < pcb) && (t < t1);
+    const int col = (wave * NQ + qb) * 16 + r;
+    const int pl = col / a.g, qh = col % a.g;
+    const int t = t0 + pl;
+    const bool ok = (pl < a.PB) && (t < t1);
     tcol[qb] = ok ? t : -1;
     const u32x4 z = {0u, 0u, 0u, 0u};
     const char* qrow = reinterpret_cast<const char*>(
@@ -660,7 +662,7 @@ __global__ __launch_bounds__((attn_threads<D, FP8>()), (512 / attn_threads<D, FP
     l += __shfl_xor(l, 32, 64);
     const int t = tcol[qb];
     if (t >= 0) {
-      const int qh = r % a.g;
+      const int qh = ((wave * NQ + qb) * 16 + r) % a.g;
       const float inv = 1.0f / l;
       float* dst = a.out + (static_cast<size_t>(tok0 + (t - p0)) * Hq + h * a.g + qh) * D + 4 * G;
 #pragma unroll
@@ -771,16 +773,18 @@ __global__ __launch_bounds__(256, 2) void prefill_pipe_kernel(PrefillArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 15, G = lane >> 4;
   const int Hq = a.H * a.g;
-  const int pcb = 16 / a.g;
 
+  // column c of the workgroup's 128 (wave, block, lane r) is query head c % g
+  // at position t0 + c / g; a position's g heads may straddle two column
+  // blocks, so only the last 128 mod g columns go unused
   int tcol[NQ];
   u32x4 qf[NQ][KS];
 #pragma unroll
   for (int qb = 0; qb < NQ; ++qb) {
-    const int cb = wave * NQ + qb;
-    const int pl = r / a.g, qh = r % a.g;
-    const int t = t0 + cb * pcb + pl;
-    const bool ok = (pl < pcb) && (t < t1);
+    const int col = (wave * NQ + qb) * 16 + r;
+    const int pl = col / a.g, qh = col % a.g;
+    const int t = t0 + pl;
+    const bool ok = (pl < a.PB) && (t < t1);
     tcol[qb] = ok ? t : -1;
     const u32x4 z = {0u, 0u, 0u, 0u};
     const char* qrow = reinterpret_cast<const char*>(
@@ -1017,7 +1021,7 @@ __global__ __launch_bounds__(256, 2) void prefill_pipe_kernel(PrefillArgs a) {
     l += __shfl_xor(l, 32, 64);
     const int t = tcol[qb];
     if (t >= 0) {
-      const int qh = r % a.g;
+      const int qh = ((wave * NQ + qb) * 16 + r) % a.g;
       const float inv = 1.0f / l;
       float* dst = a.out + (static_cast<size_t>(tok0 + (t - p0)) * Hq + h * a.g + qh) * D + 4 * G;
 #pragma unroll
@@ -1072,7 +1076,10 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   a.max_seqs = c.max_seqs;
   a.total = total_tokens;
   a.max_len = max_len;
-  a.PB = attn_threads<D, FP8>() / 64 * kNQ * (16 / c.group_size);
+  const bool pipe = !FP8 && !a.immediate;
+  // positions per attention workgroup: its (position, head) columns fill 16
+  // per column block, kNQ blocks per wave
+  a.PB = (pipe ? 256 : attn_threads<D, FP8>()) / 64 * kNQ * 16 / c.group_size;
   a.scale_log2 = c.softmax_scale * 1.4426950408889634f;
   const int NH = n * c.num_kv_heads;
   // the timing events bracket every pass
@@ -1080,7 +1087,6 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   hipLaunchKernelGGL(prefill_list_kernel, dim3(NH), dim3(kThreads), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const bool pipe = !FP8 && !a.immediate;
   if (pipe && NH > 1 && NH <= kOrderMax) {
     a.order = reinterpret_cast<int32_t*>(w + lo.ws_pf_order);
     hipLaunchKernelGGL(prefill_order_kernel, dim3(1), dim3(kThreads), 0, st, a);
