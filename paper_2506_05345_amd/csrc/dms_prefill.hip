@@ -391,7 +391,7 @@ __global__ __launch_bounds__((attn_threads<D, FP8>()), (512 / attn_threads<D, FP
   __shared__ uint32_t meta_lds[2][32];
   __shared__ int masked_lds[2];   // tile has a key hidden from some query of the block
   if (load_status(a.status) != 0) return;
-  const int hh = blockIdx.y;
+  const int hh = a.order ? a.order[blockIdx.y] : blockIdx.y;
   const int i = hh / a.H, h = hh % a.H;
   const int tok0 = a.cu[i], C = a.cu[i + 1] - a.cu[i];
   const int pb0 = blockIdx.x * a.PB;
@@ -403,15 +403,11 @@ __global__ __launch_bounds__((attn_threads<D, FP8>()), (512 / attn_threads<D, FP
   const int t0 = p0 + pb0;
   const int t1 = p0 + min(C, pb0 + a.PB);
   // band: chunk tiles from the one holding max(p0, t0 - w + 1) up to t1
-  const int band_c0 = (max(0, t0 - a.w + 1 - p0) >> 5) << 5;
-  // kept chunk keys strictly before the band: prefix of the sorted list
+  const int band_c0 = (max(0, pb0 - a.w + 1) >> 5) << 5;   // chunk-local, < C
+  // kept chunk keys strictly before the band (a prefix of the sorted list),
+  // counted by pass 0
   const int32_t* lst = a.list + static_cast<size_t>(h) * a.total + tok0;
-  int lo_i = 0, hi_i = a.list_cnt[hh];
-  while (lo_i < hi_i) {
-    const int mid = (lo_i + hi_i) >> 1;
-    if (lst[mid] < band_c0) lo_i = mid + 1; else hi_i = mid;
-  }
-  const int n_pre = lo_i;
+  const int n_pre = a.kept_before[ws_kb(a, h, i, band_c0 >> 5)];
   const int nc = (L0 + 31) >> 5;
   const int np = (n_pre + 31) >> 5;
   const int nb = (t1 - p0 - band_c0 + 31) >> 5;
@@ -1087,7 +1083,7 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   hipLaunchKernelGGL(prefill_list_kernel, dim3(NH), dim3(kThreads), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (pipe && NH > 1 && NH <= kOrderMax) {
+  if (NH > 1 && NH <= kOrderMax) {
     a.order = reinterpret_cast<int32_t*>(w + lo.ws_pf_order);
     hipLaunchKernelGGL(prefill_order_kernel, dim3(1), dim3(kThreads), 0, st, a);
     e = hipGetLastError();
