@@ -1180,15 +1180,11 @@ __global__ __launch_bounds__(kMlaThreads, 1) void prefill_mla_kernel(PrefillArgs
   const int t0 = p0 + (cb0 / cgs) * pcb;
   const int t1 = p0 + min(C, (cb1 / cgs + 1) * pcb);
   // band: chunk tiles from the one holding max(p0, t0 - w + 1) up to t1
-  const int band_c0 = (max(0, t0 - a.w + 1 - p0) >> 5) << 5;
-  // kept chunk keys strictly before the band: prefix of the sorted list
+  const int band_c0 = (max(0, t0 - a.w + 1 - p0) >> 5) << 5;   // chunk-local, < C
+  // kept chunk keys strictly before the band (a prefix of the sorted list),
+  // counted by pass 0
   const int32_t* lst = a.list + tok0;
-  int lo_i = 0, hi_i = a.list_cnt[i];
-  while (lo_i < hi_i) {
-    const int mid = (lo_i + hi_i) >> 1;
-    if (lst[mid] < band_c0) lo_i = mid + 1; else hi_i = mid;
-  }
-  const int n_pre = lo_i;
+  const int n_pre = a.kept_before[ws_kb(a, 0, i, band_c0 >> 5)];
   const int nc = (L0 + 31) >> 5;
   const int np = (n_pre + 31) >> 5;
   const int nb = (t1 - p0 - band_c0 + 31) >> 5;
