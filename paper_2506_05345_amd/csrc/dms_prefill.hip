@@ -103,6 +103,8 @@ struct PrefillArgs {
   int32_t* list_cnt;      // [n * H]
   int32_t* kept_before;   // [H][tph]: kept chunk tokens before chunk position 32 j (tile indexing)
   int32_t* order;         // [n * H]: (sequence, head) of attention grid row y, or null (row y itself)
+  int32_t* work_ctr;      // attention work items taken so far (zeroed by pass 0)
+  int nx, items;          // query blocks per grid row; rows x nx
   char* tiles;            // [2][H][tph] tiles: chunk tokens, then compacted kept tokens
   uint32_t* tmeta;        // [2][H][tph][32]: key rows of those tiles (position | flag << 31)
   float* out;             // [T, Hq, D]
@@ -159,6 +161,7 @@ __global__ __launch_bounds__(kThreads) void prefill_list_kernel(PrefillArgs a) {
     if (threadIdx.x == 0) atomicCAS(reinterpret_cast<int*>(a.status_w), 0, DMS_ERR_INVALID);
     return;
   }
+  if (hh == 0 && threadIdx.x == 0 && a.work_ctr) *a.work_ctr = 0;
   int run = 0;
   for (int c0 = 0; c0 < C; c0 += blockDim.x) {
     const int c = c0 + threadIdx.x;
@@ -738,11 +741,15 @@ __global__ __launch_bounds__(256, 2) void prefill_pipe_kernel(PrefillArgs a) {
   constexpr int OB = D / 16;       // 16-dim output blocks
   __shared__ __attribute__((aligned(16))) char tile_lds[kBuf][kTB];
   __shared__ __attribute__((aligned(16))) uint32_t meta_lds[kBuf][64];   // rows 0..31, twice
+  __shared__ int item_lds[2];
   if (load_status(a.status) != 0) return;
-  const int hh = a.order ? a.order[blockIdx.y] : blockIdx.y;
+  // attention of work item `item` = (grid row item / nx, query block item % nx)
+  auto attend = [&](int item) {
+  const int row = item / a.nx;
+  const int hh = a.order ? a.order[row] : row;
   const int i = hh / a.H, h = hh % a.H;
   const int tok0 = a.cu[i], C = a.cu[i + 1] - a.cu[i];
-  const int pb0 = blockIdx.x * a.PB;
+  const int pb0 = (item - row * a.nx) * a.PB;
   if (pb0 >= C) return;
   const int s = a.seq_ids[i];
   const int sh = s * a.H + h;
@@ -1024,9 +1031,40 @@ __global__ __launch_bounds__(256, 2) void prefill_pipe_kernel(PrefillArgs a) {
       for (int b = 0; b < OB; ++b) *reinterpret_cast<f32x4*>(dst + 16 * b) = o[qb][b] * inv;
     }
   }
+};
+
+  // Items one after another: the first from the workgroup's grid position, the
+  // rest in order from a counter that pass 0 zeroed, each fetched one item
+  // ahead.  Rows come heaviest first, so the last items to start are short
+  // and the workgroups finish together (the launch has as many workgroups as
+  // fit on the chip at once).
+  int item = blockIdx.x, buf = 0;
+  if (threadIdx.x == 0) item_lds[0] = gridDim.x + atomicAdd(a.work_ctr, 1);
+  while (item < a.items) {
+    attend(item);
+    __syncthreads();   // the fetched index is visible; every wave is done with the LDS buffers
+    const int next = item_lds[buf];
+    if (threadIdx.x == 0) item_lds[buf ^ 1] = gridDim.x + atomicAdd(a.work_ctr, 1);
+    buf ^= 1;
+    item = next;
+  }
 }
 
 constexpr int kNQ = 2;
+
+// compute units of the current device (queried once)
+int cu_count() {
+  static int n = 0;
+  if (n == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+      n = v;
+    else
+      return 256;
+  }
+  return n;
+}
 
 template <int D, bool FP8>
 hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, void* ws, void* pool,
@@ -1056,6 +1094,8 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   a.tmeta = reinterpret_cast<uint32_t*>(w + lo.ws_pf_tmeta);
   a.kept_before = reinterpret_cast<int32_t*>(w + lo.ws_pf_kb);
   a.order = nullptr;
+  a.work_ctr = a.list_cnt + lo.max_heads;   // the word after the per-head counts
+  a.nx = a.items = 0;
   a.tph = lo.pf_tiles_per_head;
   a.immediate = c.eviction == DMS_EVICT_IMMEDIATE;
   a.zero_neuron = c.decision_source == DMS_DECIDE_QUERY;
@@ -1094,10 +1134,15 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 grid((max_len + a.PB - 1) / a.PB, NH);
-  if (pipe)
-    hipLaunchKernelGGL((prefill_pipe_kernel<D>), grid, dim3(256), 0, st, a);
-  else
+  if (pipe) {
+    // as many workgroups as fit on the chip at once (two per CU), each
+    // taking work items until none is left
+    a.nx = static_cast<int>(grid.x);
+    a.items = a.nx * NH;
+    hipLaunchKernelGGL((prefill_pipe_kernel<D>), dim3(min(a.items, 2 * cu_count())), dim3(256), 0, st, a);
+  } else {
     hipLaunchKernelGGL((prefill_kernel<D, kNQ, FP8>), grid, dim3(attn_threads<D, FP8>()), 0, st, a);
+  }
   e = hipGetLastError();
   if (ev_stop) (void)hipEventRecord(ev_stop, st);
   return e;
@@ -1433,6 +1478,8 @@ hipError_t launch_prefill_mla(const dms_config& c, const Layout& lo, void* meta,
   a.tmeta = reinterpret_cast<uint32_t*>(w + lo.ws_pf_tmeta);
   a.kept_before = reinterpret_cast<int32_t*>(w + lo.ws_pf_kb);
   a.order = nullptr;
+  a.work_ctr = nullptr;
+  a.nx = a.items = 0;
   a.tph = lo.pf_tiles_per_head;
   a.immediate = c.eviction == DMS_EVICT_IMMEDIATE;
   a.zero_neuron = 0;
