@@ -393,11 +393,15 @@ __global__ __launch_bounds__((attn_threads<D, FP8>()), (512 / attn_threads<D, FP
   __shared__ __attribute__((aligned(16))) float scale_lds[2][64];   // FP8: tile scales
   __shared__ uint32_t meta_lds[2][32];
   __shared__ int masked_lds[2];   // tile has a key hidden from some query of the block
+  __shared__ int item_lds[2];
   if (load_status(a.status) != 0) return;
-  const int hh = a.order ? a.order[blockIdx.y] : blockIdx.y;
+  // attention of work item `item` = (grid row item / nx, query block item % nx)
+  auto attend = [&](int item) {
+  const int row = item / a.nx;
+  const int hh = a.order ? a.order[row] : row;
   const int i = hh / a.H, h = hh % a.H;
   const int tok0 = a.cu[i], C = a.cu[i + 1] - a.cu[i];
-  const int pb0 = blockIdx.x * a.PB;
+  const int pb0 = (item - row * a.nx) * a.PB;
   if (pb0 >= C) return;
   const int s = a.seq_ids[i];
   const int sh = s * a.H + h;
@@ -667,6 +671,19 @@ __global__ __launch_bounds__((attn_threads<D, FP8>()), (512 / attn_threads<D, FP
 #pragma unroll
       for (int b = 0; b < D / 16; ++b) *reinterpret_cast<f32x4*>(dst + 16 * b) = o[qb][b] * inv;
     }
+  }
+};
+
+  // items as in the bf16 pass: grid position first, then the counter
+  int item = blockIdx.x, buf = 0;
+  if (threadIdx.x == 0) item_lds[0] = gridDim.x + atomicAdd(a.work_ctr, 1);
+  while (item < a.items) {
+    attend(item);
+    __syncthreads();   // the fetched index is visible; every wave is done with the LDS buffers
+    const int next = item_lds[buf];
+    if (threadIdx.x == 0) item_lds[buf ^ 1] = gridDim.x + atomicAdd(a.work_ctr, 1);
+    buf ^= 1;
+    item = next;
   }
 }
 
@@ -1134,15 +1151,16 @@ hipError_t launch_prefill_d(const dms_config& c, const Layout& lo, void* meta, v
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 grid((max_len + a.PB - 1) / a.PB, NH);
-  if (pipe) {
-    // as many workgroups as fit on the chip at once (two per CU), each
-    // taking work items until none is left
-    a.nx = static_cast<int>(grid.x);
-    a.items = a.nx * NH;
+  // as many workgroups as fit on the chip at once, each taking work items
+  // until none is left
+  a.nx = static_cast<int>(grid.x);
+  a.items = a.nx * NH;
+  if (pipe)
     hipLaunchKernelGGL((prefill_pipe_kernel<D>), dim3(min(a.items, 2 * cu_count())), dim3(256), 0, st, a);
-  } else {
-    hipLaunchKernelGGL((prefill_kernel<D, kNQ, FP8>), grid, dim3(attn_threads<D, FP8>()), 0, st, a);
-  }
+  else
+    hipLaunchKernelGGL((prefill_kernel<D, kNQ, FP8>),
+                       dim3(min(a.items, 512 / attn_threads<D, FP8>() * cu_count())),
+                       dim3(attn_threads<D, FP8>()), 0, st, a);
   e = hipGetLastError();
   if (ev_stop) (void)hipEventRecord(ev_stop, st);
   return e;
