@@ -150,7 +150,19 @@ __global__ __launch_bounds__(kQThreads) void quest_bounds_kernel(QuestArgs a) {
 // into its slot (wave 0), then the bounds of that page over its live slots,
 // the new row read back after the barrier (its stores are complete and
 // visible to the block's other waves there).
-__device__ void select_head(const QuestArgs& a, int hh, int sh, int L, unsigned long long* keys, int* chosen);
+//
+// Selection operands of one lane: its query column (head r) split into the
+// negative and positive parts, and the bounds of the page it scores first
+// (page 16 wave + r), loaded before the append when that page is not the
+// one the append rewrites.
+struct SelectOps {
+  u32x4 qneg[4], qpos[4];
+  u32x4 lo[4], hi[4];
+  bool have_bounds;
+};
+__device__ void select_ops(const QuestArgs& a, int hh, int sh, int L, int skip_page, SelectOps& op);
+__device__ void select_head(const QuestArgs& a, int hh, int sh, int L, unsigned long long* keys, int* chosen,
+                            SelectOps& op);
 
 __device__ inline void append_head(const QuestArgs& a, int hh, const HeadDesc& d) {
   const int i = d.z / a.P, row = d.z % a.P;
@@ -179,9 +191,13 @@ __global__ __launch_bounds__(kQThreads) void quest_append_select_kernel(QuestArg
   if (load_status(a.status) != 0) return;
   const int hh = blockIdx.x;
   const HeadDesc d = a.desc[hh];
+  // the query and every first-round page bound but the appended page's are
+  // read before the append, so their loads overlap it
+  SelectOps op;
+  select_ops(a, hh, d.y, d.x, d.z / a.P, op);
   append_head(a, hh, d);
   __syncthreads();
-  select_head(a, hh, d.y, d.x, q_dyn, reinterpret_cast<int*>(q_dyn + a.sort_pages));
+  select_head(a, hh, d.y, d.x, q_dyn, reinterpret_cast<int*>(q_dyn + a.sort_pages), op);
 }
 
 // Sortable bits of a float (larger float -> larger unsigned).
@@ -190,9 +206,57 @@ __device__ inline uint32_t orderable(float x) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Scores as one small matrix product: for q_i >= 0 the larger of q_i lo_i,
+// q_i hi_i is q_i hi_i, else q_i lo_i, so U = [lo | hi] . [q-; q+] with
+// q- = min(q, 0), q+ = max(q, 0) (exact in bf16; the products are exact in
+// fp32).  MFMA rows are 16 pages, columns the group's heads, k the 2 D
+// entries of a page's bounds (lo then hi).  The borrowed neuron is read as 0
+// in query-decision mode.  A operand: lane (page p, G) holds bound entries
+// 32 kb + 8 G .. + 7.
+__device__ inline void page_bound_ops(const QuestArgs& a, int sh, int p, int npages, u32x4 (&lo)[4], u32x4 (&hi)[4]) {
+  const int G = (threadIdx.x & 63) >> 4;
+  const uint16_t* b = p < npages
+      ? a.st.page_bounds + static_cast<size_t>(a.st.page_table[static_cast<size_t>(sh) * a.maxp + p]) * 2 * a.D
+      : nullptr;
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) {
+    lo[kb] = (b && kb < a.D / 32) ? *reinterpret_cast<const u32x4*>(b + 32 * kb + 8 * G) : u32x4{0u, 0u, 0u, 0u};
+    hi[kb] = (b && kb < a.D / 32) ? *reinterpret_cast<const u32x4*>(b + a.D + 32 * kb + 8 * G)
+                                  : u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+// This lane's query column (head r: dims 32 kb + 8 G .. + 7) and, unless it
+// is skip_page, the bounds of its first page.
+__device__ void select_ops(const QuestArgs& a, int hh, int sh, int L, int skip_page, SelectOps& op) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int r = lane & 15, G = lane >> 4;
+  const int h = hh % a.H;
+  const uint16_t* qg = a.q + (static_cast<size_t>(hh / a.H) * a.H * a.g + h * a.g) * a.D;
+  const int npages = (L + a.P - 1) / a.P;
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) {
+    u32x4 x = {0u, 0u, 0u, 0u};
+    if (npages > a.B && r < a.g && kb < a.D / 32) x = *reinterpret_cast<const u32x4*>(qg + r * a.D + 32 * kb + 8 * G);
+    if (a.zero_neuron && r == 0 && G == 0 && kb == 0) x[0] &= 0xFFFF0000u;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      // per bf16 half: negative (sign set) -> q-, else q+
+      const uint32_t neg = ((x[w] >> 15) & 1u) * 0x0000FFFFu | ((x[w] >> 31) & 1u) * 0xFFFF0000u;
+      op.qneg[kb][w] = x[w] & neg;
+      op.qpos[kb][w] = x[w] & ~neg;
+    }
+  }
+  const int p = 16 * wave + r;
+  op.have_bounds = npages > a.B && p != skip_page;
+  if (op.have_bounds) page_bound_ops(a, sh, p, npages, op.lo, op.hi);
+}
+
 // Selection of call head hh by one block: keys (sort_pages of them) and
-// page marks (maxp) in the caller's LDS.
-__device__ void select_head(const QuestArgs& a, int hh, int sh, int L, unsigned long long* keys, int* chosen) {
+// page marks (maxp) in the caller's LDS; op from select_ops.
+__device__ void select_head(const QuestArgs& a, int hh, int sh, int L, unsigned long long* keys, int* chosen,
+                            SelectOps& op) {
   __shared__ int lds[17];
   const int npages = (L + a.P - 1) / a.P;
   const int tid = threadIdx.x;
@@ -207,51 +271,26 @@ __device__ void select_head(const QuestArgs& a, int hh, int sh, int L, unsigned 
     if (tid == 0) a.qlen[hh] = L;
     return;
   }
-  // Scores as one small matrix product: for q_i >= 0 the larger of
-  // q_i lo_i, q_i hi_i is q_i hi_i, else q_i lo_i, so U = [lo | hi] . [q-; q+]
-  // with q- = min(q, 0), q+ = max(q, 0) (exact in bf16; the products are
-  // exact in fp32).  MFMA rows are 16 pages, columns the group's heads, k the
-  // 2 D entries of a page's bounds (lo then hi).  The borrowed neuron is read
-  // as 0 in query-decision mode.
-  const int h = hh % a.H;
-  const uint16_t* qg = a.q + (static_cast<size_t>(hh / a.H) * a.H * a.g + h * a.g) * a.D;
   const int lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, G = lane >> 4;
   const int kbs = a.D / 32;                  // k-blocks per half (lo or hi)
-  u32x4 qneg[4], qpos[4];                    // this lane's column (head r): dims 32 kb + 8 G .. + 7
-#pragma unroll
-  for (int kb = 0; kb < 4; ++kb) {
-    u32x4 x = {0u, 0u, 0u, 0u};
-    if (r < a.g && kb < kbs) x = *reinterpret_cast<const u32x4*>(qg + r * a.D + 32 * kb + 8 * G);
-    if (a.zero_neuron && r == 0 && G == 0 && kb == 0) x[0] &= 0xFFFF0000u;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      // per bf16 half: negative (sign set) -> q-, else q+
-      const uint32_t neg = ((x[w] >> 15) & 1u) * 0x0000FFFFu | ((x[w] >> 31) & 1u) * 0xFFFF0000u;
-      qneg[kb][w] = x[w] & neg;
-      qpos[kb][w] = x[w] & ~neg;
-    }
-  }
   int npow = 1;
   while (npow < npages) npow <<= 1;
   for (int p = tid; p < npow; p += kQThreads) keys[p] = 0ull;
   __syncthreads();
   for (int pb = 16 * wave; pb < npages; pb += kQThreads / 4) {
-    // A operand: lane (page pb + r, G) loads bound entries 32 kb + 8 G .. + 7
     const int p = pb + r;
-    const uint16_t* b = p < npages
-        ? a.st.page_bounds + static_cast<size_t>(a.st.page_table[static_cast<size_t>(sh) * a.maxp + p]) * 2 * a.D
-        : nullptr;
+    // the first round's bounds came with the operands unless this lane's
+    // page is the one the append rewrote
+    if (pb != 16 * wave || !op.have_bounds) page_bound_ops(a, sh, p, npages, op.lo, op.hi);
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       if (kb < kbs) {
-        const u32x4 lo = b ? *reinterpret_cast<const u32x4*>(b + 32 * kb + 8 * G) : u32x4{0u, 0u, 0u, 0u};
-        const u32x4 hi = b ? *reinterpret_cast<const u32x4*>(b + a.D + 32 * kb + 8 * G) : u32x4{0u, 0u, 0u, 0u};
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, lo),
-                                                      __builtin_bit_cast(bf16x8, qneg[kb]), acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, hi),
-                                                      __builtin_bit_cast(bf16x8, qpos[kb]), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, op.lo[kb]),
+                                                      __builtin_bit_cast(bf16x8, op.qneg[kb]), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, op.hi[kb]),
+                                                      __builtin_bit_cast(bf16x8, op.qpos[kb]), acc, 0, 0, 0);
       }
     }
     // lane (head r, G) holds pages pb + 4 G + i; maximum over the group's heads
@@ -325,7 +364,9 @@ __global__ __launch_bounds__(kQThreads) void quest_select_kernel(QuestArgs a) {
   if (load_status(a.status) != 0) return;
   const int hh = blockIdx.x;
   const int sh = a.seq_ids[hh / a.H] * a.H + hh % a.H;
-  select_head(a, hh, sh, a.st.len[sh], q_dyn, reinterpret_cast<int*>(q_dyn + a.sort_pages));
+  SelectOps op;
+  select_ops(a, hh, sh, a.st.len[sh], -1, op);
+  select_head(a, hh, sh, a.st.len[sh], q_dyn, reinterpret_cast<int*>(q_dyn + a.sort_pages), op);
 }
 
 // Selection of the last decode call -> caller buffers (one thread per head).
