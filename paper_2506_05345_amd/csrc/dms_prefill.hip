@@ -814,7 +814,6 @@ __global__ __launch_bounds__(256, 2) void prefill_pipe_kernel(PrefillArgs a) {
       qf[qb][s2] = ok ? *reinterpret_cast<const u32x4*>(qrow + (32 * s2 + 8 * G) * 2) : z;
     if (a.zero_neuron && qh == 0 && G == 0) qf[qb][0][0] &= 0xFFFF0000u;
   }
-  __builtin_amdgcn_s_waitcnt(wait_vm(0));
 
   // pool page of tile k (only read for k < nc)
   auto page_of = [&](int k) { return k < nc ? pt[(32 * k) >> a.log2P] : 0; };
@@ -945,6 +944,10 @@ __global__ __launch_bounds__(256, 2) void prefill_pipe_kernel(PrefillArgs a) {
 
   for (int j = 0; j < min(kBuf - 1, ntiles); ++j) issue(j, page_of(j));
   int page = page_of(kBuf - 1);   // page of the next tile to copy
+  // the query loads and this wave's first copy are in flight together; both
+  // complete here, so that no wait the compiler places for the query loads
+  // can fall inside the loop
+  __builtin_amdgcn_s_waitcnt(wait_vm(0));
   float sc0[8], sc1[8];
   u32x4 pu1 = {0u, 0u, 0u, 0u};
 #pragma unroll
