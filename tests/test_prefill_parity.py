@@ -195,3 +195,30 @@ def test_prefill_fp8_peaked():
     _run(dict(num_layers=1, max_seqs=1, num_kv_heads=2, group_size=5, head_dim=128, window=64,
               page_size=64, num_pages=64, max_pages_per_head=16, max_chunk_tokens=512),
          [0], {0: 600}, [300], 43, 0.875, q_scale=8.0, fp8=True)
+
+
+def test_prefill_many_heads_unordered_work_items():
+    """70 sequences x 8 KV heads: 560 (sequence, head) rows, more than the
+    head ranking takes, so grid rows keep the call's order; 2 query blocks
+    per row give 1120 work items, more than the chip holds workgroups, so
+    the resident workgroups take most items from the counter."""
+    seqs = list(range(70))
+    lens = {s: 60 + (s % 7) for s in seqs}
+    _run(dict(num_layers=1, max_seqs=70, num_kv_heads=8, group_size=5, head_dim=128, window=32,
+              page_size=64, num_pages=70 * 8 * 3, max_pages_per_head=4, max_chunk_tokens=70 * 40),
+         seqs, lens, [40], 71, 0.75)
+
+
+@pytest.mark.parametrize("d,g,fp8", [(64, 16, False), (128, 5, True)])
+def test_prefill_ranked_rows_counter_items(d, g, fp8):
+    """Few heads but many query blocks: the rows are ranked by work and the
+    items outnumber the resident workgroups (800 items at d = 64, g = 16 on
+    bf16 pages; 320 at d = 128, g = 5 on FP8 pages, one workgroup per CU);
+    unequal histories so the ranking reorders the rows."""
+    H = 4 if not fp8 else 8
+    seqs = [1, 3, 0, 2]
+    lens = {1: 900, 3: 640, 0: 1000, 2: 700}
+    chunk = 400 if not fp8 else 500
+    _run(dict(num_layers=1, max_seqs=4, num_kv_heads=H, group_size=g, head_dim=d, window=48,
+              page_size=64, num_pages=4 * H * 18, max_pages_per_head=18, max_chunk_tokens=4 * chunk),
+         seqs, lens, [chunk], 83, 0.8, fp8=fp8)
