@@ -189,8 +189,9 @@ __device__ inline float key_bias_raw(const TrainArgs& a, int b, int h, int j) {
 
 // ---------------------------------------------------------------------------
 // Forward.  Workgroup = (sequence b, KV head h, block of PB query positions);
-// columns are (position, query head) pairs, 16 / g positions x g heads per
-// 16-column MFMA block, NQ blocks per wave.  Key tiles 0 .. ceil(t1 / 32) - 1
+// columns are (position, query head) pairs, the g heads of a position
+// consecutive, 16 per MFMA column block (a position's heads may straddle two
+// blocks), NQ blocks per wave.  Key tiles 0 .. ceil(t1 / 32) - 1
 // (causal) are staged through LDS: K row part, V transposed part.
 // ---------------------------------------------------------------------------
 template <int D, int NQ>
@@ -207,16 +208,16 @@ __global__ __launch_bounds__(kThreads, 2) void train_fwd_kernel(TrainArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 15, G = lane >> 4;
-  const int Hq = a.H * a.g, pcb = 16 / a.g;
+  const int Hq = a.H * a.g;
 
   int tcol[NQ];
   u32x4 qf[NQ][D / 32];
 #pragma unroll
   for (int qb = 0; qb < NQ; ++qb) {
-    const int cb = wave * NQ + qb;
-    const int pl = r / a.g, qh = r % a.g;
-    const int t = t0 + cb * pcb + pl;
-    const bool ok = (pl < pcb) && (t < t1);
+    const int col = (wave * NQ + qb) * 16 + r;
+    const int pl = col / a.g, qh = col % a.g;
+    const int t = t0 + pl;
+    const bool ok = (pl < a.PB) && (t < t1);
     tcol[qb] = ok ? t : -1;
     const uint16_t* qrow = a.q + ((static_cast<size_t>(b) * a.T + (ok ? t : 0)) * Hq + h * a.g + qh) * D;
 #pragma unroll
@@ -343,7 +344,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_fwd_kernel(TrainArgs a) {
     const float l = col_sum(l_run[qb]);
     const int t = tcol[qb];
     if (t >= 0) {
-      const int qh = r % a.g;
+      const int qh = ((wave * NQ + qb) * 16 + r) % a.g;
       float* dst = a.o_out + ((static_cast<size_t>(b) * a.T + t) * Hq + h * a.g + qh) * D + 4 * G;
       const float inv = 1.0f / l;
 #pragma unroll
@@ -404,17 +405,17 @@ __global__ __launch_bounds__(kThreads, 1) void train_dq_kernel(TrainArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 15, G = lane >> 4;
-  const int Hq = a.H * a.g, pcb = 16 / a.g;
+  const int Hq = a.H * a.g;
 
   int tcol[NQ];
   u32x4 qf[NQ][D / 32], df[NQ][D / 32];
   float lse2[NQ], dcol[NQ];
 #pragma unroll
   for (int qb = 0; qb < NQ; ++qb) {
-    const int cb = wave * NQ + qb;
-    const int pl = r / a.g, qh = r % a.g;
-    const int t = t0 + cb * pcb + pl;
-    const bool ok = (pl < pcb) && (t < t1);
+    const int col = (wave * NQ + qb) * 16 + r;
+    const int pl = col / a.g, qh = col % a.g;
+    const int t = t0 + pl;
+    const bool ok = (pl < a.PB) && (t < t1);
     tcol[qb] = ok ? t : -1;
     const size_t row = (static_cast<size_t>(b) * a.T + (ok ? t : 0)) * Hq + h * a.g + qh;
 #pragma unroll
@@ -530,7 +531,7 @@ __global__ __launch_bounds__(kThreads, 1) void train_dq_kernel(TrainArgs a) {
   for (int qb = 0; qb < NQ; ++qb) {
     const int t = tcol[qb];
     if (t >= 0) {
-      const int qh = r % a.g;
+      const int qh = ((wave * NQ + qb) * 16 + r) % a.g;
       float* dst = a.dq + ((static_cast<size_t>(b) * a.T + t) * Hq + h * a.g + qh) * D + 4 * G;
 #pragma unroll
       for (int bb = 0; bb < D / 16; ++bb) *reinterpret_cast<f32x4*>(dst + 16 * bb) = dqa[qb][bb] * scale;
@@ -770,7 +771,7 @@ TrainArgs train_args(const dms_train_config& c, const TrainLayout& l, void* ws) 
   a.g = c.group_size;
   a.w = c.window;
   a.nt = l.nt;
-  a.PB = 4 * kNQ * (16 / c.group_size);
+  a.PB = 4 * kNQ * 16 / c.group_size;   // (position, head) columns packed across column blocks
   const float scale = c.softmax_scale > 0.f ? c.softmax_scale : 1.0f / sqrtf(static_cast<float>(c.head_dim));
   a.scale_log2 = scale * kLog2e;
   return a;
