@@ -25,10 +25,16 @@
 // heads of a position consecutive, packed 16 to an MFMA column block (a
 // position's heads may straddle two blocks); each wave holds NQ column
 // blocks.  Key tiles of 32 are staged into LDS in the order the MFMA
-// operand loads consume them (no bank conflicts), double buffered, and read
-// by every wave with 16-byte LDS loads straight into operand registers.  A tile is
-// masked per element only when some query of the block does not see one of
-// its keys; the online softmax works in the exp2 domain with a lazy rescale.
+// operand loads consume them (no bank conflicts) -- by hardware copies into
+// four buffers for bf16 pages under delayed eviction, through registers into
+// two otherwise -- and read by every wave with 16-byte LDS loads straight
+// into operand registers.  A tile is masked per element only when some query
+// of the block does not see one of its keys; the online softmax works in the
+// exp2 domain with a lazy rescale.  Pass 0 also counts the kept chunk tokens
+// before every 32-aligned position and a one-block pass ranks the call's
+// (sequence, head) rows by work; the attention launch keeps as many
+// workgroups as fit on the chip, each taking (row, query block) items in
+// that order.
 #include <type_traits>
 
 #include "dms_common.h"
